@@ -1,0 +1,851 @@
+// Host side of the TPP-SD C ABI: argument validation, packed weight layout,
+// workspace layout, and the launch sequence of each entry point.
+//
+// Entry points follow Algorithm 1 of the paper: drafting (§4.3) is gamma
+// sequential draft-model passes; verification is one target pass over the
+// pending event plus the gamma drafts; accept runs the first-rejection test,
+// the adjusted-distribution replacement (Eq. (3)-(4), Theorem 1) and the
+// commit. Naive AR sampling (§4.2) is one target pass per event.
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <cmath>
+#include <string>
+#include <vector>
+
+#include "../../include/tppsd.h"
+#include "tppsd_internal.h"
+
+using namespace tppsd;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_check(const char *what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(TPPSD_E_HIP, "%s: %s", what, hipGetErrorString(e));
+  return TPPSD_OK;
+}
+
+constexpr size_t ALIGN = 256;
+inline size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+constexpr int PREFILL_CHUNK = 16;
+
+// ---- packed weight layout -------------------------------------------------
+struct Entry {
+  std::string name;
+  size_t off;
+  int64_t rows, cols;
+  int bf16;
+};
+
+// Entries are 256-byte aligned, except that a few groups are packed back to
+// back so that the kernels can read them as one matrix: [E; V_k1] (4d x d),
+// [V_w; V_mu; V_sigma] (3M x d) and their biases (3M).
+std::vector<Entry> layout(const tppsd_model_cfg &c) {
+  std::vector<Entry> v;
+  const int bf = c.prec == TPPSD_PREC_BF16;
+  const size_t me = bf ? 2 : 4;
+  size_t off = 0;
+  auto add = [&](const std::string &n, int64_t r, int64_t cl, bool mat, bool aligned) {
+    if (aligned) off = align_up(off);
+    v.push_back({n, off, r, cl, mat ? bf : 0});
+    off += (size_t)r * cl * (mat ? me : 4);
+  };
+  const int d = c.d_model, F = c.d_ffn, M = c.n_mix, K = c.n_types;
+  add("type_emb", K, d, true, true);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const std::string p = "layers." + std::to_string(l) + ".";
+    add(p + "ln1.g", d, 1, false, true);
+    add(p + "ln1.b", d, 1, false, true);
+    add(p + "qkv.w", 3 * d, d, true, true);
+    add(p + "qkv.b", 3 * d, 1, false, true);
+    add(p + "out.w", d, d, true, true);
+    add(p + "out.b", d, 1, false, true);
+    add(p + "ln2.g", d, 1, false, true);
+    add(p + "ln2.b", d, 1, false, true);
+    add(p + "ffn1.w", F, d, true, true);
+    add(p + "ffn1.b", F, 1, false, true);
+    add(p + "ffn2.w", d, F, true, true);
+    add(p + "ffn2.b", d, 1, false, true);
+  }
+  add("lnf.g", d, 1, false, true);
+  add("lnf.b", d, 1, false, true);
+  add("head.E", 3 * d, d, true, true);
+  add("head.k1.w", d, d, true, false);
+  add("head.k1.b", d, 1, false, true);
+  add("head.w.w", M, d, true, true);
+  add("head.mu.w", M, d, true, false);
+  add("head.sigma.w", M, d, true, false);
+  add("head.w.b", M, 1, false, true);
+  add("head.mu.b", M, 1, false, false);
+  add("head.sigma.b", M, 1, false, false);
+  add("head.k2.w", K, d, true, true);
+  add("head.k2.b", K, 1, false, true);
+  v.push_back({"", align_up(off), 0, 0, 0});   // sentinel: total size
+  return v;
+}
+
+int check_cfg(const tppsd_model_cfg *c) {
+  if (!c) return fail(TPPSD_E_ARG, "null model configuration");
+  if (c->n_layers < 1 || c->d_model < 16 || c->n_heads < 1 || c->d_ffn < 1 || c->n_mix < 1 || c->n_types < 1)
+    return fail(TPPSD_E_CONFIG, "model sizes must be positive (d_model >= 16)");
+  if (c->prec != TPPSD_PREC_FP32 && c->prec != TPPSD_PREC_BF16)
+    return fail(TPPSD_E_CONFIG, "unsupported precision %d", c->prec);
+  if (c->d_model % c->n_heads) return fail(TPPSD_E_CONFIG, "d_model %% n_heads != 0");
+  const int dh = c->d_model / c->n_heads;
+  if (dh != 16 && dh != 32 && dh != 64) return fail(TPPSD_E_CONFIG, "d_head %d not in {16, 32, 64}", dh);
+  if (c->d_model % 16) return fail(TPPSD_E_CONFIG, "d_model must be a multiple of 16");
+  if (c->prec == TPPSD_PREC_BF16 && (c->d_model % 32 || c->d_ffn % 32))
+    return fail(TPPSD_E_CONFIG, "bf16 models need d_model and d_ffn multiples of 32");
+  if (c->n_mix > TPPSD_MAX_MIX) return fail(TPPSD_E_CONFIG, "n_mix > %d", TPPSD_MAX_MIX);
+  if (c->n_types > TPPSD_MAX_TYPES) return fail(TPPSD_E_CONFIG, "n_types > %d", TPPSD_MAX_TYPES);
+  return TPPSD_OK;
+}
+
+}  // namespace
+
+// ---- model handle -----------------------------------------------------------
+struct LayerW {
+  const void *qkv_w, *out_w, *ffn1_w, *ffn2_w;
+  const float *ln1_g, *ln1_b, *qkv_b, *out_b, *ln2_g, *ln2_b, *ffn1_b, *ffn2_b;
+};
+
+struct tppsd_model {
+  tppsd_model_cfg cfg;
+  const char *w;
+  std::vector<LayerW> layers;
+  const void *type_emb, *Ek1_w, *mix_w, *k2_w;
+  const float *lnf_g, *lnf_b, *k1_b, *mix_b, *k2_b;
+  int bf16() const { return cfg.prec == TPPSD_PREC_BF16; }
+  int d() const { return cfg.d_model; }
+  int H() const { return cfg.n_heads; }
+  int dh() const { return cfg.d_model / cfg.n_heads; }
+  size_t act_bytes() const { return bf16() ? 2 : 4; }
+};
+
+// ---- state ------------------------------------------------------------------
+struct ModelCache {
+  char *k = nullptr, *v = nullptr;   // [L][B][H][cap][dh]
+  size_t layer_bytes = 0;
+  float *freq = nullptr;
+};
+
+struct tppsd_state {
+  const tppsd_model *T = nullptr, *D = nullptr;
+  int B = 0, cap = 0, max_gamma = 0, Pmax = 0;
+  uint64_t seed = 0;
+  unsigned flags = 0;
+  char *ws = nullptr;
+  // device header + counters
+  uint32_t *status = nullptr;
+  int32_t *n_done = nullptr;
+  unsigned long long *acc_stats = nullptr;
+  int32_t *n = nullptr, *gen = nullptr, *lenT = nullptr, *lenD = nullptr, *done = nullptr, *rnd = nullptr,
+          *zeros = nullptr;
+  float *ev_t = nullptr;
+  int32_t *ev_k = nullptr;
+  ModelCache cT, cD;
+  // activation scratch
+  float *x = nullptr;
+  void *a = nullptr, *q = nullptr, *o = nullptr, *hid = nullptr, *e = nullptr;
+  float *ar_mix = nullptr, *ar_logtype = nullptr;
+  // internal round buffers (tppsd_sample_sd)
+  tppsd_draft_buf idr{};
+  tppsd_verify_buf ivf{};
+  tppsd_accept_buf iac{};
+  // host-side run state
+  int n_gen = 0;
+  bool prefilled = false, draft_ok = false, drafted_this_round = false;
+  int32_t *host_ndone = nullptr;   // pinned, 2 slots
+  hipEvent_t poll_ev[2] = {nullptr, nullptr};
+  // timing of the verify attention kernel
+  bool timing = false;
+  std::vector<hipEvent_t> tev;
+  size_t tev_used = 0;
+  double t_ms = 0.0;
+  int64_t t_launches = 0;
+};
+
+namespace {
+
+struct WsLayout {
+  size_t total = 0;
+  size_t status, n_done, acc, n, gen, lenT, lenD, done, rnd, zeros, ev_t, ev_k;
+  size_t freqT, freqD, kT, vT, kD, vD, layerT, layerD;
+  size_t x, a, q, o, hid, e, ar_mix, ar_lt;
+  size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt;
+  size_t v_logg, v_logf, v_mix, v_lt;
+  size_t a_L, a_nnew, a_knew, a_tnew, a_taunew, a_ar, a_flags;
+};
+
+WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, int MG) {
+  WsLayout w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    off = align_up(off);
+    size_t r = off;
+    off += bytes;
+    return r;
+  };
+  const size_t Bz = (size_t)B;
+  w.status = take(4);
+  w.n_done = take(4);
+  w.acc = take(3 * 8);
+  w.n = take(Bz * 4);
+  w.gen = take(Bz * 4);
+  w.lenT = take(Bz * 4);
+  w.lenD = take(Bz * 4);
+  w.done = take(Bz * 4);
+  w.rnd = take(Bz * 4);
+  w.zeros = take(Bz * 4);
+  w.ev_t = take(Bz * cap * 4);
+  w.ev_k = take(Bz * cap * 4);
+  w.freqT = take((size_t)T->d() * 4);
+  w.freqD = take(D ? (size_t)D->d() * 4 : 0);
+  w.layerT = Bz * T->H() * cap * T->dh() * T->act_bytes();
+  w.kT = take(w.layerT * T->cfg.n_layers);
+  w.vT = take(w.layerT * T->cfg.n_layers);
+  w.layerD = D ? Bz * D->H() * cap * D->dh() * D->act_bytes() : 0;
+  w.kD = take(D ? w.layerD * D->cfg.n_layers : 0);
+  w.vD = take(D ? w.layerD * D->cfg.n_layers : 0);
+  const int Pmax = std::max(MG + 1, PREFILL_CHUNK);
+  const size_t Tm = Bz * Pmax;
+  const size_t dmax = std::max(T->d(), D ? D->d() : 0);
+  const size_t fmax = std::max(T->cfg.d_ffn, D ? D->cfg.d_ffn : 0);
+  const size_t mmax = std::max(T->cfg.n_mix, D ? D->cfg.n_mix : 0);
+  const size_t kmax = std::max(T->cfg.n_types, D ? D->cfg.n_types : 0);
+  w.x = take(Tm * dmax * 4);
+  w.a = take(Tm * dmax * 4);
+  w.q = take(Tm * dmax * 4);
+  w.o = take(Tm * dmax * 4);
+  w.hid = take(Tm * fmax * 4);
+  w.e = take(Tm * 4 * dmax * 4);
+  w.ar_mix = take(Bz * 3 * mmax * 4);
+  w.ar_lt = take(Bz * kmax * 4);
+  const size_t M = T->cfg.n_mix, K = T->cfg.n_types;
+  w.d_tau = take(Bz * MG * 4);
+  w.d_t = take(Bz * MG * 4);
+  w.d_k = take(Bz * MG * 4);
+  w.d_logg = take(Bz * MG * 4);
+  w.d_logf = take(Bz * MG * 4);
+  w.d_mix = take(Bz * MG * 3 * M * 4);
+  w.d_lt = take(Bz * MG * K * 4);
+  w.v_logg = take(Bz * MG * 4);
+  w.v_logf = take(Bz * MG * 4);
+  w.v_mix = take(Bz * (MG + 1) * 3 * M * 4);
+  w.v_lt = take(Bz * (MG + 1) * K * 4);
+  w.a_L = take(Bz * 4);
+  w.a_nnew = take(Bz * 4);
+  w.a_knew = take(Bz * (MG + 1) * 4);
+  w.a_tnew = take(Bz * (MG + 1) * 4);
+  w.a_taunew = take(Bz * (MG + 1) * 4);
+  w.a_ar = take(Bz * 4);
+  w.a_flags = take(Bz);
+  w.total = align_up(off);
+  return w;
+}
+
+// Block forward of P new positions per sequence through model m (encoder of
+// §4.2), keys/values appended at start[b] + start_off + p; optional decoder.
+int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int32_t *start, int start_off,
+            int P, const TokSrc &src, const HeadArgs *head, bool time_attn, hipStream_t st) {
+  const int B = s->B, d = m->d(), H = m->H(), dh = m->dh(), F = m->cfg.d_ffn, bf = m->bf16();
+  const int T = B * P;
+  launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const LayerW &w = m->layers[l];
+    char *kc = c.k + c.layer_bytes * l, *vc = c.v + c.layer_bytes * l;
+    launch_layernorm(s->x, s->a, bf, w.ln1_g, w.ln1_b, T, d, st);
+    Epi e{};
+    e.mode = EPI_QKV;
+    e.bias = w.qkv_b;
+    e.q = s->q;
+    e.kc = kc;
+    e.vc = vc;
+    e.start = start;
+    e.start_off = start_off;
+    e.P = P;
+    e.H = H;
+    e.dh = dh;
+    e.d = d;
+    e.cap = s->cap;
+    e.status = s->status;
+    launch_gemm(s->a, w.qkv_w, bf, T, 3 * d, d, e, st);
+    const bool timed = time_attn && s->timing;
+    if (timed) {
+      if (s->tev_used + 2 > s->tev.size()) {
+        // drain: accumulate finished pairs and reuse the events
+        hipStreamSynchronize(st);
+        for (size_t i = 0; i + 1 < s->tev_used; i += 2) {
+          float ms = 0.f;
+          hipEventElapsedTime(&ms, s->tev[i], s->tev[i + 1]);
+          s->t_ms += ms;
+        }
+        s->tev_used = 0;
+      }
+      hipEventRecord(s->tev[s->tev_used], st);
+    }
+    launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->cap, st);
+    if (timed) {
+      hipEventRecord(s->tev[s->tev_used + 1], st);
+      s->tev_used += 2;
+      s->t_launches += 1;
+    }
+    Epi eo{};
+    eo.mode = EPI_RESID;
+    eo.bias = w.out_b;
+    eo.out = s->x;
+    eo.ldo = d;
+    launch_gemm(s->o, w.out_w, bf, T, d, d, eo, st);
+    launch_layernorm(s->x, s->a, bf, w.ln2_g, w.ln2_b, T, d, st);
+    Epi e1{};
+    e1.mode = EPI_RELU;
+    e1.bias = w.ffn1_b;
+    e1.out = s->hid;
+    e1.ldo = F;
+    launch_gemm(s->a, w.ffn1_w, bf, T, F, d, e1, st);
+    Epi e2{};
+    e2.mode = EPI_RESID;
+    e2.bias = w.ffn2_b;
+    e2.out = s->x;
+    e2.ldo = d;
+    launch_gemm(s->hid, w.ffn2_w, bf, T, d, F, e2, st);
+  }
+  if (head) {
+    launch_layernorm(s->x, s->a, bf, m->lnf_g, m->lnf_b, T, d, st);
+    Epi eh{};
+    eh.mode = EPI_HEAD;
+    eh.bias = m->k1_b;
+    eh.out = s->e;
+    eh.ldo = 4 * d;
+    eh.split = 3 * d;
+    launch_gemm(s->a, m->Ek1_w, bf, T, 4 * d, d, eh, st);
+    launch_head(s->e, bf, d, m->cfg.n_mix, m->cfg.n_types, m->mix_w, m->mix_b, m->k2_w, m->k2_b, *head, st);
+  }
+  return TPPSD_OK;
+}
+
+HeadArgs head_common(tppsd_state *s) {
+  HeadArgs h{};
+  h.B = s->B;
+  h.ev_t = s->ev_t;
+  h.ev_k = s->ev_k;
+  h.ev_stride = s->cap;
+  h.n = s->n;
+  h.gen = s->gen;
+  h.lenT = s->lenT;
+  h.done = s->done;
+  h.rnd = s->rnd;
+  h.n_done = s->n_done;
+  h.n_gen = s->n_gen;
+  h.seed = s->seed;
+  h.status = s->status;
+  return h;
+}
+
+int check_draft_buf(const tppsd_draft_buf *b) {
+  if (!b || !b->tau || !b->t || !b->k || !b->logg || !b->logf || !b->mix || !b->logtype)
+    return fail(TPPSD_E_ARG, "draft buffer has a null pointer");
+  return TPPSD_OK;
+}
+int check_verify_buf(const tppsd_verify_buf *b) {
+  if (!b || !b->logg || !b->logf || !b->mix || !b->logtype)
+    return fail(TPPSD_E_ARG, "verify buffer has a null pointer");
+  return TPPSD_OK;
+}
+int check_accept_buf(const tppsd_accept_buf *b) {
+  if (!b || !b->L || !b->n_new || !b->k_new || !b->t_new || !b->tau_new || !b->ar_iter || !b->flags)
+    return fail(TPPSD_E_ARG, "accept buffer has a null pointer");
+  return TPPSD_OK;
+}
+
+int do_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
+  const tppsd_model *D = s->D;
+  for (int l = 1; l <= gamma; ++l) {
+    TokSrc src{};
+    src.ev_t = s->ev_t;
+    src.ev_k = s->ev_k;
+    src.ev_stride = s->cap;
+    src.start = s->lenD;
+    src.dr_t = out->t;
+    src.dr_k = out->k;
+    src.dr_stride = s->max_gamma;
+    HeadArgs h = head_common(s);
+    h.mode = HEAD_DRAFT;
+    h.mix = out->mix;
+    h.logtype = out->logtype;
+    h.dst_stride = s->max_gamma;
+    h.dst_row0 = l - 1;
+    h.dr_stride = s->max_gamma;
+    h.d_tau = out->tau;
+    h.d_t = out->t;
+    h.d_k = out->k;
+    h.d_logg = out->logg;
+    h.d_logf = out->logf;
+    h.slot = l - 1;
+    h.l_index = l;
+    int P, off;
+    if (l == 1) {   // re-encode the last two committed events at lenD, lenD + 1
+      P = 2;
+      off = 0;
+      src.start_off = 0;
+      src.n_ev = 2;
+      src.dr_off = 0;
+    } else {        // draft l - 1 at lenD + l
+      P = 1;
+      off = l;
+      src.start_off = l;
+      src.n_ev = 0;
+      src.dr_off = l - 2;
+    }
+    h.P = P;
+    h.p0 = P - 1;
+    int rc = forward(s, D, s->cD, s->lenD, off, P, src, &h, false, st);
+    if (rc) return rc;
+  }
+  return hip_check("tppsd_draft");
+}
+
+int do_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_verify_buf *out, hipStream_t st) {
+  TokSrc src{};
+  src.ev_t = s->ev_t;
+  src.ev_k = s->ev_k;
+  src.ev_stride = s->cap;
+  src.start = s->lenT;
+  src.start_off = 0;
+  src.n_ev = 1;
+  src.dr_t = in->t;
+  src.dr_k = in->k;
+  src.dr_stride = s->max_gamma;
+  src.dr_off = 0;
+  HeadArgs h = head_common(s);
+  h.mode = HEAD_VERIFY;
+  h.P = gamma + 1;
+  h.p0 = 0;
+  h.mix = out->mix;
+  h.logtype = out->logtype;
+  h.dst_stride = s->max_gamma + 1;
+  h.dst_row0 = 0;
+  h.gamma = gamma;
+  h.dr_tau = in->tau;
+  h.dr_k = in->k;
+  h.dr_stride = s->max_gamma;
+  h.v_logg = out->logg;
+  h.v_logf = out->logf;
+  int rc = forward(s, s->T, s->cT, s->lenT, 0, gamma + 1, src, &h, true, st);
+  if (rc) return rc;
+  return hip_check("tppsd_verify");
+}
+
+int do_accept(tppsd_state *s, int gamma, const tppsd_draft_buf *dr, const tppsd_verify_buf *vf, const float *u,
+              const tppsd_accept_buf *out, hipStream_t st) {
+  AcceptArgs a{};
+  a.B = s->B;
+  a.gamma = gamma;
+  a.M = s->T->cfg.n_mix;
+  a.K = s->T->cfg.n_types;
+  a.max_gamma = s->max_gamma;
+  a.bonus = (s->flags & TPPSD_FLAG_BONUS) ? 1 : 0;
+  a.d_tau = dr->tau;
+  a.d_t = dr->t;
+  a.d_k = dr->k;
+  a.d_logg = dr->logg;
+  a.d_logf = dr->logf;
+  a.d_mix = dr->mix;
+  a.d_logtype = dr->logtype;
+  a.v_logg = vf->logg;
+  a.v_logf = vf->logf;
+  a.v_mix = vf->mix;
+  a.v_logtype = vf->logtype;
+  a.uniforms = u;
+  a.L = out->L;
+  a.n_new = out->n_new;
+  a.k_new = out->k_new;
+  a.ar_iter = out->ar_iter;
+  a.t_new = out->t_new;
+  a.tau_new = out->tau_new;
+  a.flags = out->flags;
+  a.ev_t = s->ev_t;
+  a.ev_k = s->ev_k;
+  a.ev_stride = s->cap;
+  a.n = s->n;
+  a.gen = s->gen;
+  a.lenT = s->lenT;
+  a.lenD = s->lenD;
+  a.done = s->done;
+  a.rnd = s->rnd;
+  a.n_done = s->n_done;
+  a.n_gen = s->n_gen;
+  a.seed = s->seed;
+  a.status = s->status;
+  a.acc_stats = s->acc_stats;
+  launch_accept(a, st);
+  return hip_check("tppsd_accept");
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *tppsd_last_error(void) { return g_err.c_str(); }
+
+int tppsd_weights_bytes(const tppsd_model_cfg *cfg, size_t *bytes) {
+  if (int rc = check_cfg(cfg)) return rc;
+  if (!bytes) return fail(TPPSD_E_ARG, "null output pointer");
+  *bytes = layout(*cfg).back().off;
+  return TPPSD_OK;
+}
+
+int tppsd_weights_entry(const tppsd_model_cfg *cfg, int index, const char **name, size_t *offset, int64_t *rows,
+                        int64_t *cols, int *is_bf16) {
+  if (int rc = check_cfg(cfg)) return rc;
+  static thread_local std::vector<Entry> cache;
+  cache = layout(*cfg);
+  if (index < 0 || index >= (int)cache.size() - 1) return fail(TPPSD_E_ARG, "weight entry %d out of range", index);
+  const Entry &e = cache[index];
+  // names live in a static table so the pointer outlives this call
+  static thread_local std::vector<std::string> names;
+  if ((int)names.size() <= index) names.resize(index + 1);
+  names[index] = e.name;
+  if (name) *name = names[index].c_str();
+  if (offset) *offset = e.off;
+  if (rows) *rows = e.rows;
+  if (cols) *cols = e.cols;
+  if (is_bf16) *is_bf16 = e.bf16;
+  return TPPSD_OK;
+}
+
+int tppsd_model_create(const tppsd_model_cfg *cfg, const void *d_weights, tppsd_model **out) {
+  if (int rc = check_cfg(cfg)) return rc;
+  if (!d_weights || !out) return fail(TPPSD_E_ARG, "null weights or output pointer");
+  if ((uintptr_t)d_weights % ALIGN) return fail(TPPSD_E_ARG, "weights must be 256-byte aligned");
+  std::vector<Entry> L = layout(*cfg);
+  auto find = [&](const std::string &n) -> const char * {
+    for (const Entry &e : L)
+      if (e.name == n) return (const char *)d_weights + e.off;
+    return nullptr;
+  };
+  tppsd_model *m = new tppsd_model();
+  m->cfg = *cfg;
+  m->w = (const char *)d_weights;
+  m->type_emb = find("type_emb");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const std::string p = "layers." + std::to_string(l) + ".";
+    LayerW w;
+    w.ln1_g = (const float *)find(p + "ln1.g");
+    w.ln1_b = (const float *)find(p + "ln1.b");
+    w.qkv_w = find(p + "qkv.w");
+    w.qkv_b = (const float *)find(p + "qkv.b");
+    w.out_w = find(p + "out.w");
+    w.out_b = (const float *)find(p + "out.b");
+    w.ln2_g = (const float *)find(p + "ln2.g");
+    w.ln2_b = (const float *)find(p + "ln2.b");
+    w.ffn1_w = find(p + "ffn1.w");
+    w.ffn1_b = (const float *)find(p + "ffn1.b");
+    w.ffn2_w = find(p + "ffn2.w");
+    w.ffn2_b = (const float *)find(p + "ffn2.b");
+    m->layers.push_back(w);
+  }
+  m->lnf_g = (const float *)find("lnf.g");
+  m->lnf_b = (const float *)find("lnf.b");
+  m->Ek1_w = find("head.E");
+  m->k1_b = (const float *)find("head.k1.b");
+  m->mix_w = find("head.w.w");
+  m->mix_b = (const float *)find("head.w.b");
+  m->k2_w = find("head.k2.w");
+  m->k2_b = (const float *)find("head.k2.b");
+  *out = m;
+  return TPPSD_OK;
+}
+
+void tppsd_model_destroy(tppsd_model *m) { delete m; }
+
+int tppsd_state_bytes(const tppsd_model *T, const tppsd_model *D, int B, int max_events, int max_gamma,
+                      size_t *bytes) {
+  if (!T || !bytes) return fail(TPPSD_E_ARG, "null target model or output pointer");
+  if (B < 1 || max_events < 3 || max_gamma < 1 || max_gamma > TPPSD_MAX_GAMMA)
+    return fail(TPPSD_E_ARG, "need B >= 1, max_events >= 3, 1 <= max_gamma <= %d", TPPSD_MAX_GAMMA);
+  if (D && (D->cfg.n_mix != T->cfg.n_mix || D->cfg.n_types != T->cfg.n_types))
+    return fail(TPPSD_E_CONFIG, "draft and target must share n_mix and n_types");
+  *bytes = ws_layout(T, D, B, max_events, max_gamma).total;
+  return TPPSD_OK;
+}
+
+int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int max_events, int max_gamma,
+                       uint64_t seed, unsigned flags, void *d_ws, size_t ws_bytes, tppsd_state **out) {
+  size_t need = 0;
+  if (int rc = tppsd_state_bytes(T, D, B, max_events, max_gamma, &need)) return rc;
+  if (!d_ws || !out) return fail(TPPSD_E_ARG, "null workspace or output pointer");
+  if ((uintptr_t)d_ws % ALIGN) return fail(TPPSD_E_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < need) return fail(TPPSD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+  if (flags & ~TPPSD_FLAG_BONUS) return fail(TPPSD_E_ARG, "unknown flags 0x%x", flags);
+  const WsLayout w = ws_layout(T, D, B, max_events, max_gamma);
+  tppsd_state *s = new tppsd_state();
+  s->T = T;
+  s->D = D;
+  s->B = B;
+  s->cap = max_events;
+  s->max_gamma = max_gamma;
+  s->Pmax = std::max(max_gamma + 1, PREFILL_CHUNK);
+  s->seed = seed;
+  s->flags = flags;
+  char *ws = (char *)d_ws;
+  s->ws = ws;
+  s->status = (uint32_t *)(ws + w.status);
+  s->n_done = (int32_t *)(ws + w.n_done);
+  s->acc_stats = (unsigned long long *)(ws + w.acc);
+  s->n = (int32_t *)(ws + w.n);
+  s->gen = (int32_t *)(ws + w.gen);
+  s->lenT = (int32_t *)(ws + w.lenT);
+  s->lenD = (int32_t *)(ws + w.lenD);
+  s->done = (int32_t *)(ws + w.done);
+  s->rnd = (int32_t *)(ws + w.rnd);
+  s->zeros = (int32_t *)(ws + w.zeros);
+  s->ev_t = (float *)(ws + w.ev_t);
+  s->ev_k = (int32_t *)(ws + w.ev_k);
+  s->cT.k = ws + w.kT;
+  s->cT.v = ws + w.vT;
+  s->cT.layer_bytes = w.layerT;
+  s->cT.freq = (float *)(ws + w.freqT);
+  if (D) {
+    s->cD.k = ws + w.kD;
+    s->cD.v = ws + w.vD;
+    s->cD.layer_bytes = w.layerD;
+    s->cD.freq = (float *)(ws + w.freqD);
+  }
+  s->x = (float *)(ws + w.x);
+  s->a = ws + w.a;
+  s->q = ws + w.q;
+  s->o = ws + w.o;
+  s->hid = ws + w.hid;
+  s->e = ws + w.e;
+  s->ar_mix = (float *)(ws + w.ar_mix);
+  s->ar_logtype = (float *)(ws + w.ar_lt);
+  s->idr = {(float *)(ws + w.d_tau), (float *)(ws + w.d_t), (int32_t *)(ws + w.d_k), (float *)(ws + w.d_logg),
+            (float *)(ws + w.d_logf), (float *)(ws + w.d_mix), (float *)(ws + w.d_lt)};
+  s->ivf = {(float *)(ws + w.v_logg), (float *)(ws + w.v_logf), (float *)(ws + w.v_mix), (float *)(ws + w.v_lt)};
+  s->iac = {(int32_t *)(ws + w.a_L),      (int32_t *)(ws + w.a_nnew), (int32_t *)(ws + w.a_knew),
+            (float *)(ws + w.a_tnew),     (float *)(ws + w.a_taunew), (int32_t *)(ws + w.a_ar),
+            (uint8_t *)(ws + w.a_flags)};
+  // frequency tables of the temporal encoding: 10000^(-(j - j mod 2) / d), float32
+  for (int which = 0; which < (D ? 2 : 1); ++which) {
+    const tppsd_model *m = which ? D : T;
+    std::vector<float> f(m->d());
+    for (int j = 0; j < m->d(); ++j) f[j] = (float)pow(10000.0, -(double)(j - j % 2) / (double)m->d());
+    float *dst = which ? s->cD.freq : s->cT.freq;
+    if (hipMemcpy(dst, f.data(), f.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+      delete s;
+      return hip_check("tppsd_state_create: frequency table upload");
+    }
+  }
+  if (hipHostMalloc((void **)&s->host_ndone, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
+      hipEventCreateWithFlags(&s->poll_ev[0], hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&s->poll_ev[1], hipEventDisableTiming) != hipSuccess) {
+    tppsd_state_destroy(s);
+    return hip_check("tppsd_state_create: host buffers");
+  }
+  *out = s;
+  return TPPSD_OK;
+}
+
+void tppsd_state_destroy(tppsd_state *s) {
+  if (!s) return;
+  if (s->host_ndone) hipHostFree(s->host_ndone);
+  for (hipEvent_t e : s->poll_ev)
+    if (e) hipEventDestroy(e);
+  for (hipEvent_t e : s->tev) hipEventDestroy(e);
+  delete s;
+}
+
+int tppsd_prefill(tppsd_state *s, const float *d_t, const int32_t *d_k, int n0, int n_gen, hipStream_t st) {
+  if (!s || !d_t || !d_k) return fail(TPPSD_E_ARG, "null argument");
+  if (n0 < 2 || n_gen < 0) return fail(TPPSD_E_ARG, "need n0 >= 2 and n_gen >= 0");
+  if ((long long)n0 + n_gen + s->max_gamma + 1 > s->cap)
+    return fail(TPPSD_E_ARG, "n0 + n_gen + max_gamma + 1 = %lld exceeds max_events %d",
+                (long long)n0 + n_gen + s->max_gamma + 1, s->cap);
+  s->n_gen = n_gen;
+  launch_prefill_init(d_t, d_k, s->B, n0, n_gen, s->ev_t, s->ev_k, s->cap, s->n, s->gen, s->lenT, s->lenD, s->done,
+                      s->rnd, s->zeros, s->n_done, s->status, s->acc_stats, st);
+  // encode history events 0 .. n0 - 2 (target) and 0 .. n0 - 3 (draft) in position chunks
+  for (int which = 0; which < (s->D ? 2 : 1); ++which) {
+    const tppsd_model *m = which ? s->D : s->T;
+    const ModelCache &c = which ? s->cD : s->cT;
+    const int n_enc = n0 - 1 - which;
+    for (int c0 = 0; c0 < n_enc; c0 += PREFILL_CHUNK) {
+      const int P = std::min(PREFILL_CHUNK, n_enc - c0);
+      TokSrc src{};
+      src.ev_t = s->ev_t;
+      src.ev_k = s->ev_k;
+      src.ev_stride = s->cap;
+      src.start = s->zeros;
+      src.start_off = c0;
+      src.n_ev = P;
+      forward(s, m, c, s->zeros, c0, P, src, nullptr, false, st);
+    }
+  }
+  s->prefilled = true;
+  s->draft_ok = s->D != nullptr;
+  s->drafted_this_round = false;
+  return hip_check("tppsd_prefill");
+}
+
+static int check_round(tppsd_state *s, int gamma) {
+  if (!s) return fail(TPPSD_E_ARG, "null state");
+  if (gamma < 1 || gamma > s->max_gamma) return fail(TPPSD_E_ARG, "gamma %d outside 1..%d", gamma, s->max_gamma);
+  if (!s->prefilled) return fail(TPPSD_E_ORDER, "call tppsd_prefill first");
+  return TPPSD_OK;
+}
+
+int tppsd_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
+  if (int rc = check_round(s, gamma)) return rc;
+  if (int rc = check_draft_buf(out)) return rc;
+  if (!s->D) return fail(TPPSD_E_ORDER, "state has no draft model");
+  if (!s->draft_ok)
+    return fail(TPPSD_E_ORDER, "draft cache is stale (AR sampling or an external draft ran since prefill)");
+  int rc = do_draft(s, gamma, out, st);
+  if (rc == TPPSD_OK) s->drafted_this_round = true;
+  return rc;
+}
+
+int tppsd_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_verify_buf *out, hipStream_t st) {
+  if (int rc = check_round(s, gamma)) return rc;
+  if (int rc = check_draft_buf(in)) return rc;
+  if (int rc = check_verify_buf(out)) return rc;
+  return do_verify(s, gamma, in, out, st);
+}
+
+int tppsd_accept(tppsd_state *s, int gamma, const tppsd_draft_buf *dr, const tppsd_verify_buf *vf,
+                 const float *d_uniforms, const tppsd_accept_buf *out, hipStream_t st) {
+  if (int rc = check_round(s, gamma)) return rc;
+  if (int rc = check_draft_buf(dr)) return rc;
+  if (int rc = check_verify_buf(vf)) return rc;
+  if (int rc = check_accept_buf(out)) return rc;
+  int rc = do_accept(s, gamma, dr, vf, d_uniforms, out, st);
+  if (!s->drafted_this_round) s->draft_ok = false;   // the draft cache missed this round's events
+  s->drafted_this_round = false;
+  return rc;
+}
+
+int tppsd_sample_ar(tppsd_state *s, int n_events, float *d_t_out, int32_t *d_k_out, hipStream_t st) {
+  if (!s) return fail(TPPSD_E_ARG, "null state");
+  if (!s->prefilled) return fail(TPPSD_E_ORDER, "call tppsd_prefill first");
+  if (n_events < 0) return fail(TPPSD_E_ARG, "n_events < 0");
+  for (int i = 0; i < n_events; ++i) {
+    TokSrc src{};
+    src.ev_t = s->ev_t;
+    src.ev_k = s->ev_k;
+    src.ev_stride = s->cap;
+    src.start = s->lenT;
+    src.start_off = 0;
+    src.n_ev = 1;
+    HeadArgs h = head_common(s);
+    h.mode = HEAD_AR;
+    h.P = 1;
+    h.p0 = 0;
+    h.mix = s->ar_mix;
+    h.logtype = s->ar_logtype;
+    h.dst_stride = 1;
+    h.dst_row0 = 0;
+    h.ar_t_out = d_t_out;
+    h.ar_k_out = d_k_out;
+    h.ar_out_stride = n_events;
+    h.ar_step = i;
+    forward(s, s->T, s->cT, s->lenT, 0, 1, src, &h, false, st);
+  }
+  if (n_events > 0) s->draft_ok = false;
+  return hip_check("tppsd_sample_ar");
+}
+
+int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipStream_t st) {
+  if (int rc = check_round(s, gamma)) return rc;
+  if (!s->D) return fail(TPPSD_E_ORDER, "state has no draft model");
+  if (!s->draft_ok) return fail(TPPSD_E_ORDER, "draft cache is stale; prefill again");
+  int r = 0;
+  for (; r < max_rounds; ++r) {
+    if (r >= 1) {
+      // the done counter copied after round r - 1; waits for that round only
+      if (hipEventSynchronize(s->poll_ev[(r - 1) & 1]) != hipSuccess) return hip_check("tppsd_sample_sd: poll");
+      if (s->host_ndone[(r - 1) & 1] >= s->B) break;
+    }
+    int rc = do_draft(s, gamma, &s->idr, st);
+    if (!rc) rc = do_verify(s, gamma, &s->idr, &s->ivf, st);
+    if (!rc) rc = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, st);
+    if (rc) return rc;
+    hipMemcpyAsync(&s->host_ndone[r & 1], s->n_done, sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    hipEventRecord(s->poll_ev[r & 1], st);
+  }
+  if (rounds) *rounds = r;
+  return hip_check("tppsd_sample_sd");
+}
+
+int tppsd_read_events(tppsd_state *s, float *d_t, int32_t *d_k, int32_t *d_n, hipStream_t st) {
+  if (!s) return fail(TPPSD_E_ARG, "null state");
+  launch_copy_events(s->ev_t, s->ev_k, s->n, s->B, s->cap, d_t, d_k, d_n, st);
+  return hip_check("tppsd_read_events");
+}
+
+int tppsd_state_status(tppsd_state *s, hipStream_t st, uint32_t *bits, int32_t *n_done, int64_t *accepted,
+                       int64_t *drafted, int64_t *ar_candidates) {
+  if (!s) return fail(TPPSD_E_ARG, "null state");
+  uint32_t b = 0;
+  int32_t nd = 0;
+  unsigned long long acc[3] = {0, 0, 0};
+  if (hipMemcpyAsync(&b, s->status, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(&nd, s->n_done, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(acc, s->acc_stats, sizeof acc, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return hip_check("tppsd_state_status");
+  if (bits) *bits = b;
+  if (n_done) *n_done = nd;
+  if (accepted) *accepted = (int64_t)acc[0];
+  if (drafted) *drafted = (int64_t)acc[1];
+  if (ar_candidates) *ar_candidates = (int64_t)acc[2];
+  return TPPSD_OK;
+}
+
+int tppsd_timing_enable(tppsd_state *s, int enable) {
+  if (!s) return fail(TPPSD_E_ARG, "null state");
+  if (enable && s->tev.empty()) {
+    s->tev.resize(4096);
+    for (hipEvent_t &e : s->tev)
+      if (hipEventCreate(&e) != hipSuccess) return hip_check("tppsd_timing_enable");
+  }
+  s->timing = enable != 0;
+  s->tev_used = 0;
+  s->t_ms = 0.0;
+  s->t_launches = 0;
+  return TPPSD_OK;
+}
+
+int tppsd_timing_read(tppsd_state *s, double *ms, int64_t *launches) {
+  if (!s) return fail(TPPSD_E_ARG, "null state");
+  for (size_t i = 0; i + 1 < s->tev_used; i += 2) {
+    if (hipEventSynchronize(s->tev[i + 1]) != hipSuccess) return hip_check("tppsd_timing_read");
+    float t = 0.f;
+    hipEventElapsedTime(&t, s->tev[i], s->tev[i + 1]);
+    s->t_ms += t;
+  }
+  s->tev_used = 0;
+  if (ms) *ms = s->t_ms;
+  if (launches) *launches = s->t_launches;
+  return TPPSD_OK;
+}
+
+}  // extern "C"

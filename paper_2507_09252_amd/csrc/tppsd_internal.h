@@ -1,0 +1,120 @@
+// Internal interface between the C-ABI host library (tppsd.cpp) and the HIP
+// kernels (tppsd_kernels.hip). Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tppsd {
+
+typedef uint16_t bf16_t;   // raw bfloat16 bits
+
+// Where the P tokens of a block forward come from: token p of sequence b is
+// committed event (start[b] + start_off + p) for p < n_ev, otherwise draft
+// slot (dr_off + p - n_ev).
+struct TokSrc {
+  const float *ev_t;
+  const int32_t *ev_k;
+  int ev_stride;            // max_events
+  const int32_t *start;     // per-sequence base position
+  int start_off;
+  int n_ev;
+  const float *dr_t;
+  const int32_t *dr_k;
+  int dr_stride;            // max_gamma
+  int dr_off;
+};
+
+// GEMM epilogues: Y[r, n] = sum_k X[r, k] W[n, k]
+enum EpiMode { EPI_STORE = 0, EPI_RESID = 1, EPI_RELU = 2, EPI_QKV = 3, EPI_HEAD = 4 };
+
+struct Epi {
+  int mode;
+  const float *bias;        // [N] (HEAD: [N - split])
+  void *out;                // STORE/RELU/HEAD: act [T, ldo]; RESID: float x [T, ldo]
+  int ldo;
+  // EPI_QKV: n < d -> q[r, n]; n in [d, 2d) -> key cache; [2d, 3d) -> value cache
+  void *q;
+  void *kc, *vc;            // this layer's cache base, [B][H][cap][dh]
+  const int32_t *start;
+  int start_off;
+  int P, H, dh, d, cap;
+  uint32_t *status;
+  int split;                // EPI_HEAD: columns < split stored raw, >= split tanh(acc + bias)
+};
+
+// Decoder epilogue modes
+enum HeadMode { HEAD_VERIFY = 0, HEAD_DRAFT = 1, HEAD_AR = 2 };
+
+struct HeadArgs {
+  int mode;
+  int P, p0;                // rows p0..P-1 of each sequence are decoded
+  int B;
+  // destination of (log w, mu, log sigma) [.., 3, M] and log f [.., K]
+  float *mix, *logtype;
+  int dst_stride;           // rows per sequence in mix/logtype (HEAD_AR: 1)
+  int dst_row0;             // destination row of p0 (HEAD_DRAFT: slot)
+  // HEAD_VERIFY: log-densities at the drafts
+  int gamma;
+  const float *dr_tau;
+  const int32_t *dr_k;
+  int dr_stride;
+  float *v_logg, *v_logf;
+  // HEAD_DRAFT: proposal record (slot dst_row0)
+  float *d_tau, *d_t, *d_logg, *d_logf;
+  int32_t *d_k;
+  int slot, l_index;        // Philox slot counter word (1-based draft position)
+  // state
+  float *ev_t;
+  int32_t *ev_k;
+  int ev_stride;
+  int32_t *n, *gen, *lenT, *done, *rnd, *n_done;
+  int n_gen;
+  uint64_t seed;
+  uint32_t *status;
+  // HEAD_AR optional outputs [B, out_stride]
+  float *ar_t_out;
+  int32_t *ar_k_out;
+  int ar_out_stride, ar_step;
+};
+
+struct AcceptArgs {
+  int B, gamma, M, K, max_gamma, bonus;
+  const float *d_tau, *d_t, *d_logg, *d_logf, *d_mix, *d_logtype;
+  const int32_t *d_k;
+  const float *v_logg, *v_logf, *v_mix, *v_logtype;
+  const float *uniforms;    // nullable [B, max_gamma, 2]
+  int32_t *L, *n_new, *k_new, *ar_iter;
+  float *t_new, *tau_new;
+  uint8_t *flags;
+  float *ev_t;
+  int32_t *ev_k;
+  int ev_stride;
+  int32_t *n, *gen, *lenT, *lenD, *done, *rnd, *n_done;
+  int n_gen;
+  uint64_t seed;
+  uint32_t *status;
+  unsigned long long *acc_stats;   // [3]: accepted drafts, drafted, A-R candidates
+};
+
+// ---- launchers (tppsd_kernels.hip) ----
+void launch_embed(float *x, int T, int d, int P, const TokSrc &src, const void *wtype, int bf16,
+                  const float *freq, int K, hipStream_t st);
+void launch_layernorm(const float *x, void *y, int bf16, const float *g, const float *b, int T, int d,
+                      hipStream_t st);
+void launch_gemm(const void *X, const void *W, int bf16, int T, int N, int K, const Epi &epi,
+                 hipStream_t st);
+void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16,
+                      const int32_t *start, int start_off, const int32_t *done, int B, int P, int H,
+                      int dh, int cap, hipStream_t st);
+void launch_head(const void *e, int bf16, int d, int M, int K, const void *wmix, const float *bmix,
+                 const void *wk2, const float *bk2, const HeadArgs &a, hipStream_t st);
+void launch_accept(const AcceptArgs &a, hipStream_t st);
+void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, float *ev_t,
+                         int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
+                         int32_t *lenD, int32_t *done, int32_t *rnd, int32_t *zeros, int32_t *n_done,
+                         uint32_t *status, unsigned long long *acc_stats, hipStream_t st);
+void launch_copy_events(const float *ev_t, const int32_t *ev_k, const int32_t *n, int B, int ev_stride,
+                        float *t, int32_t *k, int32_t *nout, hipStream_t st);
+
+}  // namespace tppsd

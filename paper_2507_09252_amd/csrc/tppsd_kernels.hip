@@ -1,0 +1,815 @@
+// HIP kernels of the TPP-SD hot path for gfx950 (MI355X).
+//
+// Encoder and decoder of the CDF-based Transformer TPP (paper §4.2, App. D.4),
+// block verification and the accept / adjusted-distribution step of TPP-SD
+// (§4.3, Eq. (3)-(4), Theorem 1, Algorithm 1), and the sampling epilogues of
+// drafting and naive AR sampling (§4.2, App. A.1).
+//
+// Precision: fp32 models run fp32 everywhere. bf16 models keep matrices and
+// Linear inputs in bf16 (LN outputs, q/k/v, attention output, ReLU output, the
+// decoder's e and tanh activations), accumulate in fp32 and keep the residual
+// stream, LayerNorm statistics, softmax and all decoder math in fp32.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "tppsd_internal.h"
+#include "../../include/tppsd.h"
+
+namespace tppsd {
+
+// ---------------------------------------------------------------------------
+// scalar helpers
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// float -> bf16, round to nearest even (values here are finite)
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float ld(const T *p, size_t i);
+template <> __device__ __forceinline__ float ld<float>(const float *p, size_t i) { return p[i]; }
+template <> __device__ __forceinline__ float ld<bf16_t>(const bf16_t *p, size_t i) { return bf2f(p[i]); }
+
+template <typename T> __device__ __forceinline__ void st(T *p, size_t i, float v);
+template <> __device__ __forceinline__ void st<float>(float *p, size_t i, float v) { p[i] = v; }
+template <> __device__ __forceinline__ void st<bf16_t>(bf16_t *p, size_t i, float v) { p[i] = f2bf(v); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 (Salmon et al., SC'11) and uniforms on the 2^-24 odd grid
+// ---------------------------------------------------------------------------
+
+enum { TAG_AR = 1, TAG_DRAFT = 2, TAG_ACCEPT = 3, TAG_RES_T = 4, TAG_RES_K = 5, TAG_BONUS = 6 };
+
+__device__ __forceinline__ void philox_uniforms(uint64_t seed, uint64_t c0, uint64_t c1, uint64_t c2,
+                                                uint64_t c3, float u[4]) {
+  uint64_t x0 = c0, x1 = c1, x2 = c2, x3 = c3;
+  uint64_t k0 = seed, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B97F4A7C15ull;
+      k1 += 0xBB67AE8584CAA73Bull;
+    }
+    const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
+    uint64_t lo0 = m0 * x0, hi0 = __umul64hi(m0, x0);
+    uint64_t lo1 = m1 * x2, hi1 = __umul64hi(m1, x2);
+    uint64_t y0 = hi1 ^ x1 ^ k0, y2 = hi0 ^ x3 ^ k1;
+    x0 = y0;
+    x1 = lo1;
+    x2 = y2;
+    x3 = lo0;
+  }
+  // top 23 bits -> (2 m + 1) 2^-24, exact in float32
+  u[0] = (float)(2ull * (x0 >> 41) + 1ull) * 0x1p-24f;
+  u[1] = (float)(2ull * (x1 >> 41) + 1ull) * 0x1p-24f;
+  u[2] = (float)(2ull * (x2 >> 41) + 1ull) * 0x1p-24f;
+  u[3] = (float)(2ull * (x3 >> 41) + 1ull) * 0x1p-24f;
+}
+
+// ---------------------------------------------------------------------------
+// decoder math (log-normal mixture of §4.2; sampling as in App. A.1)
+// ---------------------------------------------------------------------------
+
+// log g(tau) = logsumexp_m [log w_m - s_m - log(2 pi)/2 - ln tau - (ln tau - mu_m)^2 / (2 e^{2 s_m})]
+__device__ float mix_logpdf(const float *logw, const float *mu, const float *s, int M, float tau) {
+  const float lt = logf(tau);
+  float mx = -INFINITY;
+  for (int m = 0; m < M; ++m) {
+    float z = lt - mu[m];
+    float c = logw[m] - s[m] - 0.918938533204672742f - lt - 0.5f * z * z * expf(-2.f * s[m]);
+    mx = fmaxf(mx, c);
+  }
+  float acc = 0.f;
+  for (int m = 0; m < M; ++m) {
+    float z = lt - mu[m];
+    float c = logw[m] - s[m] - 0.918938533204672742f - lt - 0.5f * z * z * expf(-2.f * s[m]);
+    acc += expf(c - mx);
+  }
+  return mx + logf(acc);
+}
+
+// first index m with u * C_total < C_m, C the ascending running sum of exp(logp)
+__device__ int sample_cat(const float *logp, int n, float u) {
+  float tot = 0.f;
+  for (int m = 0; m < n; ++m) tot += expf(logp[m]);
+  const float x = u * tot;
+  float c = 0.f;
+  for (int m = 0; m < n; ++m) {
+    c += expf(logp[m]);
+    if (x < c) return m;
+  }
+  return n - 1;
+}
+
+// z ~ Categorical(w), eps = Box-Muller(u1, u2), tau = exp(mu_z + sigma_z eps)
+__device__ float sample_tau(const float *logw, const float *mu, const float *s, int M, float uc, float u1,
+                            float u2) {
+  const int z = sample_cat(logw, M, uc);
+  const float eps = sqrtf(-2.f * logf(u1)) * cosf(6.28318530717958647692f * u2);
+  return expf(mu[z] + expf(s[z]) * eps);
+}
+
+// ---------------------------------------------------------------------------
+// event embedding: x = z(t) + W_type[k]   (§4.2 Encoder, App. D.4 THP encoding)
+// ---------------------------------------------------------------------------
+
+template <typename W>
+__global__ void k_embed(float *__restrict__ x, int d, int P, TokSrc src, const W *__restrict__ wtype,
+                        const float *__restrict__ freq, int K) {
+  const int tok = blockIdx.x;
+  const int b = tok / P, p = tok % P;
+  float t;
+  int k;
+  if (p < src.n_ev) {
+    const size_t i = (size_t)b * src.ev_stride + src.start[b] + src.start_off + p;
+    t = src.ev_t[i];
+    k = src.ev_k[i];
+  } else {
+    const size_t i = (size_t)b * src.dr_stride + src.dr_off + (p - src.n_ev);
+    t = src.dr_t[i];
+    k = src.dr_k[i];
+  }
+  k = min(max(k, 0), K - 1);
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    const float arg = t * freq[j];
+    const float z = (j & 1) ? cosf(arg) : sinf(arg);
+    x[(size_t)tok * d + j] = z + ld(wtype, (size_t)k * d + j);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm (biased variance, eps 1e-5), one wave per row
+// ---------------------------------------------------------------------------
+
+template <typename ACT>
+__global__ __launch_bounds__(256) void k_layernorm(const float *__restrict__ x, ACT *__restrict__ y,
+                                                   const float *__restrict__ g, const float *__restrict__ bt,
+                                                   int T, int d) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= T) return;
+  const float *xr = x + (size_t)row * d;
+  float s = 0.f;
+  for (int j = lane; j < d; j += 64) s += xr[j];
+  const float mean = wave_sum(s) / (float)d;
+  float v = 0.f;
+  for (int j = lane; j < d; j += 64) {
+    const float c = xr[j] - mean;
+    v += c * c;
+  }
+  const float var = wave_sum(v) / (float)d;
+  const float rstd = 1.f / sqrtf(var + 1e-5f);
+  for (int j = lane; j < d; j += 64) st(y, (size_t)row * d + j, (xr[j] - mean) * rstd * g[j] + bt[j]);
+}
+
+// ---------------------------------------------------------------------------
+// GEMM epilogue
+// ---------------------------------------------------------------------------
+
+template <typename ACT>
+__device__ __forceinline__ void epilogue(const Epi &e, int r, int n, float acc) {
+  switch (e.mode) {
+    case EPI_STORE:
+      st((ACT *)e.out, (size_t)r * e.ldo + n, acc + (e.bias ? e.bias[n] : 0.f));
+      break;
+    case EPI_RESID:
+      ((float *)e.out)[(size_t)r * e.ldo + n] += acc + e.bias[n];
+      break;
+    case EPI_RELU:
+      st((ACT *)e.out, (size_t)r * e.ldo + n, fmaxf(acc + e.bias[n], 0.f));
+      break;
+    case EPI_QKV: {
+      const float v = acc + e.bias[n];
+      const int which = n / e.d, c = n - which * e.d;
+      if (which == 0) {
+        st((ACT *)e.q, (size_t)r * e.d + c, v);
+      } else {
+        const int b = r / e.P, p = r - b * e.P;
+        const int h = c / e.dh, j = c - h * e.dh;
+        const int pos = e.start[b] + e.start_off + p;
+        if (pos < e.cap) {
+          ACT *cache = (ACT *)(which == 1 ? e.kc : e.vc);
+          st(cache, (((size_t)b * e.H + h) * e.cap + pos) * e.dh + j, v);
+        } else {
+          atomicOr(e.status, TPPSD_STATUS_CAPACITY);
+        }
+      }
+      break;
+    }
+    case EPI_HEAD:
+      if (n < e.split)
+        st((ACT *)e.out, (size_t)r * e.ldo + n, acc);
+      else
+        st((ACT *)e.out, (size_t)r * e.ldo + n, tanhf(acc + e.bias[n - e.split]));
+      break;
+  }
+}
+
+// fp32 GEMM on the vector ALU: 64x64 tile per 256-thread block, 4x4 per thread.
+__global__ __launch_bounds__(256) void k_gemm_f32(const float *__restrict__ X, const float *__restrict__ W,
+                                                  int T, int N, int K, Epi e) {
+  __shared__ float As[16][64 + 4];
+  __shared__ float Ws[16][64 + 4];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += 16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + 256 * i, rr = idx >> 4, kk = idx & 15;
+      const int gr = r0 + rr, gc = c0 + rr, gk = k0 + kk;
+      As[kk][rr] = (gr < T && gk < K) ? X[(size_t)gr * K + gk] : 0.f;
+      Ws[kk][rr] = (gc < N && gk < K) ? W[(size_t)gc * K + gk] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        a[i] = As[kk][ty * 4 + i];
+        w[i] = Ws[kk][tx * 4 + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * w[j];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = r0 + ty * 4 + i, n = c0 + tx * 4 + j;
+      if (r < T && n < N) epilogue<float>(e, r, n, acc[i][j]);
+    }
+}
+
+// bf16 GEMM on MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulate): 64x64 tile
+// per 256-thread block, each wave a 32x32 quadrant of 2x2 MFMA tiles. Lane l
+// holds 8 consecutive k of row (l mod 16) of each operand; the accumulator
+// holds rows 4 (l / 16) + i, column l mod 16. K must be a multiple of 32.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t *__restrict__ X, const bf16_t *__restrict__ W,
+                                                   int T, int N, int K, Epi e) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m0 = blockIdx.y * 64 + (wave >> 1) * 32;
+  const int n0 = blockIdx.x * 64 + (wave & 1) * 32;
+  const int rr = lane & 15, g = lane >> 4;
+  f32x4_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  const bf16_t *xa[2], *wb[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int row = min(m0 + 16 * i + rr, T - 1);
+    const int col = min(n0 + 16 * i + rr, N - 1);
+    xa[i] = X + (size_t)row * K + 8 * g;
+    wb[i] = W + (size_t)col * K + 8 * g;
+  }
+  for (int k0 = 0; k0 < K; k0 += 32) {
+    bf16x8_t a[2], b[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      a[i] = *(const bf16x8_t *)(xa[i] + k0);
+      b[i] = *(const bf16x8_t *)(wb[i] + k0);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int r = m0 + 16 * i + 4 * g + v, n = n0 + 16 * j + rr;
+        if (r < T && n < N) epilogue<bf16_t>(e, r, n, acc[i][j][v]);
+      }
+}
+
+// ---------------------------------------------------------------------------
+// causal attention of P new queries per (sequence, head) over the KV cache
+// (App. D.4: softmax-normalised exp(q.k / sqrt(d_head)) weights over the
+// event and its predecessors). Query p of sequence b sees cached positions
+// 0 .. start[b] + start_off + p. Online softmax over 64-key tiles.
+// ---------------------------------------------------------------------------
+
+template <typename ACT, int DH>
+__global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q, const ACT *__restrict__ kc,
+                                                      const ACT *__restrict__ vc, ACT *__restrict__ o,
+                                                      const int32_t *__restrict__ start, int start_off,
+                                                      const int32_t *__restrict__ done, int P, int H,
+                                                      int cap) {
+  constexpr int QT = 16, KT = 64, EPT = (DH + 15) / 16;
+  __shared__ float qs[QT][DH];
+  __shared__ float ks[KT][DH + 1];
+  __shared__ float vs[KT][DH + 1];
+  __shared__ float ps[QT][KT + 1];
+  const int bh = blockIdx.x, b = bh / H, h = bh - b * H;
+  const int q0 = blockIdx.y * QT;
+  const int tid = threadIdx.x, qi = tid >> 4, sub = tid & 15;
+  const int d = H * DH;
+  const int nq = min(QT, P - q0);
+  const bool skip = done != nullptr && done[b] != 0;
+  const int base = start[b] + start_off;
+  if (skip) {
+    for (int idx = tid; idx < nq * DH; idx += 256) {
+      const int qq = idx / DH, j = idx - qq * DH;
+      st(o, (size_t)(b * P + q0 + qq) * d + h * DH + j, 0.f);
+    }
+    return;
+  }
+  const float scale = 1.f / sqrtf((float)DH);
+  for (int idx = tid; idx < QT * DH; idx += 256) {
+    const int qq = idx / DH, j = idx - qq * DH;
+    qs[qq][j] = (qq < nq) ? ld(q, (size_t)(b * P + q0 + qq) * d + h * DH + j) * scale : 0.f;
+  }
+  const int my_last = base + q0 + qi;             // last key index for this thread's query
+  const int n_keys = base + q0 + nq;             // keys 0 .. n_keys-1 are needed by this tile
+  float m_run = -INFINITY, l_run = 0.f;
+  float acc[EPT];
+#pragma unroll
+  for (int i = 0; i < EPT; ++i) acc[i] = 0.f;
+  const size_t kvbase = ((size_t)b * H + h) * cap * DH;
+  for (int kt = 0; kt < n_keys; kt += KT) {
+    __syncthreads();
+    for (int idx = tid; idx < KT * DH; idx += 256) {
+      const int kk = idx / DH, j = idx - kk * DH;
+      const int key = kt + kk;
+      const bool ok = key < n_keys;
+      ks[kk][j] = ok ? ld(kc, kvbase + (size_t)key * DH + j) : 0.f;
+      vs[kk][j] = ok ? ld(vc, kvbase + (size_t)key * DH + j) : 0.f;
+    }
+    __syncthreads();
+    // scores for query qi, keys sub + 16 i
+    float sc[4];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int kk = sub + 16 * i, key = kt + kk;
+      float s = -INFINITY;
+      if (qi < nq && key <= my_last) {
+        s = 0.f;
+#pragma unroll
+        for (int j = 0; j < DH; ++j) s += qs[qi][j] * ks[kk][j];
+      }
+      sc[i] = s;
+      tmax = fmaxf(tmax, s);
+    }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) tmax = fmaxf(tmax, __shfl_xor(tmax, off, 16));
+    const float m_new = fmaxf(m_run, tmax);
+    const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float pv = (sc[i] == -INFINITY) ? 0.f : expf(sc[i] - m_new);
+      ps[qi][sub + 16 * i] = pv;
+      psum += pv;
+    }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) psum += __shfl_xor(psum, off, 16);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+      const int j = sub + 16 * i;
+      if (j < DH) {
+        float a = acc[i] * alpha;
+        for (int kk = 0; kk < KT; ++kk) a += ps[qi][kk] * vs[kk][j];
+        acc[i] = a;
+      }
+    }
+  }
+  if (qi < nq) {
+    const float inv = 1.f / l_run;
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+      const int j = sub + 16 * i;
+      if (j < DH) st(o, (size_t)(b * P + q0 + qi) * d + h * DH + j, acc[i] * inv);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// decoder: mixture parameters and type log-probabilities for selected rows,
+// followed by the verify / draft / AR epilogue. One wave per row.
+// ---------------------------------------------------------------------------
+
+template <typename ACT>
+__global__ __launch_bounds__(256) void k_head(const ACT *__restrict__ e, int d, int M, int K,
+                                              const ACT *__restrict__ wmix, const float *__restrict__ bmix,
+                                              const ACT *__restrict__ wk2, const float *__restrict__ bk2,
+                                              HeadArgs a) {
+  __shared__ float vals[4][3 * TPPSD_MAX_MIX + TPPSD_MAX_TYPES];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int rows_per_seq = a.P - a.p0;
+  const int ridx = blockIdx.x * 4 + w;
+  const bool valid = ridx < a.B * rows_per_seq;
+  const int b = valid ? ridx / rows_per_seq : 0;
+  const int p = valid ? a.p0 + (ridx - b * rows_per_seq) : 0;
+  const size_t tok = (size_t)b * a.P + p;
+  float *v = vals[w];
+  const int nout = 3 * M + K;
+  if (valid) {
+    const ACT *er = e + tok * 4 * d;
+    for (int oi = lane; oi < nout; oi += 64) {
+      const ACT *xr, *wr;
+      float bias;
+      if (oi < 3 * M) {
+        xr = er + (oi / M) * d;
+        wr = wmix + (size_t)oi * d;
+        bias = bmix[oi];
+      } else {
+        xr = er + 3 * d;
+        wr = wk2 + (size_t)(oi - 3 * M) * d;
+        bias = bk2[oi - 3 * M];
+      }
+      float acc = 0.f;
+      for (int j = 0; j < d; ++j) acc += ld(xr, j) * ld(wr, j);
+      v[oi] = acc + bias;
+    }
+  }
+  __syncthreads();
+  // log-softmax of the mixture logits (lanes < M) and type logits (lanes < K);
+  // every wave reaches every barrier, rows past the end only skip the stores
+  const float lw = (valid && lane < M) ? v[lane] : -INFINITY;
+  const float mw = wave_max(lw);
+  const float sw = wave_sum(lane < M ? expf(lw - mw) : 0.f);
+  const float lk = (valid && lane < K) ? v[3 * M + lane] : -INFINITY;
+  const float mk = wave_max(lk);
+  const float sk = wave_sum(lane < K ? expf(lk - mk) : 0.f);
+  const float logw = lw - mw - logf(sw);
+  const float logk = lk - mk - logf(sk);
+  __syncthreads();
+  if (valid && lane < M) v[lane] = logw;
+  if (valid && lane < K) v[3 * M + lane] = logk;
+  __syncthreads();
+  if (!valid) return;
+  const size_t drow = (size_t)b * a.dst_stride + a.dst_row0 + (p - a.p0);
+  float *mixr = a.mix + drow * 3 * M;
+  float *ltr = a.logtype + drow * K;
+  for (int oi = lane; oi < 3 * M; oi += 64) mixr[oi] = v[oi];
+  if (lane < K) ltr[lane] = v[3 * M + lane];
+  const bool active = a.done == nullptr || a.done[b] == 0;
+  bool bad = false;
+  for (int oi = lane; oi < nout; oi += 64) bad |= !isfinite(v[oi]);
+  if (__ballot(bad) != 0ull && active && lane == 0) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+  if (lane != 0) return;
+  const float *Lw = v, *Mu = v + M, *S = v + 2 * M, *Lk = v + 3 * M;
+  if (a.mode == HEAD_VERIFY) {
+    if (p < a.gamma) {
+      const size_t di = (size_t)b * a.dr_stride + p;
+      const float lg = mix_logpdf(Lw, Mu, S, M, a.dr_tau[di]);
+      const int kk = min(max(a.dr_k[di], 0), K - 1);
+      a.v_logg[di] = lg;
+      a.v_logf[di] = Lk[kk];
+      if (!isfinite(lg) && active) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+    }
+  } else if (a.mode == HEAD_DRAFT) {
+    float u[4];
+    philox_uniforms(a.seed, (uint64_t)b, (uint64_t)a.rnd[b], (uint64_t)a.l_index, TAG_DRAFT, u);
+    const float tau = sample_tau(Lw, Mu, S, M, u[0], u[1], u[2]);
+    const int kk = sample_cat(Lk, K, u[3]);
+    const size_t di = (size_t)b * a.dr_stride + a.slot;
+    const float tprev = (a.slot == 0) ? a.ev_t[(size_t)b * a.ev_stride + a.n[b] - 1] : a.d_t[di - 1];
+    a.d_tau[di] = tau;
+    a.d_t[di] = tprev + tau;
+    a.d_k[di] = kk;
+    a.d_logg[di] = mix_logpdf(Lw, Mu, S, M, tau);
+    a.d_logf[di] = Lk[kk];
+    if (!isfinite(tau) && active) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+  } else {  // HEAD_AR
+    if (!active) return;
+    float u[4];
+    const int g = a.gen[b];
+    philox_uniforms(a.seed, (uint64_t)b, (uint64_t)g, 0ull, TAG_AR, u);
+    const float tau = sample_tau(Lw, Mu, S, M, u[0], u[1], u[2]);
+    const int kk = sample_cat(Lk, K, u[3]);
+    const int n = a.n[b];
+    if (n >= a.ev_stride) {
+      atomicOr(a.status, TPPSD_STATUS_CAPACITY);
+      return;
+    }
+    const float tn = a.ev_t[(size_t)b * a.ev_stride + n - 1] + tau;
+    a.ev_t[(size_t)b * a.ev_stride + n] = tn;
+    a.ev_k[(size_t)b * a.ev_stride + n] = kk;
+    if (a.ar_t_out) a.ar_t_out[(size_t)b * a.ar_out_stride + a.ar_step] = tn;
+    if (a.ar_k_out) a.ar_k_out[(size_t)b * a.ar_out_stride + a.ar_step] = kk;
+    a.n[b] = n + 1;
+    a.gen[b] = g + 1;
+    a.lenT[b] = n;
+    if (!isfinite(tau)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+    if (g + 1 >= a.n_gen) {
+      a.done[b] = 1;
+      atomicAdd(a.n_done, 1);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// accept / reject, adjusted-distribution replacement and commit (§4.3,
+// Eq. (3)-(4), Theorem 1, Algorithm 1). One wave per sequence.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= a.B) return;
+  const int G = a.gamma, MG = a.max_gamma, M = a.M, K = a.K;
+  if (a.done[b]) {
+    if (lane == 0) {
+      a.L[b] = 0;
+      a.n_new[b] = 0;
+      a.flags[b] = 16;
+      a.ar_iter[b] = -1;
+    }
+    return;
+  }
+  const uint64_t r = (uint64_t)a.rnd[b];
+  // verification tests: ln u < log p_T - log p_D for the interval and the type
+  int pass_t = 1, pass_k = 1;
+  if (lane < G) {
+    float ut, uk;
+    if (a.uniforms) {
+      ut = a.uniforms[((size_t)b * MG + lane) * 2];
+      uk = a.uniforms[((size_t)b * MG + lane) * 2 + 1];
+    } else {
+      float u[4];
+      philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)(lane + 1), TAG_ACCEPT, u);
+      ut = u[0];
+      uk = u[1];
+    }
+    const size_t i = (size_t)b * MG + lane;
+    pass_t = logf(ut) < a.v_logg[i] - a.d_logg[i];
+    pass_k = logf(uk) < a.v_logf[i] - a.d_logf[i];
+  }
+  const uint64_t fail = __ballot(lane < G && !(pass_t && pass_k));
+  const int L = fail ? __ffsll((unsigned long long)fail) : G + 1;
+  int at = 1, ak = 1;
+  if (L <= G) {
+    at = __shfl(pass_t, L - 1, 64);
+    ak = __shfl(pass_k, L - 1, 64);
+  }
+  float tauL = 0.f;
+  int kL = 0, ar_j = -1, flags = 0;
+  if (L <= G) {
+    const int li = L - 1;
+    const float *Tr = a.v_mix + ((size_t)b * (MG + 1) + li) * 3 * M;
+    const float *Dr = a.d_mix + ((size_t)b * MG + li) * 3 * M;
+    if (!at) {
+      // Theorem 1: candidates tau ~ g_T, accept iff u_a < 1 - exp(-(log g_T - log g_D));
+      // candidate j = base + lane, the lowest accepted index wins.
+      for (int base = 0;; base += 64) {
+        if (base >= TPPSD_AR_ITER_CAP) {
+          if (lane == 0) atomicOr(a.status, TPPSD_STATUS_AR_CAP);
+          ar_j = TPPSD_AR_ITER_CAP;
+          break;
+        }
+        float u[4];
+        philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)(base + lane), TAG_RES_T, u);
+        const float tau = sample_tau(Tr, Tr + M, Tr + 2 * M, M, u[0], u[1], u[2]);
+        const float delta = mix_logpdf(Tr, Tr + M, Tr + 2 * M, M, tau) - mix_logpdf(Dr, Dr + M, Dr + 2 * M, M, tau);
+        const bool acc = delta > 0.f && u[3] < -expm1f(-delta);
+        const uint64_t m = __ballot(acc);
+        if (m) {
+          const int jl = __ffsll((unsigned long long)m) - 1;
+          tauL = __shfl(tau, jl, 64);
+          ar_j = base + jl;
+          break;
+        }
+        tauL = __shfl(tau, 63, 64);
+      }
+      flags |= 1;
+    } else {
+      tauL = a.d_tau[(size_t)b * MG + li];
+    }
+    if (!ak) {
+      // Eq. (4): k ~ norm(max(0, f_T - f_D))
+      float u[4];
+      philox_uniforms(a.seed, (uint64_t)b, r, 0ull, TAG_RES_K, u);
+      const float *lT = a.v_logtype + ((size_t)b * (MG + 1) + li) * K;
+      const float *lD = a.d_logtype + ((size_t)b * MG + li) * K;
+      float tot = 0.f;
+      for (int kk = 0; kk < K; ++kk) tot += fmaxf(0.f, expf(lT[kk]) - expf(lD[kk]));
+      const float x = u[0] * tot;
+      float c = 0.f;
+      kL = K - 1;
+      for (int kk = 0; kk < K; ++kk) {
+        c += fmaxf(0.f, expf(lT[kk]) - expf(lD[kk]));
+        if (x < c) {
+          kL = kk;
+          break;
+        }
+      }
+      flags |= 2;
+    } else {
+      kL = a.d_k[(size_t)b * MG + li];
+    }
+  } else if (a.bonus) {
+    const float *Tr = a.v_mix + ((size_t)b * (MG + 1) + G) * 3 * M;
+    float u[4];
+    philox_uniforms(a.seed, (uint64_t)b, r, 0ull, TAG_BONUS, u);
+    tauL = sample_tau(Tr, Tr + M, Tr + 2 * M, M, u[0], u[1], u[2]);
+    kL = sample_cat(a.v_logtype + ((size_t)b * (MG + 1) + G) * K, K, u[3]);
+    flags |= 4;
+  }
+  if (lane != 0) return;
+  const int count = (L <= G) ? L : (a.bonus ? G + 1 : G);
+  const int n = a.n[b], gen = a.gen[b];
+  const int nn = min(count, a.n_gen - gen);
+  float tp = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+  const bool last_is_new = (L <= G) || a.bonus;
+  for (int i = 0; i < count; ++i) {
+    float ti;
+    int ki;
+    if (i < count - 1 || !last_is_new) {
+      ti = a.d_tau[(size_t)b * MG + i];
+      ki = a.d_k[(size_t)b * MG + i];
+    } else {
+      ti = tauL;
+      ki = kL;
+    }
+    tp = tp + ti;
+    const size_t oi = (size_t)b * (MG + 1) + i;
+    a.t_new[oi] = tp;
+    a.tau_new[oi] = ti;
+    a.k_new[oi] = ki;
+    if (i < nn) {
+      if (n + i < a.ev_stride) {
+        a.ev_t[(size_t)b * a.ev_stride + n + i] = tp;
+        a.ev_k[(size_t)b * a.ev_stride + n + i] = ki;
+      } else {
+        atomicOr(a.status, TPPSD_STATUS_CAPACITY);
+      }
+    }
+  }
+  if (last_is_new && !isfinite(tauL)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+  const int n2 = n + nn, g2 = gen + nn;
+  a.n[b] = n2;
+  a.gen[b] = g2;
+  a.lenT[b] = n2 - 1;
+  a.lenD[b] = n2 - 2;
+  a.rnd[b] = (int)r + 1;
+  if (g2 >= a.n_gen) {
+    a.done[b] = 1;
+    atomicAdd(a.n_done, 1);
+    flags |= 8;
+  }
+  a.L[b] = L;
+  a.n_new[b] = nn;
+  a.flags[b] = (uint8_t)flags;
+  a.ar_iter[b] = ar_j;
+  atomicAdd(&a.acc_stats[0], (unsigned long long)(L - 1));
+  atomicAdd(&a.acc_stats[1], (unsigned long long)G);
+  atomicAdd(&a.acc_stats[2], (unsigned long long)(ar_j >= 0 ? ar_j + 1 : 0));
+}
+
+// ---------------------------------------------------------------------------
+// run setup and event copies
+// ---------------------------------------------------------------------------
+
+__global__ void k_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, float *ev_t,
+                               int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
+                               int32_t *lenD, int32_t *done, int32_t *rnd, int32_t *zeros, int32_t *n_done,
+                               uint32_t *status, unsigned long long *acc_stats) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < B * n0) {
+    const int b = idx / n0, i = idx - b * n0;
+    ev_t[(size_t)b * ev_stride + i] = ht[idx];
+    ev_k[(size_t)b * ev_stride + i] = hk[idx];
+  }
+  if (idx < B) {
+    n[idx] = n0;
+    gen[idx] = 0;
+    lenT[idx] = n0 - 1;
+    lenD[idx] = n0 - 2;
+    done[idx] = n_gen <= 0 ? 1 : 0;
+    rnd[idx] = 0;
+    zeros[idx] = 0;
+  }
+  if (idx == 0) {
+    *n_done = n_gen <= 0 ? B : 0;
+    *status = 0u;
+    acc_stats[0] = acc_stats[1] = acc_stats[2] = 0ull;
+  }
+}
+
+__global__ void k_copy_events(const float *ev_t, const int32_t *ev_k, const int32_t *n, int B, int ev_stride,
+                              float *t, int32_t *k, int32_t *nout) {
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < (size_t)B * ev_stride) {
+    if (t) t[idx] = ev_t[idx];
+    if (k) k[idx] = ev_k[idx];
+  }
+  if (nout && idx < (size_t)B) nout[idx] = n[idx];
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+
+void launch_embed(float *x, int T, int d, int P, const TokSrc &src, const void *wtype, int bf16,
+                  const float *freq, int K, hipStream_t s) {
+  const int threads = d >= 256 ? 256 : (d >= 128 ? 128 : 64);
+  if (bf16)
+    k_embed<bf16_t><<<T, threads, 0, s>>>(x, d, P, src, (const bf16_t *)wtype, freq, K);
+  else
+    k_embed<float><<<T, threads, 0, s>>>(x, d, P, src, (const float *)wtype, freq, K);
+}
+
+void launch_layernorm(const float *x, void *y, int bf16, const float *g, const float *b, int T, int d,
+                      hipStream_t s) {
+  const int blocks = (T + 3) / 4;
+  if (bf16)
+    k_layernorm<bf16_t><<<blocks, 256, 0, s>>>(x, (bf16_t *)y, g, b, T, d);
+  else
+    k_layernorm<float><<<blocks, 256, 0, s>>>(x, (float *)y, g, b, T, d);
+}
+
+void launch_gemm(const void *X, const void *W, int bf16, int T, int N, int K, const Epi &epi, hipStream_t s) {
+  dim3 grid((N + 63) / 64, (T + 63) / 64);
+  if (bf16)
+    k_gemm_bf16<<<grid, 256, 0, s>>>((const bf16_t *)X, (const bf16_t *)W, T, N, K, epi);
+  else
+    k_gemm_f32<<<grid, 256, 0, s>>>((const float *)X, (const float *)W, T, N, K, epi);
+}
+
+template <typename ACT>
+static void attn_dispatch(const void *q, const void *kc, const void *vc, void *o, const int32_t *start,
+                          int start_off, const int32_t *done, int B, int P, int H, int dh, int cap,
+                          hipStream_t s) {
+  dim3 grid(B * H, (P + 15) / 16);
+  const ACT *Q = (const ACT *)q, *Kc = (const ACT *)kc, *Vc = (const ACT *)vc;
+  ACT *O = (ACT *)o;
+  switch (dh) {
+    case 16: k_attn_generic<ACT, 16><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
+    case 32: k_attn_generic<ACT, 32><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
+    case 64: k_attn_generic<ACT, 64><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
+    default: k_attn_generic<ACT, 128><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
+  }
+}
+
+void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16, const int32_t *start,
+                      int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, hipStream_t s) {
+  if (bf16)
+    attn_dispatch<bf16_t>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, s);
+  else
+    attn_dispatch<float>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, s);
+}
+
+void launch_head(const void *e, int bf16, int d, int M, int K, const void *wmix, const float *bmix,
+                 const void *wk2, const float *bk2, const HeadArgs &a, hipStream_t s) {
+  const int rows = a.B * (a.P - a.p0);
+  const int blocks = (rows + 3) / 4;
+  if (bf16)
+    k_head<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t *)e, d, M, K, (const bf16_t *)wmix, bmix,
+                                          (const bf16_t *)wk2, bk2, a);
+  else
+    k_head<float><<<blocks, 256, 0, s>>>((const float *)e, d, M, K, (const float *)wmix, bmix,
+                                         (const float *)wk2, bk2, a);
+}
+
+void launch_accept(const AcceptArgs &a, hipStream_t s) { k_accept<<<(a.B + 3) / 4, 256, 0, s>>>(a); }
+
+void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, float *ev_t,
+                         int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT, int32_t *lenD,
+                         int32_t *done, int32_t *rnd, int32_t *zeros, int32_t *n_done, uint32_t *status,
+                         unsigned long long *acc_stats, hipStream_t s) {
+  const int total = B * n0 > B ? B * n0 : B;
+  k_prefill_init<<<(total + 255) / 256, 256, 0, s>>>(ht, hk, B, n0, n_gen, ev_t, ev_k, ev_stride, n, gen, lenT,
+                                                     lenD, done, rnd, zeros, n_done, status, acc_stats);
+}
+
+void launch_copy_events(const float *ev_t, const int32_t *ev_k, const int32_t *n, int B, int ev_stride, float *t,
+                        int32_t *k, int32_t *nout, hipStream_t s) {
+  const size_t total = (size_t)B * ev_stride;
+  k_copy_events<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(ev_t, ev_k, n, B, ev_stride, t, k, nout);
+}
+
+}  // namespace tppsd

@@ -1,0 +1,63 @@
+"""GPU statistical check: TPP-SD sampling on the GPU has the law of GPU AR
+sampling (App. A.2), 10^5 sequences of a small model pair with a mismatched
+draft, K = 3 types. Per output position: two-sample KS on intervals and a
+chi-square contingency test on types, Bonferroni at 1 %."""
+import numpy as np
+import pytest
+import scipy.stats
+import torch
+
+from paper_2507_09252_amd import tppsd as tp
+from paper_2507_09252_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+GAMMA, N_GEN, B = 3, 8, 100000
+TCFG = W.ModelCfg(2, 32, 2, 64, 4, 3, "fp32")
+DCFG = W.ModelCfg(1, 16, 1, 32, 4, 3, "fp32")
+
+
+def _setup():
+    wt = W.make_weights(TCFG, np.random.SeedSequence([5, 1]), "paper")
+    wd = W.mismatch_draft(W.make_weights(DCFG, np.random.SeedSequence([5, 2]), "paper"), DCFG,
+                          np.random.SeedSequence([5, 3]))
+    rng = np.random.default_rng(0)
+    ht, _ = W.hpp(20, 1.0, rng)
+    hk = rng.integers(0, 3, 20)
+    HT = torch.from_numpy(np.tile(ht.astype(np.float32), (B, 1))).cuda()
+    HK = torch.from_numpy(np.tile(hk.astype(np.int32), (B, 1))).cuda()
+    return tp.Model(TCFG, wt), tp.Model(DCFG, wd), HT, HK
+
+
+def _intervals(t, k, n0):
+    t = t.cpu().numpy()[:, n0 - 1:n0 + N_GEN]
+    return np.diff(t, axis=1), k.cpu().numpy()[:, n0:n0 + N_GEN]
+
+
+def test_gpu_sd_law_equals_gpu_ar():
+    tm, dm, HT, HK = _setup()
+    n0 = HT.shape[1]
+    cap = n0 + N_GEN + GAMMA + 1
+    ar = tp.State(tm, None, B, cap, GAMMA, seed=101)
+    ar.tppsd_prefill(HT, HK, N_GEN)
+    ar.tppsd_sample_ar(N_GEN)
+    ta, ka, _ = ar.tppsd_read_events()
+    sd = tp.State(tm, dm, B, cap, GAMMA, seed=202)
+    sd.tppsd_prefill(HT, HK, N_GEN)
+    sd.tppsd_sample_sd(GAMMA)
+    ts, ks, ns = sd.tppsd_read_events()
+    st = sd.tppsd_state_status()
+    torch.cuda.synchronize()
+    assert st["bits"] == 0 and st["n_done"] == B
+    alpha = st["accepted"] / st["drafted"]
+    assert 0.3 < alpha < 0.8
+    a = _intervals(ta, ka, n0)
+    s = _intervals(ts, ks, n0)
+    ps = []
+    for j in range(N_GEN):
+        ps.append(scipy.stats.ks_2samp(a[0][:, j], s[0][:, j]).pvalue)
+        tab = np.stack([np.bincount(a[1][:, j], minlength=3), np.bincount(s[1][:, j], minlength=3)])
+        ps.append(scipy.stats.chi2_contingency(tab)[1])
+    ps = np.array(ps)
+    print(f"alpha {alpha:.3f}, min p {ps.min():.3g}")
+    assert ps.min() > 0.01 / len(ps), ps
