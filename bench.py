@@ -1,0 +1,171 @@
+"""Benchmark: accepted events/sec of TPP-SD sampling on one MI355X, vs the GPU
+autoregressive sampler, with the verify-attention kernel's roofline and the
+CPU oracle's rate as a reported baseline.
+
+A step is one complete sampling job over the batch: prefill of the seed
+histories (encoding them into both KV caches) followed by TPP-SD rounds
+(draft, verify, accept) until every sequence has n_gen new events.
+value = B * n_gen * steps / (timed seconds). The same job with naive AR
+sampling gives the speedup denominator.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2] [--gamma G]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "accepted events/sec (1 MI355X) SD vs AR; verify MFMA util %; KV-attn HBM GB/s"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="c2")
+    ap.add_argument("--gamma", type=int, default=None)
+    ap.add_argument("--ar-steps", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-events", type=int, default=64, help="oracle sample: events per sequence")
+    ap.add_argument("--cpu-seqs", type=int, default=4, help="oracle sample: sequences")
+    return ap.parse_args()
+
+
+def attention_bytes_per_launch(wl, gamma, B):
+    """Algorithmic HBM bytes of one verify-attention launch (all layers counted
+    per launch of one layer): keys and values of every cached position plus
+    the P new ones, read once, at the run-average context n0 + n_gen / 2;
+    plus the queries read and the outputs written."""
+    c = wl.target
+    elt = 2 if c.prec == "bf16" else 4
+    P = gamma + 1
+    ctx = wl.n_hist + wl.n_gen / 2.0
+    kv = B * c.n_heads * (ctx + P) * c.d_head * 2 * elt
+    qo = B * P * c.d_model * elt * 2
+    return kv + qo
+
+
+def cpu_baseline(wl, gamma, wt, wd, ht, hk, n_seq, n_events):
+    """The oracle (float64 NumPy, one thread) on a bounded sample of the same job."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import sampler as S
+    from oracle.model import Model as OModel
+    T, D = OModel(wl.target, wt), OModel(wl.draft, wd)
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        st = S.sample_sd(T, D, ht[:n_seq], hk[:n_seq], n_events, gamma, seed=1234)
+        dt = time.perf_counter() - t0
+    ev = int(st.gen.sum())
+    return {"value": ev / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n_seq} sequences x first {n_events} generated events of {wl.name} "
+                      f"(TPP-SD, gamma={gamma}), float64 NumPy, {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the batch shards across GPUs with no exchange, see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2507_09252_amd import tppsd as tp
+    from paper_2507_09252_amd import workloads as W
+
+    wl = W.WORKLOADS[args.config]
+    gamma = args.gamma or wl.gamma
+    B, n_gen = wl.batch, wl.n_gen
+    wt, wd = W.workload_weights(wl)
+    ht, hk = W.make_histories(wl)
+    dev = torch.device("cuda:0")
+    tm, dm = tp.Model(wl.target, wt, dev), tp.Model(wl.draft, wd, dev)
+    cap = wl.n_hist + n_gen + gamma + 1
+    sd = tp.State(tm, dm, B, cap, gamma, seed=1234)
+    ar = tp.State(tm, None, B, cap, gamma, seed=1234)
+    HT, HK = torch.from_numpy(ht).to(dev), torch.from_numpy(hk).to(dev)
+
+    def sd_job():
+        sd.tppsd_prefill(HT, HK, n_gen)
+        return sd.tppsd_sample_sd(gamma)
+
+    def ar_job():
+        ar.tppsd_prefill(HT, HK, n_gen)
+        ar.tppsd_sample_ar(n_gen)
+
+    for _ in range(args.warmup):
+        sd_job()
+        ar_job()
+    torch.cuda.synchronize()
+
+    # timed SD jobs (the verify-attention launches are bracketed by HIP events)
+    sd.tppsd_timing_enable(True)
+    rounds = 0
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        rounds += sd_job()
+    torch.cuda.synchronize()
+    t_sd = time.perf_counter() - t0
+    attn_ms, attn_launches = sd.tppsd_timing_read()
+    sd.tppsd_timing_enable(False)
+    st = sd.tppsd_state_status()
+    assert st["bits"] == 0 and st["n_done"] == B, st
+
+    t0 = time.perf_counter()
+    for _ in range(args.ar_steps):
+        ar_job()
+    torch.cuda.synchronize()
+    t_ar = time.perf_counter() - t0
+    sa = ar.tppsd_state_status()
+    assert sa["bits"] == 0 and sa["n_done"] == B, sa
+
+    events = B * n_gen
+    value = events * args.steps / t_sd
+    ar_value = events * args.ar_steps / t_ar
+    alpha = st["accepted"] / max(1, st["drafted"])
+    per_launch = attention_bytes_per_launch(wl, gamma, B)
+    avg_ms = attn_ms / max(1, attn_launches)
+    achieved = per_launch / (avg_ms * 1e-3) / 1e9 if attn_launches else 0.0
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "events/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t_sd * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.prec == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.description}", "batch": B, "n_gen": n_gen, "gamma": gamma,
+                   "history_events": wl.n_hist, "weights": "random N(0, 0.02^2), seeded"},
+        "ar_value": ar_value,
+        "speedup_vs_gpu_ar": value / ar_value,
+        "alpha": alpha,
+        "events_per_round": events * args.steps / max(1, rounds),
+        "rounds_per_job": rounds / args.steps,
+        "roofline": {"bound": "hbm", "kernel": "verify attention (k_attn)", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "avg_launch_us": avg_ms * 1e3, "launches": attn_launches,
+                     "algorithmic_bytes_per_launch": per_launch},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, gamma, wt, wd, ht, hk, min(args.cpu_seqs, B),
+                                           min(args.cpu_events, n_gen))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -149,6 +149,7 @@ def make_weights(cfg: ModelCfg, ss: np.random.SeedSequence, init: str = "paper")
     """Seeded parameters as float32 arrays (bf16-representable when cfg.prec is bf16).
 
     init = "paper": matrices N(0, 0.02^2), biases 0, LN (1, 0).
+    init = "bias": as "paper" but biases N(0, 0.1^2), LN gains 1 + N(0, 0.1^2), offsets N(0, 0.1^2).
     init = "stress": matrices N(0, s^2) with s = 1/sqrt(fan_in), biases N(0, 0.1^2),
                      LN gains 1 + N(0, 0.1^2), offsets N(0, 0.1^2).
     """
@@ -162,6 +163,14 @@ def make_weights(cfg: ModelCfg, ss: np.random.SeedSequence, init: str = "paper")
                 v = np.ones(shape)
             else:
                 v = np.zeros(shape)
+        elif init == "bias":
+            # paper-scale matrices, non-zero biases and LayerNorm parameters
+            if kind == "mat":
+                v = rng.normal(0.0, 0.02, size=shape)
+            elif kind == "ln_g":
+                v = 1.0 + rng.normal(0.0, 0.1, size=shape)
+            else:
+                v = rng.normal(0.0, 0.1, size=shape)
         elif init == "stress":
             if kind == "mat":
                 fan_in = shape[1]
