@@ -77,7 +77,7 @@ extern "C" {
 
 /* Model configuration. d_model % n_heads == 0; d_head = d_model / n_heads must
  * be 16, 32 or 64; bf16 models need
- * d_model and d_ffn to be multiples of 32. */
+  * d_model and d_ffn to be multiples of 32 (16 for fp32 models). */
 typedef struct {
   int32_t n_layers, d_model, n_heads, d_ffn, n_mix, n_types, prec;
 } tppsd_model_cfg;
@@ -230,10 +230,11 @@ int tppsd_read_events(tppsd_state *s, float *d_t, int32_t *d_k, int32_t *d_n, hi
 int tppsd_state_status(tppsd_state *s, hipStream_t stream, uint32_t *bits, int32_t *n_done,
                        int64_t *accepted_drafts, int64_t *drafted, int64_t *ar_candidates);
 
-/* Per-kernel timing: when enabled, the library brackets every launch of the
- * target's verify attention kernel with HIP events on the launch stream and
- * accumulates their durations; tppsd_timing_read synchronises and returns the
- * total milliseconds and launch count since the last reset. */
+/* Per-kernel timing: when enabled, tppsd_sample_sd launches its rounds
+ * directly (instead of replaying a captured HIP graph) and brackets every
+ * launch of the target's verify attention kernel with HIP events on the
+ * caller's stream; tppsd_timing_read returns the total milliseconds and the
+ * launch count since tppsd_timing_enable. Other entry points are not timed. */
 int tppsd_timing_enable(tppsd_state *s, int enable);
 int tppsd_timing_read(tppsd_state *s, double *ms, int64_t *launches);
 

@@ -23,6 +23,8 @@ HIPCC_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     # no packed-fp32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # device code reinterprets bf16 storage as MFMA vector operands (also in LDS)
+    "-fno-strict-aliasing",
     "-Wall", "-Wno-unused-function", "-Wno-unused-variable",
 ]
 

@@ -14,6 +14,8 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
+#include <functional>
 #include <string>
 #include <vector>
 
@@ -40,6 +42,11 @@ int hip_check(const char *what) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(TPPSD_E_HIP, "%s: %s", what, hipGetErrorString(e));
   return TPPSD_OK;
+}
+
+void drop_graph(hipGraphExec_t *g) {
+  if (*g) (void)hipGraphExecDestroy(*g);
+  *g = nullptr;
 }
 
 constexpr size_t ALIGN = 256;
@@ -114,6 +121,7 @@ int check_cfg(const tppsd_model_cfg *c) {
   if (c->d_model % 16) return fail(TPPSD_E_CONFIG, "d_model must be a multiple of 16");
   if (c->prec == TPPSD_PREC_BF16 && (c->d_model % 32 || c->d_ffn % 32))
     return fail(TPPSD_E_CONFIG, "bf16 models need d_model and d_ffn multiples of 32");
+  if (c->d_ffn % 16) return fail(TPPSD_E_CONFIG, "d_ffn must be a multiple of 16");
   if (c->n_mix > TPPSD_MAX_MIX) return fail(TPPSD_E_CONFIG, "n_mix > %d", TPPSD_MAX_MIX);
   if (c->n_types > TPPSD_MAX_TYPES) return fail(TPPSD_E_CONFIG, "n_types > %d", TPPSD_MAX_TYPES);
   return TPPSD_OK;
@@ -166,6 +174,8 @@ struct tppsd_state {
   float *x = nullptr;
   void *a = nullptr, *q = nullptr, *o = nullptr, *hid = nullptr, *e = nullptr;
   float *ar_mix = nullptr, *ar_logtype = nullptr;
+  float *attn_part = nullptr;
+  int32_t *gen0 = nullptr;
   // internal round buffers (tppsd_sample_sd)
   tppsd_draft_buf idr{};
   tppsd_verify_buf ivf{};
@@ -175,13 +185,27 @@ struct tppsd_state {
   bool prefilled = false, draft_ok = false, drafted_this_round = false;
   int32_t *host_ndone = nullptr;   // pinned, 2 slots
   hipEvent_t poll_ev[2] = {nullptr, nullptr};
-  // timing of the verify attention kernel
+  // timing of the verify attention kernel: HIP events around its launches,
+  // recorded as nodes of the captured round graph (two graph instances with
+  // their own events, alternated per round and read one round behind)
   bool timing = false;
-  std::vector<hipEvent_t> tev;
-  size_t tev_used = 0;
+  std::vector<hipEvent_t> gev[2];
+  hipEvent_t *cur_ev = nullptr;      // events of the graph being captured
   double t_ms = 0.0;
   int64_t t_launches = 0;
+  // HIP graphs of the sampling loops, captured on a private stream and
+  // replayed on the caller's; keyed by what their kernel arguments embed
+  hipStream_t cap_stream = nullptr;
+  bool use_graphs = true;
+  hipGraphExec_t sd_exec[2] = {nullptr, nullptr};
+  long long sd_key = -1;
+  hipGraphExec_t ar_exec[2] = {nullptr, nullptr};   // 1 step, AR_CHUNK steps
+  long long ar_key[2] = {-1, -1};
 };
+
+namespace {
+constexpr int AR_CHUNK = 8;
+}
 
 namespace {
 
@@ -189,7 +213,7 @@ struct WsLayout {
   size_t total = 0;
   size_t status, n_done, acc, n, gen, lenT, lenD, done, rnd, zeros, ev_t, ev_k;
   size_t freqT, freqD, kT, vT, kD, vD, layerT, layerD;
-  size_t x, a, q, o, hid, e, ar_mix, ar_lt;
+  size_t x, a, q, o, hid, e, ar_mix, ar_lt, attn_part, gen0;
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt;
   size_t v_logg, v_logf, v_mix, v_lt;
   size_t a_L, a_nnew, a_knew, a_tnew, a_taunew, a_ar, a_flags;
@@ -239,6 +263,13 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   w.e = take(Tm * 4 * dmax * 4);
   w.ar_mix = take(Bz * 3 * mmax * 4);
   w.ar_lt = take(Bz * kmax * 4);
+  {
+    const int qtm = (Pmax + 15) / 16;
+    size_t pf = attn_part_floats(B, T->H(), T->dh(), qtm, cap);
+    if (D) pf = std::max(pf, attn_part_floats(B, D->H(), D->dh(), qtm, cap));
+    w.attn_part = take(pf * 4);
+  }
+  w.gen0 = take(Bz * 4);
   const size_t M = T->cfg.n_mix, K = T->cfg.n_types;
   w.d_tau = take(Bz * MG * 4);
   w.d_t = take(Bz * MG * 4);
@@ -288,26 +319,10 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     e.cap = s->cap;
     e.status = s->status;
     launch_gemm(s->a, w.qkv_w, bf, T, 3 * d, d, e, st);
-    const bool timed = time_attn && s->timing;
-    if (timed) {
-      if (s->tev_used + 2 > s->tev.size()) {
-        // drain: accumulate finished pairs and reuse the events
-        hipStreamSynchronize(st);
-        for (size_t i = 0; i + 1 < s->tev_used; i += 2) {
-          float ms = 0.f;
-          hipEventElapsedTime(&ms, s->tev[i], s->tev[i + 1]);
-          s->t_ms += ms;
-        }
-        s->tev_used = 0;
-      }
-      hipEventRecord(s->tev[s->tev_used], st);
-    }
-    launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->cap, st);
-    if (timed) {
-      hipEventRecord(s->tev[s->tev_used + 1], st);
-      s->tev_used += 2;
-      s->t_launches += 1;
-    }
+    const bool timed = time_attn && s->cur_ev != nullptr;
+    if (timed) (void)hipEventRecord(s->cur_ev[2 * l], st);
+    launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->cap, s->attn_part, st);
+    if (timed) (void)hipEventRecord(s->cur_ev[2 * l + 1], st);
     Epi eo{};
     eo.mode = EPI_RESID;
     eo.bias = w.out_b;
@@ -638,6 +653,8 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->e = ws + w.e;
   s->ar_mix = (float *)(ws + w.ar_mix);
   s->ar_logtype = (float *)(ws + w.ar_lt);
+  s->attn_part = (float *)(ws + w.attn_part);
+  s->gen0 = (int32_t *)(ws + w.gen0);
   s->idr = {(float *)(ws + w.d_tau), (float *)(ws + w.d_t), (int32_t *)(ws + w.d_k), (float *)(ws + w.d_logg),
             (float *)(ws + w.d_logf), (float *)(ws + w.d_mix), (float *)(ws + w.d_lt)};
   s->ivf = {(float *)(ws + w.v_logg), (float *)(ws + w.v_logf), (float *)(ws + w.v_mix), (float *)(ws + w.v_lt)};
@@ -655,6 +672,14 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
       return hip_check("tppsd_state_create: frequency table upload");
     }
   }
+  {
+    if (hipStreamCreateWithFlags(&s->cap_stream, hipStreamNonBlocking) != hipSuccess) {
+      tppsd_state_destroy(s);
+      return hip_check("tppsd_state_create: capture stream");
+    }
+    const char *ng = getenv("TPPSD_NO_GRAPHS");
+    s->use_graphs = !(ng && ng[0] == '1');
+  }
   if (hipHostMalloc((void **)&s->host_ndone, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&s->poll_ev[0], hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&s->poll_ev[1], hipEventDisableTiming) != hipSuccess) {
@@ -667,10 +692,16 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
 
 void tppsd_state_destroy(tppsd_state *s) {
   if (!s) return;
-  if (s->host_ndone) hipHostFree(s->host_ndone);
+  if (s->host_ndone) (void)hipHostFree(s->host_ndone);
   for (hipEvent_t e : s->poll_ev)
-    if (e) hipEventDestroy(e);
-  for (hipEvent_t e : s->tev) hipEventDestroy(e);
+    if (e) (void)hipEventDestroy(e);
+  drop_graph(&s->sd_exec[0]);
+  drop_graph(&s->sd_exec[1]);
+  for (auto &v : s->gev)
+    for (hipEvent_t e : v) (void)hipEventDestroy(e);
+  drop_graph(&s->ar_exec[0]);
+  drop_graph(&s->ar_exec[1]);
+  if (s->cap_stream) (void)hipStreamDestroy(s->cap_stream);
   delete s;
 }
 
@@ -743,53 +774,154 @@ int tppsd_accept(tppsd_state *s, int gamma, const tppsd_draft_buf *dr, const tpp
   return rc;
 }
 
+namespace {
+
+// one AR step (§4.2 naive sampling): target pass over the pending event, then a draw
+int ar_step(tppsd_state *s, int out_stride, float *d_t_out, int32_t *d_k_out, hipStream_t st) {
+  TokSrc src{};
+  src.ev_t = s->ev_t;
+  src.ev_k = s->ev_k;
+  src.ev_stride = s->cap;
+  src.start = s->lenT;
+  src.start_off = 0;
+  src.n_ev = 1;
+  HeadArgs h = head_common(s);
+  h.mode = HEAD_AR;
+  h.P = 1;
+  h.p0 = 0;
+  h.mix = s->ar_mix;
+  h.logtype = s->ar_logtype;
+  h.dst_stride = 1;
+  h.dst_row0 = 0;
+  h.ar_t_out = d_t_out;
+  h.ar_k_out = d_k_out;
+  h.ar_out_stride = out_stride;
+  h.gen0 = s->gen0;
+  return forward(s, s->T, s->cT, s->lenT, 0, 1, src, &h, false, st);
+}
+
+// Captures body() into an executable graph (on the private capture stream).
+int capture(tppsd_state *s, const std::function<int(hipStream_t)> &body, hipGraphExec_t *out) {
+  hipGraph_t g = nullptr;
+  if (hipStreamBeginCapture(s->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess)
+    return hip_check("graph capture begin");
+  const int rc = body(s->cap_stream);
+  const hipError_t e = hipStreamEndCapture(s->cap_stream, &g);
+  if (rc != TPPSD_OK || e != hipSuccess) {
+    if (g) (void)hipGraphDestroy(g);
+    return rc != TPPSD_OK ? rc : fail(TPPSD_E_HIP, "graph capture: %s", hipGetErrorString(e));
+  }
+  const hipError_t e2 = hipGraphInstantiate(out, g, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(g);
+  if (e2 != hipSuccess) return fail(TPPSD_E_HIP, "graph instantiate: %s", hipGetErrorString(e2));
+  return TPPSD_OK;
+}
+
+}  // namespace
+
 int tppsd_sample_ar(tppsd_state *s, int n_events, float *d_t_out, int32_t *d_k_out, hipStream_t st) {
   if (!s) return fail(TPPSD_E_ARG, "null state");
   if (!s->prefilled) return fail(TPPSD_E_ORDER, "call tppsd_prefill first");
   if (n_events < 0) return fail(TPPSD_E_ARG, "n_events < 0");
-  for (int i = 0; i < n_events; ++i) {
-    TokSrc src{};
-    src.ev_t = s->ev_t;
-    src.ev_k = s->ev_k;
-    src.ev_stride = s->cap;
-    src.start = s->lenT;
-    src.start_off = 0;
-    src.n_ev = 1;
-    HeadArgs h = head_common(s);
-    h.mode = HEAD_AR;
-    h.P = 1;
-    h.p0 = 0;
-    h.mix = s->ar_mix;
-    h.logtype = s->ar_logtype;
-    h.dst_stride = 1;
-    h.dst_row0 = 0;
-    h.ar_t_out = d_t_out;
-    h.ar_k_out = d_k_out;
-    h.ar_out_stride = n_events;
-    h.ar_step = i;
-    forward(s, s->T, s->cT, s->lenT, 0, 1, src, &h, false, st);
+  if (n_events == 0) return TPPSD_OK;
+  launch_snapshot(s->gen, s->gen0, s->B, st);   // output column = events generated in this call
+  int i = 0;
+  if (s->use_graphs) {
+    // graphs embed the output pointers, their stride and n_gen
+    const long long key = ((long long)(uintptr_t)d_t_out * 31 + (long long)(uintptr_t)d_k_out) * 131 +
+                          (long long)n_events * 1000003LL + s->n_gen;
+    for (int w = 0; w < 2; ++w) {
+      if (s->ar_exec[w] && s->ar_key[w] == key) continue;
+      drop_graph(&s->ar_exec[w]);
+      const int steps = w ? AR_CHUNK : 1;
+      int rc = capture(s, [&](hipStream_t cs) {
+        for (int k = 0; k < steps; ++k)
+          if (int r = ar_step(s, n_events, d_t_out, d_k_out, cs)) return r;
+        return hip_check("tppsd_sample_ar capture");
+      }, &s->ar_exec[w]);
+      if (rc) return rc;
+      s->ar_key[w] = key;
+    }
+    for (; i + AR_CHUNK <= n_events; i += AR_CHUNK)
+      if (hipGraphLaunch(s->ar_exec[1], st) != hipSuccess) return hip_check("tppsd_sample_ar: graph launch");
+    for (; i < n_events; ++i)
+      if (hipGraphLaunch(s->ar_exec[0], st) != hipSuccess) return hip_check("tppsd_sample_ar: graph launch");
+  } else {
+    for (; i < n_events; ++i)
+      if (int rc = ar_step(s, n_events, d_t_out, d_k_out, st)) return rc;
   }
-  if (n_events > 0) s->draft_ok = false;
+  s->draft_ok = false;
   return hip_check("tppsd_sample_ar");
 }
+
+namespace {
+// adds the verify-attention times recorded in event set w during its last round
+void read_round_events(tppsd_state *s, int w) {
+  for (size_t i = 0; i + 1 < s->gev[w].size(); i += 2) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, s->gev[w][i], s->gev[w][i + 1]) == hipSuccess) {
+      s->t_ms += ms;
+      s->t_launches += 1;
+    }
+  }
+}
+}  // namespace
 
 int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipStream_t st) {
   if (int rc = check_round(s, gamma)) return rc;
   if (!s->D) return fail(TPPSD_E_ORDER, "state has no draft model");
   if (!s->draft_ok) return fail(TPPSD_E_ORDER, "draft cache is stale; prefill again");
+  // timed runs launch eagerly so that host-recorded HIP events can bracket the
+  // verify-attention launches; otherwise each round replays one captured graph
+  const bool timed = s->timing;
+  const bool graphs = s->use_graphs && !timed;
+  if (graphs) {
+    const long long key = (long long)gamma * 100000007LL + s->n_gen;
+    if (!s->sd_exec[0] || s->sd_key != key) {
+      drop_graph(&s->sd_exec[0]);
+      int rc = capture(s, [&](hipStream_t cs) {
+        int r = do_draft(s, gamma, &s->idr, cs);
+        if (!r) r = do_verify(s, gamma, &s->idr, &s->ivf, cs);
+        if (!r) r = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, cs);
+        return r;
+      }, &s->sd_exec[0]);
+      if (rc) return rc;
+      s->sd_key = key;
+    }
+  }
+  if (timed) {
+    for (auto &v : s->gev)
+      if (v.empty()) {
+        v.resize(2 * s->T->cfg.n_layers);
+        for (hipEvent_t &e : v)
+          if (hipEventCreate(&e) != hipSuccess) return hip_check("tppsd_sample_sd: timing events");
+      }
+  }
   int r = 0;
   for (; r < max_rounds; ++r) {
     if (r >= 1) {
       // the done counter copied after round r - 1; waits for that round only
       if (hipEventSynchronize(s->poll_ev[(r - 1) & 1]) != hipSuccess) return hip_check("tppsd_sample_sd: poll");
+      if (timed) read_round_events(s, (r - 1) & 1);
       if (s->host_ndone[(r - 1) & 1] >= s->B) break;
     }
-    int rc = do_draft(s, gamma, &s->idr, st);
-    if (!rc) rc = do_verify(s, gamma, &s->idr, &s->ivf, st);
-    if (!rc) rc = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, st);
-    if (rc) return rc;
-    hipMemcpyAsync(&s->host_ndone[r & 1], s->n_done, sizeof(int32_t), hipMemcpyDeviceToHost, st);
-    hipEventRecord(s->poll_ev[r & 1], st);
+    if (graphs) {
+      if (hipGraphLaunch(s->sd_exec[0], st) != hipSuccess) return hip_check("tppsd_sample_sd: graph launch");
+    } else {
+      s->cur_ev = timed ? s->gev[r & 1].data() : nullptr;
+      int rc = do_draft(s, gamma, &s->idr, st);
+      if (!rc) rc = do_verify(s, gamma, &s->idr, &s->ivf, st);
+      if (!rc) rc = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, st);
+      s->cur_ev = nullptr;
+      if (rc) return rc;
+    }
+    if (hipMemcpyAsync(&s->host_ndone[r & 1], s->n_done, sizeof(int32_t), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipEventRecord(s->poll_ev[r & 1], st) != hipSuccess)
+      return hip_check("tppsd_sample_sd: poll");
+  }
+  if (timed && r == max_rounds && r >= 1) {
+    if (hipEventSynchronize(s->poll_ev[(r - 1) & 1]) != hipSuccess) return hip_check("tppsd_sample_sd: poll");
+    read_round_events(s, (r - 1) & 1);
   }
   if (rounds) *rounds = r;
   return hip_check("tppsd_sample_sd");
@@ -822,13 +954,7 @@ int tppsd_state_status(tppsd_state *s, hipStream_t st, uint32_t *bits, int32_t *
 
 int tppsd_timing_enable(tppsd_state *s, int enable) {
   if (!s) return fail(TPPSD_E_ARG, "null state");
-  if (enable && s->tev.empty()) {
-    s->tev.resize(4096);
-    for (hipEvent_t &e : s->tev)
-      if (hipEventCreate(&e) != hipSuccess) return hip_check("tppsd_timing_enable");
-  }
   s->timing = enable != 0;
-  s->tev_used = 0;
   s->t_ms = 0.0;
   s->t_launches = 0;
   return TPPSD_OK;
@@ -836,13 +962,6 @@ int tppsd_timing_enable(tppsd_state *s, int enable) {
 
 int tppsd_timing_read(tppsd_state *s, double *ms, int64_t *launches) {
   if (!s) return fail(TPPSD_E_ARG, "null state");
-  for (size_t i = 0; i + 1 < s->tev_used; i += 2) {
-    if (hipEventSynchronize(s->tev[i + 1]) != hipSuccess) return hip_check("tppsd_timing_read");
-    float t = 0.f;
-    hipEventElapsedTime(&t, s->tev[i], s->tev[i + 1]);
-    s->t_ms += t;
-  }
-  s->tev_used = 0;
   if (ms) *ms = s->t_ms;
   if (launches) *launches = s->t_launches;
   return TPPSD_OK;

@@ -72,10 +72,11 @@ struct HeadArgs {
   int n_gen;
   uint64_t seed;
   uint32_t *status;
-  // HEAD_AR optional outputs [B, out_stride]
+  // HEAD_AR optional outputs [B, out_stride], written at column gen - gen0
   float *ar_t_out;
   int32_t *ar_k_out;
-  int ar_out_stride, ar_step;
+  int ar_out_stride;
+  const int32_t *gen0;
 };
 
 struct AcceptArgs {
@@ -104,9 +105,30 @@ void launch_layernorm(const float *x, void *y, int bf16, const float *g, const f
                       hipStream_t st);
 void launch_gemm(const void *X, const void *W, int bf16, int T, int N, int K, const Epi &epi,
                  hipStream_t st);
+// Key splits of the bf16 attention for B sequences x H heads x qtiles query
+// tiles over at most max_keys keys: enough workgroups to fill the chip, each
+// split keeping at least 128 keys.
+inline int attn_splits(int B, int H, int qtiles, int max_keys) {
+  const long items = (long)B * H * qtiles;
+  int s = 1;
+  while (s < 8 && items * s < 1024 && max_keys / (2 * s) >= 128) s *= 2;
+  return s;
+}
+// floats of split partials needed for up to qtiles_max query tiles
+inline size_t attn_part_floats(int B, int H, int dh, int qtiles_max, int max_keys) {
+  size_t best = 0;
+  for (int qt = 1; qt <= qtiles_max; ++qt) {
+    const int s = attn_splits(B, H, qt, max_keys);
+    if (s > 1) {
+      const size_t n = (size_t)B * H * qt * 16 * s * (dh + 2);
+      if (n > best) best = n;
+    }
+  }
+  return best;
+}
 void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16,
                       const int32_t *start, int start_off, const int32_t *done, int B, int P, int H,
-                      int dh, int cap, hipStream_t st);
+                      int dh, int cap, float *part, hipStream_t st);
 void launch_head(const void *e, int bf16, int d, int M, int K, const void *wmix, const float *bmix,
                  const void *wk2, const float *bk2, const HeadArgs &a, hipStream_t st);
 void launch_accept(const AcceptArgs &a, hipStream_t st);
@@ -114,6 +136,7 @@ void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int 
                          int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
                          int32_t *lenD, int32_t *done, int32_t *rnd, int32_t *zeros, int32_t *n_done,
                          uint32_t *status, unsigned long long *acc_stats, hipStream_t st);
+void launch_snapshot(const int32_t *src, int32_t *dst, int B, hipStream_t st);
 void launch_copy_events(const float *ev_t, const int32_t *ev_k, const int32_t *n, int B, int ev_stride,
                         float *t, int32_t *k, int32_t *nout, hipStream_t st);
 

@@ -11,6 +11,7 @@
 // stream, LayerNorm statistics, softmax and all decoder math in fp32.
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <stdlib.h>
 #include <stdint.h>
 
 #include "tppsd_internal.h"
@@ -221,93 +222,81 @@ __device__ __forceinline__ void epilogue(const Epi &e, int r, int n, float acc) 
   }
 }
 
-// fp32 GEMM on the vector ALU: 64x64 tile per 256-thread block, 4x4 per thread.
-__global__ __launch_bounds__(256) void k_gemm_f32(const float *__restrict__ X, const float *__restrict__ W,
-                                                  int T, int N, int K, Epi e) {
-  __shared__ float As[16][64 + 4];
-  __shared__ float Ws[16][64 + 4];
-  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  float acc[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += 16) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int idx = tid + 256 * i, rr = idx >> 4, kk = idx & 15;
-      const int gr = r0 + rr, gc = c0 + rr, gk = k0 + kk;
-      As[kk][rr] = (gr < T && gk < K) ? X[(size_t)gr * K + gk] : 0.f;
-      Ws[kk][rr] = (gc < N && gk < K) ? W[(size_t)gc * K + gk] : 0.f;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
-      float a[4], w[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        a[i] = As[kk][ty * 4 + i];
-        w[i] = Ws[kk][tx * 4 + i];
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] += a[i] * w[j];
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = r0 + ty * 4 + i, n = c0 + tx * 4 + j;
-      if (r < T && n < N) epilogue<float>(e, r, n, acc[i][j]);
-    }
-}
-
-// bf16 GEMM on MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulate): 64x64 tile
-// per 256-thread block, each wave a 32x32 quadrant of 2x2 MFMA tiles. Lane l
-// holds 8 consecutive k of row (l mod 16) of each operand; the accumulator
-// holds rows 4 (l / 16) + i, column l mod 16. K must be a multiple of 32.
+// GEMM on MFMA with fp32 accumulation. A workgroup of 4 waves (2 x 2) owns a
+// (32 TM) x (32 TN) output tile; each wave owns TM x TN 16x16 accumulator
+// tiles. Operands are read straight from global memory (weights stay in L2):
+// for every 16x16 tile lane l holds row (l mod 16) of A and of W (W is stored
+// [N, K], so its rows are B's columns) over one slice of the k range; the
+// accumulator holds rows 4 (l / 16) + i, column l mod 16.
+//   bf16: v_mfma_f32_16x16x32_bf16, lane slice = 8 consecutive k, 32 k per step.
+//   fp32: v_mfma_f32_16x16x4f32, lane l loads 4 consecutive k (4 (l / 16) .. + 3)
+//         and issues one MFMA per element; across the four MFMAs the 16 k of the
+//         step are each used once, the same k for A and B (K must be a
+//         multiple of 16).
+// bf16 MFMA operands are only ever produced by whole-vector loads or by
+// bit-casting packed 32-bit words; individual __bf16 elements are never read
+// or written (element access on __bf16 vectors gave wrong values on gfx950).
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t *__restrict__ X, const bf16_t *__restrict__ W,
-                                                   int T, int N, int K, Epi e) {
+template <typename ELT> struct MfmaStep;
+template <> struct MfmaStep<bf16_t> {
+  static constexpr int KSTEP = 32;
+  typedef bf16x8_t frag;
+  static __device__ __forceinline__ frag load(const bf16_t *p, int g) { return *(const bf16x8_t *)(p + 8 * g); }
+  static __device__ __forceinline__ f32x4_t mma(frag a, frag b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct MfmaStep<float> {
+  static constexpr int KSTEP = 16;
+  typedef f32x4_t frag;
+  static __device__ __forceinline__ frag load(const float *p, int g) { return *(const f32x4_t *)(p + 4 * g); }
+  static __device__ __forceinline__ f32x4_t mma(frag a, frag b, f32x4_t c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
+  }
+};
+
+template <typename ELT, int TM, int TN>
+__global__ __launch_bounds__(256) void k_gemm_mfma(const ELT *__restrict__ X, const ELT *__restrict__ W, int T,
+                                                   int N, int K, Epi e) {
+  typedef MfmaStep<ELT> S;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int m0 = blockIdx.y * 64 + (wave >> 1) * 32;
-  const int n0 = blockIdx.x * 64 + (wave & 1) * 32;
+  const int m0 = blockIdx.y * (32 * TM) + (wave >> 1) * (16 * TM);
+  const int n0 = blockIdx.x * (32 * TN) + (wave & 1) * (16 * TN);
   const int rr = lane & 15, g = lane >> 4;
-  f32x4_t acc[2][2];
+  f32x4_t acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-  const bf16_t *xa[2], *wb[2];
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  const ELT *xa[TM], *wb[TN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int row = min(m0 + 16 * i + rr, T - 1);
-    const int col = min(n0 + 16 * i + rr, N - 1);
-    xa[i] = X + (size_t)row * K + 8 * g;
-    wb[i] = W + (size_t)col * K + 8 * g;
-  }
-  for (int k0 = 0; k0 < K; k0 += 32) {
-    bf16x8_t a[2], b[2];
+  for (int i = 0; i < TM; ++i) xa[i] = X + (size_t)min(m0 + 16 * i + rr, T - 1) * K;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      a[i] = *(const bf16x8_t *)(xa[i] + k0);
-      b[i] = *(const bf16x8_t *)(wb[i] + k0);
-    }
+  for (int j = 0; j < TN; ++j) wb[j] = W + (size_t)min(n0 + 16 * j + rr, N - 1) * K;
+  for (int k0 = 0; k0 < K; k0 += S::KSTEP) {
+    typename S::frag a[TM], b[TN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TM; ++i) a[i] = S::load(xa[i] + k0, g);
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    for (int j = 0; j < TN; ++j) b[j] = S::load(wb[j] + k0, g);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = S::mma(a[i], b[j], acc[i][j]);
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int r = m0 + 16 * i + 4 * g + v, n = n0 + 16 * j + rr;
-        if (r < T && n < N) epilogue<bf16_t>(e, r, n, acc[i][j][v]);
+        if (r < T && n < N) epilogue<ELT>(e, r, n, acc[i][j][v]);
       }
 }
 
@@ -416,6 +405,193 @@ __global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q,
   }
 }
 
+// bf16 causal attention on MFMA with split keys (flash-decoding style).
+// Grid (B * H, query tiles of 16, splits), 4 waves per workgroup. A split
+// owns a contiguous key range of its (sequence, head); its waves take 32-key
+// steps round robin and keep their own online-softmax state, merged in LDS at
+// the end. With one split the merged result is the output, otherwise the
+// split writes (max, sum, unnormalised output) and k_attn_combine merges.
+//
+// Per 32-key step, S^T = K Q^T is two 16x16 MFMA tiles whose rows are
+// permuted so that lane l ends up holding the scores of query (l mod 16)
+// for the 8 consecutive keys 8 (l / 16) .. + 7: exactly the B operand of
+// O^T = V^T P^T. The A operand (V transposed) goes through LDS.
+typedef short short4_t __attribute__((ext_vector_type(4)));
+
+template <int DH>
+__global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q, const bf16_t *__restrict__ kc,
+                                                   const bf16_t *__restrict__ vc, bf16_t *__restrict__ o,
+                                                   const int32_t *__restrict__ start, int start_off,
+                                                   const int32_t *__restrict__ done, int P, int H, int cap,
+                                                   int splits, float *__restrict__ part) {
+  constexpr int KT = 32, NDT = DH / 16, VROW = KT + 16;   // V^T rows padded to 96 bytes
+  __shared__ __attribute__((aligned(16))) bf16_t vt[4][DH][VROW];
+  __shared__ float red_m[4][16], red_l[4][16];
+  __shared__ float red_o[4][DH][17];
+  const int bh = blockIdx.x, b = bh / H, h = bh - b * H;
+  const int qt = blockIdx.y, q0 = qt * 16, split = blockIdx.z;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, rr = lane & 15, g = lane >> 4;
+  const int d = H * DH;
+  const int nq = min(16, P - q0);
+  const bool skip = done != nullptr && done[b] != 0;
+  const int base = start[b] + start_off;
+  const int n_keys = skip ? 0 : base + q0 + nq;
+  int chunk = (n_keys + splits - 1) / splits;
+  chunk = (chunk + KT - 1) / KT * KT;
+  const int k_begin = split * chunk, k_end = min(n_keys, k_begin + chunk);
+  const size_t kvbase = ((size_t)b * H + h) * cap;
+  const float scale = 1.f / sqrtf((float)DH);
+  const int my_q = q0 + rr;                 // this lane's query (column of S^T)
+  const int my_last = base + my_q;          // last key it may see
+  const bool q_ok = rr < nq;
+
+  // query fragment (B operand of S^T): Q[my_q][k-slice]
+  bf16x8_t qf[DH >= 32 ? DH / 32 : 1];
+  short4_t qf16 = {0, 0, 0, 0};
+  if (DH >= 32) {
+#pragma unroll
+    for (int c = 0; c < DH / 32; ++c) {
+      if (q_ok)
+        qf[c] = *(const bf16x8_t *)(q + (size_t)(b * P + my_q) * d + h * DH + 32 * c + 8 * g);
+      else
+        qf[c] = (bf16x8_t){};
+    }
+  } else {
+    if (q_ok) qf16 = *(const short4_t *)(q + (size_t)(b * P + my_q) * d + h * DH + 4 * g);
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t oacc[NDT];
+#pragma unroll
+  for (int t = 0; t < NDT; ++t) oacc[t] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  // permuted key rows of the two S^T halves loaded by this lane
+  const int krow0 = 8 * (rr >> 2) + (rr & 3), krow1 = krow0 + 4;
+
+  for (int kt = k_begin + wave * KT; kt < k_end; kt += 4 * KT) {
+    const size_t r0 = kvbase + min(kt + krow0, cap - 1), r1 = kvbase + min(kt + krow1, cap - 1);
+    f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    if (DH >= 32) {
+#pragma unroll
+      for (int c = 0; c < DH / 32; ++c) {
+        const bf16x8_t a0 = *(const bf16x8_t *)(kc + r0 * DH + 32 * c + 8 * g);
+        const bf16x8_t a1 = *(const bf16x8_t *)(kc + r1 * DH + 32 * c + 8 * g);
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[c], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qf[c], s1, 0, 0, 0);
+      }
+    } else {
+      const short4_t a0 = *(const short4_t *)(kc + r0 * DH + 4 * g);
+      const short4_t a1 = *(const short4_t *)(kc + r1 * DH + 4 * g);
+      s0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, qf16, s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, qf16, s1, 0, 0, 0);
+    }
+    // stage this step's values transposed: vt[wave][j][key] = V[kt + key][j]
+    for (int c = lane; c < KT * DH / 8; c += 64) {
+      const int key = c / (DH / 8), j0 = (c - key * (DH / 8)) * 8;
+      // keys past the range are zero (never-written cache slots may hold NaN bits);
+      // values move as raw 32-bit words (two bf16 each)
+      uint4 v = {0u, 0u, 0u, 0u};
+      if (kt + key < k_end) v = *(const uint4 *)(vc + (kvbase + kt + key) * DH + j0);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        vt[wave][j0 + e][key] = (bf16_t)((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu));
+    }
+    // scores of keys kt + 8g + j, j = 0..7, for query my_q
+    float sv[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int key = kt + 8 * g + j;
+      const float raw = (j < 4) ? s0[j] : s1[j - 4];
+      const bool ok = q_ok && key < k_end && key <= my_last;
+      sv[j] = ok ? raw * scale : -INFINITY;
+      mx = fmaxf(mx, sv[j]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
+    float ps = 0.f;
+    uint32_t pw[4];
+#pragma unroll
+    for (int j = 0; j < 8; j += 2) {
+      const float p0 = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
+      const float p1 = (sv[j + 1] == -INFINITY) ? 0.f : expf(sv[j + 1] - m_new);
+      ps += p0 + p1;
+      pw[j >> 1] = (uint32_t)f2bf(p0) | ((uint32_t)f2bf(p1) << 16);
+    }
+    const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, (uint4){pw[0], pw[1], pw[2], pw[3]});
+    ps += __shfl_xor(ps, 16, 64);
+    ps += __shfl_xor(ps, 32, 64);
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+#pragma unroll
+    for (int t = 0; t < NDT; ++t) {
+      oacc[t] *= alpha;
+      const bf16x8_t va = __builtin_bit_cast(bf16x8_t, *(const uint4 *)&vt[wave][16 * t + rr][8 * g]);
+      oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, oacc[t], 0, 0, 0);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  }
+  // merge the four waves: lane (rr, g) holds O^T[16 t + 4 g + i][query rr]
+  if (g == 0) {
+    red_m[wave][rr] = m_run;
+    red_l[wave][rr] = l_run;
+  }
+#pragma unroll
+  for (int t = 0; t < NDT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red_o[wave][16 * t + 4 * g + i][rr] = oacc[t][i];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 16 * DH; idx += 256) {
+    const int qq = idx / DH, j = idx - qq * DH;
+    if (qq >= nq) continue;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, red_m[w][qq]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = (red_m[w][qq] == -INFINITY) ? 0.f : expf(red_m[w][qq] - M);
+      L += red_l[w][qq] * f;
+      O += red_o[w][j][qq] * f;
+    }
+    if (splits == 1) {
+      o[(size_t)(b * P + q0 + qq) * d + h * DH + j] = f2bf(L > 0.f ? O / L : 0.f);
+    } else {
+      float *pp = part + (((size_t)bh * gridDim.y * 16 + q0 + qq) * splits + split) * (DH + 2);
+      pp[2 + j] = O;
+      if (j == 0) {
+        pp[0] = M;
+        pp[1] = L;
+      }
+    }
+  }
+}
+
+// merge of the split partials: one thread per output element
+template <int DH>
+__global__ void k_attn_combine(const float *__restrict__ part, bf16_t *__restrict__ o, int total, int P, int H,
+                               int qtiles, int splits) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;   // over B * H * P * DH
+  if (idx >= total) return;
+  const int j = idx % DH;
+  const int rest = idx / DH;
+  const int p = rest % P, bh = rest / P;
+  const int h = bh % H, b = bh / H;
+  const float *pp = part + ((size_t)bh * qtiles * 16 + p) * splits * (DH + 2);
+  float M = -INFINITY;
+  for (int s = 0; s < splits; ++s) M = fmaxf(M, pp[s * (DH + 2)]);
+  float L = 0.f, O = 0.f;
+  for (int s = 0; s < splits; ++s) {
+    const float m = pp[s * (DH + 2)];
+    const float f = (m == -INFINITY) ? 0.f : expf(m - M);
+    L += pp[s * (DH + 2) + 1] * f;
+    O += pp[s * (DH + 2) + 2 + j] * f;
+  }
+  o[(size_t)(b * P + p) * (H * DH) + h * DH + j] = f2bf(L > 0.f ? O / L : 0.f);
+}
+
 // ---------------------------------------------------------------------------
 // decoder: mixture parameters and type log-probabilities for selected rows,
 // followed by the verify / draft / AR epilogue. One wave per row.
@@ -519,8 +695,11 @@ __global__ __launch_bounds__(256) void k_head(const ACT *__restrict__ e, int d, 
     const float tn = a.ev_t[(size_t)b * a.ev_stride + n - 1] + tau;
     a.ev_t[(size_t)b * a.ev_stride + n] = tn;
     a.ev_k[(size_t)b * a.ev_stride + n] = kk;
-    if (a.ar_t_out) a.ar_t_out[(size_t)b * a.ar_out_stride + a.ar_step] = tn;
-    if (a.ar_k_out) a.ar_k_out[(size_t)b * a.ar_out_stride + a.ar_step] = kk;
+    const int col = g - a.gen0[b];
+    if (col >= 0 && col < a.ar_out_stride) {
+      if (a.ar_t_out) a.ar_t_out[(size_t)b * a.ar_out_stride + col] = tn;
+      if (a.ar_k_out) a.ar_k_out[(size_t)b * a.ar_out_stride + col] = kk;
+    }
     a.n[b] = n + 1;
     a.gen[b] = g + 1;
     a.lenT[b] = n;
@@ -720,6 +899,11 @@ __global__ void k_prefill_init(const float *ht, const int32_t *hk, int B, int n0
   }
 }
 
+__global__ void k_snapshot(const int32_t *src, int32_t *dst, int B) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < B) dst[i] = src[i];
+}
+
 __global__ void k_copy_events(const float *ev_t, const int32_t *ev_k, const int32_t *n, int B, int ev_stride,
                               float *t, int32_t *k, int32_t *nout) {
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -752,12 +936,26 @@ void launch_layernorm(const float *x, void *y, int bf16, const float *g, const f
     k_layernorm<float><<<blocks, 256, 0, s>>>(x, (float *)y, g, b, T, d);
 }
 
+template <typename ELT>
+static void gemm_dispatch(const void *X, const void *W, int T, int N, int K, const Epi &epi, hipStream_t s) {
+  // 64x64 tiles when they already give the chip a few hundred workgroups,
+  // 32x32 tiles otherwise (small row counts of draft and AR steps)
+  const long big = (long)((N + 63) / 64) * ((T + 63) / 64);
+  const ELT *x = (const ELT *)X, *w = (const ELT *)W;
+  if (big >= 512) {
+    dim3 grid((N + 63) / 64, (T + 63) / 64);
+    k_gemm_mfma<ELT, 2, 2><<<grid, 256, 0, s>>>(x, w, T, N, K, epi);
+  } else {
+    dim3 grid((N + 31) / 32, (T + 31) / 32);
+    k_gemm_mfma<ELT, 1, 1><<<grid, 256, 0, s>>>(x, w, T, N, K, epi);
+  }
+}
+
 void launch_gemm(const void *X, const void *W, int bf16, int T, int N, int K, const Epi &epi, hipStream_t s) {
-  dim3 grid((N + 63) / 64, (T + 63) / 64);
   if (bf16)
-    k_gemm_bf16<<<grid, 256, 0, s>>>((const bf16_t *)X, (const bf16_t *)W, T, N, K, epi);
+    gemm_dispatch<bf16_t>(X, W, T, N, K, epi, s);
   else
-    k_gemm_f32<<<grid, 256, 0, s>>>((const float *)X, (const float *)W, T, N, K, epi);
+    gemm_dispatch<float>(X, W, T, N, K, epi, s);
 }
 
 template <typename ACT>
@@ -771,16 +969,46 @@ static void attn_dispatch(const void *q, const void *kc, const void *vc, void *o
     case 16: k_attn_generic<ACT, 16><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
     case 32: k_attn_generic<ACT, 32><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
     case 64: k_attn_generic<ACT, 64><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
-    default: k_attn_generic<ACT, 128><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
+    default: k_attn_generic<ACT, 64><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
   }
 }
 
 void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16, const int32_t *start,
-                      int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, hipStream_t s) {
-  if (bf16)
-    attn_dispatch<bf16_t>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, s);
-  else
+                      int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, float *part,
+                      hipStream_t s) {
+  static const bool force_generic = [] {
+    const char *e = getenv("TPPSD_ATTN_GENERIC");
+    return e && e[0] == '1';
+  }();
+  if (!bf16) {
     attn_dispatch<float>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, s);
+    return;
+  }
+  if (force_generic) {
+    attn_dispatch<bf16_t>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, s);
+    return;
+  }
+  const int qtiles = (P + 15) / 16;
+  const int splits = attn_splits(B, H, qtiles, cap);
+  dim3 grid(B * H, qtiles, splits);
+  const bf16_t *Q = (const bf16_t *)q, *Kc = (const bf16_t *)kc, *Vc = (const bf16_t *)vc;
+  bf16_t *O = (bf16_t *)o;
+  const int total = B * H * P * dh;
+  const int cb = (total + 255) / 256;
+  switch (dh) {
+    case 16:
+      k_attn_mfma<16><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap, splits, part);
+      if (splits > 1) k_attn_combine<16><<<cb, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
+      break;
+    case 32:
+      k_attn_mfma<32><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap, splits, part);
+      if (splits > 1) k_attn_combine<32><<<cb, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
+      break;
+    default:
+      k_attn_mfma<64><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap, splits, part);
+      if (splits > 1) k_attn_combine<64><<<cb, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
+      break;
+  }
 }
 
 void launch_head(const void *e, int bf16, int d, int M, int K, const void *wmix, const float *bmix,
@@ -804,6 +1032,10 @@ void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int 
   const int total = B * n0 > B ? B * n0 : B;
   k_prefill_init<<<(total + 255) / 256, 256, 0, s>>>(ht, hk, B, n0, n_gen, ev_t, ev_k, ev_stride, n, gen, lenT,
                                                      lenD, done, rnd, zeros, n_done, status, acc_stats);
+}
+
+void launch_snapshot(const int32_t *src, int32_t *dst, int B, hipStream_t s) {
+  k_snapshot<<<(B + 255) / 256, 256, 0, s>>>(src, dst, B);
 }
 
 void launch_copy_events(const float *ev_t, const int32_t *ev_k, const int32_t *n, int B, int ev_stride, float *t,
