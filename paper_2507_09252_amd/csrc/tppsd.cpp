@@ -197,6 +197,7 @@ struct tppsd_state {
   // replayed on the caller's; keyed by what their kernel arguments embed
   hipStream_t cap_stream = nullptr;
   bool use_graphs = true;
+  bool fused_draft = true;   // one-launch drafting when the draft model fits it
   hipGraphExec_t sd_exec[2] = {nullptr, nullptr};
   long long sd_key = -1;
   hipGraphExec_t ar_exec[2] = {nullptr, nullptr};   // 1 step, AR_CHUNK steps
@@ -320,9 +321,9 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     e.status = s->status;
     launch_gemm(s->a, w.qkv_w, bf, T, 3 * d, d, e, st);
     const bool timed = time_attn && s->cur_ev != nullptr;
-    if (timed) (void)hipEventRecord(s->cur_ev[2 * l], st);
-    launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->cap, s->attn_part, st);
-    if (timed) (void)hipEventRecord(s->cur_ev[2 * l + 1], st);
+    launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->cap, s->attn_part,
+                     time_attn ? 1 : 0, timed ? s->cur_ev[2 * l] : nullptr, timed ? s->cur_ev[2 * l + 1] : nullptr,
+                     st);
     Epi eo{};
     eo.mode = EPI_RESID;
     eo.bias = w.out_b;
@@ -391,8 +392,60 @@ int check_accept_buf(const tppsd_accept_buf *b) {
   return TPPSD_OK;
 }
 
+int do_draft_fused(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
+  const tppsd_model *D = s->D;
+  DraftArgs a{};
+  a.B = s->B;
+  a.gamma = gamma;
+  a.d = D->d();
+  a.H = D->H();
+  a.F = D->cfg.d_ffn;
+  a.M = D->cfg.n_mix;
+  a.K = D->cfg.n_types;
+  a.L = D->cfg.n_layers;
+  for (int l = 0; l < a.L; ++l) {
+    const LayerW &w = D->layers[l];
+    a.layer[l] = {w.qkv_w, w.out_w, w.ffn1_w, w.ffn2_w, w.ln1_g, w.ln1_b, w.qkv_b,
+                  w.out_b, w.ln2_g, w.ln2_b, w.ffn1_b, w.ffn2_b};
+  }
+  a.type_emb = D->type_emb;
+  a.Ek1_w = D->Ek1_w;
+  a.mix_w = D->mix_w;
+  a.k2_w = D->k2_w;
+  a.lnf_g = D->lnf_g;
+  a.lnf_b = D->lnf_b;
+  a.k1_b = D->k1_b;
+  a.mix_b = D->mix_b;
+  a.k2_b = D->k2_b;
+  a.freq = s->cD.freq;
+  a.kc = s->cD.k;
+  a.vc = s->cD.v;
+  a.layer_bytes = s->cD.layer_bytes;
+  a.cap = s->cap;
+  a.ev_t = s->ev_t;
+  a.ev_k = s->ev_k;
+  a.ev_stride = s->cap;
+  a.n = s->n;
+  a.lenD = s->lenD;
+  a.done = s->done;
+  a.rnd = s->rnd;
+  a.seed = s->seed;
+  a.status = s->status;
+  a.d_tau = out->tau;
+  a.d_t = out->t;
+  a.d_logg = out->logg;
+  a.d_logf = out->logf;
+  a.d_mix = out->mix;
+  a.d_logtype = out->logtype;
+  a.d_k = out->k;
+  a.MG = s->max_gamma;
+  launch_draft_fused(a, D->bf16(), st);
+  return hip_check("tppsd_draft");
+}
+
 int do_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
   const tppsd_model *D = s->D;
+  if (s->fused_draft) return do_draft_fused(s, gamma, out, st);
   for (int l = 1; l <= gamma; ++l) {
     TokSrc src{};
     src.ev_t = s->ev_t;
@@ -679,6 +732,13 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
     }
     const char *ng = getenv("TPPSD_NO_GRAPHS");
     s->use_graphs = !(ng && ng[0] == '1');
+    const char *nf = getenv("TPPSD_LAYERED_DRAFT");
+    // one workgroup per sequence: worth it until the batch alone fills the chip
+    // and the layered kernels amortise weights and latency over many rows
+    // (and while contexts stay short: its attention streams each (sequence,
+    // head)'s keys with one wave)
+    s->fused_draft = D && B <= 1024 && max_events <= 2048 &&
+                     fused_draft_ok(D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn) && !(nf && nf[0] == '1');
   }
   if (hipHostMalloc((void **)&s->host_ndone, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&s->poll_ev[0], hipEventDisableTiming) != hipSuccess ||

@@ -98,20 +98,52 @@ struct AcceptArgs {
   unsigned long long *acc_stats;   // [3]: accepted drafts, drafted, A-R candidates
 };
 
+// Fused drafting: one workgroup per sequence runs all gamma draft steps.
+#define FD_MAX_LAYERS 4
+struct FusedLayerW {
+  const void *qkv_w, *out_w, *ffn1_w, *ffn2_w;
+  const float *ln1_g, *ln1_b, *qkv_b, *out_b, *ln2_g, *ln2_b, *ffn1_b, *ffn2_b;
+};
+struct DraftArgs {
+  int B, gamma, d, H, F, M, K, L;
+  FusedLayerW layer[FD_MAX_LAYERS];
+  const void *type_emb, *Ek1_w, *mix_w, *k2_w;
+  const float *lnf_g, *lnf_b, *k1_b, *mix_b, *k2_b;
+  const float *freq;
+  char *kc, *vc;            // draft cache bases; layer stride layer_bytes
+  size_t layer_bytes;
+  int cap;
+  const float *ev_t;
+  const int32_t *ev_k;
+  int ev_stride;
+  const int32_t *n, *lenD, *done, *rnd;
+  uint64_t seed;
+  uint32_t *status;
+  float *d_tau, *d_t, *d_logg, *d_logf, *d_mix, *d_logtype;
+  int32_t *d_k;
+  int MG;                   // row stride of the draft record (max_gamma)
+};
+// whether the fused draft kernel supports a model of these sizes
+inline bool fused_draft_ok(int L, int d, int H, int F) {
+  return L <= FD_MAX_LAYERS && d <= 256 && F <= 2048 && d / H <= 64;
+}
+size_t fused_draft_lds_bytes(int d, int F, int M, int K);
+
 // ---- launchers (tppsd_kernels.hip) ----
+void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t st);
 void launch_embed(float *x, int T, int d, int P, const TokSrc &src, const void *wtype, int bf16,
                   const float *freq, int K, hipStream_t st);
 void launch_layernorm(const float *x, void *y, int bf16, const float *g, const float *b, int T, int d,
                       hipStream_t st);
 void launch_gemm(const void *X, const void *W, int bf16, int T, int N, int K, const Epi &epi,
                  hipStream_t st);
-// Key splits of the bf16 attention for B sequences x H heads x qtiles query
-// tiles over at most max_keys keys: enough workgroups to fill the chip, each
-// split keeping at least 128 keys.
+// Key splits of the attention for B sequences x H heads x qtiles query tiles
+// over at most max_keys keys: enough workgroups to fill the chip, each split
+// keeping at least 512 keys (shorter splits do not pay for the merge launch).
 inline int attn_splits(int B, int H, int qtiles, int max_keys) {
   const long items = (long)B * H * qtiles;
   int s = 1;
-  while (s < 8 && items * s < 1024 && max_keys / (2 * s) >= 128) s *= 2;
+  while (s < 8 && items * s < 1024 && max_keys / (2 * s) >= 512) s *= 2;
   return s;
 }
 // floats of split partials needed for up to qtiles_max query tiles
@@ -128,7 +160,8 @@ inline size_t attn_part_floats(int B, int H, int dh, int qtiles_max, int max_key
 }
 void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16,
                       const int32_t *start, int start_off, const int32_t *done, int B, int P, int H,
-                      int dh, int cap, float *part, hipStream_t st);
+                      int dh, int cap, float *part, int verify, hipEvent_t ev0, hipEvent_t ev1,
+                      hipStream_t st);
 void launch_head(const void *e, int bf16, int d, int M, int K, const void *wmix, const float *bmix,
                  const void *wk2, const float *bk2, const HeadArgs &a, hipStream_t st);
 void launch_accept(const AcceptArgs &a, hipStream_t st);

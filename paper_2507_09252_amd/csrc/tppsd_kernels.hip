@@ -9,6 +9,7 @@
 // Linear inputs in bf16 (LN outputs, q/k/v, attention output, ReLU output, the
 // decoder's e and tanh activations), accumulate in fp32 and keep the residual
 // stream, LayerNorm statistics, softmax and all decoder math in fp32.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdlib.h>
@@ -307,7 +308,9 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const ELT *__restrict__ X, co
 // 0 .. start[b] + start_off + p. Online softmax over 64-key tiles.
 // ---------------------------------------------------------------------------
 
-template <typename ACT, int DH>
+// ROLE tags the instantiation only (1 = verify pass of the target, 0 = other
+// passes), so that profiles report the verify launches under their own name.
+template <typename ACT, int DH, int ROLE>
 __global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q, const ACT *__restrict__ kc,
                                                       const ACT *__restrict__ vc, ACT *__restrict__ o,
                                                       const int32_t *__restrict__ start, int start_off,
@@ -418,7 +421,7 @@ __global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q,
 // O^T = V^T P^T. The A operand (V transposed) goes through LDS.
 typedef short short4_t __attribute__((ext_vector_type(4)));
 
-template <int DH>
+template <int DH, int ROLE>
 __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q, const bf16_t *__restrict__ kc,
                                                    const bf16_t *__restrict__ vc, bf16_t *__restrict__ o,
                                                    const int32_t *__restrict__ start, int start_off,
@@ -569,9 +572,133 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
   }
 }
 
+// fp32 causal attention on MFMA (v_mfma_f32_16x16x4f32), same work split and
+// permuted S^T rows as the bf16 kernel. One MFMA contracts four k values, one
+// per lane group g: S^T takes d in float4 slices (element e of lane group g is
+// d = 4 g + e), and O^T = V^T P^T runs one MFMA per j = 0..7 over the keys
+// 8 g + j, which are exactly the eight scores each lane holds. V is read
+// straight from memory (16 consecutive d of one key per lane group).
+template <int DH, int ROLE>
+__global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__ q, const float *__restrict__ kc,
+                                                       const float *__restrict__ vc, float *__restrict__ o,
+                                                       const int32_t *__restrict__ start, int start_off,
+                                                       const int32_t *__restrict__ done, int P, int H, int cap,
+                                                       int splits, float *__restrict__ part) {
+  constexpr int KT = 32, NDT = DH / 16;
+  __shared__ float red_m[4][16], red_l[4][16];
+  __shared__ float red_o[4][DH][17];
+  const int bh = blockIdx.x, b = bh / H, h = bh - b * H;
+  const int qt = blockIdx.y, q0 = qt * 16, split = blockIdx.z;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, rr = lane & 15, g = lane >> 4;
+  const int d = H * DH;
+  const int nq = min(16, P - q0);
+  const bool skip = done != nullptr && done[b] != 0;
+  const int base = start[b] + start_off;
+  const int n_keys = skip ? 0 : base + q0 + nq;
+  int chunk = (n_keys + splits - 1) / splits;
+  chunk = (chunk + KT - 1) / KT * KT;
+  const int k_begin = split * chunk, k_end = min(n_keys, k_begin + chunk);
+  const size_t kvbase = ((size_t)b * H + h) * cap;
+  const float scale = 1.f / sqrtf((float)DH);
+  const int my_q = q0 + rr, my_last = base + my_q;
+  const bool q_ok = rr < nq;
+  f32x4_t qf[DH / 16];
+#pragma unroll
+  for (int c = 0; c < DH / 16; ++c)
+    qf[c] = q_ok ? *(const f32x4_t *)(q + (size_t)(b * P + my_q) * d + h * DH + 16 * c + 4 * g)
+                 : (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4_t oacc[NDT];
+#pragma unroll
+  for (int t = 0; t < NDT; ++t) oacc[t] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  const int krow0 = 8 * (rr >> 2) + (rr & 3), krow1 = krow0 + 4;
+  for (int kt = k_begin + wave * KT; kt < k_end; kt += 4 * KT) {
+    const size_t r0 = kvbase + min(kt + krow0, cap - 1), r1 = kvbase + min(kt + krow1, cap - 1);
+    f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < DH / 16; ++c) {
+      const f32x4_t a0 = *(const f32x4_t *)(kc + r0 * DH + 16 * c + 4 * g);
+      const f32x4_t a1 = *(const f32x4_t *)(kc + r1 * DH + 16 * c + 4 * g);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[e], qf[c][e], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[e], qf[c][e], s1, 0, 0, 0);
+      }
+    }
+    float sv[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int key = kt + 8 * g + j;
+      const float raw = (j < 4) ? s0[j] : s1[j - 4];
+      const bool ok = q_ok && key < k_end && key <= my_last;
+      sv[j] = ok ? raw * scale : -INFINITY;
+      mx = fmaxf(mx, sv[j]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
+    float pv[8], ps = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      pv[j] = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
+      ps += pv[j];
+    }
+    ps += __shfl_xor(ps, 16, 64);
+    ps += __shfl_xor(ps, 32, 64);
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+#pragma unroll
+    for (int t = 0; t < NDT; ++t) {
+      oacc[t] *= alpha;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        // key kt + 8 g + j, value column 16 t + rr (zero past the key range)
+        const int key = kt + 8 * g + j;
+        const float v = (key < k_end) ? vc[(kvbase + key) * DH + 16 * t + rr] : 0.f;
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(v, pv[j], oacc[t], 0, 0, 0);
+      }
+    }
+  }
+  if (g == 0) {
+    red_m[wave][rr] = m_run;
+    red_l[wave][rr] = l_run;
+  }
+#pragma unroll
+  for (int t = 0; t < NDT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red_o[wave][16 * t + 4 * g + i][rr] = oacc[t][i];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 16 * DH; idx += 256) {
+    const int qq = idx / DH, j = idx - qq * DH;
+    if (qq >= nq) continue;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) M = fmaxf(M, red_m[w][qq]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float f = (red_m[w][qq] == -INFINITY) ? 0.f : expf(red_m[w][qq] - M);
+      L += red_l[w][qq] * f;
+      O += red_o[w][j][qq] * f;
+    }
+    if (splits == 1) {
+      o[(size_t)(b * P + q0 + qq) * d + h * DH + j] = L > 0.f ? O / L : 0.f;
+    } else {
+      float *pp = part + (((size_t)bh * gridDim.y * 16 + q0 + qq) * splits + split) * (DH + 2);
+      pp[2 + j] = O;
+      if (j == 0) {
+        pp[0] = M;
+        pp[1] = L;
+      }
+    }
+  }
+}
+
 // merge of the split partials: one thread per output element
-template <int DH>
-__global__ void k_attn_combine(const float *__restrict__ part, bf16_t *__restrict__ o, int total, int P, int H,
+template <typename ACT, int DH>
+__global__ void k_attn_combine(const float *__restrict__ part, ACT *__restrict__ o, int total, int P, int H,
                                int qtiles, int splits) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;   // over B * H * P * DH
   if (idx >= total) return;
@@ -589,7 +716,7 @@ __global__ void k_attn_combine(const float *__restrict__ part, bf16_t *__restric
     L += pp[s * (DH + 2) + 1] * f;
     O += pp[s * (DH + 2) + 2 + j] * f;
   }
-  o[(size_t)(b * P + p) * (H * DH) + h * DH + j] = f2bf(L > 0.f ? O / L : 0.f);
+  st(o, (size_t)(b * P + p) * (H * DH) + h * DH + j, L > 0.f ? O / L : 0.f);
 }
 
 // ---------------------------------------------------------------------------
@@ -709,6 +836,305 @@ __global__ __launch_bounds__(256) void k_head(const ACT *__restrict__ e, int d, 
       atomicAdd(a.n_done, 1);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// fused drafting (§4.3 "Drafting", Algorithm 1's inner loop): one workgroup
+// per sequence runs all gamma sequential draft steps -- embedding, every
+// layer, decoder and the draw -- in one launch. The draft model is small, so
+// each step is a handful of matrix-vector products on at most two tokens
+// (step 1 re-encodes the last two committed events). Activations live in
+// LDS; keys/values go to the draft KV cache exactly as in the layered path,
+// with the same bf16 rounding points.
+// ---------------------------------------------------------------------------
+
+template <typename ELT> __device__ __forceinline__ float rnd_act(float v);
+template <> __device__ __forceinline__ float rnd_act<float>(float v) { return v; }
+template <> __device__ __forceinline__ float rnd_act<bf16_t>(float v) { return bf2f(f2bf(v)); }
+
+template <typename ELT> __device__ __forceinline__ void load8(const ELT *p, float w[8]);
+template <> __device__ __forceinline__ void load8<float>(const float *p, float w[8]) {
+  const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
+  w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w; w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+}
+template <> __device__ __forceinline__ void load8<bf16_t>(const bf16_t *p, float w[8]) {
+  const uint4 u = *(const uint4 *)p;
+  const uint32_t v[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    w[2 * i] = __uint_as_float(v[i] << 16);
+    w[2 * i + 1] = __uint_as_float(v[i] & 0xFFFF0000u);
+  }
+}
+
+// y[p][n] = sum_k in[p * in_stride + k] W[n * K + k] for n < N, p < P (P <= 2),
+// handed to epi(p, n, y) by one lane. Lanes split each row into 8-element
+// chunks (lpo lanes per output, a power of two) and reduce with shuffles.
+template <typename ELT, typename EPI>
+__device__ void wg_gemv(const ELT *__restrict__ W, int N, int K, const float *in, int in_stride, int P, EPI epi) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int chunks = K >> 3;
+  int lpo = 1;
+  while (lpo < chunks && lpo < 64) lpo <<= 1;
+  const int opw = 64 / lpo, sub = lane & (lpo - 1), slot = lane / lpo;
+  for (int n0 = 0; n0 < N; n0 += 4 * opw) {
+    const int n = n0 + wave * opw + slot;
+    float acc0 = 0.f, acc1 = 0.f;
+    if (n < N) {
+      for (int c = sub; c < chunks; c += lpo) {
+        float w[8];
+        load8(W + (size_t)n * K + 8 * c, w);
+        const float *x0 = in + 8 * c;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc0 += w[e] * x0[e];
+        if (P > 1) {
+          const float *x1 = in + in_stride + 8 * c;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc1 += w[e] * x1[e];
+        }
+      }
+    }
+    for (int off = lpo >> 1; off > 0; off >>= 1) {
+      acc0 += __shfl_xor(acc0, off, 64);
+      acc1 += __shfl_xor(acc1, off, 64);
+    }
+    if (n < N && sub == 0) {
+      epi(0, n, acc0);
+      if (P > 1) epi(1, n, acc1);
+    }
+  }
+}
+
+// LayerNorm of P <= 4 rows of x (stride d) into y (stride d), wave p per row
+template <typename ELT>
+__device__ void wg_layernorm(const float *x, float *y, const float *g, const float *bt, int P, int d) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (wave >= P) return;
+  const float *xr = x + wave * d;
+  float s = 0.f;
+  for (int j = lane; j < d; j += 64) s += xr[j];
+  const float mean = wave_sum(s) / (float)d;
+  float v = 0.f;
+  for (int j = lane; j < d; j += 64) {
+    const float c = xr[j] - mean;
+    v += c * c;
+  }
+  const float rstd = 1.f / sqrtf(wave_sum(v) / (float)d + 1e-5f);
+  for (int j = lane; j < d; j += 64) y[wave * d + j] = rnd_act<ELT>((xr[j] - mean) * rstd * g[j] + bt[j]);
+}
+
+// causal attention of P <= 2 new queries over the cache: one wave per
+// (query, head) pair, lanes over keys with their own online softmax, merged
+// across the wave. Query p sees cached positions 0 .. pos0 + p.
+template <typename ELT, int DH>
+__device__ void wg_attention(const float *qs, float *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
+                             int H, int P, int pos0, int d) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const float scale = 1.f / sqrtf((float)DH);
+  for (int pair = wave; pair < P * H; pair += 4) {
+    const int p = pair / H, h = pair - p * H;
+    const int last = pos0 + p;
+    float q[DH];
+#pragma unroll
+    for (int j = 0; j < DH; ++j) q[j] = qs[p * d + h * DH + j] * scale;
+    float m = -INFINITY, l = 0.f, o[DH];
+#pragma unroll
+    for (int j = 0; j < DH; ++j) o[j] = 0.f;
+    const size_t row0 = seq_row0 + (size_t)h * cap;
+    // U keys per lane per pass: their loads are issued together
+    constexpr int U = DH <= 32 ? 4 : 2;
+    for (int k0 = lane * U; k0 <= last; k0 += 64 * U) {
+      float sc[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int key = min(k0 + u, last);
+        const ELT *kr = kc + (row0 + key) * DH;
+        float a = 0.f;
+#pragma unroll
+        for (int c = 0; c < DH / 8; ++c) {
+          float w[8];
+          load8(kr + 8 * c, w);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) a += q[8 * c + e] * w[e];
+        }
+        sc[u] = (k0 + u <= last) ? a : -INFINITY;
+      }
+      float mn = m;
+#pragma unroll
+      for (int u = 0; u < U; ++u) mn = fmaxf(mn, sc[u]);
+      const float corr = expf(m - mn);
+      l *= corr;
+#pragma unroll
+      for (int j = 0; j < DH; ++j) o[j] *= corr;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (k0 + u > last) break;
+        const float pv = expf(sc[u] - mn);
+        l += pv;
+        const ELT *vr = vc + (row0 + k0 + u) * DH;
+#pragma unroll
+        for (int c = 0; c < DH / 8; ++c) {
+          float w[8];
+          load8(vr + 8 * c, w);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[8 * c + e] += pv * w[e];
+        }
+      }
+      m = mn;
+    }
+    const float M = wave_max(m);
+    const float f = (m == -INFINITY) ? 0.f : expf(m - M);
+    const float L = wave_sum(l * f);
+    float mine = 0.f;
+#pragma unroll
+    for (int j = 0; j < DH; ++j) {
+      const float t = wave_sum(o[j] * f);
+      if (lane == j) mine = t;
+    }
+    if (lane < DH) os[p * d + h * DH + lane] = rnd_act<ELT>(mine / L);
+  }
+}
+
+size_t fused_draft_lds_bytes(int d, int F, int M, int K) {
+  const int Fm = d > F ? d : F;
+  return (size_t)(2 * d + 2 * Fm + 2 * d + 2 * d + 2 * F + 4 * d + 3 * M + K + 8) * sizeof(float);
+}
+
+template <typename ELT, int DH>
+__global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float sm[];
+  __shared__ float tok_t[2], t_last;
+  __shared__ int tok_k[2];
+  const int d = a.d, F = a.F, M = a.M, K = a.K, H = a.H;
+  const int Fm = d > F ? d : F;
+  float *xs = sm;           // [2][d] residual stream
+  float *as = xs + 2 * d;   // [2][Fm] LayerNorm outputs
+  float *qs = as + 2 * Fm;  // [2][d] queries
+  float *os = qs + 2 * d;   // [2][d] attention outputs
+  float *hs = os + 2 * d;   // [2][F] FFN hidden
+  float *es = hs + 2 * F;   // [4d] decoder e | tanh activations
+  float *hv = es + 4 * d;   // [3M + K] decoder outputs
+  const int b = blockIdx.x, tid = threadIdx.x;
+  if (a.done[b]) return;
+  const int n = a.n[b], base = a.lenD[b];
+  const uint64_t r = (uint64_t)a.rnd[b];
+  const size_t seq_row0 = (size_t)b * H * a.cap;
+  const ELT *wtype = (const ELT *)a.type_emb;
+  if (tid == 0) t_last = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+  for (int l = 1; l <= a.gamma; ++l) {
+    const int P = (l == 1) ? 2 : 1;
+    const int pos0 = (l == 1) ? base : base + l;
+    if (l == 1 && tid < 2) {
+      const size_t i = (size_t)b * a.ev_stride + n - 2 + tid;
+      tok_t[tid] = a.ev_t[i];
+      tok_k[tid] = a.ev_k[i];
+    }
+    __syncthreads();
+    for (int i = tid; i < P * d; i += 256) {
+      const int p = i / d, j = i - p * d;
+      const float arg = tok_t[p] * a.freq[j];
+      const int kk = min(max(tok_k[p], 0), K - 1);
+      xs[i] = ((j & 1) ? cosf(arg) : sinf(arg)) + ld(wtype, (size_t)kk * d + j);
+    }
+    __syncthreads();
+    for (int ly = 0; ly < a.L; ++ly) {
+      const FusedLayerW &w = a.layer[ly];
+      ELT *kc = (ELT *)(a.kc + a.layer_bytes * ly);
+      ELT *vc = (ELT *)(a.vc + a.layer_bytes * ly);
+      wg_layernorm<ELT>(xs, as, w.ln1_g, w.ln1_b, P, d);
+      __syncthreads();
+      wg_gemv<ELT>((const ELT *)w.qkv_w, 3 * d, d, as, d, P, [&](int p, int nn, float acc) {
+        const float v = rnd_act<ELT>(acc + w.qkv_b[nn]);
+        const int which = nn / d, c = nn - which * d;
+        if (which == 0) {
+          qs[p * d + c] = v;
+        } else {
+          const int h = c / DH, j = c - h * DH, pos = pos0 + p;
+          if (pos < a.cap)
+            st(which == 1 ? kc : vc, (seq_row0 + (size_t)h * a.cap + pos) * DH + j, v);
+          else
+            atomicOr(a.status, TPPSD_STATUS_CAPACITY);
+        }
+      });
+      __syncthreads();
+      wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d);
+      __syncthreads();
+      wg_gemv<ELT>((const ELT *)w.out_w, d, d, os, d, P,
+                   [&](int p, int nn, float acc) { xs[p * d + nn] += acc + w.out_b[nn]; });
+      __syncthreads();
+      wg_layernorm<ELT>(xs, as, w.ln2_g, w.ln2_b, P, d);
+      __syncthreads();
+      wg_gemv<ELT>((const ELT *)w.ffn1_w, F, d, as, d, P, [&](int p, int nn, float acc) {
+        hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + w.ffn1_b[nn], 0.f));
+      });
+      __syncthreads();
+      wg_gemv<ELT>((const ELT *)w.ffn2_w, d, F, hs, F, P,
+                   [&](int p, int nn, float acc) { xs[p * d + nn] += acc + w.ffn2_b[nn]; });
+      __syncthreads();
+    }
+    // decoder on the last token
+    wg_layernorm<ELT>(xs + (P - 1) * d, as, a.lnf_g, a.lnf_b, 1, d);
+    __syncthreads();
+    wg_gemv<ELT>((const ELT *)a.Ek1_w, 4 * d, d, as, d, 1, [&](int, int nn, float acc) {
+      es[nn] = (nn < 3 * d) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + a.k1_b[nn - 3 * d]));
+    });
+    __syncthreads();
+    const ELT *mw = (const ELT *)a.mix_w;
+    for (int grp = 0; grp < 3; ++grp)
+      wg_gemv<ELT>(mw + (size_t)grp * M * d, M, d, es + grp * d, 0, 1,
+                   [&](int, int nn, float acc) { hv[grp * M + nn] = acc + a.mix_b[grp * M + nn]; });
+    wg_gemv<ELT>((const ELT *)a.k2_w, K, d, es + 3 * d, 0, 1,
+                 [&](int, int nn, float acc) { hv[3 * M + nn] = acc + a.k2_b[nn]; });
+    __syncthreads();
+    if (tid < 64) {
+      const int lane = tid;
+      const float lw = lane < M ? hv[lane] : -INFINITY;
+      const float mw2 = wave_max(lw);
+      const float sw = wave_sum(lane < M ? expf(lw - mw2) : 0.f);
+      const float lk = lane < K ? hv[3 * M + lane] : -INFINITY;
+      const float mk = wave_max(lk);
+      const float sk = wave_sum(lane < K ? expf(lk - mk) : 0.f);
+      if (lane < M) hv[lane] = lw - mw2 - logf(sw);
+      if (lane < K) hv[3 * M + lane] = lk - mk - logf(sk);
+    }
+    __syncthreads();
+    const size_t di = (size_t)b * a.MG + (l - 1);
+    for (int i = tid; i < 3 * M; i += 256) a.d_mix[di * 3 * M + i] = hv[i];
+    for (int i = tid; i < K; i += 256) a.d_logtype[di * K + i] = hv[3 * M + i];
+    if (tid == 0) {
+      float u[4];
+      philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)l, TAG_DRAFT, u);
+      const float tau = sample_tau(hv, hv + M, hv + 2 * M, M, u[0], u[1], u[2]);
+      const int kk = sample_cat(hv + 3 * M, K, u[3]);
+      const float tn = t_last + tau;
+      a.d_tau[di] = tau;
+      a.d_t[di] = tn;
+      a.d_k[di] = kk;
+      a.d_logg[di] = mix_logpdf(hv, hv + M, hv + 2 * M, M, tau);
+      a.d_logf[di] = hv[3 * M + kk];
+      if (!isfinite(tau)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+      tok_t[0] = tn;
+      tok_k[0] = kk;
+      t_last = tn;
+    }
+    __syncthreads();
+  }
+}
+
+void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
+  const size_t lds = fused_draft_lds_bytes(a.d, a.F, a.M, a.K);
+  const int dh = a.d / a.H;
+#define TPPSD_FD(ELT, DH) k_draft_fused<ELT, DH><<<a.B, 256, lds, s>>>(a)
+  if (bf16) {
+    if (dh == 16) TPPSD_FD(bf16_t, 16);
+    else if (dh == 32) TPPSD_FD(bf16_t, 32);
+    else TPPSD_FD(bf16_t, 64);
+  } else {
+    if (dh == 16) TPPSD_FD(float, 16);
+    else if (dh == 32) TPPSD_FD(float, 32);
+    else TPPSD_FD(float, 64);
+  }
+#undef TPPSD_FD
 }
 
 // ---------------------------------------------------------------------------
@@ -958,57 +1384,97 @@ void launch_gemm(const void *X, const void *W, int bf16, int T, int N, int K, co
     gemm_dispatch<float>(X, W, T, N, K, epi, s);
 }
 
-template <typename ACT>
+// ev0/ev1 (optional): HIP events stamped with the main kernel's own start and
+// stop (hipExtLaunchKernelGGL), for the verify-attention timing
+template <typename ACT, int ROLE>
 static void attn_dispatch(const void *q, const void *kc, const void *vc, void *o, const int32_t *start,
                           int start_off, const int32_t *done, int B, int P, int H, int dh, int cap,
-                          hipStream_t s) {
+                          hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   dim3 grid(B * H, (P + 15) / 16);
   const ACT *Q = (const ACT *)q, *Kc = (const ACT *)kc, *Vc = (const ACT *)vc;
   ACT *O = (ACT *)o;
+  auto go = [&](auto kern) {
+    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap);
+  };
   switch (dh) {
-    case 16: k_attn_generic<ACT, 16><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
-    case 32: k_attn_generic<ACT, 32><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
-    case 64: k_attn_generic<ACT, 64><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
-    default: k_attn_generic<ACT, 64><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap); break;
+    case 16: go(k_attn_generic<ACT, 16, ROLE>); break;
+    case 32: go(k_attn_generic<ACT, 32, ROLE>); break;
+    default: go(k_attn_generic<ACT, 64, ROLE>); break;
   }
 }
 
-void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16, const int32_t *start,
-                      int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, float *part,
-                      hipStream_t s) {
+template <int DH, int ROLE>
+static void attn_mfma(const bf16_t *Q, const bf16_t *Kc, const bf16_t *Vc, bf16_t *O, const int32_t *start,
+                      int start_off, const int32_t *done, int B, int P, int H, int cap, float *part,
+                      hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  const int qtiles = (P + 15) / 16;
+  const int splits = attn_splits(B, H, qtiles, cap);
+  dim3 grid(B * H, qtiles, splits);
+  hipExtLaunchKernelGGL(k_attn_mfma<DH, ROLE>, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off,
+                        done, P, H, cap, splits, part);
+  if (splits > 1) {
+    const int total = B * H * P * DH;
+    k_attn_combine<bf16_t, DH><<<(total + 255) / 256, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
+  }
+}
+
+template <int DH, int ROLE>
+static void attn_mfma_f32(const float *Q, const float *Kc, const float *Vc, float *O, const int32_t *start,
+                          int start_off, const int32_t *done, int B, int P, int H, int cap, float *part,
+                          hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  const int qtiles = (P + 15) / 16;
+  const int splits = attn_splits(B, H, qtiles, cap);
+  dim3 grid(B * H, qtiles, splits);
+  hipExtLaunchKernelGGL(k_attn_mfma_f32<DH, ROLE>, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start,
+                        start_off, done, P, H, cap, splits, part);
+  if (splits > 1) {
+    const int total = B * H * P * DH;
+    k_attn_combine<float, DH><<<(total + 255) / 256, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
+  }
+}
+
+template <int ROLE>
+static void attention_role(const void *q, const void *kc, const void *vc, void *o, int bf16, const int32_t *start,
+                           int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, float *part,
+                           hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   static const bool force_generic = [] {
     const char *e = getenv("TPPSD_ATTN_GENERIC");
     return e && e[0] == '1';
   }();
   if (!bf16) {
-    attn_dispatch<float>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, s);
+    if (force_generic) {
+      attn_dispatch<float, ROLE>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, ev0, ev1, s);
+      return;
+    }
+    const float *Q = (const float *)q, *Kc = (const float *)kc, *Vc = (const float *)vc;
+    float *O = (float *)o;
+    switch (dh) {
+      case 16: attn_mfma_f32<16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+      case 32: attn_mfma_f32<32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+      default: attn_mfma_f32<64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+    }
     return;
   }
   if (force_generic) {
-    attn_dispatch<bf16_t>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, s);
+    attn_dispatch<bf16_t, ROLE>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, ev0, ev1, s);
     return;
   }
-  const int qtiles = (P + 15) / 16;
-  const int splits = attn_splits(B, H, qtiles, cap);
-  dim3 grid(B * H, qtiles, splits);
   const bf16_t *Q = (const bf16_t *)q, *Kc = (const bf16_t *)kc, *Vc = (const bf16_t *)vc;
   bf16_t *O = (bf16_t *)o;
-  const int total = B * H * P * dh;
-  const int cb = (total + 255) / 256;
   switch (dh) {
-    case 16:
-      k_attn_mfma<16><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap, splits, part);
-      if (splits > 1) k_attn_combine<16><<<cb, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
-      break;
-    case 32:
-      k_attn_mfma<32><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap, splits, part);
-      if (splits > 1) k_attn_combine<32><<<cb, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
-      break;
-    default:
-      k_attn_mfma<64><<<grid, 256, 0, s>>>(Q, Kc, Vc, O, start, start_off, done, P, H, cap, splits, part);
-      if (splits > 1) k_attn_combine<64><<<cb, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
-      break;
+    case 16: attn_mfma<16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+    case 32: attn_mfma<32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+    default: attn_mfma<64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
   }
+}
+
+void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16, const int32_t *start,
+                      int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, float *part,
+                      int verify, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+  if (verify)
+    attention_role<1>(q, kc, vc, o, bf16, start, start_off, done, B, P, H, dh, cap, part, ev0, ev1, s);
+  else
+    attention_role<0>(q, kc, vc, o, bf16, start, start_off, done, B, P, H, dh, cap, part, ev0, ev1, s);
 }
 
 void launch_head(const void *e, int bf16, int d, int M, int K, const void *wmix, const float *bmix,
