@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "accepted events/sec (1 MI355X) SD vs AR; verify MFMA util %; KV-attn HBM GB/s"
 HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 KERNEL_NAME = {"bf16": "k_attn_mfma<d_head, 1> (verify attention)",
                "fp32": "k_attn_mfma_f32<d_head, 1> (verify attention)"}
 
@@ -55,6 +56,27 @@ def attention_bytes_per_launch(wl, gamma, B):
     kv = B * c.n_heads * (ctx + P) * c.d_head * 2 * elt
     qo = B * P * c.d_model * elt * 2
     return kv + qo
+
+
+def verify_pass_fraction(wl, gamma, B, verify_ms):
+    """Roofline time of one verify pass, max(flop / MFMA peak, bytes / HBM
+    peak), against its measured time (phase timing, graph-replayed). flop:
+    the GEMMs of every layer and the decoder plus QK and PV over the run-average
+    context; bytes: the K/V read and append, the weights once, the activations
+    of the pass in and out."""
+    c = wl.target
+    elt = 2 if c.prec == "bf16" else 4
+    L, d, F, M, K = c.n_layers, c.d_model, c.d_ffn, c.n_mix, c.n_types
+    P = gamma + 1
+    T = B * P
+    ctx = wl.n_hist + wl.n_gen / 2.0
+    flop = 2.0 * T * (L * (4 * d * d + 2 * d * F) + 4 * d * d + 3 * M * d + K * d) + 4.0 * T * L * d * ctx
+    w_bytes = elt * (L * (4 * d * d + 2 * d * F) + 4 * d * d + 3 * M * d + K * d)
+    bytes_ = B * L * (ctx + P) * 2 * d * elt + w_bytes + T * 8 * (3 * M + K)
+    t_bound = max(flop / (MFMA_PEAK_TFLOPS[c.prec] * 1e12), bytes_ / (HBM_PEAK_GBS * 1e9))
+    return {"flop": flop, "bytes": bytes_, "t_bound_us": t_bound * 1e6, "t_measured_us": verify_ms * 1e3,
+            "frac": t_bound / (verify_ms * 1e-3) if verify_ms else None,
+            "tflops": flop / (verify_ms * 1e-3) / 1e12 if verify_ms else None}
 
 
 def measured_traffic(wl_name):
@@ -134,13 +156,18 @@ def main():
     t_sd = time.perf_counter() - t0
     st = sd.tppsd_state_status()
     assert st["bits"] == 0 and st["n_done"] == B, st
-    # one more job with the verify-attention launches bracketed by HIP events
-    # (rounds launched directly on this stream, same kernels and data)
-    sd.tppsd_timing_enable(True)
+    # one more job with the verify attention and GEMM launches bracketed by
+    # HIP events (rounds launched directly on this stream, same kernels and
+    # data), and one with events between the draft / verify / accept graphs
+    sd.tppsd_timing_enable(tp.TIME_KERNELS)
     sd_job()
-    attn_ms, attn_launches = sd.tppsd_timing_read()
-    sd.tppsd_timing_enable(False)
+    tk = sd.tppsd_timing_read()
+    sd.tppsd_timing_enable(tp.TIME_PHASES)
+    sd_job()
+    tph = sd.tppsd_timing_read()
+    sd.tppsd_timing_enable(0)
     torch.cuda.synchronize()
+    attn_ms, attn_launches = tk["attn_ms"], tk["attn_launches"]
 
     events = B * n_gen
     ar_value = None
@@ -183,6 +210,16 @@ def main():
                      "traffic": measured_traffic(wl.name), "avg_launch_us": avg_ms * 1e3, "launches": attn_launches,
                      "algorithmic_bytes_per_launch": per_launch},
     }
+    c = wl.target
+    gemm_tflops = tk["gemm_flop"] / (tk["gemm_ms"] * 1e-3) / 1e12 if tk["gemm_ms"] else 0.0
+    gemm_peak = MFMA_PEAK_TFLOPS[c.prec]
+    out["verify_gemm"] = {"bound": "mfma", "achieved": gemm_tflops, "peak": gemm_peak, "unit": "TFLOP/s",
+                          "frac": gemm_tflops / gemm_peak, "launches": tk["gemm_launches"],
+                          "avg_launch_us": tk["gemm_ms"] * 1e3 / max(1, tk["gemm_launches"])}
+    nr = max(1, tph["rounds"])
+    out["round_us"] = {"draft": tph["draft_ms"] * 1e3 / nr, "verify": tph["verify_ms"] * 1e3 / nr,
+                       "accept": tph["accept_ms"] * 1e3 / nr, "rounds": tph["rounds"]}
+    out["verify_pass"] = verify_pass_fraction(wl, gamma, B, tph["verify_ms"] / nr)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, gamma, wt, wd, ht, hk, min(args.cpu_seqs, B),
                                            min(args.cpu_events, n_gen))

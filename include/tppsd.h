@@ -230,13 +230,29 @@ int tppsd_read_events(tppsd_state *s, float *d_t, int32_t *d_k, int32_t *d_n, hi
 int tppsd_state_status(tppsd_state *s, hipStream_t stream, uint32_t *bits, int32_t *n_done,
                        int64_t *accepted_drafts, int64_t *drafted, int64_t *ar_candidates);
 
-/* Per-kernel timing: when enabled, tppsd_sample_sd launches its rounds
- * directly (instead of replaying a captured HIP graph) and brackets every
- * launch of the target's verify attention kernel with HIP events on the
- * caller's stream; tppsd_timing_read returns the total milliseconds and the
- * launch count since tppsd_timing_enable. Other entry points are not timed. */
-int tppsd_timing_enable(tppsd_state *s, int enable);
-int tppsd_timing_read(tppsd_state *s, double *ms, int64_t *launches);
+/* Measurement of tppsd_sample_sd; the sampled events are unchanged.
+ * TPPSD_TIME_KERNELS: rounds are launched directly instead of replaying a
+ *   captured HIP graph, and every launch of the target's verify attention and
+ *   of its verify GEMMs (QKV, attention output, FFN in, FFN out, decoder E) is
+ *   bracketed by HIP events stamped with the kernel's own start and stop.
+ * TPPSD_TIME_PHASES: each round replays three captured graphs (draft, verify,
+ *   accept) with HIP events recorded between them on the caller's stream.
+ * The two modes are separate runs (both bits at once: TPPSD_E_ARG).
+ * tppsd_timing_enable resets the sums; tppsd_timing_read copies them. Other
+ * entry points are not timed. */
+#define TPPSD_TIME_KERNELS 1
+#define TPPSD_TIME_PHASES 2
+typedef struct tppsd_timing {
+  double attn_ms;          /* verify attention: summed kernel time */
+  int64_t attn_launches;
+  double gemm_ms;          /* verify GEMMs: summed kernel time */
+  int64_t gemm_launches;
+  double gemm_flop;        /* 2 * rows * N * K over the timed GEMM launches */
+  double draft_ms, verify_ms, accept_ms;   /* phase times */
+  int64_t rounds;          /* rounds timed */
+} tppsd_timing;
+int tppsd_timing_enable(tppsd_state *s, int modes);
+int tppsd_timing_read(tppsd_state *s, tppsd_timing *out);
 
 /* Thread-local description of the last error on this thread. */
 const char *tppsd_last_error(void);

@@ -44,6 +44,10 @@ int hip_check(const char *what) {
   return TPPSD_OK;
 }
 
+int hip_check_rc(hipError_t e) {
+  return e == hipSuccess ? TPPSD_OK : fail(TPPSD_E_HIP, "timing event: %s", hipGetErrorString(e));
+}
+
 void drop_graph(hipGraphExec_t *g) {
   if (*g) (void)hipGraphExecDestroy(*g);
   *g = nullptr;
@@ -150,7 +154,9 @@ struct tppsd_model {
 
 // ---- state ------------------------------------------------------------------
 struct ModelCache {
-  char *k = nullptr, *v = nullptr;   // [L][B][H][cap][dh]
+  // per layer: keys [B][H][kv_cap][dh]; values the same for fp32, in
+  // 8-position blocks [B][H][kv_cap / 8][dh][8] for bf16
+  char *k = nullptr, *v = nullptr;
   size_t layer_bytes = 0;
   float *freq = nullptr;
 };
@@ -158,6 +164,7 @@ struct ModelCache {
 struct tppsd_state {
   const tppsd_model *T = nullptr, *D = nullptr;
   int B = 0, cap = 0, max_gamma = 0, Pmax = 0;
+  int kv_cap = 0;   // KV cache positions per (sequence, head): cap rounded up to 8
   uint64_t seed = 0;
   unsigned flags = 0;
   char *ws = nullptr;
@@ -185,14 +192,18 @@ struct tppsd_state {
   bool prefilled = false, draft_ok = false, drafted_this_round = false;
   int32_t *host_ndone = nullptr;   // pinned, 2 slots
   hipEvent_t poll_ev[2] = {nullptr, nullptr};
-  // timing of the verify attention kernel: HIP events around its launches,
-  // recorded as nodes of the captured round graph (two graph instances with
-  // their own events, alternated per round and read one round behind)
-  bool timing = false;
+  // measurement (tppsd_timing_enable): two event sets alternated per round
+  // and read one round behind. Kernel mode: a pair of events around every
+  // verify attention / GEMM launch (rounds launched directly); phase mode:
+  // events between the draft, verify and accept graphs of each round.
+  int timing = 0;
   std::vector<hipEvent_t> gev[2];
-  hipEvent_t *cur_ev = nullptr;      // events of the graph being captured
-  double t_ms = 0.0;
-  int64_t t_launches = 0;
+  std::vector<hipEvent_t> pev[2];
+  hipEvent_t *cur_ev = nullptr;      // kernel events of the round being launched
+  tppsd_timing tm{};
+  double round_flop = 0.0;           // verify GEMM flops of one round
+  hipGraphExec_t phase_exec[3] = {nullptr, nullptr, nullptr};
+  long long phase_key = -1;
   // HIP graphs of the sampling loops, captured on a private stream and
   // replayed on the caller's; keyed by what their kernel arguments embed
   hipStream_t cap_stream = nullptr;
@@ -244,10 +255,11 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   w.ev_k = take(Bz * cap * 4);
   w.freqT = take((size_t)T->d() * 4);
   w.freqD = take(D ? (size_t)D->d() * 4 : 0);
-  w.layerT = Bz * T->H() * cap * T->dh() * T->act_bytes();
+  const size_t kvc = kv_stride(cap);
+  w.layerT = Bz * T->H() * kvc * T->dh() * T->act_bytes();
   w.kT = take(w.layerT * T->cfg.n_layers);
   w.vT = take(w.layerT * T->cfg.n_layers);
-  w.layerD = D ? Bz * D->H() * cap * D->dh() * D->act_bytes() : 0;
+  w.layerD = D ? Bz * D->H() * kvc * D->dh() * D->act_bytes() : 0;
   w.kD = take(D ? w.layerD * D->cfg.n_layers : 0);
   w.vD = take(D ? w.layerD * D->cfg.n_layers : 0);
   const int Pmax = std::max(MG + 1, PREFILL_CHUNK);
@@ -266,8 +278,8 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   w.ar_lt = take(Bz * kmax * 4);
   {
     const int qtm = (Pmax + 15) / 16;
-    size_t pf = attn_part_floats(B, T->H(), T->dh(), qtm, cap);
-    if (D) pf = std::max(pf, attn_part_floats(B, D->H(), D->dh(), qtm, cap));
+    size_t pf = attn_part_floats(B, T->H(), T->dh(), qtm, (int)kvc);
+    if (D) pf = std::max(pf, attn_part_floats(B, D->H(), D->dh(), qtm, (int)kvc));
     w.attn_part = take(pf * 4);
   }
   w.gen0 = take(Bz * 4);
@@ -296,15 +308,24 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
 
 // Block forward of P new positions per sequence through model m (encoder of
 // §4.2), keys/values appended at start[b] + start_off + p; optional decoder.
+// verify: the target's verify pass (its attention launches carry their own
+// kernel name; in kernel-timing mode its attention and GEMM launches are
+// bracketed by the events of s->cur_ev: attention of layer l in pair l, GEMM j
+// of the pass in pair n_layers + j).
 int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int32_t *start, int start_off,
-            int P, const TokSrc &src, const HeadArgs *head, bool time_attn, hipStream_t st) {
+            int P, const TokSrc &src, const HeadArgs *head, bool verify, hipStream_t st) {
   const int B = s->B, d = m->d(), H = m->H(), dh = m->dh(), F = m->cfg.d_ffn, bf = m->bf16();
-  const int T = B * P;
+  const int T = B * P, L = m->cfg.n_layers;
+  const bool timed = verify && s->cur_ev != nullptr;
+  auto ev = [&](int pair, int end) -> hipEvent_t { return timed ? s->cur_ev[2 * pair + end] : nullptr; };
+  // LayerNorms run inside the GEMMs that consume them where the width allows
+  const bool fuse_ln = gemm_ln_fusable(bf, d);
   launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW &w = m->layers[l];
     char *kc = c.k + c.layer_bytes * l, *vc = c.v + c.layer_bytes * l;
-    launch_layernorm(s->x, s->a, bf, w.ln1_g, w.ln1_b, T, d, st);
+    const LnA ln1{s->x, w.ln1_g, w.ln1_b}, ln2{s->x, w.ln2_g, w.ln2_b};
+    if (!fuse_ln) launch_layernorm(s->x, s->a, bf, w.ln1_g, w.ln1_b, T, d, st);
     Epi e{};
     e.mode = EPI_QKV;
     e.bias = w.qkv_b;
@@ -317,42 +338,41 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     e.H = H;
     e.dh = dh;
     e.d = d;
-    e.cap = s->cap;
+    e.cap = s->kv_cap;
     e.status = s->status;
-    launch_gemm(s->a, w.qkv_w, bf, T, 3 * d, d, e, st);
-    const bool timed = time_attn && s->cur_ev != nullptr;
-    launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->cap, s->attn_part,
-                     time_attn ? 1 : 0, timed ? s->cur_ev[2 * l] : nullptr, timed ? s->cur_ev[2 * l + 1] : nullptr,
-                     st);
+    launch_gemm(s->a, fuse_ln ? &ln1 : nullptr, w.qkv_w, bf, T, 3 * d, d, e, st, ev(L + 4 * l, 0), ev(L + 4 * l, 1));
+    launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->kv_cap, s->attn_part,
+                     verify ? 1 : 0, ev(l, 0), ev(l, 1), st);
     Epi eo{};
     eo.mode = EPI_RESID;
     eo.bias = w.out_b;
     eo.out = s->x;
     eo.ldo = d;
-    launch_gemm(s->o, w.out_w, bf, T, d, d, eo, st);
-    launch_layernorm(s->x, s->a, bf, w.ln2_g, w.ln2_b, T, d, st);
+    launch_gemm(s->o, nullptr, w.out_w, bf, T, d, d, eo, st, ev(L + 4 * l + 1, 0), ev(L + 4 * l + 1, 1));
+    if (!fuse_ln) launch_layernorm(s->x, s->a, bf, w.ln2_g, w.ln2_b, T, d, st);
     Epi e1{};
     e1.mode = EPI_RELU;
     e1.bias = w.ffn1_b;
     e1.out = s->hid;
     e1.ldo = F;
-    launch_gemm(s->a, w.ffn1_w, bf, T, F, d, e1, st);
+    launch_gemm(s->a, fuse_ln ? &ln2 : nullptr, w.ffn1_w, bf, T, F, d, e1, st, ev(L + 4 * l + 2, 0), ev(L + 4 * l + 2, 1));
     Epi e2{};
     e2.mode = EPI_RESID;
     e2.bias = w.ffn2_b;
     e2.out = s->x;
     e2.ldo = d;
-    launch_gemm(s->hid, w.ffn2_w, bf, T, d, F, e2, st);
+    launch_gemm(s->hid, nullptr, w.ffn2_w, bf, T, d, F, e2, st, ev(L + 4 * l + 3, 0), ev(L + 4 * l + 3, 1));
   }
   if (head) {
-    launch_layernorm(s->x, s->a, bf, m->lnf_g, m->lnf_b, T, d, st);
+    const LnA lnf{s->x, m->lnf_g, m->lnf_b};
+    if (!fuse_ln) launch_layernorm(s->x, s->a, bf, m->lnf_g, m->lnf_b, T, d, st);
     Epi eh{};
     eh.mode = EPI_HEAD;
     eh.bias = m->k1_b;
     eh.out = s->e;
     eh.ldo = 4 * d;
     eh.split = 3 * d;
-    launch_gemm(s->a, m->Ek1_w, bf, T, 4 * d, d, eh, st);
+    launch_gemm(s->a, fuse_ln ? &lnf : nullptr, m->Ek1_w, bf, T, 4 * d, d, eh, st, ev(5 * L, 0), ev(5 * L, 1));
     launch_head(s->e, bf, d, m->cfg.n_mix, m->cfg.n_types, m->mix_w, m->mix_b, m->k2_w, m->k2_b, *head, st);
   }
   return TPPSD_OK;
@@ -421,7 +441,7 @@ int do_draft_fused(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStr
   a.kc = s->cD.k;
   a.vc = s->cD.v;
   a.layer_bytes = s->cD.layer_bytes;
-  a.cap = s->cap;
+  a.cap = s->kv_cap;
   a.ev_t = s->ev_t;
   a.ev_k = s->ev_k;
   a.ev_stride = s->cap;
@@ -670,6 +690,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->D = D;
   s->B = B;
   s->cap = max_events;
+  s->kv_cap = kv_stride(max_events);
   s->max_gamma = max_gamma;
   s->Pmax = std::max(max_gamma + 1, PREFILL_CHUNK);
   s->seed = seed;
@@ -757,7 +778,10 @@ void tppsd_state_destroy(tppsd_state *s) {
     if (e) (void)hipEventDestroy(e);
   drop_graph(&s->sd_exec[0]);
   drop_graph(&s->sd_exec[1]);
+  for (hipGraphExec_t &g : s->phase_exec) drop_graph(&g);
   for (auto &v : s->gev)
+    for (hipEvent_t e : v) (void)hipEventDestroy(e);
+  for (auto &v : s->pev)
     for (hipEvent_t e : v) (void)hipEventDestroy(e);
   drop_graph(&s->ar_exec[0]);
   drop_graph(&s->ar_exec[1]);
@@ -915,15 +939,43 @@ int tppsd_sample_ar(tppsd_state *s, int n_events, float *d_t_out, int32_t *d_k_o
 }
 
 namespace {
-// adds the verify-attention times recorded in event set w during its last round
+// adds the times recorded in event set w during its round (read one round behind)
 void read_round_events(tppsd_state *s, int w) {
-  for (size_t i = 0; i + 1 < s->gev[w].size(); i += 2) {
-    float ms = 0.f;
-    if (hipEventElapsedTime(&ms, s->gev[w][i], s->gev[w][i + 1]) == hipSuccess) {
-      s->t_ms += ms;
-      s->t_launches += 1;
+  const int L = s->T->cfg.n_layers;
+  if (s->timing & TPPSD_TIME_KERNELS) {
+    for (size_t i = 0; i + 1 < s->gev[w].size(); i += 2) {
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, s->gev[w][i], s->gev[w][i + 1]) != hipSuccess) continue;
+      if ((int)(i / 2) < L) {
+        s->tm.attn_ms += ms;
+        s->tm.attn_launches += 1;
+      } else {
+        s->tm.gemm_ms += ms;
+        s->tm.gemm_launches += 1;
+      }
     }
+    s->tm.gemm_flop += s->round_flop;
   }
+  if (s->timing & TPPSD_TIME_PHASES) {
+    float ms[3] = {0.f, 0.f, 0.f};
+    for (int j = 0; j < 3; ++j)
+      if (hipEventElapsedTime(&ms[j], s->pev[w][j], s->pev[w][j + 1]) != hipSuccess) ms[j] = 0.f;
+    s->tm.draft_ms += ms[0];
+    s->tm.verify_ms += ms[1];
+    s->tm.accept_ms += ms[2];
+  }
+  s->tm.rounds += 1;
+}
+
+int make_events(std::vector<hipEvent_t> *v, size_t n) {
+  for (int w = 0; w < 2; ++w)
+    if (v[w].size() != n) {
+      for (hipEvent_t e : v[w]) (void)hipEventDestroy(e);
+      v[w].assign(n, nullptr);
+      for (hipEvent_t &e : v[w])
+        if (hipEventCreate(&e) != hipSuccess) return hip_check("tppsd_sample_sd: timing events");
+    }
+  return TPPSD_OK;
 }
 }  // namespace
 
@@ -931,47 +983,71 @@ int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipS
   if (int rc = check_round(s, gamma)) return rc;
   if (!s->D) return fail(TPPSD_E_ORDER, "state has no draft model");
   if (!s->draft_ok) return fail(TPPSD_E_ORDER, "draft cache is stale; prefill again");
-  // timed runs launch eagerly so that host-recorded HIP events can bracket the
-  // verify-attention launches; otherwise each round replays one captured graph
-  const bool timed = s->timing;
-  const bool graphs = s->use_graphs && !timed;
-  if (graphs) {
-    const long long key = (long long)gamma * 100000007LL + s->n_gen;
-    if (!s->sd_exec[0] || s->sd_key != key) {
-      drop_graph(&s->sd_exec[0]);
-      int rc = capture(s, [&](hipStream_t cs) {
-        int r = do_draft(s, gamma, &s->idr, cs);
-        if (!r) r = do_verify(s, gamma, &s->idr, &s->ivf, cs);
-        if (!r) r = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, cs);
-        return r;
-      }, &s->sd_exec[0]);
-      if (rc) return rc;
-      s->sd_key = key;
-    }
+  // kernel timing launches the rounds directly so that host-recorded HIP
+  // events can bracket single kernels; otherwise each round replays one
+  // captured graph, or three (draft, verify, accept) when phases are timed
+  const bool kern = (s->timing & TPPSD_TIME_KERNELS) != 0;
+  const bool phases = (s->timing & TPPSD_TIME_PHASES) != 0;
+  const bool graphs = s->use_graphs && !kern;
+  const long long key = (long long)gamma * 100000007LL + s->n_gen;
+  if (graphs && !phases && (!s->sd_exec[0] || s->sd_key != key)) {
+    drop_graph(&s->sd_exec[0]);
+    int rc = capture(s, [&](hipStream_t cs) {
+      int r = do_draft(s, gamma, &s->idr, cs);
+      if (!r) r = do_verify(s, gamma, &s->idr, &s->ivf, cs);
+      if (!r) r = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, cs);
+      return r;
+    }, &s->sd_exec[0]);
+    if (rc) return rc;
+    s->sd_key = key;
   }
-  if (timed) {
-    for (auto &v : s->gev)
-      if (v.empty()) {
-        v.resize(2 * s->T->cfg.n_layers);
-        for (hipEvent_t &e : v)
-          if (hipEventCreate(&e) != hipSuccess) return hip_check("tppsd_sample_sd: timing events");
-      }
+  if (graphs && phases && (!s->phase_exec[0] || s->phase_key != key)) {
+    for (hipGraphExec_t &g : s->phase_exec) drop_graph(&g);
+    int rc = capture(s, [&](hipStream_t cs) { return do_draft(s, gamma, &s->idr, cs); }, &s->phase_exec[0]);
+    if (!rc)
+      rc = capture(s, [&](hipStream_t cs) { return do_verify(s, gamma, &s->idr, &s->ivf, cs); },
+                   &s->phase_exec[1]);
+    if (!rc)
+      rc = capture(s, [&](hipStream_t cs) { return do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, cs); },
+                   &s->phase_exec[2]);
+    if (rc) return rc;
+    s->phase_key = key;
   }
+  if (kern) {
+    const tppsd_model *m = s->T;
+    const int L = m->cfg.n_layers;
+    const double d = m->d(), F = m->cfg.d_ffn, rows = (double)s->B * (gamma + 1);
+    s->round_flop = 2.0 * rows * (L * (3 * d * d + d * d + 2 * d * F) + 4 * d * d);
+    if (int rc = make_events(s->gev, 2 * (5 * L + 1))) return rc;
+  }
+  if (phases)
+    if (int rc = make_events(s->pev, 4)) return rc;
   int r = 0;
   for (; r < max_rounds; ++r) {
     if (r >= 1) {
       // the done counter copied after round r - 1; waits for that round only
       if (hipEventSynchronize(s->poll_ev[(r - 1) & 1]) != hipSuccess) return hip_check("tppsd_sample_sd: poll");
-      if (timed) read_round_events(s, (r - 1) & 1);
+      if (s->timing) read_round_events(s, (r - 1) & 1);
       if (s->host_ndone[(r - 1) & 1] >= s->B) break;
     }
-    if (graphs) {
+    if (graphs && phases) {
+      hipEvent_t *pe = s->pev[r & 1].data();
+      for (int j = 0; j < 3; ++j)
+        if (hipEventRecord(pe[j], st) != hipSuccess || hipGraphLaunch(s->phase_exec[j], st) != hipSuccess)
+          return hip_check("tppsd_sample_sd: phase graph launch");
+      if (hipEventRecord(pe[3], st) != hipSuccess) return hip_check("tppsd_sample_sd: phase event");
+    } else if (graphs) {
       if (hipGraphLaunch(s->sd_exec[0], st) != hipSuccess) return hip_check("tppsd_sample_sd: graph launch");
     } else {
-      s->cur_ev = timed ? s->gev[r & 1].data() : nullptr;
-      int rc = do_draft(s, gamma, &s->idr, st);
+      hipEvent_t *pe = phases ? s->pev[r & 1].data() : nullptr;
+      s->cur_ev = kern ? s->gev[r & 1].data() : nullptr;
+      int rc = pe ? hip_check_rc(hipEventRecord(pe[0], st)) : 0;
+      if (!rc) rc = do_draft(s, gamma, &s->idr, st);
+      if (!rc && pe) rc = hip_check_rc(hipEventRecord(pe[1], st));
       if (!rc) rc = do_verify(s, gamma, &s->idr, &s->ivf, st);
+      if (!rc && pe) rc = hip_check_rc(hipEventRecord(pe[2], st));
       if (!rc) rc = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, st);
+      if (!rc && pe) rc = hip_check_rc(hipEventRecord(pe[3], st));
       s->cur_ev = nullptr;
       if (rc) return rc;
     }
@@ -979,7 +1055,7 @@ int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipS
         hipEventRecord(s->poll_ev[r & 1], st) != hipSuccess)
       return hip_check("tppsd_sample_sd: poll");
   }
-  if (timed && r == max_rounds && r >= 1) {
+  if (s->timing && r == max_rounds && r >= 1) {
     if (hipEventSynchronize(s->poll_ev[(r - 1) & 1]) != hipSuccess) return hip_check("tppsd_sample_sd: poll");
     read_round_events(s, (r - 1) & 1);
   }
@@ -1012,18 +1088,20 @@ int tppsd_state_status(tppsd_state *s, hipStream_t st, uint32_t *bits, int32_t *
   return TPPSD_OK;
 }
 
-int tppsd_timing_enable(tppsd_state *s, int enable) {
+int tppsd_timing_enable(tppsd_state *s, int modes) {
   if (!s) return fail(TPPSD_E_ARG, "null state");
-  s->timing = enable != 0;
-  s->t_ms = 0.0;
-  s->t_launches = 0;
+  if (modes & ~(TPPSD_TIME_KERNELS | TPPSD_TIME_PHASES))
+    return fail(TPPSD_E_ARG, "unknown timing mode bits");
+  if ((modes & TPPSD_TIME_KERNELS) && (modes & TPPSD_TIME_PHASES))
+    return fail(TPPSD_E_ARG, "kernel and phase timing are separate runs");
+  s->timing = modes;
+  s->tm = tppsd_timing{};
   return TPPSD_OK;
 }
 
-int tppsd_timing_read(tppsd_state *s, double *ms, int64_t *launches) {
-  if (!s) return fail(TPPSD_E_ARG, "null state");
-  if (ms) *ms = s->t_ms;
-  if (launches) *launches = s->t_launches;
+int tppsd_timing_read(tppsd_state *s, tppsd_timing *out) {
+  if (!s || !out) return fail(TPPSD_E_ARG, "null argument");
+  *out = s->tm;
   return TPPSD_OK;
 }
 

@@ -135,28 +135,35 @@ void launch_embed(float *x, int T, int d, int P, const TokSrc &src, const void *
                   const float *freq, int K, hipStream_t st);
 void launch_layernorm(const float *x, void *y, int bf16, const float *g, const float *b, int T, int d,
                       hipStream_t st);
-void launch_gemm(const void *X, const void *W, int bf16, int T, int N, int K, const Epi &epi,
-                 hipStream_t st);
-// Key splits of the attention for B sequences x H heads x qtiles query tiles
-// over at most max_keys keys: enough workgroups to fill the chip, each split
-// keeping at least 512 keys (shorter splits do not pay for the merge launch).
-inline int attn_splits(int B, int H, int qtiles, int max_keys) {
-  const long items = (long)B * H * qtiles;
+// A operand given as LayerNorm(x) of the fp32 stream x [T, K] with gain g and bias b
+struct LnA {
+  const float *x, *g, *b;
+};
+// Y = A W^T into the epilogue; A is X [T, K] of the operand type, or, when ln
+// is not null, LayerNorm of ln->x computed inside the GEMM. ev0/ev1
+// (optional): HIP events stamped with the kernel's own start and stop.
+void launch_gemm(const void *X, const LnA *ln, const void *W, int bf16, int T, int N, int K, const Epi &epi,
+                 hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// whether launch_gemm can take a LayerNorm operand of width K
+bool gemm_ln_fusable(int bf16, int K);
+// Positions per (sequence, head) slab of a KV cache: the event capacity
+// rounded up to a multiple of 8 (bf16 values are stored in 8-position blocks).
+inline int kv_stride(int cap) { return (cap + 7) / 8 * 8; }
+
+// Key splits of the attention for B sequences x H heads over at most max_keys
+// keys (one workgroup serves all query tiles of a pair): enough workgroups to
+// fill the chip, each split keeping at least 512 keys (shorter splits do not
+// pay for the merge launch).
+inline int attn_splits(int B, int H, int max_keys) {
+  const long items = (long)B * H;
   int s = 1;
   while (s < 8 && items * s < 1024 && max_keys / (2 * s) >= 512) s *= 2;
   return s;
 }
-// floats of split partials needed for up to qtiles_max query tiles
+// floats of split partials for up to qtiles_max query tiles of 16
 inline size_t attn_part_floats(int B, int H, int dh, int qtiles_max, int max_keys) {
-  size_t best = 0;
-  for (int qt = 1; qt <= qtiles_max; ++qt) {
-    const int s = attn_splits(B, H, qt, max_keys);
-    if (s > 1) {
-      const size_t n = (size_t)B * H * qt * 16 * s * (dh + 2);
-      if (n > best) best = n;
-    }
-  }
-  return best;
+  const int s = attn_splits(B, H, max_keys);
+  return s > 1 ? (size_t)B * H * qtiles_max * 16 * s * (dh + 2) : 0;
 }
 void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16,
                       const int32_t *start, int start_off, const int32_t *done, int B, int P, int H,

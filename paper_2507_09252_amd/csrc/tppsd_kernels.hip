@@ -41,6 +41,19 @@ template <typename T> __device__ __forceinline__ void st(T *p, size_t i, float v
 template <> __device__ __forceinline__ void st<float>(float *p, size_t i, float v) { p[i] = v; }
 template <> __device__ __forceinline__ void st<bf16_t>(bf16_t *p, size_t i, float v) { p[i] = f2bf(v); }
 
+// Value cache element (position pos, column j) of the (sequence, head) slab
+// whose first position is row0 = (b H + h) kv_cap. fp32 values are stored
+// row per position like the keys; bf16 values in blocks of 8 positions,
+// [kv_cap / 8][dh][8], so that 8 consecutive positions of one column are one
+// 16-byte load (the operand layout of the P V matrix product).
+template <typename ACT> __device__ __forceinline__ size_t v_at(size_t row0, int pos, int j, int dh);
+template <> __device__ __forceinline__ size_t v_at<float>(size_t row0, int pos, int j, int dh) {
+  return (row0 + pos) * dh + j;
+}
+template <> __device__ __forceinline__ size_t v_at<bf16_t>(size_t row0, int pos, int j, int dh) {
+  return row0 * dh + (size_t)(pos >> 3) * (8 * dh) + j * 8 + (pos & 7);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -206,8 +219,11 @@ __device__ __forceinline__ void epilogue(const Epi &e, int r, int n, float acc) 
         const int h = c / e.dh, j = c - h * e.dh;
         const int pos = e.start[b] + e.start_off + p;
         if (pos < e.cap) {
-          ACT *cache = (ACT *)(which == 1 ? e.kc : e.vc);
-          st(cache, (((size_t)b * e.H + h) * e.cap + pos) * e.dh + j, v);
+          const size_t row0 = ((size_t)b * e.H + h) * e.cap;
+          if (which == 1)
+            st((ACT *)e.kc, (row0 + pos) * e.dh + j, v);
+          else
+            st((ACT *)e.vc, v_at<ACT>(row0, pos, j, e.dh), v);
         } else {
           atomicOr(e.status, TPPSD_STATUS_CAPACITY);
         }
@@ -301,6 +317,196 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const ELT *__restrict__ X, co
       }
 }
 
+// LDS-staged GEMM with fp32 accumulation: a workgroup of 4 waves (2 x 2)
+// owns a BM x BN output tile and walks K in stages of BK = 2 MFMA k-steps.
+// The global loads of the next D stages are in flight in a register ring
+// while the current stage is multiplied out of LDS (double-buffered, one
+// barrier per stage). Rows of both LDS tiles are padded by one 16-byte vector
+// so that the fragment reads (16 rows x 16 bytes per lane group) spread over
+// the banks.
+// LN: the A operand is LayerNorm(x) of the fp32 residual stream x [T, K]
+// (biased variance, eps 1e-5), computed as it is staged so that the
+// normalised activations never go to memory. All K of the tile's rows are in
+// the register ring at once (K <= D * BK, checked by the launcher); each
+// row's VPR vectors sit in VPR adjacent lanes, so its mean and then its
+// variance (two passes over the registers) are lane-group reductions.
+template <typename ELT> constexpr int gemm_bk() { return 2 * MfmaStep<ELT>::KSTEP; }
+constexpr int GEMM_LN_MAX_DEPTH = 8;
+
+template <typename ELT, int BM, int BN, bool LN, int D>
+__global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, const float *__restrict__ xf,
+                                                  const float *__restrict__ lg, const float *__restrict__ lb,
+                                                  const ELT *__restrict__ W, int T, int N, int K, Epi e) {
+  typedef MfmaStep<ELT> S;
+  constexpr int KS = S::KSTEP, BK = 2 * KS;
+  constexpr int VE = 16 / sizeof(ELT);             // elements per 16-byte vector
+  constexpr int LDR = BK + VE;                     // LDS row length (one vector of padding)
+  constexpr int VPR = BK / VE;                     // vectors per tile row per stage (8)
+  constexpr int AV = BM * VPR / 256, BV = BN * VPR / 256;
+  constexpr int XV = LN ? VE / 4 : 1;              // float4 of x per A vector
+  constexpr int TM = BM / 32, TN = BN / 32;
+  static_assert(AV >= 1 && BV >= 1, "tile too small for 256 threads");
+  __shared__ __attribute__((aligned(16))) ELT As[2][BM][LDR];
+  __shared__ __attribute__((aligned(16))) ELT Bs[2][BN][LDR];
+  __shared__ __attribute__((aligned(16))) float gs[LN ? D * BK : 4], bs[LN ? D * BK : 4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rr = lane & 15, g = lane >> 4;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int wm = (wave >> 1) * (BM / 2), wn = (wave & 1) * (BN / 2);
+  const int nst = (K + BK - 1) / BK;
+  // register ring: stage s lives in slot s mod D
+  uint4 ra[D][LN ? 1 : AV], rb[D][BV];
+  float4 rx[D][LN ? AV * XV : 1];
+  float mu[LN ? AV : 1], rs[LN ? AV : 1];
+  auto gload = [&](uint4 *pa, float4 *px, uint4 *pb, int k0) {
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int v = tid + 256 * i, row = v / VPR, k = k0 + (v - row * VPR) * VE;
+      const size_t r = (size_t)min(m0 + row, T - 1);
+      if (LN) {
+#pragma unroll
+        for (int c = 0; c < XV; ++c)
+          px[i * XV + c] = (k < K) ? *(const float4 *)(xf + r * K + k + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {
+        pa[i] = (k < K) ? *(const uint4 *)(X + r * K + k) : make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < BV; ++i) {
+      const int v = tid + 256 * i, row = v / VPR, k = k0 + (v - row * VPR) * VE;
+      const size_t r = (size_t)min(n0 + row, N - 1);
+      pb[i] = (k < K) ? *(const uint4 *)(W + r * K + k) : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  auto lstore = [&](int buf, const uint4 *pa, const float4 *px, const uint4 *pb, int k0) {
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int v = tid + 256 * i, row = v / VPR, kv = v - row * VPR;
+      uint4 w;
+      if (LN) {
+        const int k = k0 + kv * VE;
+        float y[VE];
+#pragma unroll
+        for (int c = 0; c < XV; ++c) {
+          // K is a multiple of 4: a float4 of x is wholly inside or past K
+          const int kk = k + 4 * c;
+          const float4 xv = px[i * XV + c];
+          if (kk < K) {
+            const float4 gv = *(const float4 *)&gs[kk], bv = *(const float4 *)&bs[kk];
+            y[4 * c + 0] = (xv.x - mu[i]) * rs[i] * gv.x + bv.x;
+            y[4 * c + 1] = (xv.y - mu[i]) * rs[i] * gv.y + bv.y;
+            y[4 * c + 2] = (xv.z - mu[i]) * rs[i] * gv.z + bv.z;
+            y[4 * c + 3] = (xv.w - mu[i]) * rs[i] * gv.w + bv.w;
+          } else {
+            y[4 * c + 0] = y[4 * c + 1] = y[4 * c + 2] = y[4 * c + 3] = 0.f;
+          }
+        }
+        if (sizeof(ELT) == 2) {
+          uint32_t pk[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) pk[q] = (uint32_t)f2bf(y[2 * q]) | ((uint32_t)f2bf(y[2 * q + 1]) << 16);
+          w = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+        } else {
+          w = make_uint4(__float_as_uint(y[0]), __float_as_uint(y[1]), __float_as_uint(y[2]), __float_as_uint(y[3]));
+        }
+      } else {
+        w = pa[i];
+      }
+      *(uint4 *)&As[buf][row][kv * VE] = w;
+    }
+#pragma unroll
+    for (int i = 0; i < BV; ++i) {
+      const int v = tid + 256 * i, row = v / VPR, kv = v - row * VPR;
+      *(uint4 *)&Bs[buf][row][kv * VE] = pb[i];
+    }
+  };
+  // the first D stages' loads go out before anything else
+#pragma unroll
+  for (int u = 0; u < D; ++u)
+    if (u < nst) gload(ra[u], rx[u], rb[u], u * BK);
+  if (LN) {
+    for (int k = tid; k < K; k += 256) {
+      gs[k] = lg[k];
+      bs[k] = lb[k];
+    }
+    // row statistics from the ring (zero-filled past K): mean, then the
+    // sum of squared deviations over the K real columns
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int kv = (tid + 256 * i) % VPR;
+      float sum = 0.f;
+#pragma unroll
+      for (int u = 0; u < D; ++u)
+        if (u < nst) {
+#pragma unroll
+          for (int c = 0; c < XV; ++c) {
+            const float4 xv = rx[u][i * XV + c];
+            sum += (xv.x + xv.y) + (xv.z + xv.w);
+          }
+        }
+#pragma unroll
+      for (int off = 1; off < VPR; off <<= 1) sum += __shfl_xor(sum, off, 64);
+      const float mean = sum / (float)K;
+      float var = 0.f;
+#pragma unroll
+      for (int u = 0; u < D; ++u)
+#pragma unroll
+        for (int c = 0; c < XV; ++c) {
+          const int k = u * BK + kv * VE + 4 * c;
+          if (k < K) {
+            const float4 xv = rx[u][i * XV + c];
+            const float a = xv.x - mean, b = xv.y - mean, cc = xv.z - mean, dd = xv.w - mean;
+            var += (a * a + b * b) + (cc * cc + dd * dd);
+          }
+        }
+#pragma unroll
+      for (int off = 1; off < VPR; off <<= 1) var += __shfl_xor(var, off, 64);
+      mu[i] = mean;
+      rs[i] = 1.f / sqrtf(var / (float)K + 1e-5f);
+    }
+    __syncthreads();
+  }
+  f32x4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < nst; s0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int st_i = s0 + u;
+      if (st_i < nst) {
+        const int buf = st_i & 1;
+        lstore(buf, ra[u], rx[u], rb[u], st_i * BK);
+        __syncthreads();
+        if (!LN && st_i + D < nst) gload(ra[u], rx[u], rb[u], (st_i + D) * BK);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          typename S::frag a[TM], b[TN];
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+            a[i] = *(const typename S::frag *)&As[buf][wm + 16 * i + rr][ks * KS + (KS / 4) * g];
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            b[j] = *(const typename S::frag *)&Bs[buf][wn + 16 * j + rr][ks * KS + (KS / 4) * g];
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = S::mma(a[i], b[j], acc[i][j]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int r = m0 + wm + 16 * i + 4 * g + v, n = n0 + wn + 16 * j + rr;
+        if (r < T && n < N) epilogue<ELT>(e, r, n, acc[i][j][v]);
+      }
+}
+
 // ---------------------------------------------------------------------------
 // causal attention of P new queries per (sequence, head) over the KV cache
 // (App. D.4: softmax-normalised exp(q.k / sqrt(d_head)) weights over the
@@ -341,20 +547,20 @@ __global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q,
     qs[qq][j] = (qq < nq) ? ld(q, (size_t)(b * P + q0 + qq) * d + h * DH + j) * scale : 0.f;
   }
   const int my_last = base + q0 + qi;             // last key index for this thread's query
-  const int n_keys = base + q0 + nq;             // keys 0 .. n_keys-1 are needed by this tile
+  const int n_keys = min(base + q0 + nq, cap);   // keys 0 .. n_keys-1 are needed by this tile
   float m_run = -INFINITY, l_run = 0.f;
   float acc[EPT];
 #pragma unroll
   for (int i = 0; i < EPT; ++i) acc[i] = 0.f;
-  const size_t kvbase = ((size_t)b * H + h) * cap * DH;
+  const size_t row0 = ((size_t)b * H + h) * cap;
   for (int kt = 0; kt < n_keys; kt += KT) {
     __syncthreads();
     for (int idx = tid; idx < KT * DH; idx += 256) {
       const int kk = idx / DH, j = idx - kk * DH;
       const int key = kt + kk;
       const bool ok = key < n_keys;
-      ks[kk][j] = ok ? ld(kc, kvbase + (size_t)key * DH + j) : 0.f;
-      vs[kk][j] = ok ? ld(vc, kvbase + (size_t)key * DH + j) : 0.f;
+      ks[kk][j] = ok ? ld(kc, (row0 + key) * DH + j) : 0.f;
+      vs[kk][j] = ok ? ld(vc, v_at<ACT>(row0, key, j, DH)) : 0.f;
     }
     __syncthreads();
     // scores for query qi, keys sub + 16 i
@@ -409,146 +615,173 @@ __global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q,
 }
 
 // bf16 causal attention on MFMA with split keys (flash-decoding style).
-// Grid (B * H, query tiles of 16, splits), 4 waves per workgroup. A split
-// owns a contiguous key range of its (sequence, head); its waves take 32-key
-// steps round robin and keep their own online-softmax state, merged in LDS at
-// the end. With one split the merged result is the output, otherwise the
-// split writes (max, sum, unnormalised output) and k_attn_combine merges.
+// Grid (B * H, 1, splits), 4 waves per workgroup; the workgroup serves all
+// QT query tiles of 16 of its (sequence, head), so each key and value is read
+// from memory once per split whatever the number of queries. A split owns a
+// contiguous key range; its waves take 32-key steps round robin and keep
+// their own online-softmax state per query tile, merged in LDS at the end.
+// With one split the merged result is the output, otherwise the split writes
+// (max, sum, unnormalised output) and k_attn_combine merges.
 //
-// Per 32-key step, S^T = K Q^T is two 16x16 MFMA tiles whose rows are
-// permuted so that lane l ends up holding the scores of query (l mod 16)
-// for the 8 consecutive keys 8 (l / 16) .. + 7: exactly the B operand of
-// O^T = V^T P^T. The A operand (V transposed) goes through LDS.
+// Per 32-key step and query tile, S^T = K Q^T is two 16x16 MFMA tiles whose
+// rows are permuted so that lane l ends up holding the scores of query
+// (l mod 16) for the 8 consecutive keys 8 (l / 16) .. + 7: exactly the B
+// operand of O^T = V^T P^T. The A operand (8 consecutive keys of one value
+// column) is one 16-byte load from the position-blocked value cache.
 typedef short short4_t __attribute__((ext_vector_type(4)));
 
-template <int DH, int ROLE>
+template <int DH, int ROLE, int QT>
 __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q, const bf16_t *__restrict__ kc,
                                                    const bf16_t *__restrict__ vc, bf16_t *__restrict__ o,
                                                    const int32_t *__restrict__ start, int start_off,
                                                    const int32_t *__restrict__ done, int P, int H, int cap,
                                                    int splits, float *__restrict__ part) {
-  constexpr int KT = 32, NDT = DH / 16, VROW = KT + 16;   // V^T rows padded to 96 bytes
-  __shared__ __attribute__((aligned(16))) bf16_t vt[4][DH][VROW];
-  __shared__ float red_m[4][16], red_l[4][16];
-  __shared__ float red_o[4][DH][17];
-  const int bh = blockIdx.x, b = bh / H, h = bh - b * H;
-  const int qt = blockIdx.y, q0 = qt * 16, split = blockIdx.z;
+  constexpr int KT = 32, NDT = DH / 16, NC = DH >= 32 ? DH / 32 : 1, NQ = 16 * QT;
+  __shared__ float red_m[4][NQ], red_l[4][NQ];
+  __shared__ float red_o[4][DH][NQ + 1];
+  const int bh = blockIdx.x, b = bh / H, h = bh - b * H, split = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, rr = lane & 15, g = lane >> 4;
   const int d = H * DH;
-  const int nq = min(16, P - q0);
   const bool skip = done != nullptr && done[b] != 0;
   const int base = start[b] + start_off;
-  const int n_keys = skip ? 0 : base + q0 + nq;
+  const int n_keys = skip ? 0 : min(base + P, cap);   // never past the cache slab
   int chunk = (n_keys + splits - 1) / splits;
   chunk = (chunk + KT - 1) / KT * KT;
   const int k_begin = split * chunk, k_end = min(n_keys, k_begin + chunk);
   const size_t kvbase = ((size_t)b * H + h) * cap;
   const float scale = 1.f / sqrtf((float)DH);
-  const int my_q = q0 + rr;                 // this lane's query (column of S^T)
-  const int my_last = base + my_q;          // last key it may see
-  const bool q_ok = rr < nq;
 
-  // query fragment (B operand of S^T): Q[my_q][k-slice]
-  bf16x8_t qf[DH >= 32 ? DH / 32 : 1];
-  short4_t qf16 = {0, 0, 0, 0};
-  if (DH >= 32) {
+  // query fragments (B operand of S^T): Q[16 t + rr][k slice of lane group g]
+  bf16x8_t qf[QT][NC];
+  short4_t qf16[QT];
 #pragma unroll
-    for (int c = 0; c < DH / 32; ++c) {
-      if (q_ok)
-        qf[c] = *(const bf16x8_t *)(q + (size_t)(b * P + my_q) * d + h * DH + 32 * c + 8 * g);
-      else
-        qf[c] = (bf16x8_t){};
+  for (int t = 0; t < QT; ++t) {
+    const int my_q = 16 * t + rr;
+    const bool q_ok = my_q < P;
+    const bf16_t *qp = q + (size_t)(b * P + (q_ok ? my_q : 0)) * d + h * DH;
+    if (DH >= 32) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) qf[t][c] = q_ok ? *(const bf16x8_t *)(qp + 32 * c + 8 * g) : (bf16x8_t){};
+    } else {
+      qf16[t] = q_ok ? *(const short4_t *)(qp + 4 * g) : (short4_t){0, 0, 0, 0};
     }
-  } else {
-    if (q_ok) qf16 = *(const short4_t *)(q + (size_t)(b * P + my_q) * d + h * DH + 4 * g);
   }
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4_t oacc[NDT];
+  float m_run[QT], l_run[QT];
+  f32x4_t oacc[QT][NDT];
 #pragma unroll
-  for (int t = 0; t < NDT; ++t) oacc[t] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+#pragma unroll
+    for (int td = 0; td < NDT; ++td) oacc[t][td] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  }
   // permuted key rows of the two S^T halves loaded by this lane
   const int krow0 = 8 * (rr >> 2) + (rr & 3), krow1 = krow0 + 4;
 
   for (int kt = k_begin + wave * KT; kt < k_end; kt += 4 * KT) {
     const size_t r0 = kvbase + min(kt + krow0, cap - 1), r1 = kvbase + min(kt + krow1, cap - 1);
-    f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    bf16x8_t a0[NC], a1[NC];
+    short4_t b0 = {0, 0, 0, 0}, b1 = {0, 0, 0, 0};
     if (DH >= 32) {
 #pragma unroll
-      for (int c = 0; c < DH / 32; ++c) {
-        const bf16x8_t a0 = *(const bf16x8_t *)(kc + r0 * DH + 32 * c + 8 * g);
-        const bf16x8_t a1 = *(const bf16x8_t *)(kc + r1 * DH + 32 * c + 8 * g);
-        s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, qf[c], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, qf[c], s1, 0, 0, 0);
+      for (int c = 0; c < NC; ++c) {
+        a0[c] = *(const bf16x8_t *)(kc + r0 * DH + 32 * c + 8 * g);
+        a1[c] = *(const bf16x8_t *)(kc + r1 * DH + 32 * c + 8 * g);
       }
     } else {
-      const short4_t a0 = *(const short4_t *)(kc + r0 * DH + 4 * g);
-      const short4_t a1 = *(const short4_t *)(kc + r1 * DH + 4 * g);
-      s0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a0, qf16, s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, qf16, s1, 0, 0, 0);
+      b0 = *(const short4_t *)(kc + r0 * DH + 4 * g);
+      b1 = *(const short4_t *)(kc + r1 * DH + 4 * g);
     }
-    // stage this step's values transposed: vt[wave][j][key] = V[kt + key][j]
-    for (int c = lane; c < KT * DH / 8; c += 64) {
-      const int key = c / (DH / 8), j0 = (c - key * (DH / 8)) * 8;
-      // keys past the range are zero (never-written cache slots may hold NaN bits);
-      // values move as raw 32-bit words (two bf16 each)
+    // values of keys kt + 8 g .. + 7, columns 16 td + rr; positions past the
+    // key range are zeroed (never-written cache slots may hold NaN bits)
+    const int k8 = kt + 8 * g, nv = k_end - k8;
+    uint4 vw[NDT];
+#pragma unroll
+    for (int td = 0; td < NDT; ++td) {
       uint4 v = {0u, 0u, 0u, 0u};
-      if (kt + key < k_end) v = *(const uint4 *)(vc + (kvbase + kt + key) * DH + j0);
-      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        vt[wave][j0 + e][key] = (bf16_t)((e & 1) ? (w[e >> 1] >> 16) : (w[e >> 1] & 0xFFFFu));
+      if (nv > 0) v = *(const uint4 *)(vc + kvbase * DH + (size_t)(k8 >> 3) * (8 * DH) + (16 * td + rr) * 8);
+      vw[td] = v;
     }
-    // scores of keys kt + 8g + j, j = 0..7, for query my_q
-    float sv[8];
-    float mx = -INFINITY;
+    if (nv > 0 && nv < 8) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int key = kt + 8 * g + j;
-      const float raw = (j < 4) ? s0[j] : s1[j - 4];
-      const bool ok = q_ok && key < k_end && key <= my_last;
-      sv[j] = ok ? raw * scale : -INFINITY;
-      mx = fmaxf(mx, sv[j]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
-    float ps = 0.f;
-    uint32_t pw[4];
+      for (int td = 0; td < NDT; ++td) {
+        uint32_t w[4] = {vw[td].x, vw[td].y, vw[td].z, vw[td].w};
 #pragma unroll
-    for (int j = 0; j < 8; j += 2) {
-      const float p0 = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
-      const float p1 = (sv[j + 1] == -INFINITY) ? 0.f : expf(sv[j + 1] - m_new);
-      ps += p0 + p1;
-      pw[j >> 1] = (uint32_t)f2bf(p0) | ((uint32_t)f2bf(p1) << 16);
+        for (int i = 0; i < 4; ++i) {
+          if (2 * i >= nv) w[i] = 0u;
+          else if (2 * i + 1 >= nv) w[i] &= 0xFFFFu;
+        }
+        vw[td] = (uint4){w[0], w[1], w[2], w[3]};
+      }
     }
-    const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, (uint4){pw[0], pw[1], pw[2], pw[3]});
-    ps += __shfl_xor(ps, 16, 64);
-    ps += __shfl_xor(ps, 32, 64);
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
 #pragma unroll
-    for (int t = 0; t < NDT; ++t) {
-      oacc[t] *= alpha;
-      const bf16x8_t va = __builtin_bit_cast(bf16x8_t, *(const uint4 *)&vt[wave][16 * t + rr][8 * g]);
-      oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb, oacc[t], 0, 0, 0);
+    for (int t = 0; t < QT; ++t) {
+      f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+      if (DH >= 32) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[c], qf[t][c], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[c], qf[t][c], s1, 0, 0, 0);
+        }
+      } else {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(b0, qf16[t], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(b1, qf16[t], s1, 0, 0, 0);
+      }
+      // scores of keys kt + 8g + j, j = 0..7, for query 16 t + rr
+      const int my_q = 16 * t + rr, my_last = base + my_q;
+      const bool q_ok = my_q < P;
+      float sv[8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int key = kt + 8 * g + j;
+        const float raw = (j < 4) ? s0[j] : s1[j - 4];
+        const bool ok = q_ok && key < k_end && key <= my_last;
+        sv[j] = ok ? raw * scale : -INFINITY;
+        mx = fmaxf(mx, sv[j]);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run[t], mx);
+      const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run[t] - m_new);
+      float ps = 0.f;
+      uint32_t pw[4];
+#pragma unroll
+      for (int j = 0; j < 8; j += 2) {
+        const float p0 = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
+        const float p1 = (sv[j + 1] == -INFINITY) ? 0.f : expf(sv[j + 1] - m_new);
+        ps += p0 + p1;
+        pw[j >> 1] = (uint32_t)f2bf(p0) | ((uint32_t)f2bf(p1) << 16);
+      }
+      const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, (uint4){pw[0], pw[1], pw[2], pw[3]});
+      ps += __shfl_xor(ps, 16, 64);
+      ps += __shfl_xor(ps, 32, 64);
+      l_run[t] = l_run[t] * alpha + ps;
+      m_run[t] = m_new;
+#pragma unroll
+      for (int td = 0; td < NDT; ++td) {
+        oacc[t][td] *= alpha;
+        oacc[t][td] =
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vw[td]), pb, oacc[t][td], 0, 0, 0);
+      }
     }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   }
-  // merge the four waves: lane (rr, g) holds O^T[16 t + 4 g + i][query rr]
-  if (g == 0) {
-    red_m[wave][rr] = m_run;
-    red_l[wave][rr] = l_run;
+  // merge the four waves: lane (rr, g) holds O^T[16 td + 4 g + i][query 16 t + rr]
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    if (g == 0) {
+      red_m[wave][16 * t + rr] = m_run[t];
+      red_l[wave][16 * t + rr] = l_run[t];
+    }
+#pragma unroll
+    for (int td = 0; td < NDT; ++td)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red_o[wave][16 * td + 4 * g + i][16 * t + rr] = oacc[t][td][i];
   }
-#pragma unroll
-  for (int t = 0; t < NDT; ++t)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) red_o[wave][16 * t + 4 * g + i][rr] = oacc[t][i];
   __syncthreads();
-  for (int idx = threadIdx.x; idx < 16 * DH; idx += 256) {
+  for (int idx = threadIdx.x; idx < NQ * DH; idx += 256) {
     const int qq = idx / DH, j = idx - qq * DH;
-    if (qq >= nq) continue;
+    if (qq >= P) continue;
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < 4; ++w) M = fmaxf(M, red_m[w][qq]);
@@ -560,9 +793,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
       O += red_o[w][j][qq] * f;
     }
     if (splits == 1) {
-      o[(size_t)(b * P + q0 + qq) * d + h * DH + j] = f2bf(L > 0.f ? O / L : 0.f);
+      o[(size_t)(b * P + qq) * d + h * DH + j] = f2bf(L > 0.f ? O / L : 0.f);
     } else {
-      float *pp = part + (((size_t)bh * gridDim.y * 16 + q0 + qq) * splits + split) * (DH + 2);
+      float *pp = part + (((size_t)bh * QT * 16 + qq) * splits + split) * (DH + 2);
       pp[2 + j] = O;
       if (j == 0) {
         pp[0] = M;
@@ -572,107 +805,130 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
   }
 }
 
-// fp32 causal attention on MFMA (v_mfma_f32_16x16x4f32), same work split and
-// permuted S^T rows as the bf16 kernel. One MFMA contracts four k values, one
-// per lane group g: S^T takes d in float4 slices (element e of lane group g is
-// d = 4 g + e), and O^T = V^T P^T runs one MFMA per j = 0..7 over the keys
-// 8 g + j, which are exactly the eight scores each lane holds. V is read
-// straight from memory (16 consecutive d of one key per lane group).
-template <int DH, int ROLE>
+// fp32 causal attention on MFMA (v_mfma_f32_16x16x4f32), same work split,
+// query tiles per workgroup and permuted S^T rows as the bf16 kernel. One
+// MFMA contracts four k values, one per lane group g: S^T takes d in float4
+// slices (element e of lane group g is d = 4 g + e), and O^T = V^T P^T runs
+// one MFMA per j = 0..7 over the keys 8 g + j, which are exactly the eight
+// scores each lane holds. V is read straight from memory (16 consecutive
+// columns of one key per lane group).
+template <int DH, int ROLE, int QT>
 __global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__ q, const float *__restrict__ kc,
                                                        const float *__restrict__ vc, float *__restrict__ o,
                                                        const int32_t *__restrict__ start, int start_off,
                                                        const int32_t *__restrict__ done, int P, int H, int cap,
                                                        int splits, float *__restrict__ part) {
-  constexpr int KT = 32, NDT = DH / 16;
-  __shared__ float red_m[4][16], red_l[4][16];
-  __shared__ float red_o[4][DH][17];
-  const int bh = blockIdx.x, b = bh / H, h = bh - b * H;
-  const int qt = blockIdx.y, q0 = qt * 16, split = blockIdx.z;
+  constexpr int KT = 32, NDT = DH / 16, NQ = 16 * QT;
+  __shared__ float red_m[4][NQ], red_l[4][NQ];
+  __shared__ float red_o[4][DH][NQ + 1];
+  const int bh = blockIdx.x, b = bh / H, h = bh - b * H, split = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, rr = lane & 15, g = lane >> 4;
   const int d = H * DH;
-  const int nq = min(16, P - q0);
   const bool skip = done != nullptr && done[b] != 0;
   const int base = start[b] + start_off;
-  const int n_keys = skip ? 0 : base + q0 + nq;
+  const int n_keys = skip ? 0 : min(base + P, cap);   // never past the cache slab
   int chunk = (n_keys + splits - 1) / splits;
   chunk = (chunk + KT - 1) / KT * KT;
   const int k_begin = split * chunk, k_end = min(n_keys, k_begin + chunk);
   const size_t kvbase = ((size_t)b * H + h) * cap;
   const float scale = 1.f / sqrtf((float)DH);
-  const int my_q = q0 + rr, my_last = base + my_q;
-  const bool q_ok = rr < nq;
-  f32x4_t qf[DH / 16];
+  f32x4_t qf[QT][DH / 16];
 #pragma unroll
-  for (int c = 0; c < DH / 16; ++c)
-    qf[c] = q_ok ? *(const f32x4_t *)(q + (size_t)(b * P + my_q) * d + h * DH + 16 * c + 4 * g)
-                 : (f32x4_t){0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4_t oacc[NDT];
+  for (int t = 0; t < QT; ++t) {
+    const int my_q = 16 * t + rr;
+    const bool q_ok = my_q < P;
+    const float *qp = q + (size_t)(b * P + (q_ok ? my_q : 0)) * d + h * DH;
 #pragma unroll
-  for (int t = 0; t < NDT; ++t) oacc[t] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < DH / 16; ++c)
+      qf[t][c] = q_ok ? *(const f32x4_t *)(qp + 16 * c + 4 * g) : (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  }
+  float m_run[QT], l_run[QT];
+  f32x4_t oacc[QT][NDT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+#pragma unroll
+    for (int td = 0; td < NDT; ++td) oacc[t][td] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  }
   const int krow0 = 8 * (rr >> 2) + (rr & 3), krow1 = krow0 + 4;
   for (int kt = k_begin + wave * KT; kt < k_end; kt += 4 * KT) {
     const size_t r0 = kvbase + min(kt + krow0, cap - 1), r1 = kvbase + min(kt + krow1, cap - 1);
-    f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t a0[DH / 16], a1[DH / 16];
 #pragma unroll
     for (int c = 0; c < DH / 16; ++c) {
-      const f32x4_t a0 = *(const f32x4_t *)(kc + r0 * DH + 16 * c + 4 * g);
-      const f32x4_t a1 = *(const f32x4_t *)(kc + r1 * DH + 16 * c + 4 * g);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[e], qf[c][e], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[e], qf[c][e], s1, 0, 0, 0);
-      }
+      a0[c] = *(const f32x4_t *)(kc + r0 * DH + 16 * c + 4 * g);
+      a1[c] = *(const f32x4_t *)(kc + r1 * DH + 16 * c + 4 * g);
     }
-    float sv[8];
-    float mx = -INFINITY;
+    // value column 16 td + rr of keys kt + 8 g + j (zero past the key range)
+    float vv[NDT][8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int key = kt + 8 * g + j;
-      const float raw = (j < 4) ? s0[j] : s1[j - 4];
-      const bool ok = q_ok && key < k_end && key <= my_last;
-      sv[j] = ok ? raw * scale : -INFINITY;
-      mx = fmaxf(mx, sv[j]);
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
-    float pv[8], ps = 0.f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      pv[j] = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
-      ps += pv[j];
-    }
-    ps += __shfl_xor(ps, 16, 64);
-    ps += __shfl_xor(ps, 32, 64);
-    l_run = l_run * alpha + ps;
-    m_run = m_new;
-#pragma unroll
-    for (int t = 0; t < NDT; ++t) {
-      oacc[t] *= alpha;
+    for (int td = 0; td < NDT; ++td)
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        // key kt + 8 g + j, value column 16 t + rr (zero past the key range)
         const int key = kt + 8 * g + j;
-        const float v = (key < k_end) ? vc[(kvbase + key) * DH + 16 * t + rr] : 0.f;
-        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(v, pv[j], oacc[t], 0, 0, 0);
+        vv[td][j] = (key < k_end) ? vc[(kvbase + key) * DH + 16 * td + rr] : 0.f;
+      }
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < DH / 16; ++c)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[c][e], qf[t][c][e], s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[c][e], qf[t][c][e], s1, 0, 0, 0);
+        }
+      const int my_q = 16 * t + rr, my_last = base + my_q;
+      const bool q_ok = my_q < P;
+      float sv[8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int key = kt + 8 * g + j;
+        const float raw = (j < 4) ? s0[j] : s1[j - 4];
+        const bool ok = q_ok && key < k_end && key <= my_last;
+        sv[j] = ok ? raw * scale : -INFINITY;
+        mx = fmaxf(mx, sv[j]);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run[t], mx);
+      const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run[t] - m_new);
+      float pv[8], ps = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        pv[j] = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
+        ps += pv[j];
+      }
+      ps += __shfl_xor(ps, 16, 64);
+      ps += __shfl_xor(ps, 32, 64);
+      l_run[t] = l_run[t] * alpha + ps;
+      m_run[t] = m_new;
+#pragma unroll
+      for (int td = 0; td < NDT; ++td) {
+        oacc[t][td] *= alpha;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          oacc[t][td] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv[td][j], pv[j], oacc[t][td], 0, 0, 0);
       }
     }
   }
-  if (g == 0) {
-    red_m[wave][rr] = m_run;
-    red_l[wave][rr] = l_run;
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    if (g == 0) {
+      red_m[wave][16 * t + rr] = m_run[t];
+      red_l[wave][16 * t + rr] = l_run[t];
+    }
+#pragma unroll
+    for (int td = 0; td < NDT; ++td)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red_o[wave][16 * td + 4 * g + i][16 * t + rr] = oacc[t][td][i];
   }
-#pragma unroll
-  for (int t = 0; t < NDT; ++t)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) red_o[wave][16 * t + 4 * g + i][rr] = oacc[t][i];
   __syncthreads();
-  for (int idx = threadIdx.x; idx < 16 * DH; idx += 256) {
+  for (int idx = threadIdx.x; idx < NQ * DH; idx += 256) {
     const int qq = idx / DH, j = idx - qq * DH;
-    if (qq >= nq) continue;
+    if (qq >= P) continue;
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < 4; ++w) M = fmaxf(M, red_m[w][qq]);
@@ -684,9 +940,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__
       O += red_o[w][j][qq] * f;
     }
     if (splits == 1) {
-      o[(size_t)(b * P + q0 + qq) * d + h * DH + j] = L > 0.f ? O / L : 0.f;
+      o[(size_t)(b * P + qq) * d + h * DH + j] = L > 0.f ? O / L : 0.f;
     } else {
-      float *pp = part + (((size_t)bh * gridDim.y * 16 + q0 + qq) * splits + split) * (DH + 2);
+      float *pp = part + (((size_t)bh * QT * 16 + qq) * splits + split) * (DH + 2);
       pp[2 + j] = O;
       if (j == 0) {
         pp[0] = M;
@@ -933,7 +1189,7 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
   const float scale = 1.f / sqrtf((float)DH);
   for (int pair = wave; pair < P * H; pair += 4) {
     const int p = pair / H, h = pair - p * H;
-    const int last = pos0 + p;
+    const int last = min(pos0 + p, cap - 1);   // never past the cache slab
     float q[DH];
 #pragma unroll
     for (int j = 0; j < DH; ++j) q[j] = qs[p * d + h * DH + j] * scale;
@@ -971,14 +1227,8 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
         if (k0 + u > last) break;
         const float pv = expf(sc[u] - mn);
         l += pv;
-        const ELT *vr = vc + (row0 + k0 + u) * DH;
 #pragma unroll
-        for (int c = 0; c < DH / 8; ++c) {
-          float w[8];
-          load8(vr + 8 * c, w);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) o[8 * c + e] += pv * w[e];
-        }
+        for (int j = 0; j < DH; ++j) o[j] += pv * ld(vc, v_at<ELT>(row0, k0 + u, j, DH));
       }
       m = mn;
     }
@@ -1050,8 +1300,9 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
           qs[p * d + c] = v;
         } else {
           const int h = c / DH, j = c - h * DH, pos = pos0 + p;
+          const size_t row0 = seq_row0 + (size_t)h * a.cap;
           if (pos < a.cap)
-            st(which == 1 ? kc : vc, (seq_row0 + (size_t)h * a.cap + pos) * DH + j, v);
+            st(which == 1 ? kc : vc, which == 1 ? (row0 + pos) * DH + j : v_at<ELT>(row0, pos, j, DH), v);
           else
             atomicOr(a.status, TPPSD_STATUS_CAPACITY);
         }
@@ -1362,26 +1613,46 @@ void launch_layernorm(const float *x, void *y, int bf16, const float *g, const f
     k_layernorm<float><<<blocks, 256, 0, s>>>(x, (float *)y, g, b, T, d);
 }
 
+bool gemm_ln_fusable(int bf16, int K) {
+  return K <= GEMM_LN_MAX_DEPTH * (bf16 ? gemm_bk<bf16_t>() : gemm_bk<float>());
+}
+
 template <typename ELT>
-static void gemm_dispatch(const void *X, const void *W, int T, int N, int K, const Epi &epi, hipStream_t s) {
-  // 64x64 tiles when they already give the chip a few hundred workgroups,
-  // 32x32 tiles otherwise (small row counts of draft and AR steps)
-  const long big = (long)((N + 63) / 64) * ((T + 63) / 64);
+static void gemm_dispatch(const void *X, const LnA *ln, const void *W, int T, int N, int K, const Epi &epi,
+                          hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const ELT *x = (const ELT *)X, *w = (const ELT *)W;
-  if (big >= 512) {
-    dim3 grid((N + 63) / 64, (T + 63) / 64);
-    k_gemm_mfma<ELT, 2, 2><<<grid, 256, 0, s>>>(x, w, T, N, K, epi);
+  const float *xf = ln ? ln->x : nullptr, *lg = ln ? ln->g : nullptr, *lb = ln ? ln->b : nullptr;
+  // 64 x 64 tiles when they give the chip a few hundred workgroups, 32 x 32
+  // otherwise (the B rows of draft and AR steps)
+  const bool big = (long)((N + 63) / 64) * ((T + 63) / 64) >= 256;
+  auto go = [&](auto kern, int bm, int bn) {
+    dim3 grid((N + bn - 1) / bn, (T + bm - 1) / bm);
+    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, x, xf, lg, lb, w, T, N, K, epi);
+  };
+  if (!ln) {
+    if (big) go(k_gemm_lds<ELT, 64, 64, false, 2>, 64, 64);
+    else go(k_gemm_lds<ELT, 32, 32, false, 2>, 32, 32);
+    return;
+  }
+  // LayerNorm operand: the ring holds all of K (depth 2, 4 or 8 stages)
+  const int nst = (K + gemm_bk<ELT>() - 1) / gemm_bk<ELT>();
+  if (nst <= 2) {
+    if (big) go(k_gemm_lds<ELT, 64, 64, true, 2>, 64, 64);
+    else go(k_gemm_lds<ELT, 32, 32, true, 2>, 32, 32);
+  } else if (nst <= 4) {
+    if (big) go(k_gemm_lds<ELT, 64, 64, true, 4>, 64, 64);
+    else go(k_gemm_lds<ELT, 32, 32, true, 4>, 32, 32);
   } else {
-    dim3 grid((N + 31) / 32, (T + 31) / 32);
-    k_gemm_mfma<ELT, 1, 1><<<grid, 256, 0, s>>>(x, w, T, N, K, epi);
+    go(k_gemm_lds<ELT, 32, 32, true, 8>, 32, 32);
   }
 }
 
-void launch_gemm(const void *X, const void *W, int bf16, int T, int N, int K, const Epi &epi, hipStream_t s) {
+void launch_gemm(const void *X, const LnA *ln, const void *W, int bf16, int T, int N, int K, const Epi &epi,
+                 hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if (bf16)
-    gemm_dispatch<bf16_t>(X, W, T, N, K, epi, s);
+    gemm_dispatch<bf16_t>(X, ln, W, T, N, K, epi, s, ev0, ev1);
   else
-    gemm_dispatch<float>(X, W, T, N, K, epi, s);
+    gemm_dispatch<float>(X, ln, W, T, N, K, epi, s, ev0, ev1);
 }
 
 // ev0/ev1 (optional): HIP events stamped with the main kernel's own start and
@@ -1403,33 +1674,32 @@ static void attn_dispatch(const void *q, const void *kc, const void *vc, void *o
   }
 }
 
-template <int DH, int ROLE>
-static void attn_mfma(const bf16_t *Q, const bf16_t *Kc, const bf16_t *Vc, bf16_t *O, const int32_t *start,
-                      int start_off, const int32_t *done, int B, int P, int H, int cap, float *part,
-                      hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+// All query tiles of a (sequence, head) share one workgroup (QT = 1..3 for
+// up to 48 new positions); the key range is split across workgroups when the
+// (sequence, head) pairs alone do not fill the chip.
+template <typename ACT, int DH, int ROLE>
+static void attn_mfma(const ACT *Q, const ACT *Kc, const ACT *Vc, ACT *O, const int32_t *start, int start_off,
+                      const int32_t *done, int B, int P, int H, int cap, float *part, hipEvent_t ev0,
+                      hipEvent_t ev1, hipStream_t s) {
   const int qtiles = (P + 15) / 16;
-  const int splits = attn_splits(B, H, qtiles, cap);
-  dim3 grid(B * H, qtiles, splits);
-  hipExtLaunchKernelGGL(k_attn_mfma<DH, ROLE>, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off,
-                        done, P, H, cap, splits, part);
-  if (splits > 1) {
-    const int total = B * H * P * DH;
-    k_attn_combine<bf16_t, DH><<<(total + 255) / 256, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
+  const int splits = attn_splits(B, H, cap);
+  dim3 grid(B * H, 1, splits);
+  auto go = [&](auto kern) {
+    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap,
+                          splits, part);
+  };
+  if constexpr (sizeof(ACT) == 2) {
+    if (qtiles == 1) go(k_attn_mfma<DH, ROLE, 1>);
+    else if (qtiles == 2) go(k_attn_mfma<DH, ROLE, 2>);
+    else go(k_attn_mfma<DH, ROLE, 3>);
+  } else {
+    if (qtiles == 1) go(k_attn_mfma_f32<DH, ROLE, 1>);
+    else if (qtiles == 2) go(k_attn_mfma_f32<DH, ROLE, 2>);
+    else go(k_attn_mfma_f32<DH, ROLE, 3>);
   }
-}
-
-template <int DH, int ROLE>
-static void attn_mfma_f32(const float *Q, const float *Kc, const float *Vc, float *O, const int32_t *start,
-                          int start_off, const int32_t *done, int B, int P, int H, int cap, float *part,
-                          hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  const int qtiles = (P + 15) / 16;
-  const int splits = attn_splits(B, H, qtiles, cap);
-  dim3 grid(B * H, qtiles, splits);
-  hipExtLaunchKernelGGL(k_attn_mfma_f32<DH, ROLE>, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start,
-                        start_off, done, P, H, cap, splits, part);
   if (splits > 1) {
     const int total = B * H * P * DH;
-    k_attn_combine<float, DH><<<(total + 255) / 256, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
+    k_attn_combine<ACT, DH><<<(total + 255) / 256, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
   }
 }
 
@@ -1449,9 +1719,9 @@ static void attention_role(const void *q, const void *kc, const void *vc, void *
     const float *Q = (const float *)q, *Kc = (const float *)kc, *Vc = (const float *)vc;
     float *O = (float *)o;
     switch (dh) {
-      case 16: attn_mfma_f32<16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
-      case 32: attn_mfma_f32<32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
-      default: attn_mfma_f32<64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+      case 16: attn_mfma<float, 16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+      case 32: attn_mfma<float, 32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+      default: attn_mfma<float, 64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
     }
     return;
   }
@@ -1462,9 +1732,9 @@ static void attention_role(const void *q, const void *kc, const void *vc, void *
   const bf16_t *Q = (const bf16_t *)q, *Kc = (const bf16_t *)kc, *Vc = (const bf16_t *)vc;
   bf16_t *O = (bf16_t *)o;
   switch (dh) {
-    case 16: attn_mfma<16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
-    case 32: attn_mfma<32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
-    default: attn_mfma<64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+    case 16: attn_mfma<bf16_t, 16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+    case 32: attn_mfma<bf16_t, 32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+    default: attn_mfma<bf16_t, 64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
   }
 }
 

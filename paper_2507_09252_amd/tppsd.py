@@ -40,6 +40,16 @@ class TppsdError(RuntimeError):
         self.code = code
 
 
+TIME_KERNELS = 1   # TPPSD_TIME_KERNELS
+TIME_PHASES = 2    # TPPSD_TIME_PHASES
+
+
+class TimingC(ctypes.Structure):
+    _fields_ = [("attn_ms", c_double), ("attn_launches", c_int64), ("gemm_ms", c_double),
+                ("gemm_launches", c_int64), ("gemm_flop", c_double), ("draft_ms", c_double),
+                ("verify_ms", c_double), ("accept_ms", c_double), ("rounds", c_int64)]
+
+
 class ModelCfgC(ctypes.Structure):
     _fields_ = [(n, c_int32) for n in ("n_layers", "d_model", "n_heads", "d_ffn", "n_mix", "n_types", "prec")]
 
@@ -87,7 +97,7 @@ def lib():
         "tppsd_read_events": (c_int, [c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
         "tppsd_state_status": (c_int, [c_void_p, c_void_p, P(c_uint32), P(c_int32), P(c_int64), P(c_int64), P(c_int64)]),
         "tppsd_timing_enable": (c_int, [c_void_p, c_int]),
-        "tppsd_timing_read": (c_int, [c_void_p, P(c_double), P(c_int64)]),
+        "tppsd_timing_read": (c_int, [c_void_p, P(TimingC)]),
         "tppsd_last_error": (c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -282,10 +292,11 @@ class State:
                                         ctypes.byref(acc), ctypes.byref(dr), ctypes.byref(ar)))
         return dict(bits=bits.value, n_done=nd.value, accepted=acc.value, drafted=dr.value, ar_candidates=ar.value)
 
-    def tppsd_timing_enable(self, enable: bool = True):
-        _check(lib().tppsd_timing_enable(self.handle, int(enable)))
+    def tppsd_timing_enable(self, modes: int):
+        """modes: 0 (off), TIME_KERNELS or TIME_PHASES."""
+        _check(lib().tppsd_timing_enable(self.handle, int(modes)))
 
     def tppsd_timing_read(self):
-        ms, n = c_double(), c_int64()
-        _check(lib().tppsd_timing_read(self.handle, ctypes.byref(ms), ctypes.byref(n)))
-        return ms.value, n.value
+        t = TimingC()
+        _check(lib().tppsd_timing_read(self.handle, ctypes.byref(t)))
+        return {name: getattr(t, name) for name, _ in TimingC._fields_}
