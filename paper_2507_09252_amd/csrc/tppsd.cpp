@@ -759,7 +759,10 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
     // (and while contexts stay short: its attention streams each (sequence,
     // head)'s keys with one wave)
     s->fused_draft = D && B <= 1024 && max_events <= 2048 &&
-                     fused_draft_ok(D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn) && !(nf && nf[0] == '1');
+                     fused_draft_ok(D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn) &&
+                     fused_draft_lds_bytes(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
+                                           D->H()) <= 64 * 1024 &&
+                     !(nf && nf[0] == '1');
   }
   if (hipHostMalloc((void **)&s->host_ndone, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&s->poll_ev[0], hipEventDisableTiming) != hipSuccess ||

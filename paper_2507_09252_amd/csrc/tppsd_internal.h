@@ -123,11 +123,16 @@ struct DraftArgs {
   int32_t *d_k;
   int MG;                   // row stride of the draft record (max_gamma)
 };
-// whether the fused draft kernel supports a model of these sizes
+// whether the fused draft kernel supports a model of these sizes: the
+// matrix-vector products need d / 8 and d_ffn / 8 to be powers of two <= 64,
+// the attention a power-of-two head count and d_head = 16 (a thread holds a
+// whole 8-position block of keys and values in registers)
 inline bool fused_draft_ok(int L, int d, int H, int F) {
-  return L <= FD_MAX_LAYERS && d <= 256 && F <= 2048 && d / H <= 64;
+  auto pow2 = [](int v) { return v > 0 && (v & (v - 1)) == 0; };
+  return L <= FD_MAX_LAYERS && d % 8 == 0 && F % 8 == 0 && pow2(d / 8) && pow2(F / 8) && d / 8 <= 64 &&
+         F / 8 <= 64 && pow2(H) && d == 16 * H;
 }
-size_t fused_draft_lds_bytes(int d, int F, int M, int K);
+size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H);
 
 // ---- launchers (tppsd_kernels.hip) ----
 void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t st);

@@ -54,15 +54,46 @@ template <> __device__ __forceinline__ size_t v_at<bf16_t>(size_t row0, int pos,
   return row0 * dh + (size_t)(pos >> 3) * (8 * dh) + j * 8 + (pos & 7);
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+// Cross-lane moves: DPP within rows of 16 lanes (quad permutes, row
+// rotations), LDS swizzles (xor masks within 32 lanes) and one bpermute for
+// lane ^ 32. The whole wave must be active.
+template <int CTRL> __device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int XOR> __device__ __forceinline__ float swz_xor(float v) {
+  static_assert(XOR < 32, "swizzle reaches 32 lanes");
+  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), (XOR << 10) | 0x1F));
+}
+// sum / max over aligned groups of `width` lanes (a power of two <= 64),
+// left in every lane of the group
+__device__ __forceinline__ float group_sum(float v, int width) {
+  if (width >= 2) v += dpp_mov<0xB1>(v);   // quad_perm(1, 0, 3, 2): lane ^ 1
+  if (width >= 4) v += dpp_mov<0x4E>(v);   // quad_perm(2, 3, 0, 1): lane ^ 2
+  if (width >= 8) v += swz_xor<4>(v);
+  if (width >= 16) v += swz_xor<8>(v);
+  if (width >= 32) v += swz_xor<16>(v);
+  if (width >= 64) v += __shfl_xor(v, 32, 64);
   return v;
 }
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_mov<0xB1>(v);
+  v += dpp_mov<0x4E>(v);
+  v += dpp_mov<0x124>(v);   // row_ror:4
+  v += dpp_mov<0x128>(v);   // row_ror:8 -> every lane holds its row's sum
+  return (__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+          __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16))) +
+         (__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
+          __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48)));
+}
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = fmaxf(v, dpp_mov<0xB1>(v));
+  v = fmaxf(v, dpp_mov<0x4E>(v));
+  v = fmaxf(v, dpp_mov<0x124>(v));
+  v = fmaxf(v, dpp_mov<0x128>(v));
+  return fmaxf(fmaxf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)),
+                     __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16))),
+               fmaxf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)),
+                     __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48))));
 }
 
 // ---------------------------------------------------------------------------
@@ -130,6 +161,32 @@ __device__ int sample_cat(const float *logp, int n, float u) {
     if (x < c) return m;
   }
   return n - 1;
+}
+
+// Wave-parallel forms of the two helpers above for n, M <= 64 (lane m holds
+// entry m): the running sum is an inclusive scan across the wave.
+__device__ int wave_sample_cat(const float *logp, int n, float u) {
+  const int lane = threadIdx.x & 63;
+  float c = lane < n ? expf(logp[lane]) : 0.f;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float o = __shfl_up(c, off, 64);
+    if (lane >= off) c += o;
+  }
+  const float tot = __shfl(c, n - 1, 64);
+  const unsigned long long hit = __ballot(lane < n && u * tot < c);
+  return hit ? (int)__builtin_ctzll(hit) : n - 1;
+}
+__device__ float wave_mix_logpdf(const float *logw, const float *mu, const float *s, int M, float tau) {
+  const int lane = threadIdx.x & 63;
+  const float lt = logf(tau);
+  float c = -INFINITY;
+  if (lane < M) {
+    const float z = lt - mu[lane];
+    c = logw[lane] - s[lane] - 0.918938533204672742f - lt - 0.5f * z * z * expf(-2.f * s[lane]);
+  }
+  const float mx = wave_max(c);
+  return mx + logf(wave_sum(lane < M ? expf(c - mx) : 0.f));
 }
 
 // z ~ Categorical(w), eps = Box-Muller(u1, u2), tau = exp(mu_z + sigma_z eps)
@@ -1123,43 +1180,41 @@ template <> __device__ __forceinline__ void load8<bf16_t>(const bf16_t *p, float
   }
 }
 
-// y[p][n] = sum_k in[p * in_stride + k] W[n * K + k] for n < N, p < P (P <= 2),
-// handed to epi(p, n, y) by one lane. Lanes split each row into 8-element
-// chunks (lpo lanes per output, a power of two) and reduce with shuffles.
-template <typename ELT, typename EPI>
-__device__ void wg_gemv(const ELT *__restrict__ W, int N, int K, const float *in, int in_stride, int P, EPI epi) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int chunks = K >> 3;
-  int lpo = 1;
-  while (lpo < chunks && lpo < 64) lpo <<= 1;
-  const int opw = 64 / lpo, sub = lane & (lpo - 1), slot = lane / lpo;
-  for (int n0 = 0; n0 < N; n0 += 4 * opw) {
-    const int n = n0 + wave * opw + slot;
-    float acc0 = 0.f, acc1 = 0.f;
-    if (n < N) {
-      for (int c = sub; c < chunks; c += lpo) {
-        float w[8];
-        load8(W + (size_t)n * K + 8 * c, w);
-        const float *x0 = in + 8 * c;
+// y[p][n] = sum_k W(n)[k] X(n, p)[k] for n < N, p < P (P <= 2), handed to
+// epi(p, n, y) by one lane. K is cut into 8-element chunks; a row's chunks
+// are shared by LPR adjacent lanes (a power of two), CPL = K / (8 LPR) <= 8
+// chunks each, loaded together before any is used, so a product costs about
+// one memory latency plus a few lane-group additions. wrow(n) gives row n of
+// W, xrow(n, p) the input that row n reads.
+template <typename ELT, int CPL, typename WF, typename XF, typename EPI>
+__device__ void wg_gemv_cpl(int N, int K, int P, WF wrow, XF xrow, EPI epi) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int lpr = (K >> 3) / CPL, rows = nt / lpr;
+  const int sub = tid % lpr;
+  for (int r0 = 0; r0 < N; r0 += rows) {
+    const int n = r0 + tid / lpr, nn = min(n, N - 1);
+    const ELT *wr = wrow(nn);
+    float w[CPL][8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc0 += w[e] * x0[e];
-        if (P > 1) {
-          const float *x1 = in + in_stride + 8 * c;
+    for (int c = 0; c < CPL; ++c) load8(wr + 8 * (sub + lpr * c), w[c]);
+    float acc[2] = {0.f, 0.f};
+    for (int p = 0; p < P; ++p) {
+      const float *x = xrow(nn, p);
+      float a = 0.f;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc1 += w[e] * x1[e];
-        }
+      for (int c = 0; c < CPL; ++c) {
+        const float *xc = x + 8 * (sub + lpr * c);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) a += w[c][e] * xc[e];
       }
+      acc[p] = group_sum(a, lpr);
     }
-    for (int off = lpo >> 1; off > 0; off >>= 1) {
-      acc0 += __shfl_xor(acc0, off, 64);
-      acc1 += __shfl_xor(acc1, off, 64);
-    }
-    if (n < N && sub == 0) {
-      epi(0, n, acc0);
-      if (P > 1) epi(1, n, acc1);
-    }
+    if (n < N && sub == 0)
+      for (int p = 0; p < P; ++p) epi(p, n, acc[p]);
   }
 }
+// chunks per lane for a K-wide product (K / 8 a power of two)
+constexpr int gemv_cpl(int K) { return (K >> 3) < 8 ? (K >> 3) : 8; }
 
 // LayerNorm of P <= 4 rows of x (stride d) into y (stride d), wave p per row
 template <typename ELT>
@@ -1179,78 +1234,186 @@ __device__ void wg_layernorm(const float *x, float *y, const float *g, const flo
   for (int j = lane; j < d; j += 64) y[wave * d + j] = rnd_act<ELT>((xr[j] - mean) * rstd * g[j] + bt[j]);
 }
 
-// causal attention of P <= 2 new queries over the cache: one wave per
-// (query, head) pair, lanes over keys with their own online softmax, merged
-// across the wave. Query p sees cached positions 0 .. pos0 + p.
+// One 32-key step of the draft attention's MFMA formulation (d_head = 16),
+// the fragments of lane (rr, g): the permuted key rows krow0 / krow1 of S^T
+// and the values of keys kt + 8 g .. + 7 in value column rr. Loads are
+// unconditional (positions clamped into the slab) and positions at or past
+// n_keys are zeroed afterwards.
+template <typename ELT> struct DraftStep;
+template <> struct DraftStep<bf16_t> {
+  short4_t k0, k1;
+  uint4 v;
+  __device__ void load(const bf16_t *kc, const bf16_t *vc, size_t row0, int kt, int n_keys, int krow0, int rr,
+                       int g) {
+    k0 = *(const short4_t *)(kc + (row0 + min(kt + krow0, n_keys - 1)) * 16 + 4 * g);
+    k1 = *(const short4_t *)(kc + (row0 + min(kt + krow0 + 4, n_keys - 1)) * 16 + 4 * g);
+    const int k8 = kt + 8 * g, nv = n_keys - k8;
+    v = *(const uint4 *)(vc + v_at<bf16_t>(row0, min(k8, n_keys - 1) & ~7, rr, 16));
+    uint32_t mk[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mk[i] = (2 * i >= nv) ? 0u : (2 * i + 1 >= nv) ? 0xFFFFu : 0xFFFFFFFFu;
+    v = make_uint4(v.x & mk[0], v.y & mk[1], v.z & mk[2], v.w & mk[3]);
+  }
+};
+template <> struct DraftStep<float> {
+  f32x4_t k0, k1;
+  float v[8];
+  __device__ void load(const float *kc, const float *vc, size_t row0, int kt, int n_keys, int krow0, int rr,
+                       int g) {
+    k0 = *(const f32x4_t *)(kc + (row0 + min(kt + krow0, n_keys - 1)) * 16 + 4 * g);
+    k1 = *(const f32x4_t *)(kc + (row0 + min(kt + krow0 + 4, n_keys - 1)) * 16 + 4 * g);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = vc[(row0 + min(kt + 8 * g + j, n_keys - 1)) * 16 + rr];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = (kt + 8 * g + j < n_keys) ? v[j] : 0.f;
+  }
+};
+
+// causal attention of P <= 2 new queries (positions pos0 .. pos0 + P - 1,
+// already in the cache) over one sequence's cache, d_head = 16, on MFMA in
+// the layout of k_attn_mfma: S^T = K Q^T with permuted key rows leaves lane
+// (rr, g) the scores of query rr for keys 8 g .. + 7, the B operand of
+// O^T = V^T P^T (queries P .. 15 of the tile are zero). Each head is served
+// by 4 / H waves (one wave per head from H = 4; more heads loop), which take
+// 32-key steps round robin; a wave loads a batch of steps (8 bf16, 4 fp32)
+// before computing any.
+// The waves of a head merge through LDS. red: LDS scratch of
+// max(4, H) * 2 * 18 floats.
 template <typename ELT, int DH>
 __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
-                             int H, int P, int pos0, int d) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const float scale = 1.f / sqrtf((float)DH);
-  for (int pair = wave; pair < P * H; pair += 4) {
-    const int p = pair / H, h = pair - p * H;
-    const int last = min(pos0 + p, cap - 1);   // never past the cache slab
-    float q[DH];
-#pragma unroll
-    for (int j = 0; j < DH; ++j) q[j] = qs[p * d + h * DH + j] * scale;
-    float m = -INFINITY, l = 0.f, o[DH];
-#pragma unroll
-    for (int j = 0; j < DH; ++j) o[j] = 0.f;
+                             int H, int P, int pos0, int d, float *red) {
+  static_assert(DH == 16, "the fused draft attention serves d_head = 16");
+  constexpr int KT = 32, NB = 4;   // steps per load batch
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rr = lane & 15, g = lane >> 4;
+  const int wph = H >= 4 ? 1 : 4 / H, wsub = wave % wph;
+  const int n_keys = min(pos0 + P, cap);
+  const float scale = 0.25f;   // 1 / sqrt(16)
+  const int krow0 = 8 * (rr >> 2) + (rr & 3);
+  for (int h = wave / wph; h < H; h += 4 / wph) {
     const size_t row0 = seq_row0 + (size_t)h * cap;
-    // U keys per lane per pass: their loads are issued together
-    constexpr int U = DH <= 32 ? 4 : 2;
-    for (int k0 = lane * U; k0 <= last; k0 += 64 * U) {
-      float sc[U];
+    // query fragment: dims 4 g .. + 3 of query rr (zero for rr >= P)
+    const float *qp = qs + min(rr, P - 1) * d + h * DH + 4 * g;
+    const float q0 = rr < P ? qp[0] : 0.f, q1 = rr < P ? qp[1] : 0.f, q2 = rr < P ? qp[2] : 0.f,
+                q3 = rr < P ? qp[3] : 0.f;
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4_t oacc = {0.f, 0.f, 0.f, 0.f};
+    for (int kb = wsub * KT; kb < n_keys; kb += NB * wph * KT) {
+      DraftStep<ELT> f[NB];
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int key = min(k0 + u, last);
-        const ELT *kr = kc + (row0 + key) * DH;
-        float a = 0.f;
+      for (int sidx = 0; sidx < NB; ++sidx)
+        f[sidx].load(kc, vc, row0, min(kb + sidx * wph * KT, n_keys - 1) & ~(KT - 1), n_keys, krow0, rr, g);
+      // scores of the whole batch first, then one online-softmax update
+      // (steps past the key range score -inf; their values were zeroed)
+      float sv[NB][8];
+      float mx = -INFINITY;
 #pragma unroll
-        for (int c = 0; c < DH / 8; ++c) {
-          float w[8];
-          load8(kr + 8 * c, w);
+      for (int sidx = 0; sidx < NB; ++sidx) {
+        const int kt = kb + sidx * wph * KT;
+        if (kt >= n_keys) {   // uniform across the wave
 #pragma unroll
-          for (int e = 0; e < 8; ++e) a += q[8 * c + e] * w[e];
+          for (int j = 0; j < 8; ++j) sv[sidx][j] = -INFINITY;
+          continue;
         }
-        sc[u] = (k0 + u <= last) ? a : -INFINITY;
+        f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (sizeof(ELT) == 2) {
+          const uint32_t w0 = (uint32_t)f2bf(q0) | ((uint32_t)f2bf(q1) << 16);
+          const uint32_t w1 = (uint32_t)f2bf(q2) | ((uint32_t)f2bf(q3) << 16);
+          const short4_t qf = __builtin_bit_cast(short4_t, make_uint2(w0, w1));
+          s0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(f[sidx].k0, qf, s0, 0, 0, 0);
+          s1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(f[sidx].k1, qf, s1, 0, 0, 0);
+        } else {
+          const float qv[4] = {q0, q1, q2, q3};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(f[sidx].k0[e], qv[e], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(f[sidx].k1[e], qv[e], s1, 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int key = kt + 8 * g + j;
+          const float raw = (j < 4) ? s0[j] : s1[j - 4];
+          sv[sidx][j] = (rr < P && key < n_keys && key <= pos0 + rr) ? raw * scale : -INFINITY;
+          mx = fmaxf(mx, sv[sidx][j]);
+        }
       }
-      float mn = m;
+      mx = fmaxf(mx, swz_xor<16>(mx));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
+      float ps = 0.f;
 #pragma unroll
-      for (int u = 0; u < U; ++u) mn = fmaxf(mn, sc[u]);
-      const float corr = expf(m - mn);
-      l *= corr;
+      for (int sidx = 0; sidx < NB; ++sidx)
 #pragma unroll
-      for (int j = 0; j < DH; ++j) o[j] *= corr;
+        for (int j = 0; j < 8; ++j) {
+          sv[sidx][j] = (sv[sidx][j] == -INFINITY) ? 0.f : expf(sv[sidx][j] - m_new);
+          ps += sv[sidx][j];
+        }
+      ps += swz_xor<16>(ps);
+      ps += __shfl_xor(ps, 32, 64);
+      l_run = l_run * alpha + ps;
+      m_run = m_new;
+      oacc *= alpha;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (k0 + u > last) break;
-        const float pv = expf(sc[u] - mn);
-        l += pv;
+      for (int sidx = 0; sidx < NB; ++sidx) {
+        if (kb + sidx * wph * KT >= n_keys) break;   // uniform across the wave
+        if constexpr (sizeof(ELT) == 2) {
+          uint32_t pw[4];
 #pragma unroll
-        for (int j = 0; j < DH; ++j) o[j] += pv * ld(vc, v_at<ELT>(row0, k0 + u, j, DH));
+          for (int j = 0; j < 8; j += 2)
+            pw[j >> 1] = (uint32_t)f2bf(sv[sidx][j]) | ((uint32_t)f2bf(sv[sidx][j + 1]) << 16);
+          const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+          oacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, f[sidx].v), pb, oacc, 0, 0, 0);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            oacc = __builtin_amdgcn_mfma_f32_16x16x4f32(f[sidx].v[j], sv[sidx][j], oacc, 0, 0, 0);
+        }
       }
-      m = mn;
     }
-    const float M = wave_max(m);
-    const float f = (m == -INFINITY) ? 0.f : expf(m - M);
-    const float L = wave_sum(l * f);
-    float mine = 0.f;
+    // lane (rr, g) holds O^T[4 g + i][query rr]
+    if (rr < P) {
+      float *r = red + ((h * wph + wsub) * 2 + rr) * (DH + 2);
+      if (g == 0) {
+        r[0] = m_run;
+        r[1] = l_run;
+      }
 #pragma unroll
-    for (int j = 0; j < DH; ++j) {
-      const float t = wave_sum(o[j] * f);
-      if (lane == j) mine = t;
+      for (int i = 0; i < 4; ++i) r[2 + 4 * g + i] = oacc[i];
     }
-    if (lane < DH) os[p * d + h * DH + lane] = rnd_act<ELT>(mine / L);
+  }
+  __syncthreads();
+  for (int idx = tid; idx < P * H * DH; idx += blockDim.x) {
+    const int p = idx / (H * DH), rest = idx - p * H * DH, hh = rest / DH, j = rest - hh * DH;
+    float M = -INFINITY;
+    for (int w = 0; w < wph; ++w) M = fmaxf(M, red[((hh * wph + w) * 2 + p) * (DH + 2)]);
+    float L = 0.f, O = 0.f;
+    for (int w = 0; w < wph; ++w) {
+      const float *r = red + ((hh * wph + w) * 2 + p) * (DH + 2);
+      const float f = (r[0] == -INFINITY) ? 0.f : expf(r[0] - M);
+      L += r[1] * f;
+      O += r[2 + j] * f;
+    }
+    os[p * d + hh * DH + j] = rnd_act<ELT>(L > 0.f ? O / L : 0.f);
   }
 }
 
-size_t fused_draft_lds_bytes(int d, int F, int M, int K) {
-  const int Fm = d > F ? d : F;
-  return (size_t)(2 * d + 2 * Fm + 2 * d + 2 * d + 2 * F + 4 * d + 3 * M + K + 8) * sizeof(float);
+// floats of the model's small fp32 vectors (LayerNorm gains and biases,
+// linear biases, time-encoding frequencies) staged in LDS by the fused draft
+inline __host__ __device__ int fused_draft_vec_floats(int L, int d, int F, int M, int K) {
+  return L * (9 * d + F) + 4 * d + 3 * M + K;
 }
 
-template <typename ELT, int DH>
+size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H) {
+  const int Fm = d > F ? d : F, dh = d / H;
+  return (size_t)(2 * d + 2 * Fm + 2 * d + 2 * d + 2 * F + 4 * d + 3 * M + K + 8 + 4 * H * 2 * (dh + 2) +
+                  fused_draft_vec_floats(L, d, F, M, K)) *
+         sizeof(float);
+}
+
+// CD / CF: chunks per lane of the matrix-vector products over d and over
+// d_ffn (gemv_cpl), fixed per model so that each product has one code path
+template <typename ELT, int DH, int CD, int CF>
 __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
   __shared__ float tok_t[2], t_last;
@@ -1264,8 +1427,39 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
   float *hs = os + 2 * d;   // [2][F] FFN hidden
   float *es = hs + 2 * F;   // [4d] decoder e | tanh activations
   float *hv = es + 4 * d;   // [3M + K] decoder outputs
+  float *red = hv + 3 * M + K + 8;   // attention merge scratch
+  float *vec = red + 4 * H * 2 * (DH + 2);   // staged small vectors
   const int b = blockIdx.x, tid = threadIdx.x;
   if (a.done[b]) return;
+  // every LayerNorm and bias vector of the model goes to LDS once, so that
+  // the per-step phases read no small vectors from memory
+  {
+    auto cp = [&](float *dst, const float *src, int cnt) {
+      for (int i = tid; i < cnt; i += blockDim.x) dst[i] = src[i];
+    };
+    for (int ly = 0; ly < a.L; ++ly) {
+      const FusedLayerW &w = a.layer[ly];
+      float *v = vec + ly * (9 * d + F);
+      cp(v, w.ln1_g, d);
+      cp(v + d, w.ln1_b, d);
+      cp(v + 2 * d, w.qkv_b, 3 * d);
+      cp(v + 5 * d, w.out_b, d);
+      cp(v + 6 * d, w.ln2_g, d);
+      cp(v + 7 * d, w.ln2_b, d);
+      cp(v + 8 * d, w.ffn1_b, F);
+      cp(v + 8 * d + F, w.ffn2_b, d);
+    }
+    float *v = vec + a.L * (9 * d + F);
+    cp(v, a.lnf_g, d);
+    cp(v + d, a.lnf_b, d);
+    cp(v + 2 * d, a.k1_b, d);
+    cp(v + 3 * d, a.mix_b, 3 * M);
+    cp(v + 3 * d + 3 * M, a.k2_b, K);
+    cp(v + 3 * d + 3 * M + K, a.freq, d);
+  }
+  const float *hvec = vec + a.L * (9 * d + F);
+  const float *lnf_g = hvec, *lnf_b = hvec + d, *k1_b = hvec + 2 * d, *mix_b = hvec + 3 * d,
+              *k2_b = hvec + 3 * d + 3 * M, *freq = hvec + 3 * d + 3 * M + K;
   const int n = a.n[b], base = a.lenD[b];
   const uint64_t r = (uint64_t)a.rnd[b];
   const size_t seq_row0 = (size_t)b * H * a.cap;
@@ -1280,9 +1474,9 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
       tok_k[tid] = a.ev_k[i];
     }
     __syncthreads();
-    for (int i = tid; i < P * d; i += 256) {
+    for (int i = tid; i < P * d; i += blockDim.x) {
       const int p = i / d, j = i - p * d;
-      const float arg = tok_t[p] * a.freq[j];
+      const float arg = tok_t[p] * freq[j];
       const int kk = min(max(tok_k[p], 0), K - 1);
       xs[i] = ((j & 1) ? cosf(arg) : sinf(arg)) + ld(wtype, (size_t)kk * d + j);
     }
@@ -1291,51 +1485,66 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
       const FusedLayerW &w = a.layer[ly];
       ELT *kc = (ELT *)(a.kc + a.layer_bytes * ly);
       ELT *vc = (ELT *)(a.vc + a.layer_bytes * ly);
-      wg_layernorm<ELT>(xs, as, w.ln1_g, w.ln1_b, P, d);
+      const float *lv = vec + ly * (9 * d + F);
+      const float *ln1_g = lv, *ln1_b = lv + d, *qkv_b = lv + 2 * d, *out_b = lv + 5 * d, *ln2_g = lv + 6 * d,
+                  *ln2_b = lv + 7 * d, *ffn1_b = lv + 8 * d, *ffn2_b = lv + 8 * d + F;
+      wg_layernorm<ELT>(xs, as, ln1_g, ln1_b, P, d);
       __syncthreads();
-      wg_gemv<ELT>((const ELT *)w.qkv_w, 3 * d, d, as, d, P, [&](int p, int nn, float acc) {
-        const float v = rnd_act<ELT>(acc + w.qkv_b[nn]);
-        const int which = nn / d, c = nn - which * d;
-        if (which == 0) {
-          qs[p * d + c] = v;
-        } else {
-          const int h = c / DH, j = c - h * DH, pos = pos0 + p;
-          const size_t row0 = seq_row0 + (size_t)h * a.cap;
-          if (pos < a.cap)
-            st(which == 1 ? kc : vc, which == 1 ? (row0 + pos) * DH + j : v_at<ELT>(row0, pos, j, DH), v);
-          else
-            atomicOr(a.status, TPPSD_STATUS_CAPACITY);
-        }
-      });
+      const ELT *wq = (const ELT *)w.qkv_w;
+      wg_gemv_cpl<ELT, CD>(
+          3 * d, d, P, [&](int nn) { return wq + (size_t)nn * d; }, [&](int, int p) { return as + p * d; },
+          [&](int p, int nn, float acc) {
+            const float v = rnd_act<ELT>(acc + qkv_b[nn]);
+            const int which = nn / d, c = nn - which * d;
+            if (which == 0) {
+              qs[p * d + c] = v;
+            } else {
+              const int h = c / DH, j = c - h * DH, pos = pos0 + p;
+              const size_t row0 = seq_row0 + (size_t)h * a.cap;
+              if (pos < a.cap)
+                st(which == 1 ? kc : vc, which == 1 ? (row0 + pos) * DH + j : v_at<ELT>(row0, pos, j, DH), v);
+              else
+                atomicOr(a.status, TPPSD_STATUS_CAPACITY);
+            }
+          });
       __syncthreads();
-      wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d);
+      wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       __syncthreads();
-      wg_gemv<ELT>((const ELT *)w.out_w, d, d, os, d, P,
-                   [&](int p, int nn, float acc) { xs[p * d + nn] += acc + w.out_b[nn]; });
+      const ELT *wo = (const ELT *)w.out_w;
+      wg_gemv_cpl<ELT, CD>(
+          d, d, P, [&](int nn) { return wo + (size_t)nn * d; }, [&](int, int p) { return os + p * d; },
+          [&](int p, int nn, float acc) { xs[p * d + nn] += acc + out_b[nn]; });
       __syncthreads();
-      wg_layernorm<ELT>(xs, as, w.ln2_g, w.ln2_b, P, d);
+      wg_layernorm<ELT>(xs, as, ln2_g, ln2_b, P, d);
       __syncthreads();
-      wg_gemv<ELT>((const ELT *)w.ffn1_w, F, d, as, d, P, [&](int p, int nn, float acc) {
-        hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + w.ffn1_b[nn], 0.f));
-      });
+      const ELT *w1 = (const ELT *)w.ffn1_w, *w2 = (const ELT *)w.ffn2_w;
+      wg_gemv_cpl<ELT, CD>(
+          F, d, P, [&](int nn) { return w1 + (size_t)nn * d; }, [&](int, int p) { return as + p * d; },
+          [&](int p, int nn, float acc) { hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + ffn1_b[nn], 0.f)); });
       __syncthreads();
-      wg_gemv<ELT>((const ELT *)w.ffn2_w, d, F, hs, F, P,
-                   [&](int p, int nn, float acc) { xs[p * d + nn] += acc + w.ffn2_b[nn]; });
+      wg_gemv_cpl<ELT, CF>(
+          d, F, P, [&](int nn) { return w2 + (size_t)nn * F; }, [&](int, int p) { return hs + p * F; },
+          [&](int p, int nn, float acc) { xs[p * d + nn] += acc + ffn2_b[nn]; });
       __syncthreads();
     }
-    // decoder on the last token
-    wg_layernorm<ELT>(xs + (P - 1) * d, as, a.lnf_g, a.lnf_b, 1, d);
+    // decoder on the last token: e = E h and tanh(V_k1 h + b1) in one pass,
+    // then the mixture (w, mu, log sigma from the slices of e) and type
+    // logits in one pass
+    wg_layernorm<ELT>(xs + (P - 1) * d, as, lnf_g, lnf_b, 1, d);
     __syncthreads();
-    wg_gemv<ELT>((const ELT *)a.Ek1_w, 4 * d, d, as, d, 1, [&](int, int nn, float acc) {
-      es[nn] = (nn < 3 * d) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + a.k1_b[nn - 3 * d]));
-    });
+    const ELT *we = (const ELT *)a.Ek1_w;
+    wg_gemv_cpl<ELT, CD>(
+        4 * d, d, 1, [&](int nn) { return we + (size_t)nn * d; }, [&](int, int) { return (const float *)as; },
+        [&](int, int nn, float acc) {
+          es[nn] = (nn < 3 * d) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * d]));
+        });
     __syncthreads();
-    const ELT *mw = (const ELT *)a.mix_w;
-    for (int grp = 0; grp < 3; ++grp)
-      wg_gemv<ELT>(mw + (size_t)grp * M * d, M, d, es + grp * d, 0, 1,
-                   [&](int, int nn, float acc) { hv[grp * M + nn] = acc + a.mix_b[grp * M + nn]; });
-    wg_gemv<ELT>((const ELT *)a.k2_w, K, d, es + 3 * d, 0, 1,
-                 [&](int, int nn, float acc) { hv[3 * M + nn] = acc + a.k2_b[nn]; });
+    const ELT *mw = (const ELT *)a.mix_w, *kw = (const ELT *)a.k2_w;
+    wg_gemv_cpl<ELT, CD>(
+        3 * M + K, d, 1,
+        [&](int nn) { return nn < 3 * M ? mw + (size_t)nn * d : kw + (size_t)(nn - 3 * M) * d; },
+        [&](int nn, int) { return (const float *)(es + (nn < 3 * M ? nn / M : 3) * d); },
+        [&](int, int nn, float acc) { hv[nn] = acc + (nn < 3 * M ? mix_b[nn] : k2_b[nn - 3 * M]); });
     __syncthreads();
     if (tid < 64) {
       const int lane = tid;
@@ -1350,40 +1559,53 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
     }
     __syncthreads();
     const size_t di = (size_t)b * a.MG + (l - 1);
-    for (int i = tid; i < 3 * M; i += 256) a.d_mix[di * 3 * M + i] = hv[i];
-    for (int i = tid; i < K; i += 256) a.d_logtype[di * K + i] = hv[3 * M + i];
-    if (tid == 0) {
+    for (int i = tid; i < 3 * M; i += blockDim.x) a.d_mix[di * 3 * M + i] = hv[i];
+    for (int i = tid; i < K; i += blockDim.x) a.d_logtype[di * K + i] = hv[3 * M + i];
+    if (tid < 64) {
+      // the draft event, drawn by wave 0: component, Box-Muller interval, type
       float u[4];
       philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)l, TAG_DRAFT, u);
-      const float tau = sample_tau(hv, hv + M, hv + 2 * M, M, u[0], u[1], u[2]);
-      const int kk = sample_cat(hv + 3 * M, K, u[3]);
-      const float tn = t_last + tau;
-      a.d_tau[di] = tau;
-      a.d_t[di] = tn;
-      a.d_k[di] = kk;
-      a.d_logg[di] = mix_logpdf(hv, hv + M, hv + 2 * M, M, tau);
-      a.d_logf[di] = hv[3 * M + kk];
-      if (!isfinite(tau)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
-      tok_t[0] = tn;
-      tok_k[0] = kk;
-      t_last = tn;
+      const int z = wave_sample_cat(hv, M, u[0]);
+      const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
+      const float tau = expf(hv[M + z] + expf(hv[2 * M + z]) * eps);
+      const int kk = wave_sample_cat(hv + 3 * M, K, u[3]);
+      const float lg = wave_mix_logpdf(hv, hv + M, hv + 2 * M, M, tau);
+      if (tid == 0) {
+        const float tn = t_last + tau;
+        a.d_tau[di] = tau;
+        a.d_t[di] = tn;
+        a.d_k[di] = kk;
+        a.d_logg[di] = lg;
+        a.d_logf[di] = hv[3 * M + kk];
+        if (!isfinite(tau)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+        tok_t[0] = tn;
+        tok_k[0] = kk;
+        t_last = tn;
+      }
     }
     __syncthreads();
   }
 }
 
 void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
-  const size_t lds = fused_draft_lds_bytes(a.d, a.F, a.M, a.K);
-  const int dh = a.d / a.H;
-#define TPPSD_FD(ELT, DH) k_draft_fused<ELT, DH><<<a.B, 256, lds, s>>>(a)
+  const size_t lds = fused_draft_lds_bytes(a.L, a.d, a.F, a.M, a.K, a.H);
+  const int cd = gemv_cpl(a.d), cf = gemv_cpl(a.F);
+  // d_head = 16 only (fused_draft_ok); chunk counts 2, 4 or 8
+  auto go = [&](auto kern) { kern<<<a.B, 256, lds, s>>>(a); };
+#define TPPSD_FD(ELT)                                                             \
+  if (cd == 2 && cf == 2) go(k_draft_fused<ELT, 16, 2, 2>);                        \
+  else if (cd == 2 && cf == 4) go(k_draft_fused<ELT, 16, 2, 4>);                   \
+  else if (cd == 2) go(k_draft_fused<ELT, 16, 2, 8>);                              \
+  else if (cd == 4 && cf == 2) go(k_draft_fused<ELT, 16, 4, 2>);                   \
+  else if (cd == 4 && cf == 4) go(k_draft_fused<ELT, 16, 4, 4>);                   \
+  else if (cd == 4) go(k_draft_fused<ELT, 16, 4, 8>);                              \
+  else if (cf == 2) go(k_draft_fused<ELT, 16, 8, 2>);                              \
+  else if (cf == 4) go(k_draft_fused<ELT, 16, 8, 4>);                              \
+  else go(k_draft_fused<ELT, 16, 8, 8>);
   if (bf16) {
-    if (dh == 16) TPPSD_FD(bf16_t, 16);
-    else if (dh == 32) TPPSD_FD(bf16_t, 32);
-    else TPPSD_FD(bf16_t, 64);
+    TPPSD_FD(bf16_t)
   } else {
-    if (dh == 16) TPPSD_FD(float, 16);
-    else if (dh == 32) TPPSD_FD(float, 32);
-    else TPPSD_FD(float, 64);
+    TPPSD_FD(float)
   }
 #undef TPPSD_FD
 }

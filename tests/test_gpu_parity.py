@@ -161,11 +161,16 @@ def test_accept_teacher_forced(case, external):
     print(f"{case.name}: checked {checked}/{case.B}; L histogram {np.bincount(res['L'])}")
 
 
-DRAFT_CASES = [small("c1", 8), small("c2", 8), small("c3", 16, n_hist=40, init="bias"), small("c5", 16, init="bias")]
+DRAFT_CASES = [small("c1", 8), small("c2", 8), small("c3", 16, n_hist=40, init="bias"), small("c5", 16, init="bias"),
+               small("c4", 4, n_hist=40, init="bias")]
 
 
+# both drafting paths: one workgroup per sequence for all gamma steps (where
+# the draft model fits it), and per-step batched kernels
+@pytest.mark.parametrize("layered", [False, True], ids=["fused", "layered"])
 @pytest.mark.parametrize("case", DRAFT_CASES, ids=_ids(DRAFT_CASES))
-def test_draft_parity(case):
+def test_draft_parity(case, layered, monkeypatch):
+    monkeypatch.setenv("TPPSD_LAYERED_DRAFT", "1" if layered else "0")
     gamma, n_gen, seed = _gamma(case), 64, 13
     wt, wd = weights(case)
     T, D, ht, hk, st_o, dr, vf = _oracle_round(case, wt, wd, gamma, n_gen, seed)
