@@ -154,6 +154,8 @@ struct tppsd_model {
 
 // ---- state ------------------------------------------------------------------
 struct ModelCache {
+  void *head_w = nullptr;   // decoder block-diagonal matrix [(3M + K)][4d]
+  float *head_b = nullptr;  // and bias [3M + K]
   // per layer: keys [B][H][kv_cap][dh]; values the same for fp32, in
   // 8-position blocks [B][H][kv_cap / 8][dh][8] for bf16
   char *k = nullptr, *v = nullptr;
@@ -180,6 +182,8 @@ struct tppsd_state {
   // activation scratch
   float *x = nullptr;
   void *a = nullptr, *q = nullptr, *o = nullptr, *hid = nullptr, *e = nullptr;
+  float *logits = nullptr;
+  bool heads_built = false;
   float *ar_mix = nullptr, *ar_logtype = nullptr;
   float *attn_part = nullptr;
   int32_t *gen0 = nullptr;
@@ -226,6 +230,7 @@ struct WsLayout {
   size_t status, n_done, acc, n, gen, lenT, lenD, done, rnd, zeros, ev_t, ev_k;
   size_t freqT, freqD, kT, vT, kD, vD, layerT, layerD;
   size_t x, a, q, o, hid, e, ar_mix, ar_lt, attn_part, gen0;
+  size_t logits, hwT, hbT, hwD, hbD;
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt;
   size_t v_logg, v_logf, v_mix, v_lt;
   size_t a_L, a_nnew, a_knew, a_tnew, a_taunew, a_ar, a_flags;
@@ -274,6 +279,11 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   w.o = take(Tm * dmax * 4);
   w.hid = take(Tm * fmax * 4);
   w.e = take(Tm * 4 * dmax * 4);
+  w.logits = take(Tm * head_ldl((int)mmax, (int)kmax) * 4);
+  w.hwT = take((size_t)(3 * T->cfg.n_mix + T->cfg.n_types) * 4 * T->d() * T->act_bytes());
+  w.hbT = take((size_t)(3 * T->cfg.n_mix + T->cfg.n_types) * 4);
+  w.hwD = take(D ? (size_t)(3 * D->cfg.n_mix + D->cfg.n_types) * 4 * D->d() * D->act_bytes() : 0);
+  w.hbD = take(D ? (size_t)(3 * D->cfg.n_mix + D->cfg.n_types) * 4 : 0);
   w.ar_mix = take(Bz * 3 * mmax * 4);
   w.ar_lt = take(Bz * kmax * 4);
   {
@@ -373,7 +383,14 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     eh.ldo = 4 * d;
     eh.split = 3 * d;
     launch_gemm(s->a, fuse_ln ? &lnf : nullptr, m->Ek1_w, bf, T, 4 * d, d, eh, st, ev(5 * L, 0), ev(5 * L, 1));
-    launch_head(s->e, bf, d, m->cfg.n_mix, m->cfg.n_types, m->mix_w, m->mix_b, m->k2_w, m->k2_b, *head, st);
+    const int M = m->cfg.n_mix, K = m->cfg.n_types, ldl = head_ldl(M, K);
+    Epi el{};
+    el.mode = EPI_F32;
+    el.bias = c.head_b;
+    el.out = s->logits;
+    el.ldo = ldl;
+    launch_gemm(s->e, nullptr, c.head_w, bf, T, 3 * M + K, 4 * d, el, st);
+    launch_head(s->logits, ldl, M, K, *head, st);
   }
   return TPPSD_OK;
 }
@@ -725,6 +742,13 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->o = ws + w.o;
   s->hid = ws + w.hid;
   s->e = ws + w.e;
+  s->logits = (float *)(ws + w.logits);
+  s->cT.head_w = ws + w.hwT;
+  s->cT.head_b = (float *)(ws + w.hbT);
+  if (D) {
+    s->cD.head_w = ws + w.hwD;
+    s->cD.head_b = (float *)(ws + w.hbD);
+  }
   s->ar_mix = (float *)(ws + w.ar_mix);
   s->ar_logtype = (float *)(ws + w.ar_lt);
   s->attn_part = (float *)(ws + w.attn_part);
@@ -799,6 +823,15 @@ int tppsd_prefill(tppsd_state *s, const float *d_t, const int32_t *d_k, int n0, 
     return fail(TPPSD_E_ARG, "n0 + n_gen + max_gamma + 1 = %lld exceeds max_events %d",
                 (long long)n0 + n_gen + s->max_gamma + 1, s->cap);
   s->n_gen = n_gen;
+  if (!s->heads_built) {
+    for (int which = 0; which < (s->D ? 2 : 1); ++which) {
+      const tppsd_model *m = which ? s->D : s->T;
+      const ModelCache &c = which ? s->cD : s->cT;
+      launch_build_head(m->mix_w, m->k2_w, m->mix_b, m->k2_b, m->bf16(), m->d(), m->cfg.n_mix, m->cfg.n_types,
+                        c.head_w, c.head_b, st);
+    }
+    s->heads_built = true;
+  }
   launch_prefill_init(d_t, d_k, s->B, n0, n_gen, s->ev_t, s->ev_k, s->cap, s->n, s->gen, s->lenT, s->lenD, s->done,
                       s->rnd, s->zeros, s->n_done, s->status, s->acc_stats, st);
   // encode history events 0 .. n0 - 2 (target) and 0 .. n0 - 3 (draft) in position chunks

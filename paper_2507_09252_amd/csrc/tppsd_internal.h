@@ -26,12 +26,12 @@ struct TokSrc {
 };
 
 // GEMM epilogues: Y[r, n] = sum_k X[r, k] W[n, k]
-enum EpiMode { EPI_STORE = 0, EPI_RESID = 1, EPI_RELU = 2, EPI_QKV = 3, EPI_HEAD = 4 };
+enum EpiMode { EPI_STORE = 0, EPI_RESID = 1, EPI_RELU = 2, EPI_QKV = 3, EPI_HEAD = 4, EPI_F32 = 5 };
 
 struct Epi {
   int mode;
   const float *bias;        // [N] (HEAD: [N - split])
-  void *out;                // STORE/RELU/HEAD: act [T, ldo]; RESID: float x [T, ldo]
+  void *out;                // STORE/RELU/HEAD: act [T, ldo]; RESID, F32: float [T, ldo]
   int ldo;
   // EPI_QKV: n < d -> q[r, n]; n in [d, 2d) -> key cache; [2d, 3d) -> value cache
   void *q;
@@ -174,8 +174,13 @@ void launch_attention(const void *q, const void *kc, const void *vc, void *o, in
                       const int32_t *start, int start_off, const int32_t *done, int B, int P, int H,
                       int dh, int cap, float *part, int verify, hipEvent_t ev0, hipEvent_t ev1,
                       hipStream_t st);
-void launch_head(const void *e, int bf16, int d, int M, int K, const void *wmix, const float *bmix,
-                 const void *wk2, const float *bk2, const HeadArgs &a, hipStream_t st);
+// decoder epilogue over the rows' logits [.., ldl] (mixture w | mu | log sigma, then types)
+void launch_head(const float *logits, int ldl, int M, int K, const HeadArgs &a, hipStream_t st);
+// the decoder's block-diagonal (3M + K) x 4d matrix and its bias (3M + K)
+void launch_build_head(const void *mix_w, const void *k2_w, const float *mix_b, const float *k2_b, int bf16, int d,
+                       int M, int K, void *hw, float *hb, hipStream_t st);
+// row stride of the decoder logits: 3M + K rounded up to 8
+inline int head_ldl(int M, int K) { return (3 * M + K + 7) / 8 * 8; }
 void launch_accept(const AcceptArgs &a, hipStream_t st);
 void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, float *ev_t,
                          int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,

@@ -293,6 +293,97 @@ __device__ __forceinline__ void epilogue(const Epi &e, int r, int n, float acc) 
       else
         st((ACT *)e.out, (size_t)r * e.ldo + n, tanhf(acc + e.bias[n - e.split]));
       break;
+    case EPI_F32:
+      ((float *)e.out)[(size_t)r * e.ldo + n] = acc + (e.bias ? e.bias[n] : 0.f);
+      break;
+  }
+}
+
+// 8 consecutive columns n .. n + 7 of row r (n a multiple of 8, all < N;
+// every destination row stride is a multiple of 8): the same arithmetic as
+// epilogue(), with 16-byte loads and stores where the layout allows.
+template <typename ACT> __device__ __forceinline__ void store8(ACT *p, const float v[8]);
+template <> __device__ __forceinline__ void store8<float>(float *p, const float v[8]) {
+  *(float4 *)p = make_float4(v[0], v[1], v[2], v[3]);
+  *(float4 *)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+template <> __device__ __forceinline__ void store8<bf16_t>(bf16_t *p, const float v[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
+  *(uint4 *)p = make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ __forceinline__ void load8f(const float *p, float v[8]) {
+  const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+template <typename ACT>
+__device__ __forceinline__ void epilogue8(const Epi &e, int r, int n, const float acc[8]) {
+  float v[8], bv[8];
+  switch (e.mode) {
+    case EPI_STORE:
+    case EPI_F32: {
+      if (e.bias) load8f(e.bias + n, bv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = acc[i] + (e.bias ? bv[i] : 0.f);
+      if (e.mode == EPI_F32) store8((float *)e.out + (size_t)r * e.ldo + n, v);
+      else store8((ACT *)e.out + (size_t)r * e.ldo + n, v);
+      break;
+    }
+    case EPI_RESID: {
+      float *x = (float *)e.out + (size_t)r * e.ldo + n;
+      float xv[8];
+      load8f(x, xv);
+      load8f(e.bias + n, bv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = xv[i] + (acc[i] + bv[i]);
+      store8(x, v);
+      break;
+    }
+    case EPI_RELU: {
+      load8f(e.bias + n, bv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = fmaxf(acc[i] + bv[i], 0.f);
+      store8((ACT *)e.out + (size_t)r * e.ldo + n, v);
+      break;
+    }
+    case EPI_QKV: {
+      load8f(e.bias + n, bv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = acc[i] + bv[i];
+      const int which = n / e.d, c = n - which * e.d;
+      if (which == 0) {
+        store8((ACT *)e.q + (size_t)r * e.d + c, v);
+      } else {
+        const int b = r / e.P, p = r - b * e.P;
+        const int h = c / e.dh, j = c - h * e.dh;
+        const int pos = e.start[b] + e.start_off + p;
+        if (pos < e.cap) {
+          const size_t row0 = ((size_t)b * e.H + h) * e.cap;
+          if (which == 1) {
+            store8((ACT *)e.kc + (row0 + pos) * e.dh + j, v);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) st((ACT *)e.vc, v_at<ACT>(row0, pos, j + i, e.dh), v[i]);
+          }
+        } else {
+          atomicOr(e.status, TPPSD_STATUS_CAPACITY);
+        }
+      }
+      break;
+    }
+    case EPI_HEAD: {
+      if (n < e.split) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = acc[i];
+      } else {
+        load8f(e.bias + (n - e.split), bv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = tanhf(acc[i] + bv[i]);
+      }
+      store8((ACT *)e.out + (size_t)r * e.ldo + n, v);
+      break;
+    }
   }
 }
 
@@ -553,15 +644,32 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
       }
     }
   }
+  // the tile goes through LDS (over the A stages, free after the last
+  // barrier) so that each thread finishes 8 consecutive columns of a row with
+  // 16-byte accesses
+  constexpr int CLD = BN + 4;
+  static_assert(sizeof(As) >= sizeof(float) * BM * CLD, "C tile must fit the A stages");
+  float *Cs = (float *)&As[0][0][0];
+  __syncthreads();   // every wave is done reading the last stage
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int r = m0 + wm + 16 * i + 4 * g + v, n = n0 + wn + 16 * j + rr;
-        if (r < T && n < N) epilogue<ELT>(e, r, n, acc[i][j][v]);
-      }
+      for (int v = 0; v < 4; ++v) Cs[(wm + 16 * i + 4 * g + v) * CLD + wn + 16 * j + rr] = acc[i][j][v];
+  __syncthreads();
+  for (int gi = tid; gi < BM * (BN / 8); gi += 256) {
+    const int row = gi / (BN / 8), c8 = gi - row * (BN / 8);
+    const int r = m0 + row, n = n0 + 8 * c8;
+    if (r >= T || n >= N) continue;
+    float cv[8];
+    load8f(Cs + row * CLD + 8 * c8, cv);
+    if (n + 8 <= N) {
+      epilogue8<ELT>(e, r, n, cv);
+    } else {
+      for (int i = 0; i < N - n; ++i) epilogue<ELT>(e, r, n + i, cv[i]);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1033,100 +1141,126 @@ __global__ void k_attn_combine(const float *__restrict__ part, ACT *__restrict__
 }
 
 // ---------------------------------------------------------------------------
-// decoder: mixture parameters and type log-probabilities for selected rows,
-// followed by the verify / draft / AR epilogue. One wave per row.
+// decoder (§4.2): the mixture parameters (V_w e1, V_mu e2, V_sigma e3) and
+// the type logits (V_k2 tanh(V_k1 h + b1)) of a row are one product of the
+// concatenated [e1 e2 e3 tanh(.)] (4d wide) with a block-diagonal
+// (3M + K) x 4d matrix built once per state from the model's heads; the
+// kernel below then takes the log-softmaxes and runs the verify / draft / AR
+// epilogue, one wave per row.
 // ---------------------------------------------------------------------------
 
-template <typename ACT>
-__global__ __launch_bounds__(256) void k_head(const ACT *__restrict__ e, int d, int M, int K,
-                                              const ACT *__restrict__ wmix, const float *__restrict__ bmix,
-                                              const ACT *__restrict__ wk2, const float *__restrict__ bk2,
+template <typename W>
+__global__ void k_build_head(const W *__restrict__ mix_w, const W *__restrict__ k2_w,
+                             const float *__restrict__ mix_b, const float *__restrict__ k2_b, int d, int M,
+                             int K, W *__restrict__ hw, float *__restrict__ hb) {
+  const int o = blockIdx.x;   // output row, < 3M + K
+  const int grp = o < 3 * M ? o / M : 3;
+  const W *src = o < 3 * M ? mix_w + (size_t)o * d : k2_w + (size_t)(o - 3 * M) * d;
+  for (int c = threadIdx.x; c < 4 * d; c += blockDim.x) {
+    const int k = c - grp * d;
+    hw[(size_t)o * 4 * d + c] = (k >= 0 && k < d) ? src[k] : (W)0;
+  }
+  if (threadIdx.x == 0) hb[o] = o < 3 * M ? mix_b[o] : k2_b[o - 3 * M];
+}
+
+__global__ __launch_bounds__(256) void k_head(const float *__restrict__ logits, int ldl, int M, int K,
                                               HeadArgs a) {
-  __shared__ float vals[4][3 * TPPSD_MAX_MIX + TPPSD_MAX_TYPES];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int rows_per_seq = a.P - a.p0;
   const int ridx = blockIdx.x * 4 + w;
-  const bool valid = ridx < a.B * rows_per_seq;
-  const int b = valid ? ridx / rows_per_seq : 0;
-  const int p = valid ? a.p0 + (ridx - b * rows_per_seq) : 0;
+  if (ridx >= a.B * rows_per_seq) return;   // whole waves; no barriers below
+  const int b = ridx / rows_per_seq;
+  const int p = a.p0 + (ridx - b * rows_per_seq);
   const size_t tok = (size_t)b * a.P + p;
-  float *v = vals[w];
-  const int nout = 3 * M + K;
-  if (valid) {
-    const ACT *er = e + tok * 4 * d;
-    for (int oi = lane; oi < nout; oi += 64) {
-      const ACT *xr, *wr;
-      float bias;
-      if (oi < 3 * M) {
-        xr = er + (oi / M) * d;
-        wr = wmix + (size_t)oi * d;
-        bias = bmix[oi];
-      } else {
-        xr = er + 3 * d;
-        wr = wk2 + (size_t)(oi - 3 * M) * d;
-        bias = bk2[oi - 3 * M];
-      }
-      float acc = 0.f;
-      for (int j = 0; j < d; ++j) acc += ld(xr, j) * ld(wr, j);
-      v[oi] = acc + bias;
-    }
-  }
-  __syncthreads();
-  // log-softmax of the mixture logits (lanes < M) and type logits (lanes < K);
-  // every wave reaches every barrier, rows past the end only skip the stores
-  const float lw = (valid && lane < M) ? v[lane] : -INFINITY;
+  const float *lr = logits + tok * ldl;
+  // lane m: mixture logit, mean and log-scale of component m; type logit m
+  const float lw = lane < M ? lr[lane] : -INFINITY;
+  const float mu = lane < M ? lr[M + lane] : 0.f;
+  const float sg = lane < M ? lr[2 * M + lane] : 0.f;
+  const float lk = lane < K ? lr[3 * M + lane] : -INFINITY;
   const float mw = wave_max(lw);
-  const float sw = wave_sum(lane < M ? expf(lw - mw) : 0.f);
-  const float lk = (valid && lane < K) ? v[3 * M + lane] : -INFINITY;
+  const float logw = lw - mw - logf(wave_sum(lane < M ? expf(lw - mw) : 0.f));
   const float mk = wave_max(lk);
-  const float sk = wave_sum(lane < K ? expf(lk - mk) : 0.f);
-  const float logw = lw - mw - logf(sw);
-  const float logk = lk - mk - logf(sk);
-  __syncthreads();
-  if (valid && lane < M) v[lane] = logw;
-  if (valid && lane < K) v[3 * M + lane] = logk;
-  __syncthreads();
-  if (!valid) return;
+  const float logk = lk - mk - logf(wave_sum(lane < K ? expf(lk - mk) : 0.f));
   const size_t drow = (size_t)b * a.dst_stride + a.dst_row0 + (p - a.p0);
   float *mixr = a.mix + drow * 3 * M;
   float *ltr = a.logtype + drow * K;
-  for (int oi = lane; oi < 3 * M; oi += 64) mixr[oi] = v[oi];
-  if (lane < K) ltr[lane] = v[3 * M + lane];
+  if (lane < M) {
+    mixr[lane] = logw;
+    mixr[M + lane] = mu;
+    mixr[2 * M + lane] = sg;
+  }
+  if (lane < K) ltr[lane] = logk;
   const bool active = a.done == nullptr || a.done[b] == 0;
-  bool bad = false;
-  for (int oi = lane; oi < nout; oi += 64) bad |= !isfinite(v[oi]);
+  const bool bad = (lane < M && !(isfinite(logw) && isfinite(mu) && isfinite(sg))) || (lane < K && !isfinite(logk));
   if (__ballot(bad) != 0ull && active && lane == 0) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
-  if (lane != 0) return;
-  const float *Lw = v, *Mu = v + M, *S = v + 2 * M, *Lk = v + 3 * M;
+  // component m's log-density term at tau, for the wave-parallel mixture sum
+  auto logpdf = [&](float tau) {
+    const float lt = logf(tau);
+    float c = -INFINITY;
+    if (lane < M) {
+      const float z = lt - mu;
+      c = logw - sg - 0.918938533204672742f - lt - 0.5f * z * z * expf(-2.f * sg);
+    }
+    const float mx = wave_max(c);
+    return mx + logf(wave_sum(lane < M ? expf(c - mx) : 0.f));
+  };
+  // categorical over the lanes' log-probabilities (scan of exp, first index
+  // whose running sum exceeds u times the total)
+  auto sample = [&](float lp, int n, float u) {
+    float c = lane < n ? expf(lp) : 0.f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float o = __shfl_up(c, off, 64);
+      if (lane >= off) c += o;
+    }
+    const float tot = __shfl(c, n - 1, 64);
+    const unsigned long long hit = __ballot(lane < n && u * tot < c);
+    return hit ? (int)__builtin_ctzll(hit) : n - 1;
+  };
+  auto draw_tau = [&](const float u[4]) {
+    const int z = sample(logw, M, u[0]);
+    const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
+    const float muz = __shfl(mu, z, 64), sz = __shfl(sg, z, 64);
+    return expf(muz + expf(sz) * eps);
+  };
   if (a.mode == HEAD_VERIFY) {
     if (p < a.gamma) {
       const size_t di = (size_t)b * a.dr_stride + p;
-      const float lg = mix_logpdf(Lw, Mu, S, M, a.dr_tau[di]);
+      const float lg = logpdf(a.dr_tau[di]);
       const int kk = min(max(a.dr_k[di], 0), K - 1);
-      a.v_logg[di] = lg;
-      a.v_logf[di] = Lk[kk];
-      if (!isfinite(lg) && active) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+      const float lf = __shfl(logk, kk, 64);
+      if (lane == 0) {
+        a.v_logg[di] = lg;
+        a.v_logf[di] = lf;
+        if (!isfinite(lg) && active) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+      }
     }
   } else if (a.mode == HEAD_DRAFT) {
     float u[4];
     philox_uniforms(a.seed, (uint64_t)b, (uint64_t)a.rnd[b], (uint64_t)a.l_index, TAG_DRAFT, u);
-    const float tau = sample_tau(Lw, Mu, S, M, u[0], u[1], u[2]);
-    const int kk = sample_cat(Lk, K, u[3]);
-    const size_t di = (size_t)b * a.dr_stride + a.slot;
-    const float tprev = (a.slot == 0) ? a.ev_t[(size_t)b * a.ev_stride + a.n[b] - 1] : a.d_t[di - 1];
-    a.d_tau[di] = tau;
-    a.d_t[di] = tprev + tau;
-    a.d_k[di] = kk;
-    a.d_logg[di] = mix_logpdf(Lw, Mu, S, M, tau);
-    a.d_logf[di] = Lk[kk];
-    if (!isfinite(tau) && active) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+    const float tau = draw_tau(u);
+    const int kk = sample(logk, K, u[3]);
+    const float lg = logpdf(tau);
+    const float lf = __shfl(logk, kk, 64);
+    if (lane == 0) {
+      const size_t di = (size_t)b * a.dr_stride + a.slot;
+      const float tprev = (a.slot == 0) ? a.ev_t[(size_t)b * a.ev_stride + a.n[b] - 1] : a.d_t[di - 1];
+      a.d_tau[di] = tau;
+      a.d_t[di] = tprev + tau;
+      a.d_k[di] = kk;
+      a.d_logg[di] = lg;
+      a.d_logf[di] = lf;
+      if (!isfinite(tau) && active) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+    }
   } else {  // HEAD_AR
     if (!active) return;
     float u[4];
     const int g = a.gen[b];
     philox_uniforms(a.seed, (uint64_t)b, (uint64_t)g, 0ull, TAG_AR, u);
-    const float tau = sample_tau(Lw, Mu, S, M, u[0], u[1], u[2]);
-    const int kk = sample_cat(Lk, K, u[3]);
+    const float tau = draw_tau(u);
+    const int kk = sample(logk, K, u[3]);
+    if (lane != 0) return;
     const int n = a.n[b];
     if (n >= a.ev_stride) {
       atomicOr(a.status, TPPSD_STATUS_CAPACITY);
@@ -1969,16 +2103,19 @@ void launch_attention(const void *q, const void *kc, const void *vc, void *o, in
     attention_role<0>(q, kc, vc, o, bf16, start, start_off, done, B, P, H, dh, cap, part, ev0, ev1, s);
 }
 
-void launch_head(const void *e, int bf16, int d, int M, int K, const void *wmix, const float *bmix,
-                 const void *wk2, const float *bk2, const HeadArgs &a, hipStream_t s) {
+void launch_head(const float *logits, int ldl, int M, int K, const HeadArgs &a, hipStream_t s) {
   const int rows = a.B * (a.P - a.p0);
-  const int blocks = (rows + 3) / 4;
+  k_head<<<(rows + 3) / 4, 256, 0, s>>>(logits, ldl, M, K, a);
+}
+
+void launch_build_head(const void *mix_w, const void *k2_w, const float *mix_b, const float *k2_b, int bf16, int d,
+                       int M, int K, void *hw, float *hb, hipStream_t s) {
   if (bf16)
-    k_head<bf16_t><<<blocks, 256, 0, s>>>((const bf16_t *)e, d, M, K, (const bf16_t *)wmix, bmix,
-                                          (const bf16_t *)wk2, bk2, a);
+    k_build_head<bf16_t><<<3 * M + K, 256, 0, s>>>((const bf16_t *)mix_w, (const bf16_t *)k2_w, mix_b, k2_b, d, M,
+                                                   K, (bf16_t *)hw, hb);
   else
-    k_head<float><<<blocks, 256, 0, s>>>((const float *)e, d, M, K, (const float *)wmix, bmix,
-                                         (const float *)wk2, bk2, a);
+    k_build_head<float><<<3 * M + K, 256, 0, s>>>((const float *)mix_w, (const float *)k2_w, mix_b, k2_b, d, M, K,
+                                                  (float *)hw, hb);
 }
 
 void launch_accept(const AcceptArgs &a, hipStream_t s) { k_accept<<<(a.B + 3) / 4, 256, 0, s>>>(a); }
