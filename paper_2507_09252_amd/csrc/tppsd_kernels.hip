@@ -1017,65 +1017,92 @@ __global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__
     for (int td = 0; td < NDT; ++td) oacc[t][td] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
   }
   const int krow0 = 8 * (rr >> 2) + (rr & 3), krow1 = krow0 + 4;
-  for (int kt = k_begin + wave * KT; kt < k_end; kt += 4 * KT) {
-    const size_t r0 = kvbase + min(kt + krow0, cap - 1), r1 = kvbase + min(kt + krow1, cap - 1);
+  // a wave loads a batch of NB of its 32-key steps before computing any
+  // (positions clamped into the range; steps past it are skipped), then takes
+  // one online-softmax update per query tile for the whole batch
+  constexpr int NB = (DH >= 32 || QT >= 2) ? 2 : 4;
+  struct Step {
     f32x4_t a0[DH / 16], a1[DH / 16];
-#pragma unroll
-    for (int c = 0; c < DH / 16; ++c) {
-      a0[c] = *(const f32x4_t *)(kc + r0 * DH + 16 * c + 4 * g);
-      a1[c] = *(const f32x4_t *)(kc + r1 * DH + 16 * c + 4 * g);
-    }
-    // value column 16 td + rr of keys kt + 8 g + j (zero past the key range)
     float vv[NDT][8];
+  };
+  const int last_step = k_end > k_begin ? k_begin + (k_end - 1 - k_begin) / KT * KT : k_begin;
+  for (int kb = k_begin + wave * KT; kb < k_end; kb += NB * 4 * KT) {
+    Step f[NB];
 #pragma unroll
-    for (int td = 0; td < NDT; ++td)
+    for (int sidx = 0; sidx < NB; ++sidx) {
+      const int kt = min(kb + sidx * 4 * KT, last_step);
+      const size_t r0 = kvbase + min(kt + krow0, cap - 1), r1 = kvbase + min(kt + krow1, cap - 1);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int key = kt + 8 * g + j;
-        vv[td][j] = (key < k_end) ? vc[(kvbase + key) * DH + 16 * td + rr] : 0.f;
+      for (int c = 0; c < DH / 16; ++c) {
+        f[sidx].a0[c] = *(const f32x4_t *)(kc + r0 * DH + 16 * c + 4 * g);
+        f[sidx].a1[c] = *(const f32x4_t *)(kc + r1 * DH + 16 * c + 4 * g);
       }
+      // value column 16 td + rr of keys kt + 8 g + j (zero past the key range)
+#pragma unroll
+      for (int td = 0; td < NDT; ++td)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int key = kt + 8 * g + j;
+          const float v = vc[(kvbase + min(key, k_end - 1)) * DH + 16 * td + rr];
+          f[sidx].vv[td][j] = (key < k_end) ? v : 0.f;
+        }
+    }
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
-      f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < DH / 16; ++c)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[c][e], qf[t][c][e], s0, 0, 0, 0);
-          s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[c][e], qf[t][c][e], s1, 0, 0, 0);
-        }
       const int my_q = 16 * t + rr, my_last = base + my_q;
       const bool q_ok = my_q < P;
-      float sv[8];
+      float sv[NB][8];
       float mx = -INFINITY;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int key = kt + 8 * g + j;
-        const float raw = (j < 4) ? s0[j] : s1[j - 4];
-        const bool ok = q_ok && key < k_end && key <= my_last;
-        sv[j] = ok ? raw * scale : -INFINITY;
-        mx = fmaxf(mx, sv[j]);
+      for (int sidx = 0; sidx < NB; ++sidx) {
+        const int kt = kb + sidx * 4 * KT;
+        if (kt >= k_end) {   // uniform across the wave
+#pragma unroll
+          for (int j = 0; j < 8; ++j) sv[sidx][j] = -INFINITY;
+          continue;
+        }
+        f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < DH / 16; ++c)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            s0 = __builtin_amdgcn_mfma_f32_16x16x4f32(f[sidx].a0[c][e], qf[t][c][e], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_16x16x4f32(f[sidx].a1[c][e], qf[t][c][e], s1, 0, 0, 0);
+          }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int key = kt + 8 * g + j;
+          const float raw = (j < 4) ? s0[j] : s1[j - 4];
+          sv[sidx][j] = (q_ok && key < k_end && key <= my_last) ? raw * scale : -INFINITY;
+          mx = fmaxf(mx, sv[sidx][j]);
+        }
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, swz_xor<16>(mx));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float m_new = fmaxf(m_run[t], mx);
       const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run[t] - m_new);
-      float pv[8], ps = 0.f;
+      float ps = 0.f;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        pv[j] = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
-        ps += pv[j];
-      }
-      ps += __shfl_xor(ps, 16, 64);
+      for (int sidx = 0; sidx < NB; ++sidx)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          sv[sidx][j] = (sv[sidx][j] == -INFINITY) ? 0.f : expf(sv[sidx][j] - m_new);
+          ps += sv[sidx][j];
+        }
+      ps += swz_xor<16>(ps);
       ps += __shfl_xor(ps, 32, 64);
       l_run[t] = l_run[t] * alpha + ps;
       m_run[t] = m_new;
 #pragma unroll
-      for (int td = 0; td < NDT; ++td) {
-        oacc[t][td] *= alpha;
+      for (int td = 0; td < NDT; ++td) oacc[t][td] *= alpha;
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          oacc[t][td] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv[td][j], pv[j], oacc[t][td], 0, 0, 0);
+      for (int sidx = 0; sidx < NB; ++sidx) {
+        if (kb + sidx * 4 * KT >= k_end) break;
+#pragma unroll
+        for (int td = 0; td < NDT; ++td)
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            oacc[t][td] = __builtin_amdgcn_mfma_f32_16x16x4f32(f[sidx].vv[td][j], sv[sidx][j], oacc[t][td], 0, 0, 0);
       }
     }
   }
@@ -1750,6 +1777,7 @@ void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
+  __shared__ float acc_pre[4][8 * 64];   // per wave: staged mixture terms (Theorem-1 loop)
   const int lane = threadIdx.x & 63;
   const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (b >= a.B) return;
@@ -1796,7 +1824,47 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     const float *Dr = a.d_mix + ((size_t)b * MG + li) * 3 * M;
     if (!at) {
       // Theorem 1: candidates tau ~ g_T, accept iff u_a < 1 - exp(-(log g_T - log g_D));
-      // candidate j = base + lane, the lowest accepted index wins.
+      // candidate j = base + lane, the lowest accepted index wins. Per
+      // component m the wave first stages, in LDS, the terms that do not
+      // depend on tau: log w_m - log sigma_m - log sqrt(2 pi), exp(-2 log
+      // sigma_m), mu_m, sigma_m for both mixtures and the running sum of w_m
+      // of the target; each lane then evaluates its candidate from LDS.
+      float *pre = acc_pre[threadIdx.x >> 6];
+      float *Ta = pre, *Te = pre + 64, *Tm = pre + 128, *Ts = pre + 192, *Tc = pre + 256;
+      float *Da = pre + 320, *De = pre + 384, *Dm = pre + 448;
+      if (lane < M) {
+        Ta[lane] = Tr[lane] - Tr[2 * M + lane] - 0.918938533204672742f;
+        Te[lane] = expf(-2.f * Tr[2 * M + lane]);
+        Tm[lane] = Tr[M + lane];
+        Ts[lane] = expf(Tr[2 * M + lane]);
+        Da[lane] = Dr[lane] - Dr[2 * M + lane] - 0.918938533204672742f;
+        De[lane] = expf(-2.f * Dr[2 * M + lane]);
+        Dm[lane] = Dr[M + lane];
+      }
+      float c = lane < M ? expf(Tr[lane]) : 0.f;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const float o = __shfl_up(c, off, 64);
+        if (lane >= off) c += o;
+      }
+      if (lane < M) Tc[lane] = c;
+      const float tot = __shfl(c, M - 1, 64);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      auto logpdf = [&](const float *A, const float *E, const float *Mu, float lt) {
+        float mx = -INFINITY;
+        for (int m = 0; m < M; ++m) {
+          const float z = lt - Mu[m];
+          mx = fmaxf(mx, A[m] - lt - 0.5f * z * z * E[m]);
+        }
+        float acc = 0.f;
+        for (int m = 0; m < M; ++m) {
+          const float z = lt - Mu[m];
+          acc += expf(A[m] - lt - 0.5f * z * z * E[m] - mx);
+        }
+        return mx + logf(acc);
+      };
       for (int base = 0;; base += 64) {
         if (base >= TPPSD_AR_ITER_CAP) {
           if (lane == 0) atomicOr(a.status, TPPSD_STATUS_AR_CAP);
@@ -1805,8 +1873,17 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
         }
         float u[4];
         philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)(base + lane), TAG_RES_T, u);
-        const float tau = sample_tau(Tr, Tr + M, Tr + 2 * M, M, u[0], u[1], u[2]);
-        const float delta = mix_logpdf(Tr, Tr + M, Tr + 2 * M, M, tau) - mix_logpdf(Dr, Dr + M, Dr + 2 * M, M, tau);
+        const float x = u[0] * tot;
+        int z = M - 1;
+        for (int m = 0; m < M; ++m)
+          if (x < Tc[m]) {
+            z = m;
+            break;
+          }
+        const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
+        const float tau = expf(Tm[z] + Ts[z] * eps);
+        const float lt = logf(tau);
+        const float delta = logpdf(Ta, Te, Tm, lt) - logpdf(Da, De, Dm, lt);
         const bool acc = delta > 0.f && u[3] < -expm1f(-delta);
         const uint64_t m = __ballot(acc);
         if (m) {
@@ -1822,23 +1899,20 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       tauL = a.d_tau[(size_t)b * MG + li];
     }
     if (!ak) {
-      // Eq. (4): k ~ norm(max(0, f_T - f_D))
+      // Eq. (4): k ~ norm(max(0, f_T - f_D)), lane kk holding type kk
       float u[4];
       philox_uniforms(a.seed, (uint64_t)b, r, 0ull, TAG_RES_K, u);
       const float *lT = a.v_logtype + ((size_t)b * (MG + 1) + li) * K;
       const float *lD = a.d_logtype + ((size_t)b * MG + li) * K;
-      float tot = 0.f;
-      for (int kk = 0; kk < K; ++kk) tot += fmaxf(0.f, expf(lT[kk]) - expf(lD[kk]));
-      const float x = u[0] * tot;
-      float c = 0.f;
-      kL = K - 1;
-      for (int kk = 0; kk < K; ++kk) {
-        c += fmaxf(0.f, expf(lT[kk]) - expf(lD[kk]));
-        if (x < c) {
-          kL = kk;
-          break;
-        }
+      float c = lane < K ? fmaxf(0.f, expf(lT[lane]) - expf(lD[lane])) : 0.f;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const float o = __shfl_up(c, off, 64);
+        if (lane >= off) c += o;
       }
+      const float tot = __shfl(c, K - 1, 64);
+      const unsigned long long hit = __ballot(lane < K && u[0] * tot < c);
+      kL = hit ? (int)__builtin_ctzll(hit) : K - 1;
       flags |= 2;
     } else {
       kL = a.d_k[(size_t)b * MG + li];
