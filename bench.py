@@ -79,16 +79,24 @@ def verify_pass_fraction(wl, gamma, B, verify_ms):
             "tflops": flop / (verify_ms * 1e-3) / 1e12 if verify_ms else None}
 
 
+def attention_source_sha256():
+    """SHA-256 over the sources that define the attention kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("tppsd_attention.hip", "tppsd_attention.h", "tppsd_device.h"):
+        with open(os.path.join(ROOT, "paper_2507_09252_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def measured_traffic(wl_name):
     """HBM bytes per verify-attention launch from the committed rocprofv3 --pmc
     runs, if the kernel source is unchanged since they were taken; else None."""
-    import hashlib
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "verify_attention_traffic.json")))
-        src = open(os.path.join(ROOT, "paper_2507_09252_amd", "csrc", "tppsd_kernels.hip"), "rb").read()
     except OSError:
         return None
-    if hashlib.sha256(src).hexdigest() != rec["kernel_source_sha256"]:
+    if attention_source_sha256() != rec["kernel_source_sha256"]:
         return None
     w = rec["workloads"].get(wl_name)
     return None if w is None else w["traffic_bytes_per_launch"]

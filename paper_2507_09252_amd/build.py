@@ -52,12 +52,14 @@ def build(verbose: bool = False) -> str:
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     os.makedirs(BUILD, exist_ok=True)
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
-    objs = []
-    for src in ("tppsd_kernels.hip", "tppsd.cpp"):
-        obj = os.path.join(BUILD, src + ".o")
-        lang = ["-x", "hip"] if src.endswith(".hip") else ["-x", "hip"]
-        _run([hipcc] + HIPCC_FLAGS + inc + lang + ["-c", os.path.join(CSRC, src), "-o", obj], verbose)
-        objs.append(obj)
+    from concurrent.futures import ThreadPoolExecutor
+    srcs = ("tppsd_kernels.hip", "tppsd_attention.hip", "tppsd.cpp")
+    objs = [os.path.join(BUILD, src + ".o") for src in srcs]
+    cmds = [[hipcc] + HIPCC_FLAGS + inc + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+            for src, obj in zip(srcs, objs)]
+    with ThreadPoolExecutor(len(cmds)) as ex:
+        for f in [ex.submit(_run, c, verbose) for c in cmds]:
+            f.result()
     tlib = _torch_lib_dir()
     tmp = LIB + ".tmp"
     _run(["g++", "-shared", "-o", tmp] + objs +

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "tppsd_attention.h"
+
 namespace tppsd {
 
 typedef uint16_t bf16_t;   // raw bfloat16 bits
@@ -151,29 +153,6 @@ void launch_gemm(const void *X, const LnA *ln, const void *W, int bf16, int T, i
                  hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // whether launch_gemm can take a LayerNorm operand of width K
 bool gemm_ln_fusable(int bf16, int K);
-// Positions per (sequence, head) slab of a KV cache: the event capacity
-// rounded up to a multiple of 8 (bf16 values are stored in 8-position blocks).
-inline int kv_stride(int cap) { return (cap + 7) / 8 * 8; }
-
-// Key splits of the attention for B sequences x H heads over at most max_keys
-// keys (one workgroup serves all query tiles of a pair): enough workgroups to
-// fill the chip, each split keeping at least 512 keys (shorter splits do not
-// pay for the merge launch).
-inline int attn_splits(int B, int H, int max_keys) {
-  const long items = (long)B * H;
-  int s = 1;
-  while (s < 8 && items * s < 1024 && max_keys / (2 * s) >= 512) s *= 2;
-  return s;
-}
-// floats of split partials for up to qtiles_max query tiles of 16
-inline size_t attn_part_floats(int B, int H, int dh, int qtiles_max, int max_keys) {
-  const int s = attn_splits(B, H, max_keys);
-  return s > 1 ? (size_t)B * H * qtiles_max * 16 * s * (dh + 2) : 0;
-}
-void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16,
-                      const int32_t *start, int start_off, const int32_t *done, int B, int P, int H,
-                      int dh, int cap, float *part, int verify, hipEvent_t ev0, hipEvent_t ev1,
-                      hipStream_t st);
 // decoder epilogue over the rows' logits [.., ldl] (mixture w | mu | log sigma, then types)
 void launch_head(const float *logits, int ldl, int M, int K, const HeadArgs &a, hipStream_t st);
 // the decoder's block-diagonal (3M + K) x 4d matrix and its bias (3M + K)
