@@ -385,7 +385,9 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const ELT *__restrict__ X, co
 }
 
 // LDS-staged GEMM with fp32 accumulation: a workgroup of 4 waves (2 x 2)
-// owns a BM x BN output tile and walks K in stages of BK = 2 MFMA k-steps.
+// owns a BM x BN output tile and walks K in stages of BK = KSN MFMA k-steps
+// (each stage costs a barrier and an LDS round trip, so tiles with few rows
+// and a long K take long stages).
 // The global loads of the next D stages are in flight in a register ring
 // while the current stage is multiplied out of LDS (double-buffered, one
 // barrier per stage). Rows of both LDS tiles are padded by one 16-byte vector
@@ -400,15 +402,15 @@ __global__ __launch_bounds__(256) void k_gemm_mfma(const ELT *__restrict__ X, co
 template <typename ELT> constexpr int gemm_bk() { return 2 * MfmaStep<ELT>::KSTEP; }
 constexpr int GEMM_LN_MAX_DEPTH = 8;
 
-template <typename ELT, int BM, int BN, bool LN, int D>
+template <typename ELT, int BM, int BN, bool LN, int D, int KSN>
 __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, const float *__restrict__ xf,
                                                   const float *__restrict__ lg, const float *__restrict__ lb,
                                                   const ELT *__restrict__ W, int T, int N, int K, Epi e) {
   typedef MfmaStep<ELT> S;
-  constexpr int KS = S::KSTEP, BK = 2 * KS;
+  constexpr int KS = S::KSTEP, BK = KSN * KS;
   constexpr int VE = 16 / sizeof(ELT);             // elements per 16-byte vector
   constexpr int LDR = BK + VE;                     // LDS row length (one vector of padding)
-  constexpr int VPR = BK / VE;                     // vectors per tile row per stage (8)
+  constexpr int VPR = BK / VE;                     // vectors per tile row per stage
   constexpr int AV = BM * VPR / 256, BV = BN * VPR / 256;
   constexpr int XV = LN ? VE / 4 : 1;              // float4 of x per A vector
   constexpr int TM = BM / 32, TN = BN / 32;
@@ -547,7 +549,7 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
         __syncthreads();
         if (!LN && st_i + D < nst) gload(ra[u], rx[u], rb[u], (st_i + D) * BK);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
+        for (int ks = 0; ks < KSN; ++ks) {
           typename S::frag a[TM], b[TN];
 #pragma unroll
           for (int i = 0; i < TM; ++i)
@@ -1484,20 +1486,28 @@ static void gemm_dispatch(const void *X, const LnA *ln, const void *W, int T, in
     hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, x, xf, lg, lb, w, T, N, K, epi);
   };
   if (!ln) {
-    if (big) go(k_gemm_lds<ELT, 64, 64, false, 2>, 64, 64);
-    else go(k_gemm_lds<ELT, 32, 32, false, 2>, 32, 32);
+    if (big) {
+      go(k_gemm_lds<ELT, 64, 64, false, 2, 2>, 64, 64);
+    } else {
+      // 32 x 32 tiles: 8 k-steps per stage for a long K over few workgroups,
+      // else 4 (more resident workgroups per CU)
+      const long tiles = (long)((N + 31) / 32) * ((T + 31) / 32);
+      if (K >= 512 && tiles < 512) go(k_gemm_lds<ELT, 32, 32, false, 2, 8>, 32, 32);
+      else go(k_gemm_lds<ELT, 32, 32, false, 2, 4>, 32, 32);
+    }
     return;
   }
-  // LayerNorm operand: the ring holds all of K (depth 2, 4 or 8 stages)
-  const int nst = (K + gemm_bk<ELT>() - 1) / gemm_bk<ELT>();
-  if (nst <= 2) {
-    if (big) go(k_gemm_lds<ELT, 64, 64, true, 2>, 64, 64);
-    else go(k_gemm_lds<ELT, 32, 32, true, 2>, 32, 32);
-  } else if (nst <= 4) {
-    if (big) go(k_gemm_lds<ELT, 64, 64, true, 4>, 64, 64);
-    else go(k_gemm_lds<ELT, 32, 32, true, 4>, 32, 32);
+  // LayerNorm operand: the ring holds all of K. 64 x 64 tiles with stages of
+  // 2 k-steps (ring depth 2 or 4) when they fill the chip, else 32 x 32 tiles
+  // with stages of 4 k-steps
+  constexpr int KS = MfmaStep<ELT>::KSTEP;
+  const int nst2 = (K + 2 * KS - 1) / (2 * KS), nst4 = (K + 4 * KS - 1) / (4 * KS);
+  if (big && nst2 <= 4) {
+    if (nst2 <= 2) go(k_gemm_lds<ELT, 64, 64, true, 2, 2>, 64, 64);
+    else go(k_gemm_lds<ELT, 64, 64, true, 4, 2>, 64, 64);
   } else {
-    go(k_gemm_lds<ELT, 32, 32, true, 8>, 32, 32);
+    if (nst4 <= 2) go(k_gemm_lds<ELT, 32, 32, true, 2, 4>, 32, 32);
+    else go(k_gemm_lds<ELT, 32, 32, true, 4, 4>, 32, 32);
   }
 }
 
