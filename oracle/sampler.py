@@ -211,6 +211,7 @@ class DraftOut:
     s: np.ndarray
     logtype: np.ndarray   # [B, g, K]
     cat_margin: np.ndarray  # [B, g]
+    rate: Optional[float] = None   # homogeneous-Poisson draft: its rate (mixture fields unused)
 
 
 @dataclasses.dataclass
@@ -260,6 +261,57 @@ def draft(D: Model, st: State, gamma: int, seed: int, rows) -> DraftOut:
                     cat_margin=st2["cm"])
 
 
+def poisson_fit(hist_t, hist_k, K: int):
+    """App. D.3: maximum-likelihood homogeneous Poisson draft from the data,
+    rate = n / T and mark probabilities p_m = n_m / n. Here the data are the
+    seed histories: n counts their inter-event intervals and T sums their time
+    spans (first to last event); the marks count every history event.
+    Returns (rate, log p [K]) with log 0 = -inf for unseen marks."""
+    hist_t = np.asarray(hist_t, dtype=np.float64)
+    hist_k = np.asarray(hist_k, dtype=np.int64)
+    n = hist_t.shape[0] * (hist_t.shape[1] - 1)
+    span = float(np.sum(hist_t[:, -1] - hist_t[:, 0]))
+    counts = np.bincount(hist_k.ravel(), minlength=K)[:K].astype(np.float64)
+    with np.errstate(divide="ignore"):
+        logp = np.log(counts / counts.sum())
+    return n / span, logp
+
+
+def draft_poisson(st: State, gamma: int, rate: float, logp, seed: int, rows) -> DraftOut:
+    """Homogeneous-Poisson drafting (App. D.3): the gamma intervals are
+    independent Exp(rate) draws and the marks independent draws from p, so
+    the whole block is drawn at once. Draft position l uses the counter
+    (sequence, round, l, DRAFT): tau = -ln(u_1) / rate by inversion of the
+    exponential CDF, k from p with u_3. The draft densities are
+    log g_D(tau) = log rate - rate tau and log f_D(k) = log p_k."""
+    rows = np.asarray(rows)
+    B = len(rows)
+    logp = np.asarray(logp, dtype=np.float64)
+    K = len(logp)
+    r = st.round
+    n = st.n[rows]
+    t_prev = st.t[rows, n - 1]
+    taus, ts, ks, lgs, lfs, cms = [], [], [], [], [], []
+    for l in range(1, gamma + 1):
+        U = uniforms(seed, st.seq0 + rows, r, l, TAG_DRAFT)
+        tau = f32(-np.log(U[:, 1]) / rate)
+        k, cm = categorical(np.broadcast_to(logp, (B, K)), U[:, 3])
+        t_hat = f32(t_prev + tau)
+        taus.append(tau)
+        ts.append(t_hat)
+        ks.append(k)
+        lgs.append(np.log(rate) - rate * tau)
+        lfs.append(logp[k])
+        cms.append(cm)
+        t_prev = t_hat
+    st2 = {key: np.stack(v, axis=1) for key, v in
+           (("tau", taus), ("t", ts), ("k", ks), ("logg", lgs), ("logf", lfs), ("cm", cms))}
+    zeros = np.zeros((B, gamma, 1))
+    return DraftOut(tau=st2["tau"], t=st2["t"], k=st2["k"], logg=st2["logg"], logf=st2["logf"],
+                    logw=zeros, mu=zeros, s=zeros,
+                    logtype=np.broadcast_to(logp, (B, gamma, K)).copy(), cat_margin=st2["cm"], rate=rate)
+
+
 def verify(T: Model, st: State, dr: DraftOut, rows) -> VerifyOut:
     """Verification (§4.3): one target pass over the pending event and the gamma
     drafts gives gamma + 1 decoder outputs; row l - 1 scores draft l."""
@@ -276,8 +328,11 @@ def verify(T: Model, st: State, dr: DraftOut, rows) -> VerifyOut:
 
 
 def resid_time(Tw, Tmu, Ts, Dw, Dmu, Ds, seed: int, b: int, r: int, literal_target=False,
-               first_chunk=None):
+               first_chunk=None, draft_rate=None):
     """Theorem 1: draw from g' = norm(max(0, g_T - g_D)) by acceptance-rejection.
+
+    g_D is the draft's log-normal mixture (Dw, Dmu, Ds), or the exponential
+    density of a homogeneous-Poisson draft when ``draft_rate`` is given.
 
     Candidates tau ~ g_T; accept iff u_a < max(0, g_T - g_D) / g_T = 1 - exp(-delta)
     with delta = log g_T(tau) - log g_D(tau) > 0. Candidate j uses the counter
@@ -296,7 +351,9 @@ def resid_time(Tw, Tmu, Ts, Dw, Dmu, Ds, seed: int, b: int, r: int, literal_targ
         tau = f32(np.exp(Tmu[z] + np.exp(Ts[z]) * eps))
         if literal_target:
             return tau[0], base, np.inf, float(zm[0])
-        delta = mixture_logpdf(Tw, Tmu, Ts, tau) - mixture_logpdf(Dw, Dmu, Ds, tau)
+        log_gd = (np.log(draft_rate) - draft_rate * tau) if draft_rate is not None \
+            else mixture_logpdf(Dw, Dmu, Ds, tau)
+        delta = mixture_logpdf(Tw, Tmu, Ts, tau) - log_gd
         with np.errstate(divide="ignore"):
             thresh = np.where(delta > 0, np.log(-np.expm1(-np.maximum(delta, 1e-300))), -np.inf)
         lu = np.log(U[:, 3])
@@ -387,7 +444,7 @@ def accept(st: State, gamma: int, dr: DraftOut, vf: VerifyOut, seed: int, rows, 
                                               dr.logw[i, li], dr.mu[i, li], dr.s[i, li], seed,
                                               st.seq0 + b, r,
                                               literal_target=resample_from_target,
-                                              first_chunk=U_rest[i])
+                                              first_chunk=U_rest[i], draft_rate=dr.rate)
                 res["ar_iter"][i] = j
                 st.ar_iters_total += j + 1
                 log_m[li] = min(log_m[li], lm)
@@ -446,6 +503,25 @@ def sd_round(T: Model, D: Model, st: State, gamma: int, seed: int, bonus=True, *
     res = accept(st, gamma, dr, vf, seed, rows, bonus=bonus, **kw)
     st.round += 1
     return dr, vf, res
+
+
+def sd_round_poisson(T: Model, st: State, gamma: int, rate: float, logp, seed: int, bonus=True, **kw):
+    rows = np.nonzero(~st.done)[0]
+    if len(rows) == 0:
+        return None
+    dr = draft_poisson(st, gamma, rate, logp, seed, rows)
+    vf = verify(T, st, dr, rows)
+    res = accept(st, gamma, dr, vf, seed, rows, bonus=bonus, **kw)
+    st.round += 1
+    return dr, vf, res
+
+
+def sample_sd_poisson(T: Model, hist_t, hist_k, n_gen: int, gamma: int, rate: float, logp, seed: int,
+                      bonus=True, seq0: int = 0, **kw) -> State:
+    st = prefill(T, None, hist_t, hist_k, n_gen, seq0=seq0)
+    while not np.all(st.done):
+        sd_round_poisson(T, st, gamma, rate, logp, seed, bonus=bonus, **kw)
+    return st
 
 
 def sample_sd(T: Model, D: Model, hist_t, hist_k, n_gen: int, gamma: int, seed: int,
