@@ -39,6 +39,7 @@ def parse():
     ap.add_argument("--gamma", type=int, default=None)
     ap.add_argument("--ar-steps", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-poisson", action="store_true", help="skip the homogeneous-Poisson draft run")
     ap.add_argument("--cpu-events", type=int, default=64, help="oracle sample: events per sequence")
     ap.add_argument("--cpu-seqs", type=int, default=4, help="oracle sample: sequences")
     return ap.parse_args()
@@ -190,6 +191,39 @@ def main():
         ar_value = events * args.ar_steps / t_ar
     value = events * args.steps / t_sd
     alpha = st["accepted"] / max(1, st["drafted"])
+    poisson = None
+    if not args.no_poisson:
+        # the same job with the homogeneous-Poisson draft (no draft model),
+        # fitted once on the device from the seed histories
+        params = tp.tppsd_poisson_fit(HT, HK, wl.target.n_types)
+        sp = tp.State(tm, None, B, cap, gamma, seed=1234)
+
+        def sp_job():
+            sp.tppsd_prefill(HT, HK, n_gen)
+            return sp.tppsd_sample_sd_poisson(gamma, params)
+
+        sp_job()
+        torch.cuda.synchronize()
+        p_rounds = 0
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            p_rounds += sp_job()
+        torch.cuda.synchronize()
+        t_sp = time.perf_counter() - t0
+        sps = sp.tppsd_state_status()
+        assert sps["bits"] == 0 and sps["n_done"] == B, sps
+        sp.tppsd_timing_enable(tp.TIME_PHASES)
+        sp_job()
+        pph = sp.tppsd_timing_read()
+        sp.tppsd_timing_enable(0)
+        p_nr = max(1, pph["rounds"])
+        p_value = events * args.steps / t_sp
+        poisson = {"value": p_value, "unit": "events/s", "alpha": sps["accepted"] / max(1, sps["drafted"]),
+                   "speedup_vs_gpu_ar": None, "rounds_per_job": p_rounds / args.steps,
+                   "ar_candidates_per_job": sps["ar_candidates"],
+                   "round_us": {"draft": pph["draft_ms"] * 1e3 / p_nr, "verify": pph["verify_ms"] * 1e3 / p_nr,
+                                "accept": pph["accept_ms"] * 1e3 / p_nr, "rounds": pph["rounds"]}}
+        del sp
     per_launch = attention_bytes_per_launch(wl, gamma, B)
     avg_ms = attn_ms / max(1, attn_launches)
     achieved = per_launch / (avg_ms * 1e-3) / 1e9 if attn_launches else 0.0
@@ -228,6 +262,9 @@ def main():
     out["round_us"] = {"draft": tph["draft_ms"] * 1e3 / nr, "verify": tph["verify_ms"] * 1e3 / nr,
                        "accept": tph["accept_ms"] * 1e3 / nr, "rounds": tph["rounds"]}
     out["verify_pass"] = verify_pass_fraction(wl, gamma, B, tph["verify_ms"] / nr)
+    if poisson is not None:
+        poisson["speedup_vs_gpu_ar"] = poisson["value"] / ar_value if ar_value else None
+        out["poisson_draft"] = poisson
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, gamma, wt, wd, ht, hk, min(args.cpu_seqs, B),
                                            min(args.cpu_events, n_gen))

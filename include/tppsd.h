@@ -98,6 +98,9 @@ typedef struct {
   float   *logf;     /* [B, max_gamma]           log f_D(k_hat_l)                */
   float   *mix;      /* [B, max_gamma, 3, M]     draft (log w, mu, log sigma)    */
   float   *logtype;  /* [B, max_gamma, K]        draft log f_D                   */
+  float   *rate;     /* [B] NULL for a Transformer draft. Non-NULL marks a
+                        homogeneous-Poisson draft (tppsd_draft_poisson writes
+                        its rate here; `mix` is then unused and may be NULL) */
 } tppsd_draft_buf;
 
 /* Verification output (§4.3 "Verification"): the target's decoder output for
@@ -178,7 +181,8 @@ int tppsd_prefill(tppsd_state *s, const float *d_t, const int32_t *d_k, int n0, 
  * from the draft model for every unfinished sequence, using the Philox
  * counters (sequence, round, l, DRAFT). Fills `out` (all of it, for positions
  * 0..gamma-1). Errors: TPPSD_E_ARG (gamma outside 1..max_gamma, null buffer
- * pointer), TPPSD_E_ORDER (no prefill, or no draft model), TPPSD_E_HIP. */
+ * pointer, out->rate not NULL), TPPSD_E_ORDER (no prefill, or no draft model),
+ * TPPSD_E_HIP. */
 int tppsd_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t stream);
 
 /* Verification (§4.3 "Verification"): one parallel target pass over the
@@ -193,7 +197,8 @@ int tppsd_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tpp
  * Position l passes iff ln u_tau < log g_T - log g_D and ln u_k < log f_T -
  * log f_D; L is the first failing position. At L each failed component is
  * redrawn from its adjusted distribution (Theorem 1 acceptance-rejection for
- * the interval, Eq. (4) for the type) and each passed component is kept; if
+ * the interval with the draft's g_D, the exponential density when draft->rate
+ * is not NULL; Eq. (4) for the type) and each passed component is kept; if
  * none failed and TPPSD_FLAG_BONUS is set, one event is drawn from the
  * target's row gamma. Events are appended (truncated at n_gen per sequence)
  * and the KV cache lengths move to the committed prefix. d_uniforms, if not
@@ -219,6 +224,40 @@ int tppsd_sample_ar(tppsd_state *s, int n_events, float *d_t_out, int32_t *d_k_o
  * counter back from the device once per round (one round behind). Returns the
  * number of rounds run in *rounds (may be NULL). Errors: as tppsd_draft. */
 int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipStream_t stream);
+
+/* ---- homogeneous-Poisson draft (App. D.3) ------------------------------------
+ * A draft with no model: intervals Exp(rate), marks drawn from fixed
+ * probabilities p, both maximum-likelihood estimates from observed sequences.
+ * Parameters live on the device as d_params [1 + K] = (rate, log p_0 .. log
+ * p_{K-1}), log 0 = -inf; K is the target's n_types. Such a state needs no
+ * draft model (tppsd_state_create with draft NULL). */
+
+/* Maximum-likelihood fit over B sequences of n0 events d_t/d_k [B, n0]
+ * (device, strictly increasing times): rate = B (n0 - 1) / sum of the spans
+ * t[n0-1] - t[0]; p_m = count of type m / count of types in [0, K) (types
+ * outside it are ignored). Writes d_params [1 + K] (device). One workgroup,
+ * enqueued on `stream`. Errors: TPPSD_E_ARG (null pointer, B < 1, n0 < 2,
+ * K outside 1..TPPSD_MAX_TYPES, B * n0 >= 2^31), TPPSD_E_HIP. */
+int tppsd_poisson_fit(const float *d_t, const int32_t *d_k, int B, int n0, int K, float *d_params,
+                      hipStream_t stream);
+
+/* Drafting from the Poisson draft: for every unfinished sequence, gamma
+ * independent draws with the Philox counters (sequence, round, l, DRAFT):
+ * tau_l = -ln(u_1) / rate, k_l the first m with u_3 * sum(p) < p_0 + .. + p_m.
+ * Writes tau, t, k, logg = log rate - rate tau, logf = log p_k, logtype (log p
+ * at every position) and rate[b]; out->rate must not be NULL. The buffer then
+ * goes to tppsd_verify and tppsd_accept as usual; accept's Theorem-1 loop uses
+ * the exponential density as g_D and Eq. (4) uses p as f_D. Errors:
+ * TPPSD_E_ARG (gamma outside 1..max_gamma, null pointer), TPPSD_E_ORDER (no
+ * prefill), TPPSD_E_HIP. */
+int tppsd_draft_poisson(tppsd_state *s, int gamma, const float *d_params, const tppsd_draft_buf *out,
+                        hipStream_t stream);
+
+/* tppsd_sample_sd with the Poisson draft of d_params (device, kept alive and
+ * unchanged while the call's work runs; graphs captured here embed the
+ * pointer). Errors: as tppsd_draft_poisson. */
+int tppsd_sample_sd_poisson(tppsd_state *s, int gamma, const float *d_params, int max_rounds, int *rounds,
+                            hipStream_t stream);
 
 /* Copies the committed events (history included) to d_t/d_k [B, max_events]
  * and the per-sequence event counts to d_n [B]. Any pointer may be NULL. */

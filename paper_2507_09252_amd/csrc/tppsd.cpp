@@ -189,6 +189,7 @@ struct tppsd_state {
   int32_t *gen0 = nullptr;
   // internal round buffers (tppsd_sample_sd)
   tppsd_draft_buf idr{};
+  tppsd_draft_buf idr_p{};   // the same with the rate array (Poisson draft)
   tppsd_verify_buf ivf{};
   tppsd_accept_buf iac{};
   // host-side run state
@@ -215,6 +216,7 @@ struct tppsd_state {
   bool fused_draft = true;   // one-launch drafting when the draft model fits it
   hipGraphExec_t sd_exec[2] = {nullptr, nullptr};
   long long sd_key = -1;
+  const float *sd_params = nullptr, *phase_params = nullptr;   // Poisson draft parameters the graphs embed
   hipGraphExec_t ar_exec[2] = {nullptr, nullptr};   // 1 step, AR_CHUNK steps
   long long ar_key[2] = {-1, -1};
 };
@@ -231,7 +233,7 @@ struct WsLayout {
   size_t freqT, freqD, kT, vT, kD, vD, layerT, layerD;
   size_t x, a, q, o, hid, e, ar_mix, ar_lt, attn_part, gen0;
   size_t logits, hwT, hbT, hwD, hbD;
-  size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt;
+  size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt, d_rate;
   size_t v_logg, v_logf, v_mix, v_lt;
   size_t a_L, a_nnew, a_knew, a_tnew, a_taunew, a_ar, a_flags;
 };
@@ -301,6 +303,7 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   w.d_logf = take(Bz * MG * 4);
   w.d_mix = take(Bz * MG * 3 * M * 4);
   w.d_lt = take(Bz * MG * K * 4);
+  w.d_rate = take(Bz * 4);
   w.v_logg = take(Bz * MG * 4);
   w.v_logf = take(Bz * MG * 4);
   w.v_mix = take(Bz * (MG + 1) * 3 * M * 4);
@@ -414,7 +417,7 @@ HeadArgs head_common(tppsd_state *s) {
 }
 
 int check_draft_buf(const tppsd_draft_buf *b) {
-  if (!b || !b->tau || !b->t || !b->k || !b->logg || !b->logf || !b->mix || !b->logtype)
+  if (!b || !b->tau || !b->t || !b->k || !b->logg || !b->logf || (!b->mix && !b->rate) || !b->logtype)
     return fail(TPPSD_E_ARG, "draft buffer has a null pointer");
   return TPPSD_OK;
 }
@@ -528,6 +531,31 @@ int do_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t 
   return hip_check("tppsd_draft");
 }
 
+int do_draft_poisson(tppsd_state *s, int gamma, const float *params, const tppsd_draft_buf *out, hipStream_t st) {
+  PoissonDraftArgs a{};
+  a.B = s->B;
+  a.gamma = gamma;
+  a.K = s->T->cfg.n_types;
+  a.MG = s->max_gamma;
+  a.params = params;
+  a.ev_t = s->ev_t;
+  a.ev_stride = s->cap;
+  a.n = s->n;
+  a.done = s->done;
+  a.rnd = s->rnd;
+  a.seed = s->seed;
+  a.status = s->status;
+  a.d_tau = out->tau;
+  a.d_t = out->t;
+  a.d_k = out->k;
+  a.d_logg = out->logg;
+  a.d_logf = out->logf;
+  a.d_logtype = out->logtype;
+  a.d_rate = out->rate;
+  launch_draft_poisson(a, st);
+  return hip_check("tppsd_draft_poisson");
+}
+
 int do_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_verify_buf *out, hipStream_t st) {
   TokSrc src{};
   src.ev_t = s->ev_t;
@@ -580,6 +608,7 @@ int do_accept(tppsd_state *s, int gamma, const tppsd_draft_buf *dr, const tppsd_
   a.v_mix = vf->mix;
   a.v_logtype = vf->logtype;
   a.uniforms = u;
+  a.d_rate = dr->rate;
   a.L = out->L;
   a.n_new = out->n_new;
   a.k_new = out->k_new;
@@ -754,7 +783,9 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->attn_part = (float *)(ws + w.attn_part);
   s->gen0 = (int32_t *)(ws + w.gen0);
   s->idr = {(float *)(ws + w.d_tau), (float *)(ws + w.d_t), (int32_t *)(ws + w.d_k), (float *)(ws + w.d_logg),
-            (float *)(ws + w.d_logf), (float *)(ws + w.d_mix), (float *)(ws + w.d_lt)};
+            (float *)(ws + w.d_logf), (float *)(ws + w.d_mix), (float *)(ws + w.d_lt), nullptr};
+  s->idr_p = s->idr;
+  s->idr_p.rate = (float *)(ws + w.d_rate);
   s->ivf = {(float *)(ws + w.v_logg), (float *)(ws + w.v_logf), (float *)(ws + w.v_mix), (float *)(ws + w.v_lt)};
   s->iac = {(int32_t *)(ws + w.a_L),      (int32_t *)(ws + w.a_nnew), (int32_t *)(ws + w.a_knew),
             (float *)(ws + w.a_tnew),     (float *)(ws + w.a_taunew), (int32_t *)(ws + w.a_ar),
@@ -867,12 +898,31 @@ static int check_round(tppsd_state *s, int gamma) {
 int tppsd_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
   if (int rc = check_round(s, gamma)) return rc;
   if (int rc = check_draft_buf(out)) return rc;
+  if (out->rate) return fail(TPPSD_E_ARG, "tppsd_draft needs out->rate == NULL (it marks a Poisson draft)");
+  if (!out->mix) return fail(TPPSD_E_ARG, "draft buffer has a null pointer");
   if (!s->D) return fail(TPPSD_E_ORDER, "state has no draft model");
   if (!s->draft_ok)
     return fail(TPPSD_E_ORDER, "draft cache is stale (AR sampling or an external draft ran since prefill)");
   int rc = do_draft(s, gamma, out, st);
   if (rc == TPPSD_OK) s->drafted_this_round = true;
   return rc;
+}
+
+int tppsd_draft_poisson(tppsd_state *s, int gamma, const float *d_params, const tppsd_draft_buf *out,
+                        hipStream_t st) {
+  if (int rc = check_round(s, gamma)) return rc;
+  if (int rc = check_draft_buf(out)) return rc;
+  if (!out->rate || !d_params) return fail(TPPSD_E_ARG, "Poisson draft needs out->rate and d_params");
+  return do_draft_poisson(s, gamma, d_params, out, st);
+}
+
+int tppsd_poisson_fit(const float *d_t, const int32_t *d_k, int B, int n0, int K, float *d_params, hipStream_t st) {
+  if (!d_t || !d_k || !d_params) return fail(TPPSD_E_ARG, "null argument");
+  if (B < 1 || n0 < 2) return fail(TPPSD_E_ARG, "need B >= 1 and n0 >= 2");
+  if (K < 1 || K > TPPSD_MAX_TYPES) return fail(TPPSD_E_ARG, "K %d outside 1..%d", K, TPPSD_MAX_TYPES);
+  if ((long long)B * n0 >= (1LL << 31)) return fail(TPPSD_E_ARG, "B * n0 too large");
+  launch_poisson_fit(d_t, d_k, B, n0, K, d_params, st);
+  return hip_check("tppsd_poisson_fit");
 }
 
 int tppsd_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_verify_buf *out, hipStream_t st) {
@@ -1015,10 +1065,14 @@ int make_events(std::vector<hipEvent_t> *v, size_t n) {
 }
 }  // namespace
 
-int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipStream_t st) {
-  if (int rc = check_round(s, gamma)) return rc;
-  if (!s->D) return fail(TPPSD_E_ORDER, "state has no draft model");
-  if (!s->draft_ok) return fail(TPPSD_E_ORDER, "draft cache is stale; prefill again");
+namespace {
+// Rounds of draft, verify and accept on the internal buffers; params == NULL
+// drafts from the draft model, otherwise from the Poisson draft of params.
+int sd_loop(tppsd_state *s, int gamma, const float *params, int max_rounds, int *rounds, hipStream_t st) {
+  const tppsd_draft_buf *dbuf = params ? &s->idr_p : &s->idr;
+  auto draft = [&](hipStream_t cs) {
+    return params ? do_draft_poisson(s, gamma, params, dbuf, cs) : do_draft(s, gamma, dbuf, cs);
+  };
   // kernel timing launches the rounds directly so that host-recorded HIP
   // events can bracket single kernels; otherwise each round replays one
   // captured graph, or three (draft, verify, accept) when phases are timed
@@ -1026,28 +1080,31 @@ int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipS
   const bool phases = (s->timing & TPPSD_TIME_PHASES) != 0;
   const bool graphs = s->use_graphs && !kern;
   const long long key = (long long)gamma * 100000007LL + s->n_gen;
-  if (graphs && !phases && (!s->sd_exec[0] || s->sd_key != key)) {
+  if (graphs && !phases && (!s->sd_exec[0] || s->sd_key != key || s->sd_params != params)) {
     drop_graph(&s->sd_exec[0]);
+    s->sd_key = -1;
     int rc = capture(s, [&](hipStream_t cs) {
-      int r = do_draft(s, gamma, &s->idr, cs);
-      if (!r) r = do_verify(s, gamma, &s->idr, &s->ivf, cs);
-      if (!r) r = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, cs);
+      int r = draft(cs);
+      if (!r) r = do_verify(s, gamma, dbuf, &s->ivf, cs);
+      if (!r) r = do_accept(s, gamma, dbuf, &s->ivf, nullptr, &s->iac, cs);
       return r;
     }, &s->sd_exec[0]);
     if (rc) return rc;
     s->sd_key = key;
+    s->sd_params = params;
   }
-  if (graphs && phases && (!s->phase_exec[0] || s->phase_key != key)) {
+  if (graphs && phases && (!s->phase_exec[0] || s->phase_key != key || s->phase_params != params)) {
     for (hipGraphExec_t &g : s->phase_exec) drop_graph(&g);
-    int rc = capture(s, [&](hipStream_t cs) { return do_draft(s, gamma, &s->idr, cs); }, &s->phase_exec[0]);
+    s->phase_key = -1;
+    int rc = capture(s, draft, &s->phase_exec[0]);
     if (!rc)
-      rc = capture(s, [&](hipStream_t cs) { return do_verify(s, gamma, &s->idr, &s->ivf, cs); },
-                   &s->phase_exec[1]);
+      rc = capture(s, [&](hipStream_t cs) { return do_verify(s, gamma, dbuf, &s->ivf, cs); }, &s->phase_exec[1]);
     if (!rc)
-      rc = capture(s, [&](hipStream_t cs) { return do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, cs); },
+      rc = capture(s, [&](hipStream_t cs) { return do_accept(s, gamma, dbuf, &s->ivf, nullptr, &s->iac, cs); },
                    &s->phase_exec[2]);
     if (rc) return rc;
     s->phase_key = key;
+    s->phase_params = params;
   }
   if (kern) {
     const tppsd_model *m = s->T;
@@ -1078,11 +1135,11 @@ int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipS
       hipEvent_t *pe = phases ? s->pev[r & 1].data() : nullptr;
       s->cur_ev = kern ? s->gev[r & 1].data() : nullptr;
       int rc = pe ? hip_check_rc(hipEventRecord(pe[0], st)) : 0;
-      if (!rc) rc = do_draft(s, gamma, &s->idr, st);
+      if (!rc) rc = draft(st);
       if (!rc && pe) rc = hip_check_rc(hipEventRecord(pe[1], st));
-      if (!rc) rc = do_verify(s, gamma, &s->idr, &s->ivf, st);
+      if (!rc) rc = do_verify(s, gamma, dbuf, &s->ivf, st);
       if (!rc && pe) rc = hip_check_rc(hipEventRecord(pe[2], st));
-      if (!rc) rc = do_accept(s, gamma, &s->idr, &s->ivf, nullptr, &s->iac, st);
+      if (!rc) rc = do_accept(s, gamma, dbuf, &s->ivf, nullptr, &s->iac, st);
       if (!rc && pe) rc = hip_check_rc(hipEventRecord(pe[3], st));
       s->cur_ev = nullptr;
       if (rc) return rc;
@@ -1097,6 +1154,25 @@ int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipS
   }
   if (rounds) *rounds = r;
   return hip_check("tppsd_sample_sd");
+}
+}  // namespace
+
+int tppsd_sample_sd(tppsd_state *s, int gamma, int max_rounds, int *rounds, hipStream_t st) {
+  if (int rc = check_round(s, gamma)) return rc;
+  if (!s->D) return fail(TPPSD_E_ORDER, "state has no draft model");
+  if (!s->draft_ok) return fail(TPPSD_E_ORDER, "draft cache is stale; prefill again");
+  return sd_loop(s, gamma, nullptr, max_rounds, rounds, st);
+}
+
+int tppsd_sample_sd_poisson(tppsd_state *s, int gamma, const float *d_params, int max_rounds, int *rounds,
+                            hipStream_t st) {
+  if (int rc = check_round(s, gamma)) return rc;
+  if (!d_params) return fail(TPPSD_E_ARG, "null d_params");
+  int r = 0;
+  const int rc = sd_loop(s, gamma, d_params, max_rounds, &r, st);
+  if (r > 0 || rc != TPPSD_OK) s->draft_ok = false;   // the draft model's cache missed these rounds
+  if (rounds) *rounds = r;
+  return rc;
 }
 
 int tppsd_read_events(tppsd_state *s, float *d_t, int32_t *d_k, int32_t *d_n, hipStream_t st) {

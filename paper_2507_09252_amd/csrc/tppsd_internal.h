@@ -87,6 +87,7 @@ struct AcceptArgs {
   const int32_t *d_k;
   const float *v_logg, *v_logf, *v_mix, *v_logtype;
   const float *uniforms;    // nullable [B, max_gamma, 2]
+  const float *d_rate;      // nullable [B]: homogeneous-Poisson draft rate (g_D exponential)
   int32_t *L, *n_new, *k_new, *ar_iter;
   float *t_new, *tau_new;
   uint8_t *flags;
@@ -135,6 +136,21 @@ inline bool fused_draft_ok(int L, int d, int H, int F) {
          F / 8 <= 64 && pow2(H) && d == 16 * H;
 }
 size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H);
+
+// Homogeneous-Poisson drafting (tppsd_poisson.hip)
+struct PoissonDraftArgs {
+  int B, gamma, K, MG;
+  const float *params;      // [1 + K]: rate, log p
+  const float *ev_t;
+  int ev_stride;
+  const int32_t *n, *done, *rnd;
+  uint64_t seed;
+  uint32_t *status;
+  float *d_tau, *d_t, *d_logg, *d_logf, *d_logtype, *d_rate;
+  int32_t *d_k;
+};
+void launch_poisson_fit(const float *t, const int32_t *k, int B, int n0, int K, float *params, hipStream_t st);
+void launch_draft_poisson(const PoissonDraftArgs &a, hipStream_t st);
 
 // ---- launchers (tppsd_kernels.hip) ----
 void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t st);

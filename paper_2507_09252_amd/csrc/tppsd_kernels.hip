@@ -16,41 +16,10 @@
 #include <stdint.h>
 
 #include "tppsd_device.h"
+#include "tppsd_philox.h"
 #include "../../include/tppsd.h"
 
 namespace tppsd {
-
-// ---------------------------------------------------------------------------
-// Philox4x64-10 (Salmon et al., SC'11) and uniforms on the 2^-24 odd grid
-// ---------------------------------------------------------------------------
-
-enum { TAG_AR = 1, TAG_DRAFT = 2, TAG_ACCEPT = 3, TAG_RES_T = 4, TAG_RES_K = 5, TAG_BONUS = 6 };
-
-__device__ __forceinline__ void philox_uniforms(uint64_t seed, uint64_t c0, uint64_t c1, uint64_t c2,
-                                                uint64_t c3, float u[4]) {
-  uint64_t x0 = c0, x1 = c1, x2 = c2, x3 = c3;
-  uint64_t k0 = seed, k1 = 0;
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
-    if (r) {
-      k0 += 0x9E3779B97F4A7C15ull;
-      k1 += 0xBB67AE8584CAA73Bull;
-    }
-    const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
-    uint64_t lo0 = m0 * x0, hi0 = __umul64hi(m0, x0);
-    uint64_t lo1 = m1 * x2, hi1 = __umul64hi(m1, x2);
-    uint64_t y0 = hi1 ^ x1 ^ k0, y2 = hi0 ^ x3 ^ k1;
-    x0 = y0;
-    x1 = lo1;
-    x2 = y2;
-    x3 = lo0;
-  }
-  // top 23 bits -> (2 m + 1) 2^-24, exact in float32
-  u[0] = (float)(2ull * (x0 >> 41) + 1ull) * 0x1p-24f;
-  u[1] = (float)(2ull * (x1 >> 41) + 1ull) * 0x1p-24f;
-  u[2] = (float)(2ull * (x2 >> 41) + 1ull) * 0x1p-24f;
-  u[3] = (float)(2ull * (x3 >> 41) + 1ull) * 0x1p-24f;
-}
 
 // ---------------------------------------------------------------------------
 // decoder math (log-normal mixture of §4.2; sampling as in App. A.1)
@@ -1247,7 +1216,12 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   if (L <= G) {
     const int li = L - 1;
     const float *Tr = a.v_mix + ((size_t)b * (MG + 1) + li) * 3 * M;
-    const float *Dr = a.d_mix + ((size_t)b * MG + li) * 3 * M;
+    // g_D: the draft's mixture, or the exponential density of a
+    // homogeneous-Poisson draft (App. D.3), log g_D = log rate - rate tau
+    const bool pois = a.d_rate != nullptr;
+    const float rate = pois ? a.d_rate[b] : 0.f;
+    const float lrate = pois ? logf(rate) : 0.f;
+    const float *Dr = pois ? nullptr : a.d_mix + ((size_t)b * MG + li) * 3 * M;
     if (!at) {
       // Theorem 1: candidates tau ~ g_T, accept iff u_a < 1 - exp(-(log g_T - log g_D));
       // candidate j = base + lane, the lowest accepted index wins. Per
@@ -1263,9 +1237,11 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
         Te[lane] = expf(-2.f * Tr[2 * M + lane]);
         Tm[lane] = Tr[M + lane];
         Ts[lane] = expf(Tr[2 * M + lane]);
-        Da[lane] = Dr[lane] - Dr[2 * M + lane] - 0.918938533204672742f;
-        De[lane] = expf(-2.f * Dr[2 * M + lane]);
-        Dm[lane] = Dr[M + lane];
+        if (!pois) {
+          Da[lane] = Dr[lane] - Dr[2 * M + lane] - 0.918938533204672742f;
+          De[lane] = expf(-2.f * Dr[2 * M + lane]);
+          Dm[lane] = Dr[M + lane];
+        }
       }
       float c = lane < M ? expf(Tr[lane]) : 0.f;
 #pragma unroll
@@ -1309,7 +1285,8 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
         const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
         const float tau = expf(Tm[z] + Ts[z] * eps);
         const float lt = logf(tau);
-        const float delta = logpdf(Ta, Te, Tm, lt) - logpdf(Da, De, Dm, lt);
+        const float lgd = pois ? lrate - rate * tau : logpdf(Da, De, Dm, lt);
+        const float delta = logpdf(Ta, Te, Tm, lt) - lgd;
         const bool acc = delta > 0.f && u[3] < -expm1f(-delta);
         const uint64_t m = __ballot(acc);
         if (m) {

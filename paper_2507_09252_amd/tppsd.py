@@ -31,6 +31,7 @@ EXPORTS = [
     "tppsd_state_bytes", "tppsd_state_create", "tppsd_state_destroy", "tppsd_prefill", "tppsd_draft",
     "tppsd_verify", "tppsd_accept", "tppsd_sample_ar", "tppsd_sample_sd", "tppsd_read_events",
     "tppsd_state_status", "tppsd_timing_enable", "tppsd_timing_read", "tppsd_last_error",
+    "tppsd_poisson_fit", "tppsd_draft_poisson", "tppsd_sample_sd_poisson",
 ]
 
 
@@ -55,7 +56,7 @@ class ModelCfgC(ctypes.Structure):
 
 
 class DraftBufC(ctypes.Structure):
-    _fields_ = [(n, c_void_p) for n in ("tau", "t", "k", "logg", "logf", "mix", "logtype")]
+    _fields_ = [(n, c_void_p) for n in ("tau", "t", "k", "logg", "logf", "mix", "logtype", "rate")]
 
 
 class VerifyBufC(ctypes.Structure):
@@ -99,6 +100,9 @@ def lib():
         "tppsd_timing_enable": (c_int, [c_void_p, c_int]),
         "tppsd_timing_read": (c_int, [c_void_p, P(TimingC)]),
         "tppsd_last_error": (c_char_p, []),
+        "tppsd_poisson_fit": (c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p, c_void_p]),
+        "tppsd_draft_poisson": (c_int, [c_void_p, c_int, c_void_p, P(DraftBufC), c_void_p]),
+        "tppsd_sample_sd_poisson": (c_int, [c_void_p, c_int, c_void_p, c_int, P(c_int), c_void_p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -181,23 +185,39 @@ class Model:
             self.handle = None
 
 
+def tppsd_poisson_fit(t: torch.Tensor, k: torch.Tensor, K: int) -> torch.Tensor:
+    """Homogeneous-Poisson draft parameters [1 + K] (rate, log p) fitted on the
+    device from sequences t/k [B, n0]."""
+    t = t.to(torch.float32).contiguous()
+    k = k.to(torch.int32).contiguous()
+    params = torch.empty(1 + K, dtype=torch.float32, device=t.device)
+    _check(lib().tppsd_poisson_fit(_ptr(t), _ptr(k), t.shape[0], t.shape[1], K, _ptr(params), _stream()))
+    return params
+
+
 # ---------------------------------------------------------------------------
 # round buffers
 # ---------------------------------------------------------------------------
 
 class DraftBuffers:
-    def __init__(self, B, max_gamma, M, K, device="cuda"):
+    """Draft record; poisson=True makes the record of a homogeneous-Poisson
+    draft (a rate array, no mixture)."""
+
+    def __init__(self, B, max_gamma, M, K, device="cuda", poisson=False):
         f = dict(dtype=torch.float32, device=device)
         self.tau = torch.zeros(B, max_gamma, **f)
         self.t = torch.zeros(B, max_gamma, **f)
         self.k = torch.zeros(B, max_gamma, dtype=torch.int32, device=device)
         self.logg = torch.zeros(B, max_gamma, **f)
         self.logf = torch.zeros(B, max_gamma, **f)
-        self.mix = torch.zeros(B, max_gamma, 3, M, **f)
+        self.mix = None if poisson else torch.zeros(B, max_gamma, 3, M, **f)
         self.logtype = torch.zeros(B, max_gamma, K, **f)
+        self.rate = torch.zeros(B, **f) if poisson else None
 
     def c(self):
-        return DraftBufC(*(t.data_ptr() for t in (self.tau, self.t, self.k, self.logg, self.logf, self.mix, self.logtype)))
+        return DraftBufC(*(None if t is None else t.data_ptr()
+                           for t in (self.tau, self.t, self.k, self.logg, self.logf, self.mix, self.logtype,
+                                     self.rate)))
 
 
 class VerifyBuffers:
@@ -262,6 +282,9 @@ class State:
     def tppsd_draft(self, gamma: int, out: DraftBuffers):
         _check(lib().tppsd_draft(self.handle, gamma, ctypes.byref(out.c()), _stream()))
 
+    def tppsd_draft_poisson(self, gamma: int, params: torch.Tensor, out: DraftBuffers):
+        _check(lib().tppsd_draft_poisson(self.handle, gamma, _ptr(params), ctypes.byref(out.c()), _stream()))
+
     def tppsd_verify(self, gamma: int, drafts: DraftBuffers, out: VerifyBuffers):
         _check(lib().tppsd_verify(self.handle, gamma, ctypes.byref(drafts.c()), ctypes.byref(out.c()), _stream()))
 
@@ -277,6 +300,12 @@ class State:
     def tppsd_sample_sd(self, gamma: int, max_rounds: int = 1 << 30) -> int:
         r = c_int()
         _check(lib().tppsd_sample_sd(self.handle, gamma, max_rounds, ctypes.byref(r), _stream()))
+        return r.value
+
+    def tppsd_sample_sd_poisson(self, gamma: int, params: torch.Tensor, max_rounds: int = 1 << 30) -> int:
+        r = c_int()
+        _check(lib().tppsd_sample_sd_poisson(self.handle, gamma, _ptr(params), max_rounds, ctypes.byref(r),
+                                             _stream()))
         return r.value
 
     def tppsd_read_events(self):

@@ -61,3 +61,36 @@ def test_gpu_sd_law_equals_gpu_ar():
     ps = np.array(ps)
     print(f"alpha {alpha:.3f}, min p {ps.min():.3g}")
     assert ps.min() > 0.01 / len(ps), ps
+
+
+def test_gpu_sd_poisson_law_equals_gpu_ar():
+    """The same check with the homogeneous-Poisson draft (App. D.3), fitted on
+    the device from the histories: Theorem 1 then runs against an
+    exponential g_D, and Eq. (4) against the fixed mark probabilities."""
+    tm, _, HT, HK = _setup()
+    n0 = HT.shape[1]
+    cap = n0 + N_GEN + GAMMA + 1
+    ar = tp.State(tm, None, B, cap, GAMMA, seed=303)
+    ar.tppsd_prefill(HT, HK, N_GEN)
+    ar.tppsd_sample_ar(N_GEN)
+    ta, ka, _ = ar.tppsd_read_events()
+    params = tp.tppsd_poisson_fit(HT[:1], HK[:1], 3)
+    sd = tp.State(tm, None, B, cap, GAMMA, seed=404)
+    sd.tppsd_prefill(HT, HK, N_GEN)
+    sd.tppsd_sample_sd_poisson(GAMMA, params)
+    ts, ks, _ = sd.tppsd_read_events()
+    st = sd.tppsd_state_status()
+    torch.cuda.synchronize()
+    assert st["bits"] == 0 and st["n_done"] == B
+    alpha = st["accepted"] / st["drafted"]
+    assert 0.05 < alpha < 0.95
+    a = _intervals(ta, ka, n0)
+    s = _intervals(ts, ks, n0)
+    ps = []
+    for j in range(N_GEN):
+        ps.append(scipy.stats.ks_2samp(a[0][:, j], s[0][:, j]).pvalue)
+        tab = np.stack([np.bincount(a[1][:, j], minlength=3), np.bincount(s[1][:, j], minlength=3)])
+        ps.append(scipy.stats.chi2_contingency(tab)[1])
+    ps = np.array(ps)
+    print(f"Poisson draft: alpha {alpha:.3f}, A-R candidates {st['ar_candidates']}, min p {ps.min():.3g}")
+    assert ps.min() > 0.01 / len(ps), ps

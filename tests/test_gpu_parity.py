@@ -113,9 +113,8 @@ def test_accept_teacher_forced(case, external):
     wt, wd = weights(case)
     T, D, ht, hk, st_o, dr, vf = _oracle_round(case, wt, wd, gamma, n_gen, seed)
     # the GPU receives exactly the values the oracle decides on (rounded to float32)
-    dr32 = S.DraftOut(**{f: (getattr(dr, f).astype(np.float32).astype(np.float64)
-                             if getattr(dr, f).dtype.kind == "f" else getattr(dr, f))
-                         for f in dr.__dataclass_fields__})
+    r32 = lambda a: a.astype(np.float32).astype(np.float64) if isinstance(a, np.ndarray) and a.dtype.kind == "f" else a
+    dr32 = S.DraftOut(**{f: r32(getattr(dr, f)) for f in dr.__dataclass_fields__})
     vf32 = S.VerifyOut(**{f: getattr(vf, f).astype(np.float32).astype(np.float64) for f in vf.__dataclass_fields__})
     rows = np.arange(case.B)
     ext = None
