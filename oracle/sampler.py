@@ -23,8 +23,15 @@ points the paper leaves open:
     counter-indexed stream and returns the first accepted one.
   * Categorical draws take the first index m with u * C_total < C_m, C the
     ascending cumulative sum of the probabilities.
-  * Generation stops after exactly n_gen new events per sequence (the last
-    round is truncated) instead of at an end time T.
+  * Generation stops after n_gen new events per sequence (the last round is
+    truncated) or, when an end time T is given, at the first event past T
+    (Algorithm 1 samples while t < T and then drops events with t > T, so
+    events are committed in order while t <= T), whichever comes first.
+  * The model log-likelihood (Eq. (2)) of the generated events is the sum of
+    the target's log g(tau_i) + log f(k_i) at each committed event, tau_i the
+    interval as drawn (event times are its float32 running sum), plus, for a
+    sequence ended by its end time T, the survival term log(1 - G(T - t_N))
+    under the distribution that followed the last committed event.
   * A seed history is prefilled; its last event is the pending one whose
     history embedding gives the next distribution.
 
@@ -37,6 +44,8 @@ import dataclasses
 from typing import Optional
 
 import numpy as np
+
+import scipy.special
 
 from .model import Model
 from .numerics import f32, logsumexp
@@ -59,6 +68,19 @@ def mixture_logpdf(logw, mu, s, tau):
     lt = np.log(np.asarray(tau, dtype=np.float64))[..., None]
     comp = logw - s - HALF_LOG_2PI - lt - (lt - mu) ** 2 / (2.0 * np.exp(2.0 * s))
     return logsumexp(comp, axis=-1)
+
+
+def mixture_log_survival(logw, mu, s, x):
+    """log(1 - G(x)) for the log-normal mixture (the survival term of Eq. (2)).
+
+    1 - G(x) = sum_m w_m P(LogNormal(mu_m, sigma_m) > x) = sum_m w_m Phi(-(ln x - mu_m) / sigma_m),
+    evaluated as a log-sum-exp of log w_m + log Phi(.) (scipy's log_ndtr). x <= 0 gives 0.
+    """
+    x = float(x)
+    if x <= 0.0:
+        return 0.0
+    z = (np.log(x) - np.asarray(mu, dtype=np.float64)) / np.exp(np.asarray(s, dtype=np.float64))
+    return float(logsumexp(np.asarray(logw, dtype=np.float64) + scipy.special.log_ndtr(-z)))
 
 
 def categorical(logp, u):
@@ -120,18 +142,37 @@ class State:
     drafted: int = 0
     accepted_drafts: int = 0
     ar_iters_total: int = 0
+    # end-time stop and model log-likelihood (Eq. (2))
+    t_end: Optional[np.ndarray] = None        # [B] float32 end times, or None (count stop only)
+    stopped: Optional[np.ndarray] = None      # [B] ended by the end time
+    stop_margin: Optional[np.ndarray] = None  # [B] min |t - T| over the end-time decisions taken
+    ll: Optional[np.ndarray] = None           # [B] log-likelihood of the generated events
+    tau: Optional[np.ndarray] = None          # [B, cap] drawn interval of each generated event
+
+    def __post_init__(self):
+        B = len(self.n)
+        if self.stopped is None:
+            self.stopped = np.zeros(B, dtype=bool)
+        if self.stop_margin is None:
+            self.stop_margin = np.full(B, np.inf)
+        if self.ll is None:
+            self.ll = np.zeros(B)
+        if self.tau is None:
+            self.tau = np.zeros_like(self.t)
 
     @property
     def done(self):
-        return self.gen >= self.n_gen
+        return (self.gen >= self.n_gen) | self.stopped
 
 
 def prefill(T: Model, D: Optional[Model], hist_t, hist_k, n_gen: int, extra: int = 64,
-            seq0: int = 0) -> State:
+            seq0: int = 0, t_end=None) -> State:
     """Store the seed histories and cache every event except the pending (last) one.
 
     The draft cache holds all but the last two events: each round's first
-    draft step re-encodes the last two committed events.
+    draft step re-encodes the last two committed events. t_end (scalar or
+    [B], rounded to float32): per-sequence end time; a sequence whose pending
+    event is already at or past it generates nothing.
     """
     hist_t = np.asarray(hist_t, dtype=np.float32).astype(np.float64)
     hist_k = np.asarray(hist_k, dtype=np.int64)
@@ -145,6 +186,10 @@ def prefill(T: Model, D: Optional[Model], hist_t, hist_k, n_gen: int, extra: int
                n_gen=n_gen, tcache=T.new_cache(B, cap), dcache=None,
                log_margin=np.full((B, n_gen), np.inf), cat_margin=np.full((B, n_gen), np.inf),
                rounds_run=np.zeros(B, dtype=np.int64), seq0=seq0)
+    if t_end is not None:
+        st.t_end = f32(np.broadcast_to(np.asarray(t_end, dtype=np.float64), (B,))).copy()
+        st.stopped = hist_t[:, -1] >= st.t_end
+        st.stop_margin = np.abs(hist_t[:, -1] - st.t_end)
     if n0 > 1:
         T.forward_block(st.tcache, hist_t[:, :n0 - 1], hist_k[:, :n0 - 1], np.zeros(B, dtype=np.int64))
     if D is not None:
@@ -154,17 +199,40 @@ def prefill(T: Model, D: Optional[Model], hist_t, hist_k, n_gen: int, extra: int
     return st
 
 
-def _commit(st: State, b: int, times, types, log_margins, cat_margins):
-    """Append new events to sequence b, truncating at n_gen generated events."""
+def _commit(st: State, b: int, times, types, taus, log_margins, cat_margins, logdens, dists):
+    """Append new events to sequence b in order until it has n_gen generated
+    events or, with an end time T, until the first event past T (which is
+    dropped; an event exactly at T is kept and ends the sequence).
+
+    logdens[j]: the target's log g(tau_j) + log f(k_j) for event j, added to
+    the log-likelihood when the event is committed; dists[j] = (log w, mu, s)
+    of the distribution event j was drawn from, whose survival at T - t_N ends
+    the log-likelihood of a sequence stopped by its end time."""
     room = st.n_gen - st.gen[b]
-    m = min(len(times), room)
-    n, g = st.n[b], st.gen[b]
-    st.t[b, n:n + m] = times[:m]
-    st.k[b, n:n + m] = types[:m]
-    st.log_margin[b, g:g + m] = log_margins[:m]
-    st.cat_margin[b, g:g + m] = cat_margins[:m]
-    st.n[b] += m
-    st.gen[b] += m
+    T_end = None if st.t_end is None else st.t_end[b]
+    m = 0
+    for j in range(len(times)):
+        if m >= room:
+            break
+        if T_end is not None:
+            st.stop_margin[b] = min(st.stop_margin[b], abs(times[j] - T_end))
+            if times[j] > T_end:
+                st.stopped[b] = True
+                st.ll[b] += mixture_log_survival(*dists[j], T_end - st.t[b, st.n[b] - 1])
+                break
+        n, g = st.n[b], st.gen[b]
+        st.t[b, n] = times[j]
+        st.k[b, n] = types[j]
+        st.tau[b, n] = taus[j]
+        st.log_margin[b, g] = log_margins[j]
+        st.cat_margin[b, g] = cat_margins[j]
+        st.ll[b] += logdens[j]
+        st.n[b] += 1
+        st.gen[b] += 1
+        m += 1
+        if T_end is not None and times[j] >= T_end:
+            st.stopped[b] = True      # survival at T - t_N = 0 adds log 1
+            break
     return m
 
 
@@ -185,11 +253,12 @@ def ar_step(T: Model, st: State, seed: int):
     tau, k, cm = sample_event(logw, mu, s, logf, U)
     for i, b in enumerate(rows):
         t_new = f32(st.t[b, st.n[b] - 1] + tau[i])
-        _commit(st, b, [t_new], [k[i]], [np.inf], [cm[i]])
+        ld = mixture_logpdf(logw[i], mu[i], s[i], tau[i]) + logf[i, k[i]]
+        _commit(st, b, [t_new], [k[i]], [tau[i]], [np.inf], [cm[i]], [ld], [(logw[i], mu[i], s[i])])
 
 
-def sample_ar(T: Model, hist_t, hist_k, n_gen: int, seed: int, seq0: int = 0) -> State:
-    st = prefill(T, None, hist_t, hist_k, n_gen, seq0=seq0)
+def sample_ar(T: Model, hist_t, hist_k, n_gen: int, seed: int, seq0: int = 0, t_end=None) -> State:
+    st = prefill(T, None, hist_t, hist_k, n_gen, seq0=seq0, t_end=t_end)
     while not np.all(st.done):
         ar_step(T, st, seed)
     return st
@@ -478,12 +547,20 @@ def accept(st: State, gamma: int, dr: DraftOut, vf: VerifyOut, seed: int, rows, 
         for tau in taus:
             t_prev = float(f32(t_prev + tau))
             times.append(t_prev)
+        # target log-densities of the round's events: verify row j scores event j
+        # (the accepted drafts at their recorded values, the event at L or the
+        # bonus event at its interval and type)
+        logdens = [vf.logg[i, j] + vf.logf[i, j] for j in range(min(L - 1, len(taus)))]
+        if len(taus) > L - 1:
+            j = len(taus) - 1
+            logdens.append(mixture_logpdf(vf.logw[i, j], vf.mu[i, j], vf.s[i, j], taus[j]) + vf.logtype[i, j, ks[j]])
+        dists = [(vf.logw[i, j], vf.mu[i, j], vf.s[i, j]) for j in range(len(taus))]
         # a decision at position l can change every event from l on
         lmc = np.minimum.accumulate(log_m[:len(times)])
         cmc = np.minimum.accumulate(cat_m[:len(times)])
         st.drafted += gamma
         st.accepted_drafts += L - 1
-        m = _commit(st, b, times, ks, lmc, cmc)
+        m = _commit(st, b, times, ks, taus, lmc, cmc, logdens, dists)
         res["L"][i] = L
         res["n_new"][i] = m
         res["flags"][i] = flags
@@ -517,16 +594,45 @@ def sd_round_poisson(T: Model, st: State, gamma: int, rate: float, logp, seed: i
 
 
 def sample_sd_poisson(T: Model, hist_t, hist_k, n_gen: int, gamma: int, rate: float, logp, seed: int,
-                      bonus=True, seq0: int = 0, **kw) -> State:
-    st = prefill(T, None, hist_t, hist_k, n_gen, seq0=seq0)
+                      bonus=True, seq0: int = 0, t_end=None, **kw) -> State:
+    st = prefill(T, None, hist_t, hist_k, n_gen, seq0=seq0, t_end=t_end)
     while not np.all(st.done):
         sd_round_poisson(T, st, gamma, rate, logp, seed, bonus=bonus, **kw)
     return st
 
 
 def sample_sd(T: Model, D: Model, hist_t, hist_k, n_gen: int, gamma: int, seed: int,
-              bonus=True, seq0: int = 0, **kw) -> State:
-    st = prefill(T, D, hist_t, hist_k, n_gen, seq0=seq0)
+              bonus=True, seq0: int = 0, t_end=None, **kw) -> State:
+    st = prefill(T, D, hist_t, hist_k, n_gen, seq0=seq0, t_end=t_end)
     while not np.all(st.done):
         sd_round(T, D, st, gamma, seed, bonus=bonus, **kw)
     return st
+
+
+# ---------------------------------------------------------------------------
+# model log-likelihood of sampled sequences (Eq. (2))
+# ---------------------------------------------------------------------------
+
+def loglik(T: Model, t, k, tau, n, first: int, t_end=None, stopped=None):
+    """Eq. (2) for each sequence b, from one cache-free forward pass over its
+    committed events 0 .. n[b] - 1: the sum over i = first .. n[b] - 1 of
+    log g(tau_i | h_{i-1}) + log f(k_i | h_{i-1}), tau_i = tau[b, i] (the
+    drawn interval), plus log(1 - G(T_b - t_{n-1} | h_{n-1})) when stopped[b]
+    (a sequence ended by its end time T_b = t_end[b]). Returns [B] totals and
+    the per-event terms [B, max n] (0 outside first .. n[b] - 1)."""
+    t = np.asarray(t, dtype=np.float64)
+    k = np.asarray(k, dtype=np.int64)
+    n = np.asarray(n, dtype=np.int64)
+    B = len(n)
+    total = np.zeros(B)
+    terms = np.zeros((B, int(n.max())))
+    for b in range(B):
+        N = int(n[b])
+        h = T.forward_full(t[b:b + 1, :N], k[b:b + 1, :N])[0]
+        logw, mu, s, logf = T.head(h)
+        for i in range(first, N):
+            terms[b, i] = mixture_logpdf(logw[i - 1], mu[i - 1], s[i - 1], tau[b, i]) + logf[i - 1, k[b, i]]
+        total[b] = terms[b].sum()
+        if stopped is not None and stopped[b]:
+            total[b] += mixture_log_survival(logw[N - 1], mu[N - 1], s[N - 1], float(t_end[b]) - t[b, N - 1])
+    return total, terms
