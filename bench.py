@@ -40,6 +40,7 @@ def parse():
     ap.add_argument("--ar-steps", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-poisson", action="store_true", help="skip the homogeneous-Poisson draft run")
+    ap.add_argument("--no-window", action="store_true", help="skip the end-time (window) runs")
     ap.add_argument("--cpu-events", type=int, default=64, help="oracle sample: events per sequence")
     ap.add_argument("--cpu-seqs", type=int, default=4, help="oracle sample: sequences")
     return ap.parse_args()
@@ -118,6 +119,45 @@ def cpu_baseline(wl, gamma, wt, wd, ht, hk, n_seq, n_events):
     return {"value": ev / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
             "sample": f"{n_seq} sequences x first {n_events} generated events of {wl.name} "
                       f"(TPP-SD, gamma={gamma}), float64 NumPy, {dt:.1f} s"}
+
+
+def window_jobs(args, wl, gamma, sd, ar, HT, HK, ht, n_gen, B):
+    """TPP-SD and AR with an end time per sequence (Algorithm 1's T): each
+    sequence's window is 0.75 n_gen of its history's mean interval after its
+    pending event, n_gen stays the cap. Reports generated events per second,
+    how the sequences ended, and the model log-likelihood (Eq. (2)) both
+    samplers accumulate: its batch means and their difference (the model-side
+    likelihood discrepancy |L_ar - L_sd|)."""
+    import torch
+    mean_iv = (ht[:, -1] - ht[:, 0]) / (ht.shape[1] - 1)
+    t_end = torch.from_numpy((ht[:, -1] + 0.75 * n_gen * mean_iv).astype(np.float32)).to(HT.device)
+    res = {}
+    for name, st, steps in (("sd", sd, args.steps), ("ar", ar, max(1, args.ar_steps))):
+        def job():
+            st.tppsd_prefill(HT, HK, n_gen, t_end=t_end)
+            if name == "sd":
+                st.tppsd_sample_sd(gamma)
+            else:
+                st.tppsd_sample_ar(n_gen)
+        job()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            job()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+        s = st.tppsd_state_status()
+        assert s["bits"] == 0 and s["n_done"] == B, s
+        _, _, n = st.tppsd_read_events()
+        ll = st.tppsd_read_loglik().cpu().numpy()
+        gen = n.cpu().numpy() - wl.n_hist
+        res[name] = {"events_per_s": float(gen.sum()) / dt, "mean_events": float(gen.mean()),
+                     "ended_by_time": float(np.mean(gen < n_gen)), "loglik_mean": float(ll.mean()),
+                     "loglik_per_event": float(ll.sum() / max(1, gen.sum()))}
+    res["speedup_vs_gpu_ar"] = res["sd"]["events_per_s"] / res["ar"]["events_per_s"]
+    res["delta_L"] = abs(res["sd"]["loglik_mean"] - res["ar"]["loglik_mean"])
+    res["window"] = "0.75 n_gen mean history intervals after the pending event"
+    return res
 
 
 def main():
@@ -252,6 +292,8 @@ def main():
                      "traffic": measured_traffic(wl.name), "avg_launch_us": avg_ms * 1e3, "launches": attn_launches,
                      "algorithmic_bytes_per_launch": per_launch},
     }
+    if not args.no_window:
+        out["window"] = window_jobs(args, wl, gamma, sd, ar, HT, HK, ht, n_gen, B)
     c = wl.target
     gemm_tflops = tk["gemm_flop"] / (tk["gemm_ms"] * 1e-3) / 1e12 if tk["gemm_ms"] else 0.0
     gemm_peak = MFMA_PEAK_TFLOPS[c.prec]

@@ -123,7 +123,8 @@ typedef struct {
   float   *tau_new;  /* [B, max_gamma + 1] their intervals                               */
   int32_t *ar_iter;  /* [B] index of the accepted Theorem-1 candidate, -1 if none drawn  */
   uint8_t *flags;    /* [B] bit0 tau redrawn, bit1 type redrawn, bit2 bonus event,
-                            bit3 sequence finished, bit4 sequence was already finished */
+                            bit3 sequence finished, bit4 sequence was already finished,
+                            bit5 finished by its end time (tppsd_prefill_window) */
 } tppsd_accept_buf;
 
 /* ---- weights ----------------------------------------------------------------- */
@@ -176,6 +177,16 @@ void tppsd_state_destroy(tppsd_state *s);
  * > max_events), TPPSD_E_HIP. */
 int tppsd_prefill(tppsd_state *s, const float *d_t, const int32_t *d_k, int n0, int n_gen,
                   hipStream_t stream);
+
+/* tppsd_prefill with an end time per sequence (Algorithm 1's T): d_t_end [B]
+ * (device, copied). Sequence b then ends at its n_gen-th new event or at its
+ * first event past d_t_end[b], whichever comes first; that event is dropped
+ * (an event exactly at the end time is kept and ends the sequence), and a
+ * sequence whose pending event is already at or past its end time generates
+ * nothing. d_t_end NULL: no end time (tppsd_prefill). Errors: as
+ * tppsd_prefill. */
+int tppsd_prefill_window(tppsd_state *s, const float *d_t, const int32_t *d_k, int n0, int n_gen,
+                         const float *d_t_end, hipStream_t stream);
 
 /* Drafting (§4.3 "Drafting", Algorithm 1's inner loop): gamma sequential draws
  * from the draft model for every unfinished sequence, using the Philox
@@ -262,6 +273,15 @@ int tppsd_sample_sd_poisson(tppsd_state *s, int gamma, const float *d_params, in
 /* Copies the committed events (history included) to d_t/d_k [B, max_events]
  * and the per-sequence event counts to d_n [B]. Any pointer may be NULL. */
 int tppsd_read_events(tppsd_state *s, float *d_t, int32_t *d_k, int32_t *d_n, hipStream_t stream);
+
+/* Model log-likelihood (Eq. (2)) of each sequence's generated events since
+ * prefill, accumulated while sampling: the target's log g(tau_i) + log f(k_i)
+ * at every committed event (tau_i the interval as drawn; event times are its
+ * float32 running sum) in float64, plus, for a sequence ended by its end
+ * time, log(1 - G(T - t_N)) under the target's distribution after its last
+ * event. AR and TPP-SD runs accumulate the same quantity. Copies [B] doubles
+ * to d_ll (device). Errors: TPPSD_E_ARG, TPPSD_E_HIP. */
+int tppsd_read_loglik(tppsd_state *s, double *d_ll, hipStream_t stream);
 
 /* Synchronises the stream and reads the sticky status bits and the number of
  * finished sequences. Accounting (may be NULL): accepted drafts, drafted

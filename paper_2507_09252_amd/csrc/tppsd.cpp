@@ -178,6 +178,8 @@ struct tppsd_state {
           *zeros = nullptr;
   float *ev_t = nullptr;
   int32_t *ev_k = nullptr;
+  float *t_end = nullptr;    // [B] end times (+inf: none)
+  double *ll = nullptr;      // [B] model log-likelihood of the generated events
   ModelCache cT, cD;
   // activation scratch
   float *x = nullptr;
@@ -229,7 +231,7 @@ namespace {
 
 struct WsLayout {
   size_t total = 0;
-  size_t status, n_done, acc, n, gen, lenT, lenD, done, rnd, zeros, ev_t, ev_k;
+  size_t status, n_done, acc, n, gen, lenT, lenD, done, rnd, zeros, ev_t, ev_k, t_end, ll;
   size_t freqT, freqD, kT, vT, kD, vD, layerT, layerD;
   size_t x, a, q, o, hid, e, ar_mix, ar_lt, attn_part, gen0;
   size_t logits, hwT, hbT, hwD, hbD;
@@ -260,6 +262,8 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   w.zeros = take(Bz * 4);
   w.ev_t = take(Bz * cap * 4);
   w.ev_k = take(Bz * cap * 4);
+  w.t_end = take(Bz * 4);
+  w.ll = take(Bz * 8);
   w.freqT = take((size_t)T->d() * 4);
   w.freqD = take(D ? (size_t)D->d() * 4 : 0);
   const size_t kvc = kv_stride(cap);
@@ -411,6 +415,8 @@ HeadArgs head_common(tppsd_state *s) {
   h.rnd = s->rnd;
   h.n_done = s->n_done;
   h.n_gen = s->n_gen;
+  h.t_end = s->t_end;
+  h.ll = s->ll;
   h.seed = s->seed;
   h.status = s->status;
   return h;
@@ -627,6 +633,8 @@ int do_accept(tppsd_state *s, int gamma, const tppsd_draft_buf *dr, const tppsd_
   a.rnd = s->rnd;
   a.n_done = s->n_done;
   a.n_gen = s->n_gen;
+  a.t_end = s->t_end;
+  a.ll = s->ll;
   a.seed = s->seed;
   a.status = s->status;
   a.acc_stats = s->acc_stats;
@@ -755,6 +763,8 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->zeros = (int32_t *)(ws + w.zeros);
   s->ev_t = (float *)(ws + w.ev_t);
   s->ev_k = (int32_t *)(ws + w.ev_k);
+  s->t_end = (float *)(ws + w.t_end);
+  s->ll = (double *)(ws + w.ll);
   s->cT.k = ws + w.kT;
   s->cT.v = ws + w.vT;
   s->cT.layer_bytes = w.layerT;
@@ -848,6 +858,11 @@ void tppsd_state_destroy(tppsd_state *s) {
 }
 
 int tppsd_prefill(tppsd_state *s, const float *d_t, const int32_t *d_k, int n0, int n_gen, hipStream_t st) {
+  return tppsd_prefill_window(s, d_t, d_k, n0, n_gen, nullptr, st);
+}
+
+int tppsd_prefill_window(tppsd_state *s, const float *d_t, const int32_t *d_k, int n0, int n_gen,
+                         const float *d_t_end, hipStream_t st) {
   if (!s || !d_t || !d_k) return fail(TPPSD_E_ARG, "null argument");
   if (n0 < 2 || n_gen < 0) return fail(TPPSD_E_ARG, "need n0 >= 2 and n_gen >= 0");
   if ((long long)n0 + n_gen + s->max_gamma + 1 > s->cap)
@@ -863,8 +878,8 @@ int tppsd_prefill(tppsd_state *s, const float *d_t, const int32_t *d_k, int n0, 
     }
     s->heads_built = true;
   }
-  launch_prefill_init(d_t, d_k, s->B, n0, n_gen, s->ev_t, s->ev_k, s->cap, s->n, s->gen, s->lenT, s->lenD, s->done,
-                      s->rnd, s->zeros, s->n_done, s->status, s->acc_stats, st);
+  launch_prefill_init(d_t, d_k, s->B, n0, n_gen, d_t_end, s->ev_t, s->ev_k, s->cap, s->n, s->gen, s->lenT, s->lenD,
+                      s->done, s->rnd, s->zeros, s->t_end, s->ll, s->n_done, s->status, s->acc_stats, st);
   // encode history events 0 .. n0 - 2 (target) and 0 .. n0 - 3 (draft) in position chunks
   for (int which = 0; which < (s->D ? 2 : 1); ++which) {
     const tppsd_model *m = which ? s->D : s->T;
@@ -1179,6 +1194,13 @@ int tppsd_read_events(tppsd_state *s, float *d_t, int32_t *d_k, int32_t *d_n, hi
   if (!s) return fail(TPPSD_E_ARG, "null state");
   launch_copy_events(s->ev_t, s->ev_k, s->n, s->B, s->cap, d_t, d_k, d_n, st);
   return hip_check("tppsd_read_events");
+}
+
+int tppsd_read_loglik(tppsd_state *s, double *d_ll, hipStream_t st) {
+  if (!s || !d_ll) return fail(TPPSD_E_ARG, "null argument");
+  if (hipMemcpyAsync(d_ll, s->ll, (size_t)s->B * sizeof(double), hipMemcpyDeviceToDevice, st) != hipSuccess)
+    return hip_check("tppsd_read_loglik");
+  return TPPSD_OK;
 }
 
 int tppsd_state_status(tppsd_state *s, hipStream_t st, uint32_t *bits, int32_t *n_done, int64_t *accepted,

@@ -72,6 +72,8 @@ struct HeadArgs {
   int ev_stride;
   int32_t *n, *gen, *lenT, *done, *rnd, *n_done;
   int n_gen;
+  const float *t_end;       // [B] end times (+inf: none)
+  double *ll;               // [B] model log-likelihood of the generated events (Eq. (2))
   uint64_t seed;
   uint32_t *status;
   // HEAD_AR optional outputs [B, out_stride], written at column gen - gen0
@@ -96,6 +98,8 @@ struct AcceptArgs {
   int ev_stride;
   int32_t *n, *gen, *lenT, *lenD, *done, *rnd, *n_done;
   int n_gen;
+  const float *t_end;       // [B] end times (+inf: none)
+  double *ll;               // [B] model log-likelihood of the generated events (Eq. (2))
   uint64_t seed;
   uint32_t *status;
   unsigned long long *acc_stats;   // [3]: accepted drafts, drafted, A-R candidates
@@ -177,10 +181,10 @@ void launch_build_head(const void *mix_w, const void *k2_w, const float *mix_b, 
 // row stride of the decoder logits: 3M + K rounded up to 8
 inline int head_ldl(int M, int K) { return (3 * M + K + 7) / 8 * 8; }
 void launch_accept(const AcceptArgs &a, hipStream_t st);
-void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, float *ev_t,
-                         int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
-                         int32_t *lenD, int32_t *done, int32_t *rnd, int32_t *zeros, int32_t *n_done,
-                         uint32_t *status, unsigned long long *acc_stats, hipStream_t st);
+void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, const float *t_end_in,
+                         float *ev_t, int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
+                         int32_t *lenD, int32_t *done, int32_t *rnd, int32_t *zeros, float *t_end, double *ll,
+                         int32_t *n_done, uint32_t *status, unsigned long long *acc_stats, hipStream_t st);
 void launch_snapshot(const int32_t *src, int32_t *dst, int B, hipStream_t st);
 void launch_copy_events(const float *ev_t, const int32_t *ev_k, const int32_t *n, int B, int ev_stride,
                         float *t, int32_t *k, int32_t *nout, hipStream_t st);

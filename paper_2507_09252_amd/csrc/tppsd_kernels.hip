@@ -82,6 +82,23 @@ __device__ float wave_mix_logpdf(const float *logw, const float *mu, const float
   return mx + logf(wave_sum(lane < M ? expf(c - mx) : 0.f));
 }
 
+// log(1 - G(x)) of the log-normal mixture whose component m sits in lane m
+// (valid = false in the other lanes): log-sum-exp over m of log w_m +
+// log Phi(-z_m), z_m = (ln x - mu_m) / sigma_m. With y = z / sqrt(2),
+// Phi(-z) = erfc(y) / 2, taken as erfcx(y) e^(-y^2) / 2 for y > 0 so that the
+// logarithm does not underflow. x <= 0 (wave-uniform) gives 0.
+__device__ float wave_log_survival(float logw, float mu, float s, bool valid, float x) {
+  if (!(x > 0.f)) return 0.f;
+  float c = -INFINITY;
+  if (valid) {
+    const float y = (logf(x) - mu) * expf(-s) * 0.707106781186547524f;
+    const float lphi = y > 0.f ? logf(0.5f * erfcxf(y)) - y * y : logf(0.5f * erfcf(y));
+    c = logw + lphi;
+  }
+  const float mx = wave_max(c);
+  return mx + logf(wave_sum(valid ? expf(c - mx) : 0.f));
+}
+
 // z ~ Categorical(w), eps = Box-Muller(u1, u2), tau = exp(mu_z + sigma_z eps)
 __device__ float sample_tau(const float *logw, const float *mu, const float *s, int M, float uc, float u1,
                             float u2) {
@@ -682,13 +699,26 @@ __global__ __launch_bounds__(256) void k_head(const float *__restrict__ logits, 
     philox_uniforms(a.seed, (uint64_t)b, (uint64_t)g, 0ull, TAG_AR, u);
     const float tau = draw_tau(u);
     const int kk = sample(logk, K, u[3]);
-    if (lane != 0) return;
     const int n = a.n[b];
+    const float tlast = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+    const float tn = tlast + tau;
+    const float T_end = a.t_end[b];
+    // Eq. (2): log-density of the committed event, or, for an event past the
+    // end time (dropped; the sequence ends), the survival log(1 - G(T - t_N))
+    const bool past = tn > T_end;
+    const float lterm = past ? wave_log_survival(logw, mu, sg, lane < M, T_end - tlast)
+                             : logpdf(tau) + __shfl(logk, kk, 64);
+    if (lane != 0) return;
+    a.ll[b] += (double)lterm;
+    if (past) {
+      a.done[b] = 1;
+      atomicAdd(a.n_done, 1);
+      return;
+    }
     if (n >= a.ev_stride) {
       atomicOr(a.status, TPPSD_STATUS_CAPACITY);
       return;
     }
-    const float tn = a.ev_t[(size_t)b * a.ev_stride + n - 1] + tau;
     a.ev_t[(size_t)b * a.ev_stride + n] = tn;
     a.ev_k[(size_t)b * a.ev_stride + n] = kk;
     const int col = g - a.gen0[b];
@@ -700,7 +730,7 @@ __global__ __launch_bounds__(256) void k_head(const float *__restrict__ logits, 
     a.gen[b] = g + 1;
     a.lenT[b] = n;
     if (!isfinite(tau)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
-    if (g + 1 >= a.n_gen) {
+    if (g + 1 >= a.n_gen || tn >= T_end) {
       a.done[b] = 1;
       atomicAdd(a.n_done, 1);
     }
@@ -1212,6 +1242,7 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     ak = __shfl(pass_k, L - 1, 64);
   }
   float tauL = 0.f;
+  float lgL = 0.f, lfL = 0.f;   // target log g, log f of the event drawn at L (or the bonus event)
   int kL = 0, ar_j = -1, flags = 0;
   if (L <= G) {
     const int li = L - 1;
@@ -1286,20 +1317,24 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
         const float tau = expf(Tm[z] + Ts[z] * eps);
         const float lt = logf(tau);
         const float lgd = pois ? lrate - rate * tau : logpdf(Da, De, Dm, lt);
-        const float delta = logpdf(Ta, Te, Tm, lt) - lgd;
+        const float lgt = logpdf(Ta, Te, Tm, lt);
+        const float delta = lgt - lgd;
         const bool acc = delta > 0.f && u[3] < -expm1f(-delta);
         const uint64_t m = __ballot(acc);
         if (m) {
           const int jl = __ffsll((unsigned long long)m) - 1;
           tauL = __shfl(tau, jl, 64);
+          lgL = __shfl(lgt, jl, 64);
           ar_j = base + jl;
           break;
         }
         tauL = __shfl(tau, 63, 64);
+        lgL = __shfl(lgt, 63, 64);
       }
       flags |= 1;
     } else {
       tauL = a.d_tau[(size_t)b * MG + li];
+      lgL = a.v_logg[(size_t)b * MG + li];
     }
     if (!ak) {
       // Eq. (4): k ~ norm(max(0, f_T - f_D)), lane kk holding type kk
@@ -1320,44 +1355,72 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     } else {
       kL = a.d_k[(size_t)b * MG + li];
     }
+    lfL = a.v_logtype[((size_t)b * (MG + 1) + li) * K + kL];
   } else if (a.bonus) {
     const float *Tr = a.v_mix + ((size_t)b * (MG + 1) + G) * 3 * M;
     float u[4];
     philox_uniforms(a.seed, (uint64_t)b, r, 0ull, TAG_BONUS, u);
     tauL = sample_tau(Tr, Tr + M, Tr + 2 * M, M, u[0], u[1], u[2]);
     kL = sample_cat(a.v_logtype + ((size_t)b * (MG + 1) + G) * K, K, u[3]);
+    lgL = wave_mix_logpdf(Tr, Tr + M, Tr + 2 * M, M, tauL);
+    lfL = a.v_logtype[((size_t)b * (MG + 1) + G) * K + kL];
     flags |= 4;
   }
-  if (lane != 0) return;
+  // commit in order: at most n_gen - gen events, and none past the end time
+  // (Algorithm 1 samples while t < T and drops events with t > T; an event
+  // exactly at T is kept and ends the sequence). Every lane runs the loop so
+  // that the survival term below can use the whole wave; lane 0 writes.
   const int count = (L <= G) ? L : (a.bonus ? G + 1 : G);
   const int n = a.n[b], gen = a.gen[b];
-  const int nn = min(count, a.n_gen - gen);
-  float tp = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+  const int room = a.n_gen - gen;
+  const float T_end = a.t_end[b];
   const bool last_is_new = (L <= G) || a.bonus;
+  float tp = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+  int nn = 0, stop_row = -1;
+  bool stopped = false;
+  float x_surv = 0.f;
+  double ll = 0.0;
   for (int i = 0; i < count; ++i) {
-    float ti;
-    int ki;
-    if (i < count - 1 || !last_is_new) {
-      ti = a.d_tau[(size_t)b * MG + i];
-      ki = a.d_k[(size_t)b * MG + i];
-    } else {
-      ti = tauL;
-      ki = kL;
-    }
+    const bool is_new = i == count - 1 && last_is_new;
+    const float ti = is_new ? tauL : a.d_tau[(size_t)b * MG + i];
+    const int ki = is_new ? kL : a.d_k[(size_t)b * MG + i];
+    const float tprev = tp;
     tp = tp + ti;
     const size_t oi = (size_t)b * (MG + 1) + i;
-    a.t_new[oi] = tp;
-    a.tau_new[oi] = ti;
-    a.k_new[oi] = ki;
-    if (i < nn) {
-      if (n + i < a.ev_stride) {
-        a.ev_t[(size_t)b * a.ev_stride + n + i] = tp;
-        a.ev_k[(size_t)b * a.ev_stride + n + i] = ki;
+    if (lane == 0) {
+      a.t_new[oi] = tp;
+      a.tau_new[oi] = ti;
+      a.k_new[oi] = ki;
+    }
+    if (stopped || i >= room) continue;
+    if (tp > T_end) {           // first event past the end time: dropped
+      stopped = true;
+      stop_row = i;
+      x_surv = T_end - tprev;
+      continue;
+    }
+    if (lane == 0) {
+      if (n + nn < a.ev_stride) {
+        a.ev_t[(size_t)b * a.ev_stride + n + nn] = tp;
+        a.ev_k[(size_t)b * a.ev_stride + n + nn] = ki;
       } else {
         atomicOr(a.status, TPPSD_STATUS_CAPACITY);
       }
     }
+    // Eq. (2): the target's log-density of the committed event (verify row i)
+    ll += is_new ? (double)lgL + (double)lfL
+                 : (double)a.v_logg[(size_t)b * MG + i] + (double)a.v_logf[(size_t)b * MG + i];
+    ++nn;
+    if (tp >= T_end) stopped = true;   // exactly at T: survival of a zero interval adds log 1
   }
+  if (stop_row >= 0) {
+    // survival log(1 - G(T - t_N)) under the distribution of the dropped event
+    const float *Sr = a.v_mix + ((size_t)b * (MG + 1) + stop_row) * 3 * M;
+    const bool v = lane < M;
+    ll += (double)wave_log_survival(v ? Sr[lane] : 0.f, v ? Sr[M + lane] : 0.f, v ? Sr[2 * M + lane] : 0.f, v,
+                                    x_surv);
+  }
+  if (lane != 0) return;
   if (last_is_new && !isfinite(tauL)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
   const int n2 = n + nn, g2 = gen + nn;
   a.n[b] = n2;
@@ -1365,10 +1428,12 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   a.lenT[b] = n2 - 1;
   a.lenD[b] = n2 - 2;
   a.rnd[b] = (int)r + 1;
-  if (g2 >= a.n_gen) {
+  a.ll[b] += ll;
+  if (g2 >= a.n_gen || stopped) {
     a.done[b] = 1;
     atomicAdd(a.n_done, 1);
     flags |= 8;
+    if (stopped) flags |= 32;
   }
   a.L[b] = L;
   a.n_new[b] = nn;
@@ -1383,10 +1448,10 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
 // run setup and event copies
 // ---------------------------------------------------------------------------
 
-__global__ void k_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, float *ev_t,
-                               int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
-                               int32_t *lenD, int32_t *done, int32_t *rnd, int32_t *zeros, int32_t *n_done,
-                               uint32_t *status, unsigned long long *acc_stats) {
+__global__ void k_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, const float *t_end_in,
+                               float *ev_t, int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
+                               int32_t *lenD, int32_t *done, int32_t *rnd, int32_t *zeros, float *t_end,
+                               double *ll, uint32_t *status, unsigned long long *acc_stats) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx < B * n0) {
     const int b = idx / n0, i = idx - b * n0;
@@ -1398,15 +1463,32 @@ __global__ void k_prefill_init(const float *ht, const int32_t *hk, int B, int n0
     gen[idx] = 0;
     lenT[idx] = n0 - 1;
     lenD[idx] = n0 - 2;
-    done[idx] = n_gen <= 0 ? 1 : 0;
+    // no end time: +inf. A pending event at or past the end time generates nothing
+    const float te = t_end_in ? t_end_in[idx] : INFINITY;
+    t_end[idx] = te;
+    done[idx] = (n_gen <= 0 || ht[(size_t)idx * n0 + n0 - 1] >= te) ? 1 : 0;
     rnd[idx] = 0;
     zeros[idx] = 0;
+    ll[idx] = 0.0;
   }
   if (idx == 0) {
-    *n_done = n_gen <= 0 ? B : 0;
     *status = 0u;
     acc_stats[0] = acc_stats[1] = acc_stats[2] = 0ull;
   }
+}
+
+// n_done = number of sequences done at the start (one workgroup)
+__global__ __launch_bounds__(256) void k_count_done(const int32_t *done, int B, int32_t *n_done) {
+  __shared__ int part[256];
+  int c = 0;
+  for (int i = threadIdx.x; i < B; i += 256) c += done[i] != 0;
+  part[threadIdx.x] = c;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *n_done = part[0];
 }
 
 __global__ void k_snapshot(const int32_t *src, int32_t *dst, int B) {
@@ -1513,13 +1595,14 @@ void launch_build_head(const void *mix_w, const void *k2_w, const float *mix_b, 
 
 void launch_accept(const AcceptArgs &a, hipStream_t s) { k_accept<<<(a.B + 3) / 4, 256, 0, s>>>(a); }
 
-void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, float *ev_t,
-                         int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT, int32_t *lenD,
-                         int32_t *done, int32_t *rnd, int32_t *zeros, int32_t *n_done, uint32_t *status,
-                         unsigned long long *acc_stats, hipStream_t s) {
+void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, const float *t_end_in,
+                         float *ev_t, int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
+                         int32_t *lenD, int32_t *done, int32_t *rnd, int32_t *zeros, float *t_end, double *ll,
+                         int32_t *n_done, uint32_t *status, unsigned long long *acc_stats, hipStream_t s) {
   const int total = B * n0 > B ? B * n0 : B;
-  k_prefill_init<<<(total + 255) / 256, 256, 0, s>>>(ht, hk, B, n0, n_gen, ev_t, ev_k, ev_stride, n, gen, lenT,
-                                                     lenD, done, rnd, zeros, n_done, status, acc_stats);
+  k_prefill_init<<<(total + 255) / 256, 256, 0, s>>>(ht, hk, B, n0, n_gen, t_end_in, ev_t, ev_k, ev_stride, n, gen,
+                                                     lenT, lenD, done, rnd, zeros, t_end, ll, status, acc_stats);
+  k_count_done<<<1, 256, 0, s>>>(done, B, n_done);
 }
 
 void launch_snapshot(const int32_t *src, int32_t *dst, int B, hipStream_t s) {

@@ -31,7 +31,8 @@ EXPORTS = [
     "tppsd_state_bytes", "tppsd_state_create", "tppsd_state_destroy", "tppsd_prefill", "tppsd_draft",
     "tppsd_verify", "tppsd_accept", "tppsd_sample_ar", "tppsd_sample_sd", "tppsd_read_events",
     "tppsd_state_status", "tppsd_timing_enable", "tppsd_timing_read", "tppsd_last_error",
-    "tppsd_poisson_fit", "tppsd_draft_poisson", "tppsd_sample_sd_poisson",
+    "tppsd_poisson_fit", "tppsd_draft_poisson", "tppsd_sample_sd_poisson", "tppsd_prefill_window",
+    "tppsd_read_loglik",
 ]
 
 
@@ -103,6 +104,8 @@ def lib():
         "tppsd_poisson_fit": (c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p, c_void_p]),
         "tppsd_draft_poisson": (c_int, [c_void_p, c_int, c_void_p, P(DraftBufC), c_void_p]),
         "tppsd_sample_sd_poisson": (c_int, [c_void_p, c_int, c_void_p, c_int, P(c_int), c_void_p]),
+        "tppsd_prefill_window": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_int, c_void_p, c_void_p]),
+        "tppsd_read_loglik": (c_int, [c_void_p, c_void_p, c_void_p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -273,11 +276,18 @@ class State:
             _lib.tppsd_state_destroy(self.handle)
             self.handle = None
 
-    def tppsd_prefill(self, t: torch.Tensor, k: torch.Tensor, n_gen: int):
+    def tppsd_prefill(self, t: torch.Tensor, k: torch.Tensor, n_gen: int, t_end: Optional[torch.Tensor] = None):
+        """t_end [B] (optional): per-sequence end time (tppsd_prefill_window)."""
         t = t.contiguous()
         k = k.to(torch.int32).contiguous()
         self._hist = (t, k)
-        _check(lib().tppsd_prefill(self.handle, _ptr(t), _ptr(k), t.shape[1], n_gen, _stream()))
+        if t_end is None:
+            _check(lib().tppsd_prefill(self.handle, _ptr(t), _ptr(k), t.shape[1], n_gen, _stream()))
+        else:
+            t_end = t_end.to(torch.float32).contiguous()
+            self._t_end = t_end
+            _check(lib().tppsd_prefill_window(self.handle, _ptr(t), _ptr(k), t.shape[1], n_gen, _ptr(t_end),
+                                              _stream()))
 
     def tppsd_draft(self, gamma: int, out: DraftBuffers):
         _check(lib().tppsd_draft(self.handle, gamma, ctypes.byref(out.c()), _stream()))
@@ -314,6 +324,11 @@ class State:
         n = torch.empty(self.B, dtype=torch.int32, device=self.ws.device)
         _check(lib().tppsd_read_events(self.handle, _ptr(t), _ptr(k), _ptr(n), _stream()))
         return t, k, n
+
+    def tppsd_read_loglik(self) -> torch.Tensor:
+        ll = torch.empty(self.B, dtype=torch.float64, device=self.ws.device)
+        _check(lib().tppsd_read_loglik(self.handle, _ptr(ll), _stream()))
+        return ll
 
     def tppsd_state_status(self):
         bits, nd, acc, dr, ar = c_uint32(), c_int32(), c_int64(), c_int64(), c_int64()

@@ -94,3 +94,45 @@ def test_gpu_sd_poisson_law_equals_gpu_ar():
     ps = np.array(ps)
     print(f"Poisson draft: alpha {alpha:.3f}, A-R candidates {st['ar_candidates']}, min p {ps.min():.3g}")
     assert ps.min() > 0.01 / len(ps), ps
+
+
+def test_gpu_window_law_sd_equals_gpu_ar():
+    """With an end time 3.0 after the pending event (Algorithm 1's T): number
+    of events in the window (chi-square), first interval and last event time
+    (two-sample KS) of GPU TPP-SD against GPU AR; both accumulate the model
+    log-likelihood of Eq. (2), whose mean over the batch must agree as well."""
+    tm, dm, HT, HK = _setup()
+    n0 = HT.shape[1]
+    n_gen = 40
+    cap = n0 + n_gen + GAMMA + 1
+    t_end = HT[:, -1] + 3.0
+    out = {}
+    for kind, seed in (("ar", 505), ("sd", 606)):
+        st = tp.State(tm, dm if kind == "sd" else None, B, cap, GAMMA, seed=seed)
+        st.tppsd_prefill(HT, HK, n_gen, t_end=t_end)
+        if kind == "ar":
+            st.tppsd_sample_ar(n_gen)
+        else:
+            st.tppsd_sample_sd(GAMMA)
+        t, k, n = st.tppsd_read_events()
+        ll = st.tppsd_read_loglik()
+        s = st.tppsd_state_status()
+        torch.cuda.synchronize()
+        assert s["bits"] == 0 and s["n_done"] == B
+        t, n, ll = t.cpu().numpy(), n.cpu().numpy(), ll.cpu().numpy()
+        gen = n - n0
+        assert gen.max() < n_gen, "the count cap bound a sequence"
+        first = t[gen > 0, n0] - t[gen > 0, n0 - 1]
+        last = t[np.arange(B), n - 1] - t[:, n0 - 1]
+        out[kind] = (gen, first, last, ll)
+    a, s_ = out["ar"], out["sd"]
+    top = int(max(a[0].max(), s_[0].max())) + 1
+    ca, cs = np.bincount(a[0], minlength=top), np.bincount(s_[0], minlength=top)
+    keep = (ca + cs) >= 10
+    ps = np.array([scipy.stats.chi2_contingency(np.stack([ca[keep], cs[keep]]))[1],
+                   scipy.stats.ks_2samp(a[1], s_[1]).pvalue, scipy.stats.ks_2samp(a[2], s_[2]).pvalue,
+                   scipy.stats.ttest_ind(a[3], s_[3], equal_var=False).pvalue])
+    print(f"window: mean events {a[0].mean():.3f} / {s_[0].mean():.3f}, mean loglik {a[3].mean():.4f} / "
+          f"{s_[3].mean():.4f}, p {ps}")
+    assert a[0].mean() > 1.0
+    assert ps.min() > 0.01 / len(ps), ps
