@@ -216,6 +216,8 @@ struct tppsd_state {
   hipStream_t cap_stream = nullptr;
   bool use_graphs = true;
   bool fused_draft = true;   // one-launch drafting when the draft model fits it
+  bool fused_w_lds = false;  // ... with its weight matrices staged in LDS
+  bool fused_attn_mfma = false;   // ... with its attention on MFMA (else vector ALU for <= 4 heads)
   hipGraphExec_t sd_exec[2] = {nullptr, nullptr};
   long long sd_key = -1;
   const float *sd_params = nullptr, *phase_params = nullptr;   // Poisson draft parameters the graphs embed
@@ -485,6 +487,8 @@ int do_draft_fused(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStr
   a.d_logtype = out->logtype;
   a.d_k = out->k;
   a.MG = s->max_gamma;
+  a.w_lds = s->fused_w_lds ? 1 : 0;
+  a.attn_mfma = s->fused_attn_mfma ? 1 : 0;
   launch_draft_fused(a, D->bf16(), st);
   return hip_check("tppsd_draft");
 }
@@ -828,6 +832,19 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
                      fused_draft_lds_bytes(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
                                            D->H()) <= 64 * 1024 &&
                      !(nf && nf[0] == '1');
+    // its weight matrices in LDS when they fit beside the rest and each
+    // workgroup has a CU to itself anyway (one workgroup per sequence)
+    const char *wg = getenv("TPPSD_DRAFT_WEIGHTS_GLOBAL");
+    const int wb = D && D->bf16() ? 2 : 4;
+    s->fused_w_lds = s->fused_draft && B <= 256 && !(wg && wg[0] == '1') &&
+                     fused_draft_lds_bytes(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
+                                           D->H()) +
+                             fused_draft_weight_elems(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix,
+                                                      D->cfg.n_types) * wb <=
+                         LDS_PER_WG - 4096;
+    if (s->fused_w_lds && allow_draft_fused_lds(LDS_PER_WG - 4096)) s->fused_w_lds = false;
+    const char *am = getenv("TPPSD_DRAFT_ATTN_MFMA");
+    s->fused_attn_mfma = am && am[0] == '1';
   }
   if (hipHostMalloc((void **)&s->host_ndone, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&s->poll_ev[0], hipEventDisableTiming) != hipSuccess ||

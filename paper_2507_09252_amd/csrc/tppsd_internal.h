@@ -129,6 +129,8 @@ struct DraftArgs {
   float *d_tau, *d_t, *d_logg, *d_logf, *d_mix, *d_logtype;
   int32_t *d_k;
   int MG;                   // row stride of the draft record (max_gamma)
+  int w_lds;                // stage the weight matrices in LDS (fused_draft_weight_elems more)
+  int attn_mfma;            // attention on MFMA even for <= 4 heads (else the vector-ALU form)
 };
 // whether the fused draft kernel supports a model of these sizes: the
 // matrix-vector products need d / 8 and d_ffn / 8 to be powers of two <= 64,
@@ -140,6 +142,10 @@ inline bool fused_draft_ok(int L, int d, int H, int F) {
          F / 8 <= 64 && pow2(H) && d == 16 * H;
 }
 size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H);
+// elements of the draft's weight matrices (per layer QKV, out, FFN; decoder)
+size_t fused_draft_weight_elems(int L, int d, int F, int M, int K);
+// LDS of one workgroup on gfx950
+constexpr size_t LDS_PER_WG = 160 * 1024;
 
 // Homogeneous-Poisson drafting (tppsd_poisson.hip)
 struct PoissonDraftArgs {
@@ -158,6 +164,8 @@ void launch_draft_poisson(const PoissonDraftArgs &a, hipStream_t st);
 
 // ---- launchers (tppsd_kernels.hip) ----
 void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t st);
+// raises the dynamic LDS limit of the fused draft kernels to `bytes`; nonzero on failure
+int allow_draft_fused_lds(size_t bytes);
 void launch_embed(float *x, int T, int d, int P, const TokSrc &src, const void *wtype, int bf16,
                   const float *freq, int K, hipStream_t st);
 void launch_layernorm(const float *x, void *y, int bf16, const float *g, const float *b, int T, int d,

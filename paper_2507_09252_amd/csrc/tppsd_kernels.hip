@@ -412,24 +412,27 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
   uint4 ra[D][LN ? 1 : AV], rb[D][BV];
   float4 rx[D][LN ? AV * XV : 1];
   float mu[LN ? AV : 1], rs[LN ? AV : 1];
+  // Loads are unconditional (rows and columns clamped into the matrices) so
+  // that no branch separates them from their use: the compiler then waits
+  // for each ring slot's own loads only, and the next stages stay in flight.
+  // Columns past K are zeroed where the stage is stored to LDS.
   auto gload = [&](uint4 *pa, float4 *px, uint4 *pb, int k0) {
 #pragma unroll
     for (int i = 0; i < AV; ++i) {
-      const int v = tid + 256 * i, row = v / VPR, k = k0 + (v - row * VPR) * VE;
+      const int v = tid + 256 * i, row = v / VPR, k = min(k0 + (v - row * VPR) * VE, K - VE);
       const size_t r = (size_t)min(m0 + row, T - 1);
       if (LN) {
 #pragma unroll
-        for (int c = 0; c < XV; ++c)
-          px[i * XV + c] = (k < K) ? *(const float4 *)(xf + r * K + k + 4 * c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int c = 0; c < XV; ++c) px[i * XV + c] = *(const float4 *)(xf + r * K + k + 4 * c);
       } else {
-        pa[i] = (k < K) ? *(const uint4 *)(X + r * K + k) : make_uint4(0u, 0u, 0u, 0u);
+        pa[i] = *(const uint4 *)(X + r * K + k);
       }
     }
 #pragma unroll
     for (int i = 0; i < BV; ++i) {
-      const int v = tid + 256 * i, row = v / VPR, k = k0 + (v - row * VPR) * VE;
+      const int v = tid + 256 * i, row = v / VPR, k = min(k0 + (v - row * VPR) * VE, K - VE);
       const size_t r = (size_t)min(n0 + row, N - 1);
-      pb[i] = (k < K) ? *(const uint4 *)(W + r * K + k) : make_uint4(0u, 0u, 0u, 0u);
+      pb[i] = *(const uint4 *)(W + r * K + k);
     }
   };
   auto lstore = [&](int buf, const uint4 *pa, const float4 *px, const uint4 *pb, int k0) {
@@ -464,14 +467,14 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
           w = make_uint4(__float_as_uint(y[0]), __float_as_uint(y[1]), __float_as_uint(y[2]), __float_as_uint(y[3]));
         }
       } else {
-        w = pa[i];
+        w = (k0 + kv * VE < K) ? pa[i] : make_uint4(0u, 0u, 0u, 0u);
       }
       *(uint4 *)&As[buf][row][kv * VE] = w;
     }
 #pragma unroll
     for (int i = 0; i < BV; ++i) {
       const int v = tid + 256 * i, row = v / VPR, kv = v - row * VPR;
-      *(uint4 *)&Bs[buf][row][kv * VE] = pb[i];
+      *(uint4 *)&Bs[buf][row][kv * VE] = (k0 + kv * VE < K) ? pb[i] : make_uint4(0u, 0u, 0u, 0u);
     }
   };
   // the first D stages' loads go out before anything else
@@ -483,17 +486,18 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
       gs[k] = lg[k];
       bs[k] = lb[k];
     }
-    // row statistics from the ring (zero-filled past K): mean, then the
-    // sum of squared deviations over the K real columns
+    // row statistics from the ring over the K real columns: mean, then the
+    // sum of squared deviations
 #pragma unroll
     for (int i = 0; i < AV; ++i) {
       const int kv = (tid + 256 * i) % VPR;
       float sum = 0.f;
 #pragma unroll
       for (int u = 0; u < D; ++u)
-        if (u < nst) {
 #pragma unroll
-          for (int c = 0; c < XV; ++c) {
+        for (int c = 0; c < XV; ++c) {
+          const int k = u * BK + kv * VE + 4 * c;
+          if (k < K) {
             const float4 xv = rx[u][i * XV + c];
             sum += (xv.x + xv.y) + (xv.z + xv.w);
           }
@@ -575,6 +579,156 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
       epilogue8<ELT>(e, r, n, cv);
     } else {
       for (int i = 0; i < N - n; ++i) epilogue<ELT>(e, r, n + i, cv[i]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 GEMM with operands moved straight from global memory into LDS
+// (global_load_lds, 16 bytes per lane) through an S-stage ring. No register
+// holds an operand in flight, so the loads of the next S - 1 stages overlap
+// the MFMAs of the current one, and each wave waits for its own loads by
+// count (s_waitcnt vmcnt). Tiles are stored unpadded with their 16-byte
+// chunks XOR-swizzled by row (chunk c of row r at c ^ (r mod chunks per
+// row)), so that the rows one MFMA fragment reads fall on different banks.
+// Needs K to be a multiple of the stage depth BK = 32 KSN.
+// ---------------------------------------------------------------------------
+
+// waits until at most CNT vector-memory operations of this wave are outstanding
+template <int CNT> __device__ __forceinline__ void wait_vmcnt() {
+  static_assert(CNT >= 0 && CNT < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((CNT & 15) | ((CNT >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+
+// One LDS array per ring slot, addressed with compile-time slot numbers (the
+// stage loop is unrolled by S) inside one inlined function that takes the
+// slots as restrict pointers: the compiler then knows that reads of one slot
+// never alias the loads still landing in the others and does not wait for
+// them. The waits are explicit and per wave.
+template <int BM, int BN, int KSN> struct DlTile {
+  static constexpr int BK = 32 * KSN, CPR = BK / 8;     // 16-byte chunks per tile row
+  static constexpr int ACH = BM * CPR, BCH = BN * CPR;  // chunks per stage
+  static constexpr int NIA = ACH / 256, NIB = BCH / 256;
+  static constexpr int NI = NIA + NIB;                   // DMA instructions per thread per stage
+  static constexpr int STAGE = (ACH + BCH) * 16;         // bytes
+  static_assert(NIA >= 1 && NIB >= 1 && ACH % 256 == 0 && BCH % 256 == 0, "tile too small for 256 threads");
+};
+
+template <int BM, int BN, int KSN, int S>
+__device__ __forceinline__ void dl_mainloop(char *__restrict__ s0, char *__restrict__ s1, char *__restrict__ s2,
+                                            char *__restrict__ s3, const bf16_t *const *srcA,
+                                            const bf16_t *const *srcB, int nst, f32x4_t (*acc)[BN / 32]) {
+  typedef DlTile<BM, BN, KSN> G;
+  constexpr int CPR = G::CPR, ACH = G::ACH, NIA = G::NIA, NIB = G::NIB, NI = G::NI, BK = G::BK;
+  constexpr int TM = BM / 32, TN = BN / 32;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rr = lane & 15, g = lane >> 4;
+  const int wm = (wave >> 1) * (BM / 2), wn = (wave & 1) * (BN / 2);
+  char *const slots[4] = {s0, s1, s2, s3};
+  auto issue = [&](char *base, int st) {
+    const int k0 = st * BK;
+#pragma unroll
+    for (int i = 0; i < NIA; ++i)
+      __builtin_amdgcn_global_load_lds((const void *)(srcA[i] + k0), (lds_ptr_t)(base + (4 * i + wave) * 1024), 16, 0,
+                                       0);
+#pragma unroll
+    for (int i = 0; i < NIB; ++i)
+      __builtin_amdgcn_global_load_lds((const void *)(srcB[i] + k0),
+                                       (lds_ptr_t)(base + ACH * 16 + (4 * i + wave) * 1024), 16, 0, 0);
+  };
+#pragma unroll
+  for (int u = 0; u < S - 1; ++u)
+    if (u < nst) issue(slots[u], u);
+  for (int s0i = 0; s0i < nst; s0i += S) {
+#pragma unroll
+    for (int u = 0; u < S; ++u) {
+      const int st = s0i + u;
+      if (st < nst) {
+        // stage st has landed once only the stages issued after it are pending
+        if (st + S - 2 < nst) wait_vmcnt<(S - 2) * NI>();
+        else wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();   // all of stage st is in LDS; stage st - 1's slot is free
+        if (st + S - 1 < nst) issue(slots[(u + S - 1) % S], st + S - 1);
+        const char *As = slots[u], *Bs = As + ACH * 16;
+#pragma unroll
+        for (int ks = 0; ks < KSN; ++ks) {
+          bf16x8_t a[TM], b[TN];
+#pragma unroll
+          for (int i = 0; i < TM; ++i) {
+            const int row = wm + 16 * i + rr;
+            a[i] = *(const bf16x8_t *)(As + (row * CPR + ((4 * ks + g) ^ (row % CPR))) * 16);
+          }
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int row = wn + 16 * j + rr;
+            b[j] = *(const bf16x8_t *)(Bs + (row * CPR + ((4 * ks + g) ^ (row % CPR))) * 16);
+          }
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int KSN, int S>
+__global__ __launch_bounds__(256) void k_gemm_dl(const bf16_t *__restrict__ X, const bf16_t *__restrict__ W, int T,
+                                                 int N, int K, Epi e) {
+  typedef DlTile<BM, BN, KSN> G;
+  constexpr int CPR = G::CPR, NIA = G::NIA, NIB = G::NIB, STAGE = G::STAGE, BK = G::BK;
+  constexpr int TM = BM / 32, TN = BN / 32, CLD = BN + 4;
+  static_assert(S >= 2 && S <= 4, "ring of 2 to 4 stages");
+  __shared__ __attribute__((aligned(1024))) char st0[STAGE];
+  __shared__ __attribute__((aligned(1024))) char st1[STAGE];
+  __shared__ __attribute__((aligned(1024))) char st2[S > 2 ? STAGE : 1024];
+  __shared__ __attribute__((aligned(1024))) char st3[S > 3 ? STAGE : 1024];
+  __shared__ __attribute__((aligned(16))) float Cs[BM * CLD];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rr = lane & 15, g = lane >> 4;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int wm = (wave >> 1) * (BM / 2), wn = (wave & 1) * (BN / 2);
+  // DMA instruction i of this thread moves chunk p = (4 i + wave) 64 + lane of
+  // the stage's A (then B) tile: row p / CPR, stored chunk p mod CPR, which
+  // holds logical chunk (p mod CPR) ^ (row mod CPR). Rows past T or N are
+  // clamped (their results are never stored).
+  const bf16_t *srcA[NIA];
+  const bf16_t *srcB[NIB];
+#pragma unroll
+  for (int i = 0; i < NIA; ++i) {
+    const int p = (4 * i + wave) * 64 + lane, row = p / CPR, c = (p % CPR) ^ (row % CPR);
+    srcA[i] = X + (size_t)min(m0 + row, T - 1) * K + 8 * c;
+  }
+#pragma unroll
+  for (int i = 0; i < NIB; ++i) {
+    const int p = (4 * i + wave) * 64 + lane, row = p / CPR, c = (p % CPR) ^ (row % CPR);
+    srcB[i] = W + (size_t)min(n0 + row, N - 1) * K + 8 * c;
+  }
+  f32x4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  dl_mainloop<BM, BN, KSN, S>(st0, st1, st2, st3, srcA, srcB, K / BK, acc);
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) Cs[(wm + 16 * i + 4 * g + v) * CLD + wn + 16 * j + rr] = acc[i][j][v];
+  __syncthreads();
+  for (int gi = tid; gi < BM * (BN / 8); gi += 256) {
+    const int row = gi / (BN / 8), c8 = gi - row * (BN / 8);
+    const int r = m0 + row, n = n0 + 8 * c8;
+    if (r >= T || n >= N) continue;
+    float cv[8];
+    load8f(Cs + row * CLD + 8 * c8, cv);
+    if (n + 8 <= N) {
+      epilogue8<bf16_t>(e, r, n, cv);
+    } else {
+      for (int i = 0; i < N - n; ++i) epilogue<bf16_t>(e, r, n + i, cv[i]);
     }
   }
 }
@@ -855,6 +1009,171 @@ template <> struct DraftStep<float> {
   }
 };
 
+// Causal attention of P <= 2 new queries on the vector ALU, for draft
+// models with at most 4 heads of width 16: the 256 threads split into H
+// groups, one per head; thread `sub` of a group takes the key units sub,
+// sub + 256 / H, ... (a unit is 4 keys for bf16 caches, half a block of the
+// blocked value layout, 2 for fp32), loads the unit's key rows and values
+// with 8- and 16-byte loads, scores them against both queries in fp32 and keeps its
+// own online softmax (max, sum, 16 output columns per query). The threads of
+// a head then merge: maximum, rescaled sums and outputs through wave
+// reductions and LDS. With only one or two queries per head the MFMA form
+// computes mostly padding; here every thread's loads go out together and
+// the step costs about one memory latency per unit a thread holds.
+// red: LDS scratch of at least 4 * 2 * 18 floats.
+template <typename ELT>
+__device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
+                                  int H, int P, int pos0, int d, float *red) {
+  constexpr int DH = 16, U = sizeof(ELT) == 2 ? 4 : 2;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tph = blockDim.x / H, h = tid / tph, sub = tid - h * tph;
+  const int n_keys = min(pos0 + P, cap);
+  const size_t row0 = seq_row0 + (size_t)h * cap;
+  float q[2][DH];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int j = 0; j < DH; ++j) q[p][j] = (p < P) ? qs[p * d + h * DH + j] * 0.25f : 0.f;   // 1 / sqrt(16)
+  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f}, o[2][DH];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int j = 0; j < DH; ++j) o[p][j] = 0.f;
+  const int nunits = (n_keys + U - 1) / U;
+  for (int u = sub; u < nunits; u += tph) {
+    const int k0 = u * U;
+    // the unit lies inside the slab (k0 < cap, the slab holds cap rounded
+    // up to 8 positions); keys at or past n_keys are masked below. Values
+    // stay packed in registers and are widened where they are used.
+    uint4 kr[8];
+    uint2 vr2[16];
+    uint4 vr4[8];
+    if constexpr (sizeof(ELT) == 2) {
+      const uint4 *kp = (const uint4 *)(kc + (row0 + k0) * DH);   // 4 rows x 16
+#pragma unroll
+      for (int i = 0; i < 8; ++i) kr[i] = kp[i];
+      // value column j of the block holding k0: 8 positions, this unit's 4 at k0 & 4
+      const bf16_t *vb = vc + v_at<bf16_t>(row0, k0 & ~7, 0, DH) + (k0 & 4);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) vr2[j] = *(const uint2 *)(vb + 8 * j);
+    } else {
+      const uint4 *kp = (const uint4 *)(kc + (row0 + k0) * DH);   // 2 rows x 16
+      const uint4 *vp = (const uint4 *)(vc + (row0 + k0) * DH);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) kr[i] = kp[i];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) vr4[i] = vp[i];
+    }
+    // element (key i, column j) of the unit's keys and values
+    auto kval = [&](int i, int j) -> float {
+      if constexpr (sizeof(ELT) == 2) {
+        const uint4 w = kr[2 * i + (j >> 3)];
+        const int e = (j & 7) >> 1;
+        const uint32_t x = e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
+        return (j & 1) ? __uint_as_float(x & 0xFFFF0000u) : __uint_as_float(x << 16);
+      } else {
+        const uint4 w = kr[4 * i + (j >> 2)];
+        const int e = j & 3;
+        return __uint_as_float(e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w);
+      }
+    };
+    auto vval = [&](int i, int j) -> float {
+      if constexpr (sizeof(ELT) == 2) {
+        const uint2 w = vr2[j];   // column j, the unit's 4 positions
+        const uint32_t x = (i >> 1) ? w.y : w.x;
+        return (i & 1) ? __uint_as_float(x & 0xFFFF0000u) : __uint_as_float(x << 16);
+      } else {
+        const uint4 w = vr4[4 * i + (j >> 2)];
+        const int e = j & 3;
+        return __uint_as_float(e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w);
+      }
+    };
+    // both queries in one pass over the unit (each key and value element is
+    // widened once); a query that does not exist (P = 1) sees only masked keys
+    float sc0[U], sc1[U], mx0 = -INFINITY, mx1 = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+      for (int j = 0; j < DH; ++j) {
+        const float kv = kval(i, j);
+        a0 += q[0][j] * kv;
+        a1 += q[1][j] * kv;
+      }
+      const int pos = k0 + i;
+      sc0[i] = (pos < n_keys && pos <= pos0) ? a0 : -INFINITY;
+      sc1[i] = (P > 1 && pos < n_keys && pos <= pos0 + 1) ? a1 : -INFINITY;
+      mx0 = fmaxf(mx0, sc0[i]);
+      mx1 = fmaxf(mx1, sc1[i]);
+    }
+    const float mn0 = fmaxf(m[0], mx0), mn1 = fmaxf(m[1], mx1);
+    // rescale factors (1 while a query has seen no key, its state being zero)
+    const float al0 = (mn0 == -INFINITY) ? 1.f : expf(m[0] - mn0);
+    const float al1 = (mn1 == -INFINITY) ? 1.f : expf(m[1] - mn1);
+    float e0[U], e1[U];
+    l[0] *= al0;
+    l[1] *= al1;
+#pragma unroll
+    for (int i = 0; i < U; ++i) {
+      e0[i] = (sc0[i] == -INFINITY) ? 0.f : expf(sc0[i] - mn0);
+      e1[i] = (sc1[i] == -INFINITY) ? 0.f : expf(sc1[i] - mn1);
+      l[0] += e0[i];
+      l[1] += e1[i];
+    }
+    // slots at or past n_keys hold stale or unwritten values: a zero weight
+    // times a non-finite value would still poison the sum, so they are skipped
+#pragma unroll
+    for (int j = 0; j < DH; ++j) {
+      float s0 = o[0][j] * al0, s1 = o[1][j] * al1;
+#pragma unroll
+      for (int i = 0; i < U; ++i) {
+        const float vv = (k0 + i < n_keys) ? vval(i, j) : 0.f;
+        s0 += e0[i] * vv;
+        s1 += e1[i] * vv;
+      }
+      o[0][j] = s0;
+      o[1][j] = s1;
+    }
+    m[0] = mn0;
+    m[1] = mn1;
+  }
+  // merge the threads of each head: per wave first, then across the head's waves
+  const int wph = tph >> 6;   // waves per head (1, 2 or 4)
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (p >= P) break;
+    const float mw = wave_max(m[p]);
+    if (lane == 0) red[wave * 36 + p * 18] = mw;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (p >= P) break;
+    float M = -INFINITY;
+    for (int w = h * wph; w < (h + 1) * wph; ++w) M = fmaxf(M, red[w * 36 + p * 18]);
+    const float f = (m[p] == -INFINITY) ? 0.f : expf(m[p] - M);
+    const float lw = wave_sum(l[p] * f);
+    float ow[DH];
+#pragma unroll
+    for (int j = 0; j < DH; ++j) ow[j] = wave_sum(o[p][j] * f);
+    if (lane == 0) {
+      red[wave * 36 + p * 18 + 1] = lw;
+#pragma unroll
+      for (int j = 0; j < DH; ++j) red[wave * 36 + p * 18 + 2 + j] = ow[j];
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < P * H * DH; idx += blockDim.x) {
+    const int p = idx / (H * DH), rest = idx - p * H * DH, hh = rest / DH, j = rest - hh * DH;
+    float L = 0.f, O = 0.f;
+    for (int w = hh * wph; w < (hh + 1) * wph; ++w) {
+      L += red[w * 36 + p * 18 + 1];
+      O += red[w * 36 + p * 18 + 2 + j];
+    }
+    os[p * d + hh * DH + j] = rnd_act<ELT>(L > 0.f ? O / L : 0.f);
+  }
+}
+
 // causal attention of P <= 2 new queries (positions pos0 .. pos0 + P - 1,
 // already in the cache) over one sequence's cache, d_head = 16, on MFMA in
 // the layout of k_attn_mfma: S^T = K Q^T with permuted key rows leaves lane
@@ -990,11 +1309,21 @@ inline __host__ __device__ int fused_draft_vec_floats(int L, int d, int F, int M
   return L * (9 * d + F) + 4 * d + 3 * M + K;
 }
 
-size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H) {
+// floats before the staged weights (activations, merge scratch, vectors),
+// rounded up to a 16-byte boundary
+inline __host__ __device__ int fused_draft_head_floats(int L, int d, int F, int M, int K, int H) {
   const int Fm = d > F ? d : F, dh = d / H;
-  return (size_t)(2 * d + 2 * Fm + 2 * d + 2 * d + 2 * F + 4 * d + 3 * M + K + 8 + 4 * H * 2 * (dh + 2) +
-                  fused_draft_vec_floats(L, d, F, M, K)) *
-         sizeof(float);
+  const int n = 2 * d + 2 * Fm + 2 * d + 2 * d + 2 * F + 4 * d + 3 * M + K + 8 + 4 * H * 2 * (dh + 2) +
+                fused_draft_vec_floats(L, d, F, M, K);
+  return (n + 3) & ~3;
+}
+
+size_t fused_draft_weight_elems(int L, int d, int F, int M, int K) {
+  return (size_t)L * (4 * d * d + 2 * F * d) + (size_t)4 * d * d + (size_t)(3 * M + K) * d;
+}
+
+size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H) {
+  return (size_t)fused_draft_head_floats(L, d, F, M, K, H) * sizeof(float);
 }
 
 // CD / CF: chunks per lane of the matrix-vector products over d and over
@@ -1043,6 +1372,32 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
     cp(v + 3 * d + 3 * M, a.k2_b, K);
     cp(v + 3 * d + 3 * M + K, a.freq, d);
   }
+  // the weight matrices too, when the host found room for them: the
+  // per-step matrix-vector products then read only LDS. LDS layout: per
+  // layer QKV (3d x d), out (d x d), FFN in (F x d), FFN out (d x F); then
+  // [E; V_k1] (4d x d), the mixture heads (3M x d), the type head (K x d).
+  ELT *const wl = (ELT *)(sm + fused_draft_head_floats(a.L, d, F, M, K, H));
+  const size_t LS = (size_t)4 * d * d + (size_t)2 * F * d;
+  if (a.w_lds) {
+    constexpr int VE = 16 / sizeof(ELT);
+    auto cpw = [&](size_t off, const void *src, size_t cnt) {   // cnt: a multiple of 16 bytes
+      const uint4 *sp = (const uint4 *)src;
+      uint4 *dp = (uint4 *)(wl + off);
+      for (size_t i = tid; i < cnt / VE; i += blockDim.x) dp[i] = sp[i];
+    };
+    for (int ly = 0; ly < a.L; ++ly) {
+      cpw(ly * LS, a.layer[ly].qkv_w, (size_t)3 * d * d);
+      cpw(ly * LS + (size_t)3 * d * d, a.layer[ly].out_w, (size_t)d * d);
+      cpw(ly * LS + (size_t)4 * d * d, a.layer[ly].ffn1_w, (size_t)F * d);
+      cpw(ly * LS + (size_t)4 * d * d + (size_t)F * d, a.layer[ly].ffn2_w, (size_t)d * F);
+    }
+    cpw(a.L * LS, a.Ek1_w, (size_t)4 * d * d);
+    cpw(a.L * LS + (size_t)4 * d * d, a.mix_w, (size_t)3 * M * d);
+    cpw(a.L * LS + (size_t)4 * d * d + (size_t)3 * M * d, a.k2_w, (size_t)K * d);
+  }
+  auto wmat = [&](const void *glob, size_t off) -> const ELT * {
+    return a.w_lds ? (const ELT *)(wl + off) : (const ELT *)glob;
+  };
   const float *hvec = vec + a.L * (9 * d + F);
   const float *lnf_g = hvec, *lnf_b = hvec + d, *k1_b = hvec + 2 * d, *mix_b = hvec + 3 * d,
               *k2_b = hvec + 3 * d + 3 * M, *freq = hvec + 3 * d + 3 * M + K;
@@ -1076,7 +1431,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
                   *ln2_b = lv + 7 * d, *ffn1_b = lv + 8 * d, *ffn2_b = lv + 8 * d + F;
       wg_layernorm<ELT>(xs, as, ln1_g, ln1_b, P, d);
       __syncthreads();
-      const ELT *wq = (const ELT *)w.qkv_w;
+      const ELT *wq = wmat(w.qkv_w, ly * LS);
       wg_gemv_cpl<ELT, CD>(
           3 * d, d, P, [&](int nn) { return wq + (size_t)nn * d; }, [&](int, int p) { return as + p * d; },
           [&](int p, int nn, float acc) {
@@ -1094,16 +1449,20 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
             }
           });
       __syncthreads();
-      wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
+      if (H <= 4 && !a.attn_mfma)
+        wg_attention_valu<ELT>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
+      else
+        wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       __syncthreads();
-      const ELT *wo = (const ELT *)w.out_w;
+      const ELT *wo = wmat(w.out_w, ly * LS + (size_t)3 * d * d);
       wg_gemv_cpl<ELT, CD>(
           d, d, P, [&](int nn) { return wo + (size_t)nn * d; }, [&](int, int p) { return os + p * d; },
           [&](int p, int nn, float acc) { xs[p * d + nn] += acc + out_b[nn]; });
       __syncthreads();
       wg_layernorm<ELT>(xs, as, ln2_g, ln2_b, P, d);
       __syncthreads();
-      const ELT *w1 = (const ELT *)w.ffn1_w, *w2 = (const ELT *)w.ffn2_w;
+      const ELT *w1 = wmat(w.ffn1_w, ly * LS + (size_t)4 * d * d);
+      const ELT *w2 = wmat(w.ffn2_w, ly * LS + (size_t)4 * d * d + (size_t)F * d);
       wg_gemv_cpl<ELT, CD>(
           F, d, P, [&](int nn) { return w1 + (size_t)nn * d; }, [&](int, int p) { return as + p * d; },
           [&](int p, int nn, float acc) { hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + ffn1_b[nn], 0.f)); });
@@ -1118,14 +1477,15 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
     // logits in one pass
     wg_layernorm<ELT>(xs + (P - 1) * d, as, lnf_g, lnf_b, 1, d);
     __syncthreads();
-    const ELT *we = (const ELT *)a.Ek1_w;
+    const ELT *we = wmat(a.Ek1_w, a.L * LS);
     wg_gemv_cpl<ELT, CD>(
         4 * d, d, 1, [&](int nn) { return we + (size_t)nn * d; }, [&](int, int) { return (const float *)as; },
         [&](int, int nn, float acc) {
           es[nn] = (nn < 3 * d) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * d]));
         });
     __syncthreads();
-    const ELT *mw = (const ELT *)a.mix_w, *kw = (const ELT *)a.k2_w;
+    const ELT *mw = wmat(a.mix_w, a.L * LS + (size_t)4 * d * d);
+    const ELT *kw = wmat(a.k2_w, a.L * LS + (size_t)4 * d * d + (size_t)3 * M * d);
     wg_gemv_cpl<ELT, CD>(
         3 * M + K, d, 1,
         [&](int nn) { return nn < 3 * M ? mw + (size_t)nn * d : kw + (size_t)(nn - 3 * M) * d; },
@@ -1174,7 +1534,8 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
 }
 
 void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
-  const size_t lds = fused_draft_lds_bytes(a.L, a.d, a.F, a.M, a.K, a.H);
+  const size_t lds = fused_draft_lds_bytes(a.L, a.d, a.F, a.M, a.K, a.H) +
+                     (a.w_lds ? fused_draft_weight_elems(a.L, a.d, a.F, a.M, a.K) * (bf16 ? 2 : 4) : 0);
   const int cd = gemv_cpl(a.d), cf = gemv_cpl(a.F);
   // d_head = 16 only (fused_draft_ok); chunk counts 2, 4 or 8
   auto go = [&](auto kern) { kern<<<a.B, 256, lds, s>>>(a); };
@@ -1194,6 +1555,22 @@ void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
     TPPSD_FD(float)
   }
 #undef TPPSD_FD
+}
+
+int allow_draft_fused_lds(size_t bytes) {
+  int bad = 0;
+  auto set = [&](auto kern) {
+    bad |= hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) !=
+           hipSuccess;
+  };
+#define TPPSD_FD(ELT)                                                                          \
+  set(k_draft_fused<ELT, 16, 2, 2>), set(k_draft_fused<ELT, 16, 2, 4>), set(k_draft_fused<ELT, 16, 2, 8>); \
+  set(k_draft_fused<ELT, 16, 4, 2>), set(k_draft_fused<ELT, 16, 4, 4>), set(k_draft_fused<ELT, 16, 4, 8>); \
+  set(k_draft_fused<ELT, 16, 8, 2>), set(k_draft_fused<ELT, 16, 8, 4>), set(k_draft_fused<ELT, 16, 8, 8>);
+  TPPSD_FD(bf16_t)
+  TPPSD_FD(float)
+#undef TPPSD_FD
+  return bad;
 }
 
 // ---------------------------------------------------------------------------
@@ -1545,6 +1922,15 @@ static void gemm_dispatch(const void *X, const LnA *ln, const void *W, int T, in
     hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, x, xf, lg, lb, w, T, N, K, epi);
   };
   if (!ln) {
+    // bf16, a few hundred 64 x 64 tiles or fewer over at least 512 rows, K a
+    // multiple of 128: direct-to-LDS ring of 32 x 32 x 128 stages (measured
+    // faster there; the register ring keeps the very tall GEMMs)
+    if (sizeof(ELT) == 2 && T >= 512 && K % 128 == 0 && (long)((N + 63) / 64) * ((T + 63) / 64) < 1024) {
+      dim3 grid((N + 31) / 32, (T + 31) / 32);
+      hipExtLaunchKernelGGL(k_gemm_dl<32, 32, 4, 3>, grid, dim3(256), 0, s, ev0, ev1, 0, (const bf16_t *)X,
+                            (const bf16_t *)W, T, N, K, epi);
+      return;
+    }
     if (big) {
       go(k_gemm_lds<ELT, 64, 64, false, 2, 2>, 64, 64);
     } else {
