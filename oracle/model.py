@@ -23,6 +23,16 @@ eps = 1e-5, no dropout, V_k1 of size D x D, E without bias, sigma kept as
 s = log(sigma). Times are float32; the encoding's argument is the float32
 product of t and the float32 frequency.
 
+AttNHP encoder (App. D.4, with cfg.encoder == "attnhp"): the temporal
+encoding uses wavelengths between m and 5M, z_j(t) = sin(t / (m (5M/m)^{j/D}))
+for even j and cos(t / (m (5M/m)^{(j-1)/D})) for odd j (the printed second
+sine read as a cosine: the pair (j-1, j) would repeat a dimension otherwise);
+h^(0) is the type embedding; each layer forms q, k, v = W [z(t); h] + b (the
+constant 1 of [1; z; h] is the bias) and updates
+h += tanh(sum_j f_ij v_j / (1 + sum_j f_ij)), f_ij = exp(q_i . k_j / sqrt(d_head))
+over j <= i, per head, heads concatenated; no LayerNorm, feed-forward block
+or output projection, and the decoder reads h^(L).
+
 bf16 mode emulates the rounding points of a bf16 implementation: every
 Linear input (LN outputs, attention output, ReLU output, the decoder's e and
 tanh activations) and q, k, v are rounded to bf16; the residual stream,
@@ -58,11 +68,16 @@ class Model:
         self.K = cfg.n_types
         self.w = {k: np.asarray(v, dtype=np.float64) for k, v in weights.items()}
         self.rb = round_bf16 if cfg.prec == "bf16" else _ident
+        self.attnhp = getattr(cfg, "encoder", "thp") == "attnhp"
 
     # ---- encoder pieces -------------------------------------------------
     def frequencies(self) -> np.ndarray:
-        """Float32 frequency table 10000^(-(j - j mod 2)/D), j = 0..D-1 (App. D.4, THP)."""
+        """Float32 frequency table (App. D.4): THP 10000^(-(j - j mod 2)/D);
+        AttNHP 1 / (m (5M/m)^((j - j mod 2)/D)), j = 0..D-1."""
         j = np.arange(self.d)
+        if self.attnhp:
+            m, M = float(self.cfg.time_m), float(self.cfg.time_M)
+            return (1.0 / (m * np.power(5.0 * M / m, (j - j % 2) / self.d))).astype(np.float32)
         return np.power(10000.0, -(j - j % 2) / self.d).astype(np.float32)
 
     def time_encoding(self, t) -> np.ndarray:
@@ -73,8 +88,28 @@ class Model:
         return np.where(j % 2 == 0, np.sin(arg), np.cos(arg))
 
     def embed(self, t, k) -> np.ndarray:
-        """X = z(t) + W^T onehot(k)  (§4.2 Encoder, summation fusion)."""
+        """X = z(t) + W^T onehot(k)  (§4.2 Encoder, summation fusion); for AttNHP
+        h^(0) = W^T onehot(k), the time entering every layer through [z(t); h]."""
+        if self.attnhp:
+            return self.w["type_emb"][np.asarray(k)].copy()
         return self.time_encoding(t) + self.w["type_emb"][np.asarray(k)]
+
+    def _attnhp_layer(self, l, x, z, kc_fn, mask):
+        """One AttNHP layer: q, k, v from [z; h] (bias = the constant input), per
+        head sum_j f v / (1 + sum_j f), h += tanh(.). kc_fn(k, v) returns the keys
+        and values attended over (the new ones, or the cache holding them)."""
+        rb = self.rb
+        p = f"layers.{l}."
+        u = np.concatenate([rb(z), rb(x)], axis=-1)
+        qkv = rb(self._lin(u, p + "qkv"))
+        q, kk, v = (self._split_heads(qkv[..., i * self.d:(i + 1) * self.d]) for i in range(3))
+        Kc, Vc = kc_fn(kk, v)
+        s = q @ np.swapaxes(Kc, -1, -2) / math.sqrt(self.dh)
+        s = np.where(mask, s, -np.inf)
+        smax = np.maximum(s.max(axis=-1, keepdims=True), 0.0)   # the 1 of the denominator is exp(0)
+        pr = np.exp(s - smax)
+        o = (pr @ Vc) / (np.exp(-smax) + pr.sum(axis=-1, keepdims=True))
+        return x + np.tanh(rb(self._merge_heads(o)))
 
     @staticmethod
     def layer_norm(x, g, b):
@@ -107,6 +142,11 @@ class Model:
         x = self.embed(t, k)
         N = x.shape[-2]
         causal = np.tril(np.ones((N, N), dtype=bool))
+        if self.attnhp:
+            z = self.time_encoding(t)
+            for l in range(self.L):
+                x = self._attnhp_layer(l, x, z, lambda kk, v: (kk, v), causal)
+            return x
         for l in range(self.L):
             p = f"layers.{l}."
             a = rb(self.layer_norm(x, self.w[p + "ln1.g"], self.w[p + "ln1.b"]))
@@ -147,6 +187,15 @@ class Model:
         rows = np.arange(B) if rows is None else np.asarray(rows, dtype=np.int64)
         bidx = rows[:, None]
         keymask = np.arange(n_keys)[None, None, :] <= pos[:, :, None]  # [B, P, n_keys]
+        if self.attnhp:
+            z = self.time_encoding(t)
+            for l in range(self.L):
+                def kc_fn(kk, v, l=l):
+                    cache.K[l][bidx, :, pos, :] = np.moveaxis(kk, 1, 2)
+                    cache.V[l][bidx, :, pos, :] = np.moveaxis(v, 1, 2)
+                    return cache.K[l][rows, :, :n_keys, :], cache.V[l][rows, :, :n_keys, :]
+                x = self._attnhp_layer(l, x, z, kc_fn, keymask[:, None, :, :])
+            return x
         for l in range(self.L):
             p = f"layers.{l}."
             a = rb(self.layer_norm(x, self.w[p + "ln1.g"], self.w[p + "ln1.b"]))

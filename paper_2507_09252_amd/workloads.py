@@ -33,6 +33,10 @@ PREC_FP32 = "fp32"
 PREC_BF16 = "bf16"
 
 
+ENC_THP = "thp"          # THP encoder: summed encoding, pre-LN softmax-attention blocks with FFN
+ENC_ATTNHP = "attnhp"    # AttNHP encoder (App. D.4): q, k, v from [1; z(t); h], h += tanh(attention)
+
+
 @dataclasses.dataclass(frozen=True)
 class ModelCfg:
     n_layers: int
@@ -42,6 +46,9 @@ class ModelCfg:
     n_mix: int
     n_types: int
     prec: str = PREC_FP32
+    encoder: str = ENC_THP
+    time_m: float = 1.0      # AttNHP time encoding: shortest wavelength scale m
+    time_M: float = 100.0    # ... and M (longest wavelength 5 M)
 
     @property
     def d_head(self) -> int:
@@ -117,6 +124,13 @@ def weight_names(cfg: ModelCfg) -> List[Tuple[str, Tuple[int, ...], str]]:
     """
     d, F, M, K = cfg.d_model, cfg.d_ffn, cfg.n_mix, cfg.n_types
     out = [("type_emb", (K, d), "mat")]
+    if cfg.encoder == ENC_ATTNHP:
+        # q, k, v = W [z(t); h] + b, W in R^{3d x 2d}: the constant input 1 of
+        # the concatenation is the bias column
+        for l in range(cfg.n_layers):
+            p = f"layers.{l}."
+            out += [(p + "qkv.w", (3 * d, 2 * d), "mat"), (p + "qkv.b", (3 * d,), "bias")]
+        return out + _decoder_names(d, M, K)
     for l in range(cfg.n_layers):
         p = f"layers.{l}."
         out += [
@@ -127,8 +141,12 @@ def weight_names(cfg: ModelCfg) -> List[Tuple[str, Tuple[int, ...], str]]:
             (p + "ffn1.w", (F, d), "mat"), (p + "ffn1.b", (F,), "bias"),
             (p + "ffn2.w", (d, F), "mat"), (p + "ffn2.b", (d,), "bias"),
         ]
-    out += [
-        ("lnf.g", (d,), "ln_g"), ("lnf.b", (d,), "ln_b"),
+    out += [("lnf.g", (d,), "ln_g"), ("lnf.b", (d,), "ln_b")]
+    return out + _decoder_names(d, M, K)
+
+
+def _decoder_names(d, M, K):
+    return [
         ("head.E", (3 * d, d), "mat"),
         ("head.w.w", (M, d), "mat"), ("head.w.b", (M,), "bias"),
         ("head.mu.w", (M, d), "mat"), ("head.mu.b", (M,), "bias"),
@@ -136,7 +154,6 @@ def weight_names(cfg: ModelCfg) -> List[Tuple[str, Tuple[int, ...], str]]:
         ("head.k1.w", (d, d), "mat"), ("head.k1.b", (d,), "bias"),
         ("head.k2.w", (K, d), "mat"), ("head.k2.b", (K,), "bias"),
     ]
-    return out
 
 
 def to_bf16_values(a: np.ndarray) -> np.ndarray:

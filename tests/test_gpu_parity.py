@@ -36,6 +36,11 @@ VERIFY_CASES = [
     small("c4", 2, n_hist=70, init="paper", mismatch=False),
     small("c5", 9, init="bias"),
     small("c5", 5),
+    # long histories over few (sequence, head) pairs: the key range is split
+    # across workgroups and the partials merged
+    small("c1", 2, n_hist=1100),
+    small("c2", 2, n_hist=1100),
+    small("c3", 1, n_hist=1100, init="bias"),
 ]
 
 # bf16 with the large-activation "stress" weights: a float32-accumulating
