@@ -72,8 +72,10 @@ def verify_pass_fraction(wl, gamma, B, verify_ms):
     P = gamma + 1
     T = B * P
     ctx = wl.n_hist + wl.n_gen / 2.0
-    flop = 2.0 * T * (L * (4 * d * d + 2 * d * F) + 4 * d * d + 3 * M * d + K * d) + 4.0 * T * L * d * ctx
-    w_bytes = elt * (L * (4 * d * d + 2 * d * F) + 4 * d * d + 3 * M * d + K * d)
+    # per layer: THP QKV, output and FFN matrices; AttNHP one 3d x 2d matrix over [z; h]
+    layer = 6 * d * d if getattr(c, "encoder", "thp") == "attnhp" else 4 * d * d + 2 * d * F
+    flop = 2.0 * T * (L * layer + 4 * d * d + 3 * M * d + K * d) + 4.0 * T * L * d * ctx
+    w_bytes = elt * (L * layer + 4 * d * d + 3 * M * d + K * d)
     bytes_ = B * L * (ctx + P) * 2 * d * elt + w_bytes + T * 8 * (3 * M + K)
     t_bound = max(flop / (MFMA_PEAK_TFLOPS[c.prec] * 1e12), bytes_ / (HBM_PEAK_GBS * 1e9))
     return {"flop": flop, "bytes": bytes_, "t_bound_us": t_bound * 1e6, "t_measured_us": verify_ms * 1e3,

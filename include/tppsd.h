@@ -75,11 +75,24 @@ extern "C" {
 #define TPPSD_MAX_MIX    64   /* mixture components M                            */
 #define TPPSD_MAX_TYPES  64   /* event types K                                   */
 
+/* ---- encoders ---------------------------------------------------------------- */
+#define TPPSD_ENC_THP    0    /* the model described above                      */
+#define TPPSD_ENC_ATTNHP 1    /* AttNHP encoder (App. D.4): h^(0) = W_type[k_i];
+                                 per layer q, k, v = W [z(t_i); h_i] + b (W is
+                                 3D x 2D, the bias the constant 1 of [1; z; h])
+                                 and h_i += tanh(sum_{j<=i} f_ij v_j / (1 + sum_{j<=i} f_ij)),
+                                 f_ij = exp(q_i . k_j / sqrt(d_head)) per head; no
+                                 LayerNorm, FFN or output projection; the decoder
+                                 reads h^(L). z_j(t) = sin / cos(t / (m (5M/m)^((j - j mod 2)/D))). */
+
 /* Model configuration. d_model % n_heads == 0; d_head = d_model / n_heads must
- * be 16, 32 or 64; bf16 models need
-  * d_model and d_ffn to be multiples of 32 (16 for fp32 models). */
+ * be 16, 32 or 64; bf16 models need d_model and d_ffn to be multiples of 32
+ * (16 for fp32 models). AttNHP models ignore d_ffn and need
+ * 0 < time_m <= time_M (the encoding's wavelength scales m, M). */
 typedef struct {
   int32_t n_layers, d_model, n_heads, d_ffn, n_mix, n_types, prec;
+  int32_t encoder;          /* TPPSD_ENC_* */
+  float time_m, time_M;     /* AttNHP time scales; unused by THP models */
 } tppsd_model_cfg;
 
 typedef struct tppsd_model tppsd_model;   /* opaque host handle, read-only after create */

@@ -68,7 +68,8 @@ struct Entry {
 
 // Entries are 256-byte aligned, except that a few groups are packed back to
 // back so that the kernels can read them as one matrix: [E; V_k1] (4d x d),
-// [V_w; V_mu; V_sigma] (3M x d) and their biases (3M).
+// [V_w; V_mu; V_sigma] (3M x d) and their biases (3M). AttNHP models have per
+// layer only qkv.w (3d x 2d, over [z; h]) and qkv.b, and no final LayerNorm.
 std::vector<Entry> layout(const tppsd_model_cfg &c) {
   std::vector<Entry> v;
   const int bf = c.prec == TPPSD_PREC_BF16;
@@ -80,8 +81,14 @@ std::vector<Entry> layout(const tppsd_model_cfg &c) {
     off += (size_t)r * cl * (mat ? me : 4);
   };
   const int d = c.d_model, F = c.d_ffn, M = c.n_mix, K = c.n_types;
+  const bool attnhp = c.encoder == TPPSD_ENC_ATTNHP;
   add("type_emb", K, d, true, true);
-  for (int l = 0; l < c.n_layers; ++l) {
+  for (int l = 0; l < c.n_layers && attnhp; ++l) {   // AttNHP: W [3d x 2d] over [z; h] and its bias
+    const std::string p = "layers." + std::to_string(l) + ".";
+    add(p + "qkv.w", 3 * d, 2 * d, true, true);
+    add(p + "qkv.b", 3 * d, 1, false, true);
+  }
+  for (int l = 0; l < c.n_layers && !attnhp; ++l) {
     const std::string p = "layers." + std::to_string(l) + ".";
     add(p + "ln1.g", d, 1, false, true);
     add(p + "ln1.b", d, 1, false, true);
@@ -96,8 +103,10 @@ std::vector<Entry> layout(const tppsd_model_cfg &c) {
     add(p + "ffn2.w", d, F, true, true);
     add(p + "ffn2.b", d, 1, false, true);
   }
-  add("lnf.g", d, 1, false, true);
-  add("lnf.b", d, 1, false, true);
+  if (!attnhp) {
+    add("lnf.g", d, 1, false, true);
+    add("lnf.b", d, 1, false, true);
+  }
   add("head.E", 3 * d, d, true, true);
   add("head.k1.w", d, d, true, false);
   add("head.k1.b", d, 1, false, true);
@@ -115,7 +124,13 @@ std::vector<Entry> layout(const tppsd_model_cfg &c) {
 
 int check_cfg(const tppsd_model_cfg *c) {
   if (!c) return fail(TPPSD_E_ARG, "null model configuration");
-  if (c->n_layers < 1 || c->d_model < 16 || c->n_heads < 1 || c->d_ffn < 1 || c->n_mix < 1 || c->n_types < 1)
+  if (c->encoder != TPPSD_ENC_THP && c->encoder != TPPSD_ENC_ATTNHP)
+    return fail(TPPSD_E_CONFIG, "unknown encoder %d", c->encoder);
+  const bool attnhp = c->encoder == TPPSD_ENC_ATTNHP;
+  if (attnhp && !(c->time_m > 0.f && c->time_M >= c->time_m))
+    return fail(TPPSD_E_CONFIG, "AttNHP needs 0 < time_m <= time_M");
+  if (c->n_layers < 1 || c->d_model < 16 || c->n_heads < 1 || (!attnhp && c->d_ffn < 1) || c->n_mix < 1 ||
+      c->n_types < 1)
     return fail(TPPSD_E_CONFIG, "model sizes must be positive (d_model >= 16)");
   if (c->prec != TPPSD_PREC_FP32 && c->prec != TPPSD_PREC_BF16)
     return fail(TPPSD_E_CONFIG, "unsupported precision %d", c->prec);
@@ -123,9 +138,9 @@ int check_cfg(const tppsd_model_cfg *c) {
   const int dh = c->d_model / c->n_heads;
   if (dh != 16 && dh != 32 && dh != 64) return fail(TPPSD_E_CONFIG, "d_head %d not in {16, 32, 64}", dh);
   if (c->d_model % 16) return fail(TPPSD_E_CONFIG, "d_model must be a multiple of 16");
-  if (c->prec == TPPSD_PREC_BF16 && (c->d_model % 32 || c->d_ffn % 32))
+  if (c->prec == TPPSD_PREC_BF16 && (c->d_model % 32 || (!attnhp && c->d_ffn % 32)))
     return fail(TPPSD_E_CONFIG, "bf16 models need d_model and d_ffn multiples of 32");
-  if (c->d_ffn % 16) return fail(TPPSD_E_CONFIG, "d_ffn must be a multiple of 16");
+  if (!attnhp && c->d_ffn % 16) return fail(TPPSD_E_CONFIG, "d_ffn must be a multiple of 16");
   if (c->n_mix > TPPSD_MAX_MIX) return fail(TPPSD_E_CONFIG, "n_mix > %d", TPPSD_MAX_MIX);
   if (c->n_types > TPPSD_MAX_TYPES) return fail(TPPSD_E_CONFIG, "n_types > %d", TPPSD_MAX_TYPES);
   return TPPSD_OK;
@@ -146,6 +161,7 @@ struct tppsd_model {
   const void *type_emb, *Ek1_w, *mix_w, *k2_w;
   const float *lnf_g, *lnf_b, *k1_b, *mix_b, *k2_b;
   int bf16() const { return cfg.prec == TPPSD_PREC_BF16; }
+  bool attnhp() const { return cfg.encoder == TPPSD_ENC_ATTNHP; }
   int d() const { return cfg.d_model; }
   int H() const { return cfg.n_heads; }
   int dh() const { return cfg.d_model / cfg.n_heads; }
@@ -183,7 +199,7 @@ struct tppsd_state {
   ModelCache cT, cD;
   // activation scratch
   float *x = nullptr;
-  void *a = nullptr, *q = nullptr, *o = nullptr, *hid = nullptr, *e = nullptr;
+  void *a = nullptr, *q = nullptr, *o = nullptr, *hid = nullptr, *e = nullptr, *u = nullptr;
   float *logits = nullptr;
   bool heads_built = false;
   float *ar_mix = nullptr, *ar_logtype = nullptr;
@@ -235,7 +251,7 @@ struct WsLayout {
   size_t total = 0;
   size_t status, n_done, acc, n, gen, lenT, lenD, done, rnd, zeros, ev_t, ev_k, t_end, ll;
   size_t freqT, freqD, kT, vT, kD, vD, layerT, layerD;
-  size_t x, a, q, o, hid, e, ar_mix, ar_lt, attn_part, gen0;
+  size_t x, a, q, o, hid, e, u, ar_mix, ar_lt, attn_part, gen0;
   size_t logits, hwT, hbT, hwD, hbD;
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt, d_rate;
   size_t v_logg, v_logf, v_mix, v_lt;
@@ -287,6 +303,7 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   w.o = take(Tm * dmax * 4);
   w.hid = take(Tm * fmax * 4);
   w.e = take(Tm * 4 * dmax * 4);
+  w.u = take(Tm * 2 * dmax * 4);   // AttNHP layer input [z; h]
   w.logits = take(Tm * head_ldl((int)mmax, (int)kmax) * 4);
   w.hwT = take((size_t)(3 * T->cfg.n_mix + T->cfg.n_types) * 4 * T->d() * T->act_bytes());
   w.hbT = take((size_t)(3 * T->cfg.n_mix + T->cfg.n_types) * 4);
@@ -339,8 +356,36 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
   auto ev = [&](int pair, int end) -> hipEvent_t { return timed ? s->cur_ev[2 * pair + end] : nullptr; };
   // LayerNorms run inside the GEMMs that consume them where the width allows
   const bool fuse_ln = gemm_ln_fusable(bf, d);
-  launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
-  for (int l = 0; l < m->cfg.n_layers; ++l) {
+  if (m->attnhp()) {
+    // AttNHP (App. D.4): per layer one GEMM over u = [z; h] for q, k, v (keys
+    // and values into the cache), attention normalised by 1 + sum f, then
+    // h += tanh(o) (refreshing u's h half and the decoder operand a = h)
+    launch_embed_attnhp(s->x, s->u, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
+    for (int l = 0; l < L; ++l) {
+      const LayerW &w = m->layers[l];
+      char *kc = c.k + c.layer_bytes * l, *vc = c.v + c.layer_bytes * l;
+      Epi e{};
+      e.mode = EPI_QKV;
+      e.bias = w.qkv_b;
+      e.q = s->q;
+      e.kc = kc;
+      e.vc = vc;
+      e.start = start;
+      e.start_off = start_off;
+      e.P = P;
+      e.H = H;
+      e.dh = dh;
+      e.d = d;
+      e.cap = s->kv_cap;
+      e.status = s->status;
+      launch_gemm(s->u, nullptr, w.qkv_w, bf, T, 3 * d, 2 * d, e, st, ev(L + 4 * l, 0), ev(L + 4 * l, 1));
+      launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->kv_cap, s->attn_part,
+                       1, verify ? 1 : 0, ev(l, 0), ev(l, 1), st);
+      launch_attnhp_update(s->x, s->o, s->u, s->a, bf, T, d, st);
+    }
+  }
+  if (!m->attnhp()) launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
+  for (int l = 0; l < m->cfg.n_layers && !m->attnhp(); ++l) {
     const LayerW &w = m->layers[l];
     char *kc = c.k + c.layer_bytes * l, *vc = c.v + c.layer_bytes * l;
     const LnA ln1{s->x, w.ln1_g, w.ln1_b}, ln2{s->x, w.ln2_g, w.ln2_b};
@@ -361,7 +406,7 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     e.status = s->status;
     launch_gemm(s->a, fuse_ln ? &ln1 : nullptr, w.qkv_w, bf, T, 3 * d, d, e, st, ev(L + 4 * l, 0), ev(L + 4 * l, 1));
     launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->kv_cap, s->attn_part,
-                     verify ? 1 : 0, ev(l, 0), ev(l, 1), st);
+                     0, verify ? 1 : 0, ev(l, 0), ev(l, 1), st);
     Epi eo{};
     eo.mode = EPI_RESID;
     eo.bias = w.out_b;
@@ -383,15 +428,17 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     launch_gemm(s->hid, nullptr, w.ffn2_w, bf, T, d, F, e2, st, ev(L + 4 * l + 3, 0), ev(L + 4 * l + 3, 1));
   }
   if (head) {
+    // THP: the decoder reads LN_f(x); AttNHP: h itself (a, written by the update)
     const LnA lnf{s->x, m->lnf_g, m->lnf_b};
-    if (!fuse_ln) launch_layernorm(s->x, s->a, bf, m->lnf_g, m->lnf_b, T, d, st);
+    const bool ln_in_gemm = fuse_ln && !m->attnhp();
+    if (!fuse_ln && !m->attnhp()) launch_layernorm(s->x, s->a, bf, m->lnf_g, m->lnf_b, T, d, st);
     Epi eh{};
     eh.mode = EPI_HEAD;
     eh.bias = m->k1_b;
     eh.out = s->e;
     eh.ldo = 4 * d;
     eh.split = 3 * d;
-    launch_gemm(s->a, fuse_ln ? &lnf : nullptr, m->Ek1_w, bf, T, 4 * d, d, eh, st, ev(5 * L, 0), ev(5 * L, 1));
+    launch_gemm(s->a, ln_in_gemm ? &lnf : nullptr, m->Ek1_w, bf, T, 4 * d, d, eh, st, ev(5 * L, 0), ev(5 * L, 1));
     const int M = m->cfg.n_mix, K = m->cfg.n_types, ldl = head_ldl(M, K);
     Epi el{};
     el.mode = EPI_F32;
@@ -785,6 +832,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->o = ws + w.o;
   s->hid = ws + w.hid;
   s->e = ws + w.e;
+  s->u = ws + w.u;
   s->logits = (float *)(ws + w.logits);
   s->cT.head_w = ws + w.hwT;
   s->cT.head_b = (float *)(ws + w.hbT);
@@ -804,11 +852,20 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->iac = {(int32_t *)(ws + w.a_L),      (int32_t *)(ws + w.a_nnew), (int32_t *)(ws + w.a_knew),
             (float *)(ws + w.a_tnew),     (float *)(ws + w.a_taunew), (int32_t *)(ws + w.a_ar),
             (uint8_t *)(ws + w.a_flags)};
-  // frequency tables of the temporal encoding: 10000^(-(j - j mod 2) / d), float32
+  // frequency tables of the temporal encoding, float32: THP 10000^(-(j - j mod 2) / d),
+  // AttNHP 1 / (m (5M/m)^((j - j mod 2) / d))
   for (int which = 0; which < (D ? 2 : 1); ++which) {
     const tppsd_model *m = which ? D : T;
     std::vector<float> f(m->d());
-    for (int j = 0; j < m->d(); ++j) f[j] = (float)pow(10000.0, -(double)(j - j % 2) / (double)m->d());
+    for (int j = 0; j < m->d(); ++j) {
+      const double e = (double)(j - j % 2) / (double)m->d();
+      if (m->attnhp()) {
+        const double tm = m->cfg.time_m, tM = m->cfg.time_M;
+        f[j] = (float)(1.0 / (tm * pow(5.0 * tM / tm, e)));
+      } else {
+        f[j] = (float)pow(10000.0, -e);
+      }
+    }
     float *dst = which ? s->cD.freq : s->cT.freq;
     if (hipMemcpy(dst, f.data(), f.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
       delete s;
@@ -827,7 +884,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
     // and the layered kernels amortise weights and latency over many rows
     // (and while contexts stay short: its attention streams each (sequence,
     // head)'s keys with one wave)
-    s->fused_draft = D && B <= 1024 && max_events <= 2048 &&
+    s->fused_draft = D && !D->attnhp() && B <= 1024 && max_events <= 2048 &&
                      fused_draft_ok(D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn) &&
                      fused_draft_lds_bytes(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
                                            D->H()) <= 64 * 1024 &&
@@ -1062,8 +1119,14 @@ void read_round_events(tppsd_state *s, int w) {
   const int L = s->T->cfg.n_layers;
   if (s->timing & TPPSD_TIME_KERNELS) {
     for (size_t i = 0; i + 1 < s->gev[w].size(); i += 2) {
+      // AttNHP layers have one GEMM (pair L + 4 l): the other pairs were never recorded
+      const int pair = (int)(i / 2);
+      if (s->T->attnhp() && pair >= L && pair < 5 * L && (pair - L) % 4) continue;
       float ms = 0.f;
-      if (hipEventElapsedTime(&ms, s->gev[w][i], s->gev[w][i + 1]) != hipSuccess) continue;
+      if (hipEventElapsedTime(&ms, s->gev[w][i], s->gev[w][i + 1]) != hipSuccess) {
+        (void)hipGetLastError();   // a failed query must not reach the next launch check
+        continue;
+      }
       if ((int)(i / 2) < L) {
         s->tm.attn_ms += ms;
         s->tm.attn_launches += 1;
@@ -1077,7 +1140,10 @@ void read_round_events(tppsd_state *s, int w) {
   if (s->timing & TPPSD_TIME_PHASES) {
     float ms[3] = {0.f, 0.f, 0.f};
     for (int j = 0; j < 3; ++j)
-      if (hipEventElapsedTime(&ms[j], s->pev[w][j], s->pev[w][j + 1]) != hipSuccess) ms[j] = 0.f;
+      if (hipEventElapsedTime(&ms[j], s->pev[w][j], s->pev[w][j + 1]) != hipSuccess) {
+        ms[j] = 0.f;
+        (void)hipGetLastError();
+      }
     s->tm.draft_ms += ms[0];
     s->tm.verify_ms += ms[1];
     s->tm.accept_ms += ms[2];
@@ -1142,7 +1208,8 @@ int sd_loop(tppsd_state *s, int gamma, const float *params, int max_rounds, int 
     const tppsd_model *m = s->T;
     const int L = m->cfg.n_layers;
     const double d = m->d(), F = m->cfg.d_ffn, rows = (double)s->B * (gamma + 1);
-    s->round_flop = 2.0 * rows * (L * (3 * d * d + d * d + 2 * d * F) + 4 * d * d);
+    s->round_flop = m->attnhp() ? 2.0 * rows * (L * (3 * d * 2 * d) + 4 * d * d)
+                                : 2.0 * rows * (L * (3 * d * d + d * d + 2 * d * F) + 4 * d * d);
     if (int rc = make_events(s->gev, 2 * (5 * L + 1))) return rc;
   }
   if (phases)

@@ -26,8 +26,9 @@ inline size_t attn_part_floats(int B, int H, int dh, int qtiles_max, int max_key
   const int s = attn_splits(B, H, max_keys);
   return s > 1 ? (size_t)B * H * qtiles_max * 16 * s * (dh + 2) : 0;
 }
+// sink: AttNHP normalisation 1 + sum f (an extra key of score 0, value 0)
 void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16,
                       const int32_t *start, int start_off, const int32_t *done, int B, int P, int H,
-                      int dh, int cap, float *part, int verify, hipEvent_t ev0, hipEvent_t ev1,
+                      int dh, int cap, float *part, int sink, int verify, hipEvent_t ev0, hipEvent_t ev1,
                       hipStream_t st);
 }  // namespace tppsd

@@ -20,12 +20,21 @@ namespace tppsd {
 
 // ROLE tags the instantiation only (1 = verify pass of the target, 0 = other
 // passes), so that profiles report the verify launches under their own name.
+// AttNHP attention (App. D.4) divides by 1 + sum f instead of sum f: the same
+// as one more key of score 0 and value 0. Applied once, where the softmax
+// state (max M, sum L, unnormalised output O) of all keys is complete.
+__device__ __forceinline__ void sink_adjust(float &M, float &L, float &O) {
+  const float ms = fmaxf(M, 0.f), f = (M == -INFINITY) ? 0.f : expf(M - ms);
+  L = L * f + expf(-ms);
+  O *= f;
+}
+
 template <typename ACT, int DH, int ROLE>
 __global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q, const ACT *__restrict__ kc,
                                                       const ACT *__restrict__ vc, ACT *__restrict__ o,
                                                       const int32_t *__restrict__ start, int start_off,
                                                       const int32_t *__restrict__ done, int P, int H,
-                                                      int cap) {
+                                                      int cap, int sink) {
   constexpr int QT = 16, KT = 64, EPT = (DH + 15) / 16;
   __shared__ float qs[QT][DH];
   __shared__ float ks[KT][DH + 1];
@@ -108,6 +117,12 @@ __global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q,
       }
     }
   }
+  if (sink) {   // the AttNHP denominator 1 + sum f: a key of score 0 and value 0
+    const float ms = fmaxf(m_run, 0.f), f = (m_run == -INFINITY) ? 0.f : expf(m_run - ms);
+    l_run = l_run * f + expf(-ms);
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) acc[i] *= f;
+  }
   if (qi < nq) {
     const float inv = 1.f / l_run;
 #pragma unroll
@@ -138,7 +153,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
                                                    const bf16_t *__restrict__ vc, bf16_t *__restrict__ o,
                                                    const int32_t *__restrict__ start, int start_off,
                                                    const int32_t *__restrict__ done, int P, int H, int cap,
-                                                   int splits, float *__restrict__ part) {
+                                                   int splits, float *__restrict__ part, int sink) {
   constexpr int KT = 32, NDT = DH / 16, NC = DH >= 32 ? DH / 32 : 1, NQ = 16 * QT;
   __shared__ float red_m[4][NQ], red_l[4][NQ];
   __shared__ float red_o[4][DH][NQ + 1];
@@ -296,6 +311,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
       O += red_o[w][j][qq] * f;
     }
     if (splits == 1) {
+      if (sink) sink_adjust(M, L, O);
       o[(size_t)(b * P + qq) * d + h * DH + j] = f2bf(L > 0.f ? O / L : 0.f);
     } else {
       float *pp = part + (((size_t)bh * QT * 16 + qq) * splits + split) * (DH + 2);
@@ -320,7 +336,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__
                                                        const float *__restrict__ vc, float *__restrict__ o,
                                                        const int32_t *__restrict__ start, int start_off,
                                                        const int32_t *__restrict__ done, int P, int H, int cap,
-                                                       int splits, float *__restrict__ part) {
+                                                       int splits, float *__restrict__ part, int sink) {
   constexpr int KT = 32, NDT = DH / 16, NQ = 16 * QT;
   __shared__ float red_m[4][NQ], red_l[4][NQ];
   __shared__ float red_o[4][DH][NQ + 1];
@@ -470,6 +486,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__
       O += red_o[w][j][qq] * f;
     }
     if (splits == 1) {
+      if (sink) sink_adjust(M, L, O);
       o[(size_t)(b * P + qq) * d + h * DH + j] = L > 0.f ? O / L : 0.f;
     } else {
       float *pp = part + (((size_t)bh * QT * 16 + qq) * splits + split) * (DH + 2);
@@ -485,7 +502,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__
 // merge of the split partials: one thread per output element
 template <typename ACT, int DH>
 __global__ void k_attn_combine(const float *__restrict__ part, ACT *__restrict__ o, int total, int P, int H,
-                               int qtiles, int splits) {
+                               int qtiles, int splits, int sink) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;   // over B * H * P * DH
   if (idx >= total) return;
   const int j = idx % DH;
@@ -502,6 +519,7 @@ __global__ void k_attn_combine(const float *__restrict__ part, ACT *__restrict__
     L += pp[s * (DH + 2) + 1] * f;
     O += pp[s * (DH + 2) + 2 + j] * f;
   }
+  if (sink) sink_adjust(M, L, O);
   st(o, (size_t)(b * P + p) * (H * DH) + h * DH + j, L > 0.f ? O / L : 0.f);
 }
 
@@ -509,13 +527,14 @@ __global__ void k_attn_combine(const float *__restrict__ part, ACT *__restrict__
 // stop (hipExtLaunchKernelGGL), for the verify-attention timing
 template <typename ACT, int ROLE>
 static void attn_dispatch(const void *q, const void *kc, const void *vc, void *o, const int32_t *start,
-                          int start_off, const int32_t *done, int B, int P, int H, int dh, int cap,
+                          int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, int sink,
                           hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   dim3 grid(B * H, (P + 15) / 16);
   const ACT *Q = (const ACT *)q, *Kc = (const ACT *)kc, *Vc = (const ACT *)vc;
   ACT *O = (ACT *)o;
   auto go = [&](auto kern) {
-    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap);
+    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap,
+                          sink);
   };
   switch (dh) {
     case 16: go(k_attn_generic<ACT, 16, ROLE>); break;
@@ -529,14 +548,14 @@ static void attn_dispatch(const void *q, const void *kc, const void *vc, void *o
 // (sequence, head) pairs alone do not fill the chip.
 template <typename ACT, int DH, int ROLE>
 static void attn_mfma(const ACT *Q, const ACT *Kc, const ACT *Vc, ACT *O, const int32_t *start, int start_off,
-                      const int32_t *done, int B, int P, int H, int cap, float *part, hipEvent_t ev0,
+                      const int32_t *done, int B, int P, int H, int cap, float *part, int sink, hipEvent_t ev0,
                       hipEvent_t ev1, hipStream_t s) {
   const int qtiles = (P + 15) / 16;
   const int splits = attn_splits(B, H, cap);
   dim3 grid(B * H, 1, splits);
   auto go = [&](auto kern) {
     hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap,
-                          splits, part);
+                          splits, part, sink);
   };
   if constexpr (sizeof(ACT) == 2) {
     if (qtiles == 1) go(k_attn_mfma<DH, ROLE, 1>);
@@ -549,52 +568,52 @@ static void attn_mfma(const ACT *Q, const ACT *Kc, const ACT *Vc, ACT *O, const 
   }
   if (splits > 1) {
     const int total = B * H * P * DH;
-    k_attn_combine<ACT, DH><<<(total + 255) / 256, 256, 0, s>>>(part, O, total, P, H, qtiles, splits);
+    k_attn_combine<ACT, DH><<<(total + 255) / 256, 256, 0, s>>>(part, O, total, P, H, qtiles, splits, sink);
   }
 }
 
 template <int ROLE>
 static void attention_role(const void *q, const void *kc, const void *vc, void *o, int bf16, const int32_t *start,
                            int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, float *part,
-                           hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+                           int sink, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   static const bool force_generic = [] {
     const char *e = getenv("TPPSD_ATTN_GENERIC");
     return e && e[0] == '1';
   }();
   if (!bf16) {
     if (force_generic) {
-      attn_dispatch<float, ROLE>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, ev0, ev1, s);
+      attn_dispatch<float, ROLE>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, sink, ev0, ev1, s);
       return;
     }
     const float *Q = (const float *)q, *Kc = (const float *)kc, *Vc = (const float *)vc;
     float *O = (float *)o;
     switch (dh) {
-      case 16: attn_mfma<float, 16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
-      case 32: attn_mfma<float, 32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
-      default: attn_mfma<float, 64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+      case 16: attn_mfma<float, 16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, sink, ev0, ev1, s); break;
+      case 32: attn_mfma<float, 32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, sink, ev0, ev1, s); break;
+      default: attn_mfma<float, 64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, sink, ev0, ev1, s); break;
     }
     return;
   }
   if (force_generic) {
-    attn_dispatch<bf16_t, ROLE>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, ev0, ev1, s);
+    attn_dispatch<bf16_t, ROLE>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, sink, ev0, ev1, s);
     return;
   }
   const bf16_t *Q = (const bf16_t *)q, *Kc = (const bf16_t *)kc, *Vc = (const bf16_t *)vc;
   bf16_t *O = (bf16_t *)o;
   switch (dh) {
-    case 16: attn_mfma<bf16_t, 16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
-    case 32: attn_mfma<bf16_t, 32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
-    default: attn_mfma<bf16_t, 64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, ev0, ev1, s); break;
+    case 16: attn_mfma<bf16_t, 16, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, sink, ev0, ev1, s); break;
+    case 32: attn_mfma<bf16_t, 32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, sink, ev0, ev1, s); break;
+    default: attn_mfma<bf16_t, 64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, sink, ev0, ev1, s); break;
   }
 }
 
 void launch_attention(const void *q, const void *kc, const void *vc, void *o, int bf16, const int32_t *start,
                       int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, float *part,
-                      int verify, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
+                      int sink, int verify, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
   if (verify)
-    attention_role<1>(q, kc, vc, o, bf16, start, start_off, done, B, P, H, dh, cap, part, ev0, ev1, s);
+    attention_role<1>(q, kc, vc, o, bf16, start, start_off, done, B, P, H, dh, cap, part, sink, ev0, ev1, s);
   else
-    attention_role<0>(q, kc, vc, o, bf16, start, start_off, done, B, P, H, dh, cap, part, ev0, ev1, s);
+    attention_role<0>(q, kc, vc, o, bf16, start, start_off, done, B, P, H, dh, cap, part, sink, ev0, ev1, s);
 }
 
 }  // namespace tppsd

@@ -170,6 +170,11 @@ void launch_embed(float *x, int T, int d, int P, const TokSrc &src, const void *
                   const float *freq, int K, hipStream_t st);
 void launch_layernorm(const float *x, void *y, int bf16, const float *g, const float *b, int T, int d,
                       hipStream_t st);
+// AttNHP: h^(0) = W_type[k] into x (fp32) and u = [z(t); h] (activation type, [T, 2d])
+void launch_embed_attnhp(float *x, void *u, int T, int d, int P, const TokSrc &src, const void *wtype, int bf16,
+                         const float *freq, int K, hipStream_t st);
+// AttNHP: x += tanh(o) (o [T, d], activation type); u[:, d:] = a = x in the activation type
+void launch_attnhp_update(float *x, const void *o, void *u, void *a, int bf16, int T, int d, hipStream_t st);
 // A operand given as LayerNorm(x) of the fp32 stream x [T, K] with gain g and bias b
 struct LnA {
   const float *x, *g, *b;

@@ -9,6 +9,7 @@
 // Linear inputs in bf16 (LN outputs, q/k/v, attention output, ReLU output, the
 // decoder's e and tanh activations), accumulate in fp32 and keep the residual
 // stream, LayerNorm statistics, softmax and all decoder math in fp32.
+#include <algorithm>
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -132,6 +133,51 @@ __global__ void k_embed(float *__restrict__ x, int d, int P, TokSrc src, const W
     const float arg = t * freq[j];
     const float z = (j & 1) ? cosf(arg) : sinf(arg);
     x[(size_t)tok * d + j] = z + ld(wtype, (size_t)k * d + j);
+  }
+}
+
+// AttNHP encoder pieces (App. D.4). The event's first-layer state is its
+// type row; the time enters every layer through the layer input
+// u = [z(t); h] (activation type, row stride 2d), z with the AttNHP
+// wavelengths (the frequency table holds 1 / (m (5M/m)^((j - j mod 2)/d))).
+template <typename W>
+__global__ void k_embed_attnhp(float *__restrict__ x, W *__restrict__ u, int d, int P, TokSrc src,
+                               const W *__restrict__ wtype, const float *__restrict__ freq, int K) {
+  const int tok = blockIdx.x;
+  const int b = tok / P, p = tok % P;
+  float t;
+  int k;
+  if (p < src.n_ev) {
+    const size_t i = (size_t)b * src.ev_stride + src.start[b] + src.start_off + p;
+    t = src.ev_t[i];
+    k = src.ev_k[i];
+  } else {
+    const size_t i = (size_t)b * src.dr_stride + src.dr_off + (p - src.n_ev);
+    t = src.dr_t[i];
+    k = src.dr_k[i];
+  }
+  k = min(max(k, 0), K - 1);
+  for (int j = threadIdx.x; j < d; j += blockDim.x) {
+    const float arg = t * freq[j];
+    const float h = ld(wtype, (size_t)k * d + j);
+    x[(size_t)tok * d + j] = h;
+    st(u, (size_t)tok * 2 * d + j, (j & 1) ? cosf(arg) : sinf(arg));
+    st(u, (size_t)tok * 2 * d + d + j, h);
+  }
+}
+
+// h += tanh(o) per element; the new h goes to the stream x, to u's h half and
+// to a (the next decoder's operand)
+template <typename ACT>
+__global__ void k_attnhp_update(float *__restrict__ x, const ACT *__restrict__ o, ACT *__restrict__ u,
+                                ACT *__restrict__ a, int T, int d) {
+  const size_t n = (size_t)T * d;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t r = i / d, j = i - r * d;
+    const float v = x[i] + tanhf(ld(o, i));
+    x[i] = v;
+    st(u, r * 2 * d + d + j, v);
+    st(a, i, v);
   }
 }
 
@@ -1894,6 +1940,24 @@ void launch_embed(float *x, int T, int d, int P, const TokSrc &src, const void *
     k_embed<bf16_t><<<T, threads, 0, s>>>(x, d, P, src, (const bf16_t *)wtype, freq, K);
   else
     k_embed<float><<<T, threads, 0, s>>>(x, d, P, src, (const float *)wtype, freq, K);
+}
+
+void launch_embed_attnhp(float *x, void *u, int T, int d, int P, const TokSrc &src, const void *wtype, int bf16,
+                         const float *freq, int K, hipStream_t s) {
+  const int threads = d >= 256 ? 256 : (d >= 128 ? 128 : 64);
+  if (bf16)
+    k_embed_attnhp<bf16_t><<<T, threads, 0, s>>>(x, (bf16_t *)u, d, P, src, (const bf16_t *)wtype, freq, K);
+  else
+    k_embed_attnhp<float><<<T, threads, 0, s>>>(x, (float *)u, d, P, src, (const float *)wtype, freq, K);
+}
+
+void launch_attnhp_update(float *x, const void *o, void *u, void *a, int bf16, int T, int d, hipStream_t s) {
+  const size_t n = (size_t)T * d;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 4096);
+  if (bf16)
+    k_attnhp_update<bf16_t><<<blocks, 256, 0, s>>>(x, (const bf16_t *)o, (bf16_t *)u, (bf16_t *)a, T, d);
+  else
+    k_attnhp_update<float><<<blocks, 256, 0, s>>>(x, (const float *)o, (float *)u, (float *)a, T, d);
 }
 
 void launch_layernorm(const float *x, void *y, int bf16, const float *g, const float *b, int T, int d,

@@ -52,8 +52,12 @@ class TimingC(ctypes.Structure):
                 ("verify_ms", c_double), ("accept_ms", c_double), ("rounds", c_int64)]
 
 
+ENCODER = {"thp": 0, "attnhp": 1}   # TPPSD_ENC_*
+
+
 class ModelCfgC(ctypes.Structure):
-    _fields_ = [(n, c_int32) for n in ("n_layers", "d_model", "n_heads", "d_ffn", "n_mix", "n_types", "prec")]
+    _fields_ = [(n, c_int32) for n in ("n_layers", "d_model", "n_heads", "d_ffn", "n_mix", "n_types", "prec",
+                                       "encoder")] + [("time_m", ctypes.c_float), ("time_M", ctypes.c_float)]
 
 
 class DraftBufC(ctypes.Structure):
@@ -129,7 +133,9 @@ def _stream():
 
 
 def cfg_c(cfg) -> ModelCfgC:
-    return ModelCfgC(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_ffn, cfg.n_mix, cfg.n_types, PREC[cfg.prec])
+    return ModelCfgC(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.d_ffn, cfg.n_mix, cfg.n_types, PREC[cfg.prec],
+                     ENCODER[getattr(cfg, "encoder", "thp")], float(getattr(cfg, "time_m", 1.0)),
+                     float(getattr(cfg, "time_M", 100.0)))
 
 
 # ---------------------------------------------------------------------------

@@ -77,8 +77,8 @@ class Workload:
         return self.target.prec
 
 
-def _cfg(L, d, H, F, M, K, prec):
-    return ModelCfg(L, d, H, F, M, K, prec)
+def _cfg(L, d, H, F, M, K, prec, enc=ENC_THP, tm=1.0, tM=100.0):
+    return ModelCfg(L, d, H, F, M, K, prec, enc, tm, tM)
 
 
 # Draft FFN width keeps the target's F/d ratio; draft M equals the target's.
@@ -103,6 +103,12 @@ WORKLOADS: Dict[str, Workload] = {
         "c5", 4, _cfg(6, 128, 4, 512, 8, 3, PREC_BF16), _cfg(1, 32, 2, 128, 8, 3, PREC_BF16),
         batch=4096, n_gen=256, gammas=(8,), n_hist=32, history="ipp_sin",
         description="throughput bf16, B=4096 x 256 events, gamma=8"),
+    # c3's data and sizes with the AttNHP encoder (App. D.4) for target and draft
+    "a3": Workload(
+        "a3", 5, _cfg(6, 256, 8, 0, 16, 22, PREC_BF16, ENC_ATTNHP, 0.01, 100.0),
+        _cfg(2, 64, 4, 0, 16, 22, PREC_BF16, ENC_ATTNHP, 0.01, 100.0),
+        batch=256, n_gen=1024, gammas=(10,), n_hist=64, history="hawkes22",
+        description="c3 with the AttNHP encoder, bf16, B=256 x 1024 events, gamma=10"),
 }
 
 

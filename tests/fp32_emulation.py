@@ -22,6 +22,8 @@ class Model32(Model):
         self.rb = lambda x: N.round_bf16(np.asarray(x, np.float32).astype(np.float64)).astype(np.float32)
 
     def embed(self, t, k):
+        if self.attnhp:
+            return self.w["type_emb"][np.asarray(k)].astype(np.float32)
         return (self.time_encoding(t).astype(np.float32) + self.w["type_emb"][np.asarray(k)]).astype(np.float32)
 
     @staticmethod

@@ -64,6 +64,9 @@ def test_config_validation(lib):
         W.ModelCfg(2, 64, 4, 48, 4, 1, "bf16"),        # d_ffn not a multiple of 32
         W.ModelCfg(2, 64, 4, 64, 65, 1, "fp32"),       # too many components
         W.ModelCfg(0, 64, 4, 64, 4, 1, "fp32"),
+        W.ModelCfg(2, 64, 4, 0, 4, 1, "fp32"),                          # THP without an FFN
+        W.ModelCfg(2, 64, 4, 0, 4, 1, "fp32", W.ENC_ATTNHP, 0.0, 10.0),  # AttNHP time scale m = 0
+        W.ModelCfg(2, 64, 4, 0, 4, 1, "fp32", W.ENC_ATTNHP, 5.0, 1.0),   # m > M
     ]
     for cfg in bad:
         with pytest.raises(tp.TppsdError) as e:

@@ -33,7 +33,7 @@ pytestmark = pytest.mark.gpu
 SEED = 1234           # bench.py's sampler seed
 # workload -> (sampled sequences, fraction of n_gen generated before the checked round)
 CASES = {"c2": ([0, 17, 63], 0.5), "c3": ([0, 37, 101, 200, 255], 0.5), "c4": ([0, 31], 0.25),
-         "c5": ([0, 1234, 4095], 0.5)}
+         "c5": ([0, 1234, 4095], 0.5), "a3": ([0, 101, 255], 0.5)}
 
 
 def _gpu_run(wl, gamma, frac):
