@@ -203,6 +203,7 @@ struct tppsd_state {
   float *logits = nullptr;
   bool heads_built = false;
   float *ar_mix = nullptr, *ar_logtype = nullptr;
+  bool block_path = true;              // k_block for the models it serves (TPPSD_LAYERED=1: layered kernels)
   float *attn_part = nullptr;
   int32_t *gen0 = nullptr;
   // internal round buffers (tppsd_sample_sd)
@@ -223,6 +224,7 @@ struct tppsd_state {
   std::vector<hipEvent_t> gev[2];
   std::vector<hipEvent_t> pev[2];
   hipEvent_t *cur_ev = nullptr;      // kernel events of the round being launched
+  std::vector<char> ev_used;         // event pairs the verify pass records (per pair of cur_ev)
   tppsd_timing tm{};
   double round_flop = 0.0;           // verify GEMM flops of one round
   hipGraphExec_t phase_exec[3] = {nullptr, nullptr, nullptr};
@@ -353,7 +355,11 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
   const int B = s->B, d = m->d(), H = m->H(), dh = m->dh(), F = m->cfg.d_ffn, bf = m->bf16();
   const int T = B * P, L = m->cfg.n_layers;
   const bool timed = verify && s->cur_ev != nullptr;
-  auto ev = [&](int pair, int end) -> hipEvent_t { return timed ? s->cur_ev[2 * pair + end] : nullptr; };
+  auto ev = [&](int pair, int end) -> hipEvent_t {
+    if (!timed) return nullptr;
+    s->ev_used[pair] = 1;
+    return s->cur_ev[2 * pair + end];
+  };
   // LayerNorms run inside the GEMMs that consume them where the width allows
   const bool fuse_ln = gemm_ln_fusable(bf, d);
   if (m->attnhp()) {
@@ -383,6 +389,84 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
                        1, verify ? 1 : 0, ev(l, 0), ev(l, 1), st);
       launch_attnhp_update(s->x, s->o, s->u, s->a, bf, T, d, st);
     }
+  }
+  if (!m->attnhp() && s->block_path && block_fusable(bf, d, F, m->cfg.n_mix, m->cfg.n_types)) {
+    // small THP models: one k_block launch between consecutive attention
+    // launches (embedding + LN1 + QKV; then output projection + FFN + the next
+    // LN1 + QKV; the last one ends with LN_f and the decoder). Without a
+    // decoder the last layer's output projection and FFN feed nothing and
+    // are skipped.
+    const int M = m->cfg.n_mix, K = m->cfg.n_types;
+    BlockArgs ba{};
+    ba.T = T;
+    ba.P = P;
+    ba.d = d;
+    ba.F = F;
+    ba.src = src;
+    ba.type_emb = m->type_emb;
+    ba.freq = c.freq;
+    ba.n_types = K;
+    ba.x = s->x;
+    ba.o = s->o;
+    ba.lnf_g = m->lnf_g;
+    ba.lnf_b = m->lnf_b;
+    ba.k1_b = m->k1_b;
+    ba.Ek1_w = m->Ek1_w;
+    ba.head_w = c.head_w;
+    ba.head_b = c.head_b;
+    ba.M = M;
+    ba.K = K;
+    if (head) ba.h = *head;
+    auto set_qkv = [&](int l) {
+      const LayerW &w = m->layers[l];
+      ba.qkv_w = w.qkv_w;
+      ba.ln1_g = w.ln1_g;
+      ba.ln1_b = w.ln1_b;
+      Epi &e = ba.qe;
+      e = Epi{};
+      e.mode = EPI_QKV;
+      e.bias = w.qkv_b;
+      e.q = s->q;
+      e.kc = c.k + c.layer_bytes * l;
+      e.vc = c.v + c.layer_bytes * l;
+      e.start = start;
+      e.start_off = start_off;
+      e.P = P;
+      e.H = H;
+      e.dh = dh;
+      e.d = d;
+      e.cap = s->kv_cap;
+      e.status = s->status;
+    };
+    ba.first = 1;
+    ba.qkv = 1;
+    ba.store_x = 1;
+    set_qkv(0);
+    launch_block(ba, bf, st, ev(L, 0), ev(L, 1));
+    for (int l = 0; l < L; ++l) {
+      char *kc = c.k + c.layer_bytes * l, *vc = c.v + c.layer_bytes * l;
+      launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->kv_cap, s->attn_part,
+                       0, verify ? 1 : 0, ev(l, 0), ev(l, 1), st);
+      const bool last = l + 1 == L;
+      if (last && !head) break;
+      const LayerW &w = m->layers[l];
+      ba.first = 0;
+      ba.pre = 1;
+      ba.out_w = w.out_w;
+      ba.out_b = w.out_b;
+      ba.ln2_g = w.ln2_g;
+      ba.ln2_b = w.ln2_b;
+      ba.ffn1_w = w.ffn1_w;
+      ba.ffn1_b = w.ffn1_b;
+      ba.ffn2_w = w.ffn2_w;
+      ba.ffn2_b = w.ffn2_b;
+      ba.qkv = !last;
+      ba.store_x = !last;
+      ba.head = last;
+      if (!last) set_qkv(l + 1);
+      launch_block(ba, bf, st, ev(L + l + 1, 0), ev(L + l + 1, 1));
+    }
+    return TPPSD_OK;
   }
   if (!m->attnhp()) launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
   for (int l = 0; l < m->cfg.n_layers && !m->attnhp(); ++l) {
@@ -879,6 +963,8 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
     }
     const char *ng = getenv("TPPSD_NO_GRAPHS");
     s->use_graphs = !(ng && ng[0] == '1');
+    const char *lay = getenv("TPPSD_LAYERED");
+    s->block_path = !(lay && lay[0] == '1');
     const char *nf = getenv("TPPSD_LAYERED_DRAFT");
     // one workgroup per sequence: worth it until the batch alone fills the chip
     // and the layered kernels amortise weights and latency over many rows
@@ -899,7 +985,10 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
                              fused_draft_weight_elems(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix,
                                                       D->cfg.n_types) * wb <=
                          LDS_PER_WG - 4096;
-    if (s->fused_w_lds && allow_draft_fused_lds(LDS_PER_WG - 4096)) s->fused_w_lds = false;
+    if (s->fused_w_lds && allow_draft_fused_lds(LDS_PER_WG - 4096)) {
+      s->fused_w_lds = false;       // weights stay in global memory
+      (void)hipGetLastError();      // the refused attribute is not an error of this call
+    }
     const char *am = getenv("TPPSD_DRAFT_ATTN_MFMA");
     s->fused_attn_mfma = am && am[0] == '1';
   }
@@ -1119,9 +1208,9 @@ void read_round_events(tppsd_state *s, int w) {
   const int L = s->T->cfg.n_layers;
   if (s->timing & TPPSD_TIME_KERNELS) {
     for (size_t i = 0; i + 1 < s->gev[w].size(); i += 2) {
-      // AttNHP layers have one GEMM (pair L + 4 l): the other pairs were never recorded
+      // pairs the pass does not use (AttNHP layers and k_block passes launch fewer kernels)
       const int pair = (int)(i / 2);
-      if (s->T->attnhp() && pair >= L && pair < 5 * L && (pair - L) % 4) continue;
+      if (pair >= (int)s->ev_used.size() || !s->ev_used[pair]) continue;
       float ms = 0.f;
       if (hipEventElapsedTime(&ms, s->gev[w][i], s->gev[w][i + 1]) != hipSuccess) {
         (void)hipGetLastError();   // a failed query must not reach the next launch check
@@ -1211,6 +1300,7 @@ int sd_loop(tppsd_state *s, int gamma, const float *params, int max_rounds, int 
     s->round_flop = m->attnhp() ? 2.0 * rows * (L * (3 * d * 2 * d) + 4 * d * d)
                                 : 2.0 * rows * (L * (3 * d * d + d * d + 2 * d * F) + 4 * d * d);
     if (int rc = make_events(s->gev, 2 * (5 * L + 1))) return rc;
+    s->ev_used.assign(5 * L + 1, 0);
   }
   if (phases)
     if (int rc = make_events(s->pev, 4)) return rc;

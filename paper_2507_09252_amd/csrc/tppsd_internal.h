@@ -147,6 +147,36 @@ size_t fused_draft_weight_elems(int L, int d, int F, int M, int K);
 // LDS of one workgroup on gfx950
 constexpr size_t LDS_PER_WG = 160 * 1024;
 
+// Fused row block of a THP forward pass (k_block): for a tile of 16 rows,
+// everything between two attention launches. first: embed the tokens (else
+// read the residual stream x); pre: output projection of o, residual, the
+// feed-forward block of the layer whose attention just ran; then qkv: the
+// next layer's LayerNorm and q, k, v (through the EPI_QKV epilogue), or head:
+// the final LayerNorm, the decoder and its epilogue. store_x writes the
+// stream back for the next launch.
+struct BlockArgs {
+  int T, P, d, F;
+  int first, pre, qkv, head, store_x;
+  TokSrc src;
+  const void *type_emb;
+  const float *freq;
+  int n_types;
+  float *x;
+  const void *o;
+  const void *out_w, *ffn1_w, *ffn2_w;
+  const float *out_b, *ln2_g, *ln2_b, *ffn1_b, *ffn2_b;
+  const void *qkv_w;
+  const float *ln1_g, *ln1_b;
+  Epi qe;                   // EPI_QKV epilogue of the next layer (bias = its qkv bias)
+  const float *lnf_g, *lnf_b, *k1_b, *head_b;
+  const void *Ek1_w, *head_w;
+  int M, K;
+  HeadArgs h;
+};
+// whether k_block serves a model of width d, FFN width F, M mixture components and K types
+bool block_fusable(int bf16, int d, int F, int M, int K);
+void launch_block(const BlockArgs &a, int bf16, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+
 // Homogeneous-Poisson drafting (tppsd_poisson.hip)
 struct PoissonDraftArgs {
   int B, gamma, K, MG;

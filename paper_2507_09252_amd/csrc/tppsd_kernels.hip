@@ -802,16 +802,10 @@ __global__ void k_build_head(const W *__restrict__ mix_w, const W *__restrict__ 
   if (threadIdx.x == 0) hb[o] = o < 3 * M ? mix_b[o] : k2_b[o - 3 * M];
 }
 
-__global__ __launch_bounds__(256) void k_head(const float *__restrict__ logits, int ldl, int M, int K,
-                                              HeadArgs a) {
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int rows_per_seq = a.P - a.p0;
-  const int ridx = blockIdx.x * 4 + w;
-  if (ridx >= a.B * rows_per_seq) return;   // whole waves; no barriers below
-  const int b = ridx / rows_per_seq;
-  const int p = a.p0 + (ridx - b * rows_per_seq);
-  const size_t tok = (size_t)b * a.P + p;
-  const float *lr = logits + tok * ldl;
+// The decoder epilogue of one row (sequence b, block position p) whose
+// logits are lr[0 .. 3M + K), run by one whole wave.
+__device__ void head_row(const float *lr, int M, int K, const HeadArgs &a, int b, int p) {
+  const int lane = threadIdx.x & 63;
   // lane m: mixture logit, mean and log-scale of component m; type logit m
   const float lw = lane < M ? lr[lane] : -INFINITY;
   const float mu = lane < M ? lr[M + lane] : 0.f;
@@ -935,6 +929,17 @@ __global__ __launch_bounds__(256) void k_head(const float *__restrict__ logits, 
       atomicAdd(a.n_done, 1);
     }
   }
+}
+
+__global__ __launch_bounds__(256) void k_head(const float *__restrict__ logits, int ldl, int M, int K,
+                                              HeadArgs a) {
+  const int w = threadIdx.x >> 6;
+  const int rows_per_seq = a.P - a.p0;
+  const int ridx = blockIdx.x * 4 + w;
+  if (ridx >= a.B * rows_per_seq) return;   // whole waves; no barriers below
+  const int b = ridx / rows_per_seq;
+  const int p = a.p0 + (ridx - b * rows_per_seq);
+  head_row(logits + ((size_t)b * a.P + p) * ldl, M, K, a, b, p);
 }
 
 // ---------------------------------------------------------------------------
@@ -1617,6 +1622,370 @@ int allow_draft_fused_lds(size_t bytes) {
   TPPSD_FD(float)
 #undef TPPSD_FD
   return bad;
+}
+
+// ---------------------------------------------------------------------------
+// Fused row block for small THP models (§4.2 Encoder and Decoder): between
+// two attention launches of a forward pass every step is row-local (output
+// projection, residual, feed-forward block, LayerNorm, next q, k, v; or the
+// decoder), so one launch runs them all over tiles of 16 rows, the rows
+// staying in LDS. Each product is a 16-row MFMA tile product with the weights
+// read from global memory (a few hundred KB: L2-resident). The rounding points
+// are those of the layered kernels.
+// ---------------------------------------------------------------------------
+
+// Workgroup barrier that orders LDS only: global loads into registers (the
+// next product's weights) stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// The weights one wave needs for a 16-row product Y = X W^T (W [N][K]
+// row-major): its 16-column tiles wave, wave + nw, ..., at most TPB of them
+// (k_block only takes shapes where this covers every tile), and of each tile
+// lane group kq = lane / 16's k range [kq K/4, (kq + 1) K/4) -- a
+// permutation of the MFMA's k slots under which a lane's share of a weight
+// row is contiguous. Loaded one step ahead of the product that uses it, so
+// that the load latency overlaps the step before.
+template <typename ELT, int K> struct WBatch {
+  static constexpr int SEG = K / 4;                           // k per lane group
+  static constexpr int TPB = SEG >= 64 ? 1 : 64 / SEG;        // column tiles per wave
+  static constexpr int NV = SEG * (int)sizeof(ELT) / 16;      // 16-byte vectors per tile
+  static_assert(NV >= 1 && SEG * sizeof(ELT) % 16 == 0, "K too small for the lane-group split");
+  uint4 w[TPB][NV];
+  __device__ __forceinline__ void load(const ELT *__restrict__ W, int N) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const int rr = lane & 15, kq = lane >> 4;
+#pragma unroll
+    for (int j = 0; j < TPB; ++j) {
+      const int n = min((wave + j * nw) * 16 + rr, N - 1);   // rows past N clamped (results unused)
+      const uint4 *wr = (const uint4 *)(W + (size_t)n * K + kq * SEG);
+#pragma unroll
+      for (int i = 0; i < NV; ++i) w[j][i] = wr[i];
+    }
+  }
+};
+
+// Y[16 x N] = X[16 x K] W^T with X in LDS (fp32 values, row stride ldx) and
+// the wave's weights in wb; epi(r, n, y) for r < 16, n < N, each element by
+// one lane. Independent accumulators are interleaved (the tiles, or for a
+// single tile four partial sums over k) so that consecutive MFMAs never wait
+// for each other's results.
+template <typename ELT, int K, typename EPI>
+__device__ __forceinline__ void tile_mm16(const WBatch<ELT, K> &wb, int N, const float *X, int ldx, EPI epi) {
+  typedef WBatch<ELT, K> WB;
+  constexpr int SEG = WB::SEG, TPB = WB::TPB;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int rr = lane & 15, kq = lane >> 4;
+  const int ntiles = (N + 15) >> 4;
+  const float *xr = X + rr * ldx + kq * SEG;
+  constexpr int NA = TPB > 1 ? TPB : 4;
+  f32x4_t acc[NA];
+#pragma unroll
+  for (int j = 0; j < NA; ++j) acc[j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+  if constexpr (sizeof(ELT) == 4) {
+    float xa[SEG];
+#pragma unroll
+    for (int i = 0; i < SEG; i += 4) {
+      const float4 v = *(const float4 *)(xr + i);
+      xa[i] = v.x; xa[i + 1] = v.y; xa[i + 2] = v.z; xa[i + 3] = v.w;
+    }
+    auto wv = [&](int j, int i) -> float {
+      const uint4 u = wb.w[j][i >> 2];
+      const uint32_t e = (i & 3) == 0 ? u.x : (i & 3) == 1 ? u.y : (i & 3) == 2 ? u.z : u.w;
+      return __uint_as_float(e);
+    };
+    if constexpr (TPB > 1) {
+#pragma unroll
+      for (int i = 0; i < SEG; ++i)
+#pragma unroll
+        for (int j = 0; j < TPB; ++j) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[i], wv(j, i), acc[j], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < SEG; ++i) acc[i & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[i], wv(0, i), acc[i & 3], 0, 0, 0);
+      acc[0] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    }
+  } else {
+    constexpr int NV = WB::NV;
+    bf16x8_t xa[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)   // LDS values are already rounded to bf16
+        w[e] = (uint32_t)f2bf(xr[8 * i + 2 * e]) | ((uint32_t)f2bf(xr[8 * i + 2 * e + 1]) << 16);
+      xa[i] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
+    }
+    if constexpr (TPB > 1) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i)
+#pragma unroll
+        for (int j = 0; j < TPB; ++j)
+          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[i], __builtin_bit_cast(bf16x8_t, wb.w[j][i]), acc[j], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < NV; ++i)
+        acc[i & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[i], __builtin_bit_cast(bf16x8_t, wb.w[0][i]), acc[i & 3], 0, 0, 0);
+      acc[0] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < TPB; ++j) {
+    const int t = wave + j * nw;
+    const int nc = t * 16 + rr;
+    if (t < ntiles && nc < N)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) epi(4 * kq + v, nc, acc[j][v]);
+  }
+}
+
+// LayerNorm (biased variance, eps 1e-5) of the tile's rows, one wave per row;
+// rows at or past nr are zero (they only feed discarded MFMA rows)
+template <typename ELT>
+__device__ __forceinline__ void tile_layernorm(const float *x, int ldx, float *y, int ldy, const float *g,
+                                               const float *bt, int nr, int d) {
+  // 16 lanes per row: a wave normalises 4 rows at once
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int sub = lane & 15;
+  for (int r = 4 * wave + (lane >> 4); r < 16; r += 4 * nw) {
+    float *yr = y + r * ldy;
+    const float *xr = x + r * ldx;
+    float s = 0.f;
+    for (int j = sub; j < d; j += 16) s += xr[j];
+    s += dpp_mov<0xB1>(s);    // lane ^ 1
+    s += dpp_mov<0x4E>(s);    // lane ^ 2
+    s += dpp_mov<0x124>(s);   // row_ror:4
+    s += dpp_mov<0x128>(s);   // row_ror:8: every lane of the row holds the sum
+    const float mean = s / (float)d;
+    float v = 0.f;
+    for (int j = sub; j < d; j += 16) {
+      const float c = xr[j] - mean;
+      v += c * c;
+    }
+    v += dpp_mov<0xB1>(v);    // lane ^ 1
+    v += dpp_mov<0x4E>(v);    // lane ^ 2
+    v += dpp_mov<0x124>(v);   // row_ror:4
+    v += dpp_mov<0x128>(v);   // row_ror:8: every lane of the row holds the sum
+    const float rstd = 1.f / sqrtf(v / (float)d + 1e-5f);
+    for (int j = sub; j < d; j += 16) yr[j] = r < nr ? rnd_act<ELT>((xr[j] - mean) * rstd * g[j] + bt[j]) : 0.f;
+  }
+}
+
+// floats of the small vectors k_block stages in LDS: out_b, LN2 (g, b),
+// ffn1_b, ffn2_b, LN1 (g, b), qkv_b, LN_f (g, b), k1_b, decoder bias
+inline __host__ __device__ int block_vec_floats(int d, int F, int M, int K) { return 13 * d + F + 3 * M + K; }
+
+template <typename ELT, int D, int F>
+__global__ __launch_bounds__(256) void k_block(BlockArgs a) {
+  constexpr int LX = D + 4, LH = (F > 4 * D ? F : 4 * D) + 4;
+  extern __shared__ __attribute__((aligned(16))) float sm[];
+  __shared__ int row_b[16], row_pos[16];
+  float *xs = sm;              // [16][LX] residual stream
+  float *as = xs + 16 * LX;    // [16][LX] LayerNorm outputs / attention outputs
+  float *hs = as + 16 * LX;    // [16][LH] FFN hidden / decoder e | tanh
+  float *hv = hs + 16 * LH;    // [16][LV] decoder logits
+  const int LV = 3 * a.M + a.K + 1;
+  float *vec = hv + 16 * LV;   // staged small vectors
+  float *out_b = vec, *ln2_g = out_b + D, *ln2_b = ln2_g + D, *ffn1_b = ln2_b + D, *ffn2_b = ffn1_b + F,
+        *ln1_g = ffn2_b + D, *ln1_b = ln1_g + D, *qkv_b = ln1_b + D, *lnf_g = qkv_b + 3 * D, *lnf_b = lnf_g + D,
+        *k1_b = lnf_b + D, *head_b = k1_b + D;
+  const int tid = threadIdx.x, r0 = blockIdx.x * 16, nr = min(16, a.T - r0);
+  // Phase 0: every global load of the launch's inputs is issued before any
+  // LDS store (the compiler keeps a load after an earlier store it cannot
+  // prove disjoint): the small vectors of the steps this launch runs, the
+  // rows of x (or the tokens) and of the attention output; then each row's
+  // sequence and cache position.
+  constexpr int VMAX = (13 * D + F + 3 * 64 + 64 + 255) / 256;   // vector floats per thread
+  float vv[VMAX];
+  {
+    const float *seg_src[12] = {a.out_b, a.ln2_g, a.ln2_b, a.ffn1_b, a.ffn2_b, a.ln1_g,
+                                a.ln1_b, a.qe.bias, a.lnf_g, a.lnf_b, a.k1_b, a.head_b};
+    const int pre = a.pre, qk = a.qkv, hd = a.head;
+    const int seg_len[12] = {pre * D, pre * D, pre * D, pre * F, pre * D, qk * D,
+                             qk * D,  qk * 3 * D, hd * D, hd * D, hd * D, hd * (3 * a.M + a.K)};
+    const int seg_off[12] = {0, D, 2 * D, 3 * D, 3 * D + F, 4 * D + F, 5 * D + F, 6 * D + F, 9 * D + F,
+                             10 * D + F, 11 * D + F, 12 * D + F};
+#pragma unroll
+    for (int i = 0; i < VMAX; ++i) {
+      const int idx = tid + 256 * i;
+      vv[i] = 0.f;
+      for (int sgi = 0; sgi < 12; ++sgi) {
+        const int o = idx - seg_off[sgi];
+        if (o >= 0 && o < seg_len[sgi]) vv[i] = seg_src[sgi][o];
+      }
+    }
+  }
+  float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int xr_ = tid / (D / 4), xc_ = tid - xr_ * (D / 4);   // one float4 of x per thread (16 D / 4 <= 256)
+  if (!a.first && xr_ < nr) xv = *(const float4 *)(a.x + (size_t)(r0 + xr_) * D + 4 * xc_);
+  constexpr int OV = 16 / sizeof(ELT);                          // o elements per 16-byte load
+  uint4 ov = make_uint4(0u, 0u, 0u, 0u);
+  const int or_ = tid / (D / OV), oc_ = tid - or_ * (D / OV);
+  if (a.pre && or_ < 16 && or_ < nr) ov = *(const uint4 *)((const ELT *)a.o + (size_t)(r0 + or_) * D + OV * oc_);
+  // the first product's weights (output projection, else the next q, k, v or
+  // the decoder's [E; V_k1]) and the feed-forward block's first matrix, issued
+  // after the row loads so that waiting for those does not wait for these
+  WBatch<ELT, D> w_a, w_f1;
+  if (a.pre)
+    w_a.load((const ELT *)a.out_w, D);
+  else if (a.qkv)
+    w_a.load((const ELT *)a.qkv_w, 3 * D);
+  else
+    w_a.load((const ELT *)a.Ek1_w, 4 * D);
+  if (a.pre) w_f1.load((const ELT *)a.ffn1_w, F);
+#pragma unroll
+  for (int i = 0; i < VMAX; ++i)
+    if (tid + 256 * i < 12 * D + F + 3 * a.M + a.K + D) vec[tid + 256 * i] = vv[i];
+  if (a.qkv && tid < 16) {
+    const int R = min(r0 + tid, a.T - 1), b = R / a.P;
+    row_b[tid] = b;
+    row_pos[tid] = a.qe.start[b] + a.qe.start_off + (R - b * a.P);
+  }
+  if (a.first) {
+    for (int idx = tid; idx < 16 * D; idx += blockDim.x) {
+      const int r = idx / D, j = idx - r * D;
+      float v = 0.f;
+      if (r < nr) {
+        const int R = r0 + r, b = R / a.P, p = R - b * a.P;
+        const TokSrc &src = a.src;
+        float t;
+        int k;
+        if (p < src.n_ev) {
+          const size_t i = (size_t)b * src.ev_stride + src.start[b] + src.start_off + p;
+          t = src.ev_t[i];
+          k = src.ev_k[i];
+        } else {
+          const size_t i = (size_t)b * src.dr_stride + src.dr_off + (p - src.n_ev);
+          t = src.dr_t[i];
+          k = src.dr_k[i];
+        }
+        k = min(max(k, 0), a.n_types - 1);
+        const float arg = t * a.freq[j];
+        v = ((j & 1) ? cosf(arg) : sinf(arg)) + ld((const ELT *)a.type_emb, (size_t)k * D + j);
+      }
+      xs[r * LX + j] = v;
+    }
+  } else if (xr_ < 16) {
+    *(float4 *)(xs + xr_ * LX + 4 * xc_) = xv;
+  }
+  if (a.pre && or_ < 16) {
+    float ovf[OV];
+    if constexpr (sizeof(ELT) == 4) {
+      ovf[0] = __uint_as_float(ov.x); ovf[1] = __uint_as_float(ov.y);
+      ovf[2] = __uint_as_float(ov.z); ovf[3] = __uint_as_float(ov.w);
+    } else {
+      const uint32_t w[4] = {ov.x, ov.y, ov.z, ov.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        ovf[2 * e] = __uint_as_float(w[e] << 16);
+        ovf[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < OV; ++e) as[or_ * LX + OV * oc_ + e] = ovf[e];
+  }
+  WBatch<ELT, D> w_n;   // after the feed-forward block: the next q, k, v or [E; V_k1]
+  if (a.pre) {
+    lds_barrier();
+    tile_mm16(w_a, D, as, LX, [&](int r, int n, float y) { xs[r * LX + n] += y + out_b[n]; });
+    lds_barrier();
+    WBatch<ELT, F> w_f2;
+    w_f2.load((const ELT *)a.ffn2_w, D);
+    tile_layernorm<ELT>(xs, LX, as, LX, ln2_g, ln2_b, nr, D);
+    lds_barrier();
+    tile_mm16(w_f1, F, as, LX,
+              [&](int r, int n, float y) { hs[r * LH + n] = rnd_act<ELT>(fmaxf(y + ffn1_b[n], 0.f)); });
+    lds_barrier();
+    if (a.qkv)
+      w_n.load((const ELT *)a.qkv_w, 3 * D);
+    else
+      w_n.load((const ELT *)a.Ek1_w, 4 * D);
+    tile_mm16(w_f2, D, hs, LH, [&](int r, int n, float y) { xs[r * LX + n] += y + ffn2_b[n]; });
+  } else {
+    w_n = w_a;
+  }
+  lds_barrier();
+  if (a.store_x)
+    for (int idx = tid; idx < nr * (D / 4); idx += blockDim.x) {
+      const int r = idx / (D / 4), c = idx - r * (D / 4);
+      *(float4 *)(a.x + (size_t)(r0 + r) * D + 4 * c) = *(const float4 *)(xs + r * LX + 4 * c);
+    }
+  if (a.qkv) {
+    tile_layernorm<ELT>(xs, LX, as, LX, ln1_g, ln1_b, nr, D);
+    lds_barrier();
+    // q to its rows, keys and values appended to the cache (the EPI_QKV
+    // arithmetic with the row's sequence and position from LDS)
+    const Epi &e = a.qe;
+    const int dh = e.dh, lg = dh == 16 ? 4 : (dh == 32 ? 5 : 6);
+    tile_mm16(w_n, 3 * D, as, LX, [&](int r, int n, float y) {
+      if (r >= nr) return;
+      const float v = y + qkv_b[n];
+      const int which = n / D, c = n - which * D;
+      if (which == 0) {
+        st((ELT *)e.q, (size_t)(r0 + r) * D + c, v);
+      } else {
+        const int pos = row_pos[r], h = c >> lg, j = c & (dh - 1);
+        if (pos < e.cap) {
+          const size_t row0 = ((size_t)row_b[r] * e.H + h) * e.cap;
+          if (which == 1)
+            st((ELT *)e.kc, (row0 + pos) * dh + j, v);
+          else
+            st((ELT *)e.vc, v_at<ELT>(row0, pos, j, dh), v);
+        } else {
+          atomicOr(e.status, TPPSD_STATUS_CAPACITY);
+        }
+      }
+    });
+  }
+  if (a.head) {
+    WBatch<ELT, 4 * D> w_h;
+    w_h.load((const ELT *)a.head_w, 3 * a.M + a.K);
+    tile_layernorm<ELT>(xs, LX, as, LX, lnf_g, lnf_b, nr, D);
+    lds_barrier();
+    tile_mm16(w_n, 4 * D, as, LX, [&](int r, int n, float y) {
+      hs[r * LH + n] = n < 3 * D ? rnd_act<ELT>(y) : rnd_act<ELT>(tanhf(y + k1_b[n - 3 * D]));
+    });
+    lds_barrier();
+    tile_mm16(w_h, 3 * a.M + a.K, hs, LH, [&](int r, int n, float y) { hv[r * LV + n] = y + head_b[n]; });
+    lds_barrier();
+    const int wave = tid >> 6, nw = blockDim.x >> 6;
+    for (int r = wave; r < nr; r += nw) {
+      const int R = r0 + r, b = R / a.P, p = R - b * a.P;
+      if (p >= a.h.p0) head_row(hv + r * LV, a.M, a.K, a.h, b, p);
+    }
+  }
+}
+
+bool block_fusable(int bf16, int d, int F, int M, int K) {
+  // instantiated widths; every product's column tiles fit one weight batch of
+  // the four waves (16 (64 / (k / 4)) columns per wave, at least 16): the
+  // decoder's 3M + K logits over k = 4d need 3M + K <= 4 * 16 * max(1, 64 / d)
+  const bool widths = (d == 32 && (F == 64 || F == 128)) || (d == 64 && (F == 128 || F == 256));
+  // a launch streams a layer's matrices through each workgroup: worth it while
+  // they are small (measured: d = 32 models gain, fp32 d = 64 / F = 256 loses
+  // to the layered kernels, whose many small workgroups spread the latency)
+  const size_t layer_bytes = (size_t)(4 * d * d + 2 * d * F) * (bf16 ? 2 : 4);
+  return widths && 3 * M + K <= 64 * (d >= 64 ? 1 : 64 / d) && layer_bytes <= 64 * 1024;
+}
+
+void launch_block(const BlockArgs &a, int bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const int LX = a.d + 4, LH = (a.F > 4 * a.d ? a.F : 4 * a.d) + 4, LV = 3 * a.M + a.K + 1;
+  const size_t lds = ((size_t)16 * (2 * LX + LH + LV) + block_vec_floats(a.d, a.F, a.M, a.K)) * sizeof(float);
+  const dim3 grid((a.T + 15) / 16);
+  auto go = [&](auto kern) { hipExtLaunchKernelGGL(kern, grid, dim3(256), lds, s, ev0, ev1, 0, a); };
+#define TPPSD_BLK(ELT)                                              \
+  if (a.d == 32 && a.F == 64) go(k_block<ELT, 32, 64>);             \
+  else if (a.d == 32) go(k_block<ELT, 32, 128>);                    \
+  else if (a.F == 128) go(k_block<ELT, 64, 128>);                   \
+  else go(k_block<ELT, 64, 256>);
+  if (bf16) {
+    TPPSD_BLK(bf16_t)
+  } else {
+    TPPSD_BLK(float)
+  }
+#undef TPPSD_BLK
 }
 
 // ---------------------------------------------------------------------------
