@@ -60,6 +60,15 @@ def attention_bytes_per_launch(wl, gamma, B):
     return kv + qo
 
 
+def verify_weight_bytes(wl):
+    """Bytes of the target's weights read by one verify pass (once)."""
+    c = wl.target
+    elt = 2 if c.prec == "bf16" else 4
+    d, F, M, K = c.d_model, c.d_ffn, c.n_mix, c.n_types
+    layer = 6 * d * d if getattr(c, "encoder", "thp") == "attnhp" else 4 * d * d + 2 * d * F
+    return elt * (c.n_layers * layer + 4 * d * d + (3 * M + K) * 4 * d)
+
+
 def verify_pass_fraction(wl, gamma, B, verify_ms):
     """Roofline time of one verify pass, max(flop / MFMA peak, bytes / HBM
     peak), against its measured time (phase timing, graph-replayed). flop:
@@ -267,6 +276,14 @@ def main():
                                 "accept": pph["accept_ms"] * 1e3 / p_nr, "rounds": pph["rounds"]}}
         del sp
     per_launch = attention_bytes_per_launch(wl, gamma, B)
+    kernel_name = KERNEL_NAME[wl.prec]
+    if attn_launches == 0 and tk["gemm_launches"] > 0:
+        # the whole verify pass is one launch (k_verify_seq, small targets): its
+        # attention is inside it, so the pass's own algorithmic bytes (every
+        # layer's K/V and queries / outputs, the weights once) over its duration
+        attn_launches, attn_ms = tk["gemm_launches"], tk["gemm_ms"]
+        per_launch = per_launch * wl.target.n_layers + verify_weight_bytes(wl)
+        kernel_name = "k_verify_seq (whole verify pass, one workgroup per sequence)"
     avg_ms = attn_ms / max(1, attn_launches)
     achieved = per_launch / (avg_ms * 1e-3) / 1e9 if attn_launches else 0.0
     out = {
@@ -289,9 +306,10 @@ def main():
         "alpha": alpha,
         "events_per_round": events * args.steps / max(1, rounds),
         "rounds_per_job": rounds / args.steps,
-        "roofline": {"bound": "hbm", "kernel": KERNEL_NAME[wl.prec], "achieved": achieved,
+        "roofline": {"bound": "hbm", "kernel": kernel_name, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": measured_traffic(wl.name), "avg_launch_us": avg_ms * 1e3, "launches": attn_launches,
+                     "traffic": measured_traffic(wl.name) if kernel_name == KERNEL_NAME[wl.prec] else None,
+                     "avg_launch_us": avg_ms * 1e3, "launches": attn_launches,
                      "algorithmic_bytes_per_launch": per_launch},
     }
     if not args.no_window:

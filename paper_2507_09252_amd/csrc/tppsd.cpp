@@ -204,6 +204,7 @@ struct tppsd_state {
   bool heads_built = false;
   float *ar_mix = nullptr, *ar_logtype = nullptr;
   bool block_path = true;              // k_block for the models it serves (TPPSD_LAYERED=1: layered kernels)
+  bool verify_seq = true;              // k_verify_seq for the targets it serves (TPPSD_LAYERED=1: off)
   float *attn_part = nullptr;
   int32_t *gen0 = nullptr;
   // internal round buffers (tppsd_sample_sd)
@@ -723,6 +724,52 @@ int do_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_
   h.dr_stride = s->max_gamma;
   h.v_logg = out->logg;
   h.v_logf = out->logf;
+  const tppsd_model *m = s->T;
+  if (s->verify_seq && !m->attnhp() &&
+      verify_seq_ok(m->bf16(), m->cfg.n_layers, m->d(), m->H(), m->cfg.d_ffn, m->cfg.n_mix, m->cfg.n_types,
+                    gamma + 1)) {
+    // small targets: the whole pass of a sequence in one workgroup
+    VerifySeqArgs a{};
+    a.P = gamma + 1;
+    a.d = m->d();
+    a.F = m->cfg.d_ffn;
+    a.H = m->H();
+    a.L = m->cfg.n_layers;
+    a.M = m->cfg.n_mix;
+    a.K = m->cfg.n_types;
+    for (int l = 0; l < a.L; ++l) {
+      const LayerW &w = m->layers[l];
+      a.layer[l] = {w.qkv_w, w.out_w, w.ffn1_w, w.ffn2_w, w.ln1_g, w.ln1_b, w.qkv_b,
+                    w.out_b, w.ln2_g, w.ln2_b, w.ffn1_b, w.ffn2_b};
+    }
+    a.type_emb = m->type_emb;
+    a.Ek1_w = m->Ek1_w;
+    a.head_w = s->cT.head_w;
+    a.lnf_g = m->lnf_g;
+    a.lnf_b = m->lnf_b;
+    a.k1_b = m->k1_b;
+    a.head_b = s->cT.head_b;
+    a.freq = s->cT.freq;
+    a.kc = s->cT.k;
+    a.vc = s->cT.v;
+    a.layer_bytes = s->cT.layer_bytes;
+    a.cap = s->kv_cap;
+    a.ev_t = s->ev_t;
+    a.ev_k = s->ev_k;
+    a.ev_stride = s->cap;
+    a.lenT = s->lenT;
+    a.done = s->done;
+    a.dr_t = in->t;
+    a.dr_k = in->k;
+    a.dr_stride = s->max_gamma;
+    a.status = s->status;
+    a.h = h;
+    const bool timed = s->cur_ev != nullptr;
+    if (timed) s->ev_used[m->cfg.n_layers] = 1;
+    launch_verify_seq(a, s->B, m->bf16(), st, timed ? s->cur_ev[2 * m->cfg.n_layers] : nullptr,
+                      timed ? s->cur_ev[2 * m->cfg.n_layers + 1] : nullptr);
+    return hip_check("tppsd_verify");
+  }
   int rc = forward(s, s->T, s->cT, s->lenT, 0, gamma + 1, src, &h, true, st);
   if (rc) return rc;
   return hip_check("tppsd_verify");
@@ -965,6 +1012,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
     s->use_graphs = !(ng && ng[0] == '1');
     const char *lay = getenv("TPPSD_LAYERED");
     s->block_path = !(lay && lay[0] == '1');
+    s->verify_seq = s->block_path;
     const char *nf = getenv("TPPSD_LAYERED_DRAFT");
     // one workgroup per sequence: worth it until the batch alone fills the chip
     // and the layered kernels amortise weights and latency over many rows

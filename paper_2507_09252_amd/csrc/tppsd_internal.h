@@ -177,6 +177,32 @@ struct BlockArgs {
 bool block_fusable(int bf16, int d, int F, int M, int K);
 void launch_block(const BlockArgs &a, int bf16, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
+// Per-sequence verify pass (k_verify_seq): one workgroup runs the whole target
+// pass of one sequence's P = gamma + 1 positions (embedding, every layer with
+// its attention, decoder, verify epilogue), the rows staying in LDS.
+struct VerifySeqArgs {
+  int P, d, F, H, L, M, K;
+  FusedLayerW layer[FD_MAX_LAYERS];
+  const void *type_emb, *Ek1_w, *head_w;
+  const float *lnf_g, *lnf_b, *k1_b, *head_b, *freq;
+  char *kc, *vc;            // target cache bases; layer stride layer_bytes
+  size_t layer_bytes;
+  int cap;
+  const float *ev_t;
+  const int32_t *ev_k;
+  int ev_stride;
+  const int32_t *lenT, *done;
+  const float *dr_t;
+  const int32_t *dr_k;
+  int dr_stride;
+  uint32_t *status;
+  HeadArgs h;               // HEAD_VERIFY
+};
+// whether k_verify_seq serves a target of these sizes for P positions
+bool verify_seq_ok(int bf16, int L, int d, int H, int F, int M, int K, int P);
+void launch_verify_seq(const VerifySeqArgs &a, int B, int bf16, hipStream_t st, hipEvent_t ev0 = nullptr,
+                       hipEvent_t ev1 = nullptr);
+
 // Homogeneous-Poisson drafting (tppsd_poisson.hip)
 struct PoissonDraftArgs {
   int B, gamma, K, MG;

@@ -1235,20 +1235,20 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
 // before computing any.
 // The waves of a head merge through LDS. red: LDS scratch of
 // max(4, H) * 2 * 18 floats.
-template <typename ELT, int DH>
+template <typename ELT, int DH, int QMAX = 2, int NB = 4>   // NB: steps per load batch
 __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
-                             int H, int P, int pos0, int d, float *red) {
+                             int H, int P, int pos0, int ld, float *red) {
   static_assert(DH == 16, "the fused draft attention serves d_head = 16");
-  constexpr int KT = 32, NB = 4;   // steps per load batch
+  constexpr int KT = 32;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rr = lane & 15, g = lane >> 4;
-  const int wph = H >= 4 ? 1 : 4 / H, wsub = wave % wph;
+  const int nw = blockDim.x >> 6, wph = H >= nw ? 1 : nw / H, wsub = wave % wph;
   const int n_keys = min(pos0 + P, cap);
   const float scale = 0.25f;   // 1 / sqrt(16)
   const int krow0 = 8 * (rr >> 2) + (rr & 3);
-  for (int h = wave / wph; h < H; h += 4 / wph) {
+  for (int h = wave / wph; h < H; h += nw / wph) {
     const size_t row0 = seq_row0 + (size_t)h * cap;
     // query fragment: dims 4 g .. + 3 of query rr (zero for rr >= P)
-    const float *qp = qs + min(rr, P - 1) * d + h * DH + 4 * g;
+    const float *qp = qs + min(rr, P - 1) * ld + h * DH + 4 * g;
     const float q0 = rr < P ? qp[0] : 0.f, q1 = rr < P ? qp[1] : 0.f, q2 = rr < P ? qp[2] : 0.f,
                 q3 = rr < P ? qp[3] : 0.f;
     float m_run = -INFINITY, l_run = 0.f;
@@ -1329,7 +1329,7 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
     }
     // lane (rr, g) holds O^T[4 g + i][query rr]
     if (rr < P) {
-      float *r = red + ((h * wph + wsub) * 2 + rr) * (DH + 2);
+      float *r = red + ((h * wph + wsub) * QMAX + rr) * (DH + 2);
       if (g == 0) {
         r[0] = m_run;
         r[1] = l_run;
@@ -1342,15 +1342,15 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
   for (int idx = tid; idx < P * H * DH; idx += blockDim.x) {
     const int p = idx / (H * DH), rest = idx - p * H * DH, hh = rest / DH, j = rest - hh * DH;
     float M = -INFINITY;
-    for (int w = 0; w < wph; ++w) M = fmaxf(M, red[((hh * wph + w) * 2 + p) * (DH + 2)]);
+    for (int w = 0; w < wph; ++w) M = fmaxf(M, red[((hh * wph + w) * QMAX + p) * (DH + 2)]);
     float L = 0.f, O = 0.f;
     for (int w = 0; w < wph; ++w) {
-      const float *r = red + ((hh * wph + w) * 2 + p) * (DH + 2);
+      const float *r = red + ((hh * wph + w) * QMAX + p) * (DH + 2);
       const float f = (r[0] == -INFINITY) ? 0.f : expf(r[0] - M);
       L += r[1] * f;
       O += r[2 + j] * f;
     }
-    os[p * d + hh * DH + j] = rnd_act<ELT>(L > 0.f ? O / L : 0.f);
+    os[p * ld + hh * DH + j] = rnd_act<ELT>(L > 0.f ? O / L : 0.f);
   }
 }
 
@@ -1643,15 +1643,15 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // The weights one wave needs for a 16-row product Y = X W^T (W [N][K]
-// row-major): its 16-column tiles wave, wave + nw, ..., at most TPB of them
-// (k_block only takes shapes where this covers every tile), and of each tile
+// row-major): its 16-column tiles wave, wave + nw, ..., at most TPW of them
+// (the callers only take shapes where this covers every tile), and of each tile
 // lane group kq = lane / 16's k range [kq K/4, (kq + 1) K/4) -- a
 // permutation of the MFMA's k slots under which a lane's share of a weight
 // row is contiguous. Loaded one step ahead of the product that uses it, so
 // that the load latency overlaps the step before.
-template <typename ELT, int K> struct WBatch {
+template <typename ELT, int K, int TPW> struct WBatch {
   static constexpr int SEG = K / 4;                           // k per lane group
-  static constexpr int TPB = SEG >= 64 ? 1 : 64 / SEG;        // column tiles per wave
+  static constexpr int TPB = TPW;                             // column tiles per wave
   static constexpr int NV = SEG * (int)sizeof(ELT) / 16;      // 16-byte vectors per tile
   static_assert(NV >= 1 && SEG * sizeof(ELT) % 16 == 0, "K too small for the lane-group split");
   uint4 w[TPB][NV];
@@ -1673,9 +1673,9 @@ template <typename ELT, int K> struct WBatch {
 // one lane. Independent accumulators are interleaved (the tiles, or for a
 // single tile four partial sums over k) so that consecutive MFMAs never wait
 // for each other's results.
-template <typename ELT, int K, typename EPI>
-__device__ __forceinline__ void tile_mm16(const WBatch<ELT, K> &wb, int N, const float *X, int ldx, EPI epi) {
-  typedef WBatch<ELT, K> WB;
+template <typename ELT, int K, int TPW, typename EPI>
+__device__ __forceinline__ void tile_mm16(const WBatch<ELT, K, TPW> &wb, int N, const float *X, int ldx, EPI epi) {
+  typedef WBatch<ELT, K, TPW> WB;
   constexpr int SEG = WB::SEG, TPB = WB::TPB;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int rr = lane & 15, kq = lane >> 4;
@@ -1780,6 +1780,9 @@ inline __host__ __device__ int block_vec_floats(int d, int F, int M, int K) { re
 template <typename ELT, int D, int F>
 __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
   constexpr int LX = D + 4, LH = (F > 4 * D ? F : 4 * D) + 4;
+  // column tiles per wave (4 waves) of each product; the decoder's 3M + K
+  // logits are at most 64 (64 / d) wide (block_fusable)
+  constexpr int TO = (D + 63) / 64, T1 = (F + 63) / 64, TE = (4 * D + 63) / 64, TH = D >= 64 ? 1 : 64 / D;
   extern __shared__ __attribute__((aligned(16))) float sm[];
   __shared__ int row_b[16], row_pos[16];
   float *xs = sm;              // [16][LX] residual stream
@@ -1827,7 +1830,8 @@ __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
   // the first product's weights (output projection, else the next q, k, v or
   // the decoder's [E; V_k1]) and the feed-forward block's first matrix, issued
   // after the row loads so that waiting for those does not wait for these
-  WBatch<ELT, D> w_a, w_f1;
+  WBatch<ELT, D, TE> w_a;
+  WBatch<ELT, D, T1> w_f1;
   if (a.pre)
     w_a.load((const ELT *)a.out_w, D);
   else if (a.qkv)
@@ -1886,12 +1890,12 @@ __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
 #pragma unroll
     for (int e = 0; e < OV; ++e) as[or_ * LX + OV * oc_ + e] = ovf[e];
   }
-  WBatch<ELT, D> w_n;   // after the feed-forward block: the next q, k, v or [E; V_k1]
+  WBatch<ELT, D, TE> w_n;   // after the feed-forward block: the next q, k, v or [E; V_k1]
   if (a.pre) {
     lds_barrier();
     tile_mm16(w_a, D, as, LX, [&](int r, int n, float y) { xs[r * LX + n] += y + out_b[n]; });
     lds_barrier();
-    WBatch<ELT, F> w_f2;
+    WBatch<ELT, F, TO> w_f2;
     w_f2.load((const ELT *)a.ffn2_w, D);
     tile_layernorm<ELT>(xs, LX, as, LX, ln2_g, ln2_b, nr, D);
     lds_barrier();
@@ -1940,7 +1944,7 @@ __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
     });
   }
   if (a.head) {
-    WBatch<ELT, 4 * D> w_h;
+    WBatch<ELT, 4 * D, TH> w_h;
     w_h.load((const ELT *)a.head_w, 3 * a.M + a.K);
     tile_layernorm<ELT>(xs, LX, as, LX, lnf_g, lnf_b, nr, D);
     lds_barrier();
@@ -1986,6 +1990,196 @@ void launch_block(const BlockArgs &a, int bf16, hipStream_t s, hipEvent_t ev0, h
     TPPSD_BLK(float)
   }
 #undef TPPSD_BLK
+}
+
+// ---------------------------------------------------------------------------
+// Per-sequence verify pass for small THP targets (§4.3 "Verification"): one
+// 512-thread workgroup runs the target over one sequence's P = gamma + 1 new
+// positions -- the pending event and the drafts -- through every layer and
+// the decoder, with the verify epilogue per row. The P rows are one 16-row
+// MFMA tile; q, the attention output and the stream stay in LDS, keys and
+// values go to the cache and the attention reads them back from it (as the
+// layered pass). Each product's weights are loaded one step ahead.
+// ---------------------------------------------------------------------------
+inline __host__ __device__ int verify_seq_vec_floats(int L, int d, int F, int M, int K) {
+  return L * (9 * d + F) + 3 * d + 3 * M + K;
+}
+
+template <typename ELT, int D, int F>
+__global__ __launch_bounds__(512) void k_verify_seq(VerifySeqArgs a) {
+  constexpr int LX = D + 4, LH = (F > 4 * D ? F : 4 * D) + 4, DH = 16;
+  // column tiles per wave (8 waves) of each product; the decoder's 3M + K
+  // logits are at most 128 (64 / d) wide (verify_seq_ok)
+  constexpr int TQ = (4 * D + 127) / 128, TO = (D + 127) / 128, T1 = (F + 127) / 128, TH = D >= 64 ? 1 : 64 / D;
+  extern __shared__ __attribute__((aligned(16))) float sm[];
+  __shared__ float tok_t[16];
+  __shared__ int tok_k[16];
+  const int LV = 3 * a.M + a.K + 1;
+  float *xs = sm, *as = xs + 16 * LX, *qs = as + 16 * LX, *os = qs + 16 * LX;
+  float *hs = os + 16 * LX;          // [16][LH] FFN hidden / decoder e | tanh
+  float *hv = hs + 16 * LH;          // [16][LV] decoder logits
+  float *red = hv + 16 * LV;         // attention merge: [8 waves][16 queries][DH + 2]
+  float *vec = red + 8 * 16 * (DH + 2);
+  const int tid = threadIdx.x, b = blockIdx.x, P = a.P, H = a.H;
+  if (a.done[b]) return;
+  const int pos0 = a.lenT[b];
+  const size_t seq_row0 = (size_t)b * H * a.cap;
+  // phase 0: the small vectors (per layer LN1 g, b, qkv_b, out_b, LN2 g, b,
+  // ffn1_b, ffn2_b; then LN_f g, b, k1_b, decoder bias), the tokens, and the
+  // first layer's q, k, v weights, all loads issued before any LDS store
+  const int nvec = verify_seq_vec_floats(a.L, D, F, a.M, a.K);
+  constexpr int VMAX = (FD_MAX_LAYERS * (9 * D + F) + 3 * D + 3 * 64 + 64 + 511) / 512;
+  float vv[VMAX];
+#pragma unroll
+  for (int i = 0; i < VMAX; ++i) {
+    int o = tid + 512 * i;
+    vv[i] = 0.f;
+    if (o < nvec) {
+      const int per = 9 * D + F;
+      if (o < a.L * per) {
+        const int ly = o / per;
+        o -= ly * per;
+        const FusedLayerW &w = a.layer[ly];
+        vv[i] = o < D ? w.ln1_g[o] : o < 2 * D ? w.ln1_b[o - D] : o < 5 * D ? w.qkv_b[o - 2 * D]
+              : o < 6 * D ? w.out_b[o - 5 * D] : o < 7 * D ? w.ln2_g[o - 6 * D] : o < 8 * D ? w.ln2_b[o - 7 * D]
+              : o < 8 * D + F ? w.ffn1_b[o - 8 * D] : w.ffn2_b[o - 8 * D - F];
+      } else {
+        o -= a.L * per;
+        vv[i] = o < D ? a.lnf_g[o] : o < 2 * D ? a.lnf_b[o - D] : o < 3 * D ? a.k1_b[o - 2 * D] : a.head_b[o - 3 * D];
+      }
+    }
+  }
+  float tt = 0.f;
+  int tk = 0;
+  if (tid < P) {
+    if (tid == 0) {   // the pending committed event
+      const size_t i = (size_t)b * a.ev_stride + pos0;
+      tt = a.ev_t[i];
+      tk = a.ev_k[i];
+    } else {          // draft tid - 1
+      const size_t i = (size_t)b * a.dr_stride + tid - 1;
+      tt = a.dr_t[i];
+      tk = a.dr_k[i];
+    }
+  }
+  WBatch<ELT, D, TQ> w_q;   // q, k, v (3D columns) or [E; V_k1] (4D)
+  w_q.load((const ELT *)a.layer[0].qkv_w, 3 * D);
+#pragma unroll
+  for (int i = 0; i < VMAX; ++i)
+    if (tid + 512 * i < nvec) vec[tid + 512 * i] = vv[i];
+  if (tid < 16) {
+    tok_t[tid] = tt;
+    tok_k[tid] = min(max(tk, 0), a.K - 1);
+  }
+  lds_barrier();
+  for (int idx = tid; idx < 16 * D; idx += blockDim.x) {
+    const int r = idx / D, j = idx - r * D;
+    float v = 0.f;
+    qs[r * LX + j] = 0.f;   // rows past P stay zero
+    os[r * LX + j] = 0.f;
+    if (r < P) {
+      const float arg = tok_t[r] * a.freq[j];
+      v = ((j & 1) ? cosf(arg) : sinf(arg)) + ld((const ELT *)a.type_emb, (size_t)tok_k[r] * D + j);
+    }
+    xs[r * LX + j] = v;
+  }
+  lds_barrier();
+  const float *hvec = vec + a.L * (9 * D + F);
+  for (int ly = 0; ly < a.L; ++ly) {
+    const FusedLayerW &w = a.layer[ly];
+    const float *lv = vec + ly * (9 * D + F);
+    const float *ln1_g = lv, *ln1_b = lv + D, *qkv_b = lv + 2 * D, *out_b = lv + 5 * D, *ln2_g = lv + 6 * D,
+                *ln2_b = lv + 7 * D, *ffn1_b = lv + 8 * D, *ffn2_b = lv + 8 * D + F;
+    ELT *kc = (ELT *)(a.kc + a.layer_bytes * ly), *vc = (ELT *)(a.vc + a.layer_bytes * ly);
+    tile_layernorm<ELT>(xs, LX, as, LX, ln1_g, ln1_b, P, D);
+    lds_barrier();
+    tile_mm16(w_q, 3 * D, as, LX, [&](int r, int n, float y) {
+      if (r >= P) return;
+      const float v = rnd_act<ELT>(y + qkv_b[n]);
+      const int which = n / D, c = n - which * D;
+      if (which == 0) {
+        qs[r * LX + c] = v;
+      } else {
+        const int pos = pos0 + r, h = c >> 4, j = c & 15;
+        if (pos < a.cap)
+          st(which == 1 ? kc : vc, which == 1 ? (seq_row0 + (size_t)h * a.cap + pos) * DH + j
+                                                : v_at<ELT>(seq_row0 + (size_t)h * a.cap, pos, j, DH), v);
+        else
+          atomicOr(a.status, TPPSD_STATUS_CAPACITY);
+      }
+    });
+    __syncthreads();   // the new keys and values are in the cache
+    // (fp32 steps take twice the registers: two per load batch)
+    wg_attention<ELT, DH, 16, sizeof(ELT) == 4 ? 2 : 4>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, LX, red);
+    // at most two weight batches live at a time (512 threads: 256 registers)
+    WBatch<ELT, D, TO> w_o;
+    w_o.load((const ELT *)w.out_w, D);
+    lds_barrier();
+    WBatch<ELT, D, T1> w_f1;
+    w_f1.load((const ELT *)w.ffn1_w, F);
+    tile_mm16(w_o, D, os, LX, [&](int r, int n, float y) { xs[r * LX + n] += y + out_b[n]; });
+    lds_barrier();
+    tile_layernorm<ELT>(xs, LX, as, LX, ln2_g, ln2_b, P, D);
+    lds_barrier();
+    WBatch<ELT, F, TO> w_f2;
+    w_f2.load((const ELT *)w.ffn2_w, D);
+    tile_mm16(w_f1, F, as, LX,
+              [&](int r, int n, float y) { hs[r * LH + n] = rnd_act<ELT>(fmaxf(y + ffn1_b[n], 0.f)); });
+    lds_barrier();
+    tile_mm16(w_f2, D, hs, LH, [&](int r, int n, float y) { xs[r * LX + n] += y + ffn2_b[n]; });
+    if (ly + 1 < a.L)
+      w_q.load((const ELT *)a.layer[ly + 1].qkv_w, 3 * D);
+    else
+      w_q.load((const ELT *)a.Ek1_w, 4 * D);
+    lds_barrier();
+  }
+  // decoder on every row: LN_f, [E; V_k1] with tanh, the block-diagonal heads
+  tile_layernorm<ELT>(xs, LX, as, LX, hvec, hvec + D, P, D);
+  lds_barrier();
+  const float *k1_b = hvec + 2 * D, *head_b = hvec + 3 * D;
+  WBatch<ELT, 4 * D, TH> w_h;
+  w_h.load((const ELT *)a.head_w, 3 * a.M + a.K);
+  tile_mm16(w_q, 4 * D, as, LX, [&](int r, int n, float y) {
+    hs[r * LH + n] = n < 3 * D ? rnd_act<ELT>(y) : rnd_act<ELT>(tanhf(y + k1_b[n - 3 * D]));
+  });
+  lds_barrier();
+  tile_mm16(w_h, 3 * a.M + a.K, hs, LH, [&](int r, int n, float y) { hv[r * LV + n] = y + head_b[n]; });
+  lds_barrier();
+  for (int r = tid >> 6; r < P; r += blockDim.x >> 6) head_row(hv + r * LV, a.M, a.K, a.h, b, r);
+}
+
+static size_t verify_seq_lds_bytes(int L, int d, int F, int M, int K) {
+  const int LX = d + 4, LH = (F > 4 * d ? F : 4 * d) + 4, LV = 3 * M + K + 1;
+  return ((size_t)16 * (4 * LX + LH + LV) + 8 * 16 * (16 + 2) + verify_seq_vec_floats(L, d, F, M, K)) * sizeof(float);
+}
+
+bool verify_seq_ok(int bf16, int L, int d, int H, int F, int M, int K, int P) {
+  // instantiated widths, d_head 16, one 16-row tile, every product's column
+  // tiles inside one weight batch of the eight waves, default LDS limit.
+  // Taken for d = 32 (measured: the verify pass of the small fp32 workload
+  // 59 -> 36 us per round). At d = 64 the gain measured 8 % of the pass, and
+  // the layered pass keeps the verify attention a kernel of its own, whose
+  // KV bandwidth is reported; d = 64 stays layered.
+  const bool widths = d == 32 && (F == 64 || F == 128);
+  (void)bf16;
+  return widths && d == 16 * H && L <= FD_MAX_LAYERS && P <= 16 && 3 * M + K <= 128 * (d >= 64 ? 1 : 64 / d) &&
+         verify_seq_lds_bytes(L, d, F, M, K) <= 64 * 1024;
+}
+
+void launch_verify_seq(const VerifySeqArgs &a, int B, int bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const size_t lds = verify_seq_lds_bytes(a.L, a.d, a.F, a.M, a.K);
+  auto go = [&](auto kern) { hipExtLaunchKernelGGL(kern, dim3(B), dim3(512), lds, s, ev0, ev1, 0, a); };
+#define TPPSD_VS(ELT)                                               \
+  if (a.d == 32 && a.F == 64) go(k_verify_seq<ELT, 32, 64>);        \
+  else if (a.d == 32) go(k_verify_seq<ELT, 32, 128>);               \
+  else if (a.F == 128) go(k_verify_seq<ELT, 64, 128>);              \
+  else go(k_verify_seq<ELT, 64, 256>);
+  if (bf16) {
+    TPPSD_VS(bf16_t)
+  } else {
+    TPPSD_VS(float)
+  }
+#undef TPPSD_VS
 }
 
 // ---------------------------------------------------------------------------
