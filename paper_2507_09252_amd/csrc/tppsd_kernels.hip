@@ -971,6 +971,14 @@ template <> __device__ __forceinline__ void load8<bf16_t>(const bf16_t *p, float
   }
 }
 
+// Workgroup barrier that orders LDS only: global loads into registers and global
+// stores stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // y[p][n] = sum_k W(n)[k] X(n, p)[k] for n < N, p < P (P <= 2), handed to
 // epi(p, n, y) by one lane. K is cut into 8-element chunks; a row's chunks
 // are shared by LPR adjacent lanes (a power of two), CPL = K / (8 LPR) <= 8
@@ -1196,7 +1204,7 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
     const float mw = wave_max(m[p]);
     if (lane == 0) red[wave * 36 + p * 18] = mw;
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     if (p >= P) break;
@@ -1213,7 +1221,7 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
       for (int j = 0; j < DH; ++j) red[wave * 36 + p * 18 + 2 + j] = ow[j];
     }
   }
-  __syncthreads();
+  lds_barrier();
   for (int idx = tid; idx < P * H * DH; idx += blockDim.x) {
     const int p = idx / (H * DH), rest = idx - p * H * DH, hh = rest / DH, j = rest - hh * DH;
     float L = 0.f, O = 0.f;
@@ -1338,7 +1346,7 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
       for (int i = 0; i < 4; ++i) r[2 + 4 * g + i] = oacc[i];
     }
   }
-  __syncthreads();
+  lds_barrier();
   for (int idx = tid; idx < P * H * DH; idx += blockDim.x) {
     const int p = idx / (H * DH), rest = idx - p * H * DH, hh = rest / DH, j = rest - hh * DH;
     float M = -INFINITY;
@@ -1384,6 +1392,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
   __shared__ float tok_t[2], t_last;
   __shared__ int tok_k[2];
+  __shared__ float pu[TPPSD_MAX_GAMMA][4];   // the draws' uniforms, one Philox block per step
   const int d = a.d, F = a.F, M = a.M, K = a.K, H = a.H;
   const int Fm = d > F ? d : F;
   float *xs = sm;           // [2][d] residual stream
@@ -1457,6 +1466,12 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
   const size_t seq_row0 = (size_t)b * H * a.cap;
   const ELT *wtype = (const ELT *)a.type_emb;
   if (tid == 0) t_last = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+  if (tid < a.gamma) {   // the uniforms depend only on the counters: drawn up front, off the step chain
+    float u[4];
+    philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)(tid + 1), TAG_DRAFT, u);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pu[tid][i] = u[i];
+  }
   for (int l = 1; l <= a.gamma; ++l) {
     const int P = (l == 1) ? 2 : 1;
     const int pos0 = (l == 1) ? base : base + l;
@@ -1465,14 +1480,14 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
       tok_t[tid] = a.ev_t[i];
       tok_k[tid] = a.ev_k[i];
     }
-    __syncthreads();
+    lds_barrier();
     for (int i = tid; i < P * d; i += blockDim.x) {
       const int p = i / d, j = i - p * d;
       const float arg = tok_t[p] * freq[j];
       const int kk = min(max(tok_k[p], 0), K - 1);
       xs[i] = ((j & 1) ? cosf(arg) : sinf(arg)) + ld(wtype, (size_t)kk * d + j);
     }
-    __syncthreads();
+    lds_barrier();
     for (int ly = 0; ly < a.L; ++ly) {
       const FusedLayerW &w = a.layer[ly];
       ELT *kc = (ELT *)(a.kc + a.layer_bytes * ly);
@@ -1481,7 +1496,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
       const float *ln1_g = lv, *ln1_b = lv + d, *qkv_b = lv + 2 * d, *out_b = lv + 5 * d, *ln2_g = lv + 6 * d,
                   *ln2_b = lv + 7 * d, *ffn1_b = lv + 8 * d, *ffn2_b = lv + 8 * d + F;
       wg_layernorm<ELT>(xs, as, ln1_g, ln1_b, P, d);
-      __syncthreads();
+      lds_barrier();
       const ELT *wq = wmat(w.qkv_w, ly * LS);
       wg_gemv_cpl<ELT, CD>(
           3 * d, d, P, [&](int nn) { return wq + (size_t)nn * d; }, [&](int, int p) { return as + p * d; },
@@ -1499,42 +1514,42 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
                 atomicOr(a.status, TPPSD_STATUS_CAPACITY);
             }
           });
-      __syncthreads();
+      __syncthreads();   // keys and values in the cache before the attention reads them
       if (H <= 4 && !a.attn_mfma)
         wg_attention_valu<ELT>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       else
         wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
-      __syncthreads();
+      lds_barrier();
       const ELT *wo = wmat(w.out_w, ly * LS + (size_t)3 * d * d);
       wg_gemv_cpl<ELT, CD>(
           d, d, P, [&](int nn) { return wo + (size_t)nn * d; }, [&](int, int p) { return os + p * d; },
           [&](int p, int nn, float acc) { xs[p * d + nn] += acc + out_b[nn]; });
-      __syncthreads();
+      lds_barrier();
       wg_layernorm<ELT>(xs, as, ln2_g, ln2_b, P, d);
-      __syncthreads();
+      lds_barrier();
       const ELT *w1 = wmat(w.ffn1_w, ly * LS + (size_t)4 * d * d);
       const ELT *w2 = wmat(w.ffn2_w, ly * LS + (size_t)4 * d * d + (size_t)F * d);
       wg_gemv_cpl<ELT, CD>(
           F, d, P, [&](int nn) { return w1 + (size_t)nn * d; }, [&](int, int p) { return as + p * d; },
           [&](int p, int nn, float acc) { hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + ffn1_b[nn], 0.f)); });
-      __syncthreads();
+      lds_barrier();
       wg_gemv_cpl<ELT, CF>(
           d, F, P, [&](int nn) { return w2 + (size_t)nn * F; }, [&](int, int p) { return hs + p * F; },
           [&](int p, int nn, float acc) { xs[p * d + nn] += acc + ffn2_b[nn]; });
-      __syncthreads();
+      lds_barrier();
     }
     // decoder on the last token: e = E h and tanh(V_k1 h + b1) in one pass,
     // then the mixture (w, mu, log sigma from the slices of e) and type
     // logits in one pass
     wg_layernorm<ELT>(xs + (P - 1) * d, as, lnf_g, lnf_b, 1, d);
-    __syncthreads();
+    lds_barrier();
     const ELT *we = wmat(a.Ek1_w, a.L * LS);
     wg_gemv_cpl<ELT, CD>(
         4 * d, d, 1, [&](int nn) { return we + (size_t)nn * d; }, [&](int, int) { return (const float *)as; },
         [&](int, int nn, float acc) {
           es[nn] = (nn < 3 * d) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * d]));
         });
-    __syncthreads();
+    lds_barrier();
     const ELT *mw = wmat(a.mix_w, a.L * LS + (size_t)4 * d * d);
     const ELT *kw = wmat(a.k2_w, a.L * LS + (size_t)4 * d * d + (size_t)3 * M * d);
     wg_gemv_cpl<ELT, CD>(
@@ -1542,7 +1557,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
         [&](int nn) { return nn < 3 * M ? mw + (size_t)nn * d : kw + (size_t)(nn - 3 * M) * d; },
         [&](int nn, int) { return (const float *)(es + (nn < 3 * M ? nn / M : 3) * d); },
         [&](int, int nn, float acc) { hv[nn] = acc + (nn < 3 * M ? mix_b[nn] : k2_b[nn - 3 * M]); });
-    __syncthreads();
+    lds_barrier();
     if (tid < 64) {
       const int lane = tid;
       const float lw = lane < M ? hv[lane] : -INFINITY;
@@ -1554,14 +1569,13 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
       if (lane < M) hv[lane] = lw - mw2 - logf(sw);
       if (lane < K) hv[3 * M + lane] = lk - mk - logf(sk);
     }
-    __syncthreads();
+    lds_barrier();
     const size_t di = (size_t)b * a.MG + (l - 1);
     for (int i = tid; i < 3 * M; i += blockDim.x) a.d_mix[di * 3 * M + i] = hv[i];
     for (int i = tid; i < K; i += blockDim.x) a.d_logtype[di * K + i] = hv[3 * M + i];
     if (tid < 64) {
       // the draft event, drawn by wave 0: component, Box-Muller interval, type
-      float u[4];
-      philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)l, TAG_DRAFT, u);
+      const float *u = pu[l - 1];
       const int z = wave_sample_cat(hv, M, u[0]);
       const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
       const float tau = expf(hv[M + z] + expf(hv[2 * M + z]) * eps);
@@ -1580,7 +1594,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
         t_last = tn;
       }
     }
-    __syncthreads();
+    lds_barrier();
   }
 }
 
@@ -1633,14 +1647,6 @@ int allow_draft_fused_lds(size_t bytes) {
 // read from global memory (a few hundred KB: L2-resident). The rounding points
 // are those of the layered kernels.
 // ---------------------------------------------------------------------------
-
-// Workgroup barrier that orders LDS only: global loads into registers (the
-// next product's weights) stay in flight across it.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 // The weights one wave needs for a 16-row product Y = X W^T (W [N][K]
 // row-major): its 16-column tiles wave, wave + nw, ..., at most TPW of them
