@@ -9,6 +9,7 @@ value = B * n_gen * steps / (timed seconds). The same job with naive AR
 sampling gives the speedup denominator.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c2] [--gamma G]
+                    [--gamma-sweep 1,2,5,10,15,20]
 """
 from __future__ import annotations
 
@@ -41,8 +42,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-poisson", action="store_true", help="skip the homogeneous-Poisson draft run")
     ap.add_argument("--no-window", action="store_true", help="skip the end-time (window) runs")
-    ap.add_argument("--cpu-events", type=int, default=64, help="oracle sample: events per sequence")
-    ap.add_argument("--cpu-seqs", type=int, default=4, help="oracle sample: sequences")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="oracle sample: target CPU seconds")
+    ap.add_argument("--cpu-seqs", type=int, default=64, help="oracle sample: at most this many sequences")
+    ap.add_argument("--gamma-sweep", default=None,
+                    help="comma-separated draft lengths: the SD job at each, against the same AR job")
     return ap.parse_args()
 
 
@@ -92,6 +95,68 @@ def verify_pass_fraction(wl, gamma, B, verify_ms):
             "tflops": flop / (verify_ms * 1e-3) / 1e12 if verify_ms else None}
 
 
+def verify_gemm_bytes(wl, gamma, B):
+    """Algorithmic HBM bytes of the GEMM launches of one verify pass (every
+    layer's products and the decoder's first one, the launches timed as
+    verify GEMMs): each operand read once, each output written once. THP
+    layer: q, k, v from the LayerNorm's fp32 input; output projection and
+    second FFN product read-modify-write the fp32 residual; the FFN hidden
+    goes out and back. AttNHP layer: one product over the 2d-wide [z; h]."""
+    c = wl.target
+    elt = 2 if c.prec == "bf16" else 4
+    d, F, L = c.d_model, c.d_ffn, c.n_layers
+    T = B * (gamma + 1)
+    if getattr(c, "encoder", "thp") == "attnhp":
+        layer = T * 2 * d * elt + 6 * d * d * elt + T * 3 * d * elt
+    else:
+        qkv = T * d * 4 + 3 * d * d * elt + T * 3 * d * elt
+        out = T * d * elt + d * d * elt + T * d * 8
+        ffn1 = T * d * 4 + d * F * elt + T * F * elt
+        ffn2 = T * F * elt + F * d * elt + T * d * 8
+        layer = qkv + out + ffn1 + ffn2
+    dec = T * d * 4 + 4 * d * d * elt + T * 4 * d * elt
+    return float(L * layer + dec)
+
+
+def gamma_sweep(args, wl, tm, dm, HT, HK, ar_value, B, n_gen):
+    """The SD job at each draft length of the sweep (one state per length,
+    one warmup job, args.steps timed jobs), against the AR job's rate."""
+    import torch
+
+    from paper_2507_09252_amd import tppsd as tp
+    rows = []
+    for g in [int(x) for x in args.gamma_sweep.split(",") if x.strip()]:
+        st = tp.State(tm, dm, B, wl.n_hist + n_gen + g + 1, g, seed=1234)
+
+        def job():
+            st.tppsd_prefill(HT, HK, n_gen)
+            return st.tppsd_sample_sd(g)
+
+        job()
+        torch.cuda.synchronize()
+        rounds = 0
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            rounds += job()
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        s = st.tppsd_state_status()
+        assert s["bits"] == 0 and s["n_done"] == B, s
+        st.tppsd_timing_enable(tp.TIME_PHASES)
+        job()
+        ph = st.tppsd_timing_read()
+        st.tppsd_timing_enable(0)
+        nr = max(1, ph["rounds"])
+        value = B * n_gen * args.steps / dt
+        rows.append({"gamma": g, "value": value, "speedup_vs_gpu_ar": value / ar_value if ar_value else None,
+                     "alpha": s["accepted"] / max(1, s["drafted"]), "rounds_per_job": rounds / args.steps,
+                     "round_us": {"draft": ph["draft_ms"] * 1e3 / nr, "verify": ph["verify_ms"] * 1e3 / nr,
+                                  "accept": ph["accept_ms"] * 1e3 / nr}})
+        print(f"gamma {g}: {value:.4g} events/s, alpha {rows[-1]['alpha']:.3f}", file=sys.stderr, flush=True)
+        del st
+    return rows
+
+
 def attention_source_sha256():
     """SHA-256 over the sources that define the attention kernels."""
     import hashlib
@@ -115,17 +180,31 @@ def measured_traffic(wl_name):
     return None if w is None else w["traffic_bytes_per_launch"]
 
 
-def cpu_baseline(wl, gamma, wt, wd, ht, hk, n_seq, n_events):
-    """The oracle (float64 NumPy, one thread) on a bounded sample of the same job."""
+def cpu_baseline(wl, gamma, wt, wd, ht, hk, budget_s, max_seqs):
+    """The oracle (float64 NumPy, one thread) on a bounded sample of the same
+    job, sized to about budget_s seconds of CPU work: starting from 8
+    sequences x 16 events, the sample grows (events per sequence first, up to
+    n_gen, then sequences, up to max_seqs) by the ratio of the budget to the
+    last run's time, until a run takes at least half the budget or the sample
+    is the whole allowed job. The last run is reported."""
     from threadpoolctl import threadpool_limits
 
     from oracle import sampler as S
     from oracle.model import Model as OModel
     T, D = OModel(wl.target, wt), OModel(wl.draft, wd)
+    top_seq = max(1, min(wl.batch, max_seqs))
+    n_seq, n_events = min(top_seq, 8), min(wl.n_gen, 16)
     with threadpool_limits(1):
-        t0 = time.perf_counter()
-        st = S.sample_sd(T, D, ht[:n_seq], hk[:n_seq], n_events, gamma, seed=1234)
-        dt = time.perf_counter() - t0
+        for _ in range(6):
+            t0 = time.perf_counter()
+            st = S.sample_sd(T, D, ht[:n_seq], hk[:n_seq], n_events, gamma, seed=1234)
+            dt = time.perf_counter() - t0
+            if dt >= 0.5 * budget_s or (n_seq == top_seq and n_events == wl.n_gen):
+                break
+            grow = min(8.0, budget_s / max(dt, 1e-3))
+            e2 = int(min(wl.n_gen, n_events * grow))
+            n_seq = int(min(top_seq, max(n_seq, n_seq * grow * n_events / e2)))
+            n_events = e2
     ev = int(st.gen.sum())
     return {"value": ev / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
             "sample": f"{n_seq} sequences x first {n_events} generated events of {wl.name} "
@@ -317,9 +396,15 @@ def main():
     c = wl.target
     gemm_tflops = tk["gemm_flop"] / (tk["gemm_ms"] * 1e-3) / 1e12 if tk["gemm_ms"] else 0.0
     gemm_peak = MFMA_PEAK_TFLOPS[c.prec]
+    # (a one-launch verify pass has no separate GEMM launches to price)
+    layered = kernel_name == KERNEL_NAME[wl.prec]
+    gemm_gbs = (verify_gemm_bytes(wl, gamma, B) * tk["rounds"] / (tk["gemm_ms"] * 1e-3) / 1e9
+                if tk["gemm_ms"] and layered else None)
     out["verify_gemm"] = {"bound": "mfma", "achieved": gemm_tflops, "peak": gemm_peak, "unit": "TFLOP/s",
                           "frac": gemm_tflops / gemm_peak, "launches": tk["gemm_launches"],
-                          "avg_launch_us": tk["gemm_ms"] * 1e3 / max(1, tk["gemm_launches"])}
+                          "avg_launch_us": tk["gemm_ms"] * 1e3 / max(1, tk["gemm_launches"]),
+                          "hbm_achieved_gbs": gemm_gbs,
+                          "hbm_frac": gemm_gbs / HBM_PEAK_GBS if gemm_gbs is not None else None}
     nr = max(1, tph["rounds"])
     out["round_us"] = {"draft": tph["draft_ms"] * 1e3 / nr, "verify": tph["verify_ms"] * 1e3 / nr,
                        "accept": tph["accept_ms"] * 1e3 / nr, "rounds": tph["rounds"]}
@@ -327,9 +412,10 @@ def main():
     if poisson is not None:
         poisson["speedup_vs_gpu_ar"] = poisson["value"] / ar_value if ar_value else None
         out["poisson_draft"] = poisson
+    if args.gamma_sweep:
+        out["gamma_sweep"] = gamma_sweep(args, wl, tm, dm, HT, HK, ar_value, B, n_gen)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, gamma, wt, wd, ht, hk, min(args.cpu_seqs, B),
-                                           min(args.cpu_events, n_gen))
+        out["cpu_baseline"] = cpu_baseline(wl, gamma, wt, wd, ht, hk, args.cpu_seconds, args.cpu_seqs)
     print(json.dumps(out), flush=True)
 
 
