@@ -385,6 +385,7 @@ def main():
         "alpha": alpha,
         "events_per_round": events * args.steps / max(1, rounds),
         "rounds_per_job": rounds / args.steps,
+        "ar_candidates_per_job": st["ar_candidates"],
         "roofline": {"bound": "hbm", "kernel": kernel_name, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(wl.name) if kernel_name == KERNEL_NAME[wl.prec] else None,

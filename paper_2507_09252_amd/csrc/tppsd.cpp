@@ -273,7 +273,7 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   const size_t Bz = (size_t)B;
   w.status = take(4);
   w.n_done = take(4);
-  w.acc = take(3 * 8);
+  w.acc = take((size_t)B * 3 * 8);   // per-sequence counters: accepted drafts, drafted, A-R candidates
   w.n = take(Bz * 4);
   w.gen = take(Bz * 4);
   w.lenT = take(Bz * 4);
@@ -1430,12 +1430,17 @@ int tppsd_state_status(tppsd_state *s, hipStream_t st, uint32_t *bits, int32_t *
   if (!s) return fail(TPPSD_E_ARG, "null state");
   uint32_t b = 0;
   int32_t nd = 0;
-  unsigned long long acc[3] = {0, 0, 0};
+  // the counters are per sequence (each owned by one wave of the accept
+  // kernel, so no atomics on shared addresses); summed here
+  std::vector<unsigned long long> per((size_t)s->B * 3);
   if (hipMemcpyAsync(&b, s->status, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
       hipMemcpyAsync(&nd, s->n_done, 4, hipMemcpyDeviceToHost, st) != hipSuccess ||
-      hipMemcpyAsync(acc, s->acc_stats, sizeof acc, hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(per.data(), s->acc_stats, per.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost,
+                     st) != hipSuccess ||
       hipStreamSynchronize(st) != hipSuccess)
     return hip_check("tppsd_state_status");
+  unsigned long long acc[3] = {0, 0, 0};
+  for (size_t i = 0; i < per.size(); ++i) acc[i % 3] += per[i];
   if (bits) *bits = b;
   if (n_done) *n_done = nd;
   if (accepted) *accepted = (int64_t)acc[0];

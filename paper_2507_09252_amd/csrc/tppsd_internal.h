@@ -102,7 +102,7 @@ struct AcceptArgs {
   double *ll;               // [B] model log-likelihood of the generated events (Eq. (2))
   uint64_t seed;
   uint32_t *status;
-  unsigned long long *acc_stats;   // [3]: accepted drafts, drafted, A-R candidates
+  unsigned long long *acc_stats;   // [B][3]: per sequence accepted drafts, drafted, A-R candidates
 };
 
 // Fused drafting: one workgroup per sequence runs all gamma draft steps.

@@ -2193,13 +2193,35 @@ void launch_verify_seq(const VerifySeqArgs &a, int B, int bf16, hipStream_t s, h
 // Eq. (3)-(4), Theorem 1, Algorithm 1). One wave per sequence.
 // ---------------------------------------------------------------------------
 
+// value of v in lane i (i uniform across the wave)
+__device__ __forceinline__ float lane_f(float v, int i) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
+}
+
 __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   __shared__ float acc_pre[4][8 * 64];   // per wave: staged mixture terms (Theorem-1 loop)
   const int lane = threadIdx.x & 63;
   const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (b >= a.B) return;
   const int G = a.gamma, MG = a.max_gamma, M = a.M, K = a.K;
-  if (a.done[b]) {
+  // every per-sequence scalar the kernel needs is loaded at once, and so is
+  // the draft record of position lane (lane < G): the commit below reads it
+  // from registers, so no load waits on another after this point except the
+  // last committed time, which needs n
+  const int is_done = a.done[b], rnd_b = a.rnd[b], n = a.n[b], gen = a.gen[b];
+  const float T_end = a.t_end[b];
+  float my_tau = 0.f, my_lg = 0.f, my_lf = 0.f, my_dg = 0.f, my_df = 0.f;
+  int my_k = 0;
+  if (lane < G) {
+    const size_t i = (size_t)b * MG + lane;
+    my_tau = a.d_tau[i];
+    my_k = a.d_k[i];
+    my_lg = a.v_logg[i];
+    my_lf = a.v_logf[i];
+    my_dg = a.d_logg[i];
+    my_df = a.d_logf[i];
+  }
+  if (is_done) {
     if (lane == 0) {
       a.L[b] = 0;
       a.n_new[b] = 0;
@@ -2208,7 +2230,8 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     }
     return;
   }
-  const uint64_t r = (uint64_t)a.rnd[b];
+  const float t_last = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+  const uint64_t r = (uint64_t)rnd_b;
   // verification tests: ln u < log p_T - log p_D for the interval and the type
   int pass_t = 1, pass_k = 1;
   if (lane < G) {
@@ -2222,9 +2245,8 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       ut = u[0];
       uk = u[1];
     }
-    const size_t i = (size_t)b * MG + lane;
-    pass_t = logf(ut) < a.v_logg[i] - a.d_logg[i];
-    pass_k = logf(uk) < a.v_logf[i] - a.d_logf[i];
+    pass_t = logf(ut) < my_lg - my_dg;
+    pass_k = logf(uk) < my_lf - my_df;
   }
   const uint64_t fail = __ballot(lane < G && !(pass_t && pass_k));
   const int L = fail ? __ffsll((unsigned long long)fail) : G + 1;
@@ -2325,8 +2347,8 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       }
       flags |= 1;
     } else {
-      tauL = a.d_tau[(size_t)b * MG + li];
-      lgL = a.v_logg[(size_t)b * MG + li];
+      tauL = lane_f(my_tau, li);
+      lgL = lane_f(my_lg, li);
     }
     if (!ak) {
       // Eq. (4): k ~ norm(max(0, f_T - f_D)), lane kk holding type kk
@@ -2334,7 +2356,8 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       philox_uniforms(a.seed, (uint64_t)b, r, 0ull, TAG_RES_K, u);
       const float *lT = a.v_logtype + ((size_t)b * (MG + 1) + li) * K;
       const float *lD = a.d_logtype + ((size_t)b * MG + li) * K;
-      float c = lane < K ? fmaxf(0.f, expf(lT[lane]) - expf(lD[lane])) : 0.f;
+      const float lt_k = lane < K ? lT[lane] : 0.f;
+      float c = lane < K ? fmaxf(0.f, expf(lt_k) - expf(lD[lane])) : 0.f;
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
         const float o = __shfl_up(c, off, 64);
@@ -2343,11 +2366,13 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       const float tot = __shfl(c, K - 1, 64);
       const unsigned long long hit = __ballot(lane < K && u[0] * tot < c);
       kL = hit ? (int)__builtin_ctzll(hit) : K - 1;
+      lfL = lane_f(lt_k, kL);
       flags |= 2;
     } else {
-      kL = a.d_k[(size_t)b * MG + li];
+      // the draft's type, kept: its target log f is the verify pass's
+      kL = __builtin_amdgcn_readlane(my_k, li);
+      lfL = lane_f(my_lf, li);
     }
-    lfL = a.v_logtype[((size_t)b * (MG + 1) + li) * K + kL];
   } else if (a.bonus) {
     const float *Tr = a.v_mix + ((size_t)b * (MG + 1) + G) * 3 * M;
     float u[4];
@@ -2363,19 +2388,17 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   // exactly at T is kept and ends the sequence). Every lane runs the loop so
   // that the survival term below can use the whole wave; lane 0 writes.
   const int count = (L <= G) ? L : (a.bonus ? G + 1 : G);
-  const int n = a.n[b], gen = a.gen[b];
   const int room = a.n_gen - gen;
-  const float T_end = a.t_end[b];
   const bool last_is_new = (L <= G) || a.bonus;
-  float tp = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+  float tp = t_last;
   int nn = 0, stop_row = -1;
   bool stopped = false;
   float x_surv = 0.f;
   double ll = 0.0;
   for (int i = 0; i < count; ++i) {
     const bool is_new = i == count - 1 && last_is_new;
-    const float ti = is_new ? tauL : a.d_tau[(size_t)b * MG + i];
-    const int ki = is_new ? kL : a.d_k[(size_t)b * MG + i];
+    const float ti = is_new ? tauL : lane_f(my_tau, i);
+    const int ki = is_new ? kL : __builtin_amdgcn_readlane(my_k, i);
     const float tprev = tp;
     tp = tp + ti;
     const size_t oi = (size_t)b * (MG + 1) + i;
@@ -2400,8 +2423,7 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       }
     }
     // Eq. (2): the target's log-density of the committed event (verify row i)
-    ll += is_new ? (double)lgL + (double)lfL
-                 : (double)a.v_logg[(size_t)b * MG + i] + (double)a.v_logf[(size_t)b * MG + i];
+    ll += is_new ? (double)lgL + (double)lfL : (double)lane_f(my_lg, i) + (double)lane_f(my_lf, i);
     ++nn;
     if (tp >= T_end) stopped = true;   // exactly at T: survival of a zero interval adds log 1
   }
@@ -2431,9 +2453,12 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   a.n_new[b] = nn;
   a.flags[b] = (uint8_t)flags;
   a.ar_iter[b] = ar_j;
-  atomicAdd(&a.acc_stats[0], (unsigned long long)(L - 1));
-  atomicAdd(&a.acc_stats[1], (unsigned long long)G);
-  atomicAdd(&a.acc_stats[2], (unsigned long long)(ar_j >= 0 ? ar_j + 1 : 0));
+  // per-sequence counters: this wave owns sequence b (a shared counter
+  // updated by every wave serialises thousands of atomics on one address)
+  unsigned long long *cs = a.acc_stats + 3 * (size_t)b;
+  cs[0] += (unsigned long long)(L - 1);
+  cs[1] += (unsigned long long)G;
+  cs[2] += (unsigned long long)(ar_j >= 0 ? ar_j + 1 : 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -2462,11 +2487,9 @@ __global__ void k_prefill_init(const float *ht, const int32_t *hk, int B, int n0
     rnd[idx] = 0;
     zeros[idx] = 0;
     ll[idx] = 0.0;
+    acc_stats[3 * idx] = acc_stats[3 * idx + 1] = acc_stats[3 * idx + 2] = 0ull;
   }
-  if (idx == 0) {
-    *status = 0u;
-    acc_stats[0] = acc_stats[1] = acc_stats[2] = 0ull;
-  }
+  if (idx == 0) *status = 0u;
 }
 
 // n_done = number of sequences done at the start (one workgroup)
