@@ -2190,7 +2190,10 @@ void launch_verify_seq(const VerifySeqArgs &a, int B, int bf16, hipStream_t s, h
 
 // ---------------------------------------------------------------------------
 // accept / reject, adjusted-distribution replacement and commit (§4.3,
-// Eq. (3)-(4), Theorem 1, Algorithm 1). One wave per sequence.
+// Eq. (3)-(4), Theorem 1, Algorithm 1). One workgroup per sequence: its four
+// waves run the same per-sequence steps (their results agree lane for lane;
+// wave 0 writes them), and share Theorem 1's candidates, 256 per step, so a
+// long acceptance-rejection loop takes a quarter of the steps.
 // ---------------------------------------------------------------------------
 
 // value of v in lane i (i uniform across the wave)
@@ -2200,8 +2203,11 @@ __device__ __forceinline__ float lane_f(float v, int i) {
 
 __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   __shared__ float acc_pre[4][8 * 64];   // per wave: staged mixture terms (Theorem-1 loop)
-  const int lane = threadIdx.x & 63;
-  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  __shared__ int ar_win[4];              // per wave: its lowest accepted candidate (INT_MAX: none)
+  __shared__ float ar_tau[4], ar_lg[4];  // ... and that candidate's tau and target log g
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const bool writer = threadIdx.x == 0;
+  const int b = blockIdx.x;
   if (b >= a.B) return;
   const int G = a.gamma, MG = a.max_gamma, M = a.M, K = a.K;
   // every per-sequence scalar the kernel needs is loaded at once, and so is
@@ -2222,7 +2228,7 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     my_df = a.d_logf[i];
   }
   if (is_done) {
-    if (lane == 0) {
+    if (writer) {
       a.L[b] = 0;
       a.n_new[b] = 0;
       a.flags[b] = 16;
@@ -2232,9 +2238,11 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   }
   const float t_last = a.ev_t[(size_t)b * a.ev_stride + n - 1];
   const uint64_t r = (uint64_t)rnd_b;
-  // verification tests: ln u < log p_T - log p_D for the interval and the type
+  // verification tests: ln u < log p_T - log p_D for the interval and the
+  // type, by wave 0; L and the two outcomes at L go to the other waves
+  __shared__ int s_res[3];
   int pass_t = 1, pass_k = 1;
-  if (lane < G) {
+  if (wave == 0 && lane < G) {
     float ut, uk;
     if (a.uniforms) {
       ut = a.uniforms[((size_t)b * MG + lane) * 2];
@@ -2248,13 +2256,22 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     pass_t = logf(ut) < my_lg - my_dg;
     pass_k = logf(uk) < my_lf - my_df;
   }
-  const uint64_t fail = __ballot(lane < G && !(pass_t && pass_k));
-  const int L = fail ? __ffsll((unsigned long long)fail) : G + 1;
-  int at = 1, ak = 1;
-  if (L <= G) {
-    at = __shfl(pass_t, L - 1, 64);
-    ak = __shfl(pass_k, L - 1, 64);
+  if (wave == 0) {
+    const uint64_t fail = __ballot(lane < G && !(pass_t && pass_k));
+    const int L0 = fail ? __ffsll((unsigned long long)fail) : G + 1;
+    // (the lane reads run on the whole wave, before the lane-0 branch)
+    const int at0 = L0 <= G ? __builtin_amdgcn_readlane(pass_t, L0 - 1) : 1;
+    const int ak0 = L0 <= G ? __builtin_amdgcn_readlane(pass_k, L0 - 1) : 1;
+    if (lane == 0) {
+      s_res[0] = L0;
+      s_res[1] = at0;
+      s_res[2] = ak0;
+    }
   }
+  __syncthreads();
+  const int L = s_res[0], at = s_res[1], ak = s_res[2];
+  // waves 1-3 only draw Theorem 1's candidates
+  if (wave != 0 && !(L <= G && !at)) return;
   float tauL = 0.f;
   float lgL = 0.f, lfL = 0.f;   // target log g, log f of the event drawn at L (or the bonus event)
   int kL = 0, ar_j = -1, flags = 0;
@@ -2269,8 +2286,8 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     const float *Dr = pois ? nullptr : a.d_mix + ((size_t)b * MG + li) * 3 * M;
     if (!at) {
       // Theorem 1: candidates tau ~ g_T, accept iff u_a < 1 - exp(-(log g_T - log g_D));
-      // candidate j = base + lane, the lowest accepted index wins. Per
-      // component m the wave first stages, in LDS, the terms that do not
+      // candidate j = base + 64 wave + lane, the lowest accepted index wins.
+      // Per component m each wave first stages, in LDS, the terms that do not
       // depend on tau: log w_m - log sigma_m - log sqrt(2 pi), exp(-2 log
       // sigma_m), mu_m, sigma_m for both mixtures and the running sum of w_m
       // of the target; each lane then evaluates its candidate from LDS.
@@ -2312,14 +2329,15 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
         }
         return mx + logf(acc);
       };
-      for (int base = 0;; base += 64) {
+      for (int base = 0;; base += 256) {
         if (base >= TPPSD_AR_ITER_CAP) {
-          if (lane == 0) atomicOr(a.status, TPPSD_STATUS_AR_CAP);
+          if (writer) atomicOr(a.status, TPPSD_STATUS_AR_CAP);
           ar_j = TPPSD_AR_ITER_CAP;
           break;
         }
         float u[4];
-        philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)(base + lane), TAG_RES_T, u);
+        const int jw = 64 * wave + lane;   // this lane's candidate: base + jw
+        philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)(base + jw), TAG_RES_T, u);
         const float x = u[0] * tot;
         int z = M - 1;
         for (int m = 0; m < M; ++m)
@@ -2334,22 +2352,36 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
         const float lgt = logpdf(Ta, Te, Tm, lt);
         const float delta = lgt - lgd;
         const bool acc = delta > 0.f && u[3] < -expm1f(-delta);
+        // the lowest accepted index of the step wins: each wave posts its
+        // first, then every wave reads the four (uniform across the group)
         const uint64_t m = __ballot(acc);
-        if (m) {
-          const int jl = __ffsll((unsigned long long)m) - 1;
-          tauL = __shfl(tau, jl, 64);
-          lgL = __shfl(lgt, jl, 64);
-          ar_j = base + jl;
+        const int jl = m ? __ffsll((unsigned long long)m) - 1 : 0;
+        if (lane == 0) ar_win[wave] = m ? 64 * wave + jl : INT_MAX;
+        if (m && lane == jl) {
+          ar_tau[wave] = tau;
+          ar_lg[wave] = lgt;
+        }
+        if (!m && wave == 3 && lane == 63) {   // the step's last candidate, kept if the cap ends the loop
+          ar_tau[3] = tau;
+          ar_lg[3] = lgt;
+        }
+        __syncthreads();
+        const int best = min(min(ar_win[0], ar_win[1]), min(ar_win[2], ar_win[3]));
+        const int bw = best == INT_MAX ? 3 : best >> 6;
+        tauL = ar_tau[bw];
+        lgL = ar_lg[bw];
+        __syncthreads();   // read before the next step posts
+        if (best != INT_MAX) {
+          ar_j = base + best;
           break;
         }
-        tauL = __shfl(tau, 63, 64);
-        lgL = __shfl(lgt, 63, 64);
       }
       flags |= 1;
     } else {
       tauL = lane_f(my_tau, li);
       lgL = lane_f(my_lg, li);
     }
+    if (wave != 0) return;   // the rest is wave 0's
     if (!ak) {
       // Eq. (4): k ~ norm(max(0, f_T - f_D)), lane kk holding type kk
       float u[4];
@@ -2386,7 +2418,7 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   // commit in order: at most n_gen - gen events, and none past the end time
   // (Algorithm 1 samples while t < T and drops events with t > T; an event
   // exactly at T is kept and ends the sequence). Every lane runs the loop so
-  // that the survival term below can use the whole wave; lane 0 writes.
+  // that the survival term below can use the whole wave; thread 0 writes.
   const int count = (L <= G) ? L : (a.bonus ? G + 1 : G);
   const int room = a.n_gen - gen;
   const bool last_is_new = (L <= G) || a.bonus;
@@ -2402,7 +2434,7 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     const float tprev = tp;
     tp = tp + ti;
     const size_t oi = (size_t)b * (MG + 1) + i;
-    if (lane == 0) {
+    if (writer) {
       a.t_new[oi] = tp;
       a.tau_new[oi] = ti;
       a.k_new[oi] = ki;
@@ -2414,7 +2446,7 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       x_surv = T_end - tprev;
       continue;
     }
-    if (lane == 0) {
+    if (writer) {
       if (n + nn < a.ev_stride) {
         a.ev_t[(size_t)b * a.ev_stride + n + nn] = tp;
         a.ev_k[(size_t)b * a.ev_stride + n + nn] = ki;
@@ -2434,7 +2466,7 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
     ll += (double)wave_log_survival(v ? Sr[lane] : 0.f, v ? Sr[M + lane] : 0.f, v ? Sr[2 * M + lane] : 0.f, v,
                                     x_surv);
   }
-  if (lane != 0) return;
+  if (!writer) return;
   if (last_is_new && !isfinite(tauL)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
   const int n2 = n + nn, g2 = gen + nn;
   a.n[b] = n2;
@@ -2453,7 +2485,7 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
   a.n_new[b] = nn;
   a.flags[b] = (uint8_t)flags;
   a.ar_iter[b] = ar_j;
-  // per-sequence counters: this wave owns sequence b (a shared counter
+  // per-sequence counters: this workgroup owns sequence b (a shared counter
   // updated by every wave serialises thousands of atomics on one address)
   unsigned long long *cs = a.acc_stats + 3 * (size_t)b;
   cs[0] += (unsigned long long)(L - 1);
@@ -2635,7 +2667,7 @@ void launch_build_head(const void *mix_w, const void *k2_w, const float *mix_b, 
                                                   (float *)hw, hb);
 }
 
-void launch_accept(const AcceptArgs &a, hipStream_t s) { k_accept<<<(a.B + 3) / 4, 256, 0, s>>>(a); }
+void launch_accept(const AcceptArgs &a, hipStream_t s) { k_accept<<<a.B, 256, 0, s>>>(a); }
 
 void launch_prefill_init(const float *ht, const int32_t *hk, int B, int n0, int n_gen, const float *t_end_in,
                          float *ev_t, int32_t *ev_k, int ev_stride, int32_t *n, int32_t *gen, int32_t *lenT,
