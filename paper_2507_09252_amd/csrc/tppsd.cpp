@@ -469,6 +469,12 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     }
     return TPPSD_OK;
   }
+  // the feed-forward block in one launch (hidden activations on chip) where
+  // there is an instance for the widths and the row tiles fill the chip;
+  // TPPSD_FFN_FUSED=0 / 1 forces the layered / fused form
+  const char *ff = getenv("TPPSD_FFN_FUSED");
+  const bool use_ffn_fused = fuse_ln && ffn_fused_ok(bf, d, m->cfg.d_ffn) &&
+                             (ff ? ff[0] == '1' : (long)T >= 256L * (d == 128 ? 64 : 32));
   if (!m->attnhp()) launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
   for (int l = 0; l < m->cfg.n_layers && !m->attnhp(); ++l) {
     const LayerW &w = m->layers[l];
@@ -498,6 +504,11 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     eo.out = s->x;
     eo.ldo = d;
     launch_gemm(s->o, nullptr, w.out_w, bf, T, d, d, eo, st, ev(L + 4 * l + 1, 0), ev(L + 4 * l + 1, 1));
+    if (use_ffn_fused) {
+      launch_ffn_fused(s->x, w.ln2_g, w.ln2_b, w.ffn1_w, w.ffn1_b, w.ffn2_w, w.ffn2_b, T, d, F, st,
+                       ev(L + 4 * l + 2, 0), ev(L + 4 * l + 2, 1));
+      continue;
+    }
     if (!fuse_ln) launch_layernorm(s->x, s->a, bf, w.ln2_g, w.ln2_b, T, d, st);
     Epi e1{};
     e1.mode = EPI_RELU;
@@ -1031,7 +1042,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
                      fused_draft_lds_bytes(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
                                            D->H()) +
                              fused_draft_weight_elems(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix,
-                                                      D->cfg.n_types) * wb <=
+                                                      D->cfg.n_types, 16 / wb) * wb <=
                          LDS_PER_WG - 4096;
     if (s->fused_w_lds && allow_draft_fused_lds(LDS_PER_WG - 4096)) {
       s->fused_w_lds = false;       // weights stay in global memory

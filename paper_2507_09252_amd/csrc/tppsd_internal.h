@@ -142,8 +142,9 @@ inline bool fused_draft_ok(int L, int d, int H, int F) {
          F / 8 <= 64 && pow2(H) && d == 16 * H;
 }
 size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H);
-// elements of the draft's weight matrices (per layer QKV, out, FFN; decoder)
-size_t fused_draft_weight_elems(int L, int d, int F, int M, int K);
+// elements of the draft's weight matrices (per layer QKV, out, FFN; decoder), each
+// row padded by pad elements (16 bytes) in LDS
+size_t fused_draft_weight_elems(int L, int d, int F, int M, int K, int pad);
 // LDS of one workgroup on gfx950
 constexpr size_t LDS_PER_WG = 160 * 1024;
 
@@ -242,6 +243,12 @@ void launch_gemm(const void *X, const LnA *ln, const void *W, int bf16, int T, i
                  hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // whether launch_gemm can take a LayerNorm operand of width K
 bool gemm_ln_fusable(int bf16, int K);
+// bf16 feed-forward block x += ReLU(LN(x) W1^T + b1) W2^T + b2 in one launch
+// (hidden activations kept on chip); false (nothing launched) for widths it
+// has no instance for
+bool launch_ffn_fused(float *x, const float *lg, const float *lb, const void *W1, const float *b1, const void *W2,
+                      const float *b2, int T, int d, int F, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
+bool ffn_fused_ok(int bf16, int d, int F);
 // decoder epilogue over the rows' logits [.., ldl] (mixture w | mu | log sigma, then types)
 void launch_head(const float *logits, int ldl, int M, int K, const HeadArgs &a, hipStream_t st);
 // the decoder's block-diagonal (3M + K) x 4d matrix and its bias (3M + K)

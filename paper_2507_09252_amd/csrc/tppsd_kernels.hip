@@ -629,6 +629,173 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
   }
 }
 
+// Workgroup barrier that orders LDS only: global loads into registers and global
+// stores stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// ---------------------------------------------------------------------------
+// Fused feed-forward block of a pre-LN THP layer (§4.2 encoder):
+// x += ReLU(LN2(x) W1^T + b1) W2^T + b2 over a tile of BM rows in one launch.
+// The hidden activations never leave the chip: they are produced FC columns
+// at a time into LDS and consumed at once by the second product, whose
+// BM x D output accumulates in registers over the chunks. The fp32 x tile
+// and its normalised bf16 copy stay in LDS from the LayerNorm to the
+// residual; the weights (small, L2-resident, read by every workgroup) go
+// straight from global memory into MFMA operand registers, the first
+// product's one chunk ahead; the barriers order LDS only, so those loads stay
+// in flight across them. Rounding points are the layered kernels': the
+// LayerNorm output and the hidden activations are bf16, products accumulate
+// in fp32, the residual adds x + (acc + b2).
+// Waves split the columns (FC / 4 hidden, D / 4 output) and each covers all
+// BM rows; a row's LayerNorm statistics come from 16 lanes holding D / 16
+// consecutive values each.
+// ---------------------------------------------------------------------------
+template <int D, int F, int BM, int FC>
+__global__ __launch_bounds__(256) void k_ffn_fused(float *__restrict__ x, const float *__restrict__ lg,
+                                                   const float *__restrict__ lb, const bf16_t *__restrict__ W1,
+                                                   const float *__restrict__ b1, const bf16_t *__restrict__ W2,
+                                                   const float *__restrict__ b2, int T) {
+  constexpr int XLD = D + 4, ALD = D + 8, HLD = FC + 8;   // row strides (pads spread LDS banks)
+  constexpr int TM = BM / 16, TNA = FC / 64, TNB = D / 64;
+  constexpr int KSA = D / 32, KSB = FC / 32, NCH = F / FC;
+  constexpr int EPL = D / 16, NP = BM / 16;               // LayerNorm: values per lane, row passes
+  static_assert(TNA >= 1 && TNB >= 1 && F % FC == 0 && BM % 16 == 0 && EPL % 4 == 0, "shape");
+  __shared__ __attribute__((aligned(16))) float xs[BM * XLD];
+  __shared__ __attribute__((aligned(16))) bf16_t as[BM * ALD];
+  __shared__ __attribute__((aligned(16))) bf16_t hs[BM * HLD];
+  __shared__ float b1s[F], b2s[D];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rr = lane & 15, g = lane >> 4;
+  const int m0 = blockIdx.x * BM;
+  // first product's weights of chunk c: wave's hidden columns c FC + wave FC/4 + 16 j + rr
+  bf16x8_t w1f[2][TNA][KSA];
+  auto load_w1 = [&](int c, bf16x8_t (&dst)[TNA][KSA]) {
+#pragma unroll
+    for (int j = 0; j < TNA; ++j)
+#pragma unroll
+      for (int ks = 0; ks < KSA; ++ks)
+        dst[j][ks] = *(const bf16x8_t *)(W1 + (size_t)(c * FC + wave * (FC / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
+  };
+  load_w1(0, w1f[0]);
+  // LayerNorm: wave w normalises rows w BM/4 + 4 p + g (16 lanes per row)
+  float4 xv[NP][EPL / 4];
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int row = wave * (BM / 4) + 4 * p + g;
+    const size_t r = (size_t)min(m0 + row, T - 1);
+#pragma unroll
+    for (int c = 0; c < EPL / 4; ++c) xv[p][c] = *(const float4 *)(x + r * D + rr * EPL + 4 * c);
+  }
+  for (int i = tid; i < F; i += 256) b1s[i] = b1[i];
+  for (int i = tid; i < D; i += 256) b2s[i] = b2[i];
+  float4 gv[EPL / 4], bv[EPL / 4];
+#pragma unroll
+  for (int c = 0; c < EPL / 4; ++c) {
+    gv[c] = *(const float4 *)(lg + rr * EPL + 4 * c);
+    bv[c] = *(const float4 *)(lb + rr * EPL + 4 * c);
+  }
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int row = wave * (BM / 4) + 4 * p + g;
+    float sum = 0.f;
+#pragma unroll
+    for (int c = 0; c < EPL / 4; ++c) sum += (xv[p][c].x + xv[p][c].y) + (xv[p][c].z + xv[p][c].w);
+    const float mean = group_sum(sum, 16) / (float)D;
+    float var = 0.f;
+#pragma unroll
+    for (int c = 0; c < EPL / 4; ++c) {
+      const float a0 = xv[p][c].x - mean, a1 = xv[p][c].y - mean, a2 = xv[p][c].z - mean, a3 = xv[p][c].w - mean;
+      var += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+    }
+    const float rs = 1.f / sqrtf(group_sum(var, 16) / (float)D + 1e-5f);
+#pragma unroll
+    for (int c = 0; c < EPL / 4; ++c) {
+      *(float4 *)&xs[row * XLD + rr * EPL + 4 * c] = xv[p][c];
+      const float y0 = (xv[p][c].x - mean) * rs * gv[c].x + bv[c].x;
+      const float y1 = (xv[p][c].y - mean) * rs * gv[c].y + bv[c].y;
+      const float y2 = (xv[p][c].z - mean) * rs * gv[c].z + bv[c].z;
+      const float y3 = (xv[p][c].w - mean) * rs * gv[c].w + bv[c].w;
+      uint2 pk;
+      pk.x = (uint32_t)f2bf(y0) | ((uint32_t)f2bf(y1) << 16);
+      pk.y = (uint32_t)f2bf(y2) | ((uint32_t)f2bf(y3) << 16);
+      *(uint2 *)&as[row * ALD + rr * EPL + 4 * c] = pk;
+    }
+  }
+  lds_barrier();
+  f32x4_t acc_o[TM][TNB];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TNB; ++j) acc_o[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    if (c + 1 < NCH) load_w1(c + 1, w1f[(c + 1) & 1]);
+    // second product's weights of chunk c: wave's output columns wave D/4 + 16 j + rr
+    bf16x8_t w2f[TNB][KSB];
+#pragma unroll
+    for (int j = 0; j < TNB; ++j)
+#pragma unroll
+      for (int ks = 0; ks < KSB; ++ks)
+        w2f[j][ks] = *(const bf16x8_t *)(W2 + (size_t)(wave * (D / 4) + 16 * j + rr) * F + c * FC + 32 * ks + 8 * g);
+    // hidden chunk: ReLU(A W1_c^T + b1) -> bf16 -> LDS
+    f32x4_t acc_h[TM][TNA];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TNA; ++j) acc_h[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSA; ++ks)
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const bf16x8_t af = *(const bf16x8_t *)&as[(16 * i + rr) * ALD + 32 * ks + 8 * g];
+#pragma unroll
+        for (int j = 0; j < TNA; ++j)
+          acc_h[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, w1f[c & 1][j][ks], acc_h[i][j], 0, 0, 0);
+      }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TNA; ++j) {
+        const int col = wave * (FC / 4) + 16 * j + rr;
+        const float bb = b1s[c * FC + col];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) hs[(16 * i + 4 * g + v) * HLD + col] = f2bf(fmaxf(acc_h[i][j][v] + bb, 0.f));
+      }
+    lds_barrier();
+#pragma unroll
+    for (int ks = 0; ks < KSB; ++ks)
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const bf16x8_t hf = *(const bf16x8_t *)&hs[(16 * i + rr) * HLD + 32 * ks + 8 * g];
+#pragma unroll
+        for (int j = 0; j < TNB; ++j)
+          acc_o[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hf, w2f[j][ks], acc_o[i][j], 0, 0, 0);
+      }
+    lds_barrier();   // the chunk's hidden tile is read before the next overwrites it
+  }
+  // residual in the LDS tile, then 16-byte stores of whole rows
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TNB; ++j) {
+      const int col = wave * (D / 4) + 16 * j + rr;
+      const float bb = b2s[col];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        float *xp = &xs[(16 * i + 4 * g + v) * XLD + col];
+        *xp = *xp + (acc_o[i][j][v] + bb);
+      }
+    }
+  lds_barrier();
+  for (int idx = tid; idx < BM * (D / 4); idx += 256) {
+    const int row = idx / (D / 4), c4 = idx - row * (D / 4);
+    if (m0 + row < T) *(float4 *)(x + (size_t)(m0 + row) * D + 4 * c4) = *(const float4 *)&xs[row * XLD + 4 * c4];
+  }
+}
+
 // ---------------------------------------------------------------------------
 // bf16 GEMM with operands moved straight from global memory into LDS
 // (global_load_lds, 16 bytes per lane) through an S-stage ring. No register
@@ -969,14 +1136,6 @@ template <> __device__ __forceinline__ void load8<bf16_t>(const bf16_t *p, float
     w[2 * i] = __uint_as_float(v[i] << 16);
     w[2 * i + 1] = __uint_as_float(v[i] & 0xFFFF0000u);
   }
-}
-
-// Workgroup barrier that orders LDS only: global loads into registers and global
-// stores stay in flight across it.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 // y[p][n] = sum_k W(n)[k] X(n, p)[k] for n < N, p < P (P <= 2), handed to
@@ -1377,8 +1536,8 @@ inline __host__ __device__ int fused_draft_head_floats(int L, int d, int F, int 
   return (n + 3) & ~3;
 }
 
-size_t fused_draft_weight_elems(int L, int d, int F, int M, int K) {
-  return (size_t)L * (4 * d * d + 2 * F * d) + (size_t)4 * d * d + (size_t)(3 * M + K) * d;
+size_t fused_draft_weight_elems(int L, int d, int F, int M, int K, int pad) {
+  return (size_t)L * ((size_t)(4 * d + F) * (d + pad) + (size_t)d * (F + pad)) + (size_t)(4 * d + 3 * M + K) * (d + pad);
 }
 
 size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H) {
@@ -1436,24 +1595,35 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
   // per-step matrix-vector products then read only LDS. LDS layout: per
   // layer QKV (3d x d), out (d x d), FFN in (F x d), FFN out (d x F); then
   // [E; V_k1] (4d x d), the mixture heads (3M x d), the type head (K x d).
+  // Each row is padded by 16 bytes: the products read one row per lane, and
+  // unpadded rows of 128 or 512 bytes would put every lane on the same banks.
+  constexpr int PD = 16 / sizeof(ELT);
   ELT *const wl = (ELT *)(sm + fused_draft_head_floats(a.L, d, F, M, K, H));
-  const size_t LS = (size_t)4 * d * d + (size_t)2 * F * d;
+  const int ldd = a.w_lds ? d + PD : d, ldf = a.w_lds ? F + PD : F;   // row strides of the matrices read
+  const size_t LS = (size_t)(4 * d + F) * (d + PD) + (size_t)d * (F + PD);
+  const size_t o_out = (size_t)3 * d * (d + PD), o_f1 = (size_t)4 * d * (d + PD),
+               o_f2 = o_f1 + (size_t)F * (d + PD), o_mix = (size_t)4 * d * (d + PD),
+               o_k2 = o_mix + (size_t)3 * M * (d + PD);
   if (a.w_lds) {
-    constexpr int VE = 16 / sizeof(ELT);
-    auto cpw = [&](size_t off, const void *src, size_t cnt) {   // cnt: a multiple of 16 bytes
+    // rows x cols (cols a multiple of 16 bytes) into rows of cols + PD
+    auto cpw = [&](size_t off, const void *src, int rows, int cols) {
+      const int vr = cols / PD;   // 16-byte vectors per row
       const uint4 *sp = (const uint4 *)src;
       uint4 *dp = (uint4 *)(wl + off);
-      for (size_t i = tid; i < cnt / VE; i += blockDim.x) dp[i] = sp[i];
+      for (int i = tid; i < rows * vr; i += blockDim.x) {
+        const int r = i / vr, c = i - r * vr;
+        dp[r * (vr + 1) + c] = sp[i];
+      }
     };
     for (int ly = 0; ly < a.L; ++ly) {
-      cpw(ly * LS, a.layer[ly].qkv_w, (size_t)3 * d * d);
-      cpw(ly * LS + (size_t)3 * d * d, a.layer[ly].out_w, (size_t)d * d);
-      cpw(ly * LS + (size_t)4 * d * d, a.layer[ly].ffn1_w, (size_t)F * d);
-      cpw(ly * LS + (size_t)4 * d * d + (size_t)F * d, a.layer[ly].ffn2_w, (size_t)d * F);
+      cpw(ly * LS, a.layer[ly].qkv_w, 3 * d, d);
+      cpw(ly * LS + o_out, a.layer[ly].out_w, d, d);
+      cpw(ly * LS + o_f1, a.layer[ly].ffn1_w, F, d);
+      cpw(ly * LS + o_f2, a.layer[ly].ffn2_w, d, F);
     }
-    cpw(a.L * LS, a.Ek1_w, (size_t)4 * d * d);
-    cpw(a.L * LS + (size_t)4 * d * d, a.mix_w, (size_t)3 * M * d);
-    cpw(a.L * LS + (size_t)4 * d * d + (size_t)3 * M * d, a.k2_w, (size_t)K * d);
+    cpw(a.L * LS, a.Ek1_w, 4 * d, d);
+    cpw(a.L * LS + o_mix, a.mix_w, 3 * M, d);
+    cpw(a.L * LS + o_k2, a.k2_w, K, d);
   }
   auto wmat = [&](const void *glob, size_t off) -> const ELT * {
     return a.w_lds ? (const ELT *)(wl + off) : (const ELT *)glob;
@@ -1499,7 +1669,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
       lds_barrier();
       const ELT *wq = wmat(w.qkv_w, ly * LS);
       wg_gemv_cpl<ELT, CD>(
-          3 * d, d, P, [&](int nn) { return wq + (size_t)nn * d; }, [&](int, int p) { return as + p * d; },
+          3 * d, d, P, [&](int nn) { return wq + (size_t)nn * ldd; }, [&](int, int p) { return as + p * d; },
           [&](int p, int nn, float acc) {
             const float v = rnd_act<ELT>(acc + qkv_b[nn]);
             const int which = nn / d, c = nn - which * d;
@@ -1520,21 +1690,21 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
       else
         wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       lds_barrier();
-      const ELT *wo = wmat(w.out_w, ly * LS + (size_t)3 * d * d);
+      const ELT *wo = wmat(w.out_w, ly * LS + o_out);
       wg_gemv_cpl<ELT, CD>(
-          d, d, P, [&](int nn) { return wo + (size_t)nn * d; }, [&](int, int p) { return os + p * d; },
+          d, d, P, [&](int nn) { return wo + (size_t)nn * ldd; }, [&](int, int p) { return os + p * d; },
           [&](int p, int nn, float acc) { xs[p * d + nn] += acc + out_b[nn]; });
       lds_barrier();
       wg_layernorm<ELT>(xs, as, ln2_g, ln2_b, P, d);
       lds_barrier();
-      const ELT *w1 = wmat(w.ffn1_w, ly * LS + (size_t)4 * d * d);
-      const ELT *w2 = wmat(w.ffn2_w, ly * LS + (size_t)4 * d * d + (size_t)F * d);
+      const ELT *w1 = wmat(w.ffn1_w, ly * LS + o_f1);
+      const ELT *w2 = wmat(w.ffn2_w, ly * LS + o_f2);
       wg_gemv_cpl<ELT, CD>(
-          F, d, P, [&](int nn) { return w1 + (size_t)nn * d; }, [&](int, int p) { return as + p * d; },
+          F, d, P, [&](int nn) { return w1 + (size_t)nn * ldd; }, [&](int, int p) { return as + p * d; },
           [&](int p, int nn, float acc) { hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + ffn1_b[nn], 0.f)); });
       lds_barrier();
       wg_gemv_cpl<ELT, CF>(
-          d, F, P, [&](int nn) { return w2 + (size_t)nn * F; }, [&](int, int p) { return hs + p * F; },
+          d, F, P, [&](int nn) { return w2 + (size_t)nn * ldf; }, [&](int, int p) { return hs + p * F; },
           [&](int p, int nn, float acc) { xs[p * d + nn] += acc + ffn2_b[nn]; });
       lds_barrier();
     }
@@ -1545,16 +1715,16 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
     lds_barrier();
     const ELT *we = wmat(a.Ek1_w, a.L * LS);
     wg_gemv_cpl<ELT, CD>(
-        4 * d, d, 1, [&](int nn) { return we + (size_t)nn * d; }, [&](int, int) { return (const float *)as; },
+        4 * d, d, 1, [&](int nn) { return we + (size_t)nn * ldd; }, [&](int, int) { return (const float *)as; },
         [&](int, int nn, float acc) {
           es[nn] = (nn < 3 * d) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * d]));
         });
     lds_barrier();
-    const ELT *mw = wmat(a.mix_w, a.L * LS + (size_t)4 * d * d);
-    const ELT *kw = wmat(a.k2_w, a.L * LS + (size_t)4 * d * d + (size_t)3 * M * d);
+    const ELT *mw = wmat(a.mix_w, a.L * LS + o_mix);
+    const ELT *kw = wmat(a.k2_w, a.L * LS + o_k2);
     wg_gemv_cpl<ELT, CD>(
         3 * M + K, d, 1,
-        [&](int nn) { return nn < 3 * M ? mw + (size_t)nn * d : kw + (size_t)(nn - 3 * M) * d; },
+        [&](int nn) { return nn < 3 * M ? mw + (size_t)nn * ldd : kw + (size_t)(nn - 3 * M) * ldd; },
         [&](int nn, int) { return (const float *)(es + (nn < 3 * M ? nn / M : 3) * d); },
         [&](int, int nn, float acc) { hv[nn] = acc + (nn < 3 * M ? mix_b[nn] : k2_b[nn - 3 * M]); });
     lds_barrier();
@@ -1600,7 +1770,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
 
 void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
   const size_t lds = fused_draft_lds_bytes(a.L, a.d, a.F, a.M, a.K, a.H) +
-                     (a.w_lds ? fused_draft_weight_elems(a.L, a.d, a.F, a.M, a.K) * (bf16 ? 2 : 4) : 0);
+                     (a.w_lds ? fused_draft_weight_elems(a.L, a.d, a.F, a.M, a.K, bf16 ? 8 : 4) * (bf16 ? 2 : 4) : 0);
   const int cd = gemv_cpl(a.d), cf = gemv_cpl(a.F);
   // d_head = 16 only (fused_draft_ok); chunk counts 2, 4 or 8
   auto go = [&](auto kern) { kern<<<a.B, 256, lds, s>>>(a); };
@@ -2642,6 +2812,20 @@ static void gemm_dispatch(const void *X, const LnA *ln, const void *W, int T, in
     if (nst4 <= 2) go(k_gemm_lds<ELT, 32, 32, true, 2, 4>, 32, 32);
     else go(k_gemm_lds<ELT, 32, 32, true, 4, 4>, 32, 32);
   }
+}
+
+bool ffn_fused_ok(int bf16, int d, int F) { return bf16 && ((d == 128 && F == 512) || (d == 256 && F == 1024)); }
+
+bool launch_ffn_fused(float *x, const float *lg, const float *lb, const void *W1, const float *b1, const void *W2,
+                      const float *b2, int T, int d, int F, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const bf16_t *w1 = (const bf16_t *)W1, *w2 = (const bf16_t *)W2;
+  auto go = [&](auto kern, int bm) {
+    hipExtLaunchKernelGGL(kern, dim3((T + bm - 1) / bm), dim3(256), 0, s, ev0, ev1, 0, x, lg, lb, w1, b1, w2, b2, T);
+    return true;
+  };
+  if (d == 128 && F == 512) return go(k_ffn_fused<128, 512, 64, 128>, 64);
+  if (d == 256 && F == 1024) return go(k_ffn_fused<256, 1024, 32, 64>, 32);
+  return false;
 }
 
 void launch_gemm(const void *X, const LnA *ln, const void *W, int bf16, int T, int N, int K, const Epi &epi,
