@@ -469,24 +469,20 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     }
     return TPPSD_OK;
   }
-  // the feed-forward block in one launch (hidden activations on chip) where
+  // the row-local part of each layer in one launch (output projection, FFN
+  // with its hidden activations on chip, the next layer's q, k, v) where
   // there is an instance for the widths and the row tiles fill the chip;
   // TPPSD_FFN_FUSED=0 / 1 forces the layered / fused form
   const char *ff = getenv("TPPSD_FFN_FUSED");
-  const bool use_ffn_fused = fuse_ln && ffn_fused_ok(bf, d, m->cfg.d_ffn) &&
-                             (ff ? ff[0] == '1' : (long)T >= 256L * (d == 128 ? 64 : 32));
-  if (!m->attnhp()) launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
-  for (int l = 0; l < m->cfg.n_layers && !m->attnhp(); ++l) {
-    const LayerW &w = m->layers[l];
-    char *kc = c.k + c.layer_bytes * l, *vc = c.v + c.layer_bytes * l;
-    const LnA ln1{s->x, w.ln1_g, w.ln1_b}, ln2{s->x, w.ln2_g, w.ln2_b};
-    if (!fuse_ln) launch_layernorm(s->x, s->a, bf, w.ln1_g, w.ln1_b, T, d, st);
+  const bool use_layer_fused = fuse_ln && !m->attnhp() && layer_fused_ok(bf, d, F) &&
+                               (ff ? ff[0] == '1' : (long)T >= 256L * layer_fused_rows(d));
+  auto qkv_epi = [&](int l) {
     Epi e{};
     e.mode = EPI_QKV;
-    e.bias = w.qkv_b;
+    e.bias = m->layers[l].qkv_b;
     e.q = s->q;
-    e.kc = kc;
-    e.vc = vc;
+    e.kc = c.k + c.layer_bytes * l;
+    e.vc = c.v + c.layer_bytes * l;
     e.start = start;
     e.start_off = start_off;
     e.P = P;
@@ -495,20 +491,51 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     e.d = d;
     e.cap = s->kv_cap;
     e.status = s->status;
-    launch_gemm(s->a, fuse_ln ? &ln1 : nullptr, w.qkv_w, bf, T, 3 * d, d, e, st, ev(L + 4 * l, 0), ev(L + 4 * l, 1));
+    return e;
+  };
+  if (!m->attnhp()) launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
+  for (int l = 0; l < m->cfg.n_layers && !m->attnhp(); ++l) {
+    const LayerW &w = m->layers[l];
+    char *kc = c.k + c.layer_bytes * l, *vc = c.v + c.layer_bytes * l;
+    const LnA ln1{s->x, w.ln1_g, w.ln1_b}, ln2{s->x, w.ln2_g, w.ln2_b};
+    if (!(use_layer_fused && l > 0)) {   // (else the previous fused launch wrote this layer's q, k, v)
+      if (!fuse_ln) launch_layernorm(s->x, s->a, bf, w.ln1_g, w.ln1_b, T, d, st);
+      const Epi e = qkv_epi(l);
+      launch_gemm(s->a, fuse_ln ? &ln1 : nullptr, w.qkv_w, bf, T, 3 * d, d, e, st, ev(L + 4 * l, 0),
+                  ev(L + 4 * l, 1));
+    }
     launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->kv_cap, s->attn_part,
                      0, verify ? 1 : 0, ev(l, 0), ev(l, 1), st);
+    if (use_layer_fused) {
+      LayerArgs la{};
+      la.x = s->x;
+      la.o = (const bf16_t *)s->o;
+      la.wo = (const bf16_t *)w.out_w;
+      la.bo = w.out_b;
+      la.ln2_g = w.ln2_g;
+      la.ln2_b = w.ln2_b;
+      la.w1 = (const bf16_t *)w.ffn1_w;
+      la.b1 = w.ffn1_b;
+      la.w2 = (const bf16_t *)w.ffn2_w;
+      la.b2 = w.ffn2_b;
+      const bool post = l + 1 < L;
+      if (post) {
+        const LayerW &wn = m->layers[l + 1];
+        la.ln1_g = wn.ln1_g;
+        la.ln1_b = wn.ln1_b;
+        la.wqkv = (const bf16_t *)wn.qkv_w;
+        la.qe = qkv_epi(l + 1);
+      }
+      la.T = T;
+      launch_layer_fused(la, d, F, post, st, ev(L + 4 * l + 1, 0), ev(L + 4 * l + 1, 1));
+      continue;
+    }
     Epi eo{};
     eo.mode = EPI_RESID;
     eo.bias = w.out_b;
     eo.out = s->x;
     eo.ldo = d;
     launch_gemm(s->o, nullptr, w.out_w, bf, T, d, d, eo, st, ev(L + 4 * l + 1, 0), ev(L + 4 * l + 1, 1));
-    if (use_ffn_fused) {
-      launch_ffn_fused(s->x, w.ln2_g, w.ln2_b, w.ffn1_w, w.ffn1_b, w.ffn2_w, w.ffn2_b, T, d, F, st,
-                       ev(L + 4 * l + 2, 0), ev(L + 4 * l + 2, 1));
-      continue;
-    }
     if (!fuse_ln) launch_layernorm(s->x, s->a, bf, w.ln2_g, w.ln2_b, T, d, st);
     Epi e1{};
     e1.mode = EPI_RELU;

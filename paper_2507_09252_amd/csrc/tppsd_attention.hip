@@ -269,7 +269,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
         const float p0 = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
         const float p1 = (sv[j + 1] == -INFINITY) ? 0.f : expf(sv[j + 1] - m_new);
         ps += p0 + p1;
-        pw[j >> 1] = (uint32_t)f2bf(p0) | ((uint32_t)f2bf(p1) << 16);
+        pw[j >> 1] = pk2bf(p0, p1);
       }
       const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, (uint4){pw[0], pw[1], pw[2], pw[3]});
       ps += __shfl_xor(ps, 16, 64);

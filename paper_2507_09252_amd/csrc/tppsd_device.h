@@ -22,11 +22,14 @@ typedef short short4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// float -> bf16, round to nearest even (values here are finite)
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+// float -> bf16, round to nearest even: gfx950's conversion instruction
+// (v_cvt_pk_bf16_f32, two values per instruction; for finite values it
+// gives the same bits as adding 0x7FFF + the kept lsb and truncating)
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+// the pair (lo, hi) packed into one word, lo in the low half
+__device__ __forceinline__ uint32_t pk2bf(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, (bf16x2_t){(__bf16)lo, (__bf16)hi});
 }
 
 template <typename T> __device__ __forceinline__ float ld(const T *p, size_t i);

@@ -243,12 +243,24 @@ void launch_gemm(const void *X, const LnA *ln, const void *W, int bf16, int T, i
                  hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // whether launch_gemm can take a LayerNorm operand of width K
 bool gemm_ln_fusable(int bf16, int K);
-// bf16 feed-forward block x += ReLU(LN(x) W1^T + b1) W2^T + b2 in one launch
-// (hidden activations kept on chip); false (nothing launched) for widths it
-// has no instance for
-bool launch_ffn_fused(float *x, const float *lg, const float *lb, const void *W1, const float *b1, const void *W2,
-                      const float *b2, int T, int d, int F, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
-bool ffn_fused_ok(int bf16, int d, int F);
+// Fused row-local part of a bf16 THP layer between two attention launches
+// (output projection + residual, feed-forward block + residual, and with
+// post the next layer's LayerNorm and q, k, v through qe), one launch over
+// tiles of layer_fused_rows(d) rows; layer_fused_ok: there is an instance
+struct LayerArgs {
+  float *x;                                  // [T][D] residual stream (in / out)
+  const bf16_t *o, *wo;                      // attention output [T][D], Wo [D][D]
+  const float *bo;
+  const float *ln2_g, *ln2_b, *b1, *b2;
+  const bf16_t *w1, *w2;                     // [F][D], [D][F]
+  const float *ln1_g, *ln1_b;                // post: the next layer's LayerNorm
+  const bf16_t *wqkv;                        // post: [3D][D]
+  Epi qe;                                    // post: EPI_QKV
+  int T;
+};
+bool layer_fused_ok(int bf16, int d, int F);
+int layer_fused_rows(int d);
+void launch_layer_fused(const LayerArgs &a, int d, int F, bool post, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 // decoder epilogue over the rows' logits [.., ldl] (mixture w | mu | log sigma, then types)
 void launch_head(const float *logits, int ldl, int M, int K, const HeadArgs &a, hipStream_t st);
 // the decoder's block-diagonal (3M + K) x 4d matrix and its bias (3M + K)

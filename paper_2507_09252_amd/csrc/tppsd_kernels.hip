@@ -266,7 +266,7 @@ template <> __device__ __forceinline__ void store8<float>(float *p, const float 
 template <> __device__ __forceinline__ void store8<bf16_t>(bf16_t *p, const float v[8]) {
   uint32_t w[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = (uint32_t)f2bf(v[2 * i]) | ((uint32_t)f2bf(v[2 * i + 1]) << 16);
+  for (int i = 0; i < 4; ++i) w[i] = pk2bf(v[2 * i], v[2 * i + 1]);
   *(uint4 *)p = make_uint4(w[0], w[1], w[2], w[3]);
 }
 __device__ __forceinline__ void load8f(const float *p, float v[8]) {
@@ -507,7 +507,7 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
         if (sizeof(ELT) == 2) {
           uint32_t pk[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) pk[q] = (uint32_t)f2bf(y[2 * q]) | ((uint32_t)f2bf(y[2 * q + 1]) << 16);
+          for (int q = 0; q < 4; ++q) pk[q] = pk2bf(y[2 * q], y[2 * q + 1]);
           w = make_uint4(pk[0], pk[1], pk[2], pk[3]);
         } else {
           w = make_uint4(__float_as_uint(y[0]), __float_as_uint(y[1]), __float_as_uint(y[2]), __float_as_uint(y[3]));
@@ -629,6 +629,25 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
   }
 }
 
+// ---------------------------------------------------------------------------
+// Fused row-local part of a pre-LN THP layer (§4.2 encoder), bf16, over a
+// tile of BM rows in one launch, between two attention launches:
+//   PRE:  x += o Wo^T + bo                      (output projection, residual)
+//         x += ReLU(LN2(x) W1^T + b1) W2^T + b2 (feed-forward block)
+//   POST: q, k, v = LN1'(x) Wqkv'^T + b         (next layer, EPI_QKV epilogue)
+// Nothing row-sized goes to HBM but o in, x out and q / k / v out: the FFN
+// hidden activations are produced FC columns at a time into LDS and
+// consumed at once by the second product, whose BM x D output accumulates
+// in registers over the chunks; the fp32 x tile stays in LDS from the first
+// residual to the last LayerNorm. Weights (small, L2-resident, read by every
+// workgroup) go straight from global memory into MFMA operand registers.
+// Rounding points are the layered kernels': LayerNorm outputs and hidden
+// activations are bf16, products accumulate in fp32, residuals add
+// x + (acc + bias). Waves split the columns (D / 4 or FC / 4 per wave) and
+// each covers all BM rows; a row's LayerNorm statistics come from 16 lanes
+// holding D / 16 consecutive values each. The barriers order LDS only, so
+// weight loads stay in flight across them.
+// ---------------------------------------------------------------------------
 // Workgroup barrier that orders LDS only: global loads into registers and global
 // stores stay in flight across it.
 __device__ __forceinline__ void lds_barrier() {
@@ -637,93 +656,144 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// ---------------------------------------------------------------------------
-// Fused feed-forward block of a pre-LN THP layer (§4.2 encoder):
-// x += ReLU(LN2(x) W1^T + b1) W2^T + b2 over a tile of BM rows in one launch.
-// The hidden activations never leave the chip: they are produced FC columns
-// at a time into LDS and consumed at once by the second product, whose
-// BM x D output accumulates in registers over the chunks. The fp32 x tile
-// and its normalised bf16 copy stay in LDS from the LayerNorm to the
-// residual; the weights (small, L2-resident, read by every workgroup) go
-// straight from global memory into MFMA operand registers, the first
-// product's one chunk ahead; the barriers order LDS only, so those loads stay
-// in flight across them. Rounding points are the layered kernels': the
-// LayerNorm output and the hidden activations are bf16, products accumulate
-// in fp32, the residual adds x + (acc + b2).
-// Waves split the columns (FC / 4 hidden, D / 4 output) and each covers all
-// BM rows; a row's LayerNorm statistics come from 16 lanes holding D / 16
-// consecutive values each.
-// ---------------------------------------------------------------------------
-template <int D, int F, int BM, int FC>
-__global__ __launch_bounds__(256) void k_ffn_fused(float *__restrict__ x, const float *__restrict__ lg,
-                                                   const float *__restrict__ lb, const bf16_t *__restrict__ W1,
-                                                   const float *__restrict__ b1, const bf16_t *__restrict__ W2,
-                                                   const float *__restrict__ b2, int T) {
+template <int D, int F, int BM, int FC, bool PRE, bool POST>
+__global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
   constexpr int XLD = D + 4, ALD = D + 8, HLD = FC + 8;   // row strides (pads spread LDS banks)
   constexpr int TM = BM / 16, TNA = FC / 64, TNB = D / 64;
-  constexpr int KSA = D / 32, KSB = FC / 32, NCH = F / FC;
+  constexpr int KSD = D / 32, KSB = FC / 32, NCH = F / FC;
   constexpr int EPL = D / 16, NP = BM / 16;               // LayerNorm: values per lane, row passes
   static_assert(TNA >= 1 && TNB >= 1 && F % FC == 0 && BM % 16 == 0 && EPL % 4 == 0, "shape");
+  static_assert(!POST || (3 * D) % 128 == 0, "q, k, v in chunks of 128 columns");
   __shared__ __attribute__((aligned(16))) float xs[BM * XLD];
   __shared__ __attribute__((aligned(16))) bf16_t as[BM * ALD];
   __shared__ __attribute__((aligned(16))) bf16_t hs[BM * HLD];
   __shared__ float b1s[F], b2s[D];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rr = lane & 15, g = lane >> 4;
-  const int m0 = blockIdx.x * BM;
-  // first product's weights of chunk c: wave's hidden columns c FC + wave FC/4 + 16 j + rr
-  bf16x8_t w1f[2][TNA][KSA];
-  auto load_w1 = [&](int c, bf16x8_t (&dst)[TNA][KSA]) {
+  const int T = a.T, m0 = blockIdx.x * BM;
+  const bf16_t *W1 = a.w1, *W2 = a.w2;
+  // first FFN product's weights of chunk c: wave's hidden columns c FC + wave FC/4 + 16 j + rr
+  bf16x8_t w1f[2][TNA][KSD];
+  auto load_w1 = [&](int c, bf16x8_t (&dst)[TNA][KSD]) {
 #pragma unroll
     for (int j = 0; j < TNA; ++j)
 #pragma unroll
-      for (int ks = 0; ks < KSA; ++ks)
+      for (int ks = 0; ks < KSD; ++ks)
         dst[j][ks] = *(const bf16x8_t *)(W1 + (size_t)(c * FC + wave * (FC / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
   };
-  load_w1(0, w1f[0]);
-  // LayerNorm: wave w normalises rows w BM/4 + 4 p + g (16 lanes per row)
+  // LayerNorm of the xs rows into as (bf16): wave w normalises rows
+  // w BM/4 + 4 p + g, 16 lanes per row; v holds the rows' values
+  auto layernorm = [&](const float4 (&v)[NP][EPL / 4], const float *lg, const float *lb) {
+    float4 gv[EPL / 4], bv[EPL / 4];
+#pragma unroll
+    for (int c = 0; c < EPL / 4; ++c) {
+      gv[c] = *(const float4 *)(lg + rr * EPL + 4 * c);
+      bv[c] = *(const float4 *)(lb + rr * EPL + 4 * c);
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const int row = wave * (BM / 4) + 4 * p + g;
+      float sum = 0.f;
+#pragma unroll
+      for (int c = 0; c < EPL / 4; ++c) sum += (v[p][c].x + v[p][c].y) + (v[p][c].z + v[p][c].w);
+      const float mean = group_sum(sum, 16) / (float)D;
+      float var = 0.f;
+#pragma unroll
+      for (int c = 0; c < EPL / 4; ++c) {
+        const float a0 = v[p][c].x - mean, a1 = v[p][c].y - mean, a2 = v[p][c].z - mean, a3 = v[p][c].w - mean;
+        var += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+      }
+      const float rs = 1.f / sqrtf(group_sum(var, 16) / (float)D + 1e-5f);
+#pragma unroll
+      for (int c = 0; c < EPL / 4; ++c) {
+        const float y0 = (v[p][c].x - mean) * rs * gv[c].x + bv[c].x;
+        const float y1 = (v[p][c].y - mean) * rs * gv[c].y + bv[c].y;
+        const float y2 = (v[p][c].z - mean) * rs * gv[c].z + bv[c].z;
+        const float y3 = (v[p][c].w - mean) * rs * gv[c].w + bv[c].w;
+        uint2 pk;
+        pk.x = pk2bf(y0, y1);
+        pk.y = pk2bf(y2, y3);
+        *(uint2 *)&as[row * ALD + rr * EPL + 4 * c] = pk;
+      }
+    }
+  };
+  auto read_rows = [&](float4 (&v)[NP][EPL / 4]) {   // this lane's LayerNorm share of the xs rows
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int c = 0; c < EPL / 4; ++c)
+        v[p][c] = *(const float4 *)&xs[(wave * (BM / 4) + 4 * p + g) * XLD + rr * EPL + 4 * c];
+  };
+  // D-wide product of the as rows with the D x D matrix W, computed
+  // transposed (W rows as the MFMA's first operand) so that lane (rr, g)
+  // holds row 16 i + rr, columns wave D/4 + 16 j + 4 g .. + 3 in acc[i][j]
+  auto prod_dd = [&](const bf16_t *W, f32x4_t (&acc)[TM][TNB]) {
+    bf16x8_t wf[TNB][KSD];
+#pragma unroll
+    for (int j = 0; j < TNB; ++j)
+#pragma unroll
+      for (int ks = 0; ks < KSD; ++ks)
+        wf[j][ks] = *(const bf16x8_t *)(W + (size_t)(wave * (D / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TNB; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSD; ++ks)
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const bf16x8_t af = *(const bf16x8_t *)&as[(16 * i + rr) * ALD + 32 * ks + 8 * g];
+#pragma unroll
+        for (int j = 0; j < TNB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j][ks], af, acc[i][j], 0, 0, 0);
+      }
+  };
+  // xs[row][col .. col + 3] += acc + bias[col ..]: one float4 per lane
+  auto resid4 = [&](int row, int col, const f32x4_t &acc, const float *bias) {
+    float4 *xp = (float4 *)&xs[row * XLD + col];
+    float4 xv4 = *xp;
+    xv4.x = xv4.x + (acc[0] + bias[col]);
+    xv4.y = xv4.y + (acc[1] + bias[col + 1]);
+    xv4.z = xv4.z + (acc[2] + bias[col + 2]);
+    xv4.w = xv4.w + (acc[3] + bias[col + 3]);
+    *xp = xv4;
+  };
+
+  // x rows (and o rows) in
   float4 xv[NP][EPL / 4];
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
     const int row = wave * (BM / 4) + 4 * p + g;
     const size_t r = (size_t)min(m0 + row, T - 1);
 #pragma unroll
-    for (int c = 0; c < EPL / 4; ++c) xv[p][c] = *(const float4 *)(x + r * D + rr * EPL + 4 * c);
+    for (int c = 0; c < EPL / 4; ++c) xv[p][c] = *(const float4 *)(a.x + r * D + rr * EPL + 4 * c);
   }
-  for (int i = tid; i < F; i += 256) b1s[i] = b1[i];
-  for (int i = tid; i < D; i += 256) b2s[i] = b2[i];
-  float4 gv[EPL / 4], bv[EPL / 4];
-#pragma unroll
-  for (int c = 0; c < EPL / 4; ++c) {
-    gv[c] = *(const float4 *)(lg + rr * EPL + 4 * c);
-    bv[c] = *(const float4 *)(lb + rr * EPL + 4 * c);
-  }
-#pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const int row = wave * (BM / 4) + 4 * p + g;
-    float sum = 0.f;
-#pragma unroll
-    for (int c = 0; c < EPL / 4; ++c) sum += (xv[p][c].x + xv[p][c].y) + (xv[p][c].z + xv[p][c].w);
-    const float mean = group_sum(sum, 16) / (float)D;
-    float var = 0.f;
-#pragma unroll
-    for (int c = 0; c < EPL / 4; ++c) {
-      const float a0 = xv[p][c].x - mean, a1 = xv[p][c].y - mean, a2 = xv[p][c].z - mean, a3 = xv[p][c].w - mean;
-      var += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
-    }
-    const float rs = 1.f / sqrtf(group_sum(var, 16) / (float)D + 1e-5f);
-#pragma unroll
-    for (int c = 0; c < EPL / 4; ++c) {
-      *(float4 *)&xs[row * XLD + rr * EPL + 4 * c] = xv[p][c];
-      const float y0 = (xv[p][c].x - mean) * rs * gv[c].x + bv[c].x;
-      const float y1 = (xv[p][c].y - mean) * rs * gv[c].y + bv[c].y;
-      const float y2 = (xv[p][c].z - mean) * rs * gv[c].z + bv[c].z;
-      const float y3 = (xv[p][c].w - mean) * rs * gv[c].w + bv[c].w;
-      uint2 pk;
-      pk.x = (uint32_t)f2bf(y0) | ((uint32_t)f2bf(y1) << 16);
-      pk.y = (uint32_t)f2bf(y2) | ((uint32_t)f2bf(y3) << 16);
-      *(uint2 *)&as[row * ALD + rr * EPL + 4 * c] = pk;
+  if (PRE) {
+    constexpr int VR = D / 8;   // 16-byte vectors per o row
+    for (int i = tid; i < BM * VR; i += 256) {
+      const int row = i / VR, c = i - row * VR;
+      *(uint4 *)&as[row * ALD + 8 * c] = *(const uint4 *)(a.o + (size_t)min(m0 + row, T - 1) * D + 8 * c);
     }
   }
+  for (int i = tid; i < F; i += 256) b1s[i] = a.b1[i];
+  for (int i = tid; i < D; i += 256) b2s[i] = a.b2[i];
+#pragma unroll
+  for (int p = 0; p < NP; ++p)
+#pragma unroll
+    for (int c = 0; c < EPL / 4; ++c) *(float4 *)&xs[(wave * (BM / 4) + 4 * p + g) * XLD + rr * EPL + 4 * c] = xv[p][c];
+  load_w1(0, w1f[0]);
+  lds_barrier();
+  if (PRE) {
+    // output projection and residual into the xs tile
+    f32x4_t acc[TM][TNB];
+    prod_dd(a.wo, acc);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TNB; ++j) resid4(16 * i + rr, wave * (D / 4) + 16 * j + 4 * g, acc[i][j], a.bo);
+    lds_barrier();   // xs complete, o operand reads done
+    read_rows(xv);
+  }
+  layernorm(xv, a.ln2_g, a.ln2_b);
   lds_barrier();
   f32x4_t acc_o[TM][TNB];
 #pragma unroll
@@ -747,22 +817,26 @@ __global__ __launch_bounds__(256) void k_ffn_fused(float *__restrict__ x, const 
 #pragma unroll
       for (int j = 0; j < TNA; ++j) acc_h[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ks = 0; ks < KSA; ++ks)
+    for (int ks = 0; ks < KSD; ++ks)
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const bf16x8_t af = *(const bf16x8_t *)&as[(16 * i + rr) * ALD + 32 * ks + 8 * g];
 #pragma unroll
         for (int j = 0; j < TNA; ++j)
-          acc_h[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, w1f[c & 1][j][ks], acc_h[i][j], 0, 0, 0);
+          acc_h[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1f[c & 1][j][ks], af, acc_h[i][j], 0, 0, 0);
       }
+    // (transposed product: lane (rr, g) holds row 16 i + rr, hidden columns
+    // wave FC/4 + 16 j + 4 g .. + 3, written as one 8-byte word)
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TNA; ++j) {
-        const int col = wave * (FC / 4) + 16 * j + rr;
-        const float bb = b1s[c * FC + col];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) hs[(16 * i + 4 * g + v) * HLD + col] = f2bf(fmaxf(acc_h[i][j][v] + bb, 0.f));
+        const int col = wave * (FC / 4) + 16 * j + 4 * g;
+        const float *bb = b1s + c * FC + col;
+        uint2 pk;
+        pk.x = pk2bf(fmaxf(acc_h[i][j][0] + bb[0], 0.f), fmaxf(acc_h[i][j][1] + bb[1], 0.f));
+        pk.y = pk2bf(fmaxf(acc_h[i][j][2] + bb[2], 0.f), fmaxf(acc_h[i][j][3] + bb[3], 0.f));
+        *(uint2 *)&hs[(16 * i + rr) * HLD + col] = pk;
       }
     lds_barrier();
 #pragma unroll
@@ -772,27 +846,65 @@ __global__ __launch_bounds__(256) void k_ffn_fused(float *__restrict__ x, const 
         const bf16x8_t hf = *(const bf16x8_t *)&hs[(16 * i + rr) * HLD + 32 * ks + 8 * g];
 #pragma unroll
         for (int j = 0; j < TNB; ++j)
-          acc_o[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hf, w2f[j][ks], acc_o[i][j], 0, 0, 0);
+          acc_o[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w2f[j][ks], hf, acc_o[i][j], 0, 0, 0);
       }
     lds_barrier();   // the chunk's hidden tile is read before the next overwrites it
   }
-  // residual in the LDS tile, then 16-byte stores of whole rows
+  // second residual in the LDS tile, then 16-byte stores of whole rows
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TNB; ++j) {
-      const int col = wave * (D / 4) + 16 * j + rr;
-      const float bb = b2s[col];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        float *xp = &xs[(16 * i + 4 * g + v) * XLD + col];
-        *xp = *xp + (acc_o[i][j][v] + bb);
-      }
-    }
+    for (int j = 0; j < TNB; ++j) resid4(16 * i + rr, wave * (D / 4) + 16 * j + 4 * g, acc_o[i][j], b2s);
   lds_barrier();
   for (int idx = tid; idx < BM * (D / 4); idx += 256) {
     const int row = idx / (D / 4), c4 = idx - row * (D / 4);
-    if (m0 + row < T) *(float4 *)(x + (size_t)(m0 + row) * D + 4 * c4) = *(const float4 *)&xs[row * XLD + 4 * c4];
+    if (m0 + row < T) *(float4 *)(a.x + (size_t)(m0 + row) * D + 4 * c4) = *(const float4 *)&xs[row * XLD + 4 * c4];
+  }
+  if (!POST) return;
+  // the next layer's LayerNorm and q, k, v, 128 columns at a time; each
+  // chunk's tile is staged in xs (free once normalised) for 8-column stores
+  read_rows(xv);
+  layernorm(xv, a.ln1_g, a.ln1_b);
+  lds_barrier();
+  constexpr int QC = 128, TNQ = QC / 64, SLD = QC + 4;
+  static_assert(BM * SLD <= BM * XLD || D >= QC, "q, k, v staging fits the x tile");
+#pragma unroll 1
+  for (int c = 0; c < 3 * D / QC; ++c) {
+    bf16x8_t wf[TNQ][KSD];
+#pragma unroll
+    for (int j = 0; j < TNQ; ++j)
+#pragma unroll
+      for (int ks = 0; ks < KSD; ++ks)
+        wf[j][ks] =
+            *(const bf16x8_t *)(a.wqkv + (size_t)(c * QC + wave * (QC / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
+    f32x4_t acc[TM][TNQ];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TNQ; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSD; ++ks)
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const bf16x8_t af = *(const bf16x8_t *)&as[(16 * i + rr) * ALD + 32 * ks + 8 * g];
+#pragma unroll
+        for (int j = 0; j < TNQ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j][ks], af, acc[i][j], 0, 0, 0);
+      }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TNQ; ++j)
+        *(f32x4_t *)&xs[(16 * i + rr) * SLD + wave * (QC / 4) + 16 * j + 4 * g] = acc[i][j];
+    lds_barrier();
+    for (int gi = tid; gi < BM * (QC / 8); gi += 256) {
+      const int row = gi / (QC / 8), c8 = gi - row * (QC / 8);
+      if (m0 + row >= T) continue;
+      float cv[8];
+      load8f(xs + row * SLD + 8 * c8, cv);
+      epilogue8<bf16_t>(a.qe, m0 + row, c * QC + 8 * c8, cv);
+    }
+    lds_barrier();   // staging read before the next chunk writes it
   }
 }
 
@@ -1439,8 +1551,8 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
         }
         f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
         if constexpr (sizeof(ELT) == 2) {
-          const uint32_t w0 = (uint32_t)f2bf(q0) | ((uint32_t)f2bf(q1) << 16);
-          const uint32_t w1 = (uint32_t)f2bf(q2) | ((uint32_t)f2bf(q3) << 16);
+          const uint32_t w0 = pk2bf(q0, q1);
+          const uint32_t w1 = pk2bf(q2, q3);
           const short4_t qf = __builtin_bit_cast(short4_t, make_uint2(w0, w1));
           s0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(f[sidx].k0, qf, s0, 0, 0, 0);
           s1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(f[sidx].k1, qf, s1, 0, 0, 0);
@@ -1484,7 +1596,7 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
           uint32_t pw[4];
 #pragma unroll
           for (int j = 0; j < 8; j += 2)
-            pw[j >> 1] = (uint32_t)f2bf(sv[sidx][j]) | ((uint32_t)f2bf(sv[sidx][j + 1]) << 16);
+            pw[j >> 1] = pk2bf(sv[sidx][j], sv[sidx][j + 1]);
           const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, make_uint4(pw[0], pw[1], pw[2], pw[3]));
           oacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, f[sidx].v), pb, oacc, 0, 0, 0);
         } else {
@@ -1891,7 +2003,7 @@ __device__ __forceinline__ void tile_mm16(const WBatch<ELT, K, TPW> &wb, int N, 
       uint32_t w[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e)   // LDS values are already rounded to bf16
-        w[e] = (uint32_t)f2bf(xr[8 * i + 2 * e]) | ((uint32_t)f2bf(xr[8 * i + 2 * e + 1]) << 16);
+        w[e] = pk2bf(xr[8 * i + 2 * e], xr[8 * i + 2 * e + 1]);
       xa[i] = __builtin_bit_cast(bf16x8_t, make_uint4(w[0], w[1], w[2], w[3]));
     }
     if constexpr (TPB > 1) {
@@ -2814,18 +2926,21 @@ static void gemm_dispatch(const void *X, const LnA *ln, const void *W, int T, in
   }
 }
 
-bool ffn_fused_ok(int bf16, int d, int F) { return bf16 && ((d == 128 && F == 512) || (d == 256 && F == 1024)); }
+bool layer_fused_ok(int bf16, int d, int F) { return bf16 && ((d == 128 && F == 512) || (d == 256 && F == 1024)); }
 
-bool launch_ffn_fused(float *x, const float *lg, const float *lb, const void *W1, const float *b1, const void *W2,
-                      const float *b2, int T, int d, int F, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  const bf16_t *w1 = (const bf16_t *)W1, *w2 = (const bf16_t *)W2;
+int layer_fused_rows(int d) { return d == 128 ? 64 : 32; }
+
+void launch_layer_fused(const LayerArgs &a, int d, int F, bool post, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   auto go = [&](auto kern, int bm) {
-    hipExtLaunchKernelGGL(kern, dim3((T + bm - 1) / bm), dim3(256), 0, s, ev0, ev1, 0, x, lg, lb, w1, b1, w2, b2, T);
-    return true;
+    hipExtLaunchKernelGGL(kern, dim3((a.T + bm - 1) / bm), dim3(256), 0, s, ev0, ev1, 0, a);
   };
-  if (d == 128 && F == 512) return go(k_ffn_fused<128, 512, 64, 128>, 64);
-  if (d == 256 && F == 1024) return go(k_ffn_fused<256, 1024, 32, 64>, 32);
-  return false;
+  if (d == 128 && F == 512) {
+    if (post) go(k_layer_fused<128, 512, 64, 128, true, true>, 64);
+    else go(k_layer_fused<128, 512, 64, 128, true, false>, 64);
+  } else {
+    if (post) go(k_layer_fused<256, 1024, 32, 64, true, true>, 32);
+    else go(k_layer_fused<256, 1024, 32, 64, true, false>, 32);
+  }
 }
 
 void launch_gemm(const void *X, const LnA *ln, const void *W, int bf16, int T, int N, int K, const Epi &epi,

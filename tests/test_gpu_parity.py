@@ -108,14 +108,15 @@ def test_verify_teacher_forced(case):
     print(f"{case.name}: max abs err logg {e1:.2e} logf {e2:.2e} mix {e3:.2e} logtype {e4:.2e}")
 
 
-# the feed-forward block as one launch (hidden activations on chip), forced
-# at these small sizes: several row tiles with a ragged last one
+# the row-local part of each layer as one launch (output projection, FFN
+# with its hidden activations on chip, next layer's q, k, v), forced at these
+# small sizes: several row tiles with a ragged last one
 FFN_FUSED_CASES = [small("c3", 5, n_hist=40, init="bias"), small("c3", 3, n_hist=40, init="paper", mismatch=False),
                    small("c5", 9, init="bias"), small("c5", 5)]
 
 
 @pytest.mark.parametrize("case", FFN_FUSED_CASES, ids=_ids(FFN_FUSED_CASES))
-def test_verify_fused_ffn(case, monkeypatch):
+def test_verify_fused_layer(case, monkeypatch):
     monkeypatch.setenv("TPPSD_FFN_FUSED", "1")
     test_verify_teacher_forced(case)
 
