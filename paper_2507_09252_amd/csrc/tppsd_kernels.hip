@@ -667,9 +667,15 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
   __shared__ __attribute__((aligned(16))) float xs[BM * XLD];
   __shared__ __attribute__((aligned(16))) bf16_t as[BM * ALD];
   __shared__ __attribute__((aligned(16))) bf16_t hs[BM * HLD];
-  __shared__ float b1s[F], b2s[D];
+  __shared__ float b1s[F], b2s[D];   // (b1s holds the q, k, v bias once the FFN is done)
+  __shared__ int rpos[POST ? BM : 1];    // POST: cache position of each row's event
+  static_assert(!POST || F >= 3 * D, "q, k, v bias fits the FFN bias array");
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, rr = lane & 15, g = lane >> 4;
   const int T = a.T, m0 = blockIdx.x * BM;
+  if (POST && tid < BM) {   // read now, used at the very end
+    const int r = min(m0 + tid, T - 1), bq = r / a.qe.P;
+    rpos[tid] = a.qe.start[bq] + a.qe.start_off + (r - bq * a.qe.P);
+  }
   const bf16_t *W1 = a.w1, *W2 = a.w2;
   // first FFN product's weights of chunk c: wave's hidden columns c FC + wave FC/4 + 16 j + rr
   bf16x8_t w1f[2][TNA][KSD];
@@ -850,6 +856,19 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
       }
     lds_barrier();   // the chunk's hidden tile is read before the next overwrites it
   }
+  constexpr int QC = 128, TNQ = QC / 64, SLD = QC + 4, NQC = POST ? 3 * D / QC : 1;
+  bf16x8_t wq[2][TNQ][KSD];
+  auto load_wq = [&](int c, bf16x8_t (&dst)[TNQ][KSD]) {
+#pragma unroll
+    for (int j = 0; j < TNQ; ++j)
+#pragma unroll
+      for (int ks = 0; ks < KSD; ++ks)
+        dst[j][ks] = *(const bf16x8_t *)(a.wqkv + (size_t)(c * QC + wave * (QC / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
+  };
+  if (POST) {
+    load_wq(0, wq[0]);
+    for (int i = tid; i < 3 * D; i += 256) b1s[i] = a.qe.bias[i];
+  }
   // second residual in the LDS tile, then 16-byte stores of whole rows
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -861,22 +880,19 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
     if (m0 + row < T) *(float4 *)(a.x + (size_t)(m0 + row) * D + 4 * c4) = *(const float4 *)&xs[row * XLD + 4 * c4];
   }
   if (!POST) return;
-  // the next layer's LayerNorm and q, k, v, 128 columns at a time; each
-  // chunk's tile is staged in xs (free once normalised) for 8-column stores
+  // the next layer's LayerNorm and q, k, v, 128 columns at a time (the next
+  // chunk's weights loading during the current one); each chunk's tile is
+  // staged in xs (free once normalised) and stored with lanes running over
+  // rows, so that the value cache's 2-byte stores of consecutive positions
+  // (one 16-byte block holds 8 positions of a column) are adjacent
   read_rows(xv);
   layernorm(xv, a.ln1_g, a.ln1_b);
   lds_barrier();
-  constexpr int QC = 128, TNQ = QC / 64, SLD = QC + 4;
-  static_assert(BM * SLD <= BM * XLD || D >= QC, "q, k, v staging fits the x tile");
-#pragma unroll 1
-  for (int c = 0; c < 3 * D / QC; ++c) {
-    bf16x8_t wf[TNQ][KSD];
+  static_assert(SLD <= XLD, "q, k, v staging fits the x tile");
+  const Epi &e = a.qe;
 #pragma unroll
-    for (int j = 0; j < TNQ; ++j)
-#pragma unroll
-      for (int ks = 0; ks < KSD; ++ks)
-        wf[j][ks] =
-            *(const bf16x8_t *)(a.wqkv + (size_t)(c * QC + wave * (QC / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
+  for (int c = 0; c < NQC; ++c) {
+    if (c + 1 < NQC) load_wq(c + 1, wq[(c + 1) & 1]);
     f32x4_t acc[TM][TNQ];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -889,7 +905,7 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
         const bf16x8_t af = *(const bf16x8_t *)&as[(16 * i + rr) * ALD + 32 * ks + 8 * g];
 #pragma unroll
         for (int j = 0; j < TNQ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j][ks], af, acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wq[c & 1][j][ks], af, acc[i][j], 0, 0, 0);
       }
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -898,11 +914,29 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
         *(f32x4_t *)&xs[(16 * i + rr) * SLD + wave * (QC / 4) + 16 * j + 4 * g] = acc[i][j];
     lds_barrier();
     for (int gi = tid; gi < BM * (QC / 8); gi += 256) {
-      const int row = gi / (QC / 8), c8 = gi - row * (QC / 8);
-      if (m0 + row >= T) continue;
-      float cv[8];
-      load8f(xs + row * SLD + 8 * c8, cv);
-      epilogue8<bf16_t>(a.qe, m0 + row, c * QC + 8 * c8, cv);
+      const int row = gi % BM, c8 = gi / BM, r = m0 + row;
+      if (r >= T) continue;
+      const int n = c * QC + 8 * c8, which = n / D, cc = n - which * D;
+      float v[8];
+      load8f(xs + row * SLD + 8 * c8, v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] += b1s[n + i];
+      if (which == 0) {
+        store8((bf16_t *)e.q + (size_t)r * D + cc, v);
+      } else {
+        const int bq = r / e.P, h = cc / e.dh, j = cc - h * e.dh, pos = rpos[row];
+        if (pos < e.cap) {
+          const size_t row0 = ((size_t)bq * e.H + h) * e.cap;
+          if (which == 1) {
+            store8((bf16_t *)e.kc + (row0 + pos) * e.dh + j, v);
+          } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) st((bf16_t *)e.vc, v_at<bf16_t>(row0, pos, j + i, e.dh), v[i]);
+          }
+        } else {
+          atomicOr(e.status, TPPSD_STATUS_CAPACITY);
+        }
+      }
     }
     lds_barrier();   // staging read before the next chunk writes it
   }
