@@ -1385,6 +1385,17 @@ template <> struct DraftStep<float> {
 // computes mostly padding; here every thread's loads go out together and
 // the step costs about one memory latency per unit a thread holds.
 // red: LDS scratch of at least 4 * 2 * 18 floats.
+// one step of a recursive-halving wave reduction of 2N values per lane: the
+// lane keeps its half (the upper one if hi), adds the partner's copy of it
+template <int N, typename X>
+__device__ __forceinline__ void halve_step(float (&v)[16], bool hi, X xchg) {
+#pragma unroll
+  for (int c = 0; c < N; ++c) {
+    const float keep = hi ? v[c + N] : v[c], give = hi ? v[c] : v[c + N];
+    v[c] = keep + xchg(give);
+  }
+}
+
 template <typename ELT>
 __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
                                   int H, int P, int pos0, int d, float *red) {
@@ -1409,9 +1420,9 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
     // the unit lies inside the slab (k0 < cap, the slab holds cap rounded
     // up to 8 positions); keys at or past n_keys are masked below. Values
     // stay packed in registers and are widened where they are used.
-    uint4 kr[8];
+    uint4 kr[U * DH * sizeof(ELT) / 16];
     uint2 vr2[16];
-    uint4 vr4[8];
+    uint4 vr4[U * DH * sizeof(ELT) / 16];
     if constexpr (sizeof(ELT) == 2) {
       const uint4 *kp = (const uint4 *)(kc + (row0 + k0) * DH);   // 4 rows x 16
 #pragma unroll
@@ -1519,12 +1530,20 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
     const float lw = wave_sum(l[p] * f);
     float ow[DH];
 #pragma unroll
-    for (int j = 0; j < DH; ++j) ow[j] = wave_sum(o[p][j] * f);
-    if (lane == 0) {
-      red[wave * 36 + p * 18 + 1] = lw;
-#pragma unroll
-      for (int j = 0; j < DH; ++j) red[wave * 36 + p * 18 + 2 + j] = ow[j];
-    }
+    for (int j = 0; j < DH; ++j) ow[j] = o[p][j] * f;
+    // the 16 column sums over the wave by recursive halving: each exchange
+    // keeps half of the columns (the half named by the lane's bit) and adds
+    // the partner's copy of that half; lane holds column (lane >> 2) & 15 at
+    // the end, summed over the 4 lanes of its quad by two more exchanges
+    halve_step<8>(ow, (lane & 32) != 0, [](float v) { return __shfl_xor(v, 32, 64); });
+    halve_step<4>(ow, (lane & 16) != 0, [](float v) { return swz_xor<16>(v); });
+    halve_step<2>(ow, (lane & 8) != 0, [](float v) { return swz_xor<8>(v); });
+    halve_step<1>(ow, (lane & 4) != 0, [](float v) { return swz_xor<4>(v); });
+    float oc = ow[0];
+    oc += dpp_mov<0x4E>(oc);   // lane ^ 2
+    oc += dpp_mov<0xB1>(oc);   // lane ^ 1
+    if (lane == 0) red[wave * 36 + p * 18 + 1] = lw;
+    if ((lane & 3) == 0) red[wave * 36 + p * 18 + 2 + (lane >> 2)] = oc;
   }
   lds_barrier();
   for (int idx = tid; idx < P * H * DH; idx += blockDim.x) {
