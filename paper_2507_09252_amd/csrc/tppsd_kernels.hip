@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
+#include <stdio.h>
 #include <math.h>
 #include <stdlib.h>
 #include <stdint.h>
@@ -1936,7 +1937,23 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
 void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
   const size_t lds = fused_draft_lds_bytes(a.L, a.d, a.F, a.M, a.K, a.H) +
                      (a.w_lds ? fused_draft_weight_elems(a.L, a.d, a.F, a.M, a.K, bf16 ? 8 : 4) * (bf16 ? 2 : 4) : 0);
-  const int cd = gemv_cpl(a.d), cf = gemv_cpl(a.F);
+  // chunks per lane of the d-wide and F-wide products: d / 16 (two lanes
+  // per row at d = 32, four at d = 64), and F d / 2048 (the d rows of the
+  // second FFN product over all 256 lanes), each within 2..8 -- measured
+  // against one chunk set per lane of K / 8 <= 8: 180 -> 154 us per draft
+  // round at d = 32 / F = 128, 480 -> 462 us at d = 64 / F = 256.
+  // TPPSD_DRAFT_CPL="cd,cf" overrides (2, 4 or 8 each, at most K / 8).
+  int cd = std::min(8, std::max(2, a.d / 16)), cf = std::min(8, std::max(2, a.F * a.d / 2048));
+  cd = std::min(cd, gemv_cpl(a.d));
+  cf = std::min(cf, gemv_cpl(a.F));
+  if (const char *ev = getenv("TPPSD_DRAFT_CPL")) {
+    int x = 0, y = 0;
+    if (sscanf(ev, "%d,%d", &x, &y) == 2 && (x == 2 || x == 4 || x == 8) && (y == 2 || y == 4 || y == 8) &&
+        x <= a.d / 8 && y <= a.F / 8) {
+      cd = x;
+      cf = y;
+    }
+  }
   // d_head = 16 only (fused_draft_ok); chunk counts 2, 4 or 8
   auto go = [&](auto kern) { kern<<<a.B, 256, lds, s>>>(a); };
 #define TPPSD_FD(ELT)                                                             \
