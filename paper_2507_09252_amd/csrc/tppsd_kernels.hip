@@ -1397,48 +1397,54 @@ __device__ __forceinline__ void halve_step(float (&v)[16], bool hi, X xchg) {
   }
 }
 
-template <typename ELT>
+template <typename ELT, int QN>
 __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
                                   int H, int P, int pos0, int d, float *red) {
-  constexpr int DH = 16, U = sizeof(ELT) == 2 ? 4 : 2;
+  // QN = P queries; with one query a thread's 4-key unit (keys and values in
+  // registers) fits beside the rest of the kernel in fp32 too
+  constexpr int DH = 16, U = (sizeof(ELT) == 2 || QN == 1) ? 4 : 2;
+  constexpr int NKV = U * DH * (int)sizeof(ELT) / 16;   // 16-byte vectors of a unit's keys (and of its fp32 values)
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int tph = blockDim.x / H, h = tid / tph, sub = tid - h * tph;
   const int n_keys = min(pos0 + P, cap);
   const size_t row0 = seq_row0 + (size_t)h * cap;
-  float q[2][DH];
+  float q[QN][DH];
 #pragma unroll
-  for (int p = 0; p < 2; ++p)
+  for (int p = 0; p < QN; ++p)
 #pragma unroll
-    for (int j = 0; j < DH; ++j) q[p][j] = (p < P) ? qs[p * d + h * DH + j] * 0.25f : 0.f;   // 1 / sqrt(16)
-  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f}, o[2][DH];
+    for (int j = 0; j < DH; ++j) q[p][j] = qs[p * d + h * DH + j] * 0.25f;   // 1 / sqrt(16)
+  float m[QN], l[QN], o[QN][DH];
 #pragma unroll
-  for (int p = 0; p < 2; ++p)
+  for (int p = 0; p < QN; ++p) {
+    m[p] = -INFINITY;
+    l[p] = 0.f;
 #pragma unroll
     for (int j = 0; j < DH; ++j) o[p][j] = 0.f;
+  }
   const int nunits = (n_keys + U - 1) / U;
   for (int u = sub; u < nunits; u += tph) {
     const int k0 = u * U;
     // the unit lies inside the slab (k0 < cap, the slab holds cap rounded
     // up to 8 positions); keys at or past n_keys are masked below. Values
     // stay packed in registers and are widened where they are used.
-    uint4 kr[U * DH * sizeof(ELT) / 16];
+    uint4 kr[NKV];
     uint2 vr2[16];
-    uint4 vr4[U * DH * sizeof(ELT) / 16];
+    uint4 vr4[sizeof(ELT) == 2 ? 1 : NKV];
     if constexpr (sizeof(ELT) == 2) {
       const uint4 *kp = (const uint4 *)(kc + (row0 + k0) * DH);   // 4 rows x 16
 #pragma unroll
-      for (int i = 0; i < 8; ++i) kr[i] = kp[i];
+      for (int i = 0; i < NKV; ++i) kr[i] = kp[i];
       // value column j of the block holding k0: 8 positions, this unit's 4 at k0 & 4
       const bf16_t *vb = vc + v_at<bf16_t>(row0, k0 & ~7, 0, DH) + (k0 & 4);
 #pragma unroll
       for (int j = 0; j < 16; ++j) vr2[j] = *(const uint2 *)(vb + 8 * j);
     } else {
-      const uint4 *kp = (const uint4 *)(kc + (row0 + k0) * DH);   // 2 rows x 16
+      const uint4 *kp = (const uint4 *)(kc + (row0 + k0) * DH);   // U rows x 16
       const uint4 *vp = (const uint4 *)(vc + (row0 + k0) * DH);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) kr[i] = kp[i];
+      for (int i = 0; i < NKV; ++i) kr[i] = kp[i];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) vr4[i] = vp[i];
+      for (int i = 0; i < NKV; ++i) vr4[i] = vp[i];
     }
     // element (key i, column j) of the unit's keys and values
     auto kval = [&](int i, int j) -> float {
@@ -1464,67 +1470,70 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
         return __uint_as_float(e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w);
       }
     };
-    // both queries in one pass over the unit (each key and value element is
-    // widened once); a query that does not exist (P = 1) sees only masked keys
-    float sc0[U], sc1[U], mx0 = -INFINITY, mx1 = -INFINITY;
+    // every query in one pass over the unit (each key and value element is
+    // widened once); query p sees keys up to position pos0 + p
+    float sc[QN][U], mx[QN];
+#pragma unroll
+    for (int p = 0; p < QN; ++p) mx[p] = -INFINITY;
 #pragma unroll
     for (int i = 0; i < U; ++i) {
-      float a0 = 0.f, a1 = 0.f;
+      float a[QN];
+#pragma unroll
+      for (int p = 0; p < QN; ++p) a[p] = 0.f;
 #pragma unroll
       for (int j = 0; j < DH; ++j) {
         const float kv = kval(i, j);
-        a0 += q[0][j] * kv;
-        a1 += q[1][j] * kv;
+#pragma unroll
+        for (int p = 0; p < QN; ++p) a[p] += q[p][j] * kv;
       }
       const int pos = k0 + i;
-      sc0[i] = (pos < n_keys && pos <= pos0) ? a0 : -INFINITY;
-      sc1[i] = (P > 1 && pos < n_keys && pos <= pos0 + 1) ? a1 : -INFINITY;
-      mx0 = fmaxf(mx0, sc0[i]);
-      mx1 = fmaxf(mx1, sc1[i]);
-    }
-    const float mn0 = fmaxf(m[0], mx0), mn1 = fmaxf(m[1], mx1);
-    // rescale factors (1 while a query has seen no key, its state being zero)
-    const float al0 = (mn0 == -INFINITY) ? 1.f : expf(m[0] - mn0);
-    const float al1 = (mn1 == -INFINITY) ? 1.f : expf(m[1] - mn1);
-    float e0[U], e1[U];
-    l[0] *= al0;
-    l[1] *= al1;
 #pragma unroll
-    for (int i = 0; i < U; ++i) {
-      e0[i] = (sc0[i] == -INFINITY) ? 0.f : expf(sc0[i] - mn0);
-      e1[i] = (sc1[i] == -INFINITY) ? 0.f : expf(sc1[i] - mn1);
-      l[0] += e0[i];
-      l[1] += e1[i];
+      for (int p = 0; p < QN; ++p) {
+        sc[p][i] = (pos < n_keys && pos <= pos0 + p) ? a[p] : -INFINITY;
+        mx[p] = fmaxf(mx[p], sc[p][i]);
+      }
+    }
+    float al[QN], ex[QN][U];
+#pragma unroll
+    for (int p = 0; p < QN; ++p) {
+      const float mn = fmaxf(m[p], mx[p]);
+      // rescale factor (1 while a query has seen no key, its state being zero)
+      al[p] = (mn == -INFINITY) ? 1.f : expf(m[p] - mn);
+      l[p] *= al[p];
+#pragma unroll
+      for (int i = 0; i < U; ++i) {
+        ex[p][i] = (sc[p][i] == -INFINITY) ? 0.f : expf(sc[p][i] - mn);
+        l[p] += ex[p][i];
+      }
+      m[p] = mn;
     }
     // slots at or past n_keys hold stale or unwritten values: a zero weight
     // times a non-finite value would still poison the sum, so they are skipped
 #pragma unroll
     for (int j = 0; j < DH; ++j) {
-      float s0 = o[0][j] * al0, s1 = o[1][j] * al1;
+      float sp[QN];
+#pragma unroll
+      for (int p = 0; p < QN; ++p) sp[p] = o[p][j] * al[p];
 #pragma unroll
       for (int i = 0; i < U; ++i) {
         const float vv = (k0 + i < n_keys) ? vval(i, j) : 0.f;
-        s0 += e0[i] * vv;
-        s1 += e1[i] * vv;
+#pragma unroll
+        for (int p = 0; p < QN; ++p) sp[p] += ex[p][i] * vv;
       }
-      o[0][j] = s0;
-      o[1][j] = s1;
+#pragma unroll
+      for (int p = 0; p < QN; ++p) o[p][j] = sp[p];
     }
-    m[0] = mn0;
-    m[1] = mn1;
   }
   // merge the threads of each head: per wave first, then across the head's waves
   const int wph = tph >> 6;   // waves per head (1, 2 or 4)
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    if (p >= P) break;
+  for (int p = 0; p < QN; ++p) {
     const float mw = wave_max(m[p]);
     if (lane == 0) red[wave * 36 + p * 18] = mw;
   }
   lds_barrier();
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    if (p >= P) break;
+  for (int p = 0; p < QN; ++p) {
     float M = -INFINITY;
     for (int w = h * wph; w < (h + 1) * wph; ++w) M = fmaxf(M, red[w * 36 + p * 18]);
     const float f = (m[p] == -INFINITY) ? 0.f : expf(m[p] - M);
@@ -1547,7 +1556,7 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
     if ((lane & 3) == 0) red[wave * 36 + p * 18 + 2 + (lane >> 2)] = oc;
   }
   lds_barrier();
-  for (int idx = tid; idx < P * H * DH; idx += blockDim.x) {
+  for (int idx = tid; idx < QN * H * DH; idx += blockDim.x) {
     const int p = idx / (H * DH), rest = idx - p * H * DH, hh = rest / DH, j = rest - hh * DH;
     float L = 0.f, O = 0.f;
     for (int w = hh * wph; w < (hh + 1) * wph; ++w) {
@@ -1852,7 +1861,8 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
           });
       __syncthreads();   // keys and values in the cache before the attention reads them
       if (H <= 4 && !a.attn_mfma)
-        wg_attention_valu<ELT>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
+        P == 2 ? wg_attention_valu<ELT, 2>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red)
+               : wg_attention_valu<ELT, 1>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       else
         wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       lds_barrier();
