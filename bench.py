@@ -186,7 +186,8 @@ def cpu_baseline(wl, gamma, wt, wd, ht, hk, budget_s, max_seqs):
     sequences x 16 events, the sample grows (events per sequence first, up to
     n_gen, then sequences, up to max_seqs) by the ratio of the budget to the
     last run's time, until a run takes at least half the budget or the sample
-    is the whole allowed job. The last run is reported."""
+    is the whole allowed job; a whole job shorter than half the budget is
+    repeated to about three quarters of it. The last run is reported."""
     from threadpoolctl import threadpool_limits
 
     from oracle import sampler as S
@@ -205,10 +206,20 @@ def cpu_baseline(wl, gamma, wt, wd, ht, hk, budget_s, max_seqs):
             e2 = int(min(wl.n_gen, n_events * grow))
             n_seq = int(min(top_seq, max(n_seq, n_seq * grow * n_events / e2)))
             n_events = e2
-    ev = int(st.gen.sum())
+        ev = int(st.gen.sum())
+        reps = 1
+        if dt < 0.5 * budget_s:
+            # the whole allowed job is shorter than the budget: repeat it
+            reps = int(min(20, np.ceil(0.75 * budget_s / max(dt, 1e-3))))
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                st = S.sample_sd(T, D, ht[:n_seq], hk[:n_seq], n_events, gamma, seed=1234)
+            dt = time.perf_counter() - t0
+            ev = int(st.gen.sum()) * reps
     return {"value": ev / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
             "sample": f"{n_seq} sequences x first {n_events} generated events of {wl.name} "
-                      f"(TPP-SD, gamma={gamma}), float64 NumPy, {dt:.1f} s"}
+                      f"(TPP-SD, gamma={gamma}){f', {reps} repetitions' if reps > 1 else ''}, "
+                      f"float64 NumPy, {dt:.1f} s"}
 
 
 def window_jobs(args, wl, gamma, sd, ar, HT, HK, ht, n_gen, B):
