@@ -96,26 +96,24 @@ def verify_pass_fraction(wl, gamma, B, verify_ms):
 
 
 def verify_gemm_bytes(wl, gamma, B):
-    """Algorithmic HBM bytes of the GEMM launches of one verify pass (every
-    layer's products and the decoder's first one, the launches timed as
-    verify GEMMs): each operand read once, each output written once. THP
-    layer: q, k, v from the LayerNorm's fp32 input; output projection and
-    second FFN product read-modify-write the fp32 residual; the FFN hidden
-    goes out and back. AttNHP layer: one product over the 2d-wide [z; h]."""
+    """Algorithmic HBM bytes of the GEMM part of one verify pass: what the
+    products must move at least, whatever the kernels. THP layer: its
+    attention output o in, the residual stream x in and out, its q, k, v out
+    (once per layer), the layer's matrices once; plus the first layer's
+    LayerNorm input and the decoder's first product (LN_f(x) in, [E; V_k1]
+    out). The layered kernels move more (the FFN hidden activations out and
+    back, x re-read per product); the fused layer kernel moves this. AttNHP
+    layer: one product over the 2d-wide [z; h] in, q, k, v out."""
     c = wl.target
     elt = 2 if c.prec == "bf16" else 4
     d, F, L = c.d_model, c.d_ffn, c.n_layers
     T = B * (gamma + 1)
     if getattr(c, "encoder", "thp") == "attnhp":
-        layer = T * 2 * d * elt + 6 * d * d * elt + T * 3 * d * elt
+        layers = L * (T * 2 * d * elt + 6 * d * d * elt + T * 3 * d * elt)
     else:
-        qkv = T * d * 4 + 3 * d * d * elt + T * 3 * d * elt
-        out = T * d * elt + d * d * elt + T * d * 8
-        ffn1 = T * d * 4 + d * F * elt + T * F * elt
-        ffn2 = T * F * elt + F * d * elt + T * d * 8
-        layer = qkv + out + ffn1 + ffn2
+        layers = L * (T * d * elt + T * d * 8 + T * 3 * d * elt + (4 * d * d + 2 * d * F) * elt) + T * d * 4
     dec = T * d * 4 + 4 * d * d * elt + T * 4 * d * elt
-    return float(L * layer + dec)
+    return float(layers + dec)
 
 
 def gamma_sweep(args, wl, tm, dm, HT, HK, ar_value, B, n_gen):

@@ -206,6 +206,9 @@ struct tppsd_state {
   bool block_path = true;              // k_block for the models it serves (TPPSD_LAYERED=1: layered kernels)
   bool verify_seq = true;              // k_verify_seq for the targets it serves (TPPSD_LAYERED=1: off)
   float *attn_part = nullptr;
+  char *packT = nullptr;               // target weights in fragment order (nullptr: no fused layer kernel)
+  size_t pack_layer = 0;
+  bool packs_built = false;
   int32_t *gen0 = nullptr;
   // internal round buffers (tppsd_sample_sd)
   tppsd_draft_buf idr{};
@@ -256,6 +259,7 @@ struct WsLayout {
   size_t freqT, freqD, kT, vT, kD, vD, layerT, layerD;
   size_t x, a, q, o, hid, e, u, ar_mix, ar_lt, attn_part, gen0;
   size_t logits, hwT, hbT, hwD, hbD;
+  size_t packT = 0, pack_layer = 0;   // target weights in MFMA fragment order (fused layer kernel), per layer
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt, d_rate;
   size_t v_logg, v_logf, v_mix, v_lt;
   size_t a_L, a_nnew, a_knew, a_tnew, a_taunew, a_ar, a_flags;
@@ -312,6 +316,11 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
   w.hbT = take((size_t)(3 * T->cfg.n_mix + T->cfg.n_types) * 4);
   w.hwD = take(D ? (size_t)(3 * D->cfg.n_mix + D->cfg.n_types) * 4 * D->d() * D->act_bytes() : 0);
   w.hbD = take(D ? (size_t)(3 * D->cfg.n_mix + D->cfg.n_types) * 4 : 0);
+  if (!T->attnhp() && layer_fused_ok(T->bf16(), T->d(), T->cfg.d_ffn)) {
+    const size_t d = T->d(), F = T->cfg.d_ffn;
+    w.pack_layer = (4 * d * d + 2 * d * F) * 2;   // Wo, W1, W2, Wqkv (bf16)
+    w.packT = take(w.pack_layer * T->cfg.n_layers);
+  }
   w.ar_mix = take(Bz * 3 * mmax * 4);
   w.ar_lt = take(Bz * kmax * 4);
   {
@@ -471,11 +480,11 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
   }
   // the row-local part of each layer in one launch (output projection, FFN
   // with its hidden activations on chip, the next layer's q, k, v) where
-  // there is an instance for the widths and the row tiles fill the chip;
+  // there is an instance for the widths and enough rows to beat the layered kernels;
   // TPPSD_FFN_FUSED=0 / 1 forces the layered / fused form
   const char *ff = getenv("TPPSD_FFN_FUSED");
-  const bool use_layer_fused = fuse_ln && !m->attnhp() && layer_fused_ok(bf, d, F) &&
-                               (ff ? ff[0] == '1' : (long)T >= 256L * layer_fused_rows(d));
+  const bool use_layer_fused = fuse_ln && !m->attnhp() && m == s->T && s->packT && layer_fused_ok(bf, d, F) &&
+                               (ff ? ff[0] == '1' : layer_fused_worth(d, T));
   auto qkv_epi = [&](int l) {
     Epi e{};
     e.mode = EPI_QKV;
@@ -510,20 +519,21 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
       LayerArgs la{};
       la.x = s->x;
       la.o = (const bf16_t *)s->o;
-      la.wo = (const bf16_t *)w.out_w;
+      const char *pk = s->packT + s->pack_layer * l;   // Wo, W1, W2 of this layer, fragment order
+      la.wo = (const bf16_t *)pk;
       la.bo = w.out_b;
       la.ln2_g = w.ln2_g;
       la.ln2_b = w.ln2_b;
-      la.w1 = (const bf16_t *)w.ffn1_w;
+      la.w1 = (const bf16_t *)(pk + (size_t)d * d * 2);
       la.b1 = w.ffn1_b;
-      la.w2 = (const bf16_t *)w.ffn2_w;
+      la.w2 = (const bf16_t *)(pk + (size_t)(d * d + F * d) * 2);
       la.b2 = w.ffn2_b;
       const bool post = l + 1 < L;
       if (post) {
         const LayerW &wn = m->layers[l + 1];
         la.ln1_g = wn.ln1_g;
         la.ln1_b = wn.ln1_b;
-        la.wqkv = (const bf16_t *)wn.qkv_w;
+        la.wqkv = (const bf16_t *)(s->packT + s->pack_layer * (l + 1) + (size_t)(d * d + 2 * F * d) * 2);
         la.qe = qkv_epi(l + 1);
       }
       la.T = T;
@@ -1003,6 +1013,8 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->e = ws + w.e;
   s->u = ws + w.u;
   s->logits = (float *)(ws + w.logits);
+  s->packT = w.pack_layer ? ws + w.packT : nullptr;
+  s->pack_layer = w.pack_layer;
   s->cT.head_w = ws + w.hwT;
   s->cT.head_b = (float *)(ws + w.hbT);
   if (D) {
@@ -1126,6 +1138,19 @@ int tppsd_prefill_window(tppsd_state *s, const float *d_t, const int32_t *d_k, i
                         c.head_w, c.head_b, st);
     }
     s->heads_built = true;
+  }
+  if (s->packT && !s->packs_built) {
+    const tppsd_model *m = s->T;
+    const int d = m->d(), F = m->cfg.d_ffn;
+    for (int l = 0; l < m->cfg.n_layers; ++l) {
+      const LayerW &w = m->layers[l];
+      char *p = s->packT + s->pack_layer * l;
+      launch_pack_frags(w.out_w, d, d, p, st);
+      launch_pack_frags(w.ffn1_w, F, d, p + (size_t)d * d * 2, st);
+      launch_pack_frags(w.ffn2_w, d, F, p + (size_t)(d * d + F * d) * 2, st);
+      launch_pack_frags(w.qkv_w, 3 * d, d, p + (size_t)(d * d + 2 * F * d) * 2, st);
+    }
+    s->packs_built = true;
   }
   launch_prefill_init(d_t, d_k, s->B, n0, n_gen, d_t_end, s->ev_t, s->ev_k, s->cap, s->n, s->gen, s->lenT, s->lenD,
                       s->done, s->rnd, s->zeros, s->t_end, s->ll, s->n_done, s->status, s->acc_stats, st);

@@ -246,10 +246,11 @@ bool gemm_ln_fusable(int bf16, int K);
 // Fused row-local part of a bf16 THP layer between two attention launches
 // (output projection + residual, feed-forward block + residual, and with
 // post the next layer's LayerNorm and q, k, v through qe), one launch over
-// tiles of layer_fused_rows(d) rows; layer_fused_ok: there is an instance
+// row tiles; layer_fused_ok: there is an instance; layer_fused_worth: it
+// beats the layered kernels at T rows
 struct LayerArgs {
   float *x;                                  // [T][D] residual stream (in / out)
-  const bf16_t *o, *wo;                      // attention output [T][D], Wo [D][D]
+  const bf16_t *o, *wo;                      // attention output [T][D], Wo [D][D] (weights: packed fragments)
   const float *bo;
   const float *ln2_g, *ln2_b, *b1, *b2;
   const bf16_t *w1, *w2;                     // [F][D], [D][F]
@@ -259,7 +260,10 @@ struct LayerArgs {
   int T;
 };
 bool layer_fused_ok(int bf16, int d, int F);
-int layer_fused_rows(int d);
+// W [N][K] bf16 into the MFMA fragment order k_layer_fused reads (N % 16 == 0,
+// K % 32 == 0; out holds N K elements)
+void launch_pack_frags(const void *W, int N, int K, void *out, hipStream_t s);
+bool layer_fused_worth(int d, long T);
 void launch_layer_fused(const LayerArgs &a, int d, int F, bool post, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 // decoder epilogue over the rows' logits [.., ldl] (mixture w | mu | log sigma, then types)
 void launch_head(const float *logits, int ldl, int M, int K, const HeadArgs &a, hipStream_t st);

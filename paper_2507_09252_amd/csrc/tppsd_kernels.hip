@@ -657,6 +657,23 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// W [N][K] (bf16, N a multiple of 16, K of 32) into MFMA operand fragments:
+// fragment (nt, ks) holds, for lane l = 16 g + r, W[16 nt + r][32 ks + 8 g ..
+// + 7] at ((nt K/32 + ks) 64 + l) 8, so that a wave reads one fragment as 1 KB
+// of contiguous memory
+__global__ void k_pack_frags(const bf16_t *__restrict__ W, int N, int K, bf16_t *__restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;   // one 16-byte vector per thread
+  const int KS = K / 32, total = (N / 16) * KS * 64;
+  if (i >= total) return;
+  const int l = i & 63, f = i >> 6, nt = f / KS, ks = f - nt * KS;
+  *(uint4 *)(out + (size_t)i * 8) = *(const uint4 *)(W + (size_t)(16 * nt + (l & 15)) * K + 32 * ks + 8 * (l >> 4));
+}
+
+void launch_pack_frags(const void *W, int N, int K, void *out, hipStream_t s) {
+  const int total = (N / 16) * (K / 32) * 64;
+  k_pack_frags<<<(total + 255) / 256, 256, 0, s>>>((const bf16_t *)W, N, K, (bf16_t *)out);
+}
+
 template <int D, int F, int BM, int FC, bool PRE, bool POST>
 __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
   constexpr int XLD = D + 4, ALD = D + 8, HLD = FC + 8;   // row strides (pads spread LDS banks)
@@ -678,6 +695,12 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
     rpos[tid] = a.qe.start[bq] + a.qe.start_off + (r - bq * a.qe.P);
   }
   const bf16_t *W1 = a.w1, *W2 = a.w2;
+  // weights are pre-packed in MFMA fragment order (k_pack_frags): fragment
+  // (16-row tile nt, 32-column step ks) of a matrix with KS steps per row is
+  // 64 lanes x 16 bytes, contiguous
+  auto frag = [&](const bf16_t *Wp, int nt, int KS, int ks) {
+    return *(const bf16x8_t *)(Wp + ((size_t)(nt * KS + ks) * 64 + lane) * 8);
+  };
   // first FFN product's weights of chunk c: wave's hidden columns c FC + wave FC/4 + 16 j + rr
   bf16x8_t w1f[2][TNA][KSD];
   auto load_w1 = [&](int c, bf16x8_t (&dst)[TNA][KSD]) {
@@ -685,7 +708,7 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
     for (int j = 0; j < TNA; ++j)
 #pragma unroll
       for (int ks = 0; ks < KSD; ++ks)
-        dst[j][ks] = *(const bf16x8_t *)(W1 + (size_t)(c * FC + wave * (FC / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
+        dst[j][ks] = frag(W1, c * (FC / 16) + wave * (FC / 64) + j, KSD, ks);
   };
   // LayerNorm of the xs rows into as (bf16): wave w normalises rows
   // w BM/4 + 4 p + g, 16 lanes per row; v holds the rows' values
@@ -739,7 +762,7 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
     for (int j = 0; j < TNB; ++j)
 #pragma unroll
       for (int ks = 0; ks < KSD; ++ks)
-        wf[j][ks] = *(const bf16x8_t *)(W + (size_t)(wave * (D / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
+        wf[j][ks] = frag(W, wave * (D / 64) + j, KSD, ks);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -816,7 +839,7 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
     for (int j = 0; j < TNB; ++j)
 #pragma unroll
       for (int ks = 0; ks < KSB; ++ks)
-        w2f[j][ks] = *(const bf16x8_t *)(W2 + (size_t)(wave * (D / 4) + 16 * j + rr) * F + c * FC + 32 * ks + 8 * g);
+        w2f[j][ks] = frag(W2, wave * (D / 64) + j, F / 32, c * (FC / 32) + ks);
     // hidden chunk: ReLU(A W1_c^T + b1) -> bf16 -> LDS
     f32x4_t acc_h[TM][TNA];
 #pragma unroll
@@ -864,7 +887,7 @@ __global__ __launch_bounds__(256) void k_layer_fused(LayerArgs a) {
     for (int j = 0; j < TNQ; ++j)
 #pragma unroll
       for (int ks = 0; ks < KSD; ++ks)
-        dst[j][ks] = *(const bf16x8_t *)(a.wqkv + (size_t)(c * QC + wave * (QC / 4) + 16 * j + rr) * D + 32 * ks + 8 * g);
+        dst[j][ks] = frag(a.wqkv, c * (QC / 16) + wave * (QC / 64) + j, KSD, ks);
   };
   if (POST) {
     load_wq(0, wq[0]);
@@ -3008,18 +3031,25 @@ static void gemm_dispatch(const void *X, const LnA *ln, const void *W, int T, in
 
 bool layer_fused_ok(int bf16, int d, int F) { return bf16 && ((d == 128 && F == 512) || (d == 256 && F == 1024)); }
 
-int layer_fused_rows(int d) { return d == 128 ? 64 : 32; }
+// Where the fused layer kernel is used by default: at d = 128 from 8192 rows
+// (32-row tiles; measured at 36864 rows: verify pass 1121 -> 810 us), at
+// d = 256 from 2048 rows (16-row tiles; at 2816 rows 501 -> 461 us; with
+// 32-row tiles it only matched the layered GEMMs)
+bool layer_fused_worth(int d, long T) { return d == 128 ? T >= 8192 : T >= 2048; }
 
 void launch_layer_fused(const LayerArgs &a, int d, int F, bool post, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   auto go = [&](auto kern, int bm) {
     hipExtLaunchKernelGGL(kern, dim3((a.T + bm - 1) / bm), dim3(256), 0, s, ev0, ev1, 0, a);
   };
+  // 32-row tiles: with the weights in fragment order, twice the workgroups
+  // beat the halved weight traffic of 64-row tiles (36864 rows at d = 128:
+  // 46 vs 58 us per layer)
   if (d == 128 && F == 512) {
-    if (post) go(k_layer_fused<128, 512, 64, 128, true, true>, 64);
-    else go(k_layer_fused<128, 512, 64, 128, true, false>, 64);
+    if (post) go(k_layer_fused<128, 512, 32, 128, true, true>, 32);
+    else go(k_layer_fused<128, 512, 32, 128, true, false>, 32);
   } else {
-    if (post) go(k_layer_fused<256, 1024, 32, 64, true, true>, 32);
-    else go(k_layer_fused<256, 1024, 32, 64, true, false>, 32);
+    if (post) go(k_layer_fused<256, 1024, 16, 64, true, true>, 16);
+    else go(k_layer_fused<256, 1024, 16, 64, true, false>, 16);
   }
 }
 
