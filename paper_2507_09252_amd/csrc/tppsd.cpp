@@ -208,6 +208,8 @@ struct tppsd_state {
   float *attn_part = nullptr;
   char *packT = nullptr;               // target weights in fragment order (nullptr: no fused layer kernel)
   size_t pack_layer = 0;
+  char *packD = nullptr;               // draft weights in fragment order
+  size_t pack_layerD = 0;
   bool packs_built = false;
   int32_t *gen0 = nullptr;
   // internal round buffers (tppsd_sample_sd)
@@ -260,6 +262,7 @@ struct WsLayout {
   size_t x, a, q, o, hid, e, u, ar_mix, ar_lt, attn_part, gen0;
   size_t logits, hwT, hbT, hwD, hbD;
   size_t packT = 0, pack_layer = 0;   // target weights in MFMA fragment order (fused layer kernel), per layer
+  size_t packD = 0, pack_layerD = 0;  // the same for the draft model
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt, d_rate;
   size_t v_logg, v_logf, v_mix, v_lt;
   size_t a_L, a_nnew, a_knew, a_tnew, a_taunew, a_ar, a_flags;
@@ -320,6 +323,11 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
     const size_t d = T->d(), F = T->cfg.d_ffn;
     w.pack_layer = (4 * d * d + 2 * d * F) * 2;   // Wo, W1, W2, Wqkv (bf16)
     w.packT = take(w.pack_layer * T->cfg.n_layers);
+  }
+  if (D && !D->attnhp() && layer_fused_ok(D->bf16(), D->d(), D->cfg.d_ffn)) {
+    const size_t d = D->d(), F = D->cfg.d_ffn;
+    w.pack_layerD = (4 * d * d + 2 * d * F) * 2;
+    w.packD = take(w.pack_layerD * D->cfg.n_layers);
   }
   w.ar_mix = take(Bz * 3 * mmax * 4);
   w.ar_lt = take(Bz * kmax * 4);
@@ -483,7 +491,9 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
   // there is an instance for the widths and enough rows to beat the layered kernels;
   // TPPSD_FFN_FUSED=0 / 1 forces the layered / fused form
   const char *ff = getenv("TPPSD_FFN_FUSED");
-  const bool use_layer_fused = fuse_ln && !m->attnhp() && m == s->T && s->packT && layer_fused_ok(bf, d, F) &&
+  char *const pack = m == s->T ? s->packT : s->packD;   // this model's weights in fragment order
+  const size_t pack_layer = m == s->T ? s->pack_layer : s->pack_layerD;
+  const bool use_layer_fused = fuse_ln && !m->attnhp() && pack && layer_fused_ok(bf, d, F) &&
                                (ff ? ff[0] == '1' : layer_fused_worth(d, T));
   auto qkv_epi = [&](int l) {
     Epi e{};
@@ -519,7 +529,7 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
       LayerArgs la{};
       la.x = s->x;
       la.o = (const bf16_t *)s->o;
-      const char *pk = s->packT + s->pack_layer * l;   // Wo, W1, W2 of this layer, fragment order
+      const char *pk = pack + pack_layer * l;   // Wo, W1, W2 of this layer, fragment order
       la.wo = (const bf16_t *)pk;
       la.bo = w.out_b;
       la.ln2_g = w.ln2_g;
@@ -533,7 +543,7 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
         const LayerW &wn = m->layers[l + 1];
         la.ln1_g = wn.ln1_g;
         la.ln1_b = wn.ln1_b;
-        la.wqkv = (const bf16_t *)(s->packT + s->pack_layer * (l + 1) + (size_t)(d * d + 2 * F * d) * 2);
+        la.wqkv = (const bf16_t *)(pack + pack_layer * (l + 1) + (size_t)(d * d + 2 * F * d) * 2);
         la.qe = qkv_epi(l + 1);
       }
       la.T = T;
@@ -1015,6 +1025,8 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->logits = (float *)(ws + w.logits);
   s->packT = w.pack_layer ? ws + w.packT : nullptr;
   s->pack_layer = w.pack_layer;
+  s->packD = w.pack_layerD ? ws + w.packD : nullptr;
+  s->pack_layerD = w.pack_layerD;
   s->cT.head_w = ws + w.hwT;
   s->cT.head_b = (float *)(ws + w.hbT);
   if (D) {
@@ -1139,16 +1151,21 @@ int tppsd_prefill_window(tppsd_state *s, const float *d_t, const int32_t *d_k, i
     }
     s->heads_built = true;
   }
-  if (s->packT && !s->packs_built) {
-    const tppsd_model *m = s->T;
-    const int d = m->d(), F = m->cfg.d_ffn;
-    for (int l = 0; l < m->cfg.n_layers; ++l) {
-      const LayerW &w = m->layers[l];
-      char *p = s->packT + s->pack_layer * l;
-      launch_pack_frags(w.out_w, d, d, p, st);
-      launch_pack_frags(w.ffn1_w, F, d, p + (size_t)d * d * 2, st);
-      launch_pack_frags(w.ffn2_w, d, F, p + (size_t)(d * d + F * d) * 2, st);
-      launch_pack_frags(w.qkv_w, 3 * d, d, p + (size_t)(d * d + 2 * F * d) * 2, st);
+  if (!s->packs_built) {
+    for (int which = 0; which < 2; ++which) {
+      const tppsd_model *m = which ? s->D : s->T;
+      char *base = which ? s->packD : s->packT;
+      const size_t stride = which ? s->pack_layerD : s->pack_layer;
+      if (!m || !base) continue;
+      const int d = m->d(), F = m->cfg.d_ffn;
+      for (int l = 0; l < m->cfg.n_layers; ++l) {
+        const LayerW &w = m->layers[l];
+        char *p = base + stride * l;
+        launch_pack_frags(w.out_w, d, d, p, st);
+        launch_pack_frags(w.ffn1_w, F, d, p + (size_t)d * d * 2, st);
+        launch_pack_frags(w.ffn2_w, d, F, p + (size_t)(d * d + F * d) * 2, st);
+        launch_pack_frags(w.qkv_w, 3 * d, d, p + (size_t)(d * d + 2 * F * d) * 2, st);
+      }
     }
     s->packs_built = true;
   }

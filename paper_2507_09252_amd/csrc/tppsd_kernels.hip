@@ -3032,10 +3032,12 @@ static void gemm_dispatch(const void *X, const LnA *ln, const void *W, int T, in
 bool layer_fused_ok(int bf16, int d, int F) { return bf16 && ((d == 128 && F == 512) || (d == 256 && F == 1024)); }
 
 // Where the fused layer kernel is used by default: at d = 128 from 8192 rows
-// (32-row tiles; measured at 36864 rows: verify pass 1121 -> 810 us), at
-// d = 256 from 2048 rows (16-row tiles; at 2816 rows 501 -> 461 us; with
-// 32-row tiles it only matched the layered GEMMs)
-bool layer_fused_worth(int d, long T) { return d == 128 ? T >= 8192 : T >= 2048; }
+// (32-row tiles; measured at 36864 rows: verify pass 1121 -> 810 us) and up
+// to 64 rows (one or two tiles replacing four launches: the 32-sequence
+// draft, 1364 -> 1346 us per round), at d = 256 from 2048 rows (16-row
+// tiles; at 2816 rows 501 -> 461 us; with 32-row tiles it only matched the
+// layered GEMMs)
+bool layer_fused_worth(int d, long T) { return d == 128 ? (T >= 8192 || T <= 64) : T >= 2048; }
 
 void launch_layer_fused(const LayerArgs &a, int d, int F, bool post, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   auto go = [&](auto kern, int bm) {
