@@ -58,20 +58,8 @@ __device__ int sample_cat(const float *logp, int n, float u) {
   return n - 1;
 }
 
-// Wave-parallel forms of the two helpers above for n, M <= 64 (lane m holds
-// entry m): the running sum is an inclusive scan across the wave.
-__device__ int wave_sample_cat(const float *logp, int n, float u) {
-  const int lane = threadIdx.x & 63;
-  float c = lane < n ? expf(logp[lane]) : 0.f;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float o = __shfl_up(c, off, 64);
-    if (lane >= off) c += o;
-  }
-  const float tot = __shfl(c, n - 1, 64);
-  const unsigned long long hit = __ballot(lane < n && u * tot < c);
-  return hit ? (int)__builtin_ctzll(hit) : n - 1;
-}
+// Wave-parallel form of the mixture log-density above for M <= 64 (lane m
+// holds component m).
 __device__ float wave_mix_logpdf(const float *logw, const float *mu, const float *s, int M, float tau) {
   const int lane = threadIdx.x & 63;
   const float lt = logf(tau);
@@ -1837,8 +1825,9 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
   if (tid < a.gamma) {   // the uniforms depend only on the counters: drawn up front, off the step chain
     float u[4];
     philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)(tid + 1), TAG_DRAFT, u);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pu[tid][i] = u[i];
+    pu[tid][0] = u[0];
+    pu[tid][1] = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);   // Box-Muller epsilon
+    pu[tid][3] = u[3];
   }
   for (int l = 1; l <= a.gamma; ++l) {
     const int P = (l == 1) ? 2 : 1;
@@ -1928,35 +1917,59 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
         [&](int, int nn, float acc) { hv[nn] = acc + (nn < 3 * M ? mix_b[nn] : k2_b[nn - 3 * M]); });
     lds_barrier();
     if (tid < 64) {
+      // wave 0, from registers: the log-softmaxes of the mixture weights and
+      // the types, the draft record, and the draft event (component,
+      // Box-Muller interval, type)
       const int lane = tid;
       const float lw = lane < M ? hv[lane] : -INFINITY;
+      const float mu_l = lane < M ? hv[M + lane] : 0.f, s_l = lane < M ? hv[2 * M + lane] : 0.f;
+      const float lk = lane < K ? hv[3 * M + lane] : -INFINITY;
       const float mw2 = wave_max(lw);
       const float sw = wave_sum(lane < M ? expf(lw - mw2) : 0.f);
-      const float lk = lane < K ? hv[3 * M + lane] : -INFINITY;
       const float mk = wave_max(lk);
       const float sk = wave_sum(lane < K ? expf(lk - mk) : 0.f);
-      if (lane < M) hv[lane] = lw - mw2 - logf(sw);
-      if (lane < K) hv[3 * M + lane] = lk - mk - logf(sk);
-    }
-    lds_barrier();
-    const size_t di = (size_t)b * a.MG + (l - 1);
-    for (int i = tid; i < 3 * M; i += blockDim.x) a.d_mix[di * 3 * M + i] = hv[i];
-    for (int i = tid; i < K; i += blockDim.x) a.d_logtype[di * K + i] = hv[3 * M + i];
-    if (tid < 64) {
-      // the draft event, drawn by wave 0: component, Box-Muller interval, type
+      const float nlw = lw - mw2 - logf(sw), nlk = lk - mk - logf(sk);
+      const size_t di = (size_t)b * a.MG + (l - 1);
+      if (lane < M) {
+        a.d_mix[di * 3 * M + lane] = nlw;
+        a.d_mix[di * 3 * M + M + lane] = mu_l;
+        a.d_mix[di * 3 * M + 2 * M + lane] = s_l;
+      }
+      if (lane < K) a.d_logtype[di * K + lane] = nlk;
+      // first index whose running sum of exp(log p) exceeds u times the total
+      auto draw = [&](float lp, int n, float u) {
+        float c = lane < n ? expf(lp) : 0.f;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const float o = __shfl_up(c, off, 64);
+          if (lane >= off) c += o;
+        }
+        const float tot = __shfl(c, n - 1, 64);
+        const unsigned long long hit = __ballot(lane < n && u * tot < c);
+        return hit ? (int)__builtin_ctzll(hit) : n - 1;
+      };
+      auto at = [](float v, int i) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i)); };
       const float *u = pu[l - 1];
-      const int z = wave_sample_cat(hv, M, u[0]);
-      const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
-      const float tau = expf(hv[M + z] + expf(hv[2 * M + z]) * eps);
-      const int kk = wave_sample_cat(hv + 3 * M, K, u[3]);
-      const float lg = wave_mix_logpdf(hv, hv + M, hv + 2 * M, M, tau);
+      const int z = draw(nlw, M, u[0]);
+      const float tau = expf(at(mu_l, z) + expf(at(s_l, z)) * u[1]);
+      const int kk = draw(nlk, K, u[3]);
+      // log g of the drawn interval under the draft mixture
+      const float lt = logf(tau);
+      float c = -INFINITY;
+      if (lane < M) {
+        const float zz = lt - mu_l;
+        c = nlw - s_l - 0.918938533204672742f - lt - 0.5f * zz * zz * expf(-2.f * s_l);
+      }
+      const float cm = wave_max(c);
+      const float lg = cm + logf(wave_sum(lane < M ? expf(c - cm) : 0.f));
+      const float lf = at(nlk, kk);
       if (tid == 0) {
         const float tn = t_last + tau;
         a.d_tau[di] = tau;
         a.d_t[di] = tn;
         a.d_k[di] = kk;
         a.d_logg[di] = lg;
-        a.d_logf[di] = hv[3 * M + kk];
+        a.d_logf[di] = lf;
         if (!isfinite(tau)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
         tok_t[0] = tn;
         tok_k[0] = kk;
