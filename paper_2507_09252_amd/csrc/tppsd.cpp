@@ -172,6 +172,11 @@ struct tppsd_model {
 struct ModelCache {
   void *head_w = nullptr;   // decoder block-diagonal matrix [(3M + K)][4d]
   float *head_b = nullptr;  // and bias [3M + K]
+  // the matrices k_block and k_verify_seq read, in their packed order
+  // (launch_pack_wbatch), for models of the widths they serve
+  char *wb = nullptr;
+  std::vector<const void *> wb_qkv, wb_out, wb_f1, wb_f2;
+  const void *wb_ek1 = nullptr, *wb_head = nullptr;
   // per layer: keys [B][H][kv_cap][dh]; values the same for fp32, in
   // 8-position blocks [B][H][kv_cap / 8][dh][8] for bf16
   char *k = nullptr, *v = nullptr;
@@ -211,6 +216,7 @@ struct tppsd_state {
   char *packD = nullptr;               // draft weights in fragment order
   size_t pack_layerD = 0;
   bool packs_built = false;
+  bool wb_built = false;
   int32_t *gen0 = nullptr;
   // internal round buffers (tppsd_sample_sd)
   tppsd_draft_buf idr{};
@@ -263,6 +269,7 @@ struct WsLayout {
   size_t logits, hwT, hbT, hwD, hbD;
   size_t packT = 0, pack_layer = 0;   // target weights in MFMA fragment order (fused layer kernel), per layer
   size_t packD = 0, pack_layerD = 0;  // the same for the draft model
+  size_t wbT = 0, wbD = 0, wb_nT = 0, wb_nD = 0;   // matrices in the k_block order (0 bytes: not served)
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt, d_rate;
   size_t v_logg, v_logf, v_mix, v_lt;
   size_t a_L, a_nnew, a_knew, a_tnew, a_taunew, a_ar, a_flags;
@@ -324,6 +331,19 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
     w.pack_layer = (4 * d * d + 2 * d * F) * 2;   // Wo, W1, W2, Wqkv (bf16)
     w.packT = take(w.pack_layer * T->cfg.n_layers);
   }
+  // per model: L x (qkv, out, ffn1, ffn2), [E; V_k1], decoder block matrix
+  auto wb_bytes = [](const tppsd_model *m) -> size_t {
+    if (!m || m->attnhp() || !block_widths(m->d(), m->cfg.d_ffn)) return 0;
+    const int d = m->d(), F = m->cfg.d_ffn;
+    const size_t layer = wbatch_packed_elems(3 * d, d) + wbatch_packed_elems(d, d) + wbatch_packed_elems(F, d) +
+                         wbatch_packed_elems(d, F);
+    return (m->cfg.n_layers * layer + wbatch_packed_elems(4 * d, d) +
+            wbatch_packed_elems(3 * m->cfg.n_mix + m->cfg.n_types, 4 * d)) * m->act_bytes();
+  };
+  w.wbT = take(wb_bytes(T));
+  w.wbD = take(wb_bytes(D));
+  w.wb_nT = wb_bytes(T);
+  w.wb_nD = wb_bytes(D);
   if (D && !D->attnhp() && layer_fused_ok(D->bf16(), D->d(), D->cfg.d_ffn)) {
     const size_t d = D->d(), F = D->cfg.d_ffn;
     w.pack_layerD = (4 * d * d + 2 * d * F) * 2;
@@ -408,7 +428,7 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
       launch_attnhp_update(s->x, s->o, s->u, s->a, bf, T, d, st);
     }
   }
-  if (!m->attnhp() && s->block_path && block_fusable(bf, d, F, m->cfg.n_mix, m->cfg.n_types)) {
+  if (!m->attnhp() && s->block_path && block_fusable(bf, d, F, m->cfg.n_mix, m->cfg.n_types, T)) {
     // small THP models: one k_block launch between consecutive attention
     // launches (embedding + LN1 + QKV; then output projection + FFN + the next
     // LN1 + QKV; the last one ends with LN_f and the decoder). Without a
@@ -429,15 +449,15 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     ba.lnf_g = m->lnf_g;
     ba.lnf_b = m->lnf_b;
     ba.k1_b = m->k1_b;
-    ba.Ek1_w = m->Ek1_w;
-    ba.head_w = c.head_w;
+    ba.Ek1_w = c.wb_ek1;   // (k_block reads its matrices in the packed order)
+    ba.head_w = c.wb_head;
     ba.head_b = c.head_b;
     ba.M = M;
     ba.K = K;
     if (head) ba.h = *head;
     auto set_qkv = [&](int l) {
       const LayerW &w = m->layers[l];
-      ba.qkv_w = w.qkv_w;
+      ba.qkv_w = c.wb_qkv[l];
       ba.ln1_g = w.ln1_g;
       ba.ln1_b = w.ln1_b;
       Epi &e = ba.qe;
@@ -470,13 +490,13 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
       const LayerW &w = m->layers[l];
       ba.first = 0;
       ba.pre = 1;
-      ba.out_w = w.out_w;
+      ba.out_w = c.wb_out[l];
       ba.out_b = w.out_b;
       ba.ln2_g = w.ln2_g;
       ba.ln2_b = w.ln2_b;
-      ba.ffn1_w = w.ffn1_w;
+      ba.ffn1_w = c.wb_f1[l];
       ba.ffn1_b = w.ffn1_b;
-      ba.ffn2_w = w.ffn2_w;
+      ba.ffn2_w = c.wb_f2[l];
       ba.ffn2_b = w.ffn2_b;
       ba.qkv = !last;
       ba.store_x = !last;
@@ -797,12 +817,13 @@ int do_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_
     a.K = m->cfg.n_types;
     for (int l = 0; l < a.L; ++l) {
       const LayerW &w = m->layers[l];
-      a.layer[l] = {w.qkv_w, w.out_w, w.ffn1_w, w.ffn2_w, w.ln1_g, w.ln1_b, w.qkv_b,
+      // (k_verify_seq reads its matrices in the packed order)
+      a.layer[l] = {s->cT.wb_qkv[l], s->cT.wb_out[l], s->cT.wb_f1[l], s->cT.wb_f2[l], w.ln1_g, w.ln1_b, w.qkv_b,
                     w.out_b, w.ln2_g, w.ln2_b, w.ffn1_b, w.ffn2_b};
     }
     a.type_emb = m->type_emb;
-    a.Ek1_w = m->Ek1_w;
-    a.head_w = s->cT.head_w;
+    a.Ek1_w = s->cT.wb_ek1;
+    a.head_w = s->cT.wb_head;
     a.lnf_g = m->lnf_g;
     a.lnf_b = m->lnf_b;
     a.k1_b = m->k1_b;
@@ -1027,6 +1048,8 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->pack_layer = w.pack_layer;
   s->packD = w.pack_layerD ? ws + w.packD : nullptr;
   s->pack_layerD = w.pack_layerD;
+  s->cT.wb = w.wb_nT ? ws + w.wbT : nullptr;
+  s->cD.wb = w.wb_nD ? ws + w.wbD : nullptr;
   s->cT.head_w = ws + w.hwT;
   s->cT.head_b = (float *)(ws + w.hbT);
   if (D) {
@@ -1150,6 +1173,35 @@ int tppsd_prefill_window(tppsd_state *s, const float *d_t, const int32_t *d_k, i
                         c.head_w, c.head_b, st);
     }
     s->heads_built = true;
+  }
+  if (!s->wb_built) {
+    for (int which = 0; which < 2; ++which) {
+      const tppsd_model *m = which ? s->D : s->T;
+      ModelCache &c = which ? s->cD : s->cT;
+      if (!m || !c.wb) continue;
+      const int d = m->d(), F = m->cfg.d_ffn, bf = m->bf16(), eb = m->act_bytes();
+      char *p = c.wb;
+      auto put = [&](const void *W, int N, int K) {
+        launch_pack_wbatch(W, N, K, bf, p, st);
+        const void *r = p;
+        p += wbatch_packed_elems(N, K) * eb;
+        return r;
+      };
+      c.wb_qkv.clear();
+      c.wb_out.clear();
+      c.wb_f1.clear();
+      c.wb_f2.clear();
+      for (int l = 0; l < m->cfg.n_layers; ++l) {
+        const LayerW &w = m->layers[l];
+        c.wb_qkv.push_back(put(w.qkv_w, 3 * d, d));
+        c.wb_out.push_back(put(w.out_w, d, d));
+        c.wb_f1.push_back(put(w.ffn1_w, F, d));
+        c.wb_f2.push_back(put(w.ffn2_w, d, F));
+      }
+      c.wb_ek1 = put(m->Ek1_w, 4 * d, d);
+      c.wb_head = put(c.head_w, 3 * m->cfg.n_mix + m->cfg.n_types, 4 * d);
+    }
+    s->wb_built = true;
   }
   if (!s->packs_built) {
     for (int which = 0; which < 2; ++which) {

@@ -174,8 +174,13 @@ struct BlockArgs {
   int M, K;
   HeadArgs h;
 };
-// whether k_block serves a model of width d, FFN width F, M mixture components and K types
-bool block_fusable(int bf16, int d, int F, int M, int K);
+// whether k_block serves a pass of T rows of a model of width d, FFN width F, M mixture components and K types
+bool block_fusable(int bf16, int d, int F, int M, int K, long T);
+// widths k_block / k_verify_seq have instances for; their weights are read
+// in the packed order launch_pack_wbatch writes (wbatch_packed_elems each)
+bool block_widths(int d, int F);
+size_t wbatch_packed_elems(int N, int K);
+void launch_pack_wbatch(const void *W, int N, int K, int bf16, void *out, hipStream_t s);
 void launch_block(const BlockArgs &a, int bf16, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 // Per-sequence verify pass (k_verify_seq): one workgroup runs the whole target

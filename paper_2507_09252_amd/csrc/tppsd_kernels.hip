@@ -2059,18 +2059,45 @@ template <typename ELT, int K, int TPW> struct WBatch {
   static constexpr int NV = SEG * (int)sizeof(ELT) / 16;      // 16-byte vectors per tile
   static_assert(NV >= 1 && SEG * sizeof(ELT) % 16 == 0, "K too small for the lane-group split");
   uint4 w[TPB][NV];
+  // W in the packed order of k_pack_wbatch: tile t's vector i for lane l at
+  // ((t NV + i) 64 + l) 16 bytes, so each load instruction of a wave reads 1 KB
+  // of contiguous memory (tiles past the matrix clamped; results unused)
   __device__ __forceinline__ void load(const ELT *__restrict__ W, int N) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    const int rr = lane & 15, kq = lane >> 4;
+    const int last = (N + 15) / 16 - 1;
 #pragma unroll
     for (int j = 0; j < TPB; ++j) {
-      const int n = min((wave + j * nw) * 16 + rr, N - 1);   // rows past N clamped (results unused)
-      const uint4 *wr = (const uint4 *)(W + (size_t)n * K + kq * SEG);
+      const int t = min(wave + j * nw, last);
+      const uint4 *wr = (const uint4 *)W + (size_t)t * NV * 64 + lane;
 #pragma unroll
-      for (int i = 0; i < NV; ++i) w[j][i] = wr[i];
+      for (int i = 0; i < NV; ++i) w[j][i] = wr[i * 64];
     }
   }
 };
+
+// W [N][K] into the WBatch order: 16-row tile t, lane l = 16 kq + r holds
+// row 16 t + r (clamped to N - 1), k segment kq K/4 .. + K/4, as K/4 * elt / 16
+// consecutive 16-byte vectors i stored at ((t NV + i) 64 + l) 16 bytes
+template <typename ELT>
+__global__ void k_pack_wbatch(const ELT *__restrict__ W, int N, int K, ELT *__restrict__ out) {
+  const int NV = (K / 4) * (int)sizeof(ELT) / 16, VE = 16 / (int)sizeof(ELT);
+  const int tiles = (N + 15) / 16, total = tiles * NV * 64;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= total) return;
+  const int l = idx & 63, ti = idx >> 6, t = ti / NV, i = ti - t * NV;
+  const int n = min(16 * t + (l & 15), N - 1), kq = l >> 4;
+  *(uint4 *)(out + (size_t)idx * VE) = *(const uint4 *)(W + (size_t)n * K + kq * (K / 4) + i * VE);
+}
+
+size_t wbatch_packed_elems(int N, int K) { return (size_t)(N + 15) / 16 * 16 * K; }
+
+void launch_pack_wbatch(const void *W, int N, int K, int bf16, void *out, hipStream_t s) {
+  const int NV = (K / 4) * (bf16 ? 2 : 4) / 16, total = (N + 15) / 16 * NV * 64;
+  if (bf16)
+    k_pack_wbatch<bf16_t><<<(total + 255) / 256, 256, 0, s>>>((const bf16_t *)W, N, K, (bf16_t *)out);
+  else
+    k_pack_wbatch<float><<<(total + 255) / 256, 256, 0, s>>>((const float *)W, N, K, (float *)out);
+}
 
 // Y[16 x N] = X[16 x K] W^T with X in LDS (fp32 values, row stride ldx) and
 // the wave's weights in wb; epi(r, n, y) for r < 16, n < N, each element by
@@ -2366,17 +2393,23 @@ __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
   }
 }
 
-bool block_fusable(int bf16, int d, int F, int M, int K) {
+bool block_widths(int d, int F) { return (d == 32 && (F == 64 || F == 128)) || (d == 64 && (F == 128 || F == 256)); }
+
+bool block_fusable(int bf16, int d, int F, int M, int K, long T) {
   // instantiated widths; every product's column tiles fit one weight batch of
   // the four waves (16 (64 / (k / 4)) columns per wave, at least 16): the
   // decoder's 3M + K logits over k = 4d need 3M + K <= 4 * 16 * max(1, 64 / d)
-  const bool widths = (d == 32 && (F == 64 || F == 128)) || (d == 64 && (F == 128 || F == 256));
+  const bool widths = block_widths(d, F);
   // a launch streams a layer's matrices through each workgroup: worth it while
-  // they are small (measured: d = 32 models gain, fp32 d = 64 / F = 256 loses
-  // to the layered kernels, whose many small workgroups spread the latency)
+  // they are small, or, for larger ones (fp32 d = 64 / F = 256, 192 KB), over
+  // many rows. Measured with the matrices in the packed order: the 704-row
+  // verify pass of that model 122.9 -> 118.4 us, its 64-row AR step slower
+  // than the layered kernels (586K -> 564K events/s)
   const size_t layer_bytes = (size_t)(4 * d * d + 2 * d * F) * (bf16 ? 2 : 4);
-  return widths && 3 * M + K <= 64 * (d >= 64 ? 1 : 64 / d) && layer_bytes <= 64 * 1024;
+  return widths && 3 * M + K <= 64 * (d >= 64 ? 1 : 64 / d) && (layer_bytes <= 64 * 1024 || T >= 512);
 }
+
+
 
 void launch_block(const BlockArgs &a, int bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const int LX = a.d + 4, LH = (a.F > 4 * a.d ? a.F : 4 * a.d) + 4, LV = 3 * a.M + a.K + 1;

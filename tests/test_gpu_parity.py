@@ -29,6 +29,9 @@ VERIFY_CASES = [
     small("c1", 5),
     small("c2", 6),
     small("c2", 4, init="paper", mismatch=False),
+    # 517 rows: the fp32 d = 64 / F = 256 target takes the row-block kernel
+    # (packed weights) from 512 rows; 33 tiles of 16, the last ragged
+    small("c2", 47, init="bias"),
     small("c3", 5, n_hist=40, init="bias"),
     small("c3", 3, n_hist=40, init="paper", mismatch=False),
     small("c3", 3, n_hist=40),
