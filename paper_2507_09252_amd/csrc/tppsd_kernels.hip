@@ -332,12 +332,10 @@ __device__ __forceinline__ void epilogue8(const Epi &e, int r, int n, const floa
   }
 }
 
-// GEMM on MFMA with fp32 accumulation. A workgroup of 4 waves (2 x 2) owns a
-// (32 TM) x (32 TN) output tile; each wave owns TM x TN 16x16 accumulator
-// tiles. Operands are read straight from global memory (weights stay in L2):
-// for every 16x16 tile lane l holds row (l mod 16) of A and of W (W is stored
-// [N, K], so its rows are B's columns) over one slice of the k range; the
-// accumulator holds rows 4 (l / 16) + i, column l mod 16.
+// One k step of an MFMA tile product with fp32 accumulation: for every 16x16
+// tile lane l holds row (l mod 16) of A and of W (W is stored [N, K], so its
+// rows are B's columns) over one slice of the k range; the accumulator holds
+// rows 4 (l / 16) + i, column l mod 16.
 //   bf16: v_mfma_f32_16x16x32_bf16, lane slice = 8 consecutive k, 32 k per step.
 //   fp32: v_mfma_f32_16x16x4f32, lane l loads 4 consecutive k (4 (l / 16) .. + 3)
 //         and issues one MFMA per element; across the four MFMAs the 16 k of the
@@ -364,46 +362,6 @@ template <> struct MfmaStep<float> {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
   }
 };
-
-template <typename ELT, int TM, int TN>
-__global__ __launch_bounds__(256) void k_gemm_mfma(const ELT *__restrict__ X, const ELT *__restrict__ W, int T,
-                                                   int N, int K, Epi e) {
-  typedef MfmaStep<ELT> S;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int m0 = blockIdx.y * (32 * TM) + (wave >> 1) * (16 * TM);
-  const int n0 = blockIdx.x * (32 * TN) + (wave & 1) * (16 * TN);
-  const int rr = lane & 15, g = lane >> 4;
-  f32x4_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-  const ELT *xa[TM], *wb[TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) xa[i] = X + (size_t)min(m0 + 16 * i + rr, T - 1) * K;
-#pragma unroll
-  for (int j = 0; j < TN; ++j) wb[j] = W + (size_t)min(n0 + 16 * j + rr, N - 1) * K;
-  for (int k0 = 0; k0 < K; k0 += S::KSTEP) {
-    typename S::frag a[TM], b[TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) a[i] = S::load(xa[i] + k0, g);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) b[j] = S::load(wb[j] + k0, g);
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = S::mma(a[i], b[j], acc[i][j]);
-  }
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int r = m0 + 16 * i + 4 * g + v, n = n0 + 16 * j + rr;
-        if (r < T && n < N) epilogue<ELT>(e, r, n, acc[i][j][v]);
-      }
-}
 
 // LDS-staged GEMM with fp32 accumulation: a workgroup of 4 waves (2 x 2)
 // owns a BM x BN output tile and walks K in stages of BK = KSN MFMA k-steps
