@@ -2166,12 +2166,14 @@ __device__ __forceinline__ void tile_layernorm(const float *x, int ldx, float *y
 // ffn1_b, ffn2_b, LN1 (g, b), qkv_b, LN_f (g, b), k1_b, decoder bias
 inline __host__ __device__ int block_vec_floats(int d, int F, int M, int K) { return 13 * d + F + 3 * M + K; }
 
-template <typename ELT, int D, int F>
-__global__ __launch_bounds__(256) void k_block(BlockArgs a) {
+template <typename ELT, int D, int F, int NT>
+__global__ __launch_bounds__(NT) void k_block(BlockArgs a) {
   constexpr int LX = D + 4, LH = (F > 4 * D ? F : 4 * D) + 4;
-  // column tiles per wave (4 waves) of each product; the decoder's 3M + K
-  // logits are at most 64 (64 / d) wide (block_fusable)
-  constexpr int TO = (D + 63) / 64, T1 = (F + 63) / 64, TE = (4 * D + 63) / 64, TH = D >= 64 ? 1 : 64 / D;
+  // column tiles per wave (NT / 64 waves) of each product; the decoder's
+  // 3M + K logits are at most 64 (64 / d) wide (block_fusable)
+  constexpr int NW = NT / 64;
+  constexpr int TO = (D / 16 + NW - 1) / NW, T1 = (F / 16 + NW - 1) / NW, TE = (4 * D / 16 + NW - 1) / NW,
+                TH = ((D >= 64 ? 1 : 64 / D) * 4 + NW - 1) / NW;
   extern __shared__ __attribute__((aligned(16))) float sm[];
   __shared__ int row_b[16], row_pos[16];
   float *xs = sm;              // [16][LX] residual stream
@@ -2189,7 +2191,7 @@ __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
   // prove disjoint): the small vectors of the steps this launch runs, the
   // rows of x (or the tokens) and of the attention output; then each row's
   // sequence and cache position.
-  constexpr int VMAX = (13 * D + F + 3 * 64 + 64 + 255) / 256;   // vector floats per thread
+  constexpr int VMAX = (13 * D + F + 3 * 64 + 64 + NT - 1) / NT;   // vector floats per thread
   float vv[VMAX];
   {
     const float *seg_src[12] = {a.out_b, a.ln2_g, a.ln2_b, a.ffn1_b, a.ffn2_b, a.ln1_g,
@@ -2201,7 +2203,7 @@ __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
                              10 * D + F, 11 * D + F, 12 * D + F};
 #pragma unroll
     for (int i = 0; i < VMAX; ++i) {
-      const int idx = tid + 256 * i;
+      const int idx = tid + NT * i;
       vv[i] = 0.f;
       for (int sgi = 0; sgi < 12; ++sgi) {
         const int o = idx - seg_off[sgi];
@@ -2210,7 +2212,7 @@ __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
     }
   }
   float4 xv = make_float4(0.f, 0.f, 0.f, 0.f);
-  const int xr_ = tid / (D / 4), xc_ = tid - xr_ * (D / 4);   // one float4 of x per thread (16 D / 4 <= 256)
+  const int xr_ = tid / (D / 4), xc_ = tid - xr_ * (D / 4);   // one float4 of x per thread (16 D / 4 <= NT)
   if (!a.first && xr_ < nr) xv = *(const float4 *)(a.x + (size_t)(r0 + xr_) * D + 4 * xc_);
   constexpr int OV = 16 / sizeof(ELT);                          // o elements per 16-byte load
   uint4 ov = make_uint4(0u, 0u, 0u, 0u);
@@ -2230,7 +2232,7 @@ __global__ __launch_bounds__(256) void k_block(BlockArgs a) {
   if (a.pre) w_f1.load((const ELT *)a.ffn1_w, F);
 #pragma unroll
   for (int i = 0; i < VMAX; ++i)
-    if (tid + 256 * i < 12 * D + F + 3 * a.M + a.K + D) vec[tid + 256 * i] = vv[i];
+    if (tid + NT * i < 12 * D + F + 3 * a.M + a.K + D) vec[tid + NT * i] = vv[i];
   if (a.qkv && tid < 16) {
     const int R = min(r0 + tid, a.T - 1), b = R / a.P;
     row_b[tid] = b;
@@ -2373,17 +2375,31 @@ void launch_block(const BlockArgs &a, int bf16, hipStream_t s, hipEvent_t ev0, h
   const int LX = a.d + 4, LH = (a.F > 4 * a.d ? a.F : 4 * a.d) + 4, LV = 3 * a.M + a.K + 1;
   const size_t lds = ((size_t)16 * (2 * LX + LH + LV) + block_vec_floats(a.d, a.F, a.M, a.K)) * sizeof(float);
   const dim3 grid((a.T + 15) / 16);
-  auto go = [&](auto kern) { hipExtLaunchKernelGGL(kern, grid, dim3(256), lds, s, ev0, ev1, 0, a); };
-#define TPPSD_BLK(ELT)                                              \
-  if (a.d == 32 && a.F == 64) go(k_block<ELT, 32, 64>);             \
-  else if (a.d == 32) go(k_block<ELT, 32, 128>);                    \
-  else if (a.F == 128) go(k_block<ELT, 64, 128>);                   \
-  else go(k_block<ELT, 64, 256>);
+  auto go = [&](auto kern, int nt) { hipExtLaunchKernelGGL(kern, grid, dim3(nt), lds, s, ev0, ev1, 0, a); };
+  // eight waves, each holding half the column tiles that four would: the
+  // products' serial MFMA chains per wave halve. Measured against four: the
+  // 704-row fp32 verify pass at d = 64 / F = 256 106.6 vs 118.6 us per round,
+  // the bf16 d = 32 / F = 128 draft step over 4096 sequences 369 vs 422 us per
+  // round; sixteen waves slower again (112 us). TPPSD_BLOCK_NT=256 keeps four
+  // (A/B measurement).
+  const char *nte = getenv("TPPSD_BLOCK_NT");
+  const int nt = nte && atoi(nte) == 256 ? 256 : 512;
+#define TPPSD_BLK(ELT, D_, F_)                 \
+  if (nt == 512)                               \
+    go(k_block<ELT, D_, F_, 512>, 512);        \
+  else                                         \
+    go(k_block<ELT, D_, F_, 256>, 256);
+#define TPPSD_BLKS(ELT)                                         \
+  if (a.d == 32 && a.F == 64) { TPPSD_BLK(ELT, 32, 64) }         \
+  else if (a.d == 32) { TPPSD_BLK(ELT, 32, 128) }                \
+  else if (a.F == 128) { TPPSD_BLK(ELT, 64, 128) }               \
+  else { TPPSD_BLK(ELT, 64, 256) }
   if (bf16) {
-    TPPSD_BLK(bf16_t)
+    TPPSD_BLKS(bf16_t)
   } else {
-    TPPSD_BLK(float)
+    TPPSD_BLKS(float)
   }
+#undef TPPSD_BLKS
 #undef TPPSD_BLK
 }
 

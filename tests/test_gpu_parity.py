@@ -124,6 +124,17 @@ def test_verify_fused_layer(case, monkeypatch):
     test_verify_teacher_forced(case)
 
 
+# the row-block kernel with four waves instead of its default eight (the
+# 517-row fp32 pass runs it; the d = 32 drafts' per-step kernels too)
+BLOCK_NT_CASES = [small("c2", 47, init="bias")]
+
+
+@pytest.mark.parametrize("case", BLOCK_NT_CASES, ids=_ids(BLOCK_NT_CASES))
+def test_verify_block_four_waves(case, monkeypatch):
+    monkeypatch.setenv("TPPSD_BLOCK_NT", "256")
+    test_verify_teacher_forced(case)
+
+
 ACCEPT_CASES = [small("c1", 64), small("c3", 48, n_hist=30, init="bias"), small("c5", 96, init="bias")]
 
 
@@ -191,6 +202,10 @@ DRAFT_CASES = [small("c1", 8), small("c2", 8), small("c3", 16, n_hist=40, init="
 @pytest.mark.parametrize("case", DRAFT_CASES, ids=_ids(DRAFT_CASES))
 def test_draft_parity(case, layered, monkeypatch):
     monkeypatch.setenv("TPPSD_LAYERED_DRAFT", "1" if layered else "0")
+    _draft_parity(case)
+
+
+def _draft_parity(case):
     gamma, n_gen, seed = _gamma(case), 64, 13
     wt, wd = weights(case)
     T, D, ht, hk, st_o, dr, vf = _oracle_round(case, wt, wd, gamma, n_gen, seed)
@@ -212,6 +227,15 @@ def test_draft_parity(case, layered, monkeypatch):
         np.testing.assert_allclose(g["logf"][b, :u], dr.logf[b, :u], atol=tol, rtol=tol)
     # categorical near-ties cut the comparison; most draft positions are still compared
     assert upto.mean() > 0.25 * gamma, upto
+
+
+# the per-step draft's row-block kernel with four waves (4096-sequence drafts
+# run it at d = 32)
+@pytest.mark.parametrize("case", [DRAFT_CASES[3]], ids=_ids(DRAFT_CASES[3:4]))
+def test_draft_block_four_waves(case, monkeypatch):
+    monkeypatch.setenv("TPPSD_BLOCK_NT", "256")
+    monkeypatch.setenv("TPPSD_LAYERED_DRAFT", "1")
+    _draft_parity(case)
 
 
 # end to end on paper-scale weights: the sampled times feed back through the
