@@ -147,3 +147,79 @@ def test_attnhp_sd_law_equals_ar():
     assert 0.2 < sd[2] < 0.9, sd[2]
     ps = _pvalues(ar, sd)
     assert ps.min() > 0.01 / len(ps), ps
+
+
+# ---------------------------------------------------------------------------
+# bf16 rounding points, pinned by an independent formulation
+# ---------------------------------------------------------------------------
+
+def _bf(x):
+    """float64 -> bfloat16 -> float64 by integer arithmetic on the IEEE bits
+    (round to nearest, ties to even: keep 7 of the 52 stored mantissa bits)."""
+    bits = x.contiguous().view(torch.int64)
+    lsb = (bits >> 45) & 1
+    return ((bits + ((1 << 44) - 1) + lsb) & ~((1 << 45) - 1)).view(torch.float64)
+
+
+ATTNHP_BF16_POINTS = ("z", "h", "qkv", "attn", "dec_h", "e", "tanh")
+
+
+def _torch_attnhp_bf16(mo: Model, t, k, skip=None):
+    """bf16 AttNHP stack + decoder with torch primitives in float64: both
+    halves of the layer input [z; h], q, k, v after the bias, the attention
+    output before tanh, and the decoder's Linear inputs (h, e, the tanh
+    output) are rounded to bfloat16; the rest stays float64. The time
+    encoding is computed here from its definition (float32 wavelength table,
+    float32 product t * omega). Returns (log w, mu, s, log f)."""
+    W_ = {n: torch.from_numpy(v) for n, v in mo.w.items()}
+
+    def rb(x, point):
+        return x if point == skip else _bf(x)
+
+    D, H, dh = mo.d, mo.H, mo.dh
+    j = torch.arange(D, dtype=torch.float64)
+    m_, M_ = float(mo.cfg.time_m), float(mo.cfg.time_M)
+    omega = (1.0 / (m_ * torch.pow(torch.tensor(5.0 * M_ / m_, dtype=torch.float64),
+                                   (j - torch.remainder(j, 2)) / D))).float()
+    arg = (torch.from_numpy(np.asarray(t, np.float32))[..., None] * omega).double()
+    z = torch.where(torch.remainder(torch.arange(D), 2) == 0, torch.sin(arg), torch.cos(arg))
+    h = W_["type_emb"][torch.from_numpy(np.asarray(k))]
+    B, N, _ = h.shape
+    allow = torch.ones(N, N + 1, dtype=torch.bool).tril(diagonal=1)   # column 0: the zero key
+    for l in range(mo.L):
+        u = torch.cat([rb(z, "z"), rb(h, "h")], -1)
+        qkv = rb(Fn.linear(u, W_[f"layers.{l}.qkv.w"], W_[f"layers.{l}.qkv.b"]), "qkv")
+        q, kk, v = (qkv[..., i * D:(i + 1) * D].reshape(B, N, H, dh).transpose(1, 2) for i in range(3))
+        zero = torch.zeros(B, H, 1, dh, dtype=torch.float64)
+        o = Fn.scaled_dot_product_attention(q, torch.cat([zero, kk], 2), torch.cat([zero, v], 2), attn_mask=allow)
+        h = h + torch.tanh(rb(o.transpose(1, 2).reshape(B, N, D), "attn"))
+    hb = rb(h, "dec_h")
+    e = rb(Fn.linear(hb, W_["head.E"]), "e")
+    logw = torch.log_softmax(Fn.linear(e[..., :D], W_["head.w.w"], W_["head.w.b"]), -1)
+    mu = Fn.linear(e[..., D:2 * D], W_["head.mu.w"], W_["head.mu.b"])
+    s = Fn.linear(e[..., 2 * D:], W_["head.sigma.w"], W_["head.sigma.b"])
+    th = rb(torch.tanh(Fn.linear(hb, W_["head.k1.w"], W_["head.k1.b"])), "tanh")
+    logf = torch.log_softmax(Fn.linear(th, W_["head.k2.w"], W_["head.k2.b"]), -1)
+    return tuple(a.numpy() for a in (logw, mu, s, logf))
+
+
+def test_attnhp_bf16_rounding_points_match_torch():
+    """The oracle's bf16 AttNHP (cache-free and cached block forward, decoder)
+    against the independent formulation to 1e-12; leaving out any single
+    rounding point moves the outputs far beyond that."""
+    rng = np.random.default_rng(12)
+    for L, d, H, init in [(2, 32, 2, "stress"), (2, 64, 4, "paper")]:
+        cfg = W.ModelCfg(L, d, H, 0, 5, 4, "bf16", W.ENC_ATTNHP, 0.01, 100.0)
+        mo = Model(cfg, W.make_weights(cfg, np.random.SeedSequence([78, L, d]), init))
+        t = np.cumsum(rng.exponential(1.0, (3, 19)), axis=1).astype(np.float32)
+        k = rng.integers(0, 4, (3, 19))
+        want = _torch_attnhp_bf16(mo, t, k)
+        for g, w in zip(mo.head(mo.forward_full(t, k)), want):
+            np.testing.assert_allclose(g, w, rtol=0, atol=1e-12)
+        cache = mo.new_cache(3, 24)
+        mo.forward_block(cache, t[:, :11], k[:, :11], np.zeros(3, np.int64))
+        for g, w in zip(mo.head(mo.forward_block(cache, t[:, 11:], k[:, 11:], np.full(3, 11))), want):
+            np.testing.assert_allclose(g, w[:, 11:], rtol=0, atol=1e-12)
+        for point in ATTNHP_BF16_POINTS:
+            alt = _torch_attnhp_bf16(mo, t, k, skip=point)
+            assert max(np.abs(a - w).max() for a, w in zip(alt, want)) > 1e-7, point

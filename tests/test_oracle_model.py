@@ -14,6 +14,7 @@ import numpy as np
 import pytest
 import scipy.stats
 import torch
+import torch.nn.functional as Fn
 
 from oracle.model import Model
 from oracle.sampler import mixture_logpdf
@@ -209,3 +210,103 @@ def test_bf16_mode_rounds():
     lf = mf.head(hf)
     lb = mb.head(hb)
     assert np.abs(lf[0] - lb[0]).max() < 5e-2
+
+
+# ---------------------------------------------------------------------------
+# bf16 rounding points, pinned by an independent formulation
+# ---------------------------------------------------------------------------
+
+def _bf(x):
+    """Round float64 values to bfloat16 (8 significant bits, round to nearest,
+    ties to even) by integer arithmetic on the IEEE bits: of the 52 stored
+    mantissa bits keep 7, adding 2^44 - 1 plus the lowest kept bit before
+    truncating. (torch's own float64 -> bfloat16 cast goes through float32,
+    a double rounding that differs at ties.)"""
+    bits = x.contiguous().view(torch.int64)
+    lsb = (bits >> 45) & 1
+    bits = (bits + ((1 << 44) - 1) + lsb) & ~((1 << 45) - 1)
+    return bits.view(torch.float64)
+
+
+def test_bf_helper_matches_torch_on_float32_values():
+    # on float32 inputs torch's cast rounds once, so the two must agree exactly (ties included)
+    g = torch.Generator().manual_seed(0)
+    x = (torch.randn(200000, generator=g) * 10).float()
+    ties = (x.view(torch.int32) & ~0xFFFF) | 0x8000          # exact midpoints between bf16 values
+    for v in (x, ties.view(torch.float32)):
+        assert torch.equal(_bf(v.double()), v.to(torch.bfloat16).double())
+
+
+BF16_POINTS = ("ln1", "qkv", "attn", "ln2", "relu", "lnf", "e", "tanh")
+
+
+def _torch_thp_bf16(m: Model, t, k, skip=None):
+    """A bf16 THP encoder + decoder written with torch primitives in float64:
+    Linear inputs (the LayerNorm outputs, the attention output, the ReLU
+    output, the decoder's LN_f output, e and the tanh output) and q, k, v
+    after the bias are cast to bfloat16 and back; everything else (residual
+    stream, LayerNorm statistics, softmax, decoder arithmetic) stays float64.
+    Returns (log w, mu, s, log f) for every event. skip names one rounding
+    point to leave out (the test's power check)."""
+    W_ = {n: torch.from_numpy(v) for n, v in m.w.items()}
+
+    def rb(x, point):
+        return x if point == skip else _bf(x)
+    d, H, dh = m.d, m.H, m.dh
+    j = torch.arange(d, dtype=torch.float64)
+    freq = torch.pow(torch.tensor(10000.0, dtype=torch.float64), -(j - torch.remainder(j, 2)) / d).float()
+    arg = (torch.from_numpy(np.asarray(t, np.float32))[..., None] * freq).double()
+    z = torch.where(torch.remainder(torch.arange(d), 2) == 0, torch.sin(arg), torch.cos(arg))
+    x = z + W_["type_emb"][torch.from_numpy(np.asarray(k))]
+    B, N, _ = x.shape
+    for l in range(m.L):
+        p = f"layers.{l}."
+        a = rb(Fn.layer_norm(x, (d,), W_[p + "ln1.g"], W_[p + "ln1.b"], eps=1e-5), "ln1")
+        qkv = rb(Fn.linear(a, W_[p + "qkv.w"], W_[p + "qkv.b"]), "qkv")
+        q, kk, v = (qkv[..., i * d:(i + 1) * d].reshape(B, N, H, dh).transpose(1, 2) for i in range(3))
+        o = Fn.scaled_dot_product_attention(q, kk, v, is_causal=True)
+        x = x + Fn.linear(rb(o.transpose(1, 2).reshape(B, N, d), "attn"), W_[p + "out.w"], W_[p + "out.b"])
+        a2 = rb(Fn.layer_norm(x, (d,), W_[p + "ln2.g"], W_[p + "ln2.b"], eps=1e-5), "ln2")
+        hid = rb(torch.relu(Fn.linear(a2, W_[p + "ffn1.w"], W_[p + "ffn1.b"])), "relu")
+        x = x + Fn.linear(hid, W_[p + "ffn2.w"], W_[p + "ffn2.b"])
+    h = rb(Fn.layer_norm(x, (d,), W_["lnf.g"], W_["lnf.b"], eps=1e-5), "lnf")
+    e = rb(Fn.linear(h, W_["head.E"]), "e")
+    logw = torch.log_softmax(Fn.linear(e[..., :d], W_["head.w.w"], W_["head.w.b"]), -1)
+    mu = Fn.linear(e[..., d:2 * d], W_["head.mu.w"], W_["head.mu.b"])
+    s = Fn.linear(e[..., 2 * d:], W_["head.sigma.w"], W_["head.sigma.b"])
+    th = rb(torch.tanh(Fn.linear(h, W_["head.k1.w"], W_["head.k1.b"])), "tanh")
+    logf = torch.log_softmax(Fn.linear(th, W_["head.k2.w"], W_["head.k2.b"]), -1)
+    return tuple(a.numpy() for a in (logw, mu, s, logf))
+
+
+@pytest.mark.parametrize("init", ["paper", "stress"])
+@pytest.mark.parametrize("L,d,H,F", [(2, 64, 4, 256), (1, 32, 2, 64)])
+def test_bf16_rounding_points_match_torch(L, d, H, F, init):
+    """The oracle's bf16 mode (forward_full, forward_block on a cache, head)
+    against the independent torch formulation: agreement to 1e-12 means every
+    rounding point is where the formulation puts it; a missing or extra
+    rounding moves outputs by about a bf16 ulp (4e-3 relative) and fails."""
+    cfg = ModelCfg(L, d, H, F, 6, 5, "bf16")
+    m = Model(cfg, make_weights(cfg, np.random.SeedSequence([98, L]), init))
+    rng = np.random.default_rng(8)
+    B, N = 3, 21
+    t = np.cumsum(rng.exponential(1.0, (B, N)), 1).astype(np.float32)
+    k = rng.integers(0, m.K, (B, N))
+    want = _torch_thp_bf16(m, t, k)
+    got = m.head(m.forward_full(t, k))
+    for g, w in zip(got, want):
+        np.testing.assert_allclose(g, w, rtol=0, atol=1e-12)
+    # the cached block pass (as verification runs it): ragged cached lengths, then a block of 6
+    cache = m.new_cache(B, N + 4)
+    pos = np.array([7, 12, 15])
+    for b in range(B):
+        m.forward_block(cache, t[b:b + 1, :pos[b]], k[b:b + 1, :pos[b]], np.array([0]), rows=[b])
+    idx = pos[:, None] + np.arange(6)
+    hb = m.forward_block(cache, np.take_along_axis(t, idx, 1), np.take_along_axis(k, idx, 1), pos)
+    got_b = m.head(hb)
+    for g, w in zip(got_b, want):
+        np.testing.assert_allclose(g, np.stack([w[b, idx[b]] for b in range(B)]), rtol=0, atol=1e-12)
+    # power: leaving out any single rounding point moves the outputs far beyond the bar
+    for point in BF16_POINTS:
+        alt = _torch_thp_bf16(m, t, k, skip=point)
+        assert max(np.abs(a - w).max() for a, w in zip(alt, want)) > 1e-7, point
