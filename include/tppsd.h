@@ -304,9 +304,10 @@ int tppsd_state_status(tppsd_state *s, hipStream_t stream, uint32_t *bits, int32
 
 /* Measurement of tppsd_sample_sd; the sampled events are unchanged.
  * TPPSD_TIME_KERNELS: rounds are launched directly instead of replaying a
- *   captured HIP graph, and every launch of the target's verify attention and
- *   of its verify GEMMs (QKV, attention output, FFN in, FFN out, decoder E) is
- *   bracketed by HIP events stamped with the kernel's own start and stop.
+ *   captured HIP graph, and every launch of the target's verify attention, of
+ *   its verify GEMMs (QKV, attention output, FFN in, FFN out, decoder E) and
+ *   of the one-launch draft kernel is bracketed by HIP events stamped with the
+ *   kernel's own start and stop.
  * TPPSD_TIME_PHASES: each round replays three captured graphs (draft, verify,
  *   accept) with HIP events recorded between them on the caller's stream.
  * The two modes are separate runs (both bits at once: TPPSD_E_ARG).
@@ -322,6 +323,8 @@ typedef struct tppsd_timing {
   double gemm_flop;        /* 2 * rows * N * K over the timed GEMM launches */
   double draft_ms, verify_ms, accept_ms;   /* phase times */
   int64_t rounds;          /* rounds timed */
+  double draft_kernel_ms;  /* one-launch draft kernel: summed kernel time */
+  int64_t draft_kernel_launches;
 } tppsd_timing;
 int tppsd_timing_enable(tppsd_state *s, int modes);
 int tppsd_timing_read(tppsd_state *s, tppsd_timing *out);

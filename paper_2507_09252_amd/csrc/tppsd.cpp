@@ -208,8 +208,6 @@ struct tppsd_state {
   float *logits = nullptr;
   bool heads_built = false;
   float *ar_mix = nullptr, *ar_logtype = nullptr;
-  bool block_path = true;              // k_block for the models it serves (TPPSD_LAYERED=1: layered kernels)
-  bool verify_seq = true;              // k_verify_seq for the targets it serves (TPPSD_LAYERED=1: off)
   float *attn_part = nullptr;
   char *packT = nullptr;               // target weights in fragment order (nullptr: no fused layer kernel)
   size_t pack_layer = 0;
@@ -244,10 +242,9 @@ struct tppsd_state {
   // HIP graphs of the sampling loops, captured on a private stream and
   // replayed on the caller's; keyed by what their kernel arguments embed
   hipStream_t cap_stream = nullptr;
-  bool use_graphs = true;
   bool fused_draft = true;   // one-launch drafting when the draft model fits it
+  bool wave_draft = false;   // ... with one wave per sequence (small draft models)
   bool fused_w_lds = false;  // ... with its weight matrices staged in LDS
-  bool fused_attn_mfma = false;   // ... with its attention on MFMA (else vector ALU for <= 4 heads)
   hipGraphExec_t sd_exec[2] = {nullptr, nullptr};
   long long sd_key = -1;
   const float *sd_params = nullptr, *phase_params = nullptr;   // Poisson draft parameters the graphs embed
@@ -428,7 +425,7 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
       launch_attnhp_update(s->x, s->o, s->u, s->a, bf, T, d, st);
     }
   }
-  if (!m->attnhp() && s->block_path && block_fusable(bf, d, F, m->cfg.n_mix, m->cfg.n_types, T)) {
+  if (!m->attnhp() && block_fusable(bf, d, F, m->cfg.n_mix, m->cfg.n_types, T)) {
     // small THP models: one k_block launch between consecutive attention
     // launches (embedding + LN1 + QKV; then output projection + FFN + the next
     // LN1 + QKV; the last one ends with LN_f and the decoder). Without a
@@ -698,14 +695,21 @@ int do_draft_fused(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStr
   a.d_k = out->k;
   a.MG = s->max_gamma;
   a.w_lds = s->fused_w_lds ? 1 : 0;
-  a.attn_mfma = s->fused_attn_mfma ? 1 : 0;
-  launch_draft_fused(a, D->bf16(), st);
+  // kernel timing: the pair after the verify pass's attention and GEMM pairs
+  const int dp = 5 * s->T->cfg.n_layers + 1;
+  const bool timed = s->cur_ev != nullptr;
+  if (timed) s->ev_used[dp] = 1;
+  if (s->wave_draft)
+    launch_draft_wave(a, D->bf16(), st, timed ? s->cur_ev[2 * dp] : nullptr, timed ? s->cur_ev[2 * dp + 1] : nullptr);
+  else
+    launch_draft_fused(a, D->bf16(), st, timed ? s->cur_ev[2 * dp] : nullptr,
+                       timed ? s->cur_ev[2 * dp + 1] : nullptr);
   return hip_check("tppsd_draft");
 }
 
 int do_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
   const tppsd_model *D = s->D;
-  if (s->fused_draft) return do_draft_fused(s, gamma, out, st);
+  if (s->wave_draft || s->fused_draft) return do_draft_fused(s, gamma, out, st);
   for (int l = 1; l <= gamma; ++l) {
     TokSrc src{};
     src.ev_t = s->ev_t;
@@ -803,7 +807,7 @@ int do_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_
   h.v_logg = out->logg;
   h.v_logf = out->logf;
   const tppsd_model *m = s->T;
-  if (s->verify_seq && !m->attnhp() &&
+  if (!m->attnhp() &&
       verify_seq_ok(m->bf16(), m->cfg.n_layers, m->d(), m->H(), m->cfg.d_ffn, m->cfg.n_mix, m->cfg.n_types,
                     gamma + 1)) {
     // small targets: the whole pass of a sequence in one workgroup
@@ -1093,16 +1097,11 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
       tppsd_state_destroy(s);
       return hip_check("tppsd_state_create: capture stream");
     }
-    const char *ng = getenv("TPPSD_NO_GRAPHS");
-    s->use_graphs = !(ng && ng[0] == '1');
-    const char *lay = getenv("TPPSD_LAYERED");
-    s->block_path = !(lay && lay[0] == '1');
-    s->verify_seq = s->block_path;
     const char *nf = getenv("TPPSD_LAYERED_DRAFT");
     // one workgroup per sequence: worth it until the batch alone fills the chip
     // and the layered kernels amortise weights and latency over many rows
-    // (and while contexts stay short: its attention streams each (sequence,
-    // head)'s keys with one wave)
+    // (and while contexts stay short: the whole sequence's draft cache
+    // streams through one CU per step)
     s->fused_draft = D && !D->attnhp() && B <= 1024 && max_events <= 2048 &&
                      fused_draft_ok(D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn) &&
                      fused_draft_lds_bytes(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
@@ -1110,9 +1109,8 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
                      !(nf && nf[0] == '1');
     // its weight matrices in LDS when they fit beside the rest and each
     // workgroup has a CU to itself anyway (one workgroup per sequence)
-    const char *wg = getenv("TPPSD_DRAFT_WEIGHTS_GLOBAL");
     const int wb = D && D->bf16() ? 2 : 4;
-    s->fused_w_lds = s->fused_draft && B <= 256 && !(wg && wg[0] == '1') &&
+    s->fused_w_lds = s->fused_draft && B <= 256 &&
                      fused_draft_lds_bytes(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
                                            D->H()) +
                              fused_draft_weight_elems(D->cfg.n_layers, D->d(), D->cfg.d_ffn, D->cfg.n_mix,
@@ -1122,8 +1120,19 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
       s->fused_w_lds = false;       // weights stay in global memory
       (void)hipGetLastError();      // the refused attribute is not an error of this call
     }
-    const char *am = getenv("TPPSD_DRAFT_ATTN_MFMA");
-    s->fused_attn_mfma = am && am[0] == '1';
+    // small draft models: one wave per sequence, the weights in LDS, where
+    // the batch fills the chip with one wave per sequence or is tiny (a
+    // workgroup's barriers then cost more than its extra lanes save).
+    // Measured, draft us per round (wave / one workgroup per sequence /
+    // per-step kernels): 4096 sequences 309 / - / 376, 64 sequences 222 /
+    // 147 / 299, 1 sequence 47 / 61 / 128
+    s->wave_draft = D && !D->attnhp() && !(nf && nf[0] == '1') && (B >= 1024 || B <= 8) &&
+                    wave_draft_ok(D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
+                                  D->bf16());
+    if (s->wave_draft && allow_draft_wave_lds(LDS_PER_WG - 4096)) {
+      s->wave_draft = false;
+      (void)hipGetLastError();
+    }
   }
   if (hipHostMalloc((void **)&s->host_ndone, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&s->poll_ev[0], hipEventDisableTiming) != hipSuccess ||
@@ -1354,7 +1363,7 @@ int tppsd_sample_ar(tppsd_state *s, int n_events, float *d_t_out, int32_t *d_k_o
   if (n_events == 0) return TPPSD_OK;
   launch_snapshot(s->gen, s->gen0, s->B, st);   // output column = events generated in this call
   int i = 0;
-  if (s->use_graphs) {
+  {
     // graphs embed the output pointers, their stride and n_gen
     const long long key = ((long long)(uintptr_t)d_t_out * 31 + (long long)(uintptr_t)d_k_out) * 131 +
                           (long long)n_events * 1000003LL + s->n_gen;
@@ -1374,9 +1383,6 @@ int tppsd_sample_ar(tppsd_state *s, int n_events, float *d_t_out, int32_t *d_k_o
       if (hipGraphLaunch(s->ar_exec[1], st) != hipSuccess) return hip_check("tppsd_sample_ar: graph launch");
     for (; i < n_events; ++i)
       if (hipGraphLaunch(s->ar_exec[0], st) != hipSuccess) return hip_check("tppsd_sample_ar: graph launch");
-  } else {
-    for (; i < n_events; ++i)
-      if (int rc = ar_step(s, n_events, d_t_out, d_k_out, st)) return rc;
   }
   s->draft_ok = false;
   return hip_check("tppsd_sample_ar");
@@ -1399,6 +1405,9 @@ void read_round_events(tppsd_state *s, int w) {
       if ((int)(i / 2) < L) {
         s->tm.attn_ms += ms;
         s->tm.attn_launches += 1;
+      } else if ((int)(i / 2) == 5 * L + 1) {
+        s->tm.draft_kernel_ms += ms;
+        s->tm.draft_kernel_launches += 1;
       } else {
         s->tm.gemm_ms += ms;
         s->tm.gemm_launches += 1;
@@ -1445,7 +1454,7 @@ int sd_loop(tppsd_state *s, int gamma, const float *params, int max_rounds, int 
   // captured graph, or three (draft, verify, accept) when phases are timed
   const bool kern = (s->timing & TPPSD_TIME_KERNELS) != 0;
   const bool phases = (s->timing & TPPSD_TIME_PHASES) != 0;
-  const bool graphs = s->use_graphs && !kern;
+  const bool graphs = !kern;
   const long long key = (long long)gamma * 100000007LL + s->n_gen;
   if (graphs && !phases && (!s->sd_exec[0] || s->sd_key != key || s->sd_params != params)) {
     drop_graph(&s->sd_exec[0]);
@@ -1479,8 +1488,9 @@ int sd_loop(tppsd_state *s, int gamma, const float *params, int max_rounds, int 
     const double d = m->d(), F = m->cfg.d_ffn, rows = (double)s->B * (gamma + 1);
     s->round_flop = m->attnhp() ? 2.0 * rows * (L * (3 * d * 2 * d) + 4 * d * d)
                                 : 2.0 * rows * (L * (3 * d * d + d * d + 2 * d * F) + 4 * d * d);
-    if (int rc = make_events(s->gev, 2 * (5 * L + 1))) return rc;
-    s->ev_used.assign(5 * L + 1, 0);
+    // pairs: attention of each layer, the pass's GEMMs, the one-launch draft
+    if (int rc = make_events(s->gev, 2 * (5 * L + 2))) return rc;
+    s->ev_used.assign(5 * L + 2, 0);
   }
   if (phases)
     if (int rc = make_events(s->pev, 4)) return rc;

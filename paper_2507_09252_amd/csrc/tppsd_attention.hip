@@ -1,6 +1,6 @@
 // Causal attention of the verify, AR, prefill and layered draft passes over
-// the KV caches (MFMA kernels for bf16 and fp32, a generic tiled kernel, and
-// the merge of key splits), with their launchers.
+// the KV caches (MFMA kernels for bf16 and fp32, and the merge of key
+// splits), with their launchers.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -27,110 +27,6 @@ __device__ __forceinline__ void sink_adjust(float &M, float &L, float &O) {
   const float ms = fmaxf(M, 0.f), f = (M == -INFINITY) ? 0.f : expf(M - ms);
   L = L * f + expf(-ms);
   O *= f;
-}
-
-template <typename ACT, int DH, int ROLE>
-__global__ __launch_bounds__(256) void k_attn_generic(const ACT *__restrict__ q, const ACT *__restrict__ kc,
-                                                      const ACT *__restrict__ vc, ACT *__restrict__ o,
-                                                      const int32_t *__restrict__ start, int start_off,
-                                                      const int32_t *__restrict__ done, int P, int H,
-                                                      int cap, int sink) {
-  constexpr int QT = 16, KT = 64, EPT = (DH + 15) / 16;
-  __shared__ float qs[QT][DH];
-  __shared__ float ks[KT][DH + 1];
-  __shared__ float vs[KT][DH + 1];
-  __shared__ float ps[QT][KT + 1];
-  const int bh = blockIdx.x, b = bh / H, h = bh - b * H;
-  const int q0 = blockIdx.y * QT;
-  const int tid = threadIdx.x, qi = tid >> 4, sub = tid & 15;
-  const int d = H * DH;
-  const int nq = min(QT, P - q0);
-  const bool skip = done != nullptr && done[b] != 0;
-  const int base = start[b] + start_off;
-  if (skip) {
-    for (int idx = tid; idx < nq * DH; idx += 256) {
-      const int qq = idx / DH, j = idx - qq * DH;
-      st(o, (size_t)(b * P + q0 + qq) * d + h * DH + j, 0.f);
-    }
-    return;
-  }
-  const float scale = 1.f / sqrtf((float)DH);
-  for (int idx = tid; idx < QT * DH; idx += 256) {
-    const int qq = idx / DH, j = idx - qq * DH;
-    qs[qq][j] = (qq < nq) ? ld(q, (size_t)(b * P + q0 + qq) * d + h * DH + j) * scale : 0.f;
-  }
-  const int my_last = base + q0 + qi;             // last key index for this thread's query
-  const int n_keys = min(base + q0 + nq, cap);   // keys 0 .. n_keys-1 are needed by this tile
-  float m_run = -INFINITY, l_run = 0.f;
-  float acc[EPT];
-#pragma unroll
-  for (int i = 0; i < EPT; ++i) acc[i] = 0.f;
-  const size_t row0 = ((size_t)b * H + h) * cap;
-  for (int kt = 0; kt < n_keys; kt += KT) {
-    __syncthreads();
-    for (int idx = tid; idx < KT * DH; idx += 256) {
-      const int kk = idx / DH, j = idx - kk * DH;
-      const int key = kt + kk;
-      const bool ok = key < n_keys;
-      ks[kk][j] = ok ? ld(kc, (row0 + key) * DH + j) : 0.f;
-      vs[kk][j] = ok ? ld(vc, v_at<ACT>(row0, key, j, DH)) : 0.f;
-    }
-    __syncthreads();
-    // scores for query qi, keys sub + 16 i
-    float sc[4];
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int kk = sub + 16 * i, key = kt + kk;
-      float s = -INFINITY;
-      if (qi < nq && key <= my_last) {
-        s = 0.f;
-#pragma unroll
-        for (int j = 0; j < DH; ++j) s += qs[qi][j] * ks[kk][j];
-      }
-      sc[i] = s;
-      tmax = fmaxf(tmax, s);
-    }
-#pragma unroll
-    for (int off = 8; off > 0; off >>= 1) tmax = fmaxf(tmax, __shfl_xor(tmax, off, 16));
-    const float m_new = fmaxf(m_run, tmax);
-    const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run - m_new);
-    float psum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float pv = (sc[i] == -INFINITY) ? 0.f : expf(sc[i] - m_new);
-      ps[qi][sub + 16 * i] = pv;
-      psum += pv;
-    }
-#pragma unroll
-    for (int off = 8; off > 0; off >>= 1) psum += __shfl_xor(psum, off, 16);
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) {
-      const int j = sub + 16 * i;
-      if (j < DH) {
-        float a = acc[i] * alpha;
-        for (int kk = 0; kk < KT; ++kk) a += ps[qi][kk] * vs[kk][j];
-        acc[i] = a;
-      }
-    }
-  }
-  if (sink) {   // the AttNHP denominator 1 + sum f: a key of score 0 and value 0
-    const float ms = fmaxf(m_run, 0.f), f = (m_run == -INFINITY) ? 0.f : expf(m_run - ms);
-    l_run = l_run * f + expf(-ms);
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) acc[i] *= f;
-  }
-  if (qi < nq) {
-    const float inv = 1.f / l_run;
-#pragma unroll
-    for (int i = 0; i < EPT; ++i) {
-      const int j = sub + 16 * i;
-      if (j < DH) st(o, (size_t)(b * P + q0 + qi) * d + h * DH + j, acc[i] * inv);
-    }
-  }
 }
 
 // bf16 causal attention on MFMA with split keys (flash-decoding style).
@@ -268,8 +164,11 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
       for (int j = 0; j < 8; j += 2) {
         const float p0 = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
         const float p1 = (sv[j + 1] == -INFINITY) ? 0.f : expf(sv[j + 1] - m_new);
-        ps += p0 + p1;
-        pw[j >> 1] = pk2bf(p0, p1);
+        // P V takes the probabilities in bf16; the normaliser sums the same
+        // rounded values, so the output stays a convex combination of values
+        const uint32_t w = pk2bf(p0, p1);
+        ps += __uint_as_float(w << 16) + __uint_as_float(w & 0xFFFF0000u);
+        pw[j >> 1] = w;
       }
       const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, (uint4){pw[0], pw[1], pw[2], pw[3]});
       ps += __shfl_xor(ps, 16, 64);
@@ -523,26 +422,6 @@ __global__ void k_attn_combine(const float *__restrict__ part, ACT *__restrict__
   st(o, (size_t)(b * P + p) * (H * DH) + h * DH + j, L > 0.f ? O / L : 0.f);
 }
 
-// ev0/ev1 (optional): HIP events stamped with the main kernel's own start and
-// stop (hipExtLaunchKernelGGL), for the verify-attention timing
-template <typename ACT, int ROLE>
-static void attn_dispatch(const void *q, const void *kc, const void *vc, void *o, const int32_t *start,
-                          int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, int sink,
-                          hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  dim3 grid(B * H, (P + 15) / 16);
-  const ACT *Q = (const ACT *)q, *Kc = (const ACT *)kc, *Vc = (const ACT *)vc;
-  ACT *O = (ACT *)o;
-  auto go = [&](auto kern) {
-    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap,
-                          sink);
-  };
-  switch (dh) {
-    case 16: go(k_attn_generic<ACT, 16, ROLE>); break;
-    case 32: go(k_attn_generic<ACT, 32, ROLE>); break;
-    default: go(k_attn_generic<ACT, 64, ROLE>); break;
-  }
-}
-
 // All query tiles of a (sequence, head) share one workgroup (QT = 1..3 for
 // up to 48 new positions); the key range is split across workgroups when the
 // (sequence, head) pairs alone do not fill the chip.
@@ -572,19 +451,13 @@ static void attn_mfma(const ACT *Q, const ACT *Kc, const ACT *Vc, ACT *O, const 
   }
 }
 
+// ev0/ev1 (optional): HIP events stamped with the main kernel's own start and
+// stop (hipExtLaunchKernelGGL), for the verify-attention timing
 template <int ROLE>
 static void attention_role(const void *q, const void *kc, const void *vc, void *o, int bf16, const int32_t *start,
                            int start_off, const int32_t *done, int B, int P, int H, int dh, int cap, float *part,
                            int sink, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-  static const bool force_generic = [] {
-    const char *e = getenv("TPPSD_ATTN_GENERIC");
-    return e && e[0] == '1';
-  }();
   if (!bf16) {
-    if (force_generic) {
-      attn_dispatch<float, ROLE>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, sink, ev0, ev1, s);
-      return;
-    }
     const float *Q = (const float *)q, *Kc = (const float *)kc, *Vc = (const float *)vc;
     float *O = (float *)o;
     switch (dh) {
@@ -592,10 +465,6 @@ static void attention_role(const void *q, const void *kc, const void *vc, void *
       case 32: attn_mfma<float, 32, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, sink, ev0, ev1, s); break;
       default: attn_mfma<float, 64, ROLE>(Q, Kc, Vc, O, start, start_off, done, B, P, H, cap, part, sink, ev0, ev1, s); break;
     }
-    return;
-  }
-  if (force_generic) {
-    attn_dispatch<bf16_t, ROLE>(q, kc, vc, o, start, start_off, done, B, P, H, dh, cap, sink, ev0, ev1, s);
     return;
   }
   const bf16_t *Q = (const bf16_t *)q, *Kc = (const bf16_t *)kc, *Vc = (const bf16_t *)vc;

@@ -130,7 +130,6 @@ struct DraftArgs {
   int32_t *d_k;
   int MG;                   // row stride of the draft record (max_gamma)
   int w_lds;                // stage the weight matrices in LDS (fused_draft_weight_elems more)
-  int attn_mfma;            // attention on MFMA even for <= 4 heads (else the vector-ALU form)
 };
 // whether the fused draft kernel supports a model of these sizes: the
 // matrix-vector products need d / 8 and d_ffn / 8 to be powers of two <= 64,
@@ -142,6 +141,15 @@ inline bool fused_draft_ok(int L, int d, int H, int F) {
          F / 8 <= 64 && pow2(H) && d == 16 * H;
 }
 size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H);
+// One wave per sequence (k_draft_wave): draft models of width 16 or 32
+// (d_head 16), F = 2 d or 4 d, at most two layers, whose transposed matrices
+// fit in LDS beside four waves' scratch
+bool wave_draft_ok(int L, int d, int H, int F, int M, int K, int bf16);
+size_t wave_draft_lds_bytes(int L, int D, int F, int M, int K, int elt);
+void launch_draft_wave(const DraftArgs &a, int bf16, hipStream_t st, hipEvent_t ev0 = nullptr,
+                       hipEvent_t ev1 = nullptr);
+// raises the dynamic LDS limit of the wave-draft kernels; nonzero on failure
+int allow_draft_wave_lds(size_t bytes);
 // elements of the draft's weight matrices (per layer QKV, out, FFN; decoder), each
 // row padded by pad elements (16 bytes) in LDS
 size_t fused_draft_weight_elems(int L, int d, int F, int M, int K, int pad);
@@ -225,7 +233,8 @@ void launch_poisson_fit(const float *t, const int32_t *k, int B, int n0, int K, 
 void launch_draft_poisson(const PoissonDraftArgs &a, hipStream_t st);
 
 // ---- launchers (tppsd_kernels.hip) ----
-void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t st);
+void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t st, hipEvent_t ev0 = nullptr,
+                        hipEvent_t ev1 = nullptr);
 // raises the dynamic LDS limit of the fused draft kernels to `bytes`; nonzero on failure
 int allow_draft_fused_lds(size_t bytes);
 void launch_embed(float *x, int T, int d, int P, const TokSrc &src, const void *wtype, int bf16,

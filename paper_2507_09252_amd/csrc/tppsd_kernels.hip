@@ -1613,7 +1613,9 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
       for (int sidx = 0; sidx < NB; ++sidx)
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          sv[sidx][j] = (sv[sidx][j] == -INFINITY) ? 0.f : expf(sv[sidx][j] - m_new);
+          // bf16: P V takes the probabilities in bf16, and the normaliser sums
+          // the same rounded values
+          sv[sidx][j] = (sv[sidx][j] == -INFINITY) ? 0.f : rnd_act<ELT>(expf(sv[sidx][j] - m_new));
           ps += sv[sidx][j];
         }
       ps += swz_xor<16>(ps);
@@ -1673,9 +1675,12 @@ inline __host__ __device__ int fused_draft_vec_floats(int L, int d, int F, int M
 
 // floats before the staged weights (activations, merge scratch, vectors),
 // rounded up to a 16-byte boundary
+// attention merge scratch: one (max, sum, output) slot per wave and query
+inline __host__ __device__ int fused_draft_red_floats(int H, int dh) { return 4 * H * 2 * (dh + 2); }
+
 inline __host__ __device__ int fused_draft_head_floats(int L, int d, int F, int M, int K, int H) {
   const int Fm = d > F ? d : F, dh = d / H;
-  const int n = 2 * d + 2 * Fm + 2 * d + 2 * d + 2 * F + 4 * d + 3 * M + K + 8 + 4 * H * 2 * (dh + 2) +
+  const int n = 2 * d + 2 * Fm + 2 * d + 2 * d + 2 * F + 4 * d + 3 * M + K + 8 + fused_draft_red_floats(H, dh) +
                 fused_draft_vec_floats(L, d, F, M, K);
   return (n + 3) & ~3;
 }
@@ -1690,8 +1695,8 @@ size_t fused_draft_lds_bytes(int L, int d, int F, int M, int K, int H) {
 
 // CD / CF: chunks per lane of the matrix-vector products over d and over
 // d_ffn (gemv_cpl), fixed per model so that each product has one code path
-template <typename ELT, int DH, int CD, int CF>
-__global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
+template <typename ELT, int DH, int CD, int CF, int NT>
+__global__ __launch_bounds__(NT) void k_draft_fused(DraftArgs a) {
   extern __shared__ __attribute__((aligned(16))) float sm[];
   __shared__ float tok_t[2], t_last;
   __shared__ int tok_k[2];
@@ -1706,7 +1711,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
   float *es = hs + 2 * F;   // [4d] decoder e | tanh activations
   float *hv = es + 4 * d;   // [3M + K] decoder outputs
   float *red = hv + 3 * M + K + 8;   // attention merge scratch
-  float *vec = red + 4 * H * 2 * (DH + 2);   // staged small vectors
+  float *vec = red + fused_draft_red_floats(H, DH);   // staged small vectors
   const int b = blockIdx.x, tid = threadIdx.x;
   if (a.done[b]) return;
   // every LayerNorm and bias vector of the model goes to LDS once, so that
@@ -1830,7 +1835,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
             }
           });
       __syncthreads();   // keys and values in the cache before the attention reads them
-      if (H <= 4 && !a.attn_mfma)
+      if (H <= 4)
         P == 2 ? wg_attention_valu<ELT, 2>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red)
                : wg_attention_valu<ELT, 1>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       else
@@ -1938,7 +1943,7 @@ __global__ __launch_bounds__(256) void k_draft_fused(DraftArgs a) {
   }
 }
 
-void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
+void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const size_t lds = fused_draft_lds_bytes(a.L, a.d, a.F, a.M, a.K, a.H) +
                      (a.w_lds ? fused_draft_weight_elems(a.L, a.d, a.F, a.M, a.K, bf16 ? 8 : 4) * (bf16 ? 2 : 4) : 0);
   // chunks per lane of the d-wide and F-wide products: d / 16 (two lanes
@@ -1946,34 +1951,25 @@ void launch_draft_fused(const DraftArgs &a, int bf16, hipStream_t s) {
   // second FFN product over all 256 lanes), each within 2..8 -- measured
   // against one chunk set per lane of K / 8 <= 8: 180 -> 154 us per draft
   // round at d = 32 / F = 128, 480 -> 462 us at d = 64 / F = 256.
-  // TPPSD_DRAFT_CPL="cd,cf" overrides (2, 4 or 8 each, at most K / 8).
   int cd = std::min(8, std::max(2, a.d / 16)), cf = std::min(8, std::max(2, a.F * a.d / 2048));
   cd = std::min(cd, gemv_cpl(a.d));
   cf = std::min(cf, gemv_cpl(a.F));
-  if (const char *ev = getenv("TPPSD_DRAFT_CPL")) {
-    int x = 0, y = 0;
-    if (sscanf(ev, "%d,%d", &x, &y) == 2 && (x == 2 || x == 4 || x == 8) && (y == 2 || y == 4 || y == 8) &&
-        x <= a.d / 8 && y <= a.F / 8) {
-      cd = x;
-      cf = y;
-    }
-  }
-  // d_head = 16 only (fused_draft_ok); chunk counts 2, 4 or 8
-  auto go = [&](auto kern) { kern<<<a.B, 256, lds, s>>>(a); };
-#define TPPSD_FD(ELT)                                                             \
-  if (cd == 2 && cf == 2) go(k_draft_fused<ELT, 16, 2, 2>);                        \
-  else if (cd == 2 && cf == 4) go(k_draft_fused<ELT, 16, 2, 4>);                   \
-  else if (cd == 2) go(k_draft_fused<ELT, 16, 2, 8>);                              \
-  else if (cd == 4 && cf == 2) go(k_draft_fused<ELT, 16, 4, 2>);                   \
-  else if (cd == 4 && cf == 4) go(k_draft_fused<ELT, 16, 4, 4>);                   \
-  else if (cd == 4) go(k_draft_fused<ELT, 16, 4, 8>);                              \
-  else if (cf == 2) go(k_draft_fused<ELT, 16, 8, 2>);                              \
-  else if (cf == 4) go(k_draft_fused<ELT, 16, 8, 4>);                              \
-  else go(k_draft_fused<ELT, 16, 8, 8>);
+  auto go = [&](auto kern, int nt) { hipExtLaunchKernelGGL(kern, dim3(a.B), dim3(nt), lds, s, ev0, ev1, 0, a); };
+  // chunk counts 2, 4 or 8; four waves
+#define TPPSD_FD(ELT, DH, NT)                                                       \
+  if (cd == 2 && cf == 2) go(k_draft_fused<ELT, DH, 2, 2, NT>, NT);                 \
+  else if (cd == 2 && cf == 4) go(k_draft_fused<ELT, DH, 2, 4, NT>, NT);            \
+  else if (cd == 2) go(k_draft_fused<ELT, DH, 2, 8, NT>, NT);                       \
+  else if (cd == 4 && cf == 2) go(k_draft_fused<ELT, DH, 4, 2, NT>, NT);            \
+  else if (cd == 4 && cf == 4) go(k_draft_fused<ELT, DH, 4, 4, NT>, NT);            \
+  else if (cd == 4) go(k_draft_fused<ELT, DH, 4, 8, NT>, NT);                       \
+  else if (cf == 2) go(k_draft_fused<ELT, DH, 8, 2, NT>, NT);                       \
+  else if (cf == 4) go(k_draft_fused<ELT, DH, 8, 4, NT>, NT);                       \
+  else go(k_draft_fused<ELT, DH, 8, 8, NT>, NT);
   if (bf16) {
-    TPPSD_FD(bf16_t)
+    TPPSD_FD(bf16_t, 16, 256)
   } else {
-    TPPSD_FD(float)
+    TPPSD_FD(float, 16, 256)
   }
 #undef TPPSD_FD
 }
@@ -1985,12 +1981,463 @@ int allow_draft_fused_lds(size_t bytes) {
            hipSuccess;
   };
 #define TPPSD_FD(ELT)                                                                          \
-  set(k_draft_fused<ELT, 16, 2, 2>), set(k_draft_fused<ELT, 16, 2, 4>), set(k_draft_fused<ELT, 16, 2, 8>); \
-  set(k_draft_fused<ELT, 16, 4, 2>), set(k_draft_fused<ELT, 16, 4, 4>), set(k_draft_fused<ELT, 16, 4, 8>); \
-  set(k_draft_fused<ELT, 16, 8, 2>), set(k_draft_fused<ELT, 16, 8, 4>), set(k_draft_fused<ELT, 16, 8, 8>);
+  set(k_draft_fused<ELT, 16, 2, 2, 256>), set(k_draft_fused<ELT, 16, 2, 4, 256>), set(k_draft_fused<ELT, 16, 2, 8, 256>); \
+  set(k_draft_fused<ELT, 16, 4, 2, 256>), set(k_draft_fused<ELT, 16, 4, 4, 256>), set(k_draft_fused<ELT, 16, 4, 8, 256>); \
+  set(k_draft_fused<ELT, 16, 8, 2, 256>), set(k_draft_fused<ELT, 16, 8, 4, 256>), set(k_draft_fused<ELT, 16, 8, 8, 256>);
   TPPSD_FD(bf16_t)
   TPPSD_FD(float)
 #undef TPPSD_FD
+  return bad;
+}
+
+// ---------------------------------------------------------------------------
+// Drafting for small draft models (§4.3 "Drafting"), one wave per sequence:
+// all gamma draft steps of a sequence run in one wave with no workgroup
+// barrier after the weights are staged. A model of width D <= 32 puts one
+// token's activations on D lanes (the two tokens of the first step on lanes
+// 0..D-1 and 32..32+D-1); every matrix-vector product reads its matrix
+// transposed from LDS ([in][out], so that lanes take consecutive outputs and
+// one input broadcast per step of the dot product), staged once per
+// workgroup of four sequences. The attention gives each lane one 8-position
+// block of a head's cache at a time (eight key rows and the value block, 16
+// bytes per load) and merges the lanes of a head by cross-lane reductions.
+// Rounding points are those of the layered kernels.
+// ---------------------------------------------------------------------------
+// LDS floats of one wave's scratch for a model of width D, FFN width F, M
+// mixture components and K types
+inline __host__ __device__ int wave_draft_scratch_floats(int D, int F, int M, int K) {
+  return 2 * 32 + 2 * 32 + 2 * 32 + 2 * 32 + 2 * F + 4 * D + 3 * M + K + 4;
+}
+// elements of the transposed weight matrices staged in LDS, and the floats of
+// the small vectors
+inline __host__ __device__ int wave_draft_weight_elems(int L, int D, int F, int M, int K) {
+  return L * (3 * D * D + D * D + D * F + F * D) + D * 4 * D + D * (3 * M + K);
+}
+inline __host__ __device__ int wave_draft_vec_floats(int L, int D, int F, int M, int K) {
+  return L * (9 * D + F) + 4 * D + 3 * M + K;
+}
+size_t wave_draft_lds_bytes(int L, int D, int F, int M, int K, int elt) {
+  const size_t w = ((size_t)wave_draft_weight_elems(L, D, F, M, K) * elt + 15) / 16 * 16;
+  return w + 4 * ((size_t)wave_draft_vec_floats(L, D, F, M, K) + 4 * (size_t)wave_draft_scratch_floats(D, F, M, K));
+}
+
+// y[p][n] = sum_k WT[k][n] x[p][k] for n < N, p < P, handed to epi(p, n, y);
+// lane takes n = lane, lane + 64, ...
+template <typename ELT, typename XF, typename EPI>
+__device__ __forceinline__ void wave_gemv(const ELT *WT, int N, int KD, int P, XF xin, EPI epi) {
+  const int lane = threadIdx.x & 63;
+  for (int n = lane; n < N; n += 64) {
+    float acc0 = 0.f, acc1 = 0.f;
+    const float *x0 = xin(n, 0), *x1 = xin(n, P - 1);
+    // a few dot-product steps' loads in flight, not all of them (registers)
+#pragma unroll 8
+    for (int k = 0; k < KD; ++k) {
+      const float w = ld(WT, (size_t)k * N + n);
+      acc0 += w * x0[k];
+      acc1 += w * x1[k];
+    }
+    epi(0, n, acc0);
+    if (P == 2) epi(1, n, acc1);
+  }
+}
+
+// LDS written by some lanes of the wave, then read by others
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// resident workgroups of four waves per CU the register allocation aims at
+// (4: 128 VGPRs with spills, c5 draft 472 us per round; 2: ~190 VGPRs, 309 us)
+#ifndef TPPSD_WAVE_DRAFT_WG_PER_CU
+#define TPPSD_WAVE_DRAFT_WG_PER_CU 2
+#endif
+template <typename ELT, int D, int F, int H>
+__global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(DraftArgs a) {
+  constexpr int DH = D / H;
+  static_assert(DH == 16 && D <= 32 && F <= 128, "one wave per sequence: d <= 32, d_head 16");
+  extern __shared__ __attribute__((aligned(16))) float smw[];
+  const int M = a.M, K = a.K, L = a.L;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  // ---- weights (transposed) and vectors, staged once per workgroup
+  ELT *wl = (ELT *)smw;
+  const int LW = 3 * D * D + D * D + D * F + F * D;   // elements per layer
+  const int NH = 3 * M + K;
+  float *vec = smw + ((size_t)wave_draft_weight_elems(L, D, F, M, K) * sizeof(ELT) + 15) / 16 * 4;
+  float *scr = vec + wave_draft_vec_floats(L, D, F, M, K) + wave * wave_draft_scratch_floats(D, F, M, K);
+  {
+    // W [N][Kd] (global) -> WT [Kd][N] (LDS)
+    auto cpt = [&](ELT *dst, const void *src, int N, int Kd) {
+      const ELT *sp = (const ELT *)src;
+      for (int i = tid; i < N * Kd; i += blockDim.x) {
+        const int n = i / Kd, k = i - n * Kd;
+        dst[(size_t)k * N + n] = sp[i];
+      }
+    };
+    for (int ly = 0; ly < L; ++ly) {
+      const FusedLayerW &w = a.layer[ly];
+      ELT *b0 = wl + (size_t)ly * LW;
+      cpt(b0, w.qkv_w, 3 * D, D);
+      cpt(b0 + 3 * D * D, w.out_w, D, D);
+      cpt(b0 + 4 * D * D, w.ffn1_w, F, D);
+      cpt(b0 + 4 * D * D + D * F, w.ffn2_w, D, F);
+    }
+    ELT *hb = wl + (size_t)L * LW;
+    cpt(hb, a.Ek1_w, 4 * D, D);
+    // the decoder heads as one [D][3M + K] matrix: columns < 3M the mixture
+    // heads (w, mu, log sigma, read from the e slices), then the type head
+    const ELT *mw = (const ELT *)a.mix_w, *kw = (const ELT *)a.k2_w;
+    for (int i = tid; i < NH * D; i += blockDim.x) {
+      const int n = i / D, k = i - n * D;
+      hb[4 * D * D + (size_t)k * NH + n] = n < 3 * M ? mw[(size_t)n * D + k] : kw[(size_t)(n - 3 * M) * D + k];
+    }
+    auto cp = [&](float *dst, const float *src, int cnt) {
+      for (int i = tid; i < cnt; i += blockDim.x) dst[i] = src[i];
+    };
+    for (int ly = 0; ly < L; ++ly) {
+      const FusedLayerW &w = a.layer[ly];
+      float *v = vec + ly * (9 * D + F);
+      cp(v, w.ln1_g, D);
+      cp(v + D, w.ln1_b, D);
+      cp(v + 2 * D, w.qkv_b, 3 * D);
+      cp(v + 5 * D, w.out_b, D);
+      cp(v + 6 * D, w.ln2_g, D);
+      cp(v + 7 * D, w.ln2_b, D);
+      cp(v + 8 * D, w.ffn1_b, F);
+      cp(v + 8 * D + F, w.ffn2_b, D);
+    }
+    float *v = vec + L * (9 * D + F);
+    cp(v, a.lnf_g, D);
+    cp(v + D, a.lnf_b, D);
+    cp(v + 2 * D, a.k1_b, D);
+    cp(v + 3 * D, a.mix_b, 3 * M);
+    cp(v + 3 * D + 3 * M, a.k2_b, K);
+    cp(v + 3 * D + 3 * M + K, a.freq, D);
+  }
+  __syncthreads();   // the only workgroup barrier: waves are independent from here
+  const int b = blockIdx.x * 4 + wave;
+  if (b >= a.B || a.done[b]) return;
+  const float *hvec = vec + L * (9 * D + F);
+  const float *lnf_g = hvec, *lnf_b = hvec + D, *k1_b = hvec + 2 * D, *mix_b = hvec + 3 * D,
+              *k2_b = hvec + 3 * D + 3 * M, *freq = hvec + 3 * D + 3 * M + K;
+  // per-wave scratch: token rows of 32 floats
+  float *xs = scr;            // [2][32] residual stream
+  float *as = xs + 64;        // [2][32] LayerNorm output
+  float *qs = as + 64;        // [2][32] queries
+  float *os = qs + 64;        // [2][32] attention output
+  float *hs = os + 64;        // [2][F] FFN hidden
+  float *es = hs + 2 * F;     // [4D] decoder e | tanh
+  float *hv = es + 4 * D;     // [3M + K] decoder outputs
+  const int n = a.n[b], base = a.lenD[b];
+  const uint64_t r = (uint64_t)a.rnd[b];
+  const size_t seq_row0 = (size_t)b * H * a.cap;
+  const ELT *wtype = (const ELT *)a.type_emb;
+  // the draws' uniforms: lane l - 1 holds step l's (Box-Muller epsilon in u[1])
+  float u0 = 0.f, eps = 0.f, u3 = 0.f;
+  if (lane < a.gamma) {
+    float u[4];
+    philox_uniforms(a.seed, (uint64_t)b, r, (uint64_t)(lane + 1), TAG_DRAFT, u);
+    u0 = u[0];
+    eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
+    u3 = u[3];
+  }
+  auto at = [](float v, int i) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i)); };
+  float t_last = a.ev_t[(size_t)b * a.ev_stride + n - 1];
+  float tok_t = 0.f;
+  int tok_k = 0;
+  // lane's token (p = lane / 32) and dimension (j = lane % 32) in the D-lane layout
+  const int lp = lane >> 5, lj = lane & 31;
+  for (int l = 1; l <= a.gamma; ++l) {
+    const int P = (l == 1) ? 2 : 1;
+    const int pos0 = (l == 1) ? base : base + l;
+    // ---- embedding
+    {
+      float t;
+      int k;
+      if (l == 1) {
+        const size_t i = (size_t)b * a.ev_stride + n - 2 + lp;
+        t = a.ev_t[i];
+        k = a.ev_k[i];
+      } else {
+        t = tok_t;
+        k = tok_k;
+      }
+      if (lj < D && lp < P) {
+        const float arg = t * freq[lj];
+        const int kk = min(max(k, 0), K - 1);
+        xs[lp * 32 + lj] = ((lj & 1) ? cosf(arg) : sinf(arg)) + ld(wtype, (size_t)kk * D + lj);
+      }
+    }
+    wave_lds_sync();
+    for (int ly = 0; ly < L; ++ly) {
+      const ELT *wq = wl + (size_t)ly * LW, *wo = wq + 3 * D * D, *w1 = wq + 4 * D * D, *w2 = w1 + D * F;
+      const float *lv = vec + ly * (9 * D + F);
+      ELT *kc = (ELT *)(a.kc + a.layer_bytes * ly);
+      ELT *vc = (ELT *)(a.vc + a.layer_bytes * ly);
+      // LayerNorm of each token over its D lanes
+      auto layernorm = [&](const float *g, const float *bt, float *dst, int np) {
+        const float xv = (lj < D && lp < np) ? xs[lp * 32 + lj] : 0.f;
+        const float mean = group_sum(xv, 32) / (float)D;
+        const float c = (lj < D) ? xv - mean : 0.f;
+        const float rstd = 1.f / sqrtf(group_sum(c * c, 32) / (float)D + 1e-5f);
+        if (lj < D && lp < np) dst[lp * 32 + lj] = rnd_act<ELT>(c * rstd * g[lj] + bt[lj]);
+        wave_lds_sync();
+      };
+      layernorm(lv, lv + D, as, P);
+      // q, k, v; keys and values of positions pos0 .. pos0 + P - 1 into the cache
+      wave_gemv<ELT>(wq, 3 * D, D, P, [&](int, int p) { return (const float *)(as + p * 32); },
+                     [&](int p, int nn, float acc) {
+                       const float v = rnd_act<ELT>(acc + lv[2 * D + nn]);
+                       const int which = nn / D, c = nn - which * D;
+                       if (which == 0) {
+                         qs[p * 32 + c] = v;
+                       } else {
+                         const int hh = c / DH, j = c - hh * DH, pos = pos0 + p;
+                         const size_t row0 = seq_row0 + (size_t)hh * a.cap;
+                         if (pos < a.cap)
+                           st(which == 1 ? kc : vc, which == 1 ? (row0 + pos) * DH + j : v_at<ELT>(row0, pos, j, DH), v);
+                         else
+                           atomicOr(a.status, TPPSD_STATUS_CAPACITY);
+                       }
+                     });
+      __threadfence_block();   // this wave's cache stores before its reads below
+      wave_lds_sync();
+      // ---- attention: head hh on lanes [hh * 64 / H, (hh + 1) * 64 / H); a lane
+      // takes units of 2 positions (the unit's key rows, and for bf16 its two
+      // positions of the position-blocked value block, for fp32 its value rows); one
+      // query at a time (two only in the first step), so that a unit, the
+      // query and its running output fit beside each other in registers
+      for (int p = 0; p < P; ++p) {
+        constexpr int LPH = 64 / H, U = 2;
+        constexpr int NKV = U * DH * (int)sizeof(ELT) / 16;   // 16-byte vectors of a unit's keys
+        const int hh = lane / LPH, sub = lane - hh * LPH;
+        const int n_keys = min(pos0 + P, a.cap), last = pos0 + p;
+        const size_t row0 = seq_row0 + (size_t)hh * a.cap;
+        float q[DH];
+#pragma unroll
+        for (int j = 0; j < DH; ++j) q[j] = qs[p * 32 + hh * DH + j] * 0.25f;   // 1 / sqrt(16)
+        float m = -INFINITY, lsum = 0.f, o[DH];
+#pragma unroll
+        for (int j = 0; j < DH; ++j) o[j] = 0.f;
+        for (int u = sub; u * U < n_keys; u += LPH) {
+          const int k0 = u * U;   // inside the slab (rounded up to 8 positions); slots past n_keys masked
+          uint4 kr[NKV];
+          uint32_t vr1[sizeof(ELT) == 2 ? 16 : 1];
+          uint4 vr4[sizeof(ELT) == 2 ? 1 : NKV];
+          const uint4 *kp = (const uint4 *)(kc + (row0 + k0) * DH);
+#pragma unroll
+          for (int i = 0; i < NKV; ++i) kr[i] = kp[i];
+          if constexpr (sizeof(ELT) == 2) {
+            // the unit's two positions of each value column's 8-position block
+            const bf16_t *vb = (const bf16_t *)vc + v_at<bf16_t>(row0, k0 & ~7, 0, DH) + (k0 & 6);
+#pragma unroll
+            for (int j = 0; j < 16; ++j) vr1[j] = *(const uint32_t *)(vb + 8 * j);
+          } else {
+            const uint4 *vp = (const uint4 *)(vc + (row0 + k0) * DH);
+#pragma unroll
+            for (int i = 0; i < NKV; ++i) vr4[i] = vp[i];
+          }
+          // element (key i, column j) of the unit's keys and values
+          auto kval = [&](int i, int j) -> float {
+            if constexpr (sizeof(ELT) == 2) {
+              const uint4 w = kr[2 * i + (j >> 3)];
+              const int e = (j & 7) >> 1;
+              const uint32_t x = e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w;
+              return (j & 1) ? __uint_as_float(x & 0xFFFF0000u) : __uint_as_float(x << 16);
+            } else {
+              const uint4 w = kr[4 * i + (j >> 2)];
+              const int e = j & 3;
+              return __uint_as_float(e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w);
+            }
+          };
+          auto vval = [&](int i, int j) -> float {
+            if constexpr (sizeof(ELT) == 2) {
+              const uint32_t x = vr1[j];
+              return (i & 1) ? __uint_as_float(x & 0xFFFF0000u) : __uint_as_float(x << 16);
+            } else {
+              const uint4 w = vr4[4 * i + (j >> 2)];
+              const int e = j & 3;
+              return __uint_as_float(e == 0 ? w.x : e == 1 ? w.y : e == 2 ? w.z : w.w);
+            }
+          };
+          float sc[U], mx = -INFINITY;
+#pragma unroll
+          for (int i = 0; i < U; ++i) {
+            float dot = 0.f;
+#pragma unroll
+            for (int j = 0; j < DH; ++j) dot += q[j] * kval(i, j);
+            sc[i] = (k0 + i < n_keys && k0 + i <= last) ? dot : -INFINITY;
+            mx = fmaxf(mx, sc[i]);
+          }
+          const float mn = fmaxf(m, mx);
+          const float al = (mn == -INFINITY) ? 1.f : expf(m - mn);
+          lsum *= al;
+#pragma unroll
+          for (int j = 0; j < DH; ++j) o[j] *= al;
+#pragma unroll
+          for (int i = 0; i < U; ++i) {
+            // masked slots hold unwritten or stale values: skipped, not weighted by 0
+            if (sc[i] == -INFINITY) continue;
+            const float e = expf(sc[i] - mn);
+            lsum += e;
+#pragma unroll
+            for (int j = 0; j < DH; ++j) o[j] += e * vval(i, j);
+          }
+          m = mn;
+        }
+        // merge the head's lanes: maximum, rescaled sums, and the 16 column
+        // sums by recursive halving (lane ends with column c of its group)
+        float M_ = m;
+        M_ = fmaxf(M_, dpp_mov<0xB1>(M_));
+        M_ = fmaxf(M_, dpp_mov<0x4E>(M_));
+        M_ = fmaxf(M_, swz_xor<4>(M_));
+        M_ = fmaxf(M_, swz_xor<8>(M_));
+        M_ = fmaxf(M_, swz_xor<16>(M_));
+        if (LPH == 64) M_ = fmaxf(M_, __shfl_xor(M_, 32, 64));
+        const float f = (m == -INFINITY) ? 0.f : expf(m - M_);
+        const float lw = group_sum(lsum * f, LPH);
+        float ow[16];
+#pragma unroll
+        for (int j = 0; j < DH; ++j) ow[j] = o[j] * f;
+        if (LPH == 64) {
+#pragma unroll
+          for (int j = 0; j < DH; ++j) ow[j] += __shfl_xor(ow[j], 32, 64);
+        }
+        halve_step<8>(ow, (lane & 16) != 0, [](float v) { return swz_xor<16>(v); });
+        halve_step<4>(ow, (lane & 8) != 0, [](float v) { return swz_xor<8>(v); });
+        halve_step<2>(ow, (lane & 4) != 0, [](float v) { return swz_xor<4>(v); });
+        halve_step<1>(ow, (lane & 2) != 0, [](float v) { return dpp_mov<0x4E>(v); });
+        const float oc = ow[0] + dpp_mov<0xB1>(ow[0]);
+        const int c = 8 * ((lane >> 4) & 1) + 4 * ((lane >> 3) & 1) + 2 * ((lane >> 2) & 1) + ((lane >> 1) & 1);
+        if ((lane & 1) == 0 && (LPH == 32 || lane < 32)) os[p * 32 + hh * DH + c] = rnd_act<ELT>(lw > 0.f ? oc / lw : 0.f);
+      }
+      wave_lds_sync();
+      // output projection + residual
+      wave_gemv<ELT>(wo, D, D, P, [&](int, int p) { return (const float *)(os + p * 32); },
+                     [&](int p, int nn, float acc) { xs[p * 32 + nn] += acc + lv[5 * D + nn]; });
+      wave_lds_sync();
+      layernorm(lv + 6 * D, lv + 7 * D, as, P);
+      wave_gemv<ELT>(w1, F, D, P, [&](int, int p) { return (const float *)(as + p * 32); },
+                     [&](int p, int nn, float acc) { hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + lv[8 * D + nn], 0.f)); });
+      wave_lds_sync();
+      wave_gemv<ELT>(w2, D, F, P, [&](int, int p) { return (const float *)(hs + p * F); },
+                     [&](int p, int nn, float acc) { xs[p * 32 + nn] += acc + lv[8 * D + F + nn]; });
+      wave_lds_sync();
+    }
+    // ---- decoder on the last token
+    {
+      const int pl = P - 1;
+      const float xv = (lj < D && lp == 0) ? xs[pl * 32 + lj] : 0.f;
+      const float mean = group_sum(xv, 32) / (float)D;
+      const float c = (lj < D) ? xv - mean : 0.f;
+      const float rstd = 1.f / sqrtf(group_sum(c * c, 32) / (float)D + 1e-5f);
+      if (lj < D && lp == 0) as[lj] = rnd_act<ELT>(c * rstd * lnf_g[lj] + lnf_b[lj]);
+      wave_lds_sync();
+    }
+    const ELT *we = wl + (size_t)L * LW, *wh = we + 4 * D * D;
+    wave_gemv<ELT>(we, 4 * D, D, 1, [&](int, int) { return (const float *)as; },
+                   [&](int, int nn, float acc) {
+                     es[nn] = (nn < 3 * D) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * D]));
+                   });
+    wave_lds_sync();
+    wave_gemv<ELT>(wh, NH, D, 1, [&](int nn, int) { return (const float *)(es + (nn < 3 * M ? nn / M : 3) * D); },
+                   [&](int, int nn, float acc) { hv[nn] = acc + (nn < 3 * M ? mix_b[nn] : k2_b[nn - 3 * M]); });
+    wave_lds_sync();
+    {
+      // the log-softmaxes, the draft record, and the draft event
+      const float lw = lane < M ? hv[lane] : -INFINITY;
+      const float mu_l = lane < M ? hv[M + lane] : 0.f, s_l = lane < M ? hv[2 * M + lane] : 0.f;
+      const float lk = lane < K ? hv[3 * M + lane] : -INFINITY;
+      const float mw2 = wave_max(lw);
+      const float sw = wave_sum(lane < M ? expf(lw - mw2) : 0.f);
+      const float mk = wave_max(lk);
+      const float sk = wave_sum(lane < K ? expf(lk - mk) : 0.f);
+      const float nlw = lw - mw2 - logf(sw), nlk = lk - mk - logf(sk);
+      const size_t di = (size_t)b * a.MG + (l - 1);
+      if (lane < M) {
+        a.d_mix[di * 3 * M + lane] = nlw;
+        a.d_mix[di * 3 * M + M + lane] = mu_l;
+        a.d_mix[di * 3 * M + 2 * M + lane] = s_l;
+      }
+      if (lane < K) a.d_logtype[di * K + lane] = nlk;
+      auto draw = [&](float lp_, int cnt, float u) {
+        float cs = lane < cnt ? expf(lp_) : 0.f;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const float oo = __shfl_up(cs, off, 64);
+          if (lane >= off) cs += oo;
+        }
+        const float tot = __shfl(cs, cnt - 1, 64);
+        const unsigned long long hit = __ballot(lane < cnt && u * tot < cs);
+        return hit ? (int)__builtin_ctzll(hit) : cnt - 1;
+      };
+      const int z = draw(nlw, M, at(u0, l - 1));
+      const float tau = expf(at(mu_l, z) + expf(at(s_l, z)) * at(eps, l - 1));
+      const int kk = draw(nlk, K, at(u3, l - 1));
+      const float lt = logf(tau);
+      float cterm = -INFINITY;
+      if (lane < M) {
+        const float zz = lt - mu_l;
+        cterm = nlw - s_l - 0.918938533204672742f - lt - 0.5f * zz * zz * expf(-2.f * s_l);
+      }
+      const float cm = wave_max(cterm);
+      const float lg = cm + logf(wave_sum(lane < M ? expf(cterm - cm) : 0.f));
+      const float lf = at(nlk, kk);
+      const float tn = t_last + tau;
+      if (lane == 0) {
+        a.d_tau[di] = tau;
+        a.d_t[di] = tn;
+        a.d_k[di] = kk;
+        a.d_logg[di] = lg;
+        a.d_logf[di] = lf;
+        if (!isfinite(tau)) atomicOr(a.status, TPPSD_STATUS_NONFINITE);
+      }
+      tok_t = tn;
+      tok_k = kk;
+      t_last = tn;
+    }
+    wave_lds_sync();
+  }
+}
+
+bool wave_draft_ok(int L, int d, int H, int F, int M, int K, int bf16) {
+  const bool shape = L <= 2 && H >= 1 && d == 16 * H && (d == 16 || d == 32) && (F == 2 * d || F == 4 * d) &&
+                     3 * M + K <= 128 && M <= 64 && K <= 64;
+  return shape && wave_draft_lds_bytes(L, d, F, M, K, bf16 ? 2 : 4) <= 128 * 1024;
+}
+
+void launch_draft_wave(const DraftArgs &a, int bf16, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const size_t lds = wave_draft_lds_bytes(a.L, a.d, a.F, a.M, a.K, bf16 ? 2 : 4);
+  auto go = [&](auto kern) {
+    hipExtLaunchKernelGGL(kern, dim3((a.B + 3) / 4), dim3(256), lds, s, ev0, ev1, 0, a);
+  };
+#define TPPSD_DW(ELT)                                                  \
+  if (a.d == 16) {                                                     \
+    if (a.F == 32) go(k_draft_wave<ELT, 16, 32, 1>);                   \
+    else go(k_draft_wave<ELT, 16, 64, 1>);                             \
+  } else {                                                             \
+    if (a.F == 64) go(k_draft_wave<ELT, 32, 64, 2>);                   \
+    else go(k_draft_wave<ELT, 32, 128, 2>);                            \
+  }
+  if (bf16) {
+    TPPSD_DW(bf16_t)
+  } else {
+    TPPSD_DW(float)
+  }
+#undef TPPSD_DW
+}
+
+int allow_draft_wave_lds(size_t bytes) {
+  int bad = 0;
+  auto set = [&](auto kern) {
+    bad |= hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) !=
+           hipSuccess;
+  };
+  set(k_draft_wave<bf16_t, 16, 32, 1>), set(k_draft_wave<bf16_t, 16, 64, 1>);
+  set(k_draft_wave<bf16_t, 32, 64, 2>), set(k_draft_wave<bf16_t, 32, 128, 2>);
+  set(k_draft_wave<float, 16, 32, 1>), set(k_draft_wave<float, 16, 64, 1>);
+  set(k_draft_wave<float, 32, 64, 2>), set(k_draft_wave<float, 32, 128, 2>);
   return bad;
 }
 

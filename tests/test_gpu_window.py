@@ -17,7 +17,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_common import (CAT_TIE, NEAR_TIE, TOL, compare_events, first_fragile, gpu_state, histories,
+from gpu_common import (CAT_TIE, NEAR_TIE, compare_events, first_fragile, gpu_state, histories, tol_of,
                         oracle_models, small, to_dev, verify_buffers_from_oracle, draft_buffers_from_oracle, weights)
 from oracle import sampler as S
 from paper_2507_09252_amd import tppsd as tp
@@ -137,7 +137,7 @@ def test_window_end_to_end(case, kind):
     ll = st.tppsd_read_loglik().cpu().numpy()
     status = st.tppsd_state_status()
     assert status["bits"] == 0 and status["n_done"] == case.B, status
-    tol = TOL[case.wl.prec]
+    tol = tol_of(case.wl)
     upto = first_fragile(ref.log_margin, ref.cat_margin, tol + NEAR_TIE, max(CAT_TIE, tol))
     frac = compare_events(t[:, n0:n0 + n_gen], k[:, n0:n0 + n_gen], ref.t[:, n0:n0 + n_gen],
                           ref.k[:, n0:n0 + n_gen], np.minimum(upto, ref.gen), rtol=RTOL_T[case.wl.prec])
