@@ -217,6 +217,21 @@ int tppsd_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream
 int tppsd_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_verify_buf *out,
                  hipStream_t stream);
 
+/* tppsd_verify for callers that cannot allocate device memory of their own
+ * for the pass's temporaries (code under HIP graph capture, serving loops
+ * that forbid allocation): the same kernels and results, with the pass's
+ * activation scratch (residual stream, layer and decoder activations, logits,
+ * attention key-split partials) in a static device array of the library
+ * instead of the state's workspace. The array holds 64 MiB per GPU, kept
+ * until the process ends; a pass that needs more (about B (gamma + 1) rows of
+ * the widest model's activations plus the key-split partials) fails with
+ * TPPSD_E_WORKSPACE. The array keeps the last call's contents and is shared by
+ * every call on that GPU: calls that overlap on one GPU race. Arguments,
+ * outputs and other errors as tppsd_verify; TPPSD_E_HIP if the array's device
+ * address cannot be resolved. */
+int tppsd_verify_noalloc(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_verify_buf *out,
+                         hipStream_t stream);
+
 /* Accept/reject and commit (§4.3, Eq. (3)-(4), Theorem 1, Algorithm 1).
  * Position l passes iff ln u_tau < log g_T - log g_D and ln u_k < log f_T -
  * log f_D; L is the first failing position. At L each failed component is

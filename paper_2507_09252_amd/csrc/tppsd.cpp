@@ -16,6 +16,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <functional>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -907,6 +908,71 @@ int do_accept(tppsd_state *s, int gamma, const tppsd_draft_buf *dr, const tppsd_
   return hip_check("tppsd_accept");
 }
 
+// ---- allocation-free verification -------------------------------------------
+// tppsd_verify_noalloc runs the verify pass with its activation scratch (the
+// residual stream, LayerNorm / attention / FFN / decoder activations, the
+// decoder logits and the attention key-split partials) in a file-scope
+// device array instead of the state's workspace, so that the call needs no
+// memory of the caller's beyond the state, its inputs and its outputs. Each
+// GPU that runs it holds the array until the process ends; every call on a
+// GPU shares that GPU's copy (overlapping calls on one GPU race).
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)64 << 20;
+static __device__ __align__(256) char scratch[NOALLOC_SCRATCH_BYTES];
+
+constexpr int NOALLOC_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+char *g_scratch[NOALLOC_MAX_DEVICES] = {};
+
+// the device address of the current device's copy of `scratch`, resolved once
+// per device (in host code the array's name only stands in for it)
+int scratch_base(char **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return hip_check("tppsd_verify_noalloc: current device");
+  if (dev < 0 || dev >= NOALLOC_MAX_DEVICES) return fail(TPPSD_E_HIP, "device %d outside the scratch table", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(TPPSD_E_HIP, "tppsd_verify_noalloc: scratch address: %s", hipGetErrorString(e));
+    g_scratch[dev] = (char *)p;
+  }
+  *out = g_scratch[dev];
+  return TPPSD_OK;
+}
+
+// offsets of the verify pass's activation scratch for B sequences of P rows
+// (the same per-buffer sizes as the state's workspace, for B * P rows)
+struct ScratchLayout {
+  size_t x, a, q, o, hid, e, u, logits, attn_part, total;
+};
+ScratchLayout scratch_layout(const tppsd_model *T, const tppsd_model *D, int B, int P, int kvc) {
+  ScratchLayout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    off = align_up(off);
+    const size_t r = off;
+    off += bytes;
+    return r;
+  };
+  const size_t Tm = (size_t)B * P;
+  const size_t dmax = std::max(T->d(), D ? D->d() : 0);
+  const size_t fmax = std::max(T->cfg.d_ffn, D ? D->cfg.d_ffn : 0);
+  const size_t mmax = std::max(T->cfg.n_mix, D ? D->cfg.n_mix : 0);
+  const size_t kmax = std::max(T->cfg.n_types, D ? D->cfg.n_types : 0);
+  L.x = take(Tm * dmax * 4);
+  L.a = take(Tm * dmax * 4);
+  L.q = take(Tm * dmax * 4);
+  L.o = take(Tm * dmax * 4);
+  L.hid = take(Tm * fmax * 4);
+  L.e = take(Tm * 4 * dmax * 4);
+  L.u = take(Tm * 2 * dmax * 4);
+  L.logits = take(Tm * head_ldl((int)mmax, (int)kmax) * 4);
+  L.attn_part = take(attn_part_floats(B, T->H(), T->dh(), (P + 15) / 16, kvc) * 4);
+  L.total = align_up(off);
+  return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1297,6 +1363,43 @@ int tppsd_verify(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tpp
   if (int rc = check_draft_buf(in)) return rc;
   if (int rc = check_verify_buf(out)) return rc;
   return do_verify(s, gamma, in, out, st);
+}
+
+int tppsd_verify_noalloc(tppsd_state *s, int gamma, const tppsd_draft_buf *in, const tppsd_verify_buf *out,
+                         hipStream_t st) {
+  if (int rc = check_round(s, gamma)) return rc;
+  if (int rc = check_draft_buf(in)) return rc;
+  if (int rc = check_verify_buf(out)) return rc;
+  const ScratchLayout L = scratch_layout(s->T, s->D, s->B, gamma + 1, s->kv_cap);
+  if (L.total > NOALLOC_SCRATCH_BYTES)
+    return fail(TPPSD_E_WORKSPACE, "tppsd_verify_noalloc needs %zu bytes of scratch for B = %d, gamma = %d; its "
+                "static array holds %zu", L.total, s->B, gamma, NOALLOC_SCRATCH_BYTES);
+  char *base = nullptr;
+  if (int rc = scratch_base(&base)) return rc;
+  // the pass's kernels take the scratch pointers from the state at launch:
+  // point them at the static array for this call, then back at the workspace
+  float *const x = s->x, *const logits = s->logits, *const part = s->attn_part;
+  void *const a = s->a, *const q = s->q, *const o = s->o, *const hid = s->hid, *const e = s->e, *const u = s->u;
+  s->x = (float *)(base + L.x);
+  s->a = base + L.a;
+  s->q = base + L.q;
+  s->o = base + L.o;
+  s->hid = base + L.hid;
+  s->e = base + L.e;
+  s->u = base + L.u;
+  s->logits = (float *)(base + L.logits);
+  s->attn_part = (float *)(base + L.attn_part);
+  const int rc = do_verify(s, gamma, in, out, st);
+  s->x = x;
+  s->a = a;
+  s->q = q;
+  s->o = o;
+  s->hid = hid;
+  s->e = e;
+  s->u = u;
+  s->logits = logits;
+  s->attn_part = part;
+  return rc;
 }
 
 int tppsd_accept(tppsd_state *s, int gamma, const tppsd_draft_buf *dr, const tppsd_verify_buf *vf,

@@ -32,7 +32,7 @@ EXPORTS = [
     "tppsd_verify", "tppsd_accept", "tppsd_sample_ar", "tppsd_sample_sd", "tppsd_read_events",
     "tppsd_state_status", "tppsd_timing_enable", "tppsd_timing_read", "tppsd_last_error",
     "tppsd_poisson_fit", "tppsd_draft_poisson", "tppsd_sample_sd_poisson", "tppsd_prefill_window",
-    "tppsd_read_loglik",
+    "tppsd_read_loglik", "tppsd_verify_noalloc",
 ]
 
 
@@ -98,6 +98,7 @@ def lib():
         "tppsd_prefill": (c_int, [c_void_p, c_void_p, c_void_p, c_int, c_int, c_void_p]),
         "tppsd_draft": (c_int, [c_void_p, c_int, P(DraftBufC), c_void_p]),
         "tppsd_verify": (c_int, [c_void_p, c_int, P(DraftBufC), P(VerifyBufC), c_void_p]),
+        "tppsd_verify_noalloc": (c_int, [c_void_p, c_int, P(DraftBufC), P(VerifyBufC), c_void_p]),
         "tppsd_accept": (c_int, [c_void_p, c_int, P(DraftBufC), P(VerifyBufC), c_void_p, P(AcceptBufC), c_void_p]),
         "tppsd_sample_ar": (c_int, [c_void_p, c_int, c_void_p, c_void_p, c_void_p]),
         "tppsd_sample_sd": (c_int, [c_void_p, c_int, c_int, P(c_int), c_void_p]),
@@ -304,6 +305,10 @@ class State:
 
     def tppsd_verify(self, gamma: int, drafts: DraftBuffers, out: VerifyBuffers):
         _check(lib().tppsd_verify(self.handle, gamma, ctypes.byref(drafts.c()), ctypes.byref(out.c()), _stream()))
+
+    def tppsd_verify_noalloc(self, gamma: int, drafts: DraftBuffers, out: VerifyBuffers):
+        _check(lib().tppsd_verify_noalloc(self.handle, gamma, ctypes.byref(drafts.c()), ctypes.byref(out.c()),
+                                          _stream()))
 
     def tppsd_accept(self, gamma: int, drafts: DraftBuffers, verify: VerifyBuffers, out: AcceptBuffers,
                      uniforms: Optional[torch.Tensor] = None):
