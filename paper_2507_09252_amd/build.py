@@ -53,7 +53,7 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
     from concurrent.futures import ThreadPoolExecutor
-    srcs = ("tppsd_kernels.hip", "tppsd_attention.hip", "tppsd_poisson.hip", "tppsd.cpp")
+    srcs = ("tppsd_kernels.hip", "tppsd_attention.hip", "tppsd_poisson.hip", "tppsd_draft_rows.hip", "tppsd.cpp")
     objs = [os.path.join(BUILD, src + ".o") for src in srcs]
     cmds = [[hipcc] + HIPCC_FLAGS + inc + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
             for src, obj in zip(srcs, objs)]

@@ -213,6 +213,7 @@ struct tppsd_state {
   char *packT = nullptr;               // target weights in fragment order (nullptr: no fused layer kernel)
   size_t pack_layer = 0;
   char *packD = nullptr;               // draft weights in fragment order
+  char *packDdec = nullptr;            // draft decoder in fragment order (row drafting)
   size_t pack_layerD = 0;
   bool packs_built = false;
   bool wb_built = false;
@@ -246,6 +247,7 @@ struct tppsd_state {
   bool fused_draft = true;   // one-launch drafting when the draft model fits it
   bool wave_draft = false;   // ... with one wave per sequence (small draft models)
   bool fused_w_lds = false;  // ... with its weight matrices staged in LDS
+  bool row_draft = false;    // split attention + one row workgroup per sequence, per step and layer
   hipGraphExec_t sd_exec[2] = {nullptr, nullptr};
   long long sd_key = -1;
   const float *sd_params = nullptr, *phase_params = nullptr;   // Poisson draft parameters the graphs embed
@@ -267,6 +269,7 @@ struct WsLayout {
   size_t logits, hwT, hbT, hwD, hbD;
   size_t packT = 0, pack_layer = 0;   // target weights in MFMA fragment order (fused layer kernel), per layer
   size_t packD = 0, pack_layerD = 0;  // the same for the draft model
+  size_t packDdec = 0;                // the draft decoder's [E; V_k1] and heads in fragment order (row drafting)
   size_t wbT = 0, wbD = 0, wb_nT = 0, wb_nD = 0;   // matrices in the k_block order (0 bytes: not served)
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt, d_rate;
   size_t v_logg, v_logf, v_mix, v_lt;
@@ -347,12 +350,19 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
     w.pack_layerD = (4 * d * d + 2 * d * F) * 2;
     w.packD = take(w.pack_layerD * D->cfg.n_layers);
   }
+  if (D && !D->attnhp() &&
+      row_draft_ok(D->bf16(), D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types, (int)kvc))
+    w.packDdec = take(rd_pack_dec_elems(D->d()) * 2);
   w.ar_mix = take(Bz * 3 * mmax * 4);
   w.ar_lt = take(Bz * kmax * 4);
   {
     const int qtm = (Pmax + 15) / 16;
     size_t pf = attn_part_floats(B, T->H(), T->dh(), qtm, (int)kvc);
     if (D) pf = std::max(pf, attn_part_floats(B, D->H(), D->dh(), qtm, (int)kvc));
+    if (D && !D->attnhp() &&
+        row_draft_ok(D->bf16(), D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types,
+                     (int)kvc))
+      pf = std::max(pf, rd_part_floats(B, D->H(), D->dh(), (int)kvc));
     w.attn_part = take(pf * 4);
   }
   w.gen0 = take(Bz * 4);
@@ -648,7 +658,7 @@ int check_accept_buf(const tppsd_accept_buf *b) {
   return TPPSD_OK;
 }
 
-int do_draft_fused(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
+DraftArgs draft_args(tppsd_state *s, int gamma, const tppsd_draft_buf *out) {
   const tppsd_model *D = s->D;
   DraftArgs a{};
   a.B = s->B;
@@ -696,6 +706,12 @@ int do_draft_fused(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStr
   a.d_k = out->k;
   a.MG = s->max_gamma;
   a.w_lds = s->fused_w_lds ? 1 : 0;
+  return a;
+}
+
+int do_draft_fused(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
+  const tppsd_model *D = s->D;
+  const DraftArgs a = draft_args(s, gamma, out);
   // kernel timing: the pair after the verify pass's attention and GEMM pairs
   const int dp = 5 * s->T->cfg.n_layers + 1;
   const bool timed = s->cur_ev != nullptr;
@@ -708,9 +724,28 @@ int do_draft_fused(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStr
   return hip_check("tppsd_draft");
 }
 
+int do_draft_rows(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
+  RowDraftArgs a{};
+  a.d = draft_args(s, gamma, out);
+  a.x = s->x;
+  a.q = (float *)s->q;
+  a.part = s->attn_part;
+  a.pk = (const bf16_t *)s->packD;
+  a.pk_e = (const bf16_t *)s->packDdec;
+  a.pk_head = (const bf16_t *)(s->packDdec + (size_t)4 * s->D->d() * s->D->d() * 2);
+  a.S = rd_splits(s->kv_cap);
+  // kernel timing: one pair from the first launch's start to the last's end
+  const int dp = 5 * s->T->cfg.n_layers + 1;
+  const bool timed = s->cur_ev != nullptr;
+  if (timed) s->ev_used[dp] = 1;
+  launch_draft_rows(a, st, timed ? s->cur_ev[2 * dp] : nullptr, timed ? s->cur_ev[2 * dp + 1] : nullptr);
+  return hip_check("tppsd_draft");
+}
+
 int do_draft(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStream_t st) {
   const tppsd_model *D = s->D;
   if (s->wave_draft || s->fused_draft) return do_draft_fused(s, gamma, out, st);
+  if (s->row_draft) return do_draft_rows(s, gamma, out, st);
   for (int l = 1; l <= gamma; ++l) {
     TokSrc src{};
     src.ev_t = s->ev_t;
@@ -1117,6 +1152,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->packT = w.pack_layer ? ws + w.packT : nullptr;
   s->pack_layer = w.pack_layer;
   s->packD = w.pack_layerD ? ws + w.packD : nullptr;
+  s->packDdec = w.packDdec ? ws + w.packDdec : nullptr;
   s->pack_layerD = w.pack_layerD;
   s->cT.wb = w.wb_nT ? ws + w.wbT : nullptr;
   s->cD.wb = w.wb_nD ? ws + w.wbD : nullptr;
@@ -1199,6 +1235,12 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
       s->wave_draft = false;
       (void)hipGetLastError();
     }
+    // otherwise, for batches too small to fill the chip with per-step GEMM
+    // tiles, the per-step split attention and one row workgroup per sequence
+    s->row_draft = D && !D->attnhp() && !s->fused_draft && !s->wave_draft && !(nf && nf[0] == '1') &&
+                   B <= 256 && s->packD && s->packDdec &&
+                   row_draft_ok(D->bf16(), D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn, D->cfg.n_mix,
+                                D->cfg.n_types, s->kv_cap);
   }
   if (hipHostMalloc((void **)&s->host_ndone, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&s->poll_ev[0], hipEventDisableTiming) != hipSuccess ||
@@ -1292,6 +1334,11 @@ int tppsd_prefill_window(tppsd_state *s, const float *d_t, const int32_t *d_k, i
         launch_pack_frags(w.ffn1_w, F, d, p + (size_t)d * d * 2, st);
         launch_pack_frags(w.ffn2_w, d, F, p + (size_t)(d * d + F * d) * 2, st);
         launch_pack_frags(w.qkv_w, 3 * d, d, p + (size_t)(d * d + 2 * F * d) * 2, st);
+      }
+      if (which && s->packDdec) {
+        launch_pack_frags(m->Ek1_w, 4 * d, d, s->packDdec, st);
+        launch_pack_rd_head(m->mix_w, m->k2_w, m->cfg.n_mix, m->cfg.n_types, d,
+                            s->packDdec + (size_t)4 * d * d * 2, st);
       }
     }
     s->packs_built = true;

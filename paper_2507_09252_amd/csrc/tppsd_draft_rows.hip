@@ -1,0 +1,573 @@
+// Drafting for small batches over long contexts (§4.3 "Drafting", the inner
+// loop of Algorithm 1), bf16 draft models.
+//
+// Each draft step runs two launches per layer:
+//  - k_rd_attn: the step's queries (two in the first step, which re-encodes
+//    the last two committed events, one after) against the draft KV cache,
+//    split over (key range, head, sequence) workgroups so that the cache
+//    streams through the whole chip; each split leaves its running maximum,
+//    sum and unnormalised output;
+//  - k_rd_rows: one workgroup per sequence merges the splits and runs every
+//    row-local step up to the next attention -- output projection and
+//    residual, the feed-forward block, then the next layer's LayerNorm and
+//    q, k, v (keys and values appended to the cache); after the last layer
+//    the decoder, the draft record, the draw, and the drawn event's
+//    embedding and layer-0 q, k, v for the next step.
+// The matrix-vector products of a sequence's one or two rows run on MFMA
+// 16-row tiles (rows past the token count are zero operands) with every weight
+// fragment of a product in flight at once, and the next product's fragments
+// loaded before the current one is multiplied out, so that a product costs
+// about one memory latency. Rounding points are those of the layered kernels:
+// LayerNorm outputs, q/k/v, the attention output, ReLU output and the
+// decoder's e and tanh activations are bf16; the residual stream, softmax and
+// decoder math are fp32.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "tppsd_device.h"
+#include "tppsd_philox.h"
+#include "../../include/tppsd.h"
+
+namespace tppsd {
+
+namespace {
+
+constexpr int RD_WAVES = RD_ROW_THREADS / 64;
+
+// ---------------------------------------------------------------------------
+// split attention: workgroup (s, h, b) takes keys [s RD_KEYS, (s + 1) RD_KEYS)
+// of head h of sequence b
+// ---------------------------------------------------------------------------
+template <int DH>
+__global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
+  constexpr int NG = 256 / DH;              // lane groups over the value blocks
+  constexpr int BPL = RD_KEYS / 8 / NG;     // value blocks per lane
+  __shared__ __attribute__((aligned(16))) float es[2][RD_KEYS];
+  __shared__ float red[2][NG][DH];
+  __shared__ float wred[2][4][2];
+  const DraftArgs &d = a.d;
+  const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  constexpr int SEG = DH * 2 / 16;          // 16-byte segments of a key row
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, seg = tid % SEG;
+  // the sequence's header words and the lane's query segments, loaded together
+  const int done = d.done[b], lenD = d.lenD[b];
+  const int P = a.step == 1 ? 2 : 1;
+  float q[2][8];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const float *qp = a.q + ((size_t)b * 2 + p) * d.d + h * DH + 8 * seg;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) q[p][j] = qp[j];
+  }
+  if (done) return;
+  const int pos0 = lenD + (a.step == 1 ? 0 : a.step);
+  const int n_keys = min(pos0 + P, d.cap);
+  const int k0 = s * RD_KEYS;
+  if (k0 >= n_keys) return;   // whole workgroup; no barrier passed yet
+  const size_t row0 = ((size_t)b * d.H + h) * d.cap;
+  const bf16_t *kc = (const bf16_t *)(d.kc + d.layer_bytes * a.layer);
+  const bf16_t *vc = (const bf16_t *)(d.vc + d.layer_bytes * a.layer);
+  // every load of the split in flight at once, each wave instruction reading
+  // 1 KB of contiguous memory (non-temporal: the cache streams through once per
+  // step and should not push the draft model's weights out of L2). Keys: lane
+  // t of load i holds 16-byte segment t % SEG of key i KPI + t / SEG. Values:
+  // lane (grp, col) holds the 8-position blocks of column col.
+  constexpr int KPI = 256 / SEG;            // keys per load
+  constexpr int NKL = RD_KEYS / KPI;        // key loads per lane
+  u32x4_t kr[NKL];
+#pragma unroll
+  for (int i = 0; i < NKL; ++i) {
+    const int pos = k0 + i * KPI + tid / SEG;
+    kr[i] = pos < n_keys ? __builtin_nontemporal_load((const u32x4_t *)(kc + (row0 + pos) * DH) + seg)
+                         : u32x4_t{0u, 0u, 0u, 0u};
+  }
+  const int col = tid % DH, grp = tid / DH;
+  u32x4_t vr[BPL];
+#pragma unroll
+  for (int i = 0; i < BPL; ++i) {
+    const int pb = k0 + 8 * (grp + i * NG);   // first position of the block
+    vr[i] = pb < n_keys ? __builtin_nontemporal_load((const u32x4_t *)(vc + v_at<bf16_t>(row0, pb, col, DH)))
+                        : u32x4_t{0u, 0u, 0u, 0u};
+  }
+  // scores, per query: q k / sqrt(d_head) (the SEG lanes of a key sum their
+  // segments); keys past the query masked
+  static_assert(SEG == 4 || SEG == 2, "key segments per quad");
+  const float scale = 1.f / sqrtf((float)DH);
+  float sc[2][NKL];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (p >= P) break;
+    const int last = pos0 + p;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NKL; ++i) {
+      const uint32_t w[4] = {kr[i][0], kr[i][1], kr[i][2], kr[i][3]};
+      float dot = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        dot += q[p][2 * e] * __uint_as_float(w[e] << 16);
+        dot += q[p][2 * e + 1] * __uint_as_float(w[e] & 0xFFFF0000u);
+      }
+      dot += dpp_mov<0xB1>(dot);                 // lane ^ 1
+      if (SEG == 4) dot += dpp_mov<0x4E>(dot);   // lane ^ 2
+      const int pos = k0 + i * KPI + tid / SEG;
+      sc[p][i] = (pos < n_keys && pos <= last) ? dot * scale : -INFINITY;
+      mx = fmaxf(mx, sc[p][i]);
+    }
+    mx = wave_max(mx);
+    if (lane == 0) wred[p][wave][0] = mx;
+  }
+  __syncthreads();
+  float mq[2] = {-INFINITY, -INFINITY};
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (p >= P) break;
+    mq[p] = fmaxf(fmaxf(wred[p][0][0], wred[p][1][0]), fmaxf(wred[p][2][0], wred[p][3][0]));
+    float ls = 0.f;
+#pragma unroll
+    for (int i = 0; i < NKL; ++i) {
+      const float e = sc[p][i] == -INFINITY ? 0.f : expf(sc[p][i] - mq[p]);
+      if (seg == 0) {
+        es[p][i * KPI + tid / SEG] = e;
+        ls += e;
+      }
+    }
+    ls = wave_sum(ls);
+    if (lane == 0) wred[p][wave][1] = ls;
+  }
+  __syncthreads();
+  // output sums: lane (grp, col) over its value blocks; slots that are not
+  // keys of the query carry weight 0 and possibly unwritten values, so they
+  // are skipped rather than multiplied
+  const int clean_end = min(n_keys, pos0 + 1);   // positions below are keys of every query
+  float o[2] = {0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < BPL; ++i) {
+    const int lb = 8 * (grp + i * NG), pb = k0 + lb;
+    if (pb >= n_keys) continue;
+    const uint32_t w[4] = {vr[i][0], vr[i][1], vr[i][2], vr[i][3]};
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] = __uint_as_float(w[e] << 16);
+      v[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+    const bool clean = pb + 8 <= clean_end;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      if (p >= P) break;
+      const float4 e0 = *(const float4 *)&es[p][lb], e1 = *(const float4 *)&es[p][lb + 4];
+      const float ee[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+      float acc = 0.f;
+      if (clean) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc += ee[t] * v[t];
+      } else {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc += ee[t] != 0.f ? ee[t] * v[t] : 0.f;
+      }
+      o[p] += acc;
+    }
+  }
+  red[0][grp][col] = o[0];
+  if (P > 1) red[1][grp][col] = o[1];
+  __syncthreads();
+  if (tid < P * DH) {
+    const int p = tid / DH, c = tid - p * DH;
+    float acc = 0.f;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) acc += red[p][g][c];
+    float *dst = a.part + ((((size_t)b * d.H + h) * a.S + s) * 2 + p) * (DH + 2);
+    dst[2 + c] = acc;
+    if (c == 0) {
+      dst[0] = p ? mq[1] : mq[0];
+      dst[1] = (wred[p][0][1] + wred[p][1][1]) + (wred[p][2][1] + wred[p][3][1]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// row kernel
+// ---------------------------------------------------------------------------
+
+// a layer's matrices in fragment order: Wo, W1, W2, Wqkv (elements)
+template <int D, int F> constexpr size_t rd_layer_elems() { return (size_t)4 * D * D + 2 * (size_t)D * F; }
+template <int D, int F> constexpr size_t rd_off_qkv() { return (size_t)D * D + 2 * (size_t)D * F; }
+
+// the decoder heads' rows -- mixture rows (w, mu, log sigma; 3 M) then type
+// rows (K), zero up to 128 -- in fragment order (K = D)
+__global__ void k_pack_rd_head(const bf16_t *__restrict__ mix_w, const bf16_t *__restrict__ k2_w, int M, int K,
+                               int D, bf16_t *__restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;   // one 16-byte vector per thread
+  const int KS = D / 32, total = 8 * KS * 64;
+  if (i >= total) return;
+  const int l = i & 63, f = i >> 6, nt = f / KS, ks = f - nt * KS;
+  const int n = 16 * nt + (l & 15), k = 32 * ks + 8 * (l >> 4);
+  uint4 v = make_uint4(0u, 0u, 0u, 0u);
+  if (n < 3 * M) v = *(const uint4 *)(mix_w + (size_t)n * D + k);
+  else if (n < 3 * M + K) v = *(const uint4 *)(k2_w + (size_t)(n - 3 * M) * D + k);
+  *(uint4 *)(out + (size_t)i * 8) = v;
+}
+
+// One wave's weight fragments of Y = X W^T for W [N][KD] bf16: its 16-column
+// tiles wave, wave + RD_WAVES, ... and every 32-wide k step of each (lane l:
+// column l % 16 of the tile, k = 8 (l / 16) .. + 7 of the step).
+template <int N, int KD> struct RdFrags {
+  static constexpr int KS = KD / 32, TILES = (N + 15) / 16, TPW = (TILES + RD_WAVES - 1) / RD_WAVES;
+  bf16x8_t f[TPW][KS];
+  // W in fragment order (fragment (tile, ks) is 64 lanes x 8 elements at
+  // (tile KS + ks) 512): one contiguous kilobyte per wave instruction
+  __device__ __forceinline__ void load_packed(const bf16_t *Wp) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      const int tile = wave + t * RD_WAVES;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        f[t][ks] = tile < TILES ? *(const bf16x8_t *)(Wp + ((size_t)(tile * KS + ks) * 64 + lane) * 8)
+                                : __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+    }
+  }
+  // rows 0 .. NR - 1 of X (bf16 in LDS, row stride ldx elements; rows
+  // r < nx read, the others zero); epi(r, n, acc) for r < NR on lanes 0..15
+  template <int NR, typename EPI>
+  __device__ __forceinline__ void mul(const bf16_t *X, int ldx, int nx, EPI epi) const {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15;
+    bf16x8_t xa[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      xa[ks] = r < nx ? *(const bf16x8_t *)(X + r * ldx + ks * 32 + 8 * (lane >> 4))
+                      : __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      const int tile = wave + t * RD_WAVES;
+      if (tile >= TILES) continue;   // wave-uniform
+      f32x4_t c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ks += 2) {
+        c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[ks], f[t][ks], c0, 0, 0, 0);
+        if (ks + 1 < KS) c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[ks + 1], f[t][ks + 1], c1, 0, 0, 0);
+      }
+      const int n = tile * 16 + r;
+      if (lane < 16 && n < N) {
+#pragma unroll
+        for (int v = 0; v < NR; ++v) epi(v, n, c0[v] + c1[v]);
+      }
+    }
+  }
+};
+
+__device__ __forceinline__ void rd_sync() { __syncthreads(); }
+
+// LayerNorm (biased variance, eps 1e-5) of rows 0 .. np - 1 of xs [2][D]
+// into bf16 rows of y (stride D); wave p takes row p
+template <int D>
+__device__ __forceinline__ void rd_layernorm(const float *xs, bf16_t *y, const float *g, const float *bt, int np) {
+  constexpr int PER = D / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (wave >= np) return;
+  float v[PER], sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    v[i] = xs[wave * D + lane + 64 * i];
+    sum += v[i];
+  }
+  const float mean = wave_sum(sum) / (float)D;
+  float sq = 0.f;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    v[i] -= mean;
+    sq += v[i] * v[i];
+  }
+  const float rstd = 1.f / sqrtf(wave_sum(sq) / (float)D + 1e-5f);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int j = lane + 64 * i;
+    y[wave * D + j] = f2bf(v[i] * rstd * g[j] + bt[j]);
+  }
+}
+
+template <int D, int F, int DH>
+struct RdShared {
+  float xs[2][D];                                      // residual stream rows
+  __attribute__((aligned(16))) bf16_t ab[2][D];       // LayerNorm / attention output rows
+  __attribute__((aligned(16))) bf16_t hb[2][F];       // FFN hidden rows
+  __attribute__((aligned(16))) bf16_t eb[4][D];       // decoder e slices (w, mu, sigma) and tanh
+  float hv[128];                                       // decoder outputs
+  float part[RD_MAX_PART];                             // the sequence's split partials
+  float tok_t;
+  int tok_k;
+};
+
+// q, k, v of rows 0 .. np - 1 (LayerNorm output in sh.ab) for the layer whose
+// weights are in fr: queries to a.q, keys and values into the layer's cache at
+// positions pos0 + row
+template <int D, int DH, typename FR>
+__device__ __forceinline__ void rd_qkv(const RowDraftArgs &a, const FR &fr, const bf16_t *xin, int np, int ly,
+                                       int b, int pos0, const float *qkv_b) {
+  const DraftArgs &d = a.d;
+  bf16_t *kc = (bf16_t *)(d.kc + d.layer_bytes * ly);
+  bf16_t *vc = (bf16_t *)(d.vc + d.layer_bytes * ly);
+  auto epi = [&](int p, int n, float acc) {
+    if (p >= np) return;
+    const float v = bf2f(f2bf(acc + qkv_b[n]));
+    const int which = n / D, c = n - which * D;
+    if (which == 0) {
+      a.q[((size_t)b * 2 + p) * D + c] = v;
+      return;
+    }
+    const int hh = c / DH, j = c - hh * DH, pos = pos0 + p;
+    const size_t row0 = ((size_t)b * d.H + hh) * d.cap;
+    if (pos < d.cap)
+      st(which == 1 ? kc : vc, which == 1 ? (row0 + pos) * DH + j : v_at<bf16_t>(row0, pos, j, DH), v);
+    else
+      atomicOr(d.status, TPPSD_STATUS_CAPACITY);
+  };
+  fr.template mul<2>(xin, D, np, epi);
+}
+
+// the THP embedding (sin / cos time encoding + type row) of event (t, k) into row p
+template <int D>
+__device__ __forceinline__ void rd_embed(const DraftArgs &d, float *xrow, float t, int k) {
+  const int tid = threadIdx.x;
+  if (tid < D) {
+    const float arg = t * d.freq[tid];
+    const int kk = min(max(k, 0), d.K - 1);
+    xrow[tid] = ((tid & 1) ? cosf(arg) : sinf(arg)) + bf2f(((const bf16_t *)d.type_emb)[(size_t)kk * D + tid]);
+  }
+}
+
+// Launch modes: step 0 embeds the last two committed events and computes
+// their layer-0 q, k, v; step l >= 1, layer ly finishes layer ly of the step's
+// rows after its attention.
+template <int D, int F, int DH>
+__global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
+  static_assert(D % 64 == 0 && F % 32 == 0 && D % 32 == 0, "row kernel widths");
+  __shared__ RdShared<D, F, DH> sh;
+  const DraftArgs &d = a.d;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int done = d.done[b], base = d.lenD[b], n = d.n[b];   // loaded together
+  if (done) return;
+  const int L = d.L, M = d.M, K = d.K;
+  float *xg = a.x + (size_t)b * 2 * D;
+  if (a.step == 0) {
+    RdFrags<3 * D, D> fq;
+    fq.load_packed(a.pk + rd_off_qkv<D, F>());
+    for (int p = 0; p < 2; ++p) {
+      const size_t i = (size_t)b * d.ev_stride + n - 2 + p;
+      rd_embed<D>(d, sh.xs[p], d.ev_t[i], d.ev_k[i]);
+    }
+    rd_sync();
+    rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[0].ln1_g, d.layer[0].ln1_b, 2);
+    for (int i = tid; i < 2 * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
+    rd_sync();
+    rd_qkv<D, DH>(a, fq, &sh.ab[0][0], 2, 0, b, base, d.layer[0].qkv_b);
+    return;
+  }
+  const int l = a.step, ly = a.layer;
+  const int P = l == 1 ? 2 : 1;
+  const int pos0 = base + (l == 1 ? 0 : l);
+  const FusedLayerW &w = d.layer[ly];
+  const bool last = ly == L - 1;
+  // this layer's output projection and both FFN products in flight, with the
+  // residual rows and every split partial of the sequence (all splits of the
+  // slab are read; those past the step's keys are ignored below)
+  RdFrags<D, D> fo;
+  RdFrags<F, D> f1;
+  RdFrags<D, F> f2;
+  const bf16_t *wl = a.pk + (size_t)ly * rd_layer_elems<D, F>();
+  fo.load_packed(wl);
+  f1.load_packed(wl + D * D);
+  f2.load_packed(wl + D * D + F * D);
+  {
+    const int cnt = d.H * a.S * 2 * (DH + 2);
+    const float *src = a.part + (size_t)b * cnt;
+    float pv[RD_MAX_PART / RD_ROW_THREADS];
+#pragma unroll
+    for (int i = 0; i < RD_MAX_PART / RD_ROW_THREADS; ++i) {
+      const int k = tid + i * RD_ROW_THREADS;
+      pv[i] = k < cnt ? src[k] : 0.f;
+    }
+    const float xv = tid < P * D ? xg[tid] : 0.f;
+#pragma unroll
+    for (int i = 0; i < RD_MAX_PART / RD_ROW_THREADS; ++i) sh.part[tid + i * RD_ROW_THREADS] = pv[i];
+    if (tid < P * D) (&sh.xs[0][0])[tid] = xv;
+  }
+  rd_sync();
+  // merge the attention splits of each (row, head): output = sum_s e^{m_s - m} o_s / sum_s e^{m_s - m} l_s
+  {
+    const int n_keys = min(pos0 + P, d.cap);
+    const int S_b = (n_keys + RD_KEYS - 1) / RD_KEYS;
+    for (int i = tid; i < P * D; i += RD_ROW_THREADS) {
+      const int p = i / D, hc = i - p * D, h = hc / DH, c = hc - h * DH;
+      const float *pp = sh.part + h * a.S * 2 * (DH + 2) + p * (DH + 2);
+      float mx = -INFINITY;
+      for (int s = 0; s < S_b; ++s) mx = fmaxf(mx, pp[s * 2 * (DH + 2)]);
+      float ls = 0.f, os = 0.f;
+      for (int s = 0; s < S_b; ++s) {
+        const float *ps = pp + s * 2 * (DH + 2);
+        const float ms = ps[0];
+        if (ms == -INFINITY) continue;
+        const float f = expf(ms - mx);
+        ls += f * ps[1];
+        os += f * ps[2 + c];
+      }
+      sh.ab[p][hc] = f2bf(ls > 0.f ? os / ls : 0.f);
+    }
+  }
+  rd_sync();
+  // output projection + residual
+  fo.template mul<2>(&sh.ab[0][0], D, P, [&](int p, int nn, float acc) {
+    if (p < P) sh.xs[p][nn] += acc + w.out_b[nn];
+  });
+  rd_sync();
+  rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], w.ln2_g, w.ln2_b, P);
+  rd_sync();
+  f1.template mul<2>(&sh.ab[0][0], D, P, [&](int p, int nn, float acc) {
+    if (p < P) sh.hb[p][nn] = f2bf(fmaxf(acc + w.ffn1_b[nn], 0.f));
+  });
+  if (!last) {
+    RdFrags<3 * D, D> fq;
+    fq.load_packed(a.pk + (size_t)(ly + 1) * rd_layer_elems<D, F>() + rd_off_qkv<D, F>());
+    rd_sync();
+    f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
+      if (p < P) sh.xs[p][nn] += acc + w.ffn2_b[nn];
+    });
+    rd_sync();
+    rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[ly + 1].ln1_g, d.layer[ly + 1].ln1_b, P);
+    for (int i = tid; i < P * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
+    rd_sync();
+    rd_qkv<D, DH>(a, fq, &sh.ab[0][0], P, ly + 1, b, pos0, d.layer[ly + 1].qkv_b);
+    return;
+  }
+  // ---- last layer: decoder on the last row, the draw, the next token
+  RdFrags<4 * D, D> fe;
+  fe.load_packed(a.pk_e);
+  rd_sync();
+  f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
+    if (p < P) sh.xs[p][nn] += acc + w.ffn2_b[nn];
+  });
+  rd_sync();
+  const int pl = P - 1;
+  rd_layernorm<D>(&sh.xs[pl][0], &sh.ab[0][0], d.lnf_g, d.lnf_b, 1);
+  // decoder heads as one product over the four e slices: column n < 3 M reads
+  // mixture row n (slice n / M), the others type-head row n - 3 M (tanh slice)
+  const int NH = 3 * M + K;
+  RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
+  fh.load_packed(a.pk_head);
+  rd_sync();
+  fe.template mul<1>(&sh.ab[0][0], D, 1, [&](int, int nn, float acc) {
+    const int slice = nn / D, c = nn - slice * D;
+    sh.eb[slice][c] = f2bf(slice < 3 ? acc : tanhf(acc + d.k1_b[c]));
+  });
+  const bool more = l < d.gamma;
+  RdFrags<3 * D, D> fq;
+  if (more) fq.load_packed(a.pk + rd_off_qkv<D, F>());
+  rd_sync();
+  fh.template mul<4>(&sh.eb[0][0], D, 4, [&](int r, int nn, float acc) {
+    if (nn < NH && r == (nn < 3 * M ? nn / M : 3)) sh.hv[nn] = acc + (nn < 3 * M ? d.mix_b[nn] : d.k2_b[nn - 3 * M]);
+  });
+  rd_sync();
+  if (wave == 0) {
+    // the log-softmaxes, the draft record and the draft event
+    const float lw = lane < M ? sh.hv[lane] : -INFINITY;
+    const float mu = lane < M ? sh.hv[M + lane] : 0.f, sg = lane < M ? sh.hv[2 * M + lane] : 0.f;
+    const float lk = lane < K ? sh.hv[3 * M + lane] : -INFINITY;
+    const float mw = wave_max(lw), mk = wave_max(lk);
+    const float logw = lw - mw - logf(wave_sum(lane < M ? expf(lw - mw) : 0.f));
+    const float logk = lk - mk - logf(wave_sum(lane < K ? expf(lk - mk) : 0.f));
+    const size_t di = (size_t)b * d.MG + (l - 1);
+    if (lane < M) {
+      d.d_mix[di * 3 * M + lane] = logw;
+      d.d_mix[di * 3 * M + M + lane] = mu;
+      d.d_mix[di * 3 * M + 2 * M + lane] = sg;
+    }
+    if (lane < K) d.d_logtype[di * K + lane] = logk;
+    const bool bad = (lane < M && !(isfinite(logw) && isfinite(mu) && isfinite(sg))) || (lane < K && !isfinite(logk));
+    float u[4];
+    philox_uniforms(d.seed, (uint64_t)b, (uint64_t)d.rnd[b], (uint64_t)l, TAG_DRAFT, u);
+    // categorical over the lanes' log-probabilities: first index whose
+    // running sum of exp exceeds u times the total
+    auto draw = [&](float lp, int cnt, float uu) {
+      float cs = lane < cnt ? expf(lp) : 0.f;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const float oo = __shfl_up(cs, off, 64);
+        if (lane >= off) cs += oo;
+      }
+      const float tot = __shfl(cs, cnt - 1, 64);
+      const unsigned long long hit = __ballot(lane < cnt && uu * tot < cs);
+      return hit ? (int)__builtin_ctzll(hit) : cnt - 1;
+    };
+    const int z = draw(logw, M, u[0]);
+    const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
+    const float tau = expf(__shfl(mu, z, 64) + expf(__shfl(sg, z, 64)) * eps);
+    const int kk = draw(logk, K, u[3]);
+    const float lt = logf(tau);
+    float cterm = -INFINITY;
+    if (lane < M) {
+      const float zz = lt - mu;
+      cterm = logw - sg - 0.918938533204672742f - lt - 0.5f * zz * zz * expf(-2.f * sg);
+    }
+    const float cm = wave_max(cterm);
+    const float lg = cm + logf(wave_sum(lane < M ? expf(cterm - cm) : 0.f));
+    const float lf = __shfl(logk, kk, 64);
+    const bool bad_any = __ballot(bad) != 0ull;
+    if (lane == 0) {
+      const float tprev = l == 1 ? d.ev_t[(size_t)b * d.ev_stride + n - 1] : d.d_t[di - 1];
+      const float tn = tprev + tau;
+      d.d_tau[di] = tau;
+      d.d_t[di] = tn;
+      d.d_k[di] = kk;
+      d.d_logg[di] = lg;
+      d.d_logf[di] = lf;
+      if (bad_any || !isfinite(tau)) atomicOr(d.status, TPPSD_STATUS_NONFINITE);
+      sh.tok_t = tn;
+      sh.tok_k = kk;
+    }
+  }
+  if (!more) return;   // workgroup-uniform
+  rd_sync();
+  // the drawn event is the next step's token, at position base + l + 1
+  rd_embed<D>(d, sh.xs[0], sh.tok_t, sh.tok_k);
+  rd_sync();
+  rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[0].ln1_g, d.layer[0].ln1_b, 1);
+  for (int i = tid; i < D; i += RD_ROW_THREADS) xg[i] = sh.xs[0][i];
+  rd_sync();
+  rd_qkv<D, DH>(a, fq, &sh.ab[0][0], 1, 0, b, base + l + 1, d.layer[0].qkv_b);
+}
+
+}  // namespace
+
+bool row_draft_ok(int bf16, int L, int d, int H, int F, int M, int K, int kv_cap) {
+  return bf16 && L >= 1 && L <= FD_MAX_LAYERS && d == 128 && H == 4 && F == 512 && M >= 1 && M <= 64 && K >= 1 &&
+         K <= 64 && 3 * M + K <= 128 && (size_t)H * rd_splits(kv_cap) * 2 * (32 + 2) <= (size_t)RD_MAX_PART;
+}
+
+void launch_pack_rd_head(const void *mix_w, const void *k2_w, int M, int K, int D, void *out, hipStream_t st) {
+  const int total = 8 * (D / 32) * 64;
+  hipLaunchKernelGGL(k_pack_rd_head, dim3((total + 255) / 256), dim3(256), 0, st, (const bf16_t *)mix_w,
+                     (const bf16_t *)k2_w, M, K, D, (bf16_t *)out);
+}
+
+void launch_draft_rows(RowDraftArgs a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+  const int B = a.d.B, H = a.d.H;
+  a.step = 0;
+  a.layer = 0;
+  hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, ev0, nullptr, 0, a);
+  for (int l = 1; l <= a.d.gamma; ++l) {
+    a.step = l;
+    for (int ly = 0; ly < a.d.L; ++ly) {
+      a.layer = ly;
+      hipLaunchKernelGGL(k_rd_attn<32>, dim3(a.S, H, B), dim3(256), 0, st, a);
+      const bool fin = l == a.d.gamma && ly == a.d.L - 1;
+      hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, nullptr,
+                            fin ? ev1 : nullptr, 0, a);
+    }
+  }
+}
+
+}  // namespace tppsd

@@ -156,6 +156,40 @@ size_t fused_draft_weight_elems(int L, int d, int F, int M, int K, int pad);
 // LDS of one workgroup on gfx950
 constexpr size_t LDS_PER_WG = 160 * 1024;
 
+// Drafting for small batches over long contexts (k_rd_attn + k_rd_rows, per
+// draft step and layer): the step's attention split over (key range, head,
+// sequence) workgroups of RD_KEYS keys, then one workgroup of RD_ROW_THREADS
+// per sequence for the row-local rest. bf16 draft models with d = 128, four
+// heads of 32, d_ffn = 512.
+constexpr int RD_KEYS = 512;
+constexpr int RD_ROW_THREADS = 512;
+// floats of one sequence's split partials the row kernel stages in LDS
+// (H S 2 (d_head + 2); 4 heads of 32 over 16384 positions)
+constexpr int RD_MAX_PART = 8704;
+struct RowDraftArgs {
+  DraftArgs d;              // model, cache, state and record pointers as for the one-launch draft
+  float *x;                 // [B][2][d] residual stream of the step's rows
+  float *q;                 // [B][2][d] queries of the step's rows (bf16-rounded values)
+  float *part;              // [B][H][S][2][d_head + 2] split partials: maximum, sum, output sums
+  const bf16_t *pk;         // per layer Wo, W1, W2, Wqkv in MFMA fragment order (launch_pack_frags)
+  const bf16_t *pk_e;       // [E; V_k1] in fragment order
+  const bf16_t *pk_head;    // decoder head rows, zero-padded to 128, in fragment order (launch_pack_rd_head)
+  int S;                    // key splits per (sequence, head): ceil(kv_cap / RD_KEYS)
+  int step;                 // draft step (1-based); 0: embed the last two committed events
+  int layer;
+};
+bool row_draft_ok(int bf16, int L, int d, int H, int F, int M, int K, int kv_cap);
+inline int rd_splits(int kv_cap) { return (kv_cap + RD_KEYS - 1) / RD_KEYS; }
+inline size_t rd_part_floats(int B, int H, int dh, int kv_cap) {
+  return (size_t)B * H * rd_splits(kv_cap) * 2 * (dh + 2);
+}
+// elements of the row kernel's packed decoder: [E; V_k1] (4 d x d) and the heads (128 x d)
+inline size_t rd_pack_dec_elems(int d) { return (size_t)4 * d * d + (size_t)128 * d; }
+void launch_pack_rd_head(const void *mix_w, const void *k2_w, int M, int K, int D, void *out, hipStream_t st);
+// all launches of one round's drafting; ev0 / ev1 (nullable) record the
+// start of the first and the end of the last
+void launch_draft_rows(RowDraftArgs a, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+
 // Fused row block of a THP forward pass (k_block): for a tile of 16 rows,
 // everything between two attention launches. first: embed the tokens (else
 // read the residual stream x); pre: output projection of o, residual, the

@@ -192,7 +192,9 @@ H8 = W.Workload("h8", 7, W.ModelCfg(2, 64, 4, 256, 16, 22, "bf16"), W.ModelCfg(1
                 batch=8, n_gen=64, gammas=(6,), n_hist=30, history="hawkes22", description="8-head bf16 draft")
 DRAFT_CASES = [small("c1", 8), small("c2", 8), small("c3", 16, n_hist=40, init="bias"), small("c5", 16, init="bias"),
                small("c4", 4, n_hist=40, init="bias"), small("c3", 8, n_hist=40, init="bias", gamma=20),
-               small("c2", 4, n_hist=40, init="bias", gamma=32), Case("h8-B6-bias", H8, 6, 30, "bias", True)]
+               small("c2", 4, n_hist=40, init="bias", gamma=32), Case("h8-B6-bias", H8, 6, 30, "bias", True),
+               # d = 128 drafts over a long history: three key splits of 512 per (sequence, head)
+               small("c4", 3, n_hist=1100, init="bias")]
 
 
 # both drafting paths: one workgroup per sequence for all gamma steps (where
