@@ -111,6 +111,31 @@ def draft_kernel_bytes(wl, B, gamma, ctx):
     return kv + model_weight_bytes(c) + rec
 
 
+def draft_attn_bytes(wl, B, gamma, ctx):
+    """Row drafting's split attention, one launch (one draft layer, one
+    step): the layer's cached keys and values up to the step's position (the
+    run-average context plus half a round's drafts), read once, the queries
+    read and the partials written (one row each)."""
+    c = wl.draft
+    keys = ctx + gamma / 2.0
+    return float(B * c.n_heads * keys * c.d_head * 2 * _elt(c) + 2 * B * 2 * c.d_model * 4)
+
+
+def draft_rows_bytes(wl, B, gamma):
+    """Row drafting's row launch, averaged over a round's 1 + L gamma
+    launches: the matrices the round's row launches read, each launch's once
+    (step 0: layer-0 q, k, v; per step and layer: output projection and FFN,
+    then the next layer's q, k, v or, after the last layer, the decoder and --
+    except in the last step -- layer-0 q, k, v), and the residual rows in and
+    out."""
+    c = wl.draft
+    d, F, L = c.d_model, c.d_ffn, c.n_layers
+    per_step = L * (d * d + 2 * d * F) + (L - 1) * 3 * d * d + _decoder_elems(c)
+    elems = 3 * d * d + gamma * per_step + (gamma - 1) * 3 * d * d
+    launches = 1 + L * gamma
+    return float(elems * _elt(c) / launches + 2 * B * 2 * d * 4)
+
+
 def run_context(wl):
     """Run-average context: contexts grow linearly over a job from n0 to n0 + n_gen."""
     return wl.n_hist + wl.n_gen / 2.0
@@ -392,9 +417,22 @@ def main():
             "bound": "hbm", "kernel": ATTN_KERNEL[wl.prec], "ms": tk["attn_ms"], "launches": tk["attn_launches"],
             "per_launch": per_attn, "unit": "GB/s", "peak": HBM_PEAK_GBS,
             "traffic": measured_traffic(wl.name)}
+    if tk["draft_attn_launches"]:
+        classes["draft_attention"] = {
+            "bound": "hbm", "kernel": "k_rd_attn<32> (row drafting: split attention, one launch per step and layer)",
+            "ms": tk["draft_attn_ms"], "launches": tk["draft_attn_launches"],
+            "per_launch": draft_attn_bytes(wl, B, gamma, ctx), "unit": "GB/s", "peak": HBM_PEAK_GBS,
+            "traffic": None}
+    if tk["draft_rows_launches"]:
+        classes["draft_rows"] = {
+            "bound": "hbm", "kernel": "k_rd_rows<128, 512, 32> (row drafting: one workgroup per sequence, "
+                                      "per step and layer)",
+            "ms": tk["draft_rows_ms"], "launches": tk["draft_rows_launches"],
+            "per_launch": draft_rows_bytes(wl, B, gamma), "unit": "GB/s", "peak": HBM_PEAK_GBS,
+            "traffic": None}
     if tk["draft_kernel_launches"]:
         classes["draft"] = {
-            "bound": "hbm", "kernel": "k_draft_fused (one launch per round: all gamma draft steps)",
+            "bound": "hbm", "kernel": "k_draft_fused / k_draft_wave (one launch per round: all gamma draft steps)",
             "ms": tk["draft_kernel_ms"], "launches": tk["draft_kernel_launches"],
             "per_launch": draft_kernel_bytes(wl, B, gamma, ctx), "unit": "GB/s", "peak": HBM_PEAK_GBS,
             "traffic": None}

@@ -320,8 +320,9 @@ int tppsd_state_status(tppsd_state *s, hipStream_t stream, uint32_t *bits, int32
 /* Measurement of tppsd_sample_sd; the sampled events are unchanged.
  * TPPSD_TIME_KERNELS: rounds are launched directly instead of replaying a
  *   captured HIP graph, and every launch of the target's verify attention, of
- *   its verify GEMMs (QKV, attention output, FFN in, FFN out, decoder E) and
- *   of the one-launch draft kernel is bracketed by HIP events stamped with the
+ *   its verify GEMMs (QKV, attention output, FFN in, FFN out, decoder E), of
+ *   the one-launch draft kernel and of each row-drafting launch (split
+ *   attention, row kernel) is bracketed by HIP events stamped with the
  *   kernel's own start and stop.
  * TPPSD_TIME_PHASES: each round replays three captured graphs (draft, verify,
  *   accept) with HIP events recorded between them on the caller's stream.
@@ -340,6 +341,10 @@ typedef struct tppsd_timing {
   int64_t rounds;          /* rounds timed */
   double draft_kernel_ms;  /* one-launch draft kernel: summed kernel time */
   int64_t draft_kernel_launches;
+  double draft_attn_ms;    /* row drafting: split attention launches, summed kernel time */
+  int64_t draft_attn_launches;
+  double draft_rows_ms;    /* row drafting: per-sequence row launches, summed kernel time */
+  int64_t draft_rows_launches;
 } tppsd_timing;
 int tppsd_timing_enable(tppsd_state *s, int modes);
 int tppsd_timing_read(tppsd_state *s, tppsd_timing *out);

@@ -541,14 +541,16 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     return e;
   };
   if (!m->attnhp()) launch_embed(s->x, T, d, P, src, m->type_emb, bf, c.freq, m->cfg.n_types, st);
+  // LayerNorm inside the consuming GEMM, or (wide rows, many rows) as its own launch
+  const bool ln_gemm = fuse_ln && !gemm_ln_split(bf, d, T);
   for (int l = 0; l < m->cfg.n_layers && !m->attnhp(); ++l) {
     const LayerW &w = m->layers[l];
     char *kc = c.k + c.layer_bytes * l, *vc = c.v + c.layer_bytes * l;
     const LnA ln1{s->x, w.ln1_g, w.ln1_b}, ln2{s->x, w.ln2_g, w.ln2_b};
     if (!(use_layer_fused && l > 0)) {   // (else the previous fused launch wrote this layer's q, k, v)
-      if (!fuse_ln) launch_layernorm(s->x, s->a, bf, w.ln1_g, w.ln1_b, T, d, st);
+      if (!ln_gemm) launch_layernorm(s->x, s->a, bf, w.ln1_g, w.ln1_b, T, d, st);
       const Epi e = qkv_epi(l);
-      launch_gemm(s->a, fuse_ln ? &ln1 : nullptr, w.qkv_w, bf, T, 3 * d, d, e, st, ev(L + 4 * l, 0),
+      launch_gemm(s->a, ln_gemm ? &ln1 : nullptr, w.qkv_w, bf, T, 3 * d, d, e, st, ev(L + 4 * l, 0),
                   ev(L + 4 * l, 1));
     }
     launch_attention(s->q, kc, vc, s->o, bf, start, start_off, s->done, B, P, H, dh, s->kv_cap, s->attn_part,
@@ -584,13 +586,13 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
     eo.out = s->x;
     eo.ldo = d;
     launch_gemm(s->o, nullptr, w.out_w, bf, T, d, d, eo, st, ev(L + 4 * l + 1, 0), ev(L + 4 * l + 1, 1));
-    if (!fuse_ln) launch_layernorm(s->x, s->a, bf, w.ln2_g, w.ln2_b, T, d, st);
+    if (!ln_gemm) launch_layernorm(s->x, s->a, bf, w.ln2_g, w.ln2_b, T, d, st);
     Epi e1{};
     e1.mode = EPI_RELU;
     e1.bias = w.ffn1_b;
     e1.out = s->hid;
     e1.ldo = F;
-    launch_gemm(s->a, fuse_ln ? &ln2 : nullptr, w.ffn1_w, bf, T, F, d, e1, st, ev(L + 4 * l + 2, 0), ev(L + 4 * l + 2, 1));
+    launch_gemm(s->a, ln_gemm ? &ln2 : nullptr, w.ffn1_w, bf, T, F, d, e1, st, ev(L + 4 * l + 2, 0), ev(L + 4 * l + 2, 1));
     Epi e2{};
     e2.mode = EPI_RESID;
     e2.bias = w.ffn2_b;
@@ -601,8 +603,8 @@ int forward(tppsd_state *s, const tppsd_model *m, const ModelCache &c, const int
   if (head) {
     // THP: the decoder reads LN_f(x); AttNHP: h itself (a, written by the update)
     const LnA lnf{s->x, m->lnf_g, m->lnf_b};
-    const bool ln_in_gemm = fuse_ln && !m->attnhp();
-    if (!fuse_ln && !m->attnhp()) launch_layernorm(s->x, s->a, bf, m->lnf_g, m->lnf_b, T, d, st);
+    const bool ln_in_gemm = fuse_ln && !m->attnhp() && !gemm_ln_split(bf, d, T);
+    if (!ln_in_gemm && !m->attnhp()) launch_layernorm(s->x, s->a, bf, m->lnf_g, m->lnf_b, T, d, st);
     Epi eh{};
     eh.mode = EPI_HEAD;
     eh.bias = m->k1_b;
@@ -734,11 +736,12 @@ int do_draft_rows(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStre
   a.pk_e = (const bf16_t *)s->packDdec;
   a.pk_head = (const bf16_t *)(s->packDdec + (size_t)4 * s->D->d() * s->D->d() * 2);
   a.S = rd_splits(s->kv_cap);
-  // kernel timing: one pair from the first launch's start to the last's end
-  const int dp = 5 * s->T->cfg.n_layers + 1;
-  const bool timed = s->cur_ev != nullptr;
-  if (timed) s->ev_used[dp] = 1;
-  launch_draft_rows(a, st, timed ? s->cur_ev[2 * dp] : nullptr, timed ? s->cur_ev[2 * dp + 1] : nullptr);
+  // kernel timing: a pair per launch, after the verify pass's and the one-launch draft's pairs
+  const int p0 = 5 * s->T->cfg.n_layers + 2, nl = rd_launches(a.d.L, gamma);
+  const bool timed = s->cur_ev != nullptr && (int)s->ev_used.size() >= p0 + nl;
+  if (timed)
+    for (int j = 0; j < nl; ++j) s->ev_used[p0 + j] = 1;
+  launch_draft_rows(a, st, timed ? s->cur_ev + 2 * p0 : nullptr);
   return hip_check("tppsd_draft");
 }
 
@@ -1552,12 +1555,22 @@ void read_round_events(tppsd_state *s, int w) {
         (void)hipGetLastError();   // a failed query must not reach the next launch check
         continue;
       }
-      if ((int)(i / 2) < L) {
+      if (pair < L) {
         s->tm.attn_ms += ms;
         s->tm.attn_launches += 1;
-      } else if ((int)(i / 2) == 5 * L + 1) {
+      } else if (pair == 5 * L + 1) {
         s->tm.draft_kernel_ms += ms;
         s->tm.draft_kernel_launches += 1;
+      } else if (pair >= 5 * L + 2) {
+        // row drafting: launch 0 and every second one after it are row launches
+        const int j = pair - (5 * L + 2);
+        if (j > 0 && (j - 1) % 2 == 0) {
+          s->tm.draft_attn_ms += ms;
+          s->tm.draft_attn_launches += 1;
+        } else {
+          s->tm.draft_rows_ms += ms;
+          s->tm.draft_rows_launches += 1;
+        }
       } else {
         s->tm.gemm_ms += ms;
         s->tm.gemm_launches += 1;
@@ -1638,9 +1651,11 @@ int sd_loop(tppsd_state *s, int gamma, const float *params, int max_rounds, int 
     const double d = m->d(), F = m->cfg.d_ffn, rows = (double)s->B * (gamma + 1);
     s->round_flop = m->attnhp() ? 2.0 * rows * (L * (3 * d * 2 * d) + 4 * d * d)
                                 : 2.0 * rows * (L * (3 * d * d + d * d + 2 * d * F) + 4 * d * d);
-    // pairs: attention of each layer, the pass's GEMMs, the one-launch draft
-    if (int rc = make_events(s->gev, 2 * (5 * L + 2))) return rc;
-    s->ev_used.assign(5 * L + 2, 0);
+    // pairs: attention of each layer, the pass's GEMMs, the one-launch draft,
+    // then one per launch of row drafting
+    const int nrd = (s->row_draft && !params) ? rd_launches(s->D->cfg.n_layers, gamma) : 0;
+    if (int rc = make_events(s->gev, 2 * (5 * L + 2 + nrd))) return rc;
+    s->ev_used.assign(5 * L + 2 + nrd, 0);
   }
   if (phases)
     if (int rc = make_events(s->pev, 4)) return rc;

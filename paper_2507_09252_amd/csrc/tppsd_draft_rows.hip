@@ -236,11 +236,30 @@ template <int N, int KD> struct RdFrags {
   __device__ __forceinline__ void mul(const bf16_t *X, int ldx, int nx, EPI epi) const {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15;
+    auto xfrag = [&](int ks) {
+      return r < nx ? *(const bf16x8_t *)(X + r * ldx + ks * 32 + 8 * (lane >> 4))
+                    : __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+    };
+    if constexpr (TPW == 1) {
+      // one tile: each A fragment is used once, read as it is needed
+      const int tile = wave;
+      if (tile >= TILES) return;   // wave-uniform
+      f32x4_t c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ks += 2) {
+        c0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xfrag(ks), f[0][ks], c0, 0, 0, 0);
+        if (ks + 1 < KS) c1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xfrag(ks + 1), f[0][ks + 1], c1, 0, 0, 0);
+      }
+      const int n = tile * 16 + r;
+      if (lane < 16 && n < N) {
+#pragma unroll
+        for (int v = 0; v < NR; ++v) epi(v, n, c0[v] + c1[v]);
+      }
+      return;
+    }
     bf16x8_t xa[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      xa[ks] = r < nx ? *(const bf16x8_t *)(X + r * ldx + ks * 32 + 8 * (lane >> 4))
-                      : __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+    for (int ks = 0; ks < KS; ++ks) xa[ks] = xfrag(ks);
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
       const int tile = wave + t * RD_WAVES;
@@ -261,6 +280,7 @@ template <int N, int KD> struct RdFrags {
 };
 
 __device__ __forceinline__ void rd_sync() { __syncthreads(); }
+
 
 // LayerNorm (biased variance, eps 1e-5) of rows 0 .. np - 1 of xs [2][D]
 // into bf16 rows of y (stride D); wave p takes row p
@@ -372,30 +392,37 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   const int pos0 = base + (l == 1 ? 0 : l);
   const FusedLayerW &w = d.layer[ly];
   const bool last = ly == L - 1;
-  // this layer's output projection and both FFN products in flight, with the
-  // residual rows and every split partial of the sequence (all splits of the
-  // slab are read; those past the step's keys are ignored below)
-  RdFrags<D, D> fo;
-  RdFrags<F, D> f1;
-  RdFrags<D, F> f2;
-  const bf16_t *wl = a.pk + (size_t)ly * rd_layer_elems<D, F>();
-  fo.load_packed(wl);
-  f1.load_packed(wl + D * D);
-  f2.load_packed(wl + D * D + F * D);
+  // every load of the launch in flight at once, in the order of use: the
+  // split partials of the sequence (all splits of the slab; those past the
+  // step's keys are ignored below) and the residual rows, the output
+  // projection and the first FFN product, then the next layer's q, k, v or
+  // the decoder, into registers; the second FFN product straight into LDS
+  constexpr int NPV = RD_MAX_PART / RD_ROW_THREADS;
+  float pv[NPV];
   {
     const int cnt = d.H * a.S * 2 * (DH + 2);
     const float *src = a.part + (size_t)b * cnt;
-    float pv[RD_MAX_PART / RD_ROW_THREADS];
 #pragma unroll
-    for (int i = 0; i < RD_MAX_PART / RD_ROW_THREADS; ++i) {
+    for (int i = 0; i < NPV; ++i) {
       const int k = tid + i * RD_ROW_THREADS;
       pv[i] = k < cnt ? src[k] : 0.f;
     }
-    const float xv = tid < P * D ? xg[tid] : 0.f;
-#pragma unroll
-    for (int i = 0; i < RD_MAX_PART / RD_ROW_THREADS; ++i) sh.part[tid + i * RD_ROW_THREADS] = pv[i];
-    if (tid < P * D) (&sh.xs[0][0])[tid] = xv;
   }
+  const float xv = tid < P * D ? xg[tid] : 0.f;
+  const bf16_t *wl = a.pk + (size_t)ly * rd_layer_elems<D, F>();
+  RdFrags<D, D> fo;
+  RdFrags<F, D> f1;
+  fo.load_packed(wl);
+  f1.load_packed(wl + D * D);
+  RdFrags<D, F> f2;
+  f2.load_packed(wl + D * D + F * D);
+  RdFrags<3 * D, D> fq;
+  RdFrags<4 * D, D> fe;
+  RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
+  if (!last) fq.load_packed(a.pk + (size_t)(ly + 1) * rd_layer_elems<D, F>() + rd_off_qkv<D, F>());
+#pragma unroll
+  for (int i = 0; i < NPV; ++i) sh.part[tid + i * RD_ROW_THREADS] = pv[i];
+  if (tid < P * D) (&sh.xs[0][0])[tid] = xv;
   rd_sync();
   // merge the attention splits of each (row, head): output = sum_s e^{m_s - m} o_s / sum_s e^{m_s - m} l_s
   {
@@ -429,13 +456,17 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   f1.template mul<2>(&sh.ab[0][0], D, P, [&](int p, int nn, float acc) {
     if (p < P) sh.hb[p][nn] = f2bf(fmaxf(acc + w.ffn1_b[nn], 0.f));
   });
+  // the first product's registers are free: the next layer's q, k, v, or the decoder
+  const bool more = l < d.gamma;
+  if (last) {
+    fe.load_packed(a.pk_e);
+    fh.load_packed(a.pk_head);
+  }
+  rd_sync();
+  f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
+    if (p < P) sh.xs[p][nn] += acc + w.ffn2_b[nn];
+  });
   if (!last) {
-    RdFrags<3 * D, D> fq;
-    fq.load_packed(a.pk + (size_t)(ly + 1) * rd_layer_elems<D, F>() + rd_off_qkv<D, F>());
-    rd_sync();
-    f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
-      if (p < P) sh.xs[p][nn] += acc + w.ffn2_b[nn];
-    });
     rd_sync();
     rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[ly + 1].ln1_g, d.layer[ly + 1].ln1_b, P);
     for (int i = tid; i < P * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
@@ -444,28 +475,18 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     return;
   }
   // ---- last layer: decoder on the last row, the draw, the next token
-  RdFrags<4 * D, D> fe;
-  fe.load_packed(a.pk_e);
-  rd_sync();
-  f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
-    if (p < P) sh.xs[p][nn] += acc + w.ffn2_b[nn];
-  });
   rd_sync();
   const int pl = P - 1;
   rd_layernorm<D>(&sh.xs[pl][0], &sh.ab[0][0], d.lnf_g, d.lnf_b, 1);
   // decoder heads as one product over the four e slices: column n < 3 M reads
   // mixture row n (slice n / M), the others type-head row n - 3 M (tanh slice)
   const int NH = 3 * M + K;
-  RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
-  fh.load_packed(a.pk_head);
   rd_sync();
   fe.template mul<1>(&sh.ab[0][0], D, 1, [&](int, int nn, float acc) {
     const int slice = nn / D, c = nn - slice * D;
     sh.eb[slice][c] = f2bf(slice < 3 ? acc : tanhf(acc + d.k1_b[c]));
   });
-  const bool more = l < d.gamma;
-  RdFrags<3 * D, D> fq;
-  if (more) fq.load_packed(a.pk + rd_off_qkv<D, F>());
+  if (more) fq.load_packed(a.pk + rd_off_qkv<D, F>());   // the next token's layer-0 q, k, v
   rd_sync();
   fh.template mul<4>(&sh.eb[0][0], D, 4, [&](int r, int nn, float acc) {
     if (nn < NH && r == (nn < 3 * M ? nn / M : 3)) sh.hv[nn] = acc + (nn < 3 * M ? d.mix_b[nn] : d.k2_b[nn - 3 * M]);
@@ -553,19 +574,23 @@ void launch_pack_rd_head(const void *mix_w, const void *k2_w, int M, int K, int 
                      (const bf16_t *)k2_w, M, K, D, (bf16_t *)out);
 }
 
-void launch_draft_rows(RowDraftArgs a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+void launch_draft_rows(RowDraftArgs a, hipStream_t st, const hipEvent_t *ev) {
   const int B = a.d.B, H = a.d.H;
+  int j = 0;   // launch index: event pair j brackets launch j
+  auto e0 = [&]() { return ev ? ev[2 * j] : nullptr; };
+  auto e1 = [&]() { return ev ? ev[2 * j + 1] : nullptr; };
   a.step = 0;
   a.layer = 0;
-  hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, ev0, nullptr, 0, a);
+  hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, e0(), e1(), 0, a);
+  ++j;
   for (int l = 1; l <= a.d.gamma; ++l) {
     a.step = l;
     for (int ly = 0; ly < a.d.L; ++ly) {
       a.layer = ly;
-      hipLaunchKernelGGL(k_rd_attn<32>, dim3(a.S, H, B), dim3(256), 0, st, a);
-      const bool fin = l == a.d.gamma && ly == a.d.L - 1;
-      hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, nullptr,
-                            fin ? ev1 : nullptr, 0, a);
+      hipExtLaunchKernelGGL(k_rd_attn<32>, dim3(a.S, H, B), dim3(256), 0, st, e0(), e1(), 0, a);
+      ++j;
+      hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, e0(), e1(), 0, a);
+      ++j;
     }
   }
 }

@@ -164,8 +164,10 @@ constexpr size_t LDS_PER_WG = 160 * 1024;
 constexpr int RD_KEYS = 512;
 constexpr int RD_ROW_THREADS = 512;
 // floats of one sequence's split partials the row kernel stages in LDS
-// (H S 2 (d_head + 2); 4 heads of 32 over 16384 positions)
-constexpr int RD_MAX_PART = 8704;
+// (H S 2 (d_head + 2): 4 heads of 32 over 8192 positions take 4352; a
+// multiple of RD_ROW_THREADS)
+constexpr int RD_MAX_PART = 4608;
+static_assert(RD_MAX_PART % RD_ROW_THREADS == 0, "partial staging: whole rounds of the row workgroup");
 struct RowDraftArgs {
   DraftArgs d;              // model, cache, state and record pointers as for the one-launch draft
   float *x;                 // [B][2][d] residual stream of the step's rows
@@ -186,9 +188,11 @@ inline size_t rd_part_floats(int B, int H, int dh, int kv_cap) {
 // elements of the row kernel's packed decoder: [E; V_k1] (4 d x d) and the heads (128 x d)
 inline size_t rd_pack_dec_elems(int d) { return (size_t)4 * d * d + (size_t)128 * d; }
 void launch_pack_rd_head(const void *mix_w, const void *k2_w, int M, int K, int D, void *out, hipStream_t st);
-// all launches of one round's drafting; ev0 / ev1 (nullable) record the
-// start of the first and the end of the last
-void launch_draft_rows(RowDraftArgs a, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// all launches of one round's drafting: the step-0 row launch, then per step
+// and layer the attention and the row launch (1 + 2 L gamma launches); ev
+// (nullable) holds an event pair per launch, in that order
+inline int rd_launches(int L, int gamma) { return 1 + 2 * L * gamma; }
+void launch_draft_rows(RowDraftArgs a, hipStream_t st, const hipEvent_t *ev = nullptr);
 
 // Fused row block of a THP forward pass (k_block): for a tile of 16 rows,
 // everything between two attention launches. first: embed the tokens (else
@@ -291,6 +295,8 @@ void launch_gemm(const void *X, const LnA *ln, const void *W, int bf16, int T, i
                  hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // whether launch_gemm can take a LayerNorm operand of width K
 bool gemm_ln_fusable(int bf16, int K);
+// the layered pass runs LayerNorm as its own launch before a plain GEMM (see the definition)
+bool gemm_ln_split(int bf16, int d, int T);
 // Fused row-local part of a bf16 THP layer between two attention launches
 // (output projection + residual, feed-forward block + residual, and with
 // post the next layer's LayerNorm and q, k, v through qe), one launch over

@@ -174,6 +174,7 @@ __global__ void k_attnhp_update(float *__restrict__ x, const ACT *__restrict__ o
 // LayerNorm (biased variance, eps 1e-5), one wave per row
 // ---------------------------------------------------------------------------
 
+constexpr int LN_REG_MAX = 16;   // row widths up to 1024 are held in registers
 template <typename ACT>
 __global__ __launch_bounds__(256) void k_layernorm(const float *__restrict__ x, ACT *__restrict__ y,
                                                    const float *__restrict__ g, const float *__restrict__ bt,
@@ -182,6 +183,31 @@ __global__ __launch_bounds__(256) void k_layernorm(const float *__restrict__ x, 
   const int lane = threadIdx.x & 63;
   if (row >= T) return;
   const float *xr = x + (size_t)row * d;
+  if (d <= 64 * LN_REG_MAX) {
+    // the row in registers, read once (same summation order as below)
+    float xv[LN_REG_MAX];
+#pragma unroll
+    for (int i = 0; i < LN_REG_MAX; ++i) xv[i] = lane + 64 * i < d ? xr[lane + 64 * i] : 0.f;
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < LN_REG_MAX; ++i)
+      if (lane + 64 * i < d) s += xv[i];
+    const float mean = wave_sum(s) / (float)d;
+    float v = 0.f;
+#pragma unroll
+    for (int i = 0; i < LN_REG_MAX; ++i)
+      if (lane + 64 * i < d) {
+        const float c = xv[i] - mean;
+        v += c * c;
+      }
+    const float rstd = 1.f / sqrtf(wave_sum(v) / (float)d + 1e-5f);
+#pragma unroll
+    for (int i = 0; i < LN_REG_MAX; ++i) {
+      const int j = lane + 64 * i;
+      if (j < d) st(y, (size_t)row * d + j, (xv[i] - mean) * rstd * g[j] + bt[j]);
+    }
+    return;
+  }
   float s = 0.f;
   for (int j = lane; j < d; j += 64) s += xr[j];
   const float mean = wave_sum(s) / (float)d;
@@ -3448,6 +3474,15 @@ void launch_layernorm(const float *x, void *y, int bf16, const float *g, const f
 bool gemm_ln_fusable(int bf16, int K) {
   return K <= GEMM_LN_MAX_DEPTH * (bf16 ? gemm_bk<bf16_t>() : gemm_bk<float>());
 }
+
+// LayerNorm as a launch of its own ahead of a plain bf16 GEMM: for wide rows
+// over many rows, where every 32 x 32 tile of the fused form reads and
+// normalises all K fp32 columns of its rows again and the plain operand takes
+// the direct-to-LDS GEMM. Measured on a verify pass of 544 rows of width 512
+// (32 sequences x 17 positions, 8 layers): the fused q, k, v and FFN-in GEMMs
+// took 15.5 and 16.3 us; LayerNorm (5.3 us) + plain GEMM brought the pass's
+// GEMMs and LayerNorms from 438 to 399 us.
+bool gemm_ln_split(int bf16, int d, int T) { return bf16 && d >= 512 && d % 128 == 0 && T >= 512; }
 
 template <typename ELT>
 static void gemm_dispatch(const void *X, const LnA *ln, const void *W, int T, int N, int K, const Epi &epi,

@@ -50,7 +50,9 @@ class TimingC(ctypes.Structure):
     _fields_ = [("attn_ms", c_double), ("attn_launches", c_int64), ("gemm_ms", c_double),
                 ("gemm_launches", c_int64), ("gemm_flop", c_double), ("draft_ms", c_double),
                 ("verify_ms", c_double), ("accept_ms", c_double), ("rounds", c_int64),
-                ("draft_kernel_ms", c_double), ("draft_kernel_launches", c_int64)]
+                ("draft_kernel_ms", c_double), ("draft_kernel_launches", c_int64),
+                ("draft_attn_ms", c_double), ("draft_attn_launches", c_int64),
+                ("draft_rows_ms", c_double), ("draft_rows_launches", c_int64)]
 
 
 ENCODER = {"thp": 0, "attnhp": 1}   # TPPSD_ENC_*

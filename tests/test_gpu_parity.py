@@ -45,6 +45,9 @@ VERIFY_CASES = [
     small("c3", 3, n_hist=40),
     small("c4", 2, n_hist=70, init="bias"),
     small("c4", 2, n_hist=70, init="paper", mismatch=False),
+    # 32 x 17 = 544 rows of width 512: LayerNorm runs as its own launch ahead
+    # of the direct-to-LDS GEMMs
+    small("c4", 32, n_hist=40, init="bias"),
     small("c5", 9, init="bias"),
     small("c5", 5),
     # long histories over few (sequence, head) pairs: the key range is split
