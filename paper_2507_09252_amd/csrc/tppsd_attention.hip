@@ -63,7 +63,14 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
   chunk = (chunk + KT - 1) / KT * KT;
   const int k_begin = split * chunk, k_end = min(n_keys, k_begin + chunk);
   const size_t kvbase = ((size_t)b * H + h) * cap;
-  const float scale = 1.f / sqrtf((float)DH);
+  // scores are kept in base-2 units (q.k / sqrt(d_head) times log2 e), so
+  // that every exponential is one exp2 instruction; maxima leave the kernel
+  // in natural units
+  const float scale2 = 1.4426950408889634f / sqrtf((float)DH);
+  constexpr float LN2 = 0.69314718055994531f;
+  // all-ones A operand: O^T rows of ones give each query's sum of the
+  // (bf16-rounded) probabilities the P V product takes
+  const bf16x8_t ones = __builtin_bit_cast(bf16x8_t, make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
 
   // query fragments (B operand of S^T): Q[16 t + rr][k slice of lane group g]
   bf16x8_t qf[QT][NC];
@@ -80,12 +87,12 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
       qf16[t] = q_ok ? *(const short4_t *)(qp + 4 * g) : (short4_t){0, 0, 0, 0};
     }
   }
-  float m_run[QT], l_run[QT];
-  f32x4_t oacc[QT][NDT];
+  float m_run[QT];
+  f32x4_t oacc[QT][NDT], lacc[QT];
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
     m_run[t] = -INFINITY;
-    l_run[t] = 0.f;
+    lacc[t] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int td = 0; td < NDT; ++td) oacc[t][td] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
   }
@@ -128,6 +135,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
         vw[td] = (uint4){w[0], w[1], w[2], w[3]};
       }
     }
+    const bool interior = kt + KT <= k_end && kt + KT <= base + 1;   // every key visible to every query
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
       f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
@@ -141,7 +149,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
         s0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(b0, qf16[t], s0, 0, 0, 0);
         s1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(b1, qf16[t], s1, 0, 0, 0);
       }
-      // scores of keys kt + 8g + j, j = 0..7, for query 16 t + rr
+      // scores of keys kt + 8g + j, j = 0..7, for query 16 t + rr (steps
+      // wholly inside every query's visible range skip the masks; padding
+      // queries then carry finite scores of zero queries, never stored)
       const int my_q = 16 * t + rr, my_last = base + my_q;
       const bool q_ok = my_q < P;
       float sv[8];
@@ -150,31 +160,27 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
       for (int j = 0; j < 8; ++j) {
         const int key = kt + 8 * g + j;
         const float raw = (j < 4) ? s0[j] : s1[j - 4];
-        const bool ok = q_ok && key < k_end && key <= my_last;
-        sv[j] = ok ? raw * scale : -INFINITY;
+        const bool ok = interior || (q_ok && key < k_end && key <= my_last);
+        sv[j] = ok ? raw * scale2 : -INFINITY;
         mx = fmaxf(mx, sv[j]);
       }
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float m_new = fmaxf(m_run[t], mx);
-      const float alpha = (m_new == -INFINITY) ? 1.f : expf(m_run[t] - m_new);
-      float ps = 0.f;
+      // (exp2 of -inf is 0: masked keys and an empty running state drop out)
+      const float m_ref = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = __builtin_amdgcn_exp2f(m_run[t] - m_ref);
       uint32_t pw[4];
 #pragma unroll
-      for (int j = 0; j < 8; j += 2) {
-        const float p0 = (sv[j] == -INFINITY) ? 0.f : expf(sv[j] - m_new);
-        const float p1 = (sv[j + 1] == -INFINITY) ? 0.f : expf(sv[j + 1] - m_new);
-        // P V takes the probabilities in bf16; the normaliser sums the same
-        // rounded values, so the output stays a convex combination of values
-        const uint32_t w = pk2bf(p0, p1);
-        ps += __uint_as_float(w << 16) + __uint_as_float(w & 0xFFFF0000u);
-        pw[j >> 1] = w;
-      }
+      for (int j = 0; j < 8; j += 2)
+        pw[j >> 1] = pk2bf(__builtin_amdgcn_exp2f(sv[j] - m_ref), __builtin_amdgcn_exp2f(sv[j + 1] - m_ref));
+      // P V takes the probabilities in bf16; the normaliser (the ones rows)
+      // sums the same rounded values, so the output stays a convex
+      // combination of values
       const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, (uint4){pw[0], pw[1], pw[2], pw[3]});
-      ps += __shfl_xor(ps, 16, 64);
-      ps += __shfl_xor(ps, 32, 64);
-      l_run[t] = l_run[t] * alpha + ps;
       m_run[t] = m_new;
+      lacc[t] *= alpha;
+      lacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb, lacc[t], 0, 0, 0);
 #pragma unroll
       for (int td = 0; td < NDT; ++td) {
         oacc[t][td] *= alpha;
@@ -188,7 +194,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
   for (int t = 0; t < QT; ++t) {
     if (g == 0) {
       red_m[wave][16 * t + rr] = m_run[t];
-      red_l[wave][16 * t + rr] = l_run[t];
+      red_l[wave][16 * t + rr] = lacc[t][0];
     }
 #pragma unroll
     for (int td = 0; td < NDT; ++td)
@@ -205,10 +211,11 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
     float L = 0.f, O = 0.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      const float f = (red_m[w][qq] == -INFINITY) ? 0.f : expf(red_m[w][qq] - M);
+      const float f = (red_m[w][qq] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(red_m[w][qq] - M);
       L += red_l[w][qq] * f;
       O += red_o[w][j][qq] * f;
     }
+    M *= LN2;   // natural units from here
     if (splits == 1) {
       if (sink) sink_adjust(M, L, O);
       o[(size_t)(b * P + qq) * d + h * DH + j] = f2bf(L > 0.f ? O / L : 0.f);
