@@ -100,6 +100,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
   const int krow0 = 8 * (rr >> 2) + (rr & 3), krow1 = krow0 + 4;
 
   for (int kt = k_begin + wave * KT; kt < k_end; kt += 4 * KT) {
+    const bool interior = kt + KT <= k_end && kt + KT <= base + 1;   // every key visible to every query
     const size_t r0 = kvbase + min(kt + krow0, cap - 1), r1 = kvbase + min(kt + krow1, cap - 1);
     bf16x8_t a0[NC], a1[NC];
     short4_t b0 = {0, 0, 0, 0}, b1 = {0, 0, 0, 0};
@@ -120,10 +121,10 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
 #pragma unroll
     for (int td = 0; td < NDT; ++td) {
       uint4 v = {0u, 0u, 0u, 0u};
-      if (nv > 0) v = *(const uint4 *)(vc + kvbase * DH + (size_t)(k8 >> 3) * (8 * DH) + (16 * td + rr) * 8);
+      if (interior || nv > 0) v = *(const uint4 *)(vc + kvbase * DH + (size_t)(k8 >> 3) * (8 * DH) + (16 * td + rr) * 8);
       vw[td] = v;
     }
-    if (nv > 0 && nv < 8) {
+    if (!interior && nv > 0 && nv < 8) {
 #pragma unroll
       for (int td = 0; td < NDT; ++td) {
         uint32_t w[4] = {vw[td].x, vw[td].y, vw[td].z, vw[td].w};
@@ -135,7 +136,6 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
         vw[td] = (uint4){w[0], w[1], w[2], w[3]};
       }
     }
-    const bool interior = kt + KT <= k_end && kt + KT <= base + 1;   // every key visible to every query
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
       f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
@@ -179,14 +179,18 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
       // combination of values
       const bf16x8_t pb = __builtin_bit_cast(bf16x8_t, (uint4){pw[0], pw[1], pw[2], pw[3]});
       m_run[t] = m_new;
-      lacc[t] *= alpha;
+      // the accumulators are rescaled only when some query's maximum rose
+      // (alpha is exactly 1 otherwise)
+      if (__ballot(alpha != 1.f) != 0ull) {
+        lacc[t] *= alpha;
+#pragma unroll
+        for (int td = 0; td < NDT; ++td) oacc[t][td] *= alpha;
+      }
       lacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb, lacc[t], 0, 0, 0);
 #pragma unroll
-      for (int td = 0; td < NDT; ++td) {
-        oacc[t][td] *= alpha;
+      for (int td = 0; td < NDT; ++td)
         oacc[t][td] =
             __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vw[td]), pb, oacc[t][td], 0, 0, 0);
-      }
     }
   }
   // merge the four waves: lane (rr, g) holds O^T[16 td + 4 g + i][query 16 t + rr]
