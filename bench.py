@@ -292,26 +292,36 @@ def gamma_sweep(args, wl, tm, dm, HT, HK, ar_value, B, n_gen):
     return rows
 
 
-def attention_source_sha256():
-    """SHA-256 over the sources that define the attention kernels."""
+# the sources each kernel class's measured traffic depends on
+TRAFFIC_SOURCES = {
+    "verify_attention": ("tppsd_attention.hip", "tppsd_attention.h", "tppsd_device.h"),
+    "draft_attention": ("tppsd_draft_rows.hip", "tppsd_internal.h", "tppsd_device.h"),
+    "draft_rows": ("tppsd_draft_rows.hip", "tppsd_internal.h", "tppsd_device.h"),
+}
+
+
+def source_sha256(files):
+    """SHA-256 over the given kernel sources (paper_2507_09252_amd/csrc)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("tppsd_attention.hip", "tppsd_attention.h", "tppsd_device.h"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2507_09252_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
-def measured_traffic(wl_name, key="workloads"):
-    """HBM bytes per verify-attention launch from the committed rocprofv3 --pmc
-    runs, if the kernel source is unchanged since they were taken; else None."""
+def measured_traffic(cls, wl_name):
+    """HBM bytes per launch of a kernel class from the committed rocprofv3
+    --pmc runs (FETCH_SIZE and WRITE_SIZE scaled by a copy of known size), if
+    the class's sources are unchanged since they were taken; else None."""
     try:
-        rec = json.load(open(os.path.join(ROOT, "profiles", "verify_attention_traffic.json")))
+        rec = json.load(open(os.path.join(ROOT, "profiles", "hbm_traffic.json")))
     except OSError:
         return None
-    if attention_source_sha256() != rec["kernel_source_sha256"]:
+    k = rec["kernels"].get(cls)
+    if k is None or source_sha256(TRAFFIC_SOURCES[cls]) != k["sources_sha256"]:
         return None
-    w = rec[key].get(wl_name)
+    w = k["workloads"].get(wl_name)
     return None if w is None else w["traffic_bytes_per_launch"]
 
 
@@ -416,20 +426,20 @@ def main():
         classes["verify_attention"] = {
             "bound": "hbm", "kernel": ATTN_KERNEL[wl.prec], "ms": tk["attn_ms"], "launches": tk["attn_launches"],
             "per_launch": per_attn, "unit": "GB/s", "peak": HBM_PEAK_GBS,
-            "traffic": measured_traffic(wl.name)}
+            "traffic": measured_traffic("verify_attention", wl.name)}
     if tk["draft_attn_launches"]:
         classes["draft_attention"] = {
             "bound": "hbm", "kernel": "k_rd_attn<32> (row drafting: split attention, one launch per step and layer)",
             "ms": tk["draft_attn_ms"], "launches": tk["draft_attn_launches"],
             "per_launch": draft_attn_bytes(wl, B, gamma, ctx), "unit": "GB/s", "peak": HBM_PEAK_GBS,
-            "traffic": None}
+            "traffic": measured_traffic("draft_attention", wl.name)}
     if tk["draft_rows_launches"]:
         classes["draft_rows"] = {
             "bound": "hbm", "kernel": "k_rd_rows<128, 512, 32> (row drafting: one workgroup per sequence, "
                                       "per step and layer)",
             "ms": tk["draft_rows_ms"], "launches": tk["draft_rows_launches"],
             "per_launch": draft_rows_bytes(wl, B, gamma), "unit": "GB/s", "peak": HBM_PEAK_GBS,
-            "traffic": None}
+            "traffic": measured_traffic("draft_rows", wl.name)}
     if tk["draft_kernel_launches"]:
         classes["draft"] = {
             "bound": "hbm", "kernel": "k_draft_fused / k_draft_wave (one launch per round: all gamma draft steps)",
