@@ -2075,7 +2075,8 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // resident workgroups of four waves per CU the register allocation aims at
-// (4: 128 VGPRs with spills, c5 draft 472 us per round; 2: ~190 VGPRs, 309 us)
+// (4: 128 VGPRs with spills, c5 draft 472 us per round; 3: 168 VGPRs, 356 us;
+// 2: ~180 VGPRs, 309 us)
 #ifndef TPPSD_WAVE_DRAFT_WG_PER_CU
 #define TPPSD_WAVE_DRAFT_WG_PER_CU 2
 #endif
