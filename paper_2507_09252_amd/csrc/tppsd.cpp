@@ -730,7 +730,7 @@ int do_draft_rows(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStre
   RowDraftArgs a{};
   a.d = draft_args(s, gamma, out);
   a.x = s->x;
-  a.q = (float *)s->q;
+  a.xn = (bf16_t *)s->a;
   a.part = s->attn_part;
   a.pk = (const bf16_t *)s->packD;
   a.pk_e = (const bf16_t *)s->packDdec;

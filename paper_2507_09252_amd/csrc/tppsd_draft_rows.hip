@@ -35,61 +35,155 @@ namespace tppsd {
 namespace {
 
 constexpr int RD_WAVES = RD_ROW_THREADS / 64;
+constexpr int RD_VEC = 2048;   // floats of a row launch's staged vectors (RdVec)
 
 // ---------------------------------------------------------------------------
 // split attention: workgroup (s, h, b) takes keys [s RD_KEYS, (s + 1) RD_KEYS)
 // of head h of sequence b
 // ---------------------------------------------------------------------------
-template <int DH>
+template <int D, int DH>
 __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
   constexpr int NG = 256 / DH;              // lane groups over the value blocks
   constexpr int BPL = RD_KEYS / 8 / NG;     // value blocks per lane
+  static_assert(DH == 32 && D % 128 == 0, "q, k, v: 32 groups of 8 lanes, 16 elements per lane and pass of 128");
   __shared__ __attribute__((aligned(16))) float es[2][RD_KEYS];
   __shared__ float red[2][NG][DH];
   __shared__ float wred[2][4][2];
+  __shared__ __attribute__((aligned(16))) bf16_t xl[2][D];        // LayerNorm'd rows of the step's tokens
+  __shared__ float qs[2][DH];                                       // queries (bf16-rounded)
+  __shared__ __attribute__((aligned(16))) bf16_t kvn[2][2][DH];   // the new keys and values [k / v][row]
   const DraftArgs &d = a.d;
   const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   constexpr int SEG = DH * 2 / 16;          // 16-byte segments of a key row
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, seg = tid % SEG;
-  // the sequence's header words and the lane's query segments, loaded together
+  // q, k, v of the step's rows: group r = tid / 8 of eight lanes takes output
+  // row r of the head, lane j = tid % 8 elements 16 j .. + 15 of every 128
+  constexpr int NC = D / 128;               // 128-element chunks per row
+  const int r = tid >> 3, j8 = tid & 7;
+  const FusedLayerW &lw = d.layer[a.layer];
+  const bf16_t *wqkv = (const bf16_t *)lw.qkv_w;
+  auto wrow = [&](int which) { return wqkv + (size_t)(which * D + h * DH + r) * D + 16 * j8; };
+  // the sequence's header words, the LayerNorm'd rows and this head's query
+  // rows of W_qkv, loaded together
   const int done = d.done[b], lenD = d.lenD[b];
   const int P = a.step == 1 ? 2 : 1;
-  float q[2][8];
+  uint4 xw = make_uint4(0u, 0u, 0u, 0u);
+  if (tid < 2 * D / 8) xw = *(const uint4 *)(a.xn + (size_t)b * 2 * D + 8 * tid);
+  uint4 wq[NC][2];
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const float *qp = a.q + ((size_t)b * 2 + p) * d.d + h * DH + 8 * seg;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) q[p][j] = qp[j];
+  for (int c = 0; c < NC; ++c) {
+    wq[c][0] = *(const uint4 *)(wrow(0) + 128 * c);
+    wq[c][1] = *(const uint4 *)(wrow(0) + 128 * c + 8);
   }
+  // (the biases too: a load issued after the cache loads would be waited for behind them)
+  const float bq = lw.qkv_b[h * DH + r], bk = lw.qkv_b[D + h * DH + r], bv = lw.qkv_b[2 * D + h * DH + r];
   if (done) return;
   const int pos0 = lenD + (a.step == 1 ? 0 : a.step);
   const int n_keys = min(pos0 + P, d.cap);
   const int k0 = s * RD_KEYS;
   if (k0 >= n_keys) return;   // whole workgroup; no barrier passed yet
   const size_t row0 = ((size_t)b * d.H + h) * d.cap;
-  const bf16_t *kc = (const bf16_t *)(d.kc + d.layer_bytes * a.layer);
-  const bf16_t *vc = (const bf16_t *)(d.vc + d.layer_bytes * a.layer);
+  bf16_t *kc = (bf16_t *)(d.kc + d.layer_bytes * a.layer);
+  bf16_t *vc = (bf16_t *)(d.vc + d.layer_bytes * a.layer);
+  // the step's new positions pos0 .. pos0 + P - 1 whose key and value this
+  // split owns (it computes and appends them; they are in no other split)
+  auto owned = [&](int p) { const int pn = pos0 + p; return p < P && pn >= k0 && pn < k0 + RD_KEYS && pn < d.cap; };
+  const bool any_owned = owned(0) || owned(1);
+  uint4 wk[NC][2], wv[NC][2];
+  if (any_owned) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      wk[c][0] = *(const uint4 *)(wrow(1) + 128 * c);
+      wk[c][1] = *(const uint4 *)(wrow(1) + 128 * c + 8);
+      wv[c][0] = *(const uint4 *)(wrow(2) + 128 * c);
+      wv[c][1] = *(const uint4 *)(wrow(2) + 128 * c + 8);
+    }
+  }
   // every load of the split in flight at once, each wave instruction reading
   // 1 KB of contiguous memory (non-temporal: the cache streams through once per
   // step and should not push the draft model's weights out of L2). Keys: lane
   // t of load i holds 16-byte segment t % SEG of key i KPI + t / SEG. Values:
-  // lane (grp, col) holds the 8-position blocks of column col.
+  // lane (grp, col) holds the 8-position blocks of column col. The slots of
+  // the step's new positions are replaced below. Slots past the key range
+  // read the range's last key or value block (unconditional loads: a load
+  // under a lane condition makes the compiler wait for every load before it),
+  // and never count: their scores are masked, their blocks skipped.
   constexpr int KPI = 256 / SEG;            // keys per load
   constexpr int NKL = RD_KEYS / KPI;        // key loads per lane
   u32x4_t kr[NKL];
 #pragma unroll
   for (int i = 0; i < NKL; ++i) {
-    const int pos = k0 + i * KPI + tid / SEG;
-    kr[i] = pos < n_keys ? __builtin_nontemporal_load((const u32x4_t *)(kc + (row0 + pos) * DH) + seg)
-                         : u32x4_t{0u, 0u, 0u, 0u};
+    const int pos = min(k0 + i * KPI + tid / SEG, n_keys - 1);
+    kr[i] = __builtin_nontemporal_load((const u32x4_t *)(kc + (row0 + pos) * DH) + seg);
   }
   const int col = tid % DH, grp = tid / DH;
   u32x4_t vr[BPL];
 #pragma unroll
   for (int i = 0; i < BPL; ++i) {
-    const int pb = k0 + 8 * (grp + i * NG);   // first position of the block
-    vr[i] = pb < n_keys ? __builtin_nontemporal_load((const u32x4_t *)(vc + v_at<bf16_t>(row0, pb, col, DH)))
-                        : u32x4_t{0u, 0u, 0u, 0u};
+    const int pb = min(k0 + 8 * (grp + i * NG), (n_keys - 1) & ~7);   // first position of the block
+    vr[i] = __builtin_nontemporal_load((const u32x4_t *)(vc + v_at<bf16_t>(row0, pb, col, DH)));
+  }
+  if (tid < 2 * D / 8) *(uint4 *)(&xl[0][0] + 8 * tid) = xw;
+  __syncthreads();
+  // dot products of a weight row slice with a row's slice, fp32 over bf16
+  auto dot16 = [&](const uint4 (&w)[NC][2], int p) {
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int hlf = 0; hlf < 2; ++hlf) {
+        const uint4 xx = *(const uint4 *)(&xl[p][0] + 128 * c + 16 * j8 + 8 * hlf);
+        const uint32_t ww[4] = {w[c][hlf].x, w[c][hlf].y, w[c][hlf].z, w[c][hlf].w};
+        const uint32_t xv[4] = {xx.x, xx.y, xx.z, xx.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc += __uint_as_float(ww[e] << 16) * __uint_as_float(xv[e] << 16);
+          acc += __uint_as_float(ww[e] & 0xFFFF0000u) * __uint_as_float(xv[e] & 0xFFFF0000u);
+        }
+      }
+    return group_sum(acc, 8);
+  };
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (p >= P) break;
+    const float qa = dot16(wq, p);
+    if (j8 == 0) qs[p][r] = bf2f(f2bf(qa + bq));
+    if (owned(p)) {   // workgroup-uniform
+      const float ka = dot16(wk, p), va = dot16(wv, p);
+      if (j8 == 0) {
+        const bf16_t kb = f2bf(ka + bk), vb = f2bf(va + bv);
+        kvn[0][p][r] = kb;
+        kvn[1][p][r] = vb;
+        const int pn = pos0 + p;
+        kc[(row0 + pn) * DH + r] = kb;
+        vc[v_at<bf16_t>(row0, pn, r, DH)] = vb;
+      }
+    }
+  }
+  __syncthreads();
+  float q[2][8];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) q[p][jj] = qs[p][8 * seg + jj];
+  // the owned new positions' keys and values replace what the loads read
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    if (!owned(p)) continue;
+    const int pn = pos0 + p;
+#pragma unroll
+    for (int i = 0; i < NKL; ++i)
+      if (k0 + i * KPI + tid / SEG == pn) kr[i] = *(const u32x4_t *)(&kvn[0][p][0] + 8 * seg);
+    const uint32_t vb = kvn[1][p][col];
+#pragma unroll
+    for (int i = 0; i < BPL; ++i) {
+      const int pb = k0 + 8 * (grp + i * NG);
+      if (pn >= pb && pn < pb + 8) {
+        const int e = pn - pb, wi = e >> 1;
+        const uint32_t old = vr[i][wi];
+        vr[i][wi] = (e & 1) ? ((old & 0x0000FFFFu) | (vb << 16)) : ((old & 0xFFFF0000u) | vb);
+      }
+    }
   }
   // scores, per query: q k / sqrt(d_head) (the SEG lanes of a key sum their
   // segments); keys past the query masked
@@ -219,15 +313,17 @@ template <int N, int KD> struct RdFrags {
   bf16x8_t f[TPW][KS];
   // W in fragment order (fragment (tile, ks) is 64 lanes x 8 elements at
   // (tile KS + ks) 512): one contiguous kilobyte per wave instruction
+  // (tiles past the matrix read its last tile, unused by mul: a load under a
+  // condition the compiler cannot prove wave-uniform would make it wait for
+  // every load issued before)
   __device__ __forceinline__ void load_packed(const bf16_t *Wp) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
-      const int tile = wave + t * RD_WAVES;
+      const int tile = min(wave + t * RD_WAVES, TILES - 1);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        f[t][ks] = tile < TILES ? *(const bf16x8_t *)(Wp + ((size_t)(tile * KS + ks) * 64 + lane) * 8)
-                                : __builtin_bit_cast(bf16x8_t, make_uint4(0u, 0u, 0u, 0u));
+        f[t][ks] = *(const bf16x8_t *)(Wp + ((size_t)(tile * KS + ks) * 64 + lane) * 8);
     }
   }
   // rows 0 .. NR - 1 of X (bf16 in LDS, row stride ldx elements; rows
@@ -318,47 +414,44 @@ struct RdShared {
   __attribute__((aligned(16))) bf16_t eb[4][D];       // decoder e slices (w, mu, sigma) and tanh
   float hv[128];                                       // decoder outputs
   float part[RD_MAX_PART];                             // the sequence's split partials
+  float vec[RD_VEC];                                   // the launch's biases and LayerNorm parameters (rd_vec_*)
   float tok_t;
   int tok_k;
 };
 
-// q, k, v of rows 0 .. np - 1 (LayerNorm output in sh.ab) for the layer whose
-// weights are in fr: queries to a.q, keys and values into the layer's cache at
-// positions pos0 + row
-template <int D, int DH, typename FR>
-__device__ __forceinline__ void rd_qkv(const RowDraftArgs &a, const FR &fr, const bf16_t *xin, int np, int ly,
-                                       int b, int pos0, const float *qkv_b) {
-  const DraftArgs &d = a.d;
-  bf16_t *kc = (bf16_t *)(d.kc + d.layer_bytes * ly);
-  bf16_t *vc = (bf16_t *)(d.vc + d.layer_bytes * ly);
-  auto epi = [&](int p, int n, float acc) {
-    if (p >= np) return;
-    const float v = bf2f(f2bf(acc + qkv_b[n]));
-    const int which = n / D, c = n - which * D;
-    if (which == 0) {
-      a.q[((size_t)b * 2 + p) * D + c] = v;
-      return;
-    }
-    const int hh = c / DH, j = c - hh * DH, pos = pos0 + p;
-    const size_t row0 = ((size_t)b * d.H + hh) * d.cap;
-    if (pos < d.cap)
-      st(which == 1 ? kc : vc, which == 1 ? (row0 + pos) * DH + j : v_at<bf16_t>(row0, pos, j, DH), v);
-    else
-      atomicOr(d.status, TPPSD_STATUS_CAPACITY);
-  };
-  fr.template mul<2>(xin, D, np, epi);
+// the LayerNorm'd rows 0 .. np - 1 (sh.ab) go to memory for the next
+// attention launch, which forms q, k, v from them; a position past the
+// cache capacity is flagged here
+template <int D>
+__device__ __forceinline__ void rd_store_xn(const RowDraftArgs &a, const bf16_t *ab, int np, int b, int pos0) {
+  const int tid = threadIdx.x;
+  if (tid < np * D / 8) *(uint4 *)(a.xn + (size_t)b * 2 * D + 8 * tid) = *(const uint4 *)(ab + 8 * tid);
+  if (tid == 0 && pos0 + np > a.d.cap) atomicOr(a.d.status, TPPSD_STATUS_CAPACITY);
 }
 
 // the THP embedding (sin / cos time encoding + type row) of event (t, k) into row p
 template <int D>
-__device__ __forceinline__ void rd_embed(const DraftArgs &d, float *xrow, float t, int k) {
+__device__ __forceinline__ void rd_embed(const DraftArgs &d, const float *freq, float *xrow, float t, int k) {
   const int tid = threadIdx.x;
   if (tid < D) {
-    const float arg = t * d.freq[tid];
+    const float arg = t * freq[tid];
     const int kk = min(max(k, 0), d.K - 1);
     xrow[tid] = ((tid & 1) ? cosf(arg) : sinf(arg)) + bf2f(((const bf16_t *)d.type_emb)[(size_t)kk * D + tid]);
   }
 }
+
+// Offsets in RdShared::vec of the small vectors a row launch reads (the
+// current layer's output / FFN biases and second LayerNorm; the next layer's
+// first LayerNorm, or LN_f, the decoder biases and the next token's layer-0
+// LayerNorm and time frequencies). They are loaded before the matrices and
+// read from LDS, so that no epilogue waits on a memory load issued behind the
+// matrices.
+template <int D, int F> struct RdVec {
+  static constexpr int OUTB = 0, LN2G = D, LN2B = 2 * D, F1B = 3 * D, F2B = 3 * D + F, N1G = 4 * D + F,
+                       N1B = 5 * D + F, K1B = 6 * D + F, MIXB = 7 * D + F, K2B = MIXB + 192, FREQ = K2B + 64,
+                       L0G = FREQ + D, L0B = L0G + D, END = L0B + D;
+  static_assert(END <= RD_VEC, "vector area");
+};
 
 // Launch modes: step 0 embeds the last two committed events and computes
 // their layer-0 q, k, v; step l >= 1, layer ly finishes layer ly of the step's
@@ -374,17 +467,15 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   const int L = d.L, M = d.M, K = d.K;
   float *xg = a.x + (size_t)b * 2 * D;
   if (a.step == 0) {
-    RdFrags<3 * D, D> fq;
-    fq.load_packed(a.pk + rd_off_qkv<D, F>());
     for (int p = 0; p < 2; ++p) {
       const size_t i = (size_t)b * d.ev_stride + n - 2 + p;
-      rd_embed<D>(d, sh.xs[p], d.ev_t[i], d.ev_k[i]);
+      rd_embed<D>(d, d.freq, sh.xs[p], d.ev_t[i], d.ev_k[i]);
     }
     rd_sync();
     rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[0].ln1_g, d.layer[0].ln1_b, 2);
     for (int i = tid; i < 2 * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
     rd_sync();
-    rd_qkv<D, DH>(a, fq, &sh.ab[0][0], 2, 0, b, base, d.layer[0].qkv_b);
+    rd_store_xn<D>(a, &sh.ab[0][0], 2, b, base);
     return;
   }
   const int l = a.step, ly = a.layer;
@@ -409,6 +500,28 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     }
   }
   const float xv = tid < P * D ? xg[tid] : 0.f;
+  // the launch's small vectors, one unconditional load per element
+  typedef RdVec<D, F> V;
+  constexpr int NVL = RD_VEC / RD_ROW_THREADS;
+  float vl[NVL];
+  {
+    struct Seg { const float *p; int off, n; };
+    const FusedLayerW &wn = d.layer[last ? 0 : ly + 1];
+    const Seg segs[] = {{w.out_b, V::OUTB, D},      {w.ln2_g, V::LN2G, D},          {w.ln2_b, V::LN2B, D},
+                        {w.ffn1_b, V::F1B, F},      {w.ffn2_b, V::F2B, D},
+                        {last ? d.lnf_g : wn.ln1_g, V::N1G, D}, {last ? d.lnf_b : wn.ln1_b, V::N1B, D},
+                        {d.k1_b, V::K1B, D},        {d.mix_b, V::MIXB, 3 * M},       {d.k2_b, V::K2B, K},
+                        {d.freq, V::FREQ, D},       {d.layer[0].ln1_g, V::L0G, D},   {d.layer[0].ln1_b, V::L0B, D}};
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int k = tid + i * RD_ROW_THREADS;
+      const float *src = w.out_b;   // (slots between segments read a valid element, unused)
+#pragma unroll
+      for (const Seg &g : segs)
+        if (k >= g.off && k < g.off + g.n) src = g.p + (k - g.off);
+      vl[i] = *src;
+    }
+  }
   const bf16_t *wl = a.pk + (size_t)ly * rd_layer_elems<D, F>();
   RdFrags<D, D> fo;
   RdFrags<F, D> f1;
@@ -416,13 +529,15 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   f1.load_packed(wl + D * D);
   RdFrags<D, F> f2;
   f2.load_packed(wl + D * D + F * D);
-  RdFrags<3 * D, D> fq;
   RdFrags<4 * D, D> fe;
   RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
-  if (!last) fq.load_packed(a.pk + (size_t)(ly + 1) * rd_layer_elems<D, F>() + rd_off_qkv<D, F>());
+  // (keeps the stores below, which wait for the partials, behind every load)
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int i = 0; i < NPV; ++i) sh.part[tid + i * RD_ROW_THREADS] = pv[i];
   if (tid < P * D) (&sh.xs[0][0])[tid] = xv;
+#pragma unroll
+  for (int i = 0; i < NVL; ++i) sh.vec[tid + i * RD_ROW_THREADS] = vl[i];
   rd_sync();
   // merge the attention splits of each (row, head): output = sum_s e^{m_s - m} o_s / sum_s e^{m_s - m} l_s
   {
@@ -448,13 +563,13 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   rd_sync();
   // output projection + residual
   fo.template mul<2>(&sh.ab[0][0], D, P, [&](int p, int nn, float acc) {
-    if (p < P) sh.xs[p][nn] += acc + w.out_b[nn];
+    if (p < P) sh.xs[p][nn] += acc + sh.vec[V::OUTB + nn];
   });
   rd_sync();
-  rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], w.ln2_g, w.ln2_b, P);
+  rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::LN2G, sh.vec + V::LN2B, P);
   rd_sync();
   f1.template mul<2>(&sh.ab[0][0], D, P, [&](int p, int nn, float acc) {
-    if (p < P) sh.hb[p][nn] = f2bf(fmaxf(acc + w.ffn1_b[nn], 0.f));
+    if (p < P) sh.hb[p][nn] = f2bf(fmaxf(acc + sh.vec[V::F1B + nn], 0.f));
   });
   // the first product's registers are free: the next layer's q, k, v, or the decoder
   const bool more = l < d.gamma;
@@ -464,32 +579,31 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   }
   rd_sync();
   f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
-    if (p < P) sh.xs[p][nn] += acc + w.ffn2_b[nn];
+    if (p < P) sh.xs[p][nn] += acc + sh.vec[V::F2B + nn];
   });
   if (!last) {
     rd_sync();
-    rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[ly + 1].ln1_g, d.layer[ly + 1].ln1_b, P);
+    rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::N1G, sh.vec + V::N1B, P);
     for (int i = tid; i < P * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
     rd_sync();
-    rd_qkv<D, DH>(a, fq, &sh.ab[0][0], P, ly + 1, b, pos0, d.layer[ly + 1].qkv_b);
+    rd_store_xn<D>(a, &sh.ab[0][0], P, b, pos0);
     return;
   }
   // ---- last layer: decoder on the last row, the draw, the next token
   rd_sync();
   const int pl = P - 1;
-  rd_layernorm<D>(&sh.xs[pl][0], &sh.ab[0][0], d.lnf_g, d.lnf_b, 1);
+  rd_layernorm<D>(&sh.xs[pl][0], &sh.ab[0][0], sh.vec + V::N1G, sh.vec + V::N1B, 1);
   // decoder heads as one product over the four e slices: column n < 3 M reads
   // mixture row n (slice n / M), the others type-head row n - 3 M (tanh slice)
   const int NH = 3 * M + K;
   rd_sync();
   fe.template mul<1>(&sh.ab[0][0], D, 1, [&](int, int nn, float acc) {
     const int slice = nn / D, c = nn - slice * D;
-    sh.eb[slice][c] = f2bf(slice < 3 ? acc : tanhf(acc + d.k1_b[c]));
+    sh.eb[slice][c] = f2bf(slice < 3 ? acc : tanhf(acc + sh.vec[V::K1B + c]));
   });
-  if (more) fq.load_packed(a.pk + rd_off_qkv<D, F>());   // the next token's layer-0 q, k, v
   rd_sync();
   fh.template mul<4>(&sh.eb[0][0], D, 4, [&](int r, int nn, float acc) {
-    if (nn < NH && r == (nn < 3 * M ? nn / M : 3)) sh.hv[nn] = acc + (nn < 3 * M ? d.mix_b[nn] : d.k2_b[nn - 3 * M]);
+    if (nn < NH && r == (nn < 3 * M ? nn / M : 3)) sh.hv[nn] = acc + sh.vec[nn < 3 * M ? V::MIXB + nn : V::K2B + nn - 3 * M];
   });
   rd_sync();
   if (wave == 0) {
@@ -553,12 +667,12 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   if (!more) return;   // workgroup-uniform
   rd_sync();
   // the drawn event is the next step's token, at position base + l + 1
-  rd_embed<D>(d, sh.xs[0], sh.tok_t, sh.tok_k);
+  rd_embed<D>(d, sh.vec + V::FREQ, sh.xs[0], sh.tok_t, sh.tok_k);
   rd_sync();
-  rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[0].ln1_g, d.layer[0].ln1_b, 1);
+  rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::L0G, sh.vec + V::L0B, 1);
   for (int i = tid; i < D; i += RD_ROW_THREADS) xg[i] = sh.xs[0][i];
   rd_sync();
-  rd_qkv<D, DH>(a, fq, &sh.ab[0][0], 1, 0, b, base + l + 1, d.layer[0].qkv_b);
+  rd_store_xn<D>(a, &sh.ab[0][0], 1, b, base + l + 1);
 }
 
 }  // namespace
@@ -587,7 +701,7 @@ void launch_draft_rows(RowDraftArgs a, hipStream_t st, const hipEvent_t *ev) {
     a.step = l;
     for (int ly = 0; ly < a.d.L; ++ly) {
       a.layer = ly;
-      hipExtLaunchKernelGGL(k_rd_attn<32>, dim3(a.S, H, B), dim3(256), 0, st, e0(), e1(), 0, a);
+      hipExtLaunchKernelGGL(k_rd_attn<128, 32>, dim3(a.S, H, B), dim3(256), 0, st, e0(), e1(), 0, a);
       ++j;
       hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, e0(), e1(), 0, a);
       ++j;

@@ -171,7 +171,7 @@ static_assert(RD_MAX_PART % RD_ROW_THREADS == 0, "partial staging: whole rounds 
 struct RowDraftArgs {
   DraftArgs d;              // model, cache, state and record pointers as for the one-launch draft
   float *x;                 // [B][2][d] residual stream of the step's rows
-  float *q;                 // [B][2][d] queries of the step's rows (bf16-rounded values)
+  bf16_t *xn;               // [B][2][d] the step's rows after the layer's LayerNorm (q, k, v input)
   float *part;              // [B][H][S][2][d_head + 2] split partials: maximum, sum, output sums
   const bf16_t *pk;         // per layer Wo, W1, W2, Wqkv in MFMA fragment order (launch_pack_frags)
   const bf16_t *pk_e;       // [E; V_k1] in fragment order
