@@ -114,17 +114,18 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
       b0 = *(const short4_t *)(kc + r0 * DH + 4 * g);
       b1 = *(const short4_t *)(kc + r1 * DH + 4 * g);
     }
-    // values of keys kt + 8 g .. + 7, columns 16 td + rr; positions past the
-    // key range are zeroed (never-written cache slots may hold NaN bits)
+    // values of keys kt + 8 g .. + 7, columns 16 td + rr; blocks past the key
+    // range read the range's last block (unconditional loads: a load under a
+    // lane condition makes the compiler wait for every load before it), and
+    // positions past the range are zeroed (never-written cache slots may hold
+    // NaN bits)
     const int k8 = kt + 8 * g, nv = k_end - k8;
+    const int k8c = min(k8, (k_end - 1) & ~7);
     uint4 vw[NDT];
 #pragma unroll
-    for (int td = 0; td < NDT; ++td) {
-      uint4 v = {0u, 0u, 0u, 0u};
-      if (interior || nv > 0) v = *(const uint4 *)(vc + kvbase * DH + (size_t)(k8 >> 3) * (8 * DH) + (16 * td + rr) * 8);
-      vw[td] = v;
-    }
-    if (!interior && nv > 0 && nv < 8) {
+    for (int td = 0; td < NDT; ++td)
+      vw[td] = *(const uint4 *)(vc + kvbase * DH + (size_t)(k8c >> 3) * (8 * DH) + (16 * td + rr) * 8);
+    if (!interior && nv < 8) {
 #pragma unroll
       for (int td = 0; td < NDT; ++td) {
         uint32_t w[4] = {vw[td].x, vw[td].y, vw[td].z, vw[td].w};
