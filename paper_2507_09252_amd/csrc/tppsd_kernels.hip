@@ -16,6 +16,7 @@
 #include <math.h>
 #include <stdlib.h>
 #include <stdint.h>
+#include <type_traits>
 
 #include "tppsd_device.h"
 #include "tppsd_philox.h"
@@ -2030,9 +2031,10 @@ int allow_draft_fused_lds(size_t bytes) {
 // Rounding points are those of the layered kernels.
 // ---------------------------------------------------------------------------
 // LDS floats of one wave's scratch for a model of width D, FFN width F, M
-// mixture components and K types
+// mixture components and K types (a multiple of 4: each wave's rows start on
+// a 16-byte boundary)
 inline __host__ __device__ int wave_draft_scratch_floats(int D, int F, int M, int K) {
-  return 2 * 32 + 2 * 32 + 2 * 32 + 2 * 32 + 2 * F + 4 * D + 3 * M + K + 4;
+  return (2 * 32 + 2 * 32 + 2 * 32 + 2 * 32 + 2 * F + 4 * D + 3 * M + K + 4 + 3) & ~3;
 }
 // elements of the transposed weight matrices staged in LDS, and the floats of
 // the small vectors
@@ -2040,7 +2042,7 @@ inline __host__ __device__ int wave_draft_weight_elems(int L, int D, int F, int 
   return L * (3 * D * D + D * D + D * F + F * D) + D * 4 * D + D * (3 * M + K);
 }
 inline __host__ __device__ int wave_draft_vec_floats(int L, int D, int F, int M, int K) {
-  return L * (9 * D + F) + 4 * D + 3 * M + K;
+  return (L * (9 * D + F) + 4 * D + 3 * M + K + 3) & ~3;
 }
 size_t wave_draft_lds_bytes(int L, int D, int F, int M, int K, int elt) {
   const size_t w = ((size_t)wave_draft_weight_elems(L, D, F, M, K) * elt + 15) / 16 * 16;
@@ -2048,9 +2050,9 @@ size_t wave_draft_lds_bytes(int L, int D, int F, int M, int K, int elt) {
 }
 
 // y[p][n] = sum_k WT[k][n] x[p][k] for n < N, p < P, handed to epi(p, n, y);
-// lane takes n = lane, lane + 64, ...
-template <typename ELT, typename XF, typename EPI>
-__device__ __forceinline__ void wave_gemv(const ELT *WT, int N, int KD, int P, XF xin, EPI epi) {
+// fp32 weights as WT [KD][N]; lane takes n = lane, lane + 64, ...
+template <int P, typename XF, typename EPI>
+__device__ __forceinline__ void wave_gemv(const float *WT, int N, int KD, XF xin, EPI epi) {
   const int lane = threadIdx.x & 63;
   for (int n = lane; n < N; n += 64) {
     float acc0 = 0.f, acc1 = 0.f;
@@ -2058,12 +2060,60 @@ __device__ __forceinline__ void wave_gemv(const ELT *WT, int N, int KD, int P, X
     // a few dot-product steps' loads in flight, not all of them (registers)
 #pragma unroll 8
     for (int k = 0; k < KD; ++k) {
-      const float w = ld(WT, (size_t)k * N + n);
+      const float w = WT[(size_t)k * N + n];
       acc0 += w * x0[k];
-      acc1 += w * x1[k];
+      if constexpr (P == 2) acc1 += w * x1[k];
     }
     epi(0, n, acc0);
-    if (P == 2) epi(1, n, acc1);
+    if constexpr (P == 2) epi(1, n, acc1);
+  }
+}
+
+// The same product in bf16: weights as [KD / 8][N] 16-byte octets (octet
+// (kq, n) holds W[n][8 kq .. 8 kq + 7]) and bf16 inputs, two products per
+// v_dot2c_f32_bf16 (each exact in fp32). Columns go 64 to a pass; a pass of at
+// most 32 columns splits the k range over the two halves of the wave and adds
+// the halves' sums. KD is a multiple of 16.
+__device__ __forceinline__ float dot2_bf(uint32_t w, uint32_t x, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, x), acc, false);
+}
+template <int P, typename XF, typename EPI>
+__device__ __forceinline__ void wave_gemv(const bf16_t *WT, int N, int KD, XF xin, EPI epi) {
+  const int lane = threadIdx.x & 63;
+  const uint4 *W = (const uint4 *)WT;
+  const int KQ = KD >> 3;
+  for (int n0 = 0; n0 < N; n0 += 64) {
+    const int rem = N - n0;
+    const bool split = rem <= 32;
+    const int c = split ? (lane & 31) : lane;
+    const int n = n0 + min(c, rem - 1);
+    const int q0 = split ? (lane >> 5) * (KQ >> 1) : 0, q1 = split ? q0 + (KQ >> 1) : KQ;
+    const uint4 *x0 = (const uint4 *)xin(n, 0), *x1 = (const uint4 *)xin(n, P - 1);
+    float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll 4
+    for (int kq = q0; kq < q1; ++kq) {
+      const uint4 w = W[(size_t)kq * N + n];
+      const uint4 xa = x0[kq];
+      acc0 = dot2_bf(w.x, xa.x, acc0);
+      acc0 = dot2_bf(w.y, xa.y, acc0);
+      acc0 = dot2_bf(w.z, xa.z, acc0);
+      acc0 = dot2_bf(w.w, xa.w, acc0);
+      if constexpr (P == 2) {
+        const uint4 xb = x1[kq];
+        acc1 = dot2_bf(w.x, xb.x, acc1);
+        acc1 = dot2_bf(w.y, xb.y, acc1);
+        acc1 = dot2_bf(w.z, xb.z, acc1);
+        acc1 = dot2_bf(w.w, xb.w, acc1);
+      }
+    }
+    if (split) {
+      acc0 += __shfl_xor(acc0, 32, 64);
+      if constexpr (P == 2) acc1 += __shfl_xor(acc1, 32, 64);
+    }
+    if (c < rem && (!split || lane < 32)) {
+      epi(0, n, acc0);
+      if constexpr (P == 2) epi(1, n, acc1);
+    }
   }
 }
 
@@ -2094,12 +2144,19 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
   float *vec = smw + ((size_t)wave_draft_weight_elems(L, D, F, M, K) * sizeof(ELT) + 15) / 16 * 4;
   float *scr = vec + wave_draft_vec_floats(L, D, F, M, K) + wave * wave_draft_scratch_floats(D, F, M, K);
   {
-    // W [N][Kd] (global) -> WT [Kd][N] (LDS)
+    // W [N][Kd] (global) -> LDS in the layout wave_gemv reads: fp32 as WT
+    // [Kd][N], bf16 as [Kd / 8][N] octets of 8 consecutive k
+    auto wt = [](int k, int n, int N) -> size_t {
+      if constexpr (sizeof(ELT) == 2)
+        return ((size_t)(k >> 3) * N + n) * 8 + (k & 7);
+      else
+        return (size_t)k * N + n;
+    };
     auto cpt = [&](ELT *dst, const void *src, int N, int Kd) {
       const ELT *sp = (const ELT *)src;
       for (int i = tid; i < N * Kd; i += blockDim.x) {
         const int n = i / Kd, k = i - n * Kd;
-        dst[(size_t)k * N + n] = sp[i];
+        dst[wt(k, n, N)] = sp[i];
       }
     };
     for (int ly = 0; ly < L; ++ly) {
@@ -2117,7 +2174,7 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
     const ELT *mw = (const ELT *)a.mix_w, *kw = (const ELT *)a.k2_w;
     for (int i = tid; i < NH * D; i += blockDim.x) {
       const int n = i / D, k = i - n * D;
-      hb[4 * D * D + (size_t)k * NH + n] = n < 3 * M ? mw[(size_t)n * D + k] : kw[(size_t)(n - 3 * M) * D + k];
+      hb[4 * D * D + wt(k, n, NH)] = n < 3 * M ? mw[(size_t)n * D + k] : kw[(size_t)(n - 3 * M) * D + k];
     }
     auto cp = [&](float *dst, const float *src, int cnt) {
       for (int i = tid; i < cnt; i += blockDim.x) dst[i] = src[i];
@@ -2148,14 +2205,22 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
   const float *hvec = vec + L * (9 * D + F);
   const float *lnf_g = hvec, *lnf_b = hvec + D, *k1_b = hvec + 2 * D, *mix_b = hvec + 3 * D,
               *k2_b = hvec + 3 * D + 3 * M, *freq = hvec + 3 * D + 3 * M + K;
-  // per-wave scratch: token rows of 32 floats
-  float *xs = scr;            // [2][32] residual stream
-  float *as = xs + 64;        // [2][32] LayerNorm output
-  float *qs = as + 64;        // [2][32] queries
-  float *os = qs + 64;        // [2][32] attention output
-  float *hs = os + 64;        // [2][F] FFN hidden
-  float *es = hs + 2 * F;     // [4D] decoder e | tanh
-  float *hv = es + 4 * D;     // [3M + K] decoder outputs
+  // per-wave scratch: token rows of 32 elements in slots of 32 floats; the
+  // rows the products read are in the weights' element type
+  using XT = typename std::conditional<sizeof(ELT) == 2, bf16_t, float>::type;
+  float *xs = scr;                         // [2][32] residual stream
+  XT *as = (XT *)(scr + 64);               // [2][32] LayerNorm output
+  float *qs = scr + 128;                   // [2][32] queries
+  XT *os = (XT *)(scr + 192);              // [2][32] attention output
+  XT *hs = (XT *)(scr + 256);              // [2][F] FFN hidden
+  XT *es = (XT *)(scr + 256 + 2 * F);      // [4D] decoder e | tanh
+  float *hv = scr + 256 + 2 * F + 4 * D;   // [3M + K] decoder outputs
+  auto gemv = [&](const ELT *W, int N, int KD, int P, auto xin, auto epi) {
+    if (P == 2)
+      wave_gemv<2>(W, N, KD, xin, epi);
+    else
+      wave_gemv<1>(W, N, KD, xin, epi);
+  };
   const int n = a.n[b], base = a.lenD[b];
   const uint64_t r = (uint64_t)a.rnd[b];
   const size_t seq_row0 = (size_t)b * H * a.cap;
@@ -2203,17 +2268,17 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
       ELT *kc = (ELT *)(a.kc + a.layer_bytes * ly);
       ELT *vc = (ELT *)(a.vc + a.layer_bytes * ly);
       // LayerNorm of each token over its D lanes
-      auto layernorm = [&](const float *g, const float *bt, float *dst, int np) {
+      auto layernorm = [&](const float *g, const float *bt, XT *dst, int np) {
         const float xv = (lj < D && lp < np) ? xs[lp * 32 + lj] : 0.f;
         const float mean = group_sum(xv, 32) / (float)D;
         const float c = (lj < D) ? xv - mean : 0.f;
         const float rstd = 1.f / sqrtf(group_sum(c * c, 32) / (float)D + 1e-5f);
-        if (lj < D && lp < np) dst[lp * 32 + lj] = rnd_act<ELT>(c * rstd * g[lj] + bt[lj]);
+        if (lj < D && lp < np) st<XT>(dst, lp * 32 + lj, rnd_act<ELT>(c * rstd * g[lj] + bt[lj]));
         wave_lds_sync();
       };
       layernorm(lv, lv + D, as, P);
       // q, k, v; keys and values of positions pos0 .. pos0 + P - 1 into the cache
-      wave_gemv<ELT>(wq, 3 * D, D, P, [&](int, int p) { return (const float *)(as + p * 32); },
+      gemv(wq, 3 * D, D, P, [&](int, int p) { return (const XT *)(as + p * 32); },
                      [&](int p, int nn, float acc) {
                        const float v = rnd_act<ELT>(acc + lv[2 * D + nn]);
                        const int which = nn / D, c = nn - which * D;
@@ -2337,18 +2402,18 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
         halve_step<1>(ow, (lane & 2) != 0, [](float v) { return dpp_mov<0x4E>(v); });
         const float oc = ow[0] + dpp_mov<0xB1>(ow[0]);
         const int c = 8 * ((lane >> 4) & 1) + 4 * ((lane >> 3) & 1) + 2 * ((lane >> 2) & 1) + ((lane >> 1) & 1);
-        if ((lane & 1) == 0 && (LPH == 32 || lane < 32)) os[p * 32 + hh * DH + c] = rnd_act<ELT>(lw > 0.f ? oc / lw : 0.f);
+        if ((lane & 1) == 0 && (LPH == 32 || lane < 32)) st<XT>(os, p * 32 + hh * DH + c, rnd_act<ELT>(lw > 0.f ? oc / lw : 0.f));
       }
       wave_lds_sync();
       // output projection + residual
-      wave_gemv<ELT>(wo, D, D, P, [&](int, int p) { return (const float *)(os + p * 32); },
+      gemv(wo, D, D, P, [&](int, int p) { return (const XT *)(os + p * 32); },
                      [&](int p, int nn, float acc) { xs[p * 32 + nn] += acc + lv[5 * D + nn]; });
       wave_lds_sync();
       layernorm(lv + 6 * D, lv + 7 * D, as, P);
-      wave_gemv<ELT>(w1, F, D, P, [&](int, int p) { return (const float *)(as + p * 32); },
-                     [&](int p, int nn, float acc) { hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + lv[8 * D + nn], 0.f)); });
+      gemv(w1, F, D, P, [&](int, int p) { return (const XT *)(as + p * 32); },
+                     [&](int p, int nn, float acc) { st<XT>(hs, p * F + nn, rnd_act<ELT>(fmaxf(acc + lv[8 * D + nn], 0.f))); });
       wave_lds_sync();
-      wave_gemv<ELT>(w2, D, F, P, [&](int, int p) { return (const float *)(hs + p * F); },
+      gemv(w2, D, F, P, [&](int, int p) { return (const XT *)(hs + p * F); },
                      [&](int p, int nn, float acc) { xs[p * 32 + nn] += acc + lv[8 * D + F + nn]; });
       wave_lds_sync();
     }
@@ -2359,16 +2424,16 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
       const float mean = group_sum(xv, 32) / (float)D;
       const float c = (lj < D) ? xv - mean : 0.f;
       const float rstd = 1.f / sqrtf(group_sum(c * c, 32) / (float)D + 1e-5f);
-      if (lj < D && lp == 0) as[lj] = rnd_act<ELT>(c * rstd * lnf_g[lj] + lnf_b[lj]);
+      if (lj < D && lp == 0) st<XT>(as, lj, rnd_act<ELT>(c * rstd * lnf_g[lj] + lnf_b[lj]));
       wave_lds_sync();
     }
     const ELT *we = wl + (size_t)L * LW, *wh = we + 4 * D * D;
-    wave_gemv<ELT>(we, 4 * D, D, 1, [&](int, int) { return (const float *)as; },
+    gemv(we, 4 * D, D, 1, [&](int, int) { return (const XT *)as; },
                    [&](int, int nn, float acc) {
-                     es[nn] = (nn < 3 * D) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * D]));
+                     st<XT>(es, nn, (nn < 3 * D) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * D])));
                    });
     wave_lds_sync();
-    wave_gemv<ELT>(wh, NH, D, 1, [&](int nn, int) { return (const float *)(es + (nn < 3 * M ? nn / M : 3) * D); },
+    gemv(wh, NH, D, 1, [&](int nn, int) { return (const XT *)(es + (nn < 3 * M ? nn / M : 3) * D); },
                    [&](int, int nn, float acc) { hv[nn] = acc + (nn < 3 * M ? mix_b[nn] : k2_b[nn - 3 * M]); });
     wave_lds_sync();
     {
