@@ -1281,8 +1281,15 @@ template <> __device__ __forceinline__ void load8<bf16_t>(const bf16_t *p, float
   }
 }
 
+// acc + w.lo x.lo + w.hi x.hi over two bf16 pairs (v_dot2c_f32_bf16; each
+// product is exact in fp32)
+__device__ __forceinline__ float dot2_bf(uint32_t w, uint32_t x, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, x), acc, false);
+}
+
 // y[p][n] = sum_k W(n)[k] X(n, p)[k] for n < N, p < P (P <= 2), handed to
-// epi(p, n, y) by one lane. K is cut into 8-element chunks; a row's chunks
+// epi(p, n, y) by one lane. bf16: the inputs X are bf16 rows too, and each
+// 8-element chunk is four v_dot2c over the raw pairs. K is cut into 8-element chunks; a row's chunks
 // are shared by LPR adjacent lanes (a power of two), CPL = K / (8 LPR) <= 8
 // chunks each, loaded together before any is used, so a product costs about
 // one memory latency plus a few lane-group additions. wrow(n) gives row n of
@@ -1295,20 +1302,39 @@ __device__ void wg_gemv_cpl(int N, int K, int P, WF wrow, XF xrow, EPI epi) {
   for (int r0 = 0; r0 < N; r0 += rows) {
     const int n = r0 + tid / lpr, nn = min(n, N - 1);
     const ELT *wr = wrow(nn);
-    float w[CPL][8];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) load8(wr + 8 * (sub + lpr * c), w[c]);
     float acc[2] = {0.f, 0.f};
-    for (int p = 0; p < P; ++p) {
-      const float *x = xrow(nn, p);
-      float a = 0.f;
+    if constexpr (sizeof(ELT) == 2) {
+      uint4 w[CPL];
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        const float *xc = x + 8 * (sub + lpr * c);
+      for (int c = 0; c < CPL; ++c) w[c] = *(const uint4 *)(wr + 8 * (sub + lpr * c));
+      for (int p = 0; p < P; ++p) {
+        const bf16_t *x = xrow(nn, p);
+        float a = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) a += w[c][e] * xc[e];
+        for (int c = 0; c < CPL; ++c) {
+          const uint4 xv = *(const uint4 *)(x + 8 * (sub + lpr * c));
+          a = dot2_bf(w[c].x, xv.x, a);
+          a = dot2_bf(w[c].y, xv.y, a);
+          a = dot2_bf(w[c].z, xv.z, a);
+          a = dot2_bf(w[c].w, xv.w, a);
+        }
+        acc[p] = group_sum(a, lpr);
       }
-      acc[p] = group_sum(a, lpr);
+    } else {
+      float w[CPL][8];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) load8(wr + 8 * (sub + lpr * c), w[c]);
+      for (int p = 0; p < P; ++p) {
+        const float *x = xrow(nn, p);
+        float a = 0.f;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          const float *xc = x + 8 * (sub + lpr * c);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) a += w[c][e] * xc[e];
+        }
+        acc[p] = group_sum(a, lpr);
+      }
     }
     if (n < N && sub == 0)
       for (int p = 0; p < P; ++p) epi(p, n, acc[p]);
@@ -1318,8 +1344,8 @@ __device__ void wg_gemv_cpl(int N, int K, int P, WF wrow, XF xrow, EPI epi) {
 constexpr int gemv_cpl(int K) { return (K >> 3) < 8 ? (K >> 3) : 8; }
 
 // LayerNorm of P <= 4 rows of x (stride d) into y (stride d), wave p per row
-template <typename ELT>
-__device__ void wg_layernorm(const float *x, float *y, const float *g, const float *bt, int P, int d) {
+template <typename ELT, typename YT>
+__device__ void wg_layernorm(const float *x, YT *y, const float *g, const float *bt, int P, int d) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   if (wave >= P) return;
   const float *xr = x + wave * d;
@@ -1332,7 +1358,7 @@ __device__ void wg_layernorm(const float *x, float *y, const float *g, const flo
     v += c * c;
   }
   const float rstd = 1.f / sqrtf(wave_sum(v) / (float)d + 1e-5f);
-  for (int j = lane; j < d; j += 64) y[wave * d + j] = rnd_act<ELT>((xr[j] - mean) * rstd * g[j] + bt[j]);
+  for (int j = lane; j < d; j += 64) st<YT>(y, wave * d + j, rnd_act<ELT>((xr[j] - mean) * rstd * g[j] + bt[j]));
 }
 
 // One 32-key step of the draft attention's MFMA formulation (d_head = 16),
@@ -1393,8 +1419,8 @@ __device__ __forceinline__ void halve_step(float (&v)[16], bool hi, X xchg) {
   }
 }
 
-template <typename ELT, int QN>
-__device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
+template <typename ELT, int QN, typename OT>
+__device__ void wg_attention_valu(const float *qs, OT *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
                                   int H, int P, int pos0, int d, float *red) {
   // QN = P queries; with one query a thread's 4-key unit (keys and values in
   // registers) fits beside the rest of the kernel in fp32 too
@@ -1409,6 +1435,15 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
   for (int p = 0; p < QN; ++p)
 #pragma unroll
     for (int j = 0; j < DH; ++j) q[p][j] = qs[p * d + h * DH + j] * 0.25f;   // 1 / sqrt(16)
+  // bf16: the scaled queries (bf16 values, scaled by a power of two) as
+  // pairs for v_dot2c against the raw key words
+  uint32_t qw[QN][sizeof(ELT) == 2 ? DH / 2 : 1];
+  if constexpr (sizeof(ELT) == 2) {
+#pragma unroll
+    for (int p = 0; p < QN; ++p)
+#pragma unroll
+      for (int e = 0; e < DH / 2; ++e) qw[p][e] = pk2bf(q[p][2 * e], q[p][2 * e + 1]);
+  }
   float m[QN], l[QN], o[QN][DH];
 #pragma unroll
   for (int p = 0; p < QN; ++p) {
@@ -1476,11 +1511,25 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
       float a[QN];
 #pragma unroll
       for (int p = 0; p < QN; ++p) a[p] = 0.f;
+      if constexpr (sizeof(ELT) == 2) {
 #pragma unroll
-      for (int j = 0; j < DH; ++j) {
-        const float kv = kval(i, j);
+        for (int hv = 0; hv < 2; ++hv) {
+          const uint4 w = kr[2 * i + hv];   // columns 8 hv .. 8 hv + 7 of key i
 #pragma unroll
-        for (int p = 0; p < QN; ++p) a[p] += q[p][j] * kv;
+          for (int p = 0; p < QN; ++p) {
+            a[p] = dot2_bf(w.x, qw[p][4 * hv], a[p]);
+            a[p] = dot2_bf(w.y, qw[p][4 * hv + 1], a[p]);
+            a[p] = dot2_bf(w.z, qw[p][4 * hv + 2], a[p]);
+            a[p] = dot2_bf(w.w, qw[p][4 * hv + 3], a[p]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < DH; ++j) {
+          const float kv = kval(i, j);
+#pragma unroll
+          for (int p = 0; p < QN; ++p) a[p] += q[p][j] * kv;
+        }
       }
       const int pos = k0 + i;
 #pragma unroll
@@ -1559,7 +1608,7 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
       L += red[w * 36 + p * 18 + 1];
       O += red[w * 36 + p * 18 + 2 + j];
     }
-    os[p * d + hh * DH + j] = rnd_act<ELT>(L > 0.f ? O / L : 0.f);
+    st<OT>(os, p * d + hh * DH + j, rnd_act<ELT>(L > 0.f ? O / L : 0.f));
   }
 }
 
@@ -1573,8 +1622,8 @@ __device__ void wg_attention_valu(const float *qs, float *os, const ELT *kc, con
 // before computing any.
 // The waves of a head merge through LDS. red: LDS scratch of
 // max(4, H) * 2 * 18 floats.
-template <typename ELT, int DH, int QMAX = 2, int NB = 4>   // NB: steps per load batch
-__device__ void wg_attention(const float *qs, float *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
+template <typename ELT, int DH, int QMAX = 2, int NB = 4, typename OT = float>   // NB: steps per load batch
+__device__ void wg_attention(const float *qs, OT *os, const ELT *kc, const ELT *vc, size_t seq_row0, int cap,
                              int H, int P, int pos0, int ld, float *red) {
   static_assert(DH == 16, "the fused draft attention serves d_head = 16");
   constexpr int KT = 32;
@@ -1690,7 +1739,7 @@ __device__ void wg_attention(const float *qs, float *os, const ELT *kc, const EL
       L += r[1] * f;
       O += r[2 + j] * f;
     }
-    os[p * ld + hh * DH + j] = rnd_act<ELT>(L > 0.f ? O / L : 0.f);
+    st<OT>(os, p * ld + hh * DH + j, rnd_act<ELT>(L > 0.f ? O / L : 0.f));
   }
 }
 
@@ -1730,13 +1779,16 @@ __global__ __launch_bounds__(NT) void k_draft_fused(DraftArgs a) {
   __shared__ float pu[TPPSD_MAX_GAMMA][4];   // the draws' uniforms, one Philox block per step
   const int d = a.d, F = a.F, M = a.M, K = a.K, H = a.H;
   const int Fm = d > F ? d : F;
-  float *xs = sm;           // [2][d] residual stream
-  float *as = xs + 2 * d;   // [2][Fm] LayerNorm outputs
-  float *qs = as + 2 * Fm;  // [2][d] queries
-  float *os = qs + 2 * d;   // [2][d] attention outputs
-  float *hs = os + 2 * d;   // [2][F] FFN hidden
-  float *es = hs + 2 * F;   // [4d] decoder e | tanh activations
-  float *hv = es + 4 * d;   // [3M + K] decoder outputs
+  // the rows the matrix-vector products read are in the weights' element
+  // type (bf16 halves of their float slots)
+  using XT = typename std::conditional<sizeof(ELT) == 2, bf16_t, float>::type;
+  float *xs = sm;                            // [2][d] residual stream
+  XT *as = (XT *)(sm + 2 * d);               // [2][Fm] LayerNorm outputs
+  float *qs = sm + 2 * d + 2 * Fm;           // [2][d] queries
+  XT *os = (XT *)(qs + 2 * d);               // [2][d] attention outputs
+  XT *hs = (XT *)(qs + 4 * d);               // [2][F] FFN hidden
+  XT *es = (XT *)(qs + 4 * d + 2 * F);       // [4d] decoder e | tanh activations
+  float *hv = qs + 8 * d + 2 * F;            // [3M + K] decoder outputs
   float *red = hv + 3 * M + K + 8;   // attention merge scratch
   float *vec = red + fused_draft_red_floats(H, DH);   // staged small vectors
   const int b = blockIdx.x, tid = threadIdx.x;
@@ -1846,7 +1898,7 @@ __global__ __launch_bounds__(NT) void k_draft_fused(DraftArgs a) {
       lds_barrier();
       const ELT *wq = wmat(w.qkv_w, ly * LS);
       wg_gemv_cpl<ELT, CD>(
-          3 * d, d, P, [&](int nn) { return wq + (size_t)nn * ldd; }, [&](int, int p) { return as + p * d; },
+          3 * d, d, P, [&](int nn) { return wq + (size_t)nn * ldd; }, [&](int, int p) { return (const XT *)(as + p * d); },
           [&](int p, int nn, float acc) {
             const float v = rnd_act<ELT>(acc + qkv_b[nn]);
             const int which = nn / d, c = nn - which * d;
@@ -1863,14 +1915,14 @@ __global__ __launch_bounds__(NT) void k_draft_fused(DraftArgs a) {
           });
       __syncthreads();   // keys and values in the cache before the attention reads them
       if (H <= 4)
-        P == 2 ? wg_attention_valu<ELT, 2>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red)
-               : wg_attention_valu<ELT, 1>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
+        P == 2 ? wg_attention_valu<ELT, 2, XT>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red)
+               : wg_attention_valu<ELT, 1, XT>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       else
-        wg_attention<ELT, DH>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
+        wg_attention<ELT, DH, 2, 4, XT>(qs, os, kc, vc, seq_row0, a.cap, H, P, pos0, d, red);
       lds_barrier();
       const ELT *wo = wmat(w.out_w, ly * LS + o_out);
       wg_gemv_cpl<ELT, CD>(
-          d, d, P, [&](int nn) { return wo + (size_t)nn * ldd; }, [&](int, int p) { return os + p * d; },
+          d, d, P, [&](int nn) { return wo + (size_t)nn * ldd; }, [&](int, int p) { return (const XT *)(os + p * d); },
           [&](int p, int nn, float acc) { xs[p * d + nn] += acc + out_b[nn]; });
       lds_barrier();
       wg_layernorm<ELT>(xs, as, ln2_g, ln2_b, P, d);
@@ -1878,11 +1930,11 @@ __global__ __launch_bounds__(NT) void k_draft_fused(DraftArgs a) {
       const ELT *w1 = wmat(w.ffn1_w, ly * LS + o_f1);
       const ELT *w2 = wmat(w.ffn2_w, ly * LS + o_f2);
       wg_gemv_cpl<ELT, CD>(
-          F, d, P, [&](int nn) { return w1 + (size_t)nn * ldd; }, [&](int, int p) { return as + p * d; },
-          [&](int p, int nn, float acc) { hs[p * F + nn] = rnd_act<ELT>(fmaxf(acc + ffn1_b[nn], 0.f)); });
+          F, d, P, [&](int nn) { return w1 + (size_t)nn * ldd; }, [&](int, int p) { return (const XT *)(as + p * d); },
+          [&](int p, int nn, float acc) { st<XT>(hs, p * F + nn, rnd_act<ELT>(fmaxf(acc + ffn1_b[nn], 0.f))); });
       lds_barrier();
       wg_gemv_cpl<ELT, CF>(
-          d, F, P, [&](int nn) { return w2 + (size_t)nn * ldf; }, [&](int, int p) { return hs + p * F; },
+          d, F, P, [&](int nn) { return w2 + (size_t)nn * ldf; }, [&](int, int p) { return (const XT *)(hs + p * F); },
           [&](int p, int nn, float acc) { xs[p * d + nn] += acc + ffn2_b[nn]; });
       lds_barrier();
     }
@@ -1893,9 +1945,9 @@ __global__ __launch_bounds__(NT) void k_draft_fused(DraftArgs a) {
     lds_barrier();
     const ELT *we = wmat(a.Ek1_w, a.L * LS);
     wg_gemv_cpl<ELT, CD>(
-        4 * d, d, 1, [&](int nn) { return we + (size_t)nn * ldd; }, [&](int, int) { return (const float *)as; },
+        4 * d, d, 1, [&](int nn) { return we + (size_t)nn * ldd; }, [&](int, int) { return (const XT *)as; },
         [&](int, int nn, float acc) {
-          es[nn] = (nn < 3 * d) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * d]));
+          st<XT>(es, nn, (nn < 3 * d) ? rnd_act<ELT>(acc) : rnd_act<ELT>(tanhf(acc + k1_b[nn - 3 * d])));
         });
     lds_barrier();
     const ELT *mw = wmat(a.mix_w, a.L * LS + o_mix);
@@ -1903,7 +1955,7 @@ __global__ __launch_bounds__(NT) void k_draft_fused(DraftArgs a) {
     wg_gemv_cpl<ELT, CD>(
         3 * M + K, d, 1,
         [&](int nn) { return nn < 3 * M ? mw + (size_t)nn * ldd : kw + (size_t)(nn - 3 * M) * ldd; },
-        [&](int nn, int) { return (const float *)(es + (nn < 3 * M ? nn / M : 3) * d); },
+        [&](int nn, int) { return (const XT *)(es + (nn < 3 * M ? nn / M : 3) * d); },
         [&](int, int nn, float acc) { hv[nn] = acc + (nn < 3 * M ? mix_b[nn] : k2_b[nn - 3 * M]); });
     lds_barrier();
     if (tid < 64) {
@@ -2074,9 +2126,6 @@ __device__ __forceinline__ void wave_gemv(const float *WT, int N, int KD, XF xin
 // v_dot2c_f32_bf16 (each exact in fp32). Columns go 64 to a pass; a pass of at
 // most 32 columns splits the k range over the two halves of the wave and adds
 // the halves' sums. KD is a multiple of 16.
-__device__ __forceinline__ float dot2_bf(uint32_t w, uint32_t x, float acc) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, x), acc, false);
-}
 template <int P, typename XF, typename EPI>
 __device__ __forceinline__ void wave_gemv(const bf16_t *WT, int N, int KD, XF xin, EPI epi) {
   const int lane = threadIdx.x & 63;
