@@ -33,6 +33,12 @@ __device__ __forceinline__ uint32_t pk2bf(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, (bf16x2_t){(__bf16)lo, (__bf16)hi});
 }
 
+// acc + w.lo x.lo + w.hi x.hi over two packed bf16 pairs (v_dot2c_f32_bf16;
+// each product is exact in fp32)
+__device__ __forceinline__ float dot2_bf(uint32_t w, uint32_t x, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, x), acc, false);
+}
+
 template <typename T> __device__ __forceinline__ float ld(const T *p, size_t i);
 template <> __device__ __forceinline__ float ld<float>(const float *p, size_t i) { return p[i]; }
 template <> __device__ __forceinline__ float ld<bf16_t>(const bf16_t *p, size_t i) { return bf2f(p[i]); }

@@ -125,7 +125,8 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
   }
   if (tid < 2 * D / 8) *(uint4 *)(&xl[0][0] + 8 * tid) = xw;
   __syncthreads();
-  // dot products of a weight row slice with a row's slice, fp32 over bf16
+  // dot products of a weight row slice with a row's slice: v_dot2c over
+  // the raw bf16 pairs (products exact in fp32)
   auto dot16 = [&](const uint4 (&w)[NC][2], int p) {
     float acc = 0.f;
 #pragma unroll
@@ -133,13 +134,10 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
 #pragma unroll
       for (int hlf = 0; hlf < 2; ++hlf) {
         const uint4 xx = *(const uint4 *)(&xl[p][0] + 128 * c + 16 * j8 + 8 * hlf);
-        const uint32_t ww[4] = {w[c][hlf].x, w[c][hlf].y, w[c][hlf].z, w[c][hlf].w};
-        const uint32_t xv[4] = {xx.x, xx.y, xx.z, xx.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc += __uint_as_float(ww[e] << 16) * __uint_as_float(xv[e] << 16);
-          acc += __uint_as_float(ww[e] & 0xFFFF0000u) * __uint_as_float(xv[e] & 0xFFFF0000u);
-        }
+        acc = dot2_bf(w[c][hlf].x, xx.x, acc);
+        acc = dot2_bf(w[c][hlf].y, xx.y, acc);
+        acc = dot2_bf(w[c][hlf].z, xx.z, acc);
+        acc = dot2_bf(w[c][hlf].w, xx.w, acc);
       }
     return group_sum(acc, 8);
   };
@@ -161,11 +159,12 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
     }
   }
   __syncthreads();
-  float q[2][8];
+  // the lane's 8 query elements (bf16 values) as pairs for v_dot2c
+  uint32_t q[2][4];
 #pragma unroll
   for (int p = 0; p < 2; ++p)
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) q[p][jj] = qs[p][8 * seg + jj];
+    for (int e = 0; e < 4; ++e) q[p][e] = pk2bf(qs[p][8 * seg + 2 * e], qs[p][8 * seg + 2 * e + 1]);
   // the owned new positions' keys and values replace what the loads read
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
@@ -197,13 +196,9 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NKL; ++i) {
-      const uint32_t w[4] = {kr[i][0], kr[i][1], kr[i][2], kr[i][3]};
       float dot = 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        dot += q[p][2 * e] * __uint_as_float(w[e] << 16);
-        dot += q[p][2 * e + 1] * __uint_as_float(w[e] & 0xFFFF0000u);
-      }
+      for (int e = 0; e < 4; ++e) dot = dot2_bf(kr[i][e], q[p][e], dot);
       dot += dpp_mov<0xB1>(dot);                 // lane ^ 1
       if (SEG == 4) dot += dpp_mov<0x4E>(dot);   // lane ^ 2
       const int pos = k0 + i * KPI + tid / SEG;

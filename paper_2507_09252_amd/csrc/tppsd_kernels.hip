@@ -1281,12 +1281,6 @@ template <> __device__ __forceinline__ void load8<bf16_t>(const bf16_t *p, float
   }
 }
 
-// acc + w.lo x.lo + w.hi x.hi over two bf16 pairs (v_dot2c_f32_bf16; each
-// product is exact in fp32)
-__device__ __forceinline__ float dot2_bf(uint32_t w, uint32_t x, float acc) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w), __builtin_bit_cast(bf16x2_t, x), acc, false);
-}
-
 // y[p][n] = sum_k W(n)[k] X(n, p)[k] for n < N, p < P (P <= 2), handed to
 // epi(p, n, y) by one lane. bf16: the inputs X are bf16 rows too, and each
 // 8-element chunk is four v_dot2c over the raw pairs. K is cut into 8-element chunks; a row's chunks
