@@ -17,6 +17,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -114,24 +115,29 @@ def draft_kernel_bytes(wl, B, gamma, ctx):
 def draft_attn_bytes(wl, B, gamma, ctx):
     """Row drafting's split attention, one launch (one draft layer, one
     step): the layer's cached keys and values up to the step's position (the
-    run-average context plus half a round's drafts), read once, the queries
-    read and the partials written (one row each)."""
+    run-average context plus half a round's drafts), read once; the layer's
+    q, k, v matrices; the step's LayerNorm'd rows in; the new keys and values
+    appended; and each 512-key split's (max, sum, d_head sums) out. Token rows
+    per step average (gamma + 1) / gamma (two in a round's first step)."""
     c = wl.draft
     keys = ctx + gamma / 2.0
-    return float(B * c.n_heads * keys * c.d_head * 2 * _elt(c) + 2 * B * 2 * c.d_model * 4)
+    rows = (gamma + 1.0) / gamma
+    splits = math.ceil(keys / 512.0)
+    e = _elt(c)
+    return float(B * c.n_heads * keys * c.d_head * 2 * e + 3 * c.d_model * c.d_model * e
+                 + B * rows * c.d_model * e + B * rows * 2 * c.d_model * e
+                 + B * c.n_heads * splits * rows * (c.d_head + 2) * 4)
 
 
 def draft_rows_bytes(wl, B, gamma):
     """Row drafting's row launch, averaged over a round's 1 + L gamma
     launches: the matrices the round's row launches read, each launch's once
-    (step 0: layer-0 q, k, v; per step and layer: output projection and FFN,
-    then the next layer's q, k, v or, after the last layer, the decoder and --
-    except in the last step -- layer-0 q, k, v), and the residual rows in and
-    out."""
+    (per step and layer the output projection and FFN; after the last layer
+    also the decoder; the step-0 launch only embeds), and the residual rows in
+    and out."""
     c = wl.draft
     d, F, L = c.d_model, c.d_ffn, c.n_layers
-    per_step = L * (d * d + 2 * d * F) + (L - 1) * 3 * d * d + _decoder_elems(c)
-    elems = 3 * d * d + gamma * per_step + (gamma - 1) * 3 * d * d
+    elems = gamma * (L * (d * d + 2 * d * F) + _decoder_elems(c))
     launches = 1 + L * gamma
     return float(elems * _elt(c) / launches + 2 * B * 2 * d * 4)
 
