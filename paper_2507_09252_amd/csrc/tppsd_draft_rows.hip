@@ -3,16 +3,17 @@
 //
 // Each draft step runs two launches per layer:
 //  - k_rd_attn: the step's queries (two in the first step, which re-encodes
-//    the last two committed events, one after) against the draft KV cache,
-//    split over (key range, head, sequence) workgroups so that the cache
-//    streams through the whole chip; each split leaves its running maximum,
-//    sum and unnormalised output;
+//    the last two committed events, one after), formed in the launch from the
+//    step's LayerNorm'd rows, against the draft KV cache, split over (key
+//    range, head, sequence) workgroups so that the cache streams through the
+//    whole chip; the split holding the step's new position also forms and
+//    appends its key and value; each split leaves its running maximum, sum
+//    and unnormalised output;
 //  - k_rd_rows: one workgroup per sequence merges the splits and runs every
 //    row-local step up to the next attention -- output projection and
-//    residual, the feed-forward block, then the next layer's LayerNorm and
-//    q, k, v (keys and values appended to the cache); after the last layer
-//    the decoder, the draft record, the draw, and the drawn event's
-//    embedding and layer-0 q, k, v for the next step.
+//    residual, the feed-forward block, then the next layer's LayerNorm; after
+//    the last layer the decoder, the draft record, the draw, and the drawn
+//    event's embedding and layer-0 LayerNorm for the next step.
 // The matrix-vector products of a sequence's one or two rows run on MFMA
 // 16-row tiles (rows past the token count are zero operands) with every weight
 // fragment of a product in flight at once, and the next product's fragments
@@ -410,6 +411,7 @@ struct RdShared {
   float hv[128];                                       // decoder outputs
   float part[RD_MAX_PART];                             // the sequence's split partials
   float vec[RD_VEC];                                   // the launch's biases and LayerNorm parameters (rd_vec_*)
+  __attribute__((aligned(16))) bf16_t temb[RD_MAX_TYPES * D];   // last layer: every type's embedding row
   float tok_t;
   int tok_k;
 };
@@ -424,14 +426,16 @@ __device__ __forceinline__ void rd_store_xn(const RowDraftArgs &a, const bf16_t 
   if (tid == 0 && pos0 + np > a.d.cap) atomicOr(a.d.status, TPPSD_STATUS_CAPACITY);
 }
 
-// the THP embedding (sin / cos time encoding + type row) of event (t, k) into row p
+// the THP embedding (sin / cos time encoding + type row) of event (t, k) into
+// row p; the type rows [K][D] from temb (memory or an LDS copy)
 template <int D>
-__device__ __forceinline__ void rd_embed(const DraftArgs &d, const float *freq, float *xrow, float t, int k) {
+__device__ __forceinline__ void rd_embed(const DraftArgs &d, const float *freq, const bf16_t *temb, float *xrow,
+                                         float t, int k) {
   const int tid = threadIdx.x;
   if (tid < D) {
     const float arg = t * freq[tid];
     const int kk = min(max(k, 0), d.K - 1);
-    xrow[tid] = ((tid & 1) ? cosf(arg) : sinf(arg)) + bf2f(((const bf16_t *)d.type_emb)[(size_t)kk * D + tid]);
+    xrow[tid] = ((tid & 1) ? cosf(arg) : sinf(arg)) + bf2f(temb[(size_t)kk * D + tid]);
   }
 }
 
@@ -448,8 +452,8 @@ template <int D, int F> struct RdVec {
   static_assert(END <= RD_VEC, "vector area");
 };
 
-// Launch modes: step 0 embeds the last two committed events and computes
-// their layer-0 q, k, v; step l >= 1, layer ly finishes layer ly of the step's
+// Launch modes: step 0 embeds the last two committed events and normalises
+// them for layer 0; step l >= 1, layer ly finishes layer ly of the step's
 // rows after its attention.
 template <int D, int F, int DH>
 __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
@@ -458,13 +462,14 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   const DraftArgs &d = a.d;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int done = d.done[b], base = d.lenD[b], n = d.n[b];   // loaded together
+  const uint64_t rnd = (uint64_t)d.rnd[b];                    // (the draw's round counter, read with them)
   if (done) return;
   const int L = d.L, M = d.M, K = d.K;
   float *xg = a.x + (size_t)b * 2 * D;
   if (a.step == 0) {
     for (int p = 0; p < 2; ++p) {
       const size_t i = (size_t)b * d.ev_stride + n - 2 + p;
-      rd_embed<D>(d, d.freq, sh.xs[p], d.ev_t[i], d.ev_k[i]);
+      rd_embed<D>(d, d.freq, (const bf16_t *)d.type_emb, sh.xs[p], d.ev_t[i], d.ev_k[i]);
     }
     rd_sync();
     rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[0].ln1_g, d.layer[0].ln1_b, 2);
@@ -478,11 +483,11 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   const int pos0 = base + (l == 1 ? 0 : l);
   const FusedLayerW &w = d.layer[ly];
   const bool last = ly == L - 1;
-  // every load of the launch in flight at once, in the order of use: the
-  // split partials of the sequence (all splits of the slab; those past the
-  // step's keys are ignored below) and the residual rows, the output
-  // projection and the first FFN product, then the next layer's q, k, v or
-  // the decoder, into registers; the second FFN product straight into LDS
+  // every load of the launch in flight at once, in the order of use, into
+  // registers: the split partials of the sequence (all splits of the slab;
+  // those past the step's keys are ignored below), the residual rows and the
+  // small vectors, then the output projection and both FFN products (after
+  // the last layer the decoder's follow once the first FFN product is done)
   constexpr int NPV = RD_MAX_PART / RD_ROW_THREADS;
   float pv[NPV];
   {
@@ -526,6 +531,10 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   f2.load_packed(wl + D * D + F * D);
   RdFrags<4 * D, D> fe;
   RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
+  // last layer: the time the drawn interval is added to (the last committed
+  // event, or the previous draft), read now rather than behind the decoder
+  float tprev = 0.f;
+  if (last) tprev = l == 1 ? d.ev_t[(size_t)b * d.ev_stride + n - 1] : d.d_t[(size_t)b * d.MG + (l - 2)];
   // (keeps the stores below, which wait for the partials, behind every load)
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -566,7 +575,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   f1.template mul<2>(&sh.ab[0][0], D, P, [&](int p, int nn, float acc) {
     if (p < P) sh.hb[p][nn] = f2bf(fmaxf(acc + sh.vec[V::F1B + nn], 0.f));
   });
-  // the first product's registers are free: the next layer's q, k, v, or the decoder
+  // the first product's registers are free: after the last layer, the decoder's fragments
   const bool more = l < d.gamma;
   if (last) {
     fe.load_packed(a.pk_e);
@@ -596,6 +605,17 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     const int slice = nn / D, c = nn - slice * D;
     sh.eb[slice][c] = f2bf(slice < 3 ? acc : tanhf(acc + sh.vec[V::K1B + c]));
   });
+  // every type's embedding row for the drawn event, in the first decoder
+  // product's freed registers (16-byte vectors, indices clamped into the
+  // table's K D / 8), to LDS after the draw
+  constexpr int NTE = RD_MAX_TYPES * D / 8 / RD_ROW_THREADS;
+  static_assert(NTE * RD_ROW_THREADS * 8 == RD_MAX_TYPES * D, "type rows over the workgroup");
+  uint4 te[NTE];
+  {
+    const int nvec = K * D / 8;
+#pragma unroll
+    for (int i = 0; i < NTE; ++i) te[i] = *((const uint4 *)d.type_emb + min(tid + i * RD_ROW_THREADS, nvec - 1));
+  }
   rd_sync();
   fh.template mul<4>(&sh.eb[0][0], D, 4, [&](int r, int nn, float acc) {
     if (nn < NH && r == (nn < 3 * M ? nn / M : 3)) sh.hv[nn] = acc + sh.vec[nn < 3 * M ? V::MIXB + nn : V::K2B + nn - 3 * M];
@@ -618,7 +638,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     if (lane < K) d.d_logtype[di * K + lane] = logk;
     const bool bad = (lane < M && !(isfinite(logw) && isfinite(mu) && isfinite(sg))) || (lane < K && !isfinite(logk));
     float u[4];
-    philox_uniforms(d.seed, (uint64_t)b, (uint64_t)d.rnd[b], (uint64_t)l, TAG_DRAFT, u);
+    philox_uniforms(d.seed, (uint64_t)b, rnd, (uint64_t)l, TAG_DRAFT, u);
     // categorical over the lanes' log-probabilities: first index whose
     // running sum of exp exceeds u times the total
     auto draw = [&](float lp, int cnt, float uu) {
@@ -647,7 +667,6 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     const float lf = __shfl(logk, kk, 64);
     const bool bad_any = __ballot(bad) != 0ull;
     if (lane == 0) {
-      const float tprev = l == 1 ? d.ev_t[(size_t)b * d.ev_stride + n - 1] : d.d_t[di - 1];
       const float tn = tprev + tau;
       d.d_tau[di] = tau;
       d.d_t[di] = tn;
@@ -660,9 +679,11 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     }
   }
   if (!more) return;   // workgroup-uniform
+#pragma unroll
+  for (int i = 0; i < NTE; ++i) *((uint4 *)sh.temb + tid + i * RD_ROW_THREADS) = te[i];
   rd_sync();
   // the drawn event is the next step's token, at position base + l + 1
-  rd_embed<D>(d, sh.vec + V::FREQ, sh.xs[0], sh.tok_t, sh.tok_k);
+  rd_embed<D>(d, sh.vec + V::FREQ, sh.temb, sh.xs[0], sh.tok_t, sh.tok_k);
   rd_sync();
   rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::L0G, sh.vec + V::L0B, 1);
   for (int i = tid; i < D; i += RD_ROW_THREADS) xg[i] = sh.xs[0][i];
@@ -674,7 +695,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
 
 bool row_draft_ok(int bf16, int L, int d, int H, int F, int M, int K, int kv_cap) {
   return bf16 && L >= 1 && L <= FD_MAX_LAYERS && d == 128 && H == 4 && F == 512 && M >= 1 && M <= 64 && K >= 1 &&
-         K <= 64 && 3 * M + K <= 128 && (size_t)H * rd_splits(kv_cap) * 2 * (32 + 2) <= (size_t)RD_MAX_PART;
+         K <= RD_MAX_TYPES && 3 * M + K <= 128 && (size_t)H * rd_splits(kv_cap) * 2 * (32 + 2) <= (size_t)RD_MAX_PART;
 }
 
 void launch_pack_rd_head(const void *mix_w, const void *k2_w, int M, int K, int D, void *out, hipStream_t st) {

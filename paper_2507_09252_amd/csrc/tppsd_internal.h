@@ -163,6 +163,8 @@ constexpr size_t LDS_PER_WG = 160 * 1024;
 // heads of 32, d_ffn = 512.
 constexpr int RD_KEYS = 512;
 constexpr int RD_ROW_THREADS = 512;
+// event types whose embedding rows the row kernel stages in LDS (all of them)
+constexpr int RD_MAX_TYPES = 32;
 // floats of one sequence's split partials the row kernel stages in LDS
 // (H S 2 (d_head + 2): 4 heads of 32 over 8192 positions take 4352; a
 // multiple of RD_ROW_THREADS)
