@@ -30,13 +30,16 @@ __device__ __forceinline__ void sink_adjust(float &M, float &L, float &O) {
 }
 
 // bf16 causal attention on MFMA with split keys (flash-decoding style).
-// Grid (B * H, 1, splits), 4 waves per workgroup; the workgroup serves all
-// QT query tiles of 16 of its (sequence, head), so each key and value is read
-// from memory once per split whatever the number of queries. A split owns a
-// contiguous key range; its waves take 32-key steps round robin and keep
-// their own online-softmax state per query tile, merged in LDS at the end.
+// Grid (B * H, 1, splits), NW = 4 or 8 waves per workgroup; the workgroup
+// serves all QT query tiles of 16 of its (sequence, head), so each key and
+// value is read from memory once per split whatever the number of queries. A
+// split owns a contiguous key range; its waves take 32-key steps round robin
+// and keep their own online-softmax state per query tile, merged in LDS at
+// the end (with eight waves, waves 4..7 first hand theirs to waves 0..3).
 // With one split the merged result is the output, otherwise the split writes
-// (max, sum, unnormalised output) and k_attn_combine merges.
+// (max, sum, unnormalised output) and k_attn_combine merges. Eight waves and
+// one split replace two splits of four waves: the same waves stream the keys,
+// and the merge launch goes away.
 //
 // Per 32-key step and query tile, S^T = K Q^T is two 16x16 MFMA tiles whose
 // rows are permuted so that lane l ends up holding the scores of query
@@ -44,13 +47,14 @@ __device__ __forceinline__ void sink_adjust(float &M, float &L, float &O) {
 // operand of O^T = V^T P^T. The A operand (8 consecutive keys of one value
 // column) is one 16-byte load from the position-blocked value cache.
 
-template <int DH, int ROLE, int QT>
-__global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q, const bf16_t *__restrict__ kc,
+template <int DH, int ROLE, int QT, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void k_attn_mfma(const bf16_t *__restrict__ q, const bf16_t *__restrict__ kc,
                                                    const bf16_t *__restrict__ vc, bf16_t *__restrict__ o,
                                                    const int32_t *__restrict__ start, int start_off,
                                                    const int32_t *__restrict__ done, int P, int H, int cap,
                                                    int splits, float *__restrict__ part, int sink) {
   constexpr int KT = 32, NDT = DH / 16, NC = DH >= 32 ? DH / 32 : 1, NQ = 16 * QT;
+  static_assert(NW == 4 || NW == 8, "four or eight waves");
   __shared__ float red_m[4][NQ], red_l[4][NQ];
   __shared__ float red_o[4][DH][NQ + 1];
   const int bh = blockIdx.x, b = bh / H, h = bh - b * H, split = blockIdx.z;
@@ -99,7 +103,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
   // permuted key rows of the two S^T halves loaded by this lane
   const int krow0 = 8 * (rr >> 2) + (rr & 3), krow1 = krow0 + 4;
 
-  for (int kt = k_begin + wave * KT; kt < k_end; kt += 4 * KT) {
+  for (int kt = k_begin + wave * KT; kt < k_end; kt += NW * KT) {
     const bool interior = kt + KT <= k_end && kt + KT <= base + 1;   // every key visible to every query
     const size_t r0 = kvbase + min(kt + krow0, cap - 1), r1 = kvbase + min(kt + krow1, cap - 1);
     bf16x8_t a0[NC], a1[NC];
@@ -194,20 +198,58 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const bf16_t *__restrict__ q,
             __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, vw[td]), pb, oacc[t][td], 0, 0, 0);
     }
   }
-  // merge the four waves: lane (rr, g) holds O^T[16 td + 4 g + i][query 16 t + rr]
+  // lane (rr, g) holds O^T[16 td + 4 g + i][query 16 t + rr]
+  if constexpr (NW == 8) {
+    // waves 4..7 hand their state to waves 0..3 (same lane layout), which
+    // fold it into theirs
+    if (wave >= 4) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        if (g == 0) {
+          red_m[wave - 4][16 * t + rr] = m_run[t];
+          red_l[wave - 4][16 * t + rr] = lacc[t][0];
+        }
+#pragma unroll
+        for (int td = 0; td < NDT; ++td)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) red_o[wave - 4][16 * td + 4 * g + i][16 * t + rr] = oacc[t][td][i];
+      }
+    }
+    __syncthreads();
+    if (wave < 4) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        const float mp = red_m[wave][16 * t + rr], lp = red_l[wave][16 * t + rr];
+        const float mn = fmaxf(m_run[t], mp);
+        const float fs = (m_run[t] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run[t] - mn);
+        const float fp = (mp == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mp - mn);
+        m_run[t] = mn;
+        lacc[t][0] = lacc[t][0] * fs + lp * fp;
+#pragma unroll
+        for (int td = 0; td < NDT; ++td)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            oacc[t][td][i] = oacc[t][td][i] * fs + red_o[wave][16 * td + 4 * g + i][16 * t + rr] * fp;
+      }
+    }
+    __syncthreads();
+  }
+  // merge the (first) four waves
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    if (g == 0) {
-      red_m[wave][16 * t + rr] = m_run[t];
-      red_l[wave][16 * t + rr] = lacc[t][0];
+    if (wave < 4) {
+      if (g == 0) {
+        red_m[wave][16 * t + rr] = m_run[t];
+        red_l[wave][16 * t + rr] = lacc[t][0];
+      }
+#pragma unroll
+      for (int td = 0; td < NDT; ++td)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red_o[wave][16 * td + 4 * g + i][16 * t + rr] = oacc[t][td][i];
     }
-#pragma unroll
-    for (int td = 0; td < NDT; ++td)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) red_o[wave][16 * td + 4 * g + i][16 * t + rr] = oacc[t][td][i];
   }
   __syncthreads();
-  for (int idx = threadIdx.x; idx < NQ * DH; idx += 256) {
+  for (int idx = threadIdx.x; idx < NQ * DH; idx += 64 * NW) {
     const int qq = idx / DH, j = idx - qq * DH;
     if (qq >= P) continue;
     float M = -INFINITY;
@@ -442,20 +484,29 @@ static void attn_mfma(const ACT *Q, const ACT *Kc, const ACT *Vc, ACT *O, const 
                       const int32_t *done, int B, int P, int H, int cap, float *part, int sink, hipEvent_t ev0,
                       hipEvent_t ev1, hipStream_t s) {
   const int qtiles = (P + 15) / 16;
-  const int splits = attn_splits(B, H, cap);
+  int splits = attn_splits(B, H, cap);
+  // bf16: two splits of four waves become one workgroup of eight
+  const bool eight = sizeof(ACT) == 2 && splits == 2;
+  if (eight) splits = 1;
   dim3 grid(B * H, 1, splits);
-  auto go = [&](auto kern) {
-    hipExtLaunchKernelGGL(kern, grid, dim3(256), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap,
+  auto go = [&](auto kern, int nt) {
+    hipExtLaunchKernelGGL(kern, grid, dim3(nt), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap,
                           splits, part, sink);
   };
   if constexpr (sizeof(ACT) == 2) {
-    if (qtiles == 1) go(k_attn_mfma<DH, ROLE, 1>);
-    else if (qtiles == 2) go(k_attn_mfma<DH, ROLE, 2>);
-    else go(k_attn_mfma<DH, ROLE, 3>);
+    if (eight) {
+      if (qtiles == 1) go(k_attn_mfma<DH, ROLE, 1, 8>, 512);
+      else if (qtiles == 2) go(k_attn_mfma<DH, ROLE, 2, 8>, 512);
+      else go(k_attn_mfma<DH, ROLE, 3, 8>, 512);
+    } else {
+      if (qtiles == 1) go(k_attn_mfma<DH, ROLE, 1>, 256);
+      else if (qtiles == 2) go(k_attn_mfma<DH, ROLE, 2>, 256);
+      else go(k_attn_mfma<DH, ROLE, 3>, 256);
+    }
   } else {
-    if (qtiles == 1) go(k_attn_mfma_f32<DH, ROLE, 1>);
-    else if (qtiles == 2) go(k_attn_mfma_f32<DH, ROLE, 2>);
-    else go(k_attn_mfma_f32<DH, ROLE, 3>);
+    if (qtiles == 1) go(k_attn_mfma_f32<DH, ROLE, 1>, 256);
+    else if (qtiles == 2) go(k_attn_mfma_f32<DH, ROLE, 2>, 256);
+    else go(k_attn_mfma_f32<DH, ROLE, 3>, 256);
   }
   if (splits > 1) {
     const int total = B * H * P * DH;

@@ -61,8 +61,9 @@ class Case:
 def small(name, B, n_hist=None, init="stress", mismatch=True, gamma=0):
     wl = W.WORKLOADS[name]
     tag = f"-g{gamma}" if gamma else ""
-    return Case(f"{name}-B{B}-{init}{'-mm' if mismatch else ''}{tag}", wl, B, n_hist or wl.n_hist, init, mismatch,
-                gamma)
+    hist = f"-h{n_hist}" if n_hist and n_hist != wl.n_hist else ""
+    return Case(f"{name}-B{B}{hist}-{init}{'-mm' if mismatch else ''}{tag}", wl, B, n_hist or wl.n_hist, init,
+                mismatch, gamma)
 
 
 def weights(case: Case):

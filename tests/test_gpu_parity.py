@@ -51,10 +51,14 @@ VERIFY_CASES = [
     small("c5", 9, init="bias"),
     small("c5", 5),
     # long histories over few (sequence, head) pairs: the key range is split
-    # across workgroups and the partials merged
+    # across workgroups and the partials merged (fp32; bf16 with four or more
+    # splits), or, where two bf16 splits would do, one workgroup of eight
+    # waves merges in LDS (c3: one query tile of d_head 32; c4: two of 64)
     small("c1", 2, n_hist=1100),
     small("c2", 2, n_hist=1100),
     small("c3", 1, n_hist=1100, init="bias"),
+    small("c4", 2, n_hist=1100, init="bias"),
+    small("c3", 1, n_hist=2100, init="bias"),
     # the c3 draft-length sweep (P = gamma + 1 = 2, 3, 6, 16, 21 verify positions)
 ] + [small("c3", 4, n_hist=40, init="bias", gamma=g) for g in (1, 2, 5, 15, 20)] + [
     # the largest draft length: 33 positions, three query tiles per (sequence, head)
