@@ -461,12 +461,11 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   __shared__ RdShared<D, F, DH> sh;
   const DraftArgs &d = a.d;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int done = d.done[b], base = d.lenD[b], n = d.n[b];   // loaded together
-  const uint64_t rnd = (uint64_t)d.rnd[b];                    // (the draw's round counter, read with them)
-  if (done) return;
   const int L = d.L, M = d.M, K = d.K;
   float *xg = a.x + (size_t)b * 2 * D;
   if (a.step == 0) {
+    const int done = d.done[b], base = d.lenD[b], n = d.n[b];
+    if (done) return;
     for (int p = 0; p < 2; ++p) {
       const size_t i = (size_t)b * d.ev_stride + n - 2 + p;
       rd_embed<D>(d, d.freq, (const bf16_t *)d.type_emb, sh.xs[p], d.ev_t[i], d.ev_k[i]);
@@ -480,7 +479,6 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   }
   const int l = a.step, ly = a.layer;
   const int P = l == 1 ? 2 : 1;
-  const int pos0 = base + (l == 1 ? 0 : l);
   const FusedLayerW &w = d.layer[ly];
   const bool last = ly == L - 1;
   // every load of the launch in flight at once, in the order of use, into
@@ -531,12 +529,20 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   f2.load_packed(wl + D * D + F * D);
   RdFrags<4 * D, D> fe;
   RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
+  // the sequence's header only now: none of the loads above needs it, and
+  // scalar loads issued beside the kernel arguments would be waited for
+  // together with them, holding every load above back by a round trip
+  __builtin_amdgcn_sched_barrier(0);
+  const int done = d.done[b], base = d.lenD[b], n = d.n[b];
+  const uint64_t rnd = (uint64_t)d.rnd[b];   // the draw's round counter
+  const int pos0 = base + (l == 1 ? 0 : l);
   // last layer: the time the drawn interval is added to (the last committed
   // event, or the previous draft), read now rather than behind the decoder
   float tprev = 0.f;
   if (last) tprev = l == 1 ? d.ev_t[(size_t)b * d.ev_stride + n - 1] : d.d_t[(size_t)b * d.MG + (l - 2)];
   // (keeps the stores below, which wait for the partials, behind every load)
   __builtin_amdgcn_sched_barrier(0);
+  if (done) return;   // workgroup-uniform; the loads above are dropped
 #pragma unroll
   for (int i = 0; i < NPV; ++i) sh.part[tid + i * RD_ROW_THREADS] = pv[i];
   if (tid < P * D) (&sh.xs[0][0])[tid] = xv;
