@@ -50,6 +50,9 @@ VERIFY_CASES = [
     small("c4", 32, n_hist=40, init="bias"),
     small("c5", 9, init="bias"),
     small("c5", 5),
+    # 256 x 9 = 2304 rows of width 128: LayerNorm-operand products over many
+    # 64 x 64 tiles, below the fused layer kernel's row threshold
+    small("c5", 256, init="bias"),
     # long histories over few (sequence, head) pairs: the key range is split
     # across workgroups and the partials merged (fp32; bf16 with four or more
     # splits), or, where two bf16 splits would do, one workgroup of eight
