@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--config", default="c4")
     ap.add_argument("--gamma", type=int, default=None)
     ap.add_argument("--ar-steps", type=int, default=1)
+    ap.add_argument("--ar-direct", action="store_true",
+                    help="AR job with its steps launched directly (no graphs), for per-dispatch counters")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-poisson", action="store_true", help="skip the homogeneous-Poisson draft run")
     ap.add_argument("--no-window", action="store_true", help="skip the end-time (window) runs")
@@ -413,7 +415,11 @@ def main():
     events = B * n_gen
     ar_value = None
     if args.ar_steps > 0:
+        if args.ar_direct:
+            ar.tppsd_timing_enable(tp.TIME_KERNELS)
         t_ar, _, _ = timed_jobs(ar, HT, HK, n_gen, args.ar_steps, ar_run)
+        if args.ar_direct:
+            ar.tppsd_timing_enable(0)
         sa = ar.tppsd_state_status()
         assert sa["bits"] == 0 and sa["n_done"] == B, sa
         ar_value = events * args.ar_steps / t_ar
@@ -501,6 +507,7 @@ def main():
                    "draft": f"{wl.draft.n_layers} layers, d {wl.draft.d_model}, {wl.draft.n_heads} heads"},
         "prefill_ms_per_step": t_pre * 1e3 / args.steps,
         "ar_value": ar_value,
+        "ar_launch": "direct (per-dispatch counters; not a throughput figure)" if args.ar_direct else "graphs",
         "speedup_vs_gpu_ar": value / ar_value if ar_value else None,
         "alpha": alpha,
         "events_per_round": events_per_round,

@@ -319,7 +319,8 @@ int tppsd_state_status(tppsd_state *s, hipStream_t stream, uint32_t *bits, int32
 
 /* Measurement of tppsd_sample_sd; the sampled events are unchanged.
  * TPPSD_TIME_KERNELS: rounds are launched directly instead of replaying a
- *   captured HIP graph, and every launch of the target's verify attention, of
+ *   captured HIP graph (and tppsd_sample_ar launches its steps directly
+ *   too, untimed), and every launch of the target's verify attention, of
  *   its verify GEMMs (QKV, attention output, FFN in, FFN out, decoder E), of
  *   the one-launch draft kernel and of each row-drafting launch (split
  *   attention, row kernel) is bracketed by HIP events stamped with the

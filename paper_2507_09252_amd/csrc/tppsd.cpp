@@ -1516,6 +1516,14 @@ int tppsd_sample_ar(tppsd_state *s, int n_events, float *d_t_out, int32_t *d_k_o
   if (n_events == 0) return TPPSD_OK;
   launch_snapshot(s->gen, s->gen0, s->B, st);   // output column = events generated in this call
   int i = 0;
+  if (s->timing & TPPSD_TIME_KERNELS) {
+    // kernel-timing runs launch each step directly (no graphs), so that
+    // per-dispatch tools see the AR step's kernels one by one
+    for (; i < n_events; ++i)
+      if (int rc = ar_step(s, n_events, d_t_out, d_k_out, st)) return rc;
+    s->draft_ok = false;
+    return hip_check("tppsd_sample_ar");
+  }
   {
     // graphs embed the output pointers, their stride and n_gen
     const long long key = ((long long)(uintptr_t)d_t_out * 31 + (long long)(uintptr_t)d_k_out) * 131 +

@@ -277,6 +277,34 @@ def test_ar_end_to_end(case):
     print(f"{case.name}: AR events compared {compared}/{generated}")
 
 
+# the kernel-timing mode launches the AR steps one by one instead of replaying
+# graphs: the same kernels in the same order, so the same events bit for bit
+AR_DIRECT_CASES = [small("c4", 2, n_hist=40, init="bias"), small("c5", 16, init="bias")]
+
+
+@pytest.mark.parametrize("case", AR_DIRECT_CASES, ids=_ids(AR_DIRECT_CASES))
+def test_ar_direct_launch_matches_graphs(case):
+    n_gen, seed = 20, 5
+    wt, wd = weights(case)
+    ht, hk = histories(case)
+    st = gpu_state(case, wt, wd, 1, n_gen, seed, draft=False)
+    runs = []
+    for direct in (False, True):
+        st.tppsd_prefill(to_dev(ht), to_dev(hk), n_gen)
+        st.tppsd_timing_enable(tp.TIME_KERNELS if direct else 0)
+        st.tppsd_sample_ar(n_gen)
+        st.tppsd_timing_enable(0)
+        t, k, n = st.tppsd_read_events()
+        status = st.tppsd_state_status()
+        assert status["bits"] == 0 and status["n_done"] == case.B, status
+        runs.append((t.cpu().numpy(), k.cpu().numpy(), n.cpu().numpy()))
+    (t0, k0, n0), (t1, k1, n1) = runs
+    assert np.array_equal(n0, n1)
+    for b in range(case.B):
+        assert np.array_equal(t0[b, :n0[b]].view(np.uint32), t1[b, :n1[b]].view(np.uint32)), b
+        assert np.array_equal(k0[b, :n0[b]], k1[b, :n1[b]]), b
+
+
 @pytest.mark.parametrize("bonus", [True, False])
 @pytest.mark.parametrize("case", E2E_CASES, ids=_ids(E2E_CASES))
 def test_sd_end_to_end(case, bonus):
