@@ -305,6 +305,7 @@ TRAFFIC_SOURCES = {
     "verify_attention": ("tppsd_attention.hip", "tppsd_attention.h", "tppsd_device.h"),
     "draft_attention": ("tppsd_draft_rows.hip", "tppsd_internal.h", "tppsd_device.h"),
     "draft_rows": ("tppsd_draft_rows.hip", "tppsd_internal.h", "tppsd_device.h"),
+    "ar_attention": ("tppsd_attention.hip", "tppsd_attention.h", "tppsd_device.h"),
 }
 
 
@@ -441,7 +442,7 @@ def main():
             "traffic": measured_traffic("verify_attention", wl.name)}
     if tk["draft_attn_launches"]:
         classes["draft_attention"] = {
-            "bound": "hbm", "kernel": "k_rd_attn<32> (row drafting: split attention, one launch per step and layer)",
+            "bound": "hbm", "kernel": "k_rd_attn<128, 32> (row drafting: split attention, one launch per step and layer)",
             "ms": tk["draft_attn_ms"], "launches": tk["draft_attn_launches"],
             "per_launch": draft_attn_bytes(wl, B, gamma, ctx), "unit": "GB/s", "peak": HBM_PEAK_GBS,
             "traffic": measured_traffic("draft_attention", wl.name)}
