@@ -68,5 +68,43 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_host_sanitized(out_dir: str, verbose: bool = False) -> str:
+    """The library with its host source (tppsd.cpp) built under
+    AddressSanitizer and UndefinedBehaviorSanitizer and the device sources as
+    in build(), whose objects it reuses (built first if missing), for CPU
+    tests of the host-side paths. Load it with the sanitizer runtime
+    preloaded (sanitizer_runtime())."""
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    dev = ("tppsd_kernels.hip", "tppsd_attention.hip", "tppsd_poisson.hip", "tppsd_draft_rows.hip")
+    objs = [os.path.join(BUILD, src + ".o") for src in dev]
+    if not all(os.path.exists(o) for o in objs):
+        build(verbose)
+    os.makedirs(out_dir, exist_ok=True)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+           "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer"]
+    flags = [f for f in HIPCC_FLAGS if f != "-O3"] + ["-O1", "-g"]
+    host_obj = os.path.join(out_dir, "tppsd_san.cpp.o")
+    _run([hipcc] + flags + san + inc + ["-x", "hip", "-c", os.path.join(CSRC, "tppsd.cpp"), "-o", host_obj], verbose)
+    tlib = _torch_lib_dir()
+    out = os.path.join(out_dir, "libtppsd_san.so")
+    _run([_clangxx(), "-shared", "-fsanitize=address,undefined", "-shared-libasan", "-o", out] + objs + [host_obj] +
+         [f"-L{tlib}", "-l:libamdhip64.so", f"-Wl,-rpath,{tlib}"], verbose)
+    return out
+
+
+def _clangxx() -> str:
+    for c in ("/opt/rocm/llvm/bin/clang++", shutil.which("amdclang++") or ""):
+        if c and os.path.exists(c):
+            return c
+    raise RuntimeError("clang++ of the ROCm toolchain not found")
+
+
+def sanitizer_runtime() -> str:
+    """Path of the AddressSanitizer runtime the sanitized library links to."""
+    r = subprocess.run([_clangxx(), "-print-file-name=libclang_rt.asan-x86_64.so"], stdout=subprocess.PIPE, text=True)
+    return r.stdout.strip()
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))

@@ -305,6 +305,56 @@ def test_ar_direct_launch_matches_graphs(case):
         assert np.array_equal(k0[b, :n0[b]], k1[b, :n1[b]]), b
 
 
+# a job run in pieces (SD rounds a few at a time, AR in two calls) continues
+# from the device state exactly: the same events and counters as one call
+RESUME_CASES = [small("c4", 2, n_hist=40, init="bias"), small("c3", 4, n_hist=30, init="bias"),
+                small("c5", 16, init="bias")]
+
+
+def _job_result(st):
+    t, k, n = st.tppsd_read_events()
+    status = st.tppsd_state_status()
+    return t.cpu().numpy(), k.cpu().numpy(), n.cpu().numpy(), status
+
+
+def _same_events(a, b, B):
+    (t0, k0, n0, s0), (t1, k1, n1, s1) = a, b
+    assert np.array_equal(n0, n1)
+    for i in range(B):
+        assert np.array_equal(t0[i, :n0[i]].view(np.uint32), t1[i, :n1[i]].view(np.uint32)), i
+        assert np.array_equal(k0[i, :n0[i]], k1[i, :n1[i]]), i
+    assert s0 == s1, (s0, s1)
+
+
+@pytest.mark.parametrize("case", RESUME_CASES, ids=_ids(RESUME_CASES))
+def test_resumed_jobs_match_one_call(case):
+    gamma, n_gen, seed = case.g, 40, 9
+    wt, wd = weights(case)
+    ht, hk = histories(case)
+    st = gpu_state(case, wt, wd, gamma, n_gen, seed)
+    st.tppsd_prefill(to_dev(ht), to_dev(hk), n_gen)
+    st.tppsd_sample_sd(gamma)
+    whole = _job_result(st)
+    st.tppsd_prefill(to_dev(ht), to_dev(hk), n_gen)
+    pieces = 0
+    while st.tppsd_state_status()["n_done"] < case.B:
+        st.tppsd_sample_sd(gamma, max_rounds=3)
+        pieces += 1
+        assert pieces < 1000
+    assert pieces > 1
+    _same_events(whole, _job_result(st), case.B)
+    assert whole[3]["bits"] == 0 and whole[3]["n_done"] == case.B
+    # AR: n_gen steps at once, then as 7 + (n_gen - 7)
+    st.tppsd_prefill(to_dev(ht), to_dev(hk), n_gen)
+    st.tppsd_sample_ar(n_gen)
+    whole = _job_result(st)
+    st.tppsd_prefill(to_dev(ht), to_dev(hk), n_gen)
+    st.tppsd_sample_ar(7)
+    st.tppsd_sample_ar(n_gen - 7)
+    _same_events(whole, _job_result(st), case.B)
+    assert whole[3]["n_done"] == case.B
+
+
 @pytest.mark.parametrize("bonus", [True, False])
 @pytest.mark.parametrize("case", E2E_CASES, ids=_ids(E2E_CASES))
 def test_sd_end_to_end(case, bonus):
