@@ -2352,6 +2352,13 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
         float q[DH];
 #pragma unroll
         for (int j = 0; j < DH; ++j) q[j] = qs[p * 32 + hh * DH + j] * 0.25f;   // 1 / sqrt(16)
+        // bf16: the scaled query (bf16 values times a power of two) as pairs
+        // for v_dot2c against the raw key words
+        uint32_t qw[sizeof(ELT) == 2 ? DH / 2 : 1];
+        if constexpr (sizeof(ELT) == 2) {
+#pragma unroll
+          for (int e = 0; e < DH / 2; ++e) qw[e] = pk2bf(q[2 * e], q[2 * e + 1]);
+        }
         float m = -INFINITY, lsum = 0.f, o[DH];
 #pragma unroll
         for (int j = 0; j < DH; ++j) o[j] = 0.f;
@@ -2400,8 +2407,19 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
 #pragma unroll
           for (int i = 0; i < U; ++i) {
             float dot = 0.f;
+            if constexpr (sizeof(ELT) == 2) {
 #pragma unroll
-            for (int j = 0; j < DH; ++j) dot += q[j] * kval(i, j);
+              for (int hv = 0; hv < 2; ++hv) {
+                const uint4 w = kr[2 * i + hv];   // columns 8 hv .. 8 hv + 7 of key i
+                dot = dot2_bf(w.x, qw[4 * hv], dot);
+                dot = dot2_bf(w.y, qw[4 * hv + 1], dot);
+                dot = dot2_bf(w.z, qw[4 * hv + 2], dot);
+                dot = dot2_bf(w.w, qw[4 * hv + 3], dot);
+              }
+            } else {
+#pragma unroll
+              for (int j = 0; j < DH; ++j) dot += q[j] * kval(i, j);
+            }
             sc[i] = (k0 + i < n_keys && k0 + i <= last) ? dot : -INFINITY;
             mx = fmaxf(mx, sc[i]);
           }
