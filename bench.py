@@ -32,7 +32,7 @@ HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
 ATTN_KERNEL = {"bf16": "k_attn_mfma<d_head, 1, QT> (verify attention)",
                "fp32": "k_attn_mfma_f32<d_head, 1, QT> (verify attention)"}
-MAX_CPU_PROCS = 16   # the GPU machine's CPU share for one GPU
+MAX_CPU_PROCS = 16   # host CPU cores available per GPU
 
 
 def parse():
