@@ -61,15 +61,27 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
   // row r of the head, lane j = tid % 8 elements 16 j .. + 15 of every 128
   constexpr int NC = D / 128;               // 128-element chunks per row
   const int r = tid >> 3, j8 = tid & 7;
-  const FusedLayerW &lw = d.layer[a.layer];
+  // Every scalar the split needs is loaded up front in two batches, one wait
+  // each: the kernel arguments, then the sequence's header words and the
+  // layer's weight pointers. (Left to itself the compiler sinks each load to
+  // the branch that first needs it and pays a round trip per branch.) The asm
+  // statements only take values, which holds each load ahead of them.
+  const int step = a.step, layer = a.layer, cap = d.cap, nh = d.H;
+  const char *kcb = d.kc, *vcb = d.vc, *xn = (const char *)a.xn;
+  const size_t lbytes = d.layer_bytes;
+  const int32_t *done_p = d.done, *len_p = d.lenD;
+  asm volatile("" ::"s"(step), "s"(layer), "s"(cap), "s"(nh), "s"(kcb), "s"(vcb), "s"(xn), "s"(lbytes), "s"(done_p),
+               "s"(len_p));
+  const FusedLayerW &lw = d.layer[layer];
   const bf16_t *wqkv = (const bf16_t *)lw.qkv_w;
+  const float *qkvb = lw.qkv_b;
+  const int done = done_p[b], lenD = len_p[b];
+  asm volatile("" ::"s"(done), "s"(lenD), "s"(wqkv), "s"(qkvb));
   auto wrow = [&](int which) { return wqkv + (size_t)(which * D + h * DH + r) * D + 16 * j8; };
-  // the sequence's header words, the LayerNorm'd rows and this head's query
-  // rows of W_qkv, loaded together
-  const int done = d.done[b], lenD = d.lenD[b];
-  const int P = a.step == 1 ? 2 : 1;
+  // the LayerNorm'd rows and this head's query rows of W_qkv
+  const int P = step == 1 ? 2 : 1;
   uint4 xw = make_uint4(0u, 0u, 0u, 0u);
-  if (tid < 2 * D / 8) xw = *(const uint4 *)(a.xn + (size_t)b * 2 * D + 8 * tid);
+  if (tid < 2 * D / 8) xw = *(const uint4 *)((const bf16_t *)xn + (size_t)b * 2 * D + 8 * tid);
   uint4 wq[NC][2];
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
@@ -77,18 +89,17 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
     wq[c][1] = *(const uint4 *)(wrow(0) + 128 * c + 8);
   }
   // (the biases too: a load issued after the cache loads would be waited for behind them)
-  const float bq = lw.qkv_b[h * DH + r], bk = lw.qkv_b[D + h * DH + r], bv = lw.qkv_b[2 * D + h * DH + r];
-  if (done) return;
-  const int pos0 = lenD + (a.step == 1 ? 0 : a.step);
-  const int n_keys = min(pos0 + P, d.cap);
+  const float bq = qkvb[h * DH + r], bk = qkvb[D + h * DH + r], bv = qkvb[2 * D + h * DH + r];
+  const int pos0 = lenD + (step == 1 ? 0 : step);
+  const int n_keys = min(pos0 + P, cap);
   const int k0 = s * RD_KEYS;
-  if (k0 >= n_keys) return;   // whole workgroup; no barrier passed yet
-  const size_t row0 = ((size_t)b * d.H + h) * d.cap;
-  bf16_t *kc = (bf16_t *)(d.kc + d.layer_bytes * a.layer);
-  bf16_t *vc = (bf16_t *)(d.vc + d.layer_bytes * a.layer);
+  if (done || k0 >= n_keys) return;   // whole workgroup; no barrier passed yet
+  const size_t row0 = ((size_t)b * nh + h) * cap;
+  bf16_t *kc = (bf16_t *)(kcb + lbytes * layer);
+  bf16_t *vc = (bf16_t *)(vcb + lbytes * layer);
   // the step's new positions pos0 .. pos0 + P - 1 whose key and value this
   // split owns (it computes and appends them; they are in no other split)
-  auto owned = [&](int p) { const int pn = pos0 + p; return p < P && pn >= k0 && pn < k0 + RD_KEYS && pn < d.cap; };
+  auto owned = [&](int p) { const int pn = pos0 + p; return p < P && pn >= k0 && pn < k0 + RD_KEYS && pn < cap; };
   const bool any_owned = owned(0) || owned(1);
   uint4 wk[NC][2], wv[NC][2];
   if (any_owned) {
@@ -188,7 +199,9 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
   // scores, per query: q k / sqrt(d_head) (the SEG lanes of a key sum their
   // segments); keys past the query masked
   static_assert(SEG == 4 || SEG == 2, "key segments per quad");
-  const float scale = 1.f / sqrtf((float)DH);
+  // scores in base-2 units (log2 e folded into 1 / sqrt(d_head)), so that
+  // every exponential is one v_exp_f32; maxima leave in natural units
+  const float scale2 = 1.4426950408889634f / sqrtf((float)DH);
   float sc[2][NKL];
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
@@ -203,7 +216,7 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
       dot += dpp_mov<0xB1>(dot);                 // lane ^ 1
       if (SEG == 4) dot += dpp_mov<0x4E>(dot);   // lane ^ 2
       const int pos = k0 + i * KPI + tid / SEG;
-      sc[p][i] = (pos < n_keys && pos <= last) ? dot * scale : -INFINITY;
+      sc[p][i] = (pos < n_keys && pos <= last) ? dot * scale2 : -INFINITY;
       mx = fmaxf(mx, sc[p][i]);
     }
     mx = wave_max(mx);
@@ -218,7 +231,7 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
     float ls = 0.f;
 #pragma unroll
     for (int i = 0; i < NKL; ++i) {
-      const float e = sc[p][i] == -INFINITY ? 0.f : expf(sc[p][i] - mq[p]);
+      const float e = sc[p][i] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[p][i] - mq[p]);
       if (seg == 0) {
         es[p][i * KPI + tid / SEG] = e;
         ls += e;
@@ -269,10 +282,10 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
     float acc = 0.f;
 #pragma unroll
     for (int g = 0; g < NG; ++g) acc += red[p][g][c];
-    float *dst = a.part + ((((size_t)b * d.H + h) * a.S + s) * 2 + p) * (DH + 2);
+    float *dst = a.part + ((((size_t)b * nh + h) * a.S + s) * 2 + p) * (DH + 2);
     dst[2 + c] = acc;
     if (c == 0) {
-      dst[0] = p ? mq[1] : mq[0];
+      dst[0] = (p ? mq[1] : mq[0]) * 0.69314718055994531f;   // natural units
       dst[1] = (wred[p][0][1] + wred[p][1][1]) + (wred[p][2][1] + wred[p][3][1]);
     }
   }
