@@ -43,7 +43,7 @@ constexpr int RD_VEC = 2048;   // floats of a row launch's staged vectors (RdVec
 // of head h of sequence b
 // ---------------------------------------------------------------------------
 template <int D, int DH>
-__global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_rd_attn(RowDraftArgs a) {
   constexpr int NG = 256 / DH;              // lane groups over the value blocks
   constexpr int BPL = RD_KEYS / 8 / NG;     // value blocks per lane
   static_assert(DH == 32 && D % 128 == 0, "q, k, v: 32 groups of 8 lanes, 16 elements per lane and pass of 128");
@@ -51,6 +51,7 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
   __shared__ float red[2][NG][DH];
   __shared__ float wred[2][4][2];
   __shared__ __attribute__((aligned(16))) bf16_t xl[2][D];        // LayerNorm'd rows of the step's tokens
+  __shared__ float bs[3][DH];                                       // the head's q, k, v biases
   __shared__ float qs[2][DH];                                       // queries (bf16-rounded)
   __shared__ __attribute__((aligned(16))) bf16_t kvn[2][2][DH];   // the new keys and values [k / v][row]
   const DraftArgs &d = a.d;
@@ -82,14 +83,15 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
   const int P = step == 1 ? 2 : 1;
   uint4 xw = make_uint4(0u, 0u, 0u, 0u);
   if (tid < 2 * D / 8) xw = *(const uint4 *)((const bf16_t *)xn + (size_t)b * 2 * D + 8 * tid);
+  // the head's biases, one per lane (staged in LDS with the rows)
+  const int bi = min(tid, 3 * DH - 1);
+  const float bias = qkvb[(bi / DH) * D + h * DH + bi % DH];
   uint4 wq[NC][2];
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     wq[c][0] = *(const uint4 *)(wrow(0) + 128 * c);
     wq[c][1] = *(const uint4 *)(wrow(0) + 128 * c + 8);
   }
-  // (the biases too: a load issued after the cache loads would be waited for behind them)
-  const float bq = qkvb[h * DH + r], bk = qkvb[D + h * DH + r], bv = qkvb[2 * D + h * DH + r];
   const int pos0 = lenD + (step == 1 ? 0 : step);
   const int n_keys = min(pos0 + P, cap);
   const int k0 = s * RD_KEYS;
@@ -136,6 +138,7 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
     vr[i] = __builtin_nontemporal_load((const u32x4_t *)(vc + v_at<bf16_t>(row0, pb, col, DH)));
   }
   if (tid < 2 * D / 8) *(uint4 *)(&xl[0][0] + 8 * tid) = xw;
+  if (tid < 3 * DH) (&bs[0][0])[tid] = bias;
   __syncthreads();
   // dot products of a weight row slice with a row's slice: v_dot2c over
   // the raw bf16 pairs (products exact in fp32)
@@ -157,11 +160,11 @@ __global__ __launch_bounds__(256) void k_rd_attn(RowDraftArgs a) {
   for (int p = 0; p < 2; ++p) {
     if (p >= P) break;
     const float qa = dot16(wq, p);
-    if (j8 == 0) qs[p][r] = bf2f(f2bf(qa + bq));
+    if (j8 == 0) qs[p][r] = bf2f(f2bf(qa + bs[0][r]));
     if (owned(p)) {   // workgroup-uniform
       const float ka = dot16(wk, p), va = dot16(wv, p);
       if (j8 == 0) {
-        const bf16_t kb = f2bf(ka + bk), vb = f2bf(va + bv);
+        const bf16_t kb = f2bf(ka + bs[1][r]), vb = f2bf(va + bs[2][r]);
         kvn[0][p][r] = kb;
         kvn[1][p][r] = vb;
         const int pn = pos0 + p;
