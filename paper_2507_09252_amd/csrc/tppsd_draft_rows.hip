@@ -436,24 +436,44 @@ struct RdShared {
 // attention launch, which forms q, k, v from them; a position past the
 // cache capacity is flagged here
 template <int D>
-__device__ __forceinline__ void rd_store_xn(const RowDraftArgs &a, const bf16_t *ab, int np, int b, int pos0) {
+__device__ __forceinline__ void rd_store_xn(bf16_t *xn, int cap, uint32_t *status, const bf16_t *ab, int np, int b,
+                                            int pos0) {
   const int tid = threadIdx.x;
-  if (tid < np * D / 8) *(uint4 *)(a.xn + (size_t)b * 2 * D + 8 * tid) = *(const uint4 *)(ab + 8 * tid);
-  if (tid == 0 && pos0 + np > a.d.cap) atomicOr(a.d.status, TPPSD_STATUS_CAPACITY);
+  if (tid < np * D / 8) *(uint4 *)(xn + (size_t)b * 2 * D + 8 * tid) = *(const uint4 *)(ab + 8 * tid);
+  if (tid == 0 && pos0 + np > cap) atomicOr(status, TPPSD_STATUS_CAPACITY);
 }
 
 // the THP embedding (sin / cos time encoding + type row) of event (t, k) into
 // row p; the type rows [K][D] from temb (memory or an LDS copy)
 template <int D>
-__device__ __forceinline__ void rd_embed(const DraftArgs &d, const float *freq, const bf16_t *temb, float *xrow,
-                                         float t, int k) {
+__device__ __forceinline__ void rd_embed(int K, const float *freq, const bf16_t *temb, float *xrow, float t, int k) {
   const int tid = threadIdx.x;
   if (tid < D) {
     const float arg = t * freq[tid];
-    const int kk = min(max(k, 0), d.K - 1);
+    const int kk = min(max(k, 0), K - 1);
     xrow[tid] = ((tid & 1) ? cosf(arg) : sinf(arg)) + bf2f(temb[(size_t)kk * D + tid]);
   }
 }
+
+// a load the compiler may issue as a scalar one wherever it can prove the
+// address uniform: the word does not change while the kernel runs (the
+// sequence's header words are written by other launches only)
+template <class T>
+__device__ __forceinline__ T load_const(const T *p) {
+  return *(const __attribute__((address_space(4))) T *)p;
+}
+
+// kernel arguments a row launch reads only late (the decoder, the draw and
+// the next token), held in registers from the start
+struct RdLate {
+  const bf16_t *pk_e, *pk_head, *temb;
+  bf16_t *xn;
+  uint32_t *status;
+  float *tau, *t, *logg, *logf, *mix, *logtype;
+  int32_t *k;
+  uint64_t seed;
+  int gamma;
+};
 
 // Offsets in RdShared::vec of the small vectors a row launch reads (the
 // current layer's output / FFN biases and second LayerNorm; the next layer's
@@ -477,36 +497,54 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   __shared__ RdShared<D, F, DH> sh;
   const DraftArgs &d = a.d;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // Scalar operands come in two batches, one wait each: the kernel arguments
+  // the first loads need, then what they point at (the layer's vector
+  // pointers, the sequence's header words) together with the arguments read
+  // late in the launch. (Left alone, the compiler loads each where it is
+  // first needed and waits there: a dozen round trips before the first
+  // barrier, more in the draw.) The asm statements only take values, which
+  // holds each load ahead of them.
   const int L = d.L, M = d.M, K = d.K;
-  float *xg = a.x + (size_t)b * 2 * D;
-  if (a.step == 0) {
+  const int l = a.step, ly = a.layer;
+  float *xa = a.x;
+  const float *part = a.part;
+  const bf16_t *pk = a.pk;
+  const int nh = d.H, S = a.S, cap = d.cap, evs = d.ev_stride, MG = d.MG;
+  const int32_t *done_p = d.done, *len_p = d.lenD, *n_p = d.n, *rnd_p = d.rnd;
+  const float *evt = d.ev_t, *dtp = d.d_t;
+  // (d.F only completes the four words from d.F to d.L, so that they come in
+  // one load and no register of it is reused while in flight)
+  asm volatile("" ::"s"(l), "s"(ly), "s"(L), "s"(M), "s"(K), "s"(nh), "s"(S), "s"(cap), "s"(evs), "s"(MG), "s"(part),
+               "s"(xa), "s"(pk), "s"(done_p), "s"(len_p), "s"(n_p), "s"(rnd_p), "s"(evt), "s"(dtp), "s"(d.F));
+  float *xg = xa + (size_t)b * 2 * D;
+  const bf16_t *wl = pk + (size_t)ly * rd_layer_elems<D, F>();
+  if (l == 0) {
     const int done = d.done[b], base = d.lenD[b], n = d.n[b];
     if (done) return;
     for (int p = 0; p < 2; ++p) {
       const size_t i = (size_t)b * d.ev_stride + n - 2 + p;
-      rd_embed<D>(d, d.freq, (const bf16_t *)d.type_emb, sh.xs[p], d.ev_t[i], d.ev_k[i]);
+      rd_embed<D>(K, d.freq, (const bf16_t *)d.type_emb, sh.xs[p], d.ev_t[i], d.ev_k[i]);
     }
     rd_sync();
     rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[0].ln1_g, d.layer[0].ln1_b, 2);
     for (int i = tid; i < 2 * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
     rd_sync();
-    rd_store_xn<D>(a, &sh.ab[0][0], 2, b, base);
+    rd_store_xn<D>(a.xn, d.cap, d.status, &sh.ab[0][0], 2, b, base);
     return;
   }
-  const int l = a.step, ly = a.layer;
   const int P = l == 1 ? 2 : 1;
-  const FusedLayerW &w = d.layer[ly];
   const bool last = ly == L - 1;
-  // every load of the launch in flight at once, in the order of use, into
-  // registers: the split partials of the sequence (all splits of the slab;
-  // those past the step's keys are ignored below), the residual rows and the
-  // small vectors, then the output projection and both FFN products (after
-  // the last layer the decoder's follow once the first FFN product is done)
+  // every vector load of the launch in flight at once, in the order of use,
+  // into registers: the split partials of the sequence (all splits of the
+  // slab; those past the step's keys are ignored below), the residual rows,
+  // the output projection, then (behind the second scalar batch) the small
+  // vectors and both FFN products (after the last layer the decoder's follow
+  // once the first FFN product is done)
   constexpr int NPV = RD_MAX_PART / RD_ROW_THREADS;
   float pv[NPV];
   {
-    const int cnt = d.H * a.S * 2 * (DH + 2);
-    const float *src = a.part + (size_t)b * cnt;
+    const int cnt = nh * S * 2 * (DH + 2);
+    const float *src = part + (size_t)b * cnt;
 #pragma unroll
     for (int i = 0; i < NPV; ++i) {
       const int k = tid + i * RD_ROW_THREADS;
@@ -514,64 +552,70 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     }
   }
   const float xv = tid < P * D ? xg[tid] : 0.f;
+  RdFrags<D, D> fo;
+  fo.load_packed(wl);
+  // second batch
+  const FusedLayerW &w = d.layer[ly];
+  const FusedLayerW &wn = d.layer[last ? 0 : ly + 1];
+  const float *outb = w.out_b, *ln2g = w.ln2_g, *ln2b = w.ln2_b, *f1b = w.ffn1_b, *f2b = w.ffn2_b;
+  const float *n1g = last ? d.lnf_g : wn.ln1_g, *n1b = last ? d.lnf_b : wn.ln1_b;
+  const float *k1b = d.k1_b, *mixb = d.mix_b, *k2b = d.k2_b, *freq = d.freq;
+  const float *l0g = d.layer[0].ln1_g, *l0b = d.layer[0].ln1_b;
+  const int done = load_const(done_p + b), base = load_const(len_p + b), n = load_const(n_p + b),
+            rnd32 = load_const(rnd_p + b);
+  const RdLate late{a.pk_e, a.pk_head, (const bf16_t *)d.type_emb, a.xn, d.status, d.d_tau, d.d_t, d.d_logg, d.d_logf,
+                    d.d_mix, d.d_logtype, d.d_k, d.seed, d.gamma};
+  asm volatile("" ::"s"(outb), "s"(ln2g), "s"(ln2b), "s"(f1b), "s"(f2b), "s"(n1g), "s"(n1b), "s"(k1b), "s"(mixb),
+               "s"(k2b), "s"(freq), "s"(l0g), "s"(l0b), "s"(done), "s"(base), "s"(n), "s"(rnd32), "s"(late.pk_e),
+               "s"(late.pk_head), "s"(late.temb), "s"(late.xn), "s"(late.status), "s"(late.tau), "s"(late.t),
+               "s"(late.logg), "s"(late.logf), "s"(late.mix), "s"(late.logtype), "s"(late.k), "s"(late.seed),
+               "s"(late.gamma));
+  const uint64_t rnd = (uint64_t)rnd32;   // the draw's round counter
   // the launch's small vectors, one unconditional load per element
   typedef RdVec<D, F> V;
   constexpr int NVL = RD_VEC / RD_ROW_THREADS;
   float vl[NVL];
   {
     struct Seg { const float *p; int off, n; };
-    const FusedLayerW &wn = d.layer[last ? 0 : ly + 1];
-    const Seg segs[] = {{w.out_b, V::OUTB, D},      {w.ln2_g, V::LN2G, D},          {w.ln2_b, V::LN2B, D},
-                        {w.ffn1_b, V::F1B, F},      {w.ffn2_b, V::F2B, D},
-                        {last ? d.lnf_g : wn.ln1_g, V::N1G, D}, {last ? d.lnf_b : wn.ln1_b, V::N1B, D},
-                        {d.k1_b, V::K1B, D},        {d.mix_b, V::MIXB, 3 * M},       {d.k2_b, V::K2B, K},
-                        {d.freq, V::FREQ, D},       {d.layer[0].ln1_g, V::L0G, D},   {d.layer[0].ln1_b, V::L0B, D}};
+    const Seg segs[] = {{outb, V::OUTB, D}, {ln2g, V::LN2G, D},       {ln2b, V::LN2B, D},   {f1b, V::F1B, F},
+                        {f2b, V::F2B, D},   {n1g, V::N1G, D},         {n1b, V::N1B, D},     {k1b, V::K1B, D},
+                        {mixb, V::MIXB, 3 * M}, {k2b, V::K2B, K},     {freq, V::FREQ, D},   {l0g, V::L0G, D},
+                        {l0b, V::L0B, D}};
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
       const int k = tid + i * RD_ROW_THREADS;
-      const float *src = w.out_b;   // (slots between segments read a valid element, unused)
+      const float *src = outb;   // (slots between segments read a valid element, unused)
 #pragma unroll
       for (const Seg &g : segs)
         if (k >= g.off && k < g.off + g.n) src = g.p + (k - g.off);
       vl[i] = *src;
     }
   }
-  const bf16_t *wl = a.pk + (size_t)ly * rd_layer_elems<D, F>();
-  RdFrags<D, D> fo;
   RdFrags<F, D> f1;
-  fo.load_packed(wl);
   f1.load_packed(wl + D * D);
   RdFrags<D, F> f2;
   f2.load_packed(wl + D * D + F * D);
   RdFrags<4 * D, D> fe;
   RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
-  // the sequence's header only now: none of the loads above needs it, and
-  // scalar loads issued beside the kernel arguments would be waited for
-  // together with them, holding every load above back by a round trip
-  __builtin_amdgcn_sched_barrier(0);
-  const int done = d.done[b], base = d.lenD[b], n = d.n[b];
-  const uint64_t rnd = (uint64_t)d.rnd[b];   // the draw's round counter
   const int pos0 = base + (l == 1 ? 0 : l);
   // last layer: the time the drawn interval is added to (the last committed
   // event, or the previous draft), read now rather than behind the decoder
   float tprev = 0.f;
-  if (last) tprev = l == 1 ? d.ev_t[(size_t)b * d.ev_stride + n - 1] : d.d_t[(size_t)b * d.MG + (l - 2)];
+  if (last) tprev = l == 1 ? evt[(size_t)b * evs + n - 1] : dtp[(size_t)b * MG + (l - 2)];
   // (keeps the stores below, which wait for the partials, behind every load)
   __builtin_amdgcn_sched_barrier(0);
   if (done) return;   // workgroup-uniform; the loads above are dropped
 #pragma unroll
   for (int i = 0; i < NPV; ++i) sh.part[tid + i * RD_ROW_THREADS] = pv[i];
   if (tid < P * D) (&sh.xs[0][0])[tid] = xv;
-#pragma unroll
-  for (int i = 0; i < NVL; ++i) sh.vec[tid + i * RD_ROW_THREADS] = vl[i];
   rd_sync();
   // merge the attention splits of each (row, head): output = sum_s e^{m_s - m} o_s / sum_s e^{m_s - m} l_s
   {
-    const int n_keys = min(pos0 + P, d.cap);
+    const int n_keys = min(pos0 + P, cap);
     const int S_b = (n_keys + RD_KEYS - 1) / RD_KEYS;
     for (int i = tid; i < P * D; i += RD_ROW_THREADS) {
       const int p = i / D, hc = i - p * D, h = hc / DH, c = hc - h * DH;
-      const float *pp = sh.part + h * a.S * 2 * (DH + 2) + p * (DH + 2);
+      const float *pp = sh.part + h * S * 2 * (DH + 2) + p * (DH + 2);
       float mx = -INFINITY;
       for (int s = 0; s < S_b; ++s) mx = fmaxf(mx, pp[s * 2 * (DH + 2)]);
       float ls = 0.f, os = 0.f;
@@ -586,6 +630,10 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
       sh.ab[p][hc] = f2bf(ls > 0.f ? os / ls : 0.f);
     }
   }
+  // the small vectors (issued behind the output projection's fragments, so
+  // this waits for those too, which the next product needs anyway)
+#pragma unroll
+  for (int i = 0; i < NVL; ++i) sh.vec[tid + i * RD_ROW_THREADS] = vl[i];
   rd_sync();
   // output projection + residual
   fo.template mul<2>(&sh.ab[0][0], D, P, [&](int p, int nn, float acc) {
@@ -598,10 +646,10 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     if (p < P) sh.hb[p][nn] = f2bf(fmaxf(acc + sh.vec[V::F1B + nn], 0.f));
   });
   // the first product's registers are free: after the last layer, the decoder's fragments
-  const bool more = l < d.gamma;
+  const bool more = l < late.gamma;
   if (last) {
-    fe.load_packed(a.pk_e);
-    fh.load_packed(a.pk_head);
+    fe.load_packed(late.pk_e);
+    fh.load_packed(late.pk_head);
   }
   rd_sync();
   f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
@@ -612,7 +660,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::N1G, sh.vec + V::N1B, P);
     for (int i = tid; i < P * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
     rd_sync();
-    rd_store_xn<D>(a, &sh.ab[0][0], P, b, pos0);
+    rd_store_xn<D>(late.xn, cap, late.status, &sh.ab[0][0], P, b, pos0);
     return;
   }
   // ---- last layer: decoder on the last row, the draw, the next token
@@ -636,7 +684,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   {
     const int nvec = K * D / 8;
 #pragma unroll
-    for (int i = 0; i < NTE; ++i) te[i] = *((const uint4 *)d.type_emb + min(tid + i * RD_ROW_THREADS, nvec - 1));
+    for (int i = 0; i < NTE; ++i) te[i] = *((const uint4 *)late.temb + min(tid + i * RD_ROW_THREADS, nvec - 1));
   }
   rd_sync();
   fh.template mul<4>(&sh.eb[0][0], D, 4, [&](int r, int nn, float acc) {
@@ -651,16 +699,16 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     const float mw = wave_max(lw), mk = wave_max(lk);
     const float logw = lw - mw - logf(wave_sum(lane < M ? expf(lw - mw) : 0.f));
     const float logk = lk - mk - logf(wave_sum(lane < K ? expf(lk - mk) : 0.f));
-    const size_t di = (size_t)b * d.MG + (l - 1);
+    const size_t di = (size_t)b * MG + (l - 1);
     if (lane < M) {
-      d.d_mix[di * 3 * M + lane] = logw;
-      d.d_mix[di * 3 * M + M + lane] = mu;
-      d.d_mix[di * 3 * M + 2 * M + lane] = sg;
+      late.mix[di * 3 * M + lane] = logw;
+      late.mix[di * 3 * M + M + lane] = mu;
+      late.mix[di * 3 * M + 2 * M + lane] = sg;
     }
-    if (lane < K) d.d_logtype[di * K + lane] = logk;
+    if (lane < K) late.logtype[di * K + lane] = logk;
     const bool bad = (lane < M && !(isfinite(logw) && isfinite(mu) && isfinite(sg))) || (lane < K && !isfinite(logk));
     float u[4];
-    philox_uniforms(d.seed, (uint64_t)b, rnd, (uint64_t)l, TAG_DRAFT, u);
+    philox_uniforms(late.seed, (uint64_t)b, rnd, (uint64_t)l, TAG_DRAFT, u);
     // categorical over the lanes' log-probabilities: first index whose
     // running sum of exp exceeds u times the total
     auto draw = [&](float lp, int cnt, float uu) {
@@ -690,12 +738,12 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     const bool bad_any = __ballot(bad) != 0ull;
     if (lane == 0) {
       const float tn = tprev + tau;
-      d.d_tau[di] = tau;
-      d.d_t[di] = tn;
-      d.d_k[di] = kk;
-      d.d_logg[di] = lg;
-      d.d_logf[di] = lf;
-      if (bad_any || !isfinite(tau)) atomicOr(d.status, TPPSD_STATUS_NONFINITE);
+      late.tau[di] = tau;
+      late.t[di] = tn;
+      late.k[di] = kk;
+      late.logg[di] = lg;
+      late.logf[di] = lf;
+      if (bad_any || !isfinite(tau)) atomicOr(late.status, TPPSD_STATUS_NONFINITE);
       sh.tok_t = tn;
       sh.tok_k = kk;
     }
@@ -705,12 +753,12 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   for (int i = 0; i < NTE; ++i) *((uint4 *)sh.temb + tid + i * RD_ROW_THREADS) = te[i];
   rd_sync();
   // the drawn event is the next step's token, at position base + l + 1
-  rd_embed<D>(d, sh.vec + V::FREQ, sh.temb, sh.xs[0], sh.tok_t, sh.tok_k);
+  rd_embed<D>(K, sh.vec + V::FREQ, sh.temb, sh.xs[0], sh.tok_t, sh.tok_k);
   rd_sync();
   rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::L0G, sh.vec + V::L0B, 1);
   for (int i = tid; i < D; i += RD_ROW_THREADS) xg[i] = sh.xs[0][i];
   rd_sync();
-  rd_store_xn<D>(a, &sh.ab[0][0], 1, b, base + l + 1);
+  rd_store_xn<D>(late.xn, cap, late.status, &sh.ab[0][0], 1, b, base + l + 1);
 }
 
 }  // namespace
