@@ -214,6 +214,7 @@ struct tppsd_state {
   size_t pack_layer = 0;
   char *packD = nullptr;               // draft weights in fragment order
   char *packDdec = nullptr;            // draft decoder in fragment order (row drafting)
+  float *rd_rng = nullptr;             // [B][max_gamma][4] the draft draws' random numbers (row drafting)
   size_t pack_layerD = 0;
   bool packs_built = false;
   bool wb_built = false;
@@ -270,6 +271,7 @@ struct WsLayout {
   size_t packT = 0, pack_layer = 0;   // target weights in MFMA fragment order (fused layer kernel), per layer
   size_t packD = 0, pack_layerD = 0;  // the same for the draft model
   size_t packDdec = 0;                // the draft decoder's [E; V_k1] and heads in fragment order (row drafting)
+  size_t rd_rng = 0;                  // the draft draws' random numbers per sequence and step (row drafting)
   size_t wbT = 0, wbD = 0, wb_nT = 0, wb_nD = 0;   // matrices in the k_block order (0 bytes: not served)
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt, d_rate;
   size_t v_logg, v_logf, v_mix, v_lt;
@@ -351,8 +353,10 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
     w.packD = take(w.pack_layerD * D->cfg.n_layers);
   }
   if (D && !D->attnhp() &&
-      row_draft_ok(D->bf16(), D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types, (int)kvc))
+      row_draft_ok(D->bf16(), D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types, (int)kvc)) {
     w.packDdec = take(rd_pack_dec_elems(D->d()) * 2);
+    w.rd_rng = take(Bz * MG * 4 * 4);
+  }
   w.ar_mix = take(Bz * 3 * mmax * 4);
   w.ar_lt = take(Bz * kmax * 4);
   {
@@ -732,6 +736,7 @@ int do_draft_rows(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStre
   a.x = s->x;
   a.xn = (bf16_t *)s->a;
   a.part = s->attn_part;
+  a.rng = s->rd_rng;
   a.pk = (const bf16_t *)s->packD;
   a.pk_e = (const bf16_t *)s->packDdec;
   a.pk_head = (const bf16_t *)(s->packDdec + (size_t)4 * s->D->d() * s->D->d() * 2);
@@ -1156,6 +1161,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->pack_layer = w.pack_layer;
   s->packD = w.pack_layerD ? ws + w.packD : nullptr;
   s->packDdec = w.packDdec ? ws + w.packDdec : nullptr;
+  s->rd_rng = w.rd_rng ? (float *)(ws + w.rd_rng) : nullptr;
   s->pack_layerD = w.pack_layerD;
   s->cT.wb = w.wb_nT ? ws + w.wbT : nullptr;
   s->cD.wb = w.wb_nD ? ws + w.wbD : nullptr;

@@ -91,6 +91,23 @@ __device__ __forceinline__ float wave_sum(float v) {
          (__int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48)));
 }
+// inclusive running sum over the wave (lane i: v_0 + ... + v_i), DPP only:
+// shifts by 1, 2, 4, 8 within rows of 16 lanes, then each row's last lane
+// broadcast onward (row_bcast:15 into rows 1 and 3, row_bcast:31 into rows 2
+// and 3). Lanes a shift leaves without a source add the 0 they start from.
+__device__ __forceinline__ float wave_cumsum(float v) {
+  v += dpp_mov<0x111>(v);   // row_shr:1
+  v += dpp_mov<0x112>(v);   // row_shr:2
+  v += dpp_mov<0x114>(v);   // row_shr:4
+  v += dpp_mov<0x118>(v);   // row_shr:8
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false));
+  return v;
+}
+// lane i's value of v (i wave-uniform)
+__device__ __forceinline__ float lane_val(float v, int i) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
+}
 __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, dpp_mov<0xB1>(v));
   v = fmaxf(v, dpp_mov<0x4E>(v));

@@ -471,7 +471,6 @@ struct RdLate {
   uint32_t *status;
   float *tau, *t, *logg, *logf, *mix, *logtype;
   int32_t *k;
-  uint64_t seed;
   int gamma;
 };
 
@@ -507,20 +506,31 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   const int L = d.L, M = d.M, K = d.K;
   const int l = a.step, ly = a.layer;
   float *xa = a.x;
-  const float *part = a.part;
+  const float *part = a.part, *rngp = a.rng;
   const bf16_t *pk = a.pk;
   const int nh = d.H, S = a.S, cap = d.cap, evs = d.ev_stride, MG = d.MG;
-  const int32_t *done_p = d.done, *len_p = d.lenD, *n_p = d.n, *rnd_p = d.rnd;
+  const int32_t *done_p = d.done, *len_p = d.lenD, *n_p = d.n;
   const float *evt = d.ev_t, *dtp = d.d_t;
   // (d.F only completes the four words from d.F to d.L, so that they come in
   // one load and no register of it is reused while in flight)
   asm volatile("" ::"s"(l), "s"(ly), "s"(L), "s"(M), "s"(K), "s"(nh), "s"(S), "s"(cap), "s"(evs), "s"(MG), "s"(part),
-               "s"(xa), "s"(pk), "s"(done_p), "s"(len_p), "s"(n_p), "s"(rnd_p), "s"(evt), "s"(dtp), "s"(d.F));
+               "s"(xa), "s"(pk), "s"(done_p), "s"(len_p), "s"(n_p), "s"(evt), "s"(dtp), "s"(d.F),
+               "s"(rngp));
   float *xg = xa + (size_t)b * 2 * D;
   const bf16_t *wl = pk + (size_t)ly * rd_layer_elems<D, F>();
   if (l == 0) {
     const int done = d.done[b], base = d.lenD[b], n = d.n[b];
     if (done) return;
+    // every step's draw numbers for the round, which depend on no result of
+    // the steps: thread j takes step j + 1 (u for the component, the
+    // Box-Muller normal deviate, u for the type)
+    const uint64_t rnd = (uint64_t)d.rnd[b];
+    for (int j = tid; j < d.gamma; j += RD_ROW_THREADS) {
+      float u[4];
+      philox_uniforms(d.seed, (uint64_t)b, rnd, (uint64_t)(j + 1), TAG_DRAFT, u);
+      const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
+      *(float4 *)(a.rng + ((size_t)b * MG + j) * 4) = make_float4(u[0], eps, u[3], 0.f);
+    }
     for (int p = 0; p < 2; ++p) {
       const size_t i = (size_t)b * d.ev_stride + n - 2 + p;
       rd_embed<D>(K, d.freq, (const bf16_t *)d.type_emb, sh.xs[p], d.ev_t[i], d.ev_k[i]);
@@ -561,16 +571,20 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   const float *n1g = last ? d.lnf_g : wn.ln1_g, *n1b = last ? d.lnf_b : wn.ln1_b;
   const float *k1b = d.k1_b, *mixb = d.mix_b, *k2b = d.k2_b, *freq = d.freq;
   const float *l0g = d.layer[0].ln1_g, *l0b = d.layer[0].ln1_b;
-  const int done = load_const(done_p + b), base = load_const(len_p + b), n = load_const(n_p + b),
-            rnd32 = load_const(rnd_p + b);
+  const int done = load_const(done_p + b), base = load_const(len_p + b), n = load_const(n_p + b);
+  // the step's draw: u for the component, the normal deviate, u for the type
+  // (every step's, written by the step-0 launch; read in every layer, used in
+  // the last)
+  const float *rs = rngp + ((size_t)b * MG + (l - 1)) * 4;
+  const float u_z = load_const(rs), eps = load_const(rs + 1), u_k = load_const(rs + 2);
   const RdLate late{a.pk_e, a.pk_head, (const bf16_t *)d.type_emb, a.xn, d.status, d.d_tau, d.d_t, d.d_logg, d.d_logf,
-                    d.d_mix, d.d_logtype, d.d_k, d.seed, d.gamma};
+                    d.d_mix, d.d_logtype, d.d_k, d.gamma};
   asm volatile("" ::"s"(outb), "s"(ln2g), "s"(ln2b), "s"(f1b), "s"(f2b), "s"(n1g), "s"(n1b), "s"(k1b), "s"(mixb),
-               "s"(k2b), "s"(freq), "s"(l0g), "s"(l0b), "s"(done), "s"(base), "s"(n), "s"(rnd32), "s"(late.pk_e),
+               "s"(k2b), "s"(freq), "s"(l0g), "s"(l0b), "s"(done), "s"(base), "s"(n), "s"(u_z), "s"(eps), "s"(u_k),
+               "s"(late.pk_e),
                "s"(late.pk_head), "s"(late.temb), "s"(late.xn), "s"(late.status), "s"(late.tau), "s"(late.t),
-               "s"(late.logg), "s"(late.logf), "s"(late.mix), "s"(late.logtype), "s"(late.k), "s"(late.seed),
+               "s"(late.logg), "s"(late.logf), "s"(late.mix), "s"(late.logtype), "s"(late.k),
                "s"(late.gamma));
-  const uint64_t rnd = (uint64_t)rnd32;   // the draw's round counter
   // the launch's small vectors, one unconditional load per element
   typedef RdVec<D, F> V;
   constexpr int NVL = RD_VEC / RD_ROW_THREADS;
@@ -707,25 +721,18 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     }
     if (lane < K) late.logtype[di * K + lane] = logk;
     const bool bad = (lane < M && !(isfinite(logw) && isfinite(mu) && isfinite(sg))) || (lane < K && !isfinite(logk));
-    float u[4];
-    philox_uniforms(late.seed, (uint64_t)b, rnd, (uint64_t)l, TAG_DRAFT, u);
     // categorical over the lanes' log-probabilities: first index whose
     // running sum of exp exceeds u times the total
     auto draw = [&](float lp, int cnt, float uu) {
       float cs = lane < cnt ? expf(lp) : 0.f;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const float oo = __shfl_up(cs, off, 64);
-        if (lane >= off) cs += oo;
-      }
-      const float tot = __shfl(cs, cnt - 1, 64);
+      cs = wave_cumsum(cs);
+      const float tot = lane_val(cs, cnt - 1);
       const unsigned long long hit = __ballot(lane < cnt && uu * tot < cs);
       return hit ? (int)__builtin_ctzll(hit) : cnt - 1;
     };
-    const int z = draw(logw, M, u[0]);
-    const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
-    const float tau = expf(__shfl(mu, z, 64) + expf(__shfl(sg, z, 64)) * eps);
-    const int kk = draw(logk, K, u[3]);
+    const int z = draw(logw, M, u_z);
+    const float tau = expf(lane_val(mu, z) + expf(lane_val(sg, z)) * eps);
+    const int kk = draw(logk, K, u_k);
     const float lt = logf(tau);
     float cterm = -INFINITY;
     if (lane < M) {
@@ -734,7 +741,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     }
     const float cm = wave_max(cterm);
     const float lg = cm + logf(wave_sum(lane < M ? expf(cterm - cm) : 0.f));
-    const float lf = __shfl(logk, kk, 64);
+    const float lf = lane_val(logk, kk);
     const bool bad_any = __ballot(bad) != 0ull;
     if (lane == 0) {
       const float tn = tprev + tau;

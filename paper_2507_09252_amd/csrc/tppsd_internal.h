@@ -175,6 +175,8 @@ struct RowDraftArgs {
   float *x;                 // [B][2][d] residual stream of the step's rows
   bf16_t *xn;               // [B][2][d] the step's rows after the layer's LayerNorm (q, k, v input)
   float *part;              // [B][H][S][2][d_head + 2] split partials: maximum, sum, output sums
+  float *rng;               // [B][MG][4] per draft step: u for the component, the normal deviate, u for the
+                            // type (written by the step-0 launch)
   const bf16_t *pk;         // per layer Wo, W1, W2, Wqkv in MFMA fragment order (launch_pack_frags)
   const bf16_t *pk_e;       // [E; V_k1] in fragment order
   const bf16_t *pk_head;    // decoder head rows, zero-padded to 128, in fragment order (launch_pack_rd_head)

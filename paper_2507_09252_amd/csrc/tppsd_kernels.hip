@@ -1152,19 +1152,15 @@ __device__ void head_row(const float *lr, int M, int K, const HeadArgs &a, int b
   // whose running sum exceeds u times the total)
   auto sample = [&](float lp, int n, float u) {
     float c = lane < n ? expf(lp) : 0.f;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const float o = __shfl_up(c, off, 64);
-      if (lane >= off) c += o;
-    }
-    const float tot = __shfl(c, n - 1, 64);
+    c = wave_cumsum(c);
+    const float tot = lane_val(c, n - 1);
     const unsigned long long hit = __ballot(lane < n && u * tot < c);
     return hit ? (int)__builtin_ctzll(hit) : n - 1;
   };
   auto draw_tau = [&](const float u[4]) {
     const int z = sample(logw, M, u[0]);
     const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
-    const float muz = __shfl(mu, z, 64), sz = __shfl(sg, z, 64);
+    const float muz = lane_val(mu, z), sz = lane_val(sg, z);
     return expf(muz + expf(sz) * eps);
   };
   if (a.mode == HEAD_VERIFY) {
@@ -1172,7 +1168,7 @@ __device__ void head_row(const float *lr, int M, int K, const HeadArgs &a, int b
       const size_t di = (size_t)b * a.dr_stride + p;
       const float lg = logpdf(a.dr_tau[di]);
       const int kk = min(max(a.dr_k[di], 0), K - 1);
-      const float lf = __shfl(logk, kk, 64);
+      const float lf = lane_val(logk, kk);
       if (lane == 0) {
         a.v_logg[di] = lg;
         a.v_logf[di] = lf;
@@ -1185,7 +1181,7 @@ __device__ void head_row(const float *lr, int M, int K, const HeadArgs &a, int b
     const float tau = draw_tau(u);
     const int kk = sample(logk, K, u[3]);
     const float lg = logpdf(tau);
-    const float lf = __shfl(logk, kk, 64);
+    const float lf = lane_val(logk, kk);
     if (lane == 0) {
       const size_t di = (size_t)b * a.dr_stride + a.slot;
       const float tprev = (a.slot == 0) ? a.ev_t[(size_t)b * a.ev_stride + a.n[b] - 1] : a.d_t[di - 1];
@@ -1211,7 +1207,7 @@ __device__ void head_row(const float *lr, int M, int K, const HeadArgs &a, int b
     // end time (dropped; the sequence ends), the survival log(1 - G(T - t_N))
     const bool past = tn > T_end;
     const float lterm = past ? wave_log_survival(logw, mu, sg, lane < M, T_end - tlast)
-                             : logpdf(tau) + __shfl(logk, kk, 64);
+                             : logpdf(tau) + lane_val(logk, kk);
     if (lane != 0) return;
     a.ll[b] += (double)lterm;
     if (past) {
@@ -1975,12 +1971,8 @@ __global__ __launch_bounds__(NT) void k_draft_fused(DraftArgs a) {
       // first index whose running sum of exp(log p) exceeds u times the total
       auto draw = [&](float lp, int n, float u) {
         float c = lane < n ? expf(lp) : 0.f;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const float o = __shfl_up(c, off, 64);
-          if (lane >= off) c += o;
-        }
-        const float tot = __shfl(c, n - 1, 64);
+        c = wave_cumsum(c);
+        const float tot = lane_val(c, n - 1);
         const unsigned long long hit = __ballot(lane < n && u * tot < c);
         return hit ? (int)__builtin_ctzll(hit) : n - 1;
       };
@@ -2516,12 +2508,8 @@ __global__ __launch_bounds__(256, TPPSD_WAVE_DRAFT_WG_PER_CU) void k_draft_wave(
       if (lane < K) a.d_logtype[di * K + lane] = nlk;
       auto draw = [&](float lp_, int cnt, float u) {
         float cs = lane < cnt ? expf(lp_) : 0.f;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const float oo = __shfl_up(cs, off, 64);
-          if (lane >= off) cs += oo;
-        }
-        const float tot = __shfl(cs, cnt - 1, 64);
+        cs = wave_cumsum(cs);
+        const float tot = lane_val(cs, cnt - 1);
         const unsigned long long hit = __ballot(lane < cnt && u * tot < cs);
         return hit ? (int)__builtin_ctzll(hit) : cnt - 1;
       };
@@ -3311,13 +3299,9 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
         }
       }
       float c = lane < M ? expf(Tr[lane]) : 0.f;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const float o = __shfl_up(c, off, 64);
-        if (lane >= off) c += o;
-      }
+      c = wave_cumsum(c);
       if (lane < M) Tc[lane] = c;
-      const float tot = __shfl(c, M - 1, 64);
+      const float tot = lane_val(c, M - 1);
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -3395,12 +3379,8 @@ __global__ __launch_bounds__(256) void k_accept(AcceptArgs a) {
       const float *lD = a.d_logtype + ((size_t)b * MG + li) * K;
       const float lt_k = lane < K ? lT[lane] : 0.f;
       float c = lane < K ? fmaxf(0.f, expf(lt_k) - expf(lD[lane])) : 0.f;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const float o = __shfl_up(c, off, 64);
-        if (lane >= off) c += o;
-      }
-      const float tot = __shfl(c, K - 1, 64);
+      c = wave_cumsum(c);
+      const float tot = lane_val(c, K - 1);
       const unsigned long long hit = __ballot(lane < K && u[0] * tot < c);
       kL = hit ? (int)__builtin_ctzll(hit) : K - 1;
       lfL = lane_f(lt_k, kL);

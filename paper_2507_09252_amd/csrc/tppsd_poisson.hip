@@ -59,13 +59,9 @@ __global__ __launch_bounds__(256) void k_draft_poisson(PoissonDraftArgs a) {
   const float rate = a.params[0];
   const float lp = lane < K ? a.params[1 + lane] : -INFINITY;
   float c = lane < K ? expf(lp) : 0.f;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float o = __shfl_up(c, off, 64);
-    if (lane >= off) c += o;
-  }
+  c = wave_cumsum(c);
   cdf[w][lane] = c;
-  const float tot = __shfl(c, K - 1, 64);
+  const float tot = lane_val(c, K - 1);
   // if rounding puts u_3 C_K at C_K, the last type of positive probability
   const unsigned long long pos = __ballot(lane < K && lp > -INFINITY);
   const int k_last = pos ? 63 - __builtin_clzll(pos) : K - 1;
