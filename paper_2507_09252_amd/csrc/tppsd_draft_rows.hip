@@ -705,34 +705,32 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     if (nn < NH && r == (nn < 3 * M ? nn / M : 3)) sh.hv[nn] = acc + sh.vec[nn < 3 * M ? V::MIXB + nn : V::K2B + nn - 3 * M];
   });
   rd_sync();
+  // the log-softmaxes, the draft record and the draft event: wave 0 takes
+  // the mixture (component, interval, log g), wave 1 the type (the two
+  // chains are independent)
+  const size_t di = (size_t)b * MG + (l - 1);
+  // categorical over the lanes' log-probabilities: first index whose running
+  // sum of exp exceeds u times the total
+  auto draw = [&](float lp, int cnt, float uu) {
+    float cs = lane < cnt ? expf(lp) : 0.f;
+    cs = wave_cumsum(cs);
+    const float tot = lane_val(cs, cnt - 1);
+    const unsigned long long hit = __ballot(lane < cnt && uu * tot < cs);
+    return hit ? (int)__builtin_ctzll(hit) : cnt - 1;
+  };
   if (wave == 0) {
-    // the log-softmaxes, the draft record and the draft event
     const float lw = lane < M ? sh.hv[lane] : -INFINITY;
     const float mu = lane < M ? sh.hv[M + lane] : 0.f, sg = lane < M ? sh.hv[2 * M + lane] : 0.f;
-    const float lk = lane < K ? sh.hv[3 * M + lane] : -INFINITY;
-    const float mw = wave_max(lw), mk = wave_max(lk);
+    const float mw = wave_max(lw);
     const float logw = lw - mw - logf(wave_sum(lane < M ? expf(lw - mw) : 0.f));
-    const float logk = lk - mk - logf(wave_sum(lane < K ? expf(lk - mk) : 0.f));
-    const size_t di = (size_t)b * MG + (l - 1);
     if (lane < M) {
       late.mix[di * 3 * M + lane] = logw;
       late.mix[di * 3 * M + M + lane] = mu;
       late.mix[di * 3 * M + 2 * M + lane] = sg;
     }
-    if (lane < K) late.logtype[di * K + lane] = logk;
-    const bool bad = (lane < M && !(isfinite(logw) && isfinite(mu) && isfinite(sg))) || (lane < K && !isfinite(logk));
-    // categorical over the lanes' log-probabilities: first index whose
-    // running sum of exp exceeds u times the total
-    auto draw = [&](float lp, int cnt, float uu) {
-      float cs = lane < cnt ? expf(lp) : 0.f;
-      cs = wave_cumsum(cs);
-      const float tot = lane_val(cs, cnt - 1);
-      const unsigned long long hit = __ballot(lane < cnt && uu * tot < cs);
-      return hit ? (int)__builtin_ctzll(hit) : cnt - 1;
-    };
+    const bool bad = lane < M && !(isfinite(logw) && isfinite(mu) && isfinite(sg));
     const int z = draw(logw, M, u_z);
     const float tau = expf(lane_val(mu, z) + expf(lane_val(sg, z)) * eps);
-    const int kk = draw(logk, K, u_k);
     const float lt = logf(tau);
     float cterm = -INFINITY;
     if (lane < M) {
@@ -741,17 +739,27 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     }
     const float cm = wave_max(cterm);
     const float lg = cm + logf(wave_sum(lane < M ? expf(cterm - cm) : 0.f));
-    const float lf = lane_val(logk, kk);
     const bool bad_any = __ballot(bad) != 0ull;
     if (lane == 0) {
       const float tn = tprev + tau;
       late.tau[di] = tau;
       late.t[di] = tn;
-      late.k[di] = kk;
       late.logg[di] = lg;
-      late.logf[di] = lf;
       if (bad_any || !isfinite(tau)) atomicOr(late.status, TPPSD_STATUS_NONFINITE);
       sh.tok_t = tn;
+    }
+  } else if (wave == 1) {
+    const float lk = lane < K ? sh.hv[3 * M + lane] : -INFINITY;
+    const float mk = wave_max(lk);
+    const float logk = lk - mk - logf(wave_sum(lane < K ? expf(lk - mk) : 0.f));
+    if (lane < K) late.logtype[di * K + lane] = logk;
+    const bool bad_any = __ballot(lane < K && !isfinite(logk)) != 0ull;
+    const int kk = draw(logk, K, u_k);
+    const float lf = lane_val(logk, kk);
+    if (lane == 0) {
+      late.k[di] = kk;
+      late.logf[di] = lf;
+      if (bad_any) atomicOr(late.status, TPPSD_STATUS_NONFINITE);
       sh.tok_k = kk;
     }
   }
