@@ -29,6 +29,17 @@ HIPCC_FLAGS = [
 ]
 
 
+# per-source additions: the row-drafting kernels take their first scalar
+# arguments preloaded into registers (gfx950 kernel-argument preloading; a
+# code object prologue loads them where the firmware does not)
+FILE_FLAGS = {"tppsd_draft_rows.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=8"]}
+
+
+def source_flags(src: str) -> list:
+    """hipcc flags for one source file of the library."""
+    return HIPCC_FLAGS + FILE_FLAGS.get(os.path.basename(src), [])
+
+
 def _torch_lib_dir() -> str:
     import importlib.util
     spec = importlib.util.find_spec("torch")
@@ -55,7 +66,7 @@ def build(verbose: bool = False) -> str:
     from concurrent.futures import ThreadPoolExecutor
     srcs = ("tppsd_kernels.hip", "tppsd_attention.hip", "tppsd_poisson.hip", "tppsd_draft_rows.hip", "tppsd.cpp")
     objs = [os.path.join(BUILD, src + ".o") for src in srcs]
-    cmds = [[hipcc] + HIPCC_FLAGS + inc + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmds = [[hipcc] + source_flags(src) + inc + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
             for src, obj in zip(srcs, objs)]
     with ThreadPoolExecutor(len(cmds)) as ex:
         for f in [ex.submit(_run, c, verbose) for c in cmds]:

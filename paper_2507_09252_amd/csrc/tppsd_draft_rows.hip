@@ -38,12 +38,24 @@ namespace {
 constexpr int RD_WAVES = RD_ROW_THREADS / 64;
 constexpr int RD_VEC = 2048;   // floats of a row launch's staged vectors (RdVec)
 
+// a load the compiler may issue as a scalar one wherever it can prove the
+// address uniform: the word does not change while the kernel runs (the
+// sequence's header words and draw numbers are written by other launches
+// only)
+template <class T>
+__device__ __forceinline__ T load_const(const T *p) {
+  return *(const __attribute__((address_space(4))) T *)p;
+}
+
 // ---------------------------------------------------------------------------
 // split attention: workgroup (s, h, b) takes keys [s RD_KEYS, (s + 1) RD_KEYS)
 // of head h of sequence b
 // ---------------------------------------------------------------------------
 template <int D, int DH>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_rd_attn(RowDraftArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_rd_attn(const int32_t *done_p,
+                                                                                          const int32_t *len_p,
+                                                                                          int step, int layer,
+                                                                                          RowDraftArgs a) {
   constexpr int NG = 256 / DH;              // lane groups over the value blocks
   constexpr int BPL = RD_KEYS / 8 / NG;     // value blocks per lane
   static_assert(DH == 32 && D % 128 == 0, "q, k, v: 32 groups of 8 lanes, 16 elements per lane and pass of 128");
@@ -62,22 +74,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   // row r of the head, lane j = tid % 8 elements 16 j .. + 15 of every 128
   constexpr int NC = D / 128;               // 128-element chunks per row
   const int r = tid >> 3, j8 = tid & 7;
-  // Every scalar the split needs is loaded up front in two batches, one wait
-  // each: the kernel arguments, then the sequence's header words and the
-  // layer's weight pointers. (Left to itself the compiler sinks each load to
-  // the branch that first needs it and pays a round trip per branch.) The asm
-  // statements only take values, which holds each load ahead of them.
-  const int step = a.step, layer = a.layer, cap = d.cap, nh = d.H;
+  // The leading arguments (the header words' arrays, step and layer) arrive
+  // preloaded in registers; every other scalar the split needs (kernel
+  // arguments, the layer's weight pointers, the sequence's header words) is
+  // loaded up front in one batch and waited for once. (Left to itself the
+  // compiler sinks each load to the branch that first needs it and pays a
+  // round trip per branch.) The asm statement only takes values, which holds
+  // each load ahead of it.
+  const int cap = d.cap, nh = d.H;
   const char *kcb = d.kc, *vcb = d.vc, *xn = (const char *)a.xn;
   const size_t lbytes = d.layer_bytes;
-  const int32_t *done_p = d.done, *len_p = d.lenD;
-  asm volatile("" ::"s"(step), "s"(layer), "s"(cap), "s"(nh), "s"(kcb), "s"(vcb), "s"(xn), "s"(lbytes), "s"(done_p),
-               "s"(len_p));
   const FusedLayerW &lw = d.layer[layer];
   const bf16_t *wqkv = (const bf16_t *)lw.qkv_w;
   const float *qkvb = lw.qkv_b;
-  const int done = done_p[b], lenD = len_p[b];
-  asm volatile("" ::"s"(done), "s"(lenD), "s"(wqkv), "s"(qkvb));
+  const int done = load_const(done_p + b), lenD = load_const(len_p + b);
+  asm volatile("" ::"s"(cap), "s"(nh), "s"(kcb), "s"(vcb), "s"(xn), "s"(lbytes), "s"(wqkv), "s"(qkvb), "s"(done),
+               "s"(lenD));
   auto wrow = [&](int which) { return wqkv + (size_t)(which * D + h * DH + r) * D + 16 * j8; };
   // the LayerNorm'd rows and this head's query rows of W_qkv
   const int P = step == 1 ? 2 : 1;
@@ -455,14 +467,6 @@ __device__ __forceinline__ void rd_embed(int K, const float *freq, const bf16_t 
   }
 }
 
-// a load the compiler may issue as a scalar one wherever it can prove the
-// address uniform: the word does not change while the kernel runs (the
-// sequence's header words are written by other launches only)
-template <class T>
-__device__ __forceinline__ T load_const(const T *p) {
-  return *(const __attribute__((address_space(4))) T *)p;
-}
-
 // kernel arguments a row launch reads only late (the decoder, the draw and
 // the next token), held in registers from the start
 struct RdLate {
@@ -491,31 +495,21 @@ template <int D, int F> struct RdVec {
 // them for layer 0; step l >= 1, layer ly finishes layer ly of the step's
 // rows after its attention.
 template <int D, int F, int DH>
-__global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
+__global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_p, const int32_t *len_p,
+                                                            const float *part, float *xa, const bf16_t *pk, int l,
+                                                            int ly, int part_cnt, RowDraftArgs a) {
   static_assert(D % 64 == 0 && F % 32 == 0 && D % 32 == 0, "row kernel widths");
   __shared__ RdShared<D, F, DH> sh;
   const DraftArgs &d = a.d;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // Scalar operands come in two batches, one wait each: the kernel arguments
-  // the first loads need, then what they point at (the layer's vector
-  // pointers, the sequence's header words) together with the arguments read
-  // late in the launch. (Left alone, the compiler loads each where it is
-  // first needed and waits there: a dozen round trips before the first
-  // barrier, more in the draw.) The asm statements only take values, which
-  // holds each load ahead of them.
-  const int L = d.L, M = d.M, K = d.K;
-  const int l = a.step, ly = a.layer;
-  float *xa = a.x;
-  const float *part = a.part, *rngp = a.rng;
-  const bf16_t *pk = a.pk;
-  const int nh = d.H, S = a.S, cap = d.cap, evs = d.ev_stride, MG = d.MG;
-  const int32_t *done_p = d.done, *len_p = d.lenD, *n_p = d.n;
-  const float *evt = d.ev_t, *dtp = d.d_t;
-  // (d.F only completes the four words from d.F to d.L, so that they come in
-  // one load and no register of it is reused while in flight)
-  asm volatile("" ::"s"(l), "s"(ly), "s"(L), "s"(M), "s"(K), "s"(nh), "s"(S), "s"(cap), "s"(evs), "s"(MG), "s"(part),
-               "s"(xa), "s"(pk), "s"(done_p), "s"(len_p), "s"(n_p), "s"(evt), "s"(dtp), "s"(d.F),
-               "s"(rngp));
+  // The leading arguments (the header words' arrays, the partials, the
+  // residual rows, the packed matrices, step, layer and the partials per
+  // sequence) arrive preloaded in registers, so the first loads and the
+  // header words need no kernel-argument load. Every other scalar comes in
+  // one batch, waited for once. (Left alone, the compiler loads each where it
+  // is first needed and waits there: a dozen round trips before the first
+  // barrier, more in the draw.) The asm statement only takes values, which
+  // holds each load ahead of it.
   float *xg = xa + (size_t)b * 2 * D;
   const bf16_t *wl = pk + (size_t)ly * rd_layer_elems<D, F>();
   if (l == 0) {
@@ -523,17 +517,20 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     if (done) return;
     // every step's draw numbers for the round, which depend on no result of
     // the steps: thread j takes step j + 1 (u for the component, the
-    // Box-Muller normal deviate, u for the type)
+    // Box-Muller normal deviate, u for the type), and step 1's previous time,
+    // the last committed event's (a later step's is written by the step
+    // before it)
     const uint64_t rnd = (uint64_t)d.rnd[b];
+    const float t_last = d.ev_t[(size_t)b * d.ev_stride + n - 1];
     for (int j = tid; j < d.gamma; j += RD_ROW_THREADS) {
       float u[4];
       philox_uniforms(d.seed, (uint64_t)b, rnd, (uint64_t)(j + 1), TAG_DRAFT, u);
       const float eps = sqrtf(-2.f * logf(u[1])) * cosf(6.28318530717958647692f * u[2]);
-      *(float4 *)(a.rng + ((size_t)b * MG + j) * 4) = make_float4(u[0], eps, u[3], 0.f);
+      *(float4 *)(a.rng + ((size_t)b * d.MG + j) * 4) = make_float4(u[0], eps, u[3], j == 0 ? t_last : 0.f);
     }
     for (int p = 0; p < 2; ++p) {
       const size_t i = (size_t)b * d.ev_stride + n - 2 + p;
-      rd_embed<D>(K, d.freq, (const bf16_t *)d.type_emb, sh.xs[p], d.ev_t[i], d.ev_k[i]);
+      rd_embed<D>(d.K, d.freq, (const bf16_t *)d.type_emb, sh.xs[p], d.ev_t[i], d.ev_k[i]);
     }
     rd_sync();
     rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[0].ln1_g, d.layer[0].ln1_b, 2);
@@ -543,48 +540,53 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
     return;
   }
   const int P = l == 1 ? 2 : 1;
-  const bool last = ly == L - 1;
   // every vector load of the launch in flight at once, in the order of use,
   // into registers: the split partials of the sequence (all splits of the
   // slab; those past the step's keys are ignored below), the residual rows,
-  // the output projection, then (behind the second scalar batch) the small
-  // vectors and both FFN products (after the last layer the decoder's follow
-  // once the first FFN product is done)
+  // the output projection, then (behind the scalar batch) the small vectors
+  // and both FFN products (after the last layer the decoder's follow once the
+  // first FFN product is done)
   constexpr int NPV = RD_MAX_PART / RD_ROW_THREADS;
   float pv[NPV];
   {
-    const int cnt = nh * S * 2 * (DH + 2);
-    const float *src = part + (size_t)b * cnt;
+    const float *src = part + (size_t)b * part_cnt;
 #pragma unroll
     for (int i = 0; i < NPV; ++i) {
       const int k = tid + i * RD_ROW_THREADS;
-      pv[i] = k < cnt ? src[k] : 0.f;
+      pv[i] = k < part_cnt ? src[k] : 0.f;
     }
   }
   const float xv = tid < P * D ? xg[tid] : 0.f;
   RdFrags<D, D> fo;
   fo.load_packed(wl);
-  // second batch
+  // the scalar batch
+  const int L = d.L, M = d.M, K = d.K;
+  const int nh = d.H, S = a.S, cap = d.cap, MG = d.MG;
+  float *rngp = a.rng;
   const FusedLayerW &w = d.layer[ly];
-  const FusedLayerW &wn = d.layer[last ? 0 : ly + 1];
+  const FusedLayerW &wn = d.layer[min(ly + 1, FD_MAX_LAYERS - 1)];   // the next layer's (unused after the last)
   const float *outb = w.out_b, *ln2g = w.ln2_g, *ln2b = w.ln2_b, *f1b = w.ffn1_b, *f2b = w.ffn2_b;
-  const float *n1g = last ? d.lnf_g : wn.ln1_g, *n1b = last ? d.lnf_b : wn.ln1_b;
+  const float *ln1g_next = wn.ln1_g, *ln1b_next = wn.ln1_b, *lnfg = d.lnf_g, *lnfb = d.lnf_b;
   const float *k1b = d.k1_b, *mixb = d.mix_b, *k2b = d.k2_b, *freq = d.freq;
   const float *l0g = d.layer[0].ln1_g, *l0b = d.layer[0].ln1_b;
-  const int done = load_const(done_p + b), base = load_const(len_p + b), n = load_const(n_p + b);
-  // the step's draw: u for the component, the normal deviate, u for the type
-  // (every step's, written by the step-0 launch; read in every layer, used in
-  // the last)
-  const float *rs = rngp + ((size_t)b * MG + (l - 1)) * 4;
-  const float u_z = load_const(rs), eps = load_const(rs + 1), u_k = load_const(rs + 2);
+  const int done = load_const(done_p + b), base = load_const(len_p + b);
   const RdLate late{a.pk_e, a.pk_head, (const bf16_t *)d.type_emb, a.xn, d.status, d.d_tau, d.d_t, d.d_logg, d.d_logf,
                     d.d_mix, d.d_logtype, d.d_k, d.gamma};
-  asm volatile("" ::"s"(outb), "s"(ln2g), "s"(ln2b), "s"(f1b), "s"(f2b), "s"(n1g), "s"(n1b), "s"(k1b), "s"(mixb),
-               "s"(k2b), "s"(freq), "s"(l0g), "s"(l0b), "s"(done), "s"(base), "s"(n), "s"(u_z), "s"(eps), "s"(u_k),
-               "s"(late.pk_e),
-               "s"(late.pk_head), "s"(late.temb), "s"(late.xn), "s"(late.status), "s"(late.tau), "s"(late.t),
-               "s"(late.logg), "s"(late.logf), "s"(late.mix), "s"(late.logtype), "s"(late.k),
-               "s"(late.gamma));
+  // (d.F only completes the four words from d.F to d.L, so that they come in
+  // one load and no register of it is reused while in flight)
+  asm volatile("" ::"s"(L), "s"(M), "s"(K), "s"(d.F), "s"(nh), "s"(S), "s"(cap), "s"(MG), "s"(rngp), "s"(outb), "s"(ln2g), "s"(ln2b), "s"(f1b), "s"(f2b), "s"(ln1g_next),
+               "s"(ln1b_next), "s"(lnfg), "s"(lnfb), "s"(k1b), "s"(mixb), "s"(k2b), "s"(freq), "s"(l0g), "s"(l0b),
+               "s"(done), "s"(base), "s"(late.pk_e), "s"(late.pk_head), "s"(late.temb), "s"(late.xn),
+               "s"(late.status), "s"(late.tau), "s"(late.t), "s"(late.logg), "s"(late.logf), "s"(late.mix),
+               "s"(late.logtype), "s"(late.k), "s"(late.gamma));
+  const bool last = ly == L - 1;
+  const float *n1g = last ? lnfg : ln1g_next, *n1b = last ? lnfb : ln1b_next;
+  // read late, waited for where used: the step's draw numbers (u for the
+  // component, the normal deviate, u for the type) and the time the drawn
+  // interval is added to (the last committed event's, or the previous
+  // draft's)
+  const float *rs = rngp + ((size_t)b * MG + (l - 1)) * 4;
+  const float u_z = load_const(rs), eps = load_const(rs + 1), u_k = load_const(rs + 2), tprev = load_const(rs + 3);
   // the launch's small vectors, one unconditional load per element
   typedef RdVec<D, F> V;
   constexpr int NVL = RD_VEC / RD_ROW_THREADS;
@@ -612,10 +614,6 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
   RdFrags<4 * D, D> fe;
   RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
   const int pos0 = base + (l == 1 ? 0 : l);
-  // last layer: the time the drawn interval is added to (the last committed
-  // event, or the previous draft), read now rather than behind the decoder
-  float tprev = 0.f;
-  if (last) tprev = l == 1 ? evt[(size_t)b * evs + n - 1] : dtp[(size_t)b * MG + (l - 2)];
   // (keeps the stores below, which wait for the partials, behind every load)
   __builtin_amdgcn_sched_barrier(0);
   if (done) return;   // workgroup-uniform; the loads above are dropped
@@ -746,6 +744,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(RowDraftArgs a) {
       late.t[di] = tn;
       late.logg[di] = lg;
       if (bad_any || !isfinite(tau)) atomicOr(late.status, TPPSD_STATUS_NONFINITE);
+      if (more) rngp[((size_t)b * MG + l) * 4 + 3] = tn;   // the next step's previous time
       sh.tok_t = tn;
     }
   } else if (wave == 1) {
@@ -791,20 +790,28 @@ void launch_pack_rd_head(const void *mix_w, const void *k2_w, int M, int K, int 
 
 void launch_draft_rows(RowDraftArgs a, hipStream_t st, const hipEvent_t *ev) {
   const int B = a.d.B, H = a.d.H;
+  const int part_cnt = H * a.S * 2 * (32 + 2);   // split partials per sequence
   int j = 0;   // launch index: event pair j brackets launch j
   auto e0 = [&]() { return ev ? ev[2 * j] : nullptr; };
   auto e1 = [&]() { return ev ? ev[2 * j + 1] : nullptr; };
+  // (the row kernel's leading arguments, preloaded into registers, repeat
+  // fields of a that its first loads need)
+  auto rows = [&]() {
+    hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, e0(), e1(), 0, a.d.done,
+                          a.d.lenD, (const float *)a.part, a.x, a.pk, a.step, a.layer, part_cnt, a);
+  };
   a.step = 0;
   a.layer = 0;
-  hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, e0(), e1(), 0, a);
+  rows();
   ++j;
   for (int l = 1; l <= a.d.gamma; ++l) {
     a.step = l;
     for (int ly = 0; ly < a.d.L; ++ly) {
       a.layer = ly;
-      hipExtLaunchKernelGGL(k_rd_attn<128, 32>, dim3(a.S, H, B), dim3(256), 0, st, e0(), e1(), 0, a);
+      hipExtLaunchKernelGGL(k_rd_attn<128, 32>, dim3(a.S, H, B), dim3(256), 0, st, e0(), e1(), 0, a.d.done,
+                            a.d.lenD, a.step, a.layer, a);
       ++j;
-      hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, e0(), e1(), 0, a);
+      rows();
       ++j;
     }
   }
