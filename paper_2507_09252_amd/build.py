@@ -29,10 +29,13 @@ HIPCC_FLAGS = [
 ]
 
 
-# per-source additions: the row-drafting kernels take their first scalar
-# arguments preloaded into registers (gfx950 kernel-argument preloading; a
-# code object prologue loads them where the firmware does not)
-FILE_FLAGS = {"tppsd_draft_rows.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=8"]}
+# Kernels take their leading scalar arguments preloaded into registers
+# (gfx950 kernel-argument preloading, as many as fit the user SGPRs; a code
+# object prologue loads them where the firmware does not), so that their
+# first loads need no kernel-argument load.
+PRELOAD = ["-mllvm", "-amdgpu-kernarg-preload-count=16"]
+FILE_FLAGS = {"tppsd_draft_rows.hip": PRELOAD, "tppsd_kernels.hip": PRELOAD, "tppsd_attention.hip": PRELOAD,
+              "tppsd_poisson.hip": PRELOAD}
 
 
 def source_flags(src: str) -> list:
