@@ -176,6 +176,14 @@ __global__ void k_attnhp_update(float *__restrict__ x, const ACT *__restrict__ o
 // ---------------------------------------------------------------------------
 
 constexpr int LN_REG_MAX = 16;   // row widths up to 1024 are held in registers
+constexpr int LN_VEC_MAX = 4;    // as 16-byte vectors when the width is a multiple of 4
+// four consecutive outputs (the index a multiple of 4)
+__device__ __forceinline__ void st4(float *p, size_t i, float a, float b, float c, float d) {
+  *(float4 *)(p + i) = make_float4(a, b, c, d);
+}
+__device__ __forceinline__ void st4(bf16_t *p, size_t i, float a, float b, float c, float d) {
+  *(uint2 *)(p + i) = make_uint2(pk2bf(a, b), pk2bf(c, d));
+}
 template <typename ACT>
 __global__ __launch_bounds__(256) void k_layernorm(const float *__restrict__ x, ACT *__restrict__ y,
                                                    const float *__restrict__ g, const float *__restrict__ bt,
@@ -184,6 +192,42 @@ __global__ __launch_bounds__(256) void k_layernorm(const float *__restrict__ x, 
   const int lane = threadIdx.x & 63;
   if (row >= T) return;
   const float *xr = x + (size_t)row * d;
+  const bool vec = d % 4 == 0 && d <= 4 * 64 * LN_VEC_MAX &&
+                   (((uintptr_t)x | (uintptr_t)g | (uintptr_t)bt) & 15) == 0 && ((uintptr_t)y & 7) == 0;
+  if (vec) {
+    // lane owns columns 4 (lane + 64 i) .. + 3: the row, gain and bias as
+    // 16-byte loads, all issued before the reductions, and 4 columns per store
+    float4 xv[LN_VEC_MAX], gv[LN_VEC_MAX], bv[LN_VEC_MAX];
+#pragma unroll
+    for (int i = 0; i < LN_VEC_MAX; ++i) {
+      const int j = 4 * (lane + 64 * i), jc = min(j, d - 4);   // (columns past the row re-read its last four, unused)
+      xv[i] = *(const float4 *)(xr + jc);
+      gv[i] = *(const float4 *)(g + jc);
+      bv[i] = *(const float4 *)(bt + jc);
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < LN_VEC_MAX; ++i)
+      if (4 * (lane + 64 * i) < d) s += (xv[i].x + xv[i].y) + (xv[i].z + xv[i].w);
+    const float mean = wave_sum(s) / (float)d;
+    float v = 0.f;
+#pragma unroll
+    for (int i = 0; i < LN_VEC_MAX; ++i)
+      if (4 * (lane + 64 * i) < d) {
+        const float c0 = xv[i].x - mean, c1 = xv[i].y - mean, c2 = xv[i].z - mean, c3 = xv[i].w - mean;
+        v += (c0 * c0 + c1 * c1) + (c2 * c2 + c3 * c3);
+      }
+    const float rstd = 1.f / sqrtf(wave_sum(v) / (float)d + 1e-5f);
+#pragma unroll
+    for (int i = 0; i < LN_VEC_MAX; ++i) {
+      const int j = 4 * (lane + 64 * i);
+      if (j >= d) continue;
+      const float o0 = (xv[i].x - mean) * rstd * gv[i].x + bv[i].x, o1 = (xv[i].y - mean) * rstd * gv[i].y + bv[i].y;
+      const float o2 = (xv[i].z - mean) * rstd * gv[i].z + bv[i].z, o3 = (xv[i].w - mean) * rstd * gv[i].w + bv[i].w;
+      st4(y, (size_t)row * d + j, o0, o1, o2, o3);
+    }
+    return;
+  }
   if (d <= 64 * LN_REG_MAX) {
     // the row in registers, read once (same summation order as below)
     float xv[LN_REG_MAX];
