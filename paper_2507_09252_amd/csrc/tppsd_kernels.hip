@@ -333,47 +333,72 @@ __device__ __forceinline__ void load8f(const float *p, float v[8]) {
   const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
   v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
+// The operands of an 8-column epilogue that do not depend on the product
+// (bias, the residual's row, the row's cache position), fetched apart so that
+// a kernel can load them before its main loop.
+struct Epi8In {
+  float bv[8], xv[8];
+  int pos;
+};
+__device__ __forceinline__ void epilogue8_fetch(const Epi &e, int r, int n, Epi8In &in) {
+  switch (e.mode) {
+    case EPI_STORE:
+    case EPI_F32:
+      if (e.bias) load8f(e.bias + n, in.bv);
+      break;
+    case EPI_RESID:
+      load8f((const float *)e.out + (size_t)r * e.ldo + n, in.xv);
+      load8f(e.bias + n, in.bv);
+      break;
+    case EPI_RELU:
+      load8f(e.bias + n, in.bv);
+      break;
+    case EPI_QKV:
+      load8f(e.bias + n, in.bv);
+      if (n >= e.d) {
+        const int b = r / e.P;
+        in.pos = e.start[b] + e.start_off + (r - b * e.P);
+      }
+      break;
+    case EPI_HEAD:
+      if (n >= e.split) load8f(e.bias + (n - e.split), in.bv);
+      break;
+  }
+}
 template <typename ACT>
-__device__ __forceinline__ void epilogue8(const Epi &e, int r, int n, const float acc[8]) {
-  float v[8], bv[8];
+__device__ __forceinline__ void epilogue8(const Epi &e, int r, int n, const float acc[8], const Epi8In &in) {
+  float v[8];
   switch (e.mode) {
     case EPI_STORE:
     case EPI_F32: {
-      if (e.bias) load8f(e.bias + n, bv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = acc[i] + (e.bias ? bv[i] : 0.f);
+      for (int i = 0; i < 8; ++i) v[i] = acc[i] + (e.bias ? in.bv[i] : 0.f);
       if (e.mode == EPI_F32) store8((float *)e.out + (size_t)r * e.ldo + n, v);
       else store8((ACT *)e.out + (size_t)r * e.ldo + n, v);
       break;
     }
     case EPI_RESID: {
-      float *x = (float *)e.out + (size_t)r * e.ldo + n;
-      float xv[8];
-      load8f(x, xv);
-      load8f(e.bias + n, bv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = xv[i] + (acc[i] + bv[i]);
-      store8(x, v);
+      for (int i = 0; i < 8; ++i) v[i] = in.xv[i] + (acc[i] + in.bv[i]);
+      store8((float *)e.out + (size_t)r * e.ldo + n, v);
       break;
     }
     case EPI_RELU: {
-      load8f(e.bias + n, bv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = fmaxf(acc[i] + bv[i], 0.f);
+      for (int i = 0; i < 8; ++i) v[i] = fmaxf(acc[i] + in.bv[i], 0.f);
       store8((ACT *)e.out + (size_t)r * e.ldo + n, v);
       break;
     }
     case EPI_QKV: {
-      load8f(e.bias + n, bv);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = acc[i] + bv[i];
+      for (int i = 0; i < 8; ++i) v[i] = acc[i] + in.bv[i];
       const int which = n / e.d, c = n - which * e.d;
       if (which == 0) {
         store8((ACT *)e.q + (size_t)r * e.d + c, v);
       } else {
-        const int b = r / e.P, p = r - b * e.P;
+        const int b = r / e.P;
         const int h = c / e.dh, j = c - h * e.dh;
-        const int pos = e.start[b] + e.start_off + p;
+        const int pos = in.pos;
         if (pos < e.cap) {
           const size_t row0 = ((size_t)b * e.H + h) * e.cap;
           if (which == 1) {
@@ -393,9 +418,8 @@ __device__ __forceinline__ void epilogue8(const Epi &e, int r, int n, const floa
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] = acc[i];
       } else {
-        load8f(e.bias + (n - e.split), bv);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = tanhf(acc[i] + bv[i]);
+        for (int i = 0; i < 8; ++i) v[i] = tanhf(acc[i] + in.bv[i]);
       }
       store8((ACT *)e.out + (size_t)r * e.ldo + n, v);
       break;
@@ -640,7 +664,9 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
     float cv[8];
     load8f(Cs + row * CLD + 8 * c8, cv);
     if (n + 8 <= N) {
-      epilogue8<ELT>(e, r, n, cv);
+      Epi8In in;
+      epilogue8_fetch(e, r, n, in);
+      epilogue8<ELT>(e, r, n, cv, in);
     } else {
       for (int i = 0; i < N - n; ++i) epilogue<ELT>(e, r, n + i, cv[i]);
     }
@@ -1106,6 +1132,17 @@ __global__ __launch_bounds__(256) void k_gemm_dl(const bf16_t *__restrict__ X, c
     const int p = (4 * i + wave) * 64 + lane, row = p / CPR, c = (p % CPR) ^ (row % CPR);
     srcB[i] = W + (size_t)min(n0 + row, N - 1) * K + 8 * c;
   }
+  // the epilogue's operands that do not depend on the product, loaded
+  // before the main loop (older than its loads, so its counted waits still
+  // hold), so that the epilogue waits on no memory
+  constexpr int NEP = (BM * (BN / 8) + 255) / 256;
+  Epi8In ein[NEP];
+#pragma unroll
+  for (int k = 0; k < NEP; ++k) {
+    const int gi = tid + 256 * k, row = gi / (BN / 8), c8 = gi - row * (BN / 8);
+    const int r = m0 + row, n = n0 + 8 * c8;
+    if (gi < BM * (BN / 8) && r < T && n + 8 <= N) epilogue8_fetch(e, r, n, ein[k]);
+  }
   f32x4_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -1119,14 +1156,15 @@ __global__ __launch_bounds__(256) void k_gemm_dl(const bf16_t *__restrict__ X, c
 #pragma unroll
       for (int v = 0; v < 4; ++v) Cs[(wm + 16 * i + 4 * g + v) * CLD + wn + 16 * j + rr] = acc[i][j][v];
   __syncthreads();
-  for (int gi = tid; gi < BM * (BN / 8); gi += 256) {
-    const int row = gi / (BN / 8), c8 = gi - row * (BN / 8);
+#pragma unroll
+  for (int k = 0; k < NEP; ++k) {
+    const int gi = tid + 256 * k, row = gi / (BN / 8), c8 = gi - row * (BN / 8);
     const int r = m0 + row, n = n0 + 8 * c8;
-    if (r >= T || n >= N) continue;
+    if (gi >= BM * (BN / 8) || r >= T || n >= N) continue;
     float cv[8];
     load8f(Cs + row * CLD + 8 * c8, cv);
     if (n + 8 <= N) {
-      epilogue8<bf16_t>(e, r, n, cv);
+      epilogue8<bf16_t>(e, r, n, cv, ein[k]);
     } else {
       for (int i = 0; i < N - n; ++i) epilogue<bf16_t>(e, r, n + i, cv[i]);
     }
