@@ -569,6 +569,17 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
 #pragma unroll
   for (int u = 0; u < D; ++u)
     if (u < nst) gload(ra[u], rx[u], rb[u], u * BK);
+  // then, for tiles of one epilogue item per thread, the epilogue's operands
+  // that do not depend on the product, so that the epilogue waits on no
+  // memory (larger tiles fetch them in the epilogue: the registers would
+  // cost occupancy)
+  constexpr bool EPRE = BM * (BN / 8) <= 256;
+  Epi8In ein;
+  if (EPRE) {
+    const int row = tid / (BN / 8), c8 = tid - row * (BN / 8);
+    const int r = m0 + row, n = n0 + 8 * c8;
+    if (tid < BM * (BN / 8) && r < T && n + 8 <= N) epilogue8_fetch(e, r, n, ein);
+  }
   if (LN) {
     for (int k = tid; k < K; k += 256) {
       gs[k] = lg[k];
@@ -664,9 +675,8 @@ __global__ __launch_bounds__(256) void k_gemm_lds(const ELT *__restrict__ X, con
     float cv[8];
     load8f(Cs + row * CLD + 8 * c8, cv);
     if (n + 8 <= N) {
-      Epi8In in;
-      epilogue8_fetch(e, r, n, in);
-      epilogue8<ELT>(e, r, n, cv, in);
+      if (!EPRE) epilogue8_fetch(e, r, n, ein);
+      epilogue8<ELT>(e, r, n, cv, ein);
     } else {
       for (int i = 0; i < N - n; ++i) epilogue<ELT>(e, r, n + i, cv[i]);
     }
