@@ -48,10 +48,10 @@ __device__ __forceinline__ void sink_adjust(float &M, float &L, float &O) {
 // column) is one 16-byte load from the position-blocked value cache.
 
 template <int DH, int ROLE, int QT, int NW = 4>
-__global__ __launch_bounds__(64 * NW) void k_attn_mfma(const bf16_t *__restrict__ q, const bf16_t *__restrict__ kc,
-                                                   const bf16_t *__restrict__ vc, bf16_t *__restrict__ o,
-                                                   const int32_t *__restrict__ start, int start_off,
-                                                   const int32_t *__restrict__ done, int P, int H, int cap,
+__global__ __launch_bounds__(64 * NW) void k_attn_mfma(int H, int P, const int32_t *__restrict__ start,
+                                                   const int32_t *__restrict__ done, int start_off,
+                                                   const bf16_t *__restrict__ q, const bf16_t *__restrict__ kc,
+                                                   const bf16_t *__restrict__ vc, bf16_t *__restrict__ o, int cap,
                                                    int splits, float *__restrict__ part, int sink) {
   constexpr int KT = 32, NDT = DH / 16, NC = DH >= 32 ? DH / 32 : 1, NQ = 16 * QT;
   static_assert(NW == 4 || NW == 8, "four or eight waves");
@@ -60,8 +60,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(const bf16_t *__restrict_
   const int bh = blockIdx.x, b = bh / H, h = bh - b * H, split = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, rr = lane & 15, g = lane >> 4;
   const int d = H * DH;
-  const bool skip = done != nullptr && done[b] != 0;
-  const int base = start[b] + start_off;
+  // the header words in one batch with the remaining arguments (the leading
+  // ones arrive preloaded; the finished flag is read unconditionally, from
+  // the start array when there is none)
+  const int dv = done ? done[b] : start[b];
+  const int sv = start[b];
+  asm volatile("" ::"s"(dv), "s"(sv), "s"(cap), "s"(splits));
+  const bool skip = done != nullptr && dv != 0;
+  const int base = sv + start_off;
   const int n_keys = skip ? 0 : min(base + P, cap);   // never past the cache slab
   int chunk = (n_keys + splits - 1) / splits;
   chunk = (chunk + KT - 1) / KT * KT;
@@ -285,10 +291,10 @@ __global__ __launch_bounds__(64 * NW) void k_attn_mfma(const bf16_t *__restrict_
 // scores each lane holds. V is read straight from memory (16 consecutive
 // columns of one key per lane group).
 template <int DH, int ROLE, int QT>
-__global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__ q, const float *__restrict__ kc,
-                                                       const float *__restrict__ vc, float *__restrict__ o,
-                                                       const int32_t *__restrict__ start, int start_off,
-                                                       const int32_t *__restrict__ done, int P, int H, int cap,
+__global__ __launch_bounds__(256) void k_attn_mfma_f32(int H, int P, const int32_t *__restrict__ start,
+                                                       const int32_t *__restrict__ done, int start_off,
+                                                       const float *__restrict__ q, const float *__restrict__ kc,
+                                                       const float *__restrict__ vc, float *__restrict__ o, int cap,
                                                        int splits, float *__restrict__ part, int sink) {
   constexpr int KT = 32, NDT = DH / 16, NQ = 16 * QT;
   __shared__ float red_m[4][NQ], red_l[4][NQ];
@@ -296,8 +302,14 @@ __global__ __launch_bounds__(256) void k_attn_mfma_f32(const float *__restrict__
   const int bh = blockIdx.x, b = bh / H, h = bh - b * H, split = blockIdx.z;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, rr = lane & 15, g = lane >> 4;
   const int d = H * DH;
-  const bool skip = done != nullptr && done[b] != 0;
-  const int base = start[b] + start_off;
+  // the header words in one batch with the remaining arguments (the leading
+  // ones arrive preloaded; the finished flag is read unconditionally, from
+  // the start array when there is none)
+  const int dv = done ? done[b] : start[b];
+  const int sv = start[b];
+  asm volatile("" ::"s"(dv), "s"(sv), "s"(cap), "s"(splits));
+  const bool skip = done != nullptr && dv != 0;
+  const int base = sv + start_off;
   const int n_keys = skip ? 0 : min(base + P, cap);   // never past the cache slab
   int chunk = (n_keys + splits - 1) / splits;
   chunk = (chunk + KT - 1) / KT * KT;
@@ -490,7 +502,7 @@ static void attn_mfma(const ACT *Q, const ACT *Kc, const ACT *Vc, ACT *O, const 
   if (eight) splits = 1;
   dim3 grid(B * H, 1, splits);
   auto go = [&](auto kern, int nt) {
-    hipExtLaunchKernelGGL(kern, grid, dim3(nt), 0, s, ev0, ev1, 0, Q, Kc, Vc, O, start, start_off, done, P, H, cap,
+    hipExtLaunchKernelGGL(kern, grid, dim3(nt), 0, s, ev0, ev1, 0, H, P, start, done, start_off, Q, Kc, Vc, O, cap,
                           splits, part, sink);
   };
   if constexpr (sizeof(ACT) == 2) {
