@@ -215,6 +215,7 @@ struct tppsd_state {
   char *packD = nullptr;               // draft weights in fragment order
   char *packDdec = nullptr;            // draft decoder in fragment order (row drafting)
   float *rd_rng = nullptr;             // [B][max_gamma][4] the draft draws' random numbers (row drafting)
+  float *rd_fpart = nullptr;           // [B][RD_FSPLIT][2][d] FFN outputs per hidden slice (row drafting)
   size_t pack_layerD = 0;
   bool packs_built = false;
   bool wb_built = false;
@@ -272,6 +273,7 @@ struct WsLayout {
   size_t packD = 0, pack_layerD = 0;  // the same for the draft model
   size_t packDdec = 0;                // the draft decoder's [E; V_k1] and heads in fragment order (row drafting)
   size_t rd_rng = 0;                  // the draft draws' random numbers per sequence and step (row drafting)
+  size_t rd_fpart = 0;                // FFN outputs per hidden slice of a non-last layer (row drafting)
   size_t wbT = 0, wbD = 0, wb_nT = 0, wb_nD = 0;   // matrices in the k_block order (0 bytes: not served)
   size_t d_tau, d_t, d_k, d_logg, d_logf, d_mix, d_lt, d_rate;
   size_t v_logg, v_logf, v_mix, v_lt;
@@ -356,6 +358,7 @@ WsLayout ws_layout(const tppsd_model *T, const tppsd_model *D, int B, int cap, i
       row_draft_ok(D->bf16(), D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn, D->cfg.n_mix, D->cfg.n_types, (int)kvc)) {
     w.packDdec = take(rd_pack_dec_elems(D->d()) * 2);
     w.rd_rng = take(Bz * MG * 4 * 4);
+    w.rd_fpart = take(Bz * RD_FSPLIT * 2 * D->d() * 4);
   }
   w.ar_mix = take(Bz * 3 * mmax * 4);
   w.ar_lt = take(Bz * kmax * 4);
@@ -737,6 +740,7 @@ int do_draft_rows(tppsd_state *s, int gamma, const tppsd_draft_buf *out, hipStre
   a.xn = (bf16_t *)s->a;
   a.part = s->attn_part;
   a.rng = s->rd_rng;
+  a.fpart = s->rd_fpart;
   a.pk = (const bf16_t *)s->packD;
   a.pk_e = (const bf16_t *)s->packDdec;
   a.pk_head = (const bf16_t *)(s->packDdec + (size_t)4 * s->D->d() * s->D->d() * 2);
@@ -1162,6 +1166,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
   s->packD = w.pack_layerD ? ws + w.packD : nullptr;
   s->packDdec = w.packDdec ? ws + w.packDdec : nullptr;
   s->rd_rng = w.rd_rng ? (float *)(ws + w.rd_rng) : nullptr;
+  s->rd_fpart = w.rd_fpart ? (float *)(ws + w.rd_fpart) : nullptr;
   s->pack_layerD = w.pack_layerD;
   s->cT.wb = w.wb_nT ? ws + w.wbT : nullptr;
   s->cD.wb = w.wb_nD ? ws + w.wbD : nullptr;

@@ -64,6 +64,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   __shared__ float wred[2][4][2];
   __shared__ __attribute__((aligned(16))) bf16_t xl[2][D];        // LayerNorm'd rows of the step's tokens
   __shared__ float bs[3][DH];                                       // the head's q, k, v biases
+  __shared__ float lnred[4][2];                                     // per wave: LayerNorm partial sums
+  __shared__ float lngb[2 * D];                                     // LayerNorm gain, then bias
   __shared__ float qs[2][DH];                                       // queries (bf16-rounded)
   __shared__ __attribute__((aligned(16))) bf16_t kvn[2][2][DH];   // the new keys and values [k / v][row]
   const DraftArgs &d = a.d;
@@ -87,14 +89,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   const FusedLayerW &lw = d.layer[layer];
   const bf16_t *wqkv = (const bf16_t *)lw.qkv_w;
   const float *qkvb = lw.qkv_b;
+  const float *xres = a.x, *fpart = a.fpart, *l1g = lw.ln1_g, *l1b = lw.ln1_b;
   const int done = load_const(done_p + b), lenD = load_const(len_p + b);
   asm volatile("" ::"s"(cap), "s"(nh), "s"(kcb), "s"(vcb), "s"(xn), "s"(lbytes), "s"(wqkv), "s"(qkvb), "s"(done),
-               "s"(lenD));
+               "s"(lenD), "s"(xres), "s"(fpart), "s"(l1g), "s"(l1b));
   auto wrow = [&](int which) { return wqkv + (size_t)(which * D + h * DH + r) * D + 16 * j8; };
   // the LayerNorm'd rows and this head's query rows of W_qkv
   const int P = step == 1 ? 2 : 1;
+  // Layer 0 reads them as stored (by the last layer of the step before, or
+  // step 0). Every later layer follows one whose FFN ran in RD_FSPLIT slices:
+  // it forms them from the residual rows plus the slices' outputs and applies
+  // its LayerNorm itself, thread t taking column t mod D of row t / D (the
+  // gain and bias loaded with them).
+  static_assert(2 * D == 256, "one column of the two rows per thread");
+  const bool comb = layer > 0;
   uint4 xw = make_uint4(0u, 0u, 0u, 0u);
-  if (tid < 2 * D / 8) xw = *(const uint4 *)((const bf16_t *)xn + (size_t)b * 2 * D + 8 * tid);
+  float cx[1 + RD_FSPLIT], cgb = 0.f;   // cgb: gain (t < D) or bias (t >= D) of column t mod D, staged in LDS
+  if (comb) {
+    const int rw = tid / D, cc = tid % D;
+    cx[0] = xres[((size_t)b * 2 + rw) * D + cc];
+#pragma unroll
+    for (int j = 0; j < RD_FSPLIT; ++j) cx[1 + j] = fpart[(((size_t)b * RD_FSPLIT + j) * 2 + rw) * D + cc];
+    cgb = rw ? l1b[cc] : l1g[cc];
+  } else if (tid < 2 * D / 8) {
+    xw = *(const uint4 *)((const bf16_t *)xn + (size_t)b * 2 * D + 8 * tid);
+  }
   // the head's biases, one per lane (staged in LDS with the rows)
   const int bi = min(tid, 3 * DH - 1);
   const float bias = qkvb[(bi / DH) * D + h * DH + bi % DH];
@@ -149,7 +168,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     const int pb = min(k0 + 8 * (grp + i * NG), (n_keys - 1) & ~7);   // first position of the block
     vr[i] = __builtin_nontemporal_load((const u32x4_t *)(vc + v_at<bf16_t>(row0, pb, col, DH)));
   }
-  if (tid < 2 * D / 8) *(uint4 *)(&xl[0][0] + 8 * tid) = xw;
+  if (comb) {
+    // LayerNorm (biased variance, eps 1e-5) of each row over its two waves
+    const int rw = tid / D, cc = tid % D;
+    float x = cx[0];
+#pragma unroll
+    for (int j = 0; j < RD_FSPLIT; ++j) x += cx[1 + j];
+    const float s1 = wave_sum(x);
+    if (lane == 0) lnred[wave][0] = s1;
+    lngb[tid] = cgb;
+    __syncthreads();
+    const float mean = (lnred[2 * rw][0] + lnred[2 * rw + 1][0]) / (float)D;
+    const float dx = x - mean;
+    const float s2 = wave_sum(dx * dx);
+    if (lane == 0) lnred[wave][1] = s2;
+    __syncthreads();
+    const float rstd = 1.f / sqrtf((lnred[2 * rw][1] + lnred[2 * rw + 1][1]) / (float)D + 1e-5f);
+    xl[rw][cc] = f2bf(dx * rstd * lngb[cc] + lngb[D + cc]);
+  } else if (tid < 2 * D / 8) {
+    *(uint4 *)(&xl[0][0] + 8 * tid) = xw;
+  }
   if (tid < 3 * DH) (&bs[0][0])[tid] = bias;
   __syncthreads();
   // dot products of a weight row slice with a row's slice: v_dot2c over
@@ -350,6 +388,18 @@ template <int N, int KD> struct RdFrags {
         f[t][ks] = *(const bf16x8_t *)(Wp + ((size_t)(tile * KS + ks) * 64 + lane) * 8);
     }
   }
+  // the same for the k steps ks0 .. ks0 + KS - 1 of a packed matrix of
+  // ks_all k steps per tile (a slice of its inner dimension)
+  __device__ __forceinline__ void load_packed_k(const bf16_t *Wp, int ks_all, int ks0) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      const int tile = min(wave + t * RD_WAVES, TILES - 1);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        f[t][ks] = *(const bf16x8_t *)(Wp + ((size_t)(tile * ks_all + ks0 + ks) * 64 + lane) * 8);
+    }
+  }
   // rows 0 .. NR - 1 of X (bf16 in LDS, row stride ldx elements; rows
   // r < nx read, the others zero); epi(r, n, acc) for r < NR on lanes 0..15
   template <int NR, typename EPI>
@@ -494,7 +544,7 @@ template <int D, int F> struct RdVec {
 // Launch modes: step 0 embeds the last two committed events and normalises
 // them for layer 0; step l >= 1, layer ly finishes layer ly of the step's
 // rows after its attention.
-template <int D, int F, int DH>
+template <int D, int F, int DH, bool SPLIT>
 __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_p, const int32_t *len_p,
                                                             const float *part, float *xa, const bf16_t *pk, int l,
                                                             int ly, int part_cnt, RowDraftArgs a) {
@@ -556,7 +606,15 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
       pv[i] = k < part_cnt ? src[k] : 0.f;
     }
   }
-  const float xv = tid < P * D ? xg[tid] : 0.f;
+  // the residual rows: after a layer whose FFN ran in slices, the rows plus
+  // every slice's output
+  const float *fp_in = a.fpart + (size_t)b * RD_FSPLIT * 2 * D;
+  float xv = 0.f, xs_in[RD_FSPLIT];
+  if (tid < P * D) {
+    xv = xg[tid];
+#pragma unroll
+    for (int j = 0; j < RD_FSPLIT; ++j) xs_in[j] = ly > 0 ? fp_in[j * 2 * D + tid] : 0.f;
+  }
   RdFrags<D, D> fo;
   fo.load_packed(wl);
   // the scalar batch
@@ -607,10 +665,16 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
       vl[i] = *src;
     }
   }
-  RdFrags<F, D> f1;
-  f1.load_packed(wl + D * D);
-  RdFrags<D, F> f2;
-  f2.load_packed(wl + D * D + F * D);
+  // a non-last layer's launch (SPLIT) has RD_FSPLIT workgroups per sequence,
+  // workgroup j taking hidden units j F / RD_FSPLIT .. of the FFN: its rows of
+  // W1 and its columns of W2
+  constexpr int FS = SPLIT ? F / RD_FSPLIT : F;
+  const int js = SPLIT ? blockIdx.y : 0;
+  RdFrags<FS, D> f1;
+  f1.load_packed(wl + D * D + (size_t)js * FS * D);
+  RdFrags<D, FS> f2;
+  if (SPLIT) f2.load_packed_k(wl + D * D + F * D, F / 32, js * (FS / 32));
+  else f2.load_packed(wl + D * D + F * D);
   RdFrags<4 * D, D> fe;
   RdFrags<128, D> fh;   // the heads' rows (mixture, then type; zero past 3 M + K), packed
   const int pos0 = base + (l == 1 ? 0 : l);
@@ -619,7 +683,12 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
   if (done) return;   // workgroup-uniform; the loads above are dropped
 #pragma unroll
   for (int i = 0; i < NPV; ++i) sh.part[tid + i * RD_ROW_THREADS] = pv[i];
-  if (tid < P * D) (&sh.xs[0][0])[tid] = xv;
+  if (tid < P * D) {
+    float x = xv;
+#pragma unroll
+    for (int j = 0; j < RD_FSPLIT; ++j) x += xs_in[j];
+    (&sh.xs[0][0])[tid] = x;
+  }
   rd_sync();
   // merge the attention splits of each (row, head): output = sum_s e^{m_s - m} o_s / sum_s e^{m_s - m} l_s
   {
@@ -655,7 +724,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
   rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::LN2G, sh.vec + V::LN2B, P);
   rd_sync();
   f1.template mul<2>(&sh.ab[0][0], D, P, [&](int p, int nn, float acc) {
-    if (p < P) sh.hb[p][nn] = f2bf(fmaxf(acc + sh.vec[V::F1B + nn], 0.f));
+    if (p < P) sh.hb[p][nn] = f2bf(fmaxf(acc + sh.vec[V::F1B + js * FS + nn], 0.f));
   });
   // the first product's registers are free: after the last layer, the decoder's fragments
   const bool more = l < late.gamma;
@@ -664,6 +733,17 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
     fh.load_packed(late.pk_head);
   }
   rd_sync();
+  if constexpr (SPLIT) {
+    // this slice's share of the FFN output, to memory; the next launches add
+    // the slices to the rows, which workgroup 0 stores with the FFN's bias
+    float *fp_out = a.fpart + ((size_t)b * RD_FSPLIT + js) * 2 * D;
+    f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
+      if (p < P) fp_out[p * D + nn] = acc;
+    });
+    if (js == 0)
+      for (int i = tid; i < P * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i] + sh.vec[V::F2B + i % D];
+    return;
+  }
   f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
     if (p < P) sh.xs[p][nn] += acc + sh.vec[V::F2B + nn];
   });
@@ -795,10 +875,16 @@ void launch_draft_rows(RowDraftArgs a, hipStream_t st, const hipEvent_t *ev) {
   auto e0 = [&]() { return ev ? ev[2 * j] : nullptr; };
   auto e1 = [&]() { return ev ? ev[2 * j + 1] : nullptr; };
   // (the row kernel's leading arguments, preloaded into registers, repeat
-  // fields of a that its first loads need)
+  // fields of a that its first loads need; a non-last layer's launch has
+  // RD_FSPLIT workgroups per sequence)
   auto rows = [&]() {
-    hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32>, dim3(B), dim3(RD_ROW_THREADS), 0, st, e0(), e1(), 0, a.d.done,
-                          a.d.lenD, (const float *)a.part, a.x, a.pk, a.step, a.layer, part_cnt, a);
+    if (a.step > 0 && a.layer < a.d.L - 1)
+      hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32, true>, dim3(B, RD_FSPLIT), dim3(RD_ROW_THREADS), 0, st, e0(),
+                            e1(), 0, a.d.done, a.d.lenD, (const float *)a.part, a.x, a.pk, a.step, a.layer, part_cnt,
+                            a);
+    else
+      hipExtLaunchKernelGGL(k_rd_rows<128, 512, 32, false>, dim3(B), dim3(RD_ROW_THREADS), 0, st, e0(), e1(), 0,
+                            a.d.done, a.d.lenD, (const float *)a.part, a.x, a.pk, a.step, a.layer, part_cnt, a);
   };
   a.step = 0;
   a.layer = 0;

@@ -169,12 +169,14 @@ constexpr int RD_MAX_TYPES = 32;
 // (H S 2 (d_head + 2): 4 heads of 32 over 8192 positions take 4352; a
 // multiple of RD_ROW_THREADS)
 constexpr int RD_MAX_PART = 4608;
+constexpr int RD_FSPLIT = 4;    // workgroups per sequence of a non-last layer's row launch (FFN hidden slices)
 static_assert(RD_MAX_PART % RD_ROW_THREADS == 0, "partial staging: whole rounds of the row workgroup");
 struct RowDraftArgs {
   DraftArgs d;              // model, cache, state and record pointers as for the one-launch draft
   float *x;                 // [B][2][d] residual stream of the step's rows
   bf16_t *xn;               // [B][2][d] the step's rows after the layer's LayerNorm (q, k, v input)
   float *part;              // [B][H][S][2][d_head + 2] split partials: maximum, sum, output sums
+  float *fpart;             // [B][RD_FSPLIT][2][d] a non-last layer's FFN output, per slice of its hidden units
   float *rng;               // [B][MG][4] per draft step: u for the component, the normal deviate, u for the
                             // type (written by the step-0 launch)
   const bf16_t *pk;         // per layer Wo, W1, W2, Wqkv in MFMA fragment order (launch_pack_frags)
