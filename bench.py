@@ -135,13 +135,15 @@ def draft_rows_bytes(wl, B, gamma):
     """Row drafting's row launch, averaged over a round's 1 + L gamma
     launches: the matrices the round's row launches read, each launch's once
     (per step and layer the output projection and FFN; after the last layer
-    also the decoder; the step-0 launch only embeds), and the residual rows in
-    and out."""
+    also the decoder; the step-0 launch only embeds), the residual rows in
+    and out, and a non-last layer's FFN output in its four hidden-unit slices
+    (fp32, written, then read by the next row launch)."""
     c = wl.draft
     d, F, L = c.d_model, c.d_ffn, c.n_layers
     elems = gamma * (L * (d * d + 2 * d * F) + _decoder_elems(c))
     launches = 1 + L * gamma
-    return float(elems * _elt(c) / launches + 2 * B * 2 * d * 4)
+    slices = (L - 1) * gamma * 2 * 4 * B * d * 4
+    return float((elems * _elt(c) + slices) / launches + 2 * B * 2 * d * 4)
 
 
 def run_context(wl):
@@ -448,8 +450,8 @@ def main():
             "traffic": measured_traffic("draft_attention", wl.name)}
     if tk["draft_rows_launches"]:
         classes["draft_rows"] = {
-            "bound": "hbm", "kernel": "k_rd_rows<128, 512, 32> (row drafting: one workgroup per sequence, "
-                                      "per step and layer)",
+            "bound": "hbm", "kernel": "k_rd_rows<128, 512, 32, split> (row drafting, per step and layer: four workgroups "
+                                      "per sequence for a non-last layer, one for the last)",
             "ms": tk["draft_rows_ms"], "launches": tk["draft_rows_launches"],
             "per_launch": draft_rows_bytes(wl, B, gamma), "unit": "GB/s", "peak": HBM_PEAK_GBS,
             "traffic": measured_traffic("draft_rows", wl.name)}
