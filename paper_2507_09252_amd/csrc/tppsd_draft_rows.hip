@@ -9,11 +9,14 @@
 //    whole chip; the split holding the step's new position also forms and
 //    appends its key and value; each split leaves its running maximum, sum
 //    and unnormalised output;
-//  - k_rd_rows: one workgroup per sequence merges the splits and runs every
-//    row-local step up to the next attention -- output projection and
-//    residual, the feed-forward block, then the next layer's LayerNorm; after
-//    the last layer the decoder, the draft record, the draw, and the drawn
-//    event's embedding and layer-0 LayerNorm for the next step.
+//  - k_rd_rows: merges the splits and runs every row-local step up to the
+//    next attention -- output projection and residual, the feed-forward
+//    block; for a non-last layer four workgroups per sequence, each taking a
+//    quarter of the FFN's hidden units (the next layer's attention adds their
+//    outputs to the rows and applies its LayerNorm); for the last layer one
+//    workgroup per sequence, which also runs the decoder, the draft record,
+//    the draw, and the drawn event's embedding and layer-0 LayerNorm for the
+//    next step.
 // The matrix-vector products of a sequence's one or two rows run on MFMA
 // 16-row tiles (rows past the token count are zero operands) with every weight
 // fragment of a product in flight at once, and the next product's fragments
