@@ -87,35 +87,34 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   // round trip per branch.) The asm statement only takes values, which holds
   // each load ahead of it.
   const int cap = d.cap, nh = d.H;
-  const char *kcb = d.kc, *vcb = d.vc, *xn = (const char *)a.xn;
+  const char *kcb = d.kc, *vcb = d.vc;
   const size_t lbytes = d.layer_bytes;
   const FusedLayerW &lw = d.layer[layer];
   const bf16_t *wqkv = (const bf16_t *)lw.qkv_w;
   const float *qkvb = lw.qkv_b;
   const float *xres = a.x, *fpart = a.fpart, *l1g = lw.ln1_g, *l1b = lw.ln1_b;
   const int done = load_const(done_p + b), lenD = load_const(len_p + b);
-  asm volatile("" ::"s"(cap), "s"(nh), "s"(kcb), "s"(vcb), "s"(xn), "s"(lbytes), "s"(wqkv), "s"(qkvb), "s"(done),
+  asm volatile("" ::"s"(cap), "s"(nh), "s"(kcb), "s"(vcb), "s"(lbytes), "s"(wqkv), "s"(qkvb), "s"(done),
                "s"(lenD), "s"(xres), "s"(fpart), "s"(l1g), "s"(l1b));
   auto wrow = [&](int which) { return wqkv + (size_t)(which * D + h * DH + r) * D + 16 * j8; };
   // the LayerNorm'd rows and this head's query rows of W_qkv
   const int P = step == 1 ? 2 : 1;
-  // Layer 0 reads them as stored (by the last layer of the step before, or
-  // step 0). Every later layer follows one whose FFN ran in RD_FSPLIT slices:
-  // it forms them from the residual rows plus the slices' outputs and applies
-  // its LayerNorm itself, thread t taking column t mod D of row t / D (the
-  // gain and bias loaded with them).
+  // The launch applies the layer's LayerNorm itself to the residual rows
+  // (stored by the launch before), thread t taking column t mod D of row
+  // t / D; after a layer whose FFN ran in RD_FSPLIT slices (every layer but
+  // the first) it first adds the slices' outputs. Every load is issued
+  // unconditionally (layer 0 reads slices it then ignores) so that no branch
+  // separates a load from its use; the gain (t < D) or bias (t >= D) of
+  // column t mod D is staged in LDS.
   static_assert(2 * D == 256, "one column of the two rows per thread");
   const bool comb = layer > 0;
-  uint4 xw = make_uint4(0u, 0u, 0u, 0u);
-  float cx[1 + RD_FSPLIT], cgb = 0.f;   // cgb: gain (t < D) or bias (t >= D) of column t mod D, staged in LDS
-  if (comb) {
+  float cx[1 + RD_FSPLIT], cgb;
+  {
     const int rw = tid / D, cc = tid % D;
     cx[0] = xres[((size_t)b * 2 + rw) * D + cc];
 #pragma unroll
     for (int j = 0; j < RD_FSPLIT; ++j) cx[1 + j] = fpart[(((size_t)b * RD_FSPLIT + j) * 2 + rw) * D + cc];
     cgb = rw ? l1b[cc] : l1g[cc];
-  } else if (tid < 2 * D / 8) {
-    xw = *(const uint4 *)((const bf16_t *)xn + (size_t)b * 2 * D + 8 * tid);
   }
   // the head's biases, one per lane (staged in LDS with the rows)
   const int bi = min(tid, 3 * DH - 1);
@@ -171,12 +170,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     const int pb = min(k0 + 8 * (grp + i * NG), (n_keys - 1) & ~7);   // first position of the block
     vr[i] = __builtin_nontemporal_load((const u32x4_t *)(vc + v_at<bf16_t>(row0, pb, col, DH)));
   }
-  if (comb) {
+  // (keeps the rows' sums below the cache loads: formed ahead of them they
+  // would wait for the rows' loads before the cache loads go out)
+  __builtin_amdgcn_sched_barrier(0);
+  {
     // LayerNorm (biased variance, eps 1e-5) of each row over its two waves
     const int rw = tid / D, cc = tid % D;
-    float x = cx[0];
+    float xs = cx[0];
 #pragma unroll
-    for (int j = 0; j < RD_FSPLIT; ++j) x += cx[1 + j];
+    for (int j = 0; j < RD_FSPLIT; ++j) xs += cx[1 + j];
+    const float x = comb ? xs : cx[0];   // (a select: stale slices never enter layer 0's rows)
     const float s1 = wave_sum(x);
     if (lane == 0) lnred[wave][0] = s1;
     lngb[tid] = cgb;
@@ -188,8 +191,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     __syncthreads();
     const float rstd = 1.f / sqrtf((lnred[2 * rw][1] + lnred[2 * rw + 1][1]) / (float)D + 1e-5f);
     xl[rw][cc] = f2bf(dx * rstd * lngb[cc] + lngb[D + cc]);
-  } else if (tid < 2 * D / 8) {
-    *(uint4 *)(&xl[0][0] + 8 * tid) = xw;
   }
   if (tid < 3 * DH) (&bs[0][0])[tid] = bias;
   __syncthreads();
@@ -497,15 +498,10 @@ struct RdShared {
   int tok_k;
 };
 
-// the LayerNorm'd rows 0 .. np - 1 (sh.ab) go to memory for the next
-// attention launch, which forms q, k, v from them; a position past the
-// cache capacity is flagged here
-template <int D>
-__device__ __forceinline__ void rd_store_xn(bf16_t *xn, int cap, uint32_t *status, const bf16_t *ab, int np, int b,
-                                            int pos0) {
-  const int tid = threadIdx.x;
-  if (tid < np * D / 8) *(uint4 *)(xn + (size_t)b * 2 * D + 8 * tid) = *(const uint4 *)(ab + 8 * tid);
-  if (tid == 0 && pos0 + np > cap) atomicOr(status, TPPSD_STATUS_CAPACITY);
+// the next step's positions pos0 .. pos0 + np - 1: one past the cache
+// capacity is flagged
+__device__ __forceinline__ void rd_flag_capacity(int cap, uint32_t *status, int np, int pos0) {
+  if (threadIdx.x == 0 && pos0 + np > cap) atomicOr(status, TPPSD_STATUS_CAPACITY);
 }
 
 // the THP embedding (sin / cos time encoding + type row) of event (t, k) into
@@ -524,7 +520,6 @@ __device__ __forceinline__ void rd_embed(int K, const float *freq, const bf16_t 
 // the next token), held in registers from the start
 struct RdLate {
   const bf16_t *pk_e, *pk_head, *temb;
-  bf16_t *xn;
   uint32_t *status;
   float *tau, *t, *logg, *logf, *mix, *logtype;
   int32_t *k;
@@ -532,15 +527,14 @@ struct RdLate {
 };
 
 // Offsets in RdShared::vec of the small vectors a row launch reads (the
-// current layer's output / FFN biases and second LayerNorm; the next layer's
-// first LayerNorm, or LN_f, the decoder biases and the next token's layer-0
-// LayerNorm and time frequencies). They are loaded before the matrices and
+// current layer's output / FFN biases and second LayerNorm; LN_f, the decoder
+// biases and the next token's time frequencies). They are loaded before the matrices and
 // read from LDS, so that no epilogue waits on a memory load issued behind the
 // matrices.
 template <int D, int F> struct RdVec {
   static constexpr int OUTB = 0, LN2G = D, LN2B = 2 * D, F1B = 3 * D, F2B = 3 * D + F, N1G = 4 * D + F,
                        N1B = 5 * D + F, K1B = 6 * D + F, MIXB = 7 * D + F, K2B = MIXB + 192, FREQ = K2B + 64,
-                       L0G = FREQ + D, L0B = L0G + D, END = L0B + D;
+                       END = FREQ + D;
   static_assert(END <= RD_VEC, "vector area");
 };
 
@@ -586,10 +580,8 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
       rd_embed<D>(d.K, d.freq, (const bf16_t *)d.type_emb, sh.xs[p], d.ev_t[i], d.ev_k[i]);
     }
     rd_sync();
-    rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], d.layer[0].ln1_g, d.layer[0].ln1_b, 2);
     for (int i = tid; i < 2 * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
-    rd_sync();
-    rd_store_xn<D>(a.xn, d.cap, d.status, &sh.ab[0][0], 2, b, base);
+    rd_flag_capacity(d.cap, d.status, 2, base);
     return;
   }
   const int P = l == 1 ? 2 : 1;
@@ -625,23 +617,20 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
   const int nh = d.H, S = a.S, cap = d.cap, MG = d.MG;
   float *rngp = a.rng;
   const FusedLayerW &w = d.layer[ly];
-  const FusedLayerW &wn = d.layer[min(ly + 1, FD_MAX_LAYERS - 1)];   // the next layer's (unused after the last)
   const float *outb = w.out_b, *ln2g = w.ln2_g, *ln2b = w.ln2_b, *f1b = w.ffn1_b, *f2b = w.ffn2_b;
-  const float *ln1g_next = wn.ln1_g, *ln1b_next = wn.ln1_b, *lnfg = d.lnf_g, *lnfb = d.lnf_b;
+  const float *n1g = d.lnf_g, *n1b = d.lnf_b;   // LN_f (the last layer's launch)
   const float *k1b = d.k1_b, *mixb = d.mix_b, *k2b = d.k2_b, *freq = d.freq;
-  const float *l0g = d.layer[0].ln1_g, *l0b = d.layer[0].ln1_b;
   const int done = load_const(done_p + b), base = load_const(len_p + b);
-  const RdLate late{a.pk_e, a.pk_head, (const bf16_t *)d.type_emb, a.xn, d.status, d.d_tau, d.d_t, d.d_logg, d.d_logf,
+  const RdLate late{a.pk_e, a.pk_head, (const bf16_t *)d.type_emb, d.status, d.d_tau, d.d_t, d.d_logg, d.d_logf,
                     d.d_mix, d.d_logtype, d.d_k, d.gamma};
   // (d.F only completes the four words from d.F to d.L, so that they come in
   // one load and no register of it is reused while in flight)
-  asm volatile("" ::"s"(L), "s"(M), "s"(K), "s"(d.F), "s"(nh), "s"(S), "s"(cap), "s"(MG), "s"(rngp), "s"(outb), "s"(ln2g), "s"(ln2b), "s"(f1b), "s"(f2b), "s"(ln1g_next),
-               "s"(ln1b_next), "s"(lnfg), "s"(lnfb), "s"(k1b), "s"(mixb), "s"(k2b), "s"(freq), "s"(l0g), "s"(l0b),
-               "s"(done), "s"(base), "s"(late.pk_e), "s"(late.pk_head), "s"(late.temb), "s"(late.xn),
+  asm volatile("" ::"s"(L), "s"(M), "s"(K), "s"(d.F), "s"(nh), "s"(S), "s"(cap), "s"(MG), "s"(rngp), "s"(outb),
+               "s"(ln2g), "s"(ln2b), "s"(f1b), "s"(f2b), "s"(n1g), "s"(n1b), "s"(k1b), "s"(mixb), "s"(k2b),
+               "s"(freq), "s"(done), "s"(base), "s"(late.pk_e), "s"(late.pk_head), "s"(late.temb),
                "s"(late.status), "s"(late.tau), "s"(late.t), "s"(late.logg), "s"(late.logf), "s"(late.mix),
                "s"(late.logtype), "s"(late.k), "s"(late.gamma));
   const bool last = ly == L - 1;
-  const float *n1g = last ? lnfg : ln1g_next, *n1b = last ? lnfb : ln1b_next;
   // read late, waited for where used: the step's draw numbers (u for the
   // component, the normal deviate, u for the type) and the time the drawn
   // interval is added to (the last committed event's, or the previous
@@ -656,8 +645,7 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
     struct Seg { const float *p; int off, n; };
     const Seg segs[] = {{outb, V::OUTB, D}, {ln2g, V::LN2G, D},       {ln2b, V::LN2B, D},   {f1b, V::F1B, F},
                         {f2b, V::F2B, D},   {n1g, V::N1G, D},         {n1b, V::N1B, D},     {k1b, V::K1B, D},
-                        {mixb, V::MIXB, 3 * M}, {k2b, V::K2B, K},     {freq, V::FREQ, D},   {l0g, V::L0G, D},
-                        {l0b, V::L0B, D}};
+                        {mixb, V::MIXB, 3 * M}, {k2b, V::K2B, K},     {freq, V::FREQ, D}};
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
       const int k = tid + i * RD_ROW_THREADS;
@@ -750,15 +738,8 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
   f2.template mul<2>(&sh.hb[0][0], F, P, [&](int p, int nn, float acc) {
     if (p < P) sh.xs[p][nn] += acc + sh.vec[V::F2B + nn];
   });
-  if (!last) {
-    rd_sync();
-    rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::N1G, sh.vec + V::N1B, P);
-    for (int i = tid; i < P * D; i += RD_ROW_THREADS) xg[i] = (&sh.xs[0][0])[i];
-    rd_sync();
-    rd_store_xn<D>(late.xn, cap, late.status, &sh.ab[0][0], P, b, pos0);
-    return;
-  }
-  // ---- last layer: decoder on the last row, the draw, the next token
+  // ---- last layer (a launch without slices runs only for it and step 0):
+  // decoder on the last row, the draw, the next token
   rd_sync();
   const int pl = P - 1;
   rd_layernorm<D>(&sh.xs[pl][0], &sh.ab[0][0], sh.vec + V::N1G, sh.vec + V::N1B, 1);
@@ -850,12 +831,11 @@ __global__ __launch_bounds__(RD_ROW_THREADS) void k_rd_rows(const int32_t *done_
   for (int i = 0; i < NTE; ++i) *((uint4 *)sh.temb + tid + i * RD_ROW_THREADS) = te[i];
   rd_sync();
   // the drawn event is the next step's token, at position base + l + 1
+  // (its row goes to memory as the residual; the next attention launch
+  // applies layer 0's LayerNorm)
   rd_embed<D>(K, sh.vec + V::FREQ, sh.temb, sh.xs[0], sh.tok_t, sh.tok_k);
-  rd_sync();
-  rd_layernorm<D>(&sh.xs[0][0], &sh.ab[0][0], sh.vec + V::L0G, sh.vec + V::L0B, 1);
-  for (int i = tid; i < D; i += RD_ROW_THREADS) xg[i] = sh.xs[0][i];
-  rd_sync();
-  rd_store_xn<D>(late.xn, cap, late.status, &sh.ab[0][0], 1, b, base + l + 1);
+  if (tid < D) xg[tid] = sh.xs[0][tid];   // (the element this thread wrote)
+  rd_flag_capacity(cap, late.status, 1, base + l + 1);
 }
 
 }  // namespace
