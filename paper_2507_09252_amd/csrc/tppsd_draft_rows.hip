@@ -4,7 +4,8 @@
 // Each draft step runs two launches per layer:
 //  - k_rd_attn: the step's queries (two in the first step, which re-encodes
 //    the last two committed events, one after), formed in the launch from the
-//    step's LayerNorm'd rows, against the draft KV cache, split over (key
+//    step's residual rows (the launch applies the layer's LayerNorm), against
+//    the draft KV cache, split over (key
 //    range, head, sequence) workgroups so that the cache streams through the
 //    whole chip; the split holding the step's new position also forms and
 //    appends its key and value; each split leaves its running maximum, sum
@@ -12,11 +13,10 @@
 //  - k_rd_rows: merges the splits and runs every row-local step up to the
 //    next attention -- output projection and residual, the feed-forward
 //    block; for a non-last layer four workgroups per sequence, each taking a
-//    quarter of the FFN's hidden units (the next layer's attention adds their
-//    outputs to the rows and applies its LayerNorm); for the last layer one
-//    workgroup per sequence, which also runs the decoder, the draft record,
-//    the draw, and the drawn event's embedding and layer-0 LayerNorm for the
-//    next step.
+//    quarter of the FFN's hidden units (the next layer's launches add their
+//    outputs to the rows); for the last layer one workgroup per sequence,
+//    which also runs the decoder, the draft record, the draw, and the drawn
+//    event's embedding (the next step's residual row).
 // The matrix-vector products of a sequence's one or two rows run on MFMA
 // 16-row tiles (rows past the token count are zero operands) with every weight
 // fragment of a product in flight at once, and the next product's fragments
