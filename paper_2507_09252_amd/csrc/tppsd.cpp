@@ -249,7 +249,7 @@ struct tppsd_state {
   bool fused_draft = true;   // one-launch drafting when the draft model fits it
   bool wave_draft = false;   // ... with one wave per sequence (small draft models)
   bool fused_w_lds = false;  // ... with its weight matrices staged in LDS
-  bool row_draft = false;    // split attention + one row workgroup per sequence, per step and layer
+  bool row_draft = false;    // split attention + row workgroups per sequence, per step and layer
   hipGraphExec_t sd_exec[2] = {nullptr, nullptr};
   long long sd_key = -1;
   const float *sd_params = nullptr, *phase_params = nullptr;   // Poisson draft parameters the graphs embed
@@ -1250,7 +1250,7 @@ int tppsd_state_create(const tppsd_model *T, const tppsd_model *D, int B, int ma
       (void)hipGetLastError();
     }
     // otherwise, for batches too small to fill the chip with per-step GEMM
-    // tiles, the per-step split attention and one row workgroup per sequence
+    // tiles, the per-step split attention and the row workgroups per sequence
     s->row_draft = D && !D->attnhp() && !s->fused_draft && !s->wave_draft && !(nf && nf[0] == '1') &&
                    B <= 256 && s->packD && s->packDdec &&
                    row_draft_ok(D->bf16(), D->cfg.n_layers, D->d(), D->H(), D->cfg.d_ffn, D->cfg.n_mix,

@@ -200,11 +200,16 @@ def test_accept_teacher_forced(case, external):
 # on MFMA (the vector-ALU form serves up to four heads)
 H8 = W.Workload("h8", 7, W.ModelCfg(2, 64, 4, 256, 16, 22, "bf16"), W.ModelCfg(1, 128, 8, 256, 16, 22, "bf16"),
                 batch=8, n_gen=64, gammas=(6,), n_hist=30, history="hawkes22", description="8-head bf16 draft")
+# a three-layer row-drafting draft (d 128, four heads of 32, F 512): its middle
+# layer runs the FFN in four slices and takes its rows as the residual plus the
+# first layer's slices, a form the two-layer c4 draft does not reach
+R3 = W.Workload("r3", 8, W.ModelCfg(2, 64, 4, 256, 16, 5, "bf16"), W.ModelCfg(3, 128, 4, 512, 16, 5, "bf16"),
+                batch=4, n_gen=64, gammas=(6,), n_hist=600, history="hawkes5", description="3-layer row draft")
 DRAFT_CASES = [small("c1", 8), small("c2", 8), small("c3", 16, n_hist=40, init="bias"), small("c5", 16, init="bias"),
                small("c4", 4, n_hist=40, init="bias"), small("c3", 8, n_hist=40, init="bias", gamma=20),
                small("c2", 4, n_hist=40, init="bias", gamma=32), Case("h8-B6-bias", H8, 6, 30, "bias", True),
                # d = 128 drafts over a long history: three key splits of 512 per (sequence, head)
-               small("c4", 3, n_hist=1100, init="bias")]
+               small("c4", 3, n_hist=1100, init="bias"), Case("r3-B4-h600-bias", R3, 4, 600, "bias", True)]
 
 
 # both drafting paths: one workgroup per sequence for all gamma steps (where
