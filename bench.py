@@ -119,12 +119,12 @@ def draft_attn_bytes(wl, B, gamma, ctx):
     step): the layer's cached keys and values up to the step's position (the
     run-average context plus half a round's drafts), read once; the layer's
     q, k, v matrices; the step's LayerNorm'd rows in; the new keys and values
-    appended; and each 512-key split's (max, sum, d_head sums) out. Token rows
+    appended; and each 384-key split's (max, sum, d_head sums) out. Token rows
     per step average (gamma + 1) / gamma (two in a round's first step)."""
     c = wl.draft
     keys = ctx + gamma / 2.0
     rows = (gamma + 1.0) / gamma
-    splits = math.ceil(keys / 512.0)
+    splits = math.ceil(keys / 384.0)
     e = _elt(c)
     return float(B * c.n_heads * keys * c.d_head * 2 * e + 3 * c.d_model * c.d_model * e
                  + B * rows * c.d_model * e + B * rows * 2 * c.d_model * e

@@ -55,7 +55,7 @@ __device__ __forceinline__ T load_const(const T *p) {
 // of head h of sequence b
 // ---------------------------------------------------------------------------
 template <int D, int DH>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void k_rd_attn(const int32_t *done_p,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_rd_attn(const int32_t *done_p,
                                                                                           const int32_t *len_p,
                                                                                           int step, int layer,
                                                                                           RowDraftArgs a) {

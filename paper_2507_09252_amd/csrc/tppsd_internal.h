@@ -161,7 +161,7 @@ constexpr size_t LDS_PER_WG = 160 * 1024;
 // sequence) workgroups of RD_KEYS keys, then workgroups of RD_ROW_THREADS for
 // the row-local rest (RD_FSPLIT per sequence for a non-last layer, one for the
 // last). bf16 draft models with d = 128, four heads of 32, d_ffn = 512.
-constexpr int RD_KEYS = 512;
+constexpr int RD_KEYS = 384;
 constexpr int RD_ROW_THREADS = 512;
 // event types whose embedding rows the row kernel stages in LDS (all of them)
 constexpr int RD_MAX_TYPES = 32;

@@ -208,7 +208,7 @@ R3 = W.Workload("r3", 8, W.ModelCfg(2, 64, 4, 256, 16, 5, "bf16"), W.ModelCfg(3,
 DRAFT_CASES = [small("c1", 8), small("c2", 8), small("c3", 16, n_hist=40, init="bias"), small("c5", 16, init="bias"),
                small("c4", 4, n_hist=40, init="bias"), small("c3", 8, n_hist=40, init="bias", gamma=20),
                small("c2", 4, n_hist=40, init="bias", gamma=32), Case("h8-B6-bias", H8, 6, 30, "bias", True),
-               # d = 128 drafts over a long history: three key splits of 512 per (sequence, head)
+               # d = 128 drafts over a long history: four key splits of 384 per (sequence, head)
                small("c4", 3, n_hist=1100, init="bias"), Case("r3-B4-h600-bias", R3, 4, 600, "bias", True)]
 
 
