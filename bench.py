@@ -369,7 +369,8 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the batch shards across GPUs with no exchange, see DESIGN.md)", file=sys.stderr)
+              "(the batch shards across GPUs with no exchange: one process per GPU over its own sequences)",
+              file=sys.stderr)
         sys.exit(2)
     from paper_2507_09252_amd import workloads as W
     wl = W.WORKLOADS[args.config]
